@@ -1,0 +1,273 @@
+"""CPU oracle for quantize-once MX convolution (MicroQonv).
+
+TEST INFRASTRUCTURE ONLY.  Only the test suite, ``__graft_entry__.smoke()``
+and the CPU-baseline leg of ``bench.py`` may import this package.  The GPU
+library never links, loads or calls it, and it shares no code with it.
+
+This module is a thin ctypes layer over ``mxoracle.c`` (plain fp64 loops, see
+that file's header for the definitions and the passages of the paper each one
+follows).  ``build()`` compiles it with gcc; ``load()`` builds on first use.
+
+Parity: every function here is pinned by the ``-m "not gpu"`` tests in
+``tests/test_oracle_pins.py`` (hand-worked blocks, brute-force element
+rounding, torch's float8 cast, torch's fp64 convolutions, the brute-force
+direct convolutions, invariants).  Nothing here is "parity unpinned".
+"""
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "mxoracle.c")
+_LIB = os.path.join(_HERE, "libmxoracle.so")
+
+E4M3, E2M1 = 0, 1
+NCHW, NHWC, CBF = 0, 1, 2
+ACT, WEIGHT = 0, 1
+
+_lib = None
+
+
+def build():
+    """Compile the oracle (plain C, -O2, OpenMP over the outermost loops)."""
+    cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11",
+           "-o", _LIB + ".tmp", _SRC, "-lm"]
+    subprocess.check_call(cmd)
+    os.replace(_LIB + ".tmp", _LIB)
+
+
+def load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        build()
+    lib = ctypes.CDLL(_LIB)
+    P = ctypes.c_void_p
+    i32, i64, dbl = ctypes.c_int, ctypes.c_int64, ctypes.c_double
+    sig = {
+        "o_encode": (i32, [dbl, i32]),
+        "o_decode": (dbl, [i32, i32]),
+        "o_scale_value": (dbl, [i32]),
+        "o_scale_code": (i32, [dbl, i32]),
+        "o_codes_bytes": (i64, [i32, i32, i32, i32, i32, i32]),
+        "o_scales_bytes": (i64, [i32, i32, i32, i32, i32, i32]),
+        "o_quantize": (i32, [P, i32, i32, i32, i32, i32, i32, i32, P, P]),
+        "o_dequant": (i32, [P, P, i32, i32, i32, i32, i32, i32, P]),
+        "o_conv_out": (i32, [P, P, P]),
+        "o_im2col_cbf": (i32, [P, i32, P, P, P, P]),
+        "o_im2col_codes_bytes": (i64, [P, i32]),
+        "o_im2col_scales_bytes": (i64, [P, i32]),
+        "o_fwd": (i32, [P, i32, P, P, P, P, P, P]),
+        "o_wgrad": (i32, [P, i32, P, P, P, P, P, P]),
+        "o_dgrad": (i32, [P, i32, P, P, P, P, P, P]),
+        "o_direct_fwd": (i32, [P, P, P, P]),
+        "o_direct_dgrad": (i32, [P, P, P, P]),
+        "o_direct_wgrad": (i32, [P, P, P, P]),
+        "o_fwd_at": (i32, [P, i32, P, P, P, P, P, i64, P, P]),
+        "o_dgrad_at": (i32, [P, i32, P, P, P, P, P, i64, P, P]),
+        "o_wgrad_at": (i32, [P, i32, P, P, P, P, P, i64, P, P]),
+        "o_quantize_1d": (i32, [P, i64, i64, i32, i32, P, P]),
+        "o_counter_get": (i64, []),
+        "o_counter_reset": (None, []),
+        "o_set_threads": (None, [i32]),
+        "o_get_threads": (i32, []),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _ptr(a):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _check(rc, what):
+    if rc != 0:
+        raise ValueError(f"oracle {what} failed with code {rc}")
+
+
+def _conv_params(conv):
+    """conv: dict with n, cin, cout, h, w, kh, kw, sh, sw, ph, pw."""
+    keys = ("n", "cin", "cout", "h", "w", "kh", "kw", "sh", "sw", "ph", "pw")
+    return np.array([int(conv[k]) for k in keys], dtype=np.int32)
+
+
+def set_threads(t):
+    load().o_set_threads(int(t))
+
+
+def get_threads():
+    return load().o_get_threads()
+
+
+def encode(v, fmt):
+    return load().o_encode(float(v), fmt)
+
+
+def decode(code, fmt):
+    return load().o_decode(int(code), fmt)
+
+
+def scale_code(amax, fmt):
+    return load().o_scale_code(float(amax), fmt)
+
+
+def codes_bytes(role, fmt, n, c, h, w):
+    return load().o_codes_bytes(role, fmt, n, c, h, w)
+
+
+def scales_bytes(role, fmt, n, c, h, w):
+    return load().o_scales_bytes(role, fmt, n, c, h, w)
+
+
+def quantize(src, layout, role, fmt, n, c, h, w):
+    """src: float32 array holding the logical (n, c, h, w) tensor in `layout`.
+    Returns (codes uint8, scales uint8) in the MX-CBF layout."""
+    lib = load()
+    src = np.ascontiguousarray(src, dtype=np.float32)
+    nb = lib.o_codes_bytes(role, fmt, n, c, h, w)
+    ns = lib.o_scales_bytes(role, fmt, n, c, h, w)
+    if nb < 0:
+        raise ValueError("bad geometry")
+    codes = np.zeros(nb, dtype=np.uint8)
+    scales = np.zeros(ns, dtype=np.uint8)
+    _check(lib.o_quantize(_ptr(src), layout, role, fmt, n, c, h, w, _ptr(codes), _ptr(scales)),
+           "quantize")
+    return codes, scales
+
+
+def dequant(codes, scales, role, fmt, n, c, h, w):
+    lib = load()
+    out = np.zeros((n, c, h, w), dtype=np.float64)
+    codes = np.ascontiguousarray(codes, dtype=np.uint8)
+    scales = np.ascontiguousarray(scales, dtype=np.uint8)
+    _check(lib.o_dequant(_ptr(codes), _ptr(scales), role, fmt, n, c, h, w, _ptr(out)), "dequant")
+    return out
+
+
+def conv_out(conv):
+    p = _conv_params(conv)
+    ho = ctypes.c_int()
+    wo = ctypes.c_int()
+    _check(load().o_conv_out(_ptr(p), ctypes.byref(ho), ctypes.byref(wo)), "conv_out")
+    return ho.value, wo.value
+
+
+def im2col_cbf(conv, fmt, xcodes, xscales):
+    lib = load()
+    p = _conv_params(conv)
+    cb = lib.o_im2col_codes_bytes(_ptr(p), fmt)
+    sb = lib.o_im2col_scales_bytes(_ptr(p), fmt)
+    cc = np.zeros(cb, dtype=np.uint8)
+    cs = np.zeros(sb, dtype=np.uint8)
+    _check(lib.o_im2col_cbf(_ptr(p), fmt, _ptr(np.ascontiguousarray(xcodes)),
+                            _ptr(np.ascontiguousarray(xscales)), _ptr(cc), _ptr(cs)), "im2col")
+    return cc, cs
+
+
+def _gemm(name, conv, fmt, a, b, shape):
+    lib = load()
+    p = _conv_params(conv)
+    out = np.zeros(shape, dtype=np.float64)
+    sabs = np.zeros(shape, dtype=np.float64)
+    (ac, as_), (bc, bs) = a, b
+    _check(getattr(lib, name)(_ptr(p), fmt, _ptr(np.ascontiguousarray(ac)),
+                              _ptr(np.ascontiguousarray(as_)), _ptr(np.ascontiguousarray(bc)),
+                              _ptr(np.ascontiguousarray(bs)), _ptr(out), _ptr(sabs)), name)
+    return out, sabs
+
+
+def fwd(conv, fmt, w, x):
+    """w, x: (codes, scales) pairs.  Returns (Y NCHW fp64, sum|products|)."""
+    ho, wo = conv_out(conv)
+    return _gemm("o_fwd", conv, fmt, w, x, (conv["n"], conv["cout"], ho, wo))
+
+
+def dgrad(conv, fmt, w, gy):
+    return _gemm("o_dgrad", conv, fmt, w, gy, (conv["n"], conv["cin"], conv["h"], conv["w"]))
+
+
+def wgrad(conv, fmt, gy, x):
+    return _gemm("o_wgrad", conv, fmt, gy, x, (conv["cout"], conv["cin"], conv["kh"], conv["kw"]))
+
+
+def _at(name, conv, fmt, a, b, idx):
+    lib = load()
+    p = _conv_params(conv)
+    idx = np.ascontiguousarray(idx, dtype=np.int32).reshape(-1, 4)
+    out = np.zeros(len(idx), dtype=np.float64)
+    sabs = np.zeros(len(idx), dtype=np.float64)
+    (ac, as_), (bc, bs) = a, b
+    _check(getattr(lib, name)(_ptr(p), fmt, _ptr(np.ascontiguousarray(ac)),
+                              _ptr(np.ascontiguousarray(as_)), _ptr(np.ascontiguousarray(bc)),
+                              _ptr(np.ascontiguousarray(bs)), _ptr(idx), len(idx), _ptr(out),
+                              _ptr(sabs)), name)
+    return out, sabs
+
+
+def fwd_at(conv, fmt, w, x, idx):
+    """idx rows (n, co, ho, wo)."""
+    return _at("o_fwd_at", conv, fmt, w, x, idx)
+
+
+def dgrad_at(conv, fmt, w, gy, idx):
+    """idx rows (n, ci, h, w)."""
+    return _at("o_dgrad_at", conv, fmt, w, gy, idx)
+
+
+def wgrad_at(conv, fmt, gy, x, idx):
+    """idx rows (co, ci, kh, kw)."""
+    return _at("o_wgrad_at", conv, fmt, gy, x, idx)
+
+
+def direct_fwd(conv, w, x):
+    ho, wo = conv_out(conv)
+    y = np.zeros((conv["n"], conv["cout"], ho, wo), dtype=np.float64)
+    _check(load().o_direct_fwd(_ptr(_conv_params(conv)), _ptr(np.ascontiguousarray(w, np.float64)),
+                               _ptr(np.ascontiguousarray(x, np.float64)), _ptr(y)), "direct_fwd")
+    return y
+
+
+def direct_dgrad(conv, w, gy):
+    gx = np.zeros((conv["n"], conv["cin"], conv["h"], conv["w"]), dtype=np.float64)
+    _check(load().o_direct_dgrad(_ptr(_conv_params(conv)), _ptr(np.ascontiguousarray(w, np.float64)),
+                                 _ptr(np.ascontiguousarray(gy, np.float64)), _ptr(gx)), "direct_dgrad")
+    return gx
+
+
+def direct_wgrad(conv, gy, x):
+    gw = np.zeros((conv["cout"], conv["cin"], conv["kh"], conv["kw"]), dtype=np.float64)
+    _check(load().o_direct_wgrad(_ptr(_conv_params(conv)), _ptr(np.ascontiguousarray(gy, np.float64)),
+                                 _ptr(np.ascontiguousarray(x, np.float64)), _ptr(gw)), "direct_wgrad")
+    return gw
+
+
+def quantize_1d(m, direction, fmt):
+    """Naive comparator's quantizer on a 2-D fp32 matrix: 1-D blocks of 32
+    along rows (direction 0) or columns (direction 1)."""
+    lib = load()
+    m = np.ascontiguousarray(m, dtype=np.float32)
+    rows, cols = m.shape
+    bits = 8 if fmt == E4M3 else 4
+    codes = np.zeros((rows * cols * bits + 7) // 8, dtype=np.uint8)
+    if direction == 0:
+        scales = np.zeros(rows * ((cols + 31) // 32), dtype=np.uint8)
+    else:
+        scales = np.zeros(((rows + 31) // 32) * cols, dtype=np.uint8)
+    _check(lib.o_quantize_1d(_ptr(m), rows, cols, direction, fmt, _ptr(codes), _ptr(scales)),
+           "quantize_1d")
+    return codes, scales
+
+
+def counter_get():
+    return load().o_counter_get()
+
+
+def counter_reset():
+    load().o_counter_reset()

@@ -1,0 +1,810 @@
+/*
+ * mxoracle.c -- CPU oracle for quantize-once MX convolution (MicroQonv).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may link, load or
+ * call this file: only the test suite, the smoke check and the CPU-baseline
+ * leg of the benchmark do.  It shares no code, header, table or constant
+ * with the GPU library; the only thing the two sides have in common is the
+ * seeded input generator, which holds none of the method's arithmetic.
+ *
+ * Everything here is a plain, slow, obviously-correct definition written
+ * in fp64 loops (OpenMP only splits the outermost loop of the big ones):
+ *
+ *   o_encode / o_decode   one element to/from FP8 E4M3 or FP4 E2M1 (OCP MX
+ *                         element formats; the paper's number formats are
+ *                         introduced in Sec. II-D and Sec. III-A).
+ *   o_quantize            microscaling quantizer, Sec. III-A Eqs. (4)-(6) in
+ *                         its OCP-MX form: one E8M0 power-of-two scale per
+ *                         square block (Sec. IV-B), elements rounded to
+ *                         nearest-even with saturation.
+ *   o_dequant             fake quantization: element value times the block
+ *                         scale (Sec. III-A, below Eq. (6)).
+ *   o_im2col_cbf          channel-batch-first im2col applied to MX codes
+ *                         (Sec. IV-A; Fig. 3).
+ *   o_fwd / o_wgrad /     the three GEMMs of Sec. IV-B,
+ *   o_dgrad                 Y_f = W_f X',  G_Wf = G_Yf X'^T,  G_X' = W_f^T G_Yf,
+ *                         on dequantized operands, with the reordering back to
+ *                         NCHW/OIHW (a col2im scatter-add for G_X').
+ *   o_direct_*            brute-force definitions of Eqs. (1)-(3).
+ *   o_*_at                single outputs of Eqs. (1)-(3), for sampled checks
+ *                         at sizes where the full GEMMs are too slow.
+ *   o_quantize_1d         the naive comparator's quantizer: 1-D blocks of 32
+ *                         along one matrix direction (Sec. III-C, Dacapo).
+ *
+ * Readings of the paper that this file fixes (the paper uses NVFP with 8x8
+ * blocks; the build uses OCP MX):
+ *   - scale code = clamp(floor(log2 amax) - emax, -127, 127) + 127 where
+ *     emax is 8 for E4M3 and 2 for E2M1; amax == 0 gives code 0; a block
+ *     holding a NaN or infinity gets code 0xFF and all-zero element codes.
+ *   - elements: x * 2^-s rounded to nearest, ties to even, magnitudes above
+ *     the format maximum saturate (448 or 6); the sign of zero is kept.
+ *   - block = 32 channels x Bn batch samples at one pixel, Bn = min(32, N);
+ *     for weights 32 input channels x 32 output channels at one tap.
+ *   - code layout [N/Bn][H][W][Cp][Bn] (Bn fastest), scales
+ *     [N/Bn][H][W][Cp/32]; FP4 packs two consecutive codes per byte, the
+ *     even one in the low nibble.  Cp = C rounded up to 32; padding is +0.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <fenv.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+enum { O_E4M3 = 0, O_E2M1 = 1 };
+enum { O_NCHW = 0, O_NHWC = 1, O_CBF = 2 };
+enum { O_ACT = 0, O_WEIGHT = 1 };
+
+/* ------------------------------------------------------------------ */
+/* element formats                                                     */
+/* ------------------------------------------------------------------ */
+typedef struct {
+    int bits, mbits, bias, emax;
+    double maxval;      /* largest finite magnitude */
+    double min_normal;  /* 2^(1-bias) */
+    double quantum;     /* subnormal spacing 2^(1-bias-mbits) */
+} o_fmt;
+
+static int fmt_get(int fmt, o_fmt *f)
+{
+    if (fmt == O_E4M3) {
+        f->bits = 8; f->mbits = 3; f->bias = 7; f->emax = 8;
+        f->maxval = 448.0; f->min_normal = ldexp(1.0, -6); f->quantum = ldexp(1.0, -9);
+        return 0;
+    }
+    if (fmt == O_E2M1) {
+        f->bits = 4; f->mbits = 1; f->bias = 1; f->emax = 2;
+        f->maxval = 6.0; f->min_normal = 1.0; f->quantum = 0.5;
+        return 0;
+    }
+    return -2;
+}
+
+/* Round v (already divided by the block scale) to the element format:
+ * nearest value, ties to the even code, saturating, sign of zero kept.
+ * The route is frexp + nearbyint in the default rounding mode, which is
+ * round-half-to-even. */
+int o_encode(double v, int fmt)
+{
+    o_fmt f;
+    if (fmt_get(fmt, &f)) return -1;
+    int sign = signbit(v) ? 1 : 0;
+    double a = fabs(v);
+    if (a > f.maxval) a = f.maxval;
+    int code;
+    if (a < f.min_normal) {
+        code = (int)nearbyint(a / f.quantum);          /* 0 .. 2^mbits */
+    } else {
+        int e2;
+        double m = frexp(a, &e2);                       /* a = m 2^e2, m in [0.5,1) */
+        int ue = e2 - 1;                                /* a = (1+frac) 2^ue */
+        double frac = m * 2.0 - 1.0;
+        int q = (int)nearbyint(frac * (double)(1 << f.mbits));
+        code = ((ue + f.bias) << f.mbits) + q;          /* q == 2^mbits carries */
+    }
+    return code | (sign << (f.bits - 1));
+}
+
+double o_decode(int code, int fmt)
+{
+    o_fmt f;
+    if (fmt_get(fmt, &f)) return NAN;
+    int sign = (code >> (f.bits - 1)) & 1;
+    int mag = code & ((1 << (f.bits - 1)) - 1);
+    if (fmt == O_E4M3 && mag == 0x7F) return NAN;
+    int ef = mag >> f.mbits, mf = mag & ((1 << f.mbits) - 1);
+    double v;
+    if (ef == 0) v = mf * f.quantum;
+    else v = ldexp(1.0 + (double)mf / (double)(1 << f.mbits), ef - f.bias);
+    return sign ? -v : v;
+}
+
+/* E8M0 scale code -> 2^(code-127); 0xFF is NaN. */
+double o_scale_value(int scode)
+{
+    if (scode == 0xFF) return NAN;
+    return ldexp(1.0, scode - 127);
+}
+
+/* Scale code of a block with largest magnitude amax (finite). */
+int o_scale_code(double amax, int fmt)
+{
+    o_fmt f;
+    if (fmt_get(fmt, &f)) return -1;
+    if (amax == 0.0) return 0;
+    int e2;
+    frexp(amax, &e2);
+    int e = e2 - 1;                                  /* floor(log2 amax) */
+    int s = e - f.emax;
+    if (s < -127) s = -127;
+    if (s > 127) s = 127;
+    return s + 127;
+}
+
+/* ------------------------------------------------------------------ */
+/* tensor geometry of an MX tensor                                     */
+/* ------------------------------------------------------------------ */
+typedef struct { int n, c, h, w, bn, np, cp, bits; } o_geom;
+
+static int geom_init(o_geom *g, int role, int fmt, int n, int c, int h, int w)
+{
+    o_fmt f;
+    if (fmt_get(fmt, &f)) return -2;
+    if (n <= 0 || c <= 0 || h <= 0 || w <= 0) return -2;
+    g->n = n; g->c = c; g->h = h; g->w = w; g->bits = f.bits;
+    g->cp = (c + 31) / 32 * 32;
+    if (role == O_WEIGHT) {
+        g->bn = 32;
+        g->np = (n + 31) / 32 * 32;
+    } else if (role == O_ACT) {
+        if (n >= 32) {
+            if (n % 32) return -3;
+            g->bn = 32;
+        } else {
+            if (32 % n) return -3;
+            g->bn = n;
+        }
+        g->np = n;
+        if (fmt == O_E2M1 && g->bn == 1) return -3;
+    } else {
+        return -2;
+    }
+    return 0;
+}
+
+int64_t o_codes_bytes(int role, int fmt, int n, int c, int h, int w)
+{
+    o_geom g;
+    if (geom_init(&g, role, fmt, n, c, h, w)) return -1;
+    int64_t elems = (int64_t)g.np * g.h * g.w * g.cp;
+    return g.bits == 8 ? elems : elems / 2;
+}
+
+int64_t o_scales_bytes(int role, int fmt, int n, int c, int h, int w)
+{
+    o_geom g;
+    if (geom_init(&g, role, fmt, n, c, h, w)) return -1;
+    return (int64_t)(g.np / g.bn) * g.h * g.w * (g.cp / 32);
+}
+
+/* linear position of element (nb, hh, ww, cc, j) in the code array */
+static int64_t code_pos(const o_geom *g, int nb, int hh, int ww, int cc, int j)
+{
+    return ((((int64_t)nb * g->h + hh) * g->w + ww) * g->cp + cc) * g->bn + j;
+}
+
+static int64_t scale_pos(const o_geom *g, int nb, int hh, int ww, int cb)
+{
+    return (((int64_t)nb * g->h + hh) * g->w + ww) * (g->cp / 32) + cb;
+}
+
+static void put_code(uint8_t *codes, int bits, int64_t pos, int code)
+{
+    if (bits == 8) { codes[pos] = (uint8_t)code; return; }
+    uint8_t *b = &codes[pos >> 1];
+    if (pos & 1) *b = (uint8_t)((*b & 0x0F) | (code << 4));
+    else         *b = (uint8_t)((*b & 0xF0) | (code & 0x0F));
+}
+
+static int get_code(const uint8_t *codes, int bits, int64_t pos)
+{
+    if (bits == 8) return codes[pos];
+    uint8_t b = codes[pos >> 1];
+    return (pos & 1) ? (b >> 4) : (b & 0x0F);
+}
+
+/* value of logical element (n, c, h, w) of a float source in a layout */
+static double src_at(const float *src, int layout, const o_geom *g, int n, int c, int h, int w)
+{
+    int64_t i;
+    if (layout == O_NCHW)      i = (((int64_t)n * g->c + c) * g->h + h) * g->w + w;
+    else if (layout == O_NHWC) i = (((int64_t)n * g->h + h) * g->w + w) * g->c + c;
+    else {                                  /* [N/Bn][H][W][C][Bn], real C */
+        int nb = n / g->bn, j = n % g->bn;
+        i = ((((int64_t)nb * g->h + h) * g->w + w) * g->c + c) * g->bn + j;
+    }
+    return (double)src[i];
+}
+
+static int64_t o_quantized_count = 0;
+int64_t o_counter_get(void) { return o_quantized_count; }
+void o_counter_reset(void) { o_quantized_count = 0; }
+
+void o_set_threads(int t)
+{
+#ifdef _OPENMP
+    if (t > 0) omp_set_num_threads(t);
+#else
+    (void)t;
+#endif
+}
+
+int o_get_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+/* Quantize a float tensor into MX-CBF codes and E8M0 scales.
+ * src: logical (n, c, h, w) tensor in `layout` (weights: OIHW, i.e. NCHW
+ * with n = Cout, c = Cin).  codes/scales sized by o_codes_bytes/o_scales_bytes.
+ * Returns 0, or a negative error. */
+int o_quantize(const float *src, int layout, int role, int fmt,
+               int n, int c, int h, int w, uint8_t *codes, uint8_t *scales)
+{
+    o_geom g;
+    o_fmt f;
+    int rc = geom_init(&g, role, fmt, n, c, h, w);
+    if (rc) return rc;
+    fmt_get(fmt, &f);
+    if (layout < O_NCHW || layout > O_CBF) return -2;
+    if (layout == O_CBF && role != O_ACT) return -2;
+    int ngroups = g.np / g.bn, ncb = g.cp / 32;
+    int64_t ntiles = (int64_t)ngroups * g.h * g.w * ncb;
+    fesetround(FE_TONEAREST);
+    #pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < ntiles; t++) {
+        int cb = (int)(t % ncb);
+        int64_t r = t / ncb;
+        int ww = (int)(r % g.w); r /= g.w;
+        int hh = (int)(r % g.h);
+        int nb = (int)(r / g.h);
+        double vals[32][32];
+        double amax = 0.0;
+        int nonfinite = 0;
+        for (int ci = 0; ci < 32; ci++) {
+            for (int j = 0; j < g.bn; j++) {
+                int nn = nb * g.bn + j, cc = cb * 32 + ci;
+                double x = (nn < g.n && cc < g.c) ? src_at(src, layout, &g, nn, cc, hh, ww) : 0.0;
+                vals[ci][j] = x;
+                if (!isfinite(x)) nonfinite = 1;
+                else if (fabs(x) > amax) amax = fabs(x);
+            }
+        }
+        int scode = nonfinite ? 0xFF : o_scale_code(amax, fmt);
+        scales[scale_pos(&g, nb, hh, ww, cb)] = (uint8_t)scode;
+        int s = scode - 127;
+        for (int ci = 0; ci < 32; ci++) {
+            for (int j = 0; j < g.bn; j++) {
+                int code = nonfinite ? 0 : o_encode(ldexp(vals[ci][j], -s), fmt);
+                put_code(codes, g.bits, code_pos(&g, nb, hh, ww, cb * 32 + ci, j), code);
+            }
+        }
+    }
+    o_quantized_count += (int64_t)g.n * g.c * g.h * g.w;
+    return 0;
+}
+
+/* Dequantize to a real-sized fp64 tensor (n, c, h, w) in NCHW order. */
+int o_dequant(const uint8_t *codes, const uint8_t *scales, int role, int fmt,
+              int n, int c, int h, int w, double *out)
+{
+    o_geom g;
+    int rc = geom_init(&g, role, fmt, n, c, h, w);
+    if (rc) return rc;
+    #pragma omp parallel for schedule(static)
+    for (int nn = 0; nn < n; nn++)
+        for (int cc = 0; cc < c; cc++)
+            for (int hh = 0; hh < h; hh++)
+                for (int ww = 0; ww < w; ww++) {
+                    int nb = nn / g.bn, j = nn % g.bn;
+                    int code = get_code(codes, g.bits, code_pos(&g, nb, hh, ww, cc, j));
+                    int sc = scales[scale_pos(&g, nb, hh, ww, cc / 32)];
+                    out[(((int64_t)nn * c + cc) * h + hh) * w + ww] =
+                        o_decode(code, fmt) * o_scale_value(sc);
+                }
+    return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* convolution geometry                                                */
+/* ------------------------------------------------------------------ */
+typedef struct { int n, cin, cout, h, w, kh, kw, sh, sw, ph, pw, ho, wo; } o_conv;
+
+static int conv_init(o_conv *cv, const int *p)
+{
+    cv->n = p[0]; cv->cin = p[1]; cv->cout = p[2]; cv->h = p[3]; cv->w = p[4];
+    cv->kh = p[5]; cv->kw = p[6]; cv->sh = p[7]; cv->sw = p[8]; cv->ph = p[9]; cv->pw = p[10];
+    if (cv->n <= 0 || cv->cin <= 0 || cv->cout <= 0 || cv->h <= 0 || cv->w <= 0 ||
+        cv->kh <= 0 || cv->kw <= 0 || cv->sh <= 0 || cv->sw <= 0 || cv->ph < 0 || cv->pw < 0)
+        return -2;
+    /* cross-correlation with zero padding, dilation 1 */
+    cv->ho = (cv->h + 2 * cv->ph - cv->kh) / cv->sh + 1;
+    cv->wo = (cv->w + 2 * cv->pw - cv->kw) / cv->sw + 1;
+    if (cv->h + 2 * cv->ph < cv->kh || cv->w + 2 * cv->pw < cv->kw) return -3;
+    return 0;
+}
+
+int o_conv_out(const int *p, int *ho, int *wo)
+{
+    o_conv cv;
+    int rc = conv_init(&cv, p);
+    if (rc) return rc;
+    *ho = cv.ho; *wo = cv.wo;
+    return 0;
+}
+
+/* Channel-batch-first im2col on MX codes (Sec. IV-A):
+ *   X'[nb][ho][wo][kh][kw][c][j] = X[nb][ho*sh+kh-ph][wo*sw+kw-pw][c][j],
+ * copying codes and the block's scale; taps that fall in the zero padding
+ * become all-zero blocks with scale code 0 (the quantization of a +0 block). */
+int o_im2col_cbf(const int *p, int fmt, const uint8_t *xcodes, const uint8_t *xscales,
+                 uint8_t *ccodes, uint8_t *cscales)
+{
+    o_conv cv;
+    o_geom gx, gc;
+    int rc = conv_init(&cv, p);
+    if (rc) return rc;
+    if ((rc = geom_init(&gx, O_ACT, fmt, cv.n, cv.cin, cv.h, cv.w))) return rc;
+    /* the im2col tensor viewed as an activation tensor with
+     * H = Ho*Wo*Kh*Kw pixels and W = 1 */
+    if ((rc = geom_init(&gc, O_ACT, fmt, cv.n, cv.cin, cv.ho * cv.wo * cv.kh * cv.kw, 1))) return rc;
+    int ngroups = cv.n / gx.bn;
+    for (int nb = 0; nb < ngroups; nb++)
+      for (int oh = 0; oh < cv.ho; oh++)
+        for (int ow = 0; ow < cv.wo; ow++)
+          for (int a = 0; a < cv.kh; a++)
+            for (int b = 0; b < cv.kw; b++) {
+              int ih = oh * cv.sh + a - cv.ph, iw = ow * cv.sw + b - cv.pw;
+              int inside = ih >= 0 && ih < cv.h && iw >= 0 && iw < cv.w;
+              int pix = ((oh * cv.wo + ow) * cv.kh + a) * cv.kw + b;
+              for (int cb = 0; cb < gx.cp / 32; cb++)
+                cscales[scale_pos(&gc, nb, pix, 0, cb)] =
+                    inside ? xscales[scale_pos(&gx, nb, ih, iw, cb)] : 0;
+              for (int cc = 0; cc < gx.cp; cc++)
+                for (int j = 0; j < gx.bn; j++)
+                  put_code(ccodes, gc.bits, code_pos(&gc, nb, pix, 0, cc, j),
+                           inside ? get_code(xcodes, gx.bits, code_pos(&gx, nb, ih, iw, cc, j)) : 0);
+            }
+    return 0;
+}
+
+int64_t o_im2col_codes_bytes(const int *p, int fmt)
+{
+    o_conv cv;
+    if (conv_init(&cv, p)) return -1;
+    return o_codes_bytes(O_ACT, fmt, cv.n, cv.cin, cv.ho * cv.wo * cv.kh * cv.kw, 1);
+}
+
+int64_t o_im2col_scales_bytes(const int *p, int fmt)
+{
+    o_conv cv;
+    if (conv_init(&cv, p)) return -1;
+    return o_scales_bytes(O_ACT, fmt, cv.n, cv.cin, cv.ho * cv.wo * cv.kh * cv.kw, 1);
+}
+
+/* ------------------------------------------------------------------ */
+/* the three GEMMs of Sec. IV-B on dequantized operands                */
+/* ------------------------------------------------------------------ */
+/* Dequantized X' as a (Kh Kw Cin) x (Ho Wo N) matrix: row (kh, kw, ci) with
+ * ci fastest, column (ho, wo, n) with n fastest (the paper's X'_{Cin,N}). */
+static double *build_xcol(const o_conv *cv, int fmt, const uint8_t *xcodes, const uint8_t *xscales)
+{
+    int pp[11] = {cv->n, cv->cin, cv->cout, cv->h, cv->w, cv->kh, cv->kw, cv->sh, cv->sw, cv->ph, cv->pw};
+    int64_t cb = o_im2col_codes_bytes(pp, fmt), sb = o_im2col_scales_bytes(pp, fmt);
+    uint8_t *cc = (uint8_t *)calloc((size_t)cb, 1), *cs = (uint8_t *)calloc((size_t)sb, 1);
+    int hcol = cv->ho * cv->wo * cv->kh * cv->kw;
+    double *xd = (double *)malloc(sizeof(double) * (size_t)cv->n * cv->cin * hcol);
+    int64_t K = (int64_t)cv->kh * cv->kw * cv->cin, NC = (int64_t)cv->ho * cv->wo * cv->n;
+    double *xcol = (double *)malloc(sizeof(double) * (size_t)(K * NC));
+    o_im2col_cbf(pp, fmt, xcodes, xscales, cc, cs);
+    o_dequant(cc, cs, O_ACT, fmt, cv->n, cv->cin, hcol, 1, xd);     /* [n][ci][pix] */
+    #pragma omp parallel for schedule(static)
+    for (int64_t pix = 0; pix < (int64_t)cv->ho * cv->wo; pix++)
+        for (int a = 0; a < cv->kh; a++)
+            for (int b = 0; b < cv->kw; b++)
+                for (int ci = 0; ci < cv->cin; ci++)
+                    for (int nn = 0; nn < cv->n; nn++) {
+                        int64_t row = ((int64_t)a * cv->kw + b) * cv->cin + ci;
+                        int64_t col = pix * cv->n + nn;
+                        int64_t p4 = (pix * cv->kh + a) * cv->kw + b;
+                        xcol[row * NC + col] = xd[((int64_t)nn * cv->cin + ci) * hcol + p4];
+                    }
+    free(cc); free(cs); free(xd);
+    return xcol;
+}
+
+/* W_f as Cout x (Kh Kw Cin), row-major. */
+static double *build_wf(const o_conv *cv, int fmt, const uint8_t *wcodes, const uint8_t *wscales)
+{
+    double *wd = (double *)malloc(sizeof(double) * (size_t)cv->cout * cv->cin * cv->kh * cv->kw);
+    o_dequant(wcodes, wscales, O_WEIGHT, fmt, cv->cout, cv->cin, cv->kh, cv->kw, wd);
+    int64_t K = (int64_t)cv->kh * cv->kw * cv->cin;
+    double *wf = (double *)malloc(sizeof(double) * (size_t)(cv->cout * K));
+    for (int co = 0; co < cv->cout; co++)
+        for (int ci = 0; ci < cv->cin; ci++)
+            for (int a = 0; a < cv->kh; a++)
+                for (int b = 0; b < cv->kw; b++)
+                    wf[co * K + ((int64_t)a * cv->kw + b) * cv->cin + ci] =
+                        wd[(((int64_t)co * cv->cin + ci) * cv->kh + a) * cv->kw + b];
+    free(wd);
+    return wf;
+}
+
+/* G_Yf as Cout x (Ho Wo N), row-major, column (ho, wo, n) with n fastest. */
+static double *build_gyf(const o_conv *cv, int fmt, const uint8_t *gcodes, const uint8_t *gscales)
+{
+    int64_t NC = (int64_t)cv->ho * cv->wo * cv->n;
+    double *gd = (double *)malloc(sizeof(double) * (size_t)(NC * cv->cout));
+    o_dequant(gcodes, gscales, O_ACT, fmt, cv->n, cv->cout, cv->ho, cv->wo, gd);
+    double *gf = (double *)malloc(sizeof(double) * (size_t)(NC * cv->cout));
+    for (int nn = 0; nn < cv->n; nn++)
+        for (int co = 0; co < cv->cout; co++)
+            for (int oh = 0; oh < cv->ho; oh++)
+                for (int ow = 0; ow < cv->wo; ow++)
+                    gf[co * NC + ((int64_t)oh * cv->wo + ow) * cv->n + nn] =
+                        gd[(((int64_t)nn * cv->cout + co) * cv->ho + oh) * cv->wo + ow];
+    free(gd);
+    return gf;
+}
+
+/* Forward: Y_f = W_f X', reordered to Y[n][co][ho][wo].  sabs (optional)
+ * receives sum_k |W_f[co][k] X'[k][col]|, the scale of the rounding error. */
+int o_fwd(const int *p, int fmt, const uint8_t *wcodes, const uint8_t *wscales,
+          const uint8_t *xcodes, const uint8_t *xscales, double *y, double *sabs)
+{
+    o_conv cv;
+    o_geom g;
+    int rc = conv_init(&cv, p);
+    if (rc) return rc;
+    if ((rc = geom_init(&g, O_ACT, fmt, cv.n, cv.cin, cv.h, cv.w))) return rc;
+    double *xcol = build_xcol(&cv, fmt, xcodes, xscales);
+    double *wf = build_wf(&cv, fmt, wcodes, wscales);
+    int64_t K = (int64_t)cv.kh * cv.kw * cv.cin, NC = (int64_t)cv.ho * cv.wo * cv.n;
+    #pragma omp parallel for schedule(dynamic)
+    for (int co = 0; co < cv.cout; co++) {
+        double *acc = (double *)calloc((size_t)NC, sizeof(double));
+        double *aab = (double *)calloc((size_t)NC, sizeof(double));
+        for (int64_t k = 0; k < K; k++) {
+            double a = wf[co * K + k];
+            const double *xr = &xcol[k * NC];
+            for (int64_t col = 0; col < NC; col++) {
+                acc[col] += a * xr[col];
+                aab[col] += fabs(a * xr[col]);
+            }
+        }
+        for (int64_t col = 0; col < NC; col++) {
+            int nn = (int)(col % cv.n);
+            int64_t pix = col / cv.n;
+            int64_t o = ((int64_t)nn * cv.cout + co) * cv.ho * cv.wo + pix;
+            y[o] = acc[col];
+            if (sabs) sabs[o] = aab[col];
+        }
+        free(acc); free(aab);
+    }
+    free(xcol); free(wf);
+    return 0;
+}
+
+/* Weight gradient: G_Wf = G_Yf X'^T, reordered to G_W[co][ci][kh][kw]. */
+int o_wgrad(const int *p, int fmt, const uint8_t *gcodes, const uint8_t *gscales,
+            const uint8_t *xcodes, const uint8_t *xscales, double *gw, double *sabs)
+{
+    o_conv cv;
+    o_geom g;
+    int rc = conv_init(&cv, p);
+    if (rc) return rc;
+    if ((rc = geom_init(&g, O_ACT, fmt, cv.n, cv.cin, cv.h, cv.w))) return rc;
+    double *xcol = build_xcol(&cv, fmt, xcodes, xscales);
+    double *gf = build_gyf(&cv, fmt, gcodes, gscales);
+    int64_t K = (int64_t)cv.kh * cv.kw * cv.cin, NC = (int64_t)cv.ho * cv.wo * cv.n;
+    #pragma omp parallel for schedule(dynamic) collapse(2)
+    for (int co = 0; co < cv.cout; co++)
+        for (int64_t k = 0; k < K; k++) {
+            double acc = 0.0, aab = 0.0;
+            const double *gr = &gf[co * NC], *xr = &xcol[k * NC];
+            for (int64_t col = 0; col < NC; col++) {
+                acc += gr[col] * xr[col];
+                aab += fabs(gr[col] * xr[col]);
+            }
+            int ci = (int)(k % cv.cin);
+            int64_t tap = k / cv.cin;
+            int a = (int)(tap / cv.kw), b = (int)(tap % cv.kw);
+            int64_t o = (((int64_t)co * cv.cin + ci) * cv.kh + a) * cv.kw + b;
+            gw[o] = acc;
+            if (sabs) sabs[o] = aab;
+        }
+    free(xcol); free(gf);
+    return 0;
+}
+
+/* Input gradient: G_X' = W_f^T G_Yf, then the col2im scatter-add that turns
+ * the (Kh Kw Cin) x (Ho Wo N) matrix back into G_X[n][ci][h][w]. */
+int o_dgrad(const int *p, int fmt, const uint8_t *wcodes, const uint8_t *wscales,
+            const uint8_t *gcodes, const uint8_t *gscales, double *gx, double *sabs)
+{
+    o_conv cv;
+    o_geom g;
+    int rc = conv_init(&cv, p);
+    if (rc) return rc;
+    if ((rc = geom_init(&g, O_ACT, fmt, cv.n, cv.cout, cv.ho, cv.wo))) return rc;
+    double *wf = build_wf(&cv, fmt, wcodes, wscales);
+    double *gf = build_gyf(&cv, fmt, gcodes, gscales);
+    int64_t K = (int64_t)cv.kh * cv.kw * cv.cin, NC = (int64_t)cv.ho * cv.wo * cv.n;
+    double *gcol = (double *)malloc(sizeof(double) * (size_t)(K * NC));
+    double *scol = (double *)malloc(sizeof(double) * (size_t)(K * NC));
+    #pragma omp parallel for schedule(dynamic)
+    for (int64_t k = 0; k < K; k++) {
+        double *acc = &gcol[k * NC], *aab = &scol[k * NC];
+        for (int64_t col = 0; col < NC; col++) { acc[col] = 0.0; aab[col] = 0.0; }
+        for (int co = 0; co < cv.cout; co++) {
+            double a = wf[co * K + k];
+            const double *gr = &gf[co * NC];
+            for (int64_t col = 0; col < NC; col++) {
+                acc[col] += a * gr[col];
+                aab[col] += fabs(a * gr[col]);
+            }
+        }
+    }
+    int64_t nx = (int64_t)cv.n * cv.cin * cv.h * cv.w;
+    for (int64_t i = 0; i < nx; i++) { gx[i] = 0.0; if (sabs) sabs[i] = 0.0; }
+    /* col2im: parallel over (n, ci) rows, which own disjoint outputs */
+    #pragma omp parallel for schedule(static) collapse(2)
+    for (int nn = 0; nn < cv.n; nn++)
+        for (int ci = 0; ci < cv.cin; ci++)
+            for (int oh = 0; oh < cv.ho; oh++)
+                for (int ow = 0; ow < cv.wo; ow++)
+                    for (int a = 0; a < cv.kh; a++)
+                        for (int b = 0; b < cv.kw; b++) {
+                            int ih = oh * cv.sh + a - cv.ph, iw = ow * cv.sw + b - cv.pw;
+                            if (ih < 0 || ih >= cv.h || iw < 0 || iw >= cv.w) continue;
+                            int64_t k = ((int64_t)a * cv.kw + b) * cv.cin + ci;
+                            int64_t col = ((int64_t)oh * cv.wo + ow) * cv.n + nn;
+                            int64_t o = (((int64_t)nn * cv.cin + ci) * cv.h + ih) * cv.w + iw;
+                            gx[o] += gcol[k * NC + col];
+                            if (sabs) sabs[o] += scol[k * NC + col];
+                        }
+    free(wf); free(gf); free(gcol); free(scol);
+    return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* brute-force definitions, Eqs. (1)-(3), on fp64 NCHW tensors          */
+/* ------------------------------------------------------------------ */
+int o_direct_fwd(const int *p, const double *w, const double *x, double *y)
+{
+    o_conv cv;
+    int rc = conv_init(&cv, p);
+    if (rc) return rc;
+    #pragma omp parallel for schedule(static) collapse(2)
+    for (int nn = 0; nn < cv.n; nn++)
+        for (int co = 0; co < cv.cout; co++)
+            for (int oh = 0; oh < cv.ho; oh++)
+                for (int ow = 0; ow < cv.wo; ow++) {
+                    double s = 0.0;
+                    for (int ci = 0; ci < cv.cin; ci++)
+                        for (int a = 0; a < cv.kh; a++)
+                            for (int b = 0; b < cv.kw; b++) {
+                                int ih = oh * cv.sh + a - cv.ph, iw = ow * cv.sw + b - cv.pw;
+                                if (ih < 0 || ih >= cv.h || iw < 0 || iw >= cv.w) continue;
+                                s += w[(((int64_t)co * cv.cin + ci) * cv.kh + a) * cv.kw + b] *
+                                     x[(((int64_t)nn * cv.cin + ci) * cv.h + ih) * cv.w + iw];
+                            }
+                    y[(((int64_t)nn * cv.cout + co) * cv.ho + oh) * cv.wo + ow] = s;
+                }
+    return 0;
+}
+
+/* G_X[n][ci][h][w] = sum over (co, kh, kw, ho, wo) with ho*sh+kh-ph == h and
+ * wo*sw+kw-pw == w of W[co][ci][kh][kw] G_Y[n][co][ho][wo] (Eq. (2): the
+ * convolution of G_Y with the channel-swapped kernel). */
+int o_direct_dgrad(const int *p, const double *w, const double *gy, double *gx)
+{
+    o_conv cv;
+    int rc = conv_init(&cv, p);
+    if (rc) return rc;
+    #pragma omp parallel for schedule(static) collapse(2)
+    for (int nn = 0; nn < cv.n; nn++)
+        for (int ci = 0; ci < cv.cin; ci++)
+            for (int ih = 0; ih < cv.h; ih++)
+                for (int iw = 0; iw < cv.w; iw++) {
+                    double s = 0.0;
+                    for (int co = 0; co < cv.cout; co++)
+                        for (int a = 0; a < cv.kh; a++)
+                            for (int b = 0; b < cv.kw; b++) {
+                                int th = ih + cv.ph - a, tw = iw + cv.pw - b;
+                                if (th < 0 || tw < 0 || th % cv.sh || tw % cv.sw) continue;
+                                int oh = th / cv.sh, ow = tw / cv.sw;
+                                if (oh >= cv.ho || ow >= cv.wo) continue;
+                                s += w[(((int64_t)co * cv.cin + ci) * cv.kh + a) * cv.kw + b] *
+                                     gy[(((int64_t)nn * cv.cout + co) * cv.ho + oh) * cv.wo + ow];
+                            }
+                    gx[(((int64_t)nn * cv.cin + ci) * cv.h + ih) * cv.w + iw] = s;
+                }
+    return 0;
+}
+
+int o_direct_wgrad(const int *p, const double *gy, const double *x, double *gw)
+{
+    o_conv cv;
+    int rc = conv_init(&cv, p);
+    if (rc) return rc;
+    #pragma omp parallel for schedule(static) collapse(2)
+    for (int co = 0; co < cv.cout; co++)
+        for (int ci = 0; ci < cv.cin; ci++)
+            for (int a = 0; a < cv.kh; a++)
+                for (int b = 0; b < cv.kw; b++) {
+                    double s = 0.0;
+                    for (int nn = 0; nn < cv.n; nn++)
+                        for (int oh = 0; oh < cv.ho; oh++)
+                            for (int ow = 0; ow < cv.wo; ow++) {
+                                int ih = oh * cv.sh + a - cv.ph, iw = ow * cv.sw + b - cv.pw;
+                                if (ih < 0 || ih >= cv.h || iw < 0 || iw >= cv.w) continue;
+                                s += gy[(((int64_t)nn * cv.cout + co) * cv.ho + oh) * cv.wo + ow] *
+                                     x[(((int64_t)nn * cv.cin + ci) * cv.h + ih) * cv.w + iw];
+                            }
+                    gw[(((int64_t)co * cv.cin + ci) * cv.kh + a) * cv.kw + b] = s;
+                }
+    return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* single outputs, straight from the MX codes (sampled checks)         */
+/* ------------------------------------------------------------------ */
+static double mx_elem(const uint8_t *codes, const uint8_t *scales, const o_geom *g, int fmt,
+                      int nn, int cc, int hh, int ww)
+{
+    int nb = nn / g->bn, j = nn % g->bn;
+    int code = get_code(codes, g->bits, code_pos(g, nb, hh, ww, cc, j));
+    return o_decode(code, fmt) * o_scale_value(scales[scale_pos(g, nb, hh, ww, cc / 32)]);
+}
+
+/* idx: cnt x 4 ints (n, co, ho, wo); out/sabs: cnt doubles */
+int o_fwd_at(const int *p, int fmt, const uint8_t *wcodes, const uint8_t *wscales,
+             const uint8_t *xcodes, const uint8_t *xscales, const int *idx, int64_t cnt,
+             double *out, double *sabs)
+{
+    o_conv cv;
+    o_geom gw, gx;
+    int rc = conv_init(&cv, p);
+    if (rc) return rc;
+    if ((rc = geom_init(&gw, O_WEIGHT, fmt, cv.cout, cv.cin, cv.kh, cv.kw))) return rc;
+    if ((rc = geom_init(&gx, O_ACT, fmt, cv.n, cv.cin, cv.h, cv.w))) return rc;
+    #pragma omp parallel for schedule(dynamic)
+    for (int64_t i = 0; i < cnt; i++) {
+        int nn = idx[4 * i], co = idx[4 * i + 1], oh = idx[4 * i + 2], ow = idx[4 * i + 3];
+        double s = 0.0, sa = 0.0;
+        for (int ci = 0; ci < cv.cin; ci++)
+            for (int a = 0; a < cv.kh; a++)
+                for (int b = 0; b < cv.kw; b++) {
+                    int ih = oh * cv.sh + a - cv.ph, iw = ow * cv.sw + b - cv.pw;
+                    if (ih < 0 || ih >= cv.h || iw < 0 || iw >= cv.w) continue;
+                    double t = mx_elem(wcodes, wscales, &gw, fmt, co, ci, a, b) *
+                               mx_elem(xcodes, xscales, &gx, fmt, nn, ci, ih, iw);
+                    s += t; sa += fabs(t);
+                }
+        out[i] = s; sabs[i] = sa;
+    }
+    return 0;
+}
+
+/* idx: cnt x 4 ints (n, ci, h, w) */
+int o_dgrad_at(const int *p, int fmt, const uint8_t *wcodes, const uint8_t *wscales,
+               const uint8_t *gcodes, const uint8_t *gscales, const int *idx, int64_t cnt,
+               double *out, double *sabs)
+{
+    o_conv cv;
+    o_geom gw, gg;
+    int rc = conv_init(&cv, p);
+    if (rc) return rc;
+    if ((rc = geom_init(&gw, O_WEIGHT, fmt, cv.cout, cv.cin, cv.kh, cv.kw))) return rc;
+    if ((rc = geom_init(&gg, O_ACT, fmt, cv.n, cv.cout, cv.ho, cv.wo))) return rc;
+    #pragma omp parallel for schedule(dynamic)
+    for (int64_t i = 0; i < cnt; i++) {
+        int nn = idx[4 * i], ci = idx[4 * i + 1], ih = idx[4 * i + 2], iw = idx[4 * i + 3];
+        double s = 0.0, sa = 0.0;
+        for (int co = 0; co < cv.cout; co++)
+            for (int a = 0; a < cv.kh; a++)
+                for (int b = 0; b < cv.kw; b++) {
+                    int th = ih + cv.ph - a, tw = iw + cv.pw - b;
+                    if (th < 0 || tw < 0 || th % cv.sh || tw % cv.sw) continue;
+                    int oh = th / cv.sh, ow = tw / cv.sw;
+                    if (oh >= cv.ho || ow >= cv.wo) continue;
+                    double t = mx_elem(wcodes, wscales, &gw, fmt, co, ci, a, b) *
+                               mx_elem(gcodes, gscales, &gg, fmt, nn, co, oh, ow);
+                    s += t; sa += fabs(t);
+                }
+        out[i] = s; sabs[i] = sa;
+    }
+    return 0;
+}
+
+/* idx: cnt x 4 ints (co, ci, kh, kw) */
+int o_wgrad_at(const int *p, int fmt, const uint8_t *gcodes, const uint8_t *gscales,
+               const uint8_t *xcodes, const uint8_t *xscales, const int *idx, int64_t cnt,
+               double *out, double *sabs)
+{
+    o_conv cv;
+    o_geom gx, gg;
+    int rc = conv_init(&cv, p);
+    if (rc) return rc;
+    if ((rc = geom_init(&gx, O_ACT, fmt, cv.n, cv.cin, cv.h, cv.w))) return rc;
+    if ((rc = geom_init(&gg, O_ACT, fmt, cv.n, cv.cout, cv.ho, cv.wo))) return rc;
+    #pragma omp parallel for schedule(dynamic)
+    for (int64_t i = 0; i < cnt; i++) {
+        int co = idx[4 * i], ci = idx[4 * i + 1], a = idx[4 * i + 2], b = idx[4 * i + 3];
+        double s = 0.0, sa = 0.0;
+        for (int nn = 0; nn < cv.n; nn++)
+            for (int oh = 0; oh < cv.ho; oh++)
+                for (int ow = 0; ow < cv.wo; ow++) {
+                    int ih = oh * cv.sh + a - cv.ph, iw = ow * cv.sw + b - cv.pw;
+                    if (ih < 0 || ih >= cv.h || iw < 0 || iw >= cv.w) continue;
+                    double t = mx_elem(gcodes, gscales, &gg, fmt, nn, co, oh, ow) *
+                               mx_elem(xcodes, xscales, &gx, fmt, nn, ci, ih, iw);
+                    s += t; sa += fabs(t);
+                }
+        out[i] = s; sabs[i] = sa;
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* naive comparator's quantizer (Sec. III-C: quantize in line blocks)   */
+/* ------------------------------------------------------------------ */
+/* m: rows x cols fp32 matrix, row-major.  dir 0: blocks of 32 consecutive
+ * elements along a row (the last block of a row is short if cols % 32);
+ * dir 1: blocks of 32 consecutive elements down a column.  codes: one
+ * code per element at the element's own position (FP4: two per byte,
+ * even position low); scales: dir 0 -> [rows][ceil(cols/32)],
+ * dir 1 -> [ceil(rows/32)][cols]. */
+int o_quantize_1d(const float *m, int64_t rows, int64_t cols, int dir, int fmt,
+                  uint8_t *codes, uint8_t *scales)
+{
+    o_fmt f;
+    if (fmt_get(fmt, &f)) return -2;
+    if (rows <= 0 || cols <= 0 || (dir != 0 && dir != 1)) return -2;
+    int64_t nbr = dir == 0 ? rows : (rows + 31) / 32;
+    int64_t nbc = dir == 0 ? (cols + 31) / 32 : cols;
+    fesetround(FE_TONEAREST);
+    #pragma omp parallel for schedule(static)
+    for (int64_t bi = 0; bi < nbr * nbc; bi++) {
+        int64_t br = bi / nbc, bc = bi % nbc;
+        int64_t pos[32];
+        int cnt = 0;
+        for (int t = 0; t < 32; t++) {
+            int64_t r = dir == 0 ? br : br * 32 + t;
+            int64_t c = dir == 0 ? bc * 32 + t : bc;
+            if (r < rows && c < cols) pos[cnt++] = r * cols + c;
+        }
+        double amax = 0.0;
+        int nonfinite = 0;
+        for (int t = 0; t < cnt; t++) {
+            double x = m[pos[t]];
+            if (!isfinite(x)) nonfinite = 1;
+            else if (fabs(x) > amax) amax = fabs(x);
+        }
+        int scode = nonfinite ? 0xFF : o_scale_code(amax, fmt);
+        scales[bi] = (uint8_t)scode;
+        for (int t = 0; t < cnt; t++) {
+            int code = nonfinite ? 0 : o_encode(ldexp((double)m[pos[t]], -(scode - 127)), fmt);
+            put_code(codes, f.bits, pos[t], code);
+        }
+    }
+    o_quantized_count += rows * cols;
+    return 0;
+}

@@ -1,0 +1,478 @@
+"""Pins for the CPU oracle (no GPU).
+
+Each test checks the oracle against something other than itself: the
+hand-worked blocks in tests/golden/, brute-force enumeration of the element
+formats, torch's float8 cast, torch's fp64 convolutions, F.unfold, the
+brute-force direct convolutions of Eqs. (1)-(3), and invariants of the
+quantizer.  A plausible slip in the oracle (a dropped term, a wrong sign or
+index, a transposed operand, the wrong rounding) fails at least one.
+"""
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+import oracle
+from paper_2609_28358_amd import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+FMTS = {"E4M3": oracle.E4M3, "E2M1": oracle.E2M1}
+EMAX = {oracle.E4M3: 8, oracle.E2M1: 2}
+MAXV = {oracle.E4M3: 448.0, oracle.E2M1: 6.0}
+
+
+def _parse_num(t):
+    t = t.strip()
+    if "0x" in t and "p" in t:
+        return float.fromhex(t)
+    if t.startswith("0x") or t.startswith("0X"):
+        return int(t, 16)
+    return float(t)
+
+
+def _golden_blocks():
+    rows = []
+    with open(os.path.join(GOLDEN, "mx_blocks.txt")) as f:
+        for line in f:
+            if not line.strip() or line.startswith("#"):
+                continue
+            name, fmt, vals, scale, codes = [p.strip() for p in line.split("|")]
+            rows.append((name, FMTS[fmt], [_parse_num(v) for v in vals.split()],
+                         int(scale), [int(_parse_num(c)) for c in codes.split()]))
+    return rows
+
+
+def _code_at(codes, fmt, pos):
+    if fmt == oracle.E4M3:
+        return int(codes[pos])
+    b = int(codes[pos // 2])
+    return (b >> 4) if pos % 2 else (b & 0xF)
+
+
+@pytest.mark.parametrize("row", _golden_blocks(), ids=lambda r: r[0])
+def test_hand_worked_blocks(row):
+    name, fmt, vals, scale, codes = row
+    x = np.zeros((32, 32, 1, 1), dtype=np.float32)     # N=32, C=32: one tile
+    for i, v in enumerate(vals):
+        x[i, 0, 0, 0] = v                               # sample i, channel 0
+    c, s = oracle.quantize(x, oracle.NCHW, oracle.ACT, fmt, 32, 32, 1, 1)
+    assert s.tolist() == [scale]
+    # code position of (channel 0, sample i) is i (samples fastest)
+    got = [_code_at(c, fmt, i) for i in range(len(vals))]
+    assert got == codes
+    # every untouched element is +0
+    rest = [_code_at(c, fmt, i) for i in range(len(vals), 32 * 32)]
+    assert all(r == 0 for r in rest)
+
+
+# ---------------------------------------------------------------- elements
+def _grid(fmt):
+    """(code, value) of every finite non-negative code."""
+    if fmt == oracle.E4M3:
+        u = torch.arange(0, 0x7F, dtype=torch.uint8)       # 0x7F is NaN
+        v = u.view(torch.float8_e4m3fn).double()
+        return list(zip(u.tolist(), v.tolist()))
+    mags = [0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0]         # E2M1 by definition
+    return list(enumerate(mags))
+
+
+def _brute_encode(v, fmt):
+    grid = _grid(fmt)
+    sign = 1 if math.copysign(1.0, v) < 0 else 0
+    a = min(abs(v), MAXV[fmt])
+    best = min(abs(a - g) for _, g in grid)
+    cands = [c for c, g in grid if abs(a - g) == best]
+    if len(cands) > 1:
+        cands = [c for c in cands if c % 2 == 0]            # tie -> even code
+    assert len(cands) == 1
+    bits = 8 if fmt == oracle.E4M3 else 4
+    return cands[0] | (sign << (bits - 1))
+
+
+@pytest.mark.parametrize("fmt", [oracle.E4M3, oracle.E2M1])
+def test_encode_matches_brute_force(fmt):
+    grid = [g for _, g in _grid(fmt)]
+    pts = set()
+    for a, b in zip(grid[:-1], grid[1:]):                  # values, midpoints, neighbours
+        m = (a + b) / 2
+        for t in (a, b, m, np.nextafter(m, -1), np.nextafter(m, 2)):
+            pts.add(float(t))
+    top = MAXV[fmt]
+    for t in (top, top * 1.03, top * 1.07, top * 1.2, 2 ** (EMAX[fmt] + 1) * 0.999):
+        pts.add(t)
+    rng = np.random.default_rng(7)
+    pts.update((rng.random(3000) * 2 ** (EMAX[fmt] + 1)).tolist())
+    pts.update((rng.random(2000) * grid[2] * 2).tolist())   # subnormal range
+    for v in sorted(pts):
+        for s in (v, -v):
+            assert oracle.encode(s, fmt) == _brute_encode(s, fmt), (s, fmt)
+
+
+def test_encode_e4m3_matches_torch_cast():
+    rng = np.random.default_rng(11)
+    mag = 2.0 ** rng.uniform(-14, 9.2, size=20000)
+    v = (mag * np.where(rng.random(20000) < 0.5, -1, 1)).astype(np.float32)
+    ref = torch.clamp(torch.from_numpy(v), -448, 448).to(torch.float8_e4m3fn).view(torch.uint8)
+    got = [oracle.encode(float(t), oracle.E4M3) for t in v]
+    assert got == ref.tolist()
+
+
+@pytest.mark.parametrize("fmt", [oracle.E4M3, oracle.E2M1])
+def test_decode_matches_format_grid(fmt):
+    for code, val in _grid(fmt):
+        assert oracle.decode(code, fmt) == val
+        neg = code | (0x80 if fmt == oracle.E4M3 else 0x8)
+        assert oracle.decode(neg, fmt) == -val
+
+
+# ---------------------------------------------------------------- quantizer
+def _rand_tensor(shape, seed, spread=6.0):
+    rng = np.random.default_rng(seed)
+    mag = 2.0 ** rng.uniform(-spread, spread, size=shape)
+    return (rng.standard_normal(shape) * mag).astype(np.float32)
+
+
+@pytest.mark.parametrize("fmt", [oracle.E4M3, oracle.E2M1])
+def test_scale_puts_block_max_in_top_binade(fmt):
+    n, c, h, w = 32, 64, 3, 2
+    x = _rand_tensor((n, c, h, w), 3)
+    codes, scales = oracle.quantize(x, oracle.NCHW, oracle.ACT, fmt, n, c, h, w)
+    for hh in range(h):
+        for ww in range(w):
+            for cb in range(2):
+                blk = x[:, cb * 32:(cb + 1) * 32, hh, ww].astype(np.float64)
+                amax = np.abs(blk).max()
+                s = int(scales[(hh * w + ww) * 2 + cb]) - 127
+                scaled = amax / 2.0 ** s
+                assert 2.0 ** EMAX[fmt] <= scaled < 2.0 ** (EMAX[fmt] + 1)
+
+
+@pytest.mark.parametrize("fmt", [oracle.E4M3, oracle.E2M1])
+def test_dequant_error_bound(fmt):
+    """|x - deq(q(x))| <= half a quantum of x's binade, except clipping in
+    the block's top binade (amax above the format maximum saturates)."""
+    n, c, h, w = 32, 32, 2, 2
+    x = _rand_tensor((n, c, h, w), 5).astype(np.float64)
+    codes, scales = oracle.quantize(x.astype(np.float32), oracle.NCHW, oracle.ACT, fmt, n, c, h, w)
+    d = oracle.dequant(codes, scales, oracle.ACT, fmt, n, c, h, w)
+    mbits = 3 if fmt == oracle.E4M3 else 1
+    minexp = -6 if fmt == oracle.E4M3 else 0
+    for hh in range(h):
+        for ww in range(w):
+            s = int(scales[hh * w + ww]) - 127
+            for i in range(n):
+                for cc in range(c):
+                    v = x[i, cc, hh, ww] / 2.0 ** s
+                    if abs(v) >= MAXV[fmt]:
+                        assert abs(d[i, cc, hh, ww] / 2.0 ** s) == MAXV[fmt]
+                        continue
+                    e = max(math.floor(math.log2(abs(v))) if v != 0 else minexp, minexp)
+                    half_q = 2.0 ** (e - mbits) / 2
+                    assert abs(v - d[i, cc, hh, ww] / 2.0 ** s) <= half_q
+
+
+@pytest.mark.parametrize("fmt", [oracle.E4M3, oracle.E2M1])
+def test_quantizer_invariants(fmt):
+    n, c, h, w = 32, 40, 2, 3                      # ragged channels: padded to 64
+    x = _rand_tensor((n, c, h, w), 9)
+    codes, scales = oracle.quantize(x, oracle.NCHW, oracle.ACT, fmt, n, c, h, w)
+    # sign symmetry: codes(-x) = codes(x) with every real element's sign flipped
+    cn, sn = oracle.quantize(-x, oracle.NCHW, oracle.ACT, fmt, n, c, h, w)
+    assert np.array_equal(sn, scales)
+    d = oracle.dequant(codes, scales, oracle.ACT, fmt, n, c, h, w)
+    dn = oracle.dequant(cn, sn, oracle.ACT, fmt, n, c, h, w)
+    assert np.array_equal(np.signbit(dn), ~np.signbit(d))
+    assert np.array_equal(np.abs(dn), np.abs(d))
+    # power-of-two equivariance: scale shifts by k, codes unchanged
+    for k in (-5, 3):
+        ck, sk = oracle.quantize(x * np.float32(2.0 ** k), oracle.NCHW, oracle.ACT, fmt, n, c, h, w)
+        assert np.array_equal(ck, codes)
+        assert np.array_equal(sk.astype(int), scales.astype(int) + k)
+    # idempotence: re-quantizing the dequantized tensor is the identity
+    c2, s2 = oracle.quantize(d.astype(np.float32), oracle.NCHW, oracle.ACT, fmt, n, c, h, w)
+    assert np.array_equal(c2, codes) and np.array_equal(s2, scales)
+
+
+def _pos(n, c, h, w, bn, H, W, Cp):
+    """Stated code layout [N/Bn][H][W][Cp][Bn] (a spec, not the method)."""
+    return ((((n // bn) * H + h) * W + w) * Cp + c) * bn + n % bn
+
+
+@pytest.mark.parametrize("fmt", [oracle.E4M3, oracle.E2M1])
+@pytest.mark.parametrize("N", [2, 16, 64])
+def test_layout_single_element(fmt, N):
+    C, H, W = 40, 3, 5
+    Cp, bn = 64, min(32, N)
+    rng = np.random.default_rng(N)
+    for _ in range(6):
+        n, c, h, w = (int(rng.integers(N)), int(rng.integers(C)), int(rng.integers(H)),
+                      int(rng.integers(W)))
+        x = np.zeros((N, C, H, W), dtype=np.float32)
+        x[n, c, h, w] = -1.0
+        codes, scales = oracle.quantize(x, oracle.NCHW, oracle.ACT, fmt, N, C, H, W)
+        pos = _pos(n, c, h, w, bn, H, W, Cp)
+        # -1.0 alone: scale 2^-emax, element -2^emax = -256 (0xF8) or -4 (0xE)
+        top = 0xF8 if fmt == oracle.E4M3 else 0xE
+        nz = [i for i in range(len(codes) * (1 if fmt == oracle.E4M3 else 2))
+              if _code_at(codes, fmt, i)]
+        assert nz == [pos] and _code_at(codes, fmt, pos) == top
+        spos = (((n // bn) * H + h) * W + w) * (Cp // 32) + c // 32
+        assert [i for i, s in enumerate(scales) if s] == [spos]
+        assert scales[spos] == 127 - EMAX[fmt]
+
+
+@pytest.mark.parametrize("fmt", [oracle.E4M3, oracle.E2M1])
+def test_source_layouts_agree(fmt):
+    N, C, H, W = 64, 40, 3, 4
+    x = torch.from_numpy(_rand_tensor((N, C, H, W), 21))
+    ref = oracle.quantize(x.numpy(), oracle.NCHW, oracle.ACT, fmt, N, C, H, W)
+    nhwc = x.permute(0, 2, 3, 1).contiguous().numpy()
+    cbf = synth.nchw_to_cbf(x, 32).numpy()
+    for lay, arr in ((oracle.NHWC, nhwc), (oracle.CBF, cbf)):
+        got = oracle.quantize(arr, lay, oracle.ACT, fmt, N, C, H, W)
+        assert np.array_equal(got[0], ref[0]) and np.array_equal(got[1], ref[1])
+
+
+def test_weight_role_pads_both_channel_dims():
+    """Weight tiles are 32 Cin x 32 Cout at one tap; both dims pad to 32."""
+    co, ci = 48, 20
+    w = _rand_tensor((co, ci, 3, 3), 4)
+    codes, scales = oracle.quantize(w, oracle.NCHW, oracle.WEIGHT, oracle.E4M3, co, ci, 3, 3)
+    assert len(codes) == 64 * 3 * 3 * 32 and len(scales) == 2 * 9
+    d = oracle.dequant(codes, scales, oracle.WEIGHT, oracle.E4M3, co, ci, 3, 3)
+    for cob in range(2):
+        for a in range(3):
+            for b in range(3):
+                blk = w[cob * 32:(cob + 1) * 32, :, a, b].astype(np.float64)
+                e = math.floor(math.log2(np.abs(blk).max()))
+                assert scales[(cob * 3 + a) * 3 + b] == e - 8 + 127
+                err = np.abs(d[cob * 32:(cob + 1) * 32, :, a, b] - blk)
+                # half a top-binade quantum, or the clip of [1.75, 2) * 2^e to 448 * 2^s
+                clip = np.abs(blk).max() - 1.75 * 2.0 ** e
+                assert err.max() <= max(2.0 ** (e - 4), clip)
+
+
+def test_bad_batch_rejected():
+    for n in (3, 48, 20):
+        assert oracle.codes_bytes(oracle.ACT, oracle.E4M3, n, 32, 1, 1) < 0
+    assert oracle.codes_bytes(oracle.ACT, oracle.E2M1, 1, 32, 1, 1) < 0
+    assert oracle.codes_bytes(oracle.ACT, oracle.E4M3, 1, 32, 1, 1) == 32
+
+
+# ---------------------------------------------------------------- im2col
+CONVS = [
+    synth.conv_dict(2, 32, 32, 8, 8, 3, 1, 1),
+    synth.conv_dict(4, 40, 24, 7, 6, 3, 2, 1),
+    synth.conv_dict(32, 32, 64, 5, 5, 1, 1, 0),
+    dict(n=8, cin=33, cout=20, h=9, w=7, kh=3, kw=2, sh=2, sw=1, ph=1, pw=0),
+    synth.conv_dict(64, 64, 32, 4, 4, 3, 1, 1),
+    synth.conv_dict(2, 16, 8, 9, 9, 5, 2, 2),
+]
+
+
+def _unfold_as_tensor(x, cv):
+    """fp32 im2col via F.unfold, viewed as (N, C, Ho*Wo*Kh*Kw, 1) with pixel
+    index ((ho*Wo+wo)*Kh+kh)*Kw+kw."""
+    ho, wo = synth.out_hw(cv)
+    u = F.unfold(x, (cv["kh"], cv["kw"]), padding=(cv["ph"], cv["pw"]), stride=(cv["sh"], cv["sw"]))
+    n, c = x.shape[:2]
+    u = u.reshape(n, c, cv["kh"] * cv["kw"], ho * wo).permute(0, 1, 3, 2)
+    return u.reshape(n, c, ho * wo * cv["kh"] * cv["kw"], 1).contiguous()
+
+
+@pytest.mark.parametrize("fmt", [oracle.E4M3, oracle.E2M1])
+@pytest.mark.parametrize("cv", CONVS, ids=lambda c: f"n{c['n']}c{c['cin']}k{c['kh']}{c['kw']}s{c['sh']}")
+def test_im2col_commutes_with_quantize(fmt, cv):
+    """quantize(im2col(X)) == im2col_cbf(quantize(X)), bit for bit (Sec. IV-B:
+    quantizing X_{Cin,N} keeps its blocks whole through the CBF im2col)."""
+    x = torch.from_numpy(_rand_tensor((cv["n"], cv["cin"], cv["h"], cv["w"]), 31))
+    q = oracle.quantize(x.numpy(), oracle.NCHW, oracle.ACT, fmt, cv["n"], cv["cin"], cv["h"], cv["w"])
+    col = oracle.im2col_cbf(cv, fmt, *q)
+    xu = _unfold_as_tensor(x, cv)
+    ref = oracle.quantize(xu.numpy(), oracle.NCHW, oracle.ACT, fmt, cv["n"], cv["cin"], xu.shape[2], 1)
+    assert np.array_equal(col[0], ref[0]) and np.array_equal(col[1], ref[1])
+
+
+def test_im2col_index_map_brute_force():
+    cv = CONVS[1]
+    fmt = oracle.E4M3
+    x = _rand_tensor((cv["n"], cv["cin"], cv["h"], cv["w"]), 2)
+    xc, xs = oracle.quantize(x, oracle.NCHW, oracle.ACT, fmt, cv["n"], cv["cin"], cv["h"], cv["w"])
+    cc, cs = oracle.im2col_cbf(cv, fmt, xc, xs)
+    ho, wo = synth.out_hw(cv)
+    bn, Cp = cv["n"], 64
+    xt = xc.reshape(1, cv["h"], cv["w"], Cp, bn)
+    ct = cc.reshape(1, ho, wo, cv["kh"], cv["kw"], Cp, bn)
+    xst = xs.reshape(1, cv["h"], cv["w"], 2)
+    cst = cs.reshape(1, ho, wo, cv["kh"], cv["kw"], 2)
+    for oh in range(ho):
+        for ow in range(wo):
+            for a in range(cv["kh"]):
+                for b in range(cv["kw"]):
+                    ih, iw = oh * cv["sh"] + a - cv["ph"], ow * cv["sw"] + b - cv["pw"]
+                    if 0 <= ih < cv["h"] and 0 <= iw < cv["w"]:
+                        assert np.array_equal(ct[0, oh, ow, a, b], xt[0, ih, iw])
+                        assert np.array_equal(cst[0, oh, ow, a, b], xst[0, ih, iw])
+                    else:
+                        assert not ct[0, oh, ow, a, b].any() and not cst[0, oh, ow, a, b].any()
+
+
+# ---------------------------------------------------------------- GEMMs
+def _quantized_layer(cv, fmt, seed):
+    x, w, gy = synth.layer_inputs(cv, seed, kind="unit")
+    ho, wo = synth.out_hw(cv)
+    qx = oracle.quantize(x.numpy(), oracle.NCHW, oracle.ACT, fmt, cv["n"], cv["cin"], cv["h"], cv["w"])
+    qw = oracle.quantize(w.numpy(), oracle.NCHW, oracle.WEIGHT, fmt, cv["cout"], cv["cin"], cv["kh"], cv["kw"])
+    qg = oracle.quantize(gy.numpy(), oracle.NCHW, oracle.ACT, fmt, cv["n"], cv["cout"], ho, wo)
+    xd = oracle.dequant(*qx, oracle.ACT, fmt, cv["n"], cv["cin"], cv["h"], cv["w"])
+    wd = oracle.dequant(*qw, oracle.WEIGHT, fmt, cv["cout"], cv["cin"], cv["kh"], cv["kw"])
+    gd = oracle.dequant(*qg, oracle.ACT, fmt, cv["n"], cv["cout"], ho, wo)
+    return qx, qw, qg, xd, wd, gd
+
+
+def _close(a, b, s):
+    scale = np.maximum(s, 1e-300)
+    return np.max(np.abs(a - b) / scale) <= 1e-12
+
+
+@pytest.mark.parametrize("fmt", [oracle.E4M3, oracle.E2M1])
+@pytest.mark.parametrize("cv", CONVS, ids=lambda c: f"n{c['n']}c{c['cin']}k{c['kh']}{c['kw']}s{c['sh']}")
+def test_gemms_match_torch_fp64(fmt, cv):
+    qx, qw, qg, xd, wd, gd = _quantized_layer(cv, fmt, 5)
+    st, pd = (cv["sh"], cv["sw"]), (cv["ph"], cv["pw"])
+    X, Wt, G = map(torch.from_numpy, (xd, wd, gd))
+    y, sy = oracle.fwd(cv, fmt, qw, qx)
+    gx, sgx = oracle.dgrad(cv, fmt, qw, qg)
+    gw, sgw = oracle.wgrad(cv, fmt, qg, qx)
+    y_ref = F.conv2d(X, Wt, stride=st, padding=pd).numpy()
+    gx_ref = torch.nn.grad.conv2d_input(X.shape, Wt, G, stride=st, padding=pd).numpy()
+    gw_ref = torch.nn.grad.conv2d_weight(X, Wt.shape, G, stride=st, padding=pd).numpy()
+    assert _close(y, y_ref, sy) and _close(gx, gx_ref, sgx) and _close(gw, gw_ref, sgw)
+    # the absolute-product sums bound the results and are torch's |.| convs
+    sy_ref = F.conv2d(X.abs(), Wt.abs(), stride=st, padding=pd).numpy()
+    assert np.allclose(sy, sy_ref, rtol=1e-12, atol=0)
+    assert np.all(np.abs(y) <= sy * (1 + 1e-12))
+    sgw_ref = torch.nn.grad.conv2d_weight(X.abs(), Wt.shape, G.abs(), stride=st, padding=pd).numpy()
+    assert np.allclose(sgw, sgw_ref, rtol=1e-12, atol=0)
+
+
+@pytest.mark.parametrize("cv", CONVS[:4], ids=lambda c: f"n{c['n']}c{c['cin']}k{c['kh']}{c['kw']}s{c['sh']}")
+def test_gemms_match_direct_definitions(cv):
+    fmt = oracle.E4M3
+    qx, qw, qg, xd, wd, gd = _quantized_layer(cv, fmt, 6)
+    y, sy = oracle.fwd(cv, fmt, qw, qx)
+    gx, sgx = oracle.dgrad(cv, fmt, qw, qg)
+    gw, sgw = oracle.wgrad(cv, fmt, qg, qx)
+    assert _close(y, oracle.direct_fwd(cv, wd, xd), sy)
+    assert _close(gx, oracle.direct_dgrad(cv, wd, gd), sgx)
+    assert _close(gw, oracle.direct_wgrad(cv, gd, xd), sgw)
+
+
+@pytest.mark.parametrize("cv", CONVS[:4], ids=lambda c: f"n{c['n']}c{c['cin']}k{c['kh']}{c['kw']}s{c['sh']}")
+def test_single_output_routines_match_full(cv):
+    fmt = oracle.E2M1
+    qx, qw, qg, xd, wd, gd = _quantized_layer(cv, fmt, 8)
+    ho, wo = synth.out_hw(cv)
+    rng = np.random.default_rng(0)
+    y, sy = oracle.fwd(cv, fmt, qw, qx)
+    idx = np.stack([rng.integers(0, d, 50) for d in (cv["n"], cv["cout"], ho, wo)], 1)
+    v, s = oracle.fwd_at(cv, fmt, qw, qx, idx)
+    assert _close(v, y[tuple(idx.T)], s) and np.allclose(s, sy[tuple(idx.T)], rtol=1e-12)
+    gx, sgx = oracle.dgrad(cv, fmt, qw, qg)
+    idx = np.stack([rng.integers(0, d, 50) for d in (cv["n"], cv["cin"], cv["h"], cv["w"])], 1)
+    v, s = oracle.dgrad_at(cv, fmt, qw, qg, idx)
+    assert _close(v, gx[tuple(idx.T)], s) and np.allclose(s, sgx[tuple(idx.T)], rtol=1e-12)
+    gw, sgw = oracle.wgrad(cv, fmt, qg, qx)
+    idx = np.stack([rng.integers(0, d, 50) for d in (cv["cout"], cv["cin"], cv["kh"], cv["kw"])], 1)
+    v, s = oracle.wgrad_at(cv, fmt, qg, qx, idx)
+    assert _close(v, gw[tuple(idx.T)], s) and np.allclose(s, sgw[tuple(idx.T)], rtol=1e-12)
+
+
+def test_pointwise_conv_is_a_matmul():
+    cv = synth.conv_dict(32, 64, 48, 3, 3, 1, 1, 0)
+    fmt = oracle.E4M3
+    qx, qw, qg, xd, wd, gd = _quantized_layer(cv, fmt, 10)
+    y, sy = oracle.fwd(cv, fmt, qw, qx)
+    ref = np.einsum("oc,nchw->nohw", wd[:, :, 0, 0], xd)
+    assert _close(y, ref, sy)
+
+
+def test_lossless_inputs_reproduce_plain_convolution():
+    """Inputs already on the MX grid pass through quantization unchanged, so
+    the MX convolution equals torch's fp64 convolution of the raw inputs."""
+    cv = synth.conv_dict(32, 32, 32, 6, 6, 3, 1, 1)
+    fmt = oracle.E4M3
+    qx, qw, qg, xd, wd, gd = _quantized_layer(cv, fmt, 12)
+    # xd, wd are exactly representable; quantize them again from fp32
+    qx2 = oracle.quantize(xd.astype(np.float32), oracle.NCHW, oracle.ACT, fmt, 32, 32, 6, 6)
+    qw2 = oracle.quantize(wd.astype(np.float32), oracle.NCHW, oracle.WEIGHT, fmt, 32, 32, 3, 3)
+    y, sy = oracle.fwd(cv, fmt, qw2, qx2)
+    ref = F.conv2d(torch.from_numpy(xd), torch.from_numpy(wd), padding=1).numpy()
+    assert _close(y, ref, sy)
+
+
+# ---------------------------------------------------------------- Table I
+def _table1():
+    out = {}
+    with open(os.path.join(GOLDEN, "table1.txt")) as f:
+        for line in f:
+            if line.startswith("#") or not line.strip():
+                continue
+            p = [t.strip() for t in line.split("|")]
+            out[p[0]] = [float(t) for t in p[1:]]
+    return out
+
+
+def test_table1_quantization_counts():
+    """Per-element quantization counts of Table I at Kh=Kw=3, s=1, p=1:
+    quantize-once sees each of X, W, G_Y once; the naive line-block path
+    quantizes the im2col'd activations and W, G_Y once per GEMM direction."""
+    t1 = _table1()
+    cv = synth.conv_dict(32, 32, 32, 8, 8, 3, 1, 1)
+    fmt = oracle.E2M1
+    x, w, gy = synth.layer_inputs(cv, 1, kind="unit")
+    nX, nW, nG = x.numel(), w.numel(), gy.numel()
+    # quantize once (MicroQonv)
+    counts = []
+    for t, role, shape in ((x, oracle.ACT, x.shape), (w, oracle.WEIGHT, w.shape), (gy, oracle.ACT, gy.shape)):
+        oracle.counter_reset()
+        oracle.quantize(t.numpy(), oracle.NCHW, role, fmt, *shape)
+        counts.append(oracle.counter_get())
+    assert [counts[0] / nX, counts[1] / nW, counts[2] / nG] == t1["MicroQonv"][:3]
+    # naive: im2col'd X quantized along K (fwd) and along (pixel, n) (wgrad);
+    # W_f along K and along Cout; G_Yf along (pixel, n) and along Cout
+    xu = _unfold_as_tensor(x, cv)                                   # N, C, P*9, 1
+    ho, wo = synth.out_hw(cv)
+    xcol = xu.reshape(cv["n"], cv["cin"], ho * wo, 9).permute(3, 1, 2, 0).reshape(9 * cv["cin"], -1)
+    wf = w.permute(0, 2, 3, 1).reshape(cv["cout"], -1)
+    gf = gy.permute(1, 2, 3, 0).reshape(cv["cout"], -1)
+    naive = []
+    for m in (xcol, wf, gf):
+        oracle.counter_reset()
+        oracle.quantize_1d(m.numpy(), 0, fmt)
+        oracle.quantize_1d(m.numpy(), 1, fmt)
+        naive.append(oracle.counter_get())
+    assert [naive[0] / nX, naive[1] / nW, naive[2] / nG] == t1["Dacapo"][:3]
+
+
+def test_quantize_1d_blocks_follow_direction():
+    m = _rand_tensor((70, 45), 3)
+    r_idx, c_idx = np.meshgrid(np.arange(70), np.arange(45), indexing="ij")
+    for d in (0, 1):
+        codes, scales = oracle.quantize_1d(m, d, oracle.E4M3)
+        if d == 0:      # blocks of 32 along each row: scales [70][2]
+            blk = r_idx * 2 + c_idx // 32
+        else:           # blocks of 32 down each column: scales [3][45]
+            blk = (r_idx // 32) * 45 + c_idx
+        s = scales[blk].astype(np.float64) - 127
+        for b in np.unique(blk):
+            sel = blk == b
+            amax = np.abs(m[sel].astype(np.float64)).max()
+            sb = s[sel][0]
+            assert 2.0 ** 8 <= amax / 2.0 ** sb < 2.0 ** 9
+        ref = torch.clamp(torch.from_numpy(m.astype(np.float64) / 2.0 ** s), -448, 448)
+        ref = ref.to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+        assert np.array_equal(codes.reshape(70, 45), ref)
