@@ -1,0 +1,200 @@
+/*
+ * mxconv.h -- quantize-once MX convolution on MI355X (gfx950).
+ *
+ * The hot path of MicroQonv: each convolution tensor (activations X, weights
+ * W, output gradients G_Y) is quantized exactly once into an OCP-MX format
+ * whose shared E8M0 scale covers a square block spanning both directions in
+ * which the tensor is contracted (Sec. IV-B); activations are quantized
+ * before a channel-batch-first im2col (Sec. IV-A), which then only moves
+ * codes; the three convolution GEMMs of Sec. II-C / Sec. IV-B (forward,
+ * input gradient, weight gradient) consume the MX codes directly on the
+ * block-scaled matrix cores.
+ *
+ * ---------------------------------------------------------------------------
+ * Formats
+ *   MXC_E4M3: FP8 E4M3 elements (OCP "E4M3FN": bias 7, max 448, no inf),
+ *             1 byte per element.
+ *   MXC_E2M1: FP4 E2M1 elements (max 6), two per byte, the element at the
+ *             even position in the low nibble.
+ *   Scales: one E8M0 byte per block, value 2^(code-127); 0xFF marks a block
+ *   that held a NaN or infinity.
+ *
+ * Quantization rule (per block, the OCP-MX reading of Sec. III-A Eqs. (4)-(6)):
+ *   s = clamp(floor(log2 max|x|) - emax, -127, 127), emax = 8 (E4M3) or 2
+ *   (E2M1); scale code = s + 127 (code 0 when the block is all zero);
+ *   element = x * 2^-s rounded to nearest, ties to even, saturating to the
+ *   largest finite element; the sign of zero is kept; a non-finite block
+ *   gets scale 0xFF and all-zero element codes.
+ *
+ * MX tensor layout ("MX-CBF").  A logical tensor (n, c, h, w) -- for weights
+ * (Cout, Cin, Kh, Kw) -- is stored as
+ *   codes  [Np/Bn][h][w][Cp][Bn]   (Bn fastest)
+ *   scales [Np/Bn][h][w][Cp/32]
+ * with Cp = c rounded up to 32.  One block = 32 channels x Bn batch samples at
+ * one pixel (Sec. IV-A's X_{Cin,N}: at each (h, w) all channels of all
+ * samples are contiguous; Sec. IV-B's square blocks along Cin and N).
+ *   role MXC_ACT:    Bn = 32 if n >= 32 (n must be a multiple of 32),
+ *                    else Bn = n (n must divide 32); Np = n.
+ *                    E2M1 needs Bn >= 2.
+ *   role MXC_WEIGHT: Bn = 32, Np = n rounded up to 32, i.e. a block is
+ *                    32 Cin x 32 Cout at one tap (Sec. IV-B: W_f is blocked
+ *                    along Cin and Cout).
+ * Padding channels / output channels hold +0 codes and never change a scale.
+ *
+ * Float layouts (mxc_layout) for quantize inputs and fwd/dgrad outputs:
+ *   MXC_NCHW  plain (n, c, h, w) row-major (weights: OIHW);
+ *   MXC_NHWC  (n, h, w, c);
+ *   MXC_CBF   channel-batch-first fp32: [n/Bn][h][w][c][Bn] with the real c
+ *             and the activation Bn above (Sec. IV-A's layout, unquantized).
+ *
+ * Convolution (mxc_conv): cross-correlation with zero padding, dilation 1,
+ * groups 1; Ho = (h + 2 ph - kh) / sh + 1, Wo likewise (Sec. II-A, Eq. (1)
+ * with the stride/padding the paper states the method is independent of).
+ *
+ * ---------------------------------------------------------------------------
+ * Conventions for every entry point
+ *   - Device pointers are caller-owned (allocated by the caller, e.g. as
+ *     PyTorch tensors); the library never allocates, frees or synchronizes
+ *     and keeps no global state.  All pointers to device memory must be
+ *     16-byte aligned.
+ *   - Work is enqueued on `stream` (a hipStream_t passed as void*; NULL is
+ *     the default stream) and runs asynchronously.
+ *   - Arguments are validated on the host before anything is launched; a
+ *     non-zero return means nothing was enqueued (except MXC_ERR_HIP).
+ *   - Outputs are overwritten, never accumulated into.
+ * Return codes: */
+#ifndef MXCONV_H
+#define MXCONV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MXC_OK             0
+#define MXC_ERR_NULL      (-1)  /* a required pointer is NULL */
+#define MXC_ERR_ARG       (-2)  /* bad enum value or non-positive size */
+#define MXC_ERR_SHAPE     (-3)  /* batch rule broken, empty output, unsupported geometry */
+#define MXC_ERR_ALIGN     (-4)  /* device pointer not 16-byte aligned */
+#define MXC_ERR_HIP       (-5)  /* the HIP runtime reported a launch error */
+#define MXC_ERR_WORKSPACE (-6)  /* workspace missing or smaller than required */
+
+typedef enum { MXC_E4M3 = 0, MXC_E2M1 = 1 } mxc_fmt;
+typedef enum { MXC_F32 = 0, MXC_BF16 = 1 } mxc_dtype;
+typedef enum { MXC_NCHW = 0, MXC_NHWC = 1, MXC_CBF = 2 } mxc_layout;
+typedef enum { MXC_ACT = 0, MXC_WEIGHT = 1 } mxc_role;
+
+/* One convolution layer: batch n, channels cin -> cout, input h x w,
+ * kernel kh x kw, stride sh, sw, zero padding ph, pw. */
+typedef struct mxc_conv {
+    int32_t n, cin, cout, h, w;
+    int32_t kh, kw, sh, sw, ph, pw;
+} mxc_conv;
+
+/* ------------------------------------------------------------------ sizes */
+/* Bytes of the code / scale arrays of an MX tensor (see layout above);
+ * 0 if the arguments are invalid. */
+size_t mxconv_codes_bytes(int role, int fmt, int n, int c, int h, int w);
+size_t mxconv_scales_bytes(int role, int fmt, int n, int c, int h, int w);
+
+/* Output spatial size of a layer; returns an error code. */
+int mxconv_out_size(const mxc_conv* cv, int* ho, int* wo);
+
+/* Bytes of the explicit CBF im2col codes / scales (mxconv_im2col_cbf). */
+size_t mxconv_im2col_codes_bytes(const mxc_conv* cv, int fmt);
+size_t mxconv_im2col_scales_bytes(const mxc_conv* cv, int fmt);
+
+/* Workspace bytes mxconv_wgrad needs for its split-K partial sums (may be 0). */
+size_t mxconv_wgrad_workspace_bytes(const mxc_conv* cv, int fmt);
+
+/* ------------------------------------------------------------------ a1 */
+/* Quantize a float tensor once into an MX tensor (Sec. III-A Eqs. (4)-(6) in
+ * OCP-MX form, with Sec. IV-B's square blocks; Sec. IV-C: every tensor is
+ * quantized once, activations before im2col).
+ *   src     device, logical (n, c, h, w) tensor of `dtype` (fp32 or bf16) in
+ *           `layout` (NCHW / NHWC / CBF; CBF only for role MXC_ACT).
+ *           Weights are passed as OIHW (layout NCHW) with n = Cout, c = Cin,
+ *           h = Kh, w = Kw.
+ *   role    MXC_ACT (X, G_Y) or MXC_WEIGHT (W).
+ *   codes   device, mxconv_codes_bytes(role, fmt, n, c, h, w) bytes, written.
+ *   scales  device, mxconv_scales_bytes(...) bytes, written.
+ * Errors: NULL, ARG (enum, sizes), SHAPE (batch rule), ALIGN, HIP. */
+int mxconv_quantize(const void* src, int dtype, int layout, int role, int fmt,
+                    int n, int c, int h, int w,
+                    void* codes, uint8_t* scales, void* stream);
+
+/* ------------------------------------------------------------------ a2 */
+/* Channel-batch-first im2col on MX codes (Sec. IV-A, X'_{Cin,N}): for every
+ * output pixel (ho, wo) and tap (kh, kw), the block of the input pixel
+ * (ho*sh+kh-ph, wo*sw+kw-pw) is copied whole -- codes and scale, no
+ * requantization; taps in the zero padding give all-zero blocks with scale
+ * code 0.
+ *   x_codes / x_scales   device, the quantized activation (role ACT,
+ *                        n = cv->n, c = cv->cin, h = cv->h, w = cv->w).
+ *   col_codes            device, [n/Bn][Ho][Wo][Kh][Kw][Cp][Bn] codes,
+ *                        mxconv_im2col_codes_bytes bytes.
+ *   col_scales           device, [n/Bn][Ho][Wo][Kh][Kw][Cp/32],
+ *                        mxconv_im2col_scales_bytes bytes.
+ * Errors: NULL, ARG, SHAPE, ALIGN, HIP. */
+int mxconv_im2col_cbf(const mxc_conv* cv, int fmt,
+                      const void* x_codes, const uint8_t* x_scales,
+                      void* col_codes, uint8_t* col_scales, void* stream);
+
+/* ------------------------------------------------------------------ a3 */
+/* Forward convolution Y = W * X (Eq. (1)) as the GEMM Y_f = W_f X'
+ * (Sec. II-C, with Sec. IV-B's reshaping), the im2col being implicit: the
+ * kernel reads the X blocks of each tap straight from the MX-CBF tensor.
+ * Each 32-element K block is multiplied with its two E8M0 scales as in
+ * Eq. (7); accumulation is fp32.
+ *   w_codes / w_scales   device, W quantized with role MXC_WEIGHT
+ *                        (n = cout, c = cin, h = kh, w = kw).
+ *   x_codes / x_scales   device, X quantized with role MXC_ACT.
+ *   y                    device fp32, n x cout x Ho x Wo in y_layout
+ *                        (MXC_NCHW or MXC_CBF).
+ * Errors: NULL, ARG, SHAPE, ALIGN, HIP. */
+int mxconv_fwd(const mxc_conv* cv, int fmt,
+               const void* w_codes, const uint8_t* w_scales,
+               const void* x_codes, const uint8_t* x_scales,
+               float* y, int y_layout, void* stream);
+
+/* ------------------------------------------------------------------ a4 */
+/* Input gradient G_X = W^T * G_Y (Eq. (2)), i.e. G_X' = W_f^T G_Yf followed
+ * by the col2im that folds G_X' back onto input pixels (Sec. II-C,
+ * Sec. IV-B).  Computed as an implicit transposed convolution: for each
+ * input pixel the kernel gathers the G_Y blocks of the taps that reach it,
+ * so nothing is scattered.  Operands are the same stored codes as in the
+ * forward pass (W) and the once-quantized G_Y.
+ *   gy_codes / gy_scales  device, G_Y quantized with role MXC_ACT
+ *                         (n, cout, Ho, Wo).
+ *   gx                    device fp32, n x cin x h x w in gx_layout
+ *                         (MXC_NCHW or MXC_CBF).
+ * Errors: NULL, ARG, SHAPE, ALIGN, HIP. */
+int mxconv_dgrad(const mxc_conv* cv, int fmt,
+                 const void* w_codes, const uint8_t* w_scales,
+                 const void* gy_codes, const uint8_t* gy_scales,
+                 float* gx, int gx_layout, void* stream);
+
+/* ------------------------------------------------------------------ a5 */
+/* Weight gradient G_W[co][ci] = sum_n G_Y[n][co] * X[n][ci] (Eq. (3)), i.e.
+ * G_Wf = G_Yf X'^T (Sec. II-C, Sec. IV-B), contracted over (pixel, sample)
+ * with one 32-element K block per pixel's batch block, reading the same
+ * once-quantized X codes as the forward pass.  Split over K across the GPU;
+ * partial sums go to `workspace` and are reduced in fp32.
+ *   gw          device fp32, cout x cin x kh x kw (OIHW), written.
+ *   workspace   device, >= mxconv_wgrad_workspace_bytes(cv, fmt) bytes
+ *               (may be NULL when that is 0); contents are scratch.
+ * Errors: NULL, ARG, SHAPE, ALIGN, WORKSPACE, HIP. */
+int mxconv_wgrad(const mxc_conv* cv, int fmt,
+                 const void* gy_codes, const uint8_t* gy_scales,
+                 const void* x_codes, const uint8_t* x_scales,
+                 float* gw, void* workspace, size_t ws_bytes, void* stream);
+
+/* Human-readable text for a return code (static storage). */
+const char* mxconv_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MXCONV_H */

@@ -1,0 +1,685 @@
+// conv_gemm.hip -- a3/a4/a5: the three convolution GEMMs on MX operands
+// (Sec. II-C and Sec. IV-B: Y_f = W_f X', G_X' = W_f^T G_Yf folded back by
+// col2im, G_Wf = G_Yf X'^T), on gfx950 block-scaled MFMA
+// (v_mfma_scale_f32_32x32x64_f8f6f4): every 32-element K block of an
+// operand row carries its own E8M0 scale, which is exactly Eq. (7).
+//
+// All three kernels share one scheme.  A workgroup (4 waves) owns a BM x BN
+// output tile; a K step is two MX blocks (K = 64).  Per step the operands'
+// blocks are copied into LDS in their stored layout -- a block is a
+// contiguous [32 rows][Bn samples] slab of codes -- double-buffered so the
+// next step's global loads overlap this step's MFMAs.  Whether an operand is
+// read along its rows or across them, the transposition happens in the LDS
+// read (ds_read_b64_tr_b8 / _b4), so no data is ever rearranged:
+//   fwd   A = W   (rows co, K ci): weight block [ci][co], read transposed
+//         B = X'  (cols (pixel, n), K ci): X block [ci][n], read transposed;
+//             the im2col is implicit, each tap's block is fetched from the
+//             source pixel ho*sh+kh-ph, wo*sw+kw-pw (zero outside).
+//   dgrad A = W^T (rows ci, K co): weight block [ci][co], read along rows
+//         B = G_Y (cols (pixel, n), K co), read transposed; the output is
+//             split into sh x sw stride phases so every tap a workgroup
+//             visits reaches all its pixels (the col2im becomes a gather).
+//   wgrad A = G_Y (rows co, K n) and B = X at the tap-shifted pixel
+//             (cols (tap, ci), K n), both read along rows; one K block is
+//             one pixel's batch block (padded with zeros when Bn < 32);
+//             split over K, partials reduced in fp32 by a second kernel.
+#include "mx_internal.h"
+
+namespace mxc {
+namespace {
+
+constexpr int BM = 64;    // output rows per workgroup (2 MFMA row blocks)
+constexpr int BN = 128;   // output columns per workgroup (4 MFMA column blocks)
+constexpr int NT = 256;   // 4 waves: wave w owns rows 32*(w&1), columns 64*(w>>1)
+
+template <int UNIT> struct Vec;
+template <> struct Vec<16> { typedef uint4 T; };
+template <> struct Vec<8> { typedef uint2 T; };
+template <> struct Vec<4> { typedef uint32_t T; };
+template <> struct Vec<2> { typedef unsigned short T; };
+template <> struct Vec<1> { typedef uint8_t T; };
+
+template <int UNIT>
+__device__ __forceinline__ typename Vec<UNIT>::T vzero() {
+    typename Vec<UNIT>::T z;
+    __builtin_memset(&z, 0, sizeof(z));
+    return z;
+}
+
+// MFMA fragment from a K-major LDS tile ([block][k][col] bytes, row stride
+// `stride`): lane (col c, half h) receives the elements the block-scaled MFMA
+// expects (see mfma_mx), gathered by transposing reads.
+template <int FMT>
+__device__ __forceinline__ v8i frag_tr(const uint8_t* base, int stride, int colbase) {
+    const int l = threadIdx.x & 63;
+    const int i = l & 15, gi = l >> 4, cg = gi & 1, h = gi >> 1;
+    v8i r;
+    if (FMT == MXC_E4M3) {
+#pragma unroll
+        for (int blk = 0; blk < 2; blk++)
+#pragma unroll
+            for (int hf = 0; hf < 2; hf++) {
+                const int row = blk * 32 + 16 * h + 8 * hf + (i >> 1);
+                const int col = colbase + 16 * cg + 8 * (i & 1);
+                const v2i v = lds_tr8(base + row * stride + col);
+                r[4 * blk + 2 * hf] = v[0];
+                r[4 * blk + 2 * hf + 1] = v[1];
+            }
+    } else {
+#pragma unroll
+        for (int hf = 0; hf < 2; hf++) {
+            const int row = h * 32 + 16 * hf + i;
+            const v2i v = lds_tr4(base + row * stride + ((colbase + 16 * cg) >> 1));
+            r[2 * hf] = v[0];
+            r[2 * hf + 1] = v[1];
+        }
+        r[4] = r[5] = r[6] = r[7] = 0;
+    }
+    return r;
+}
+
+// MFMA fragment from a row-major LDS tile ([row][block][32 elements], row
+// stride `stride`).
+template <int FMT>
+__device__ __forceinline__ v8i frag_rows(const uint8_t* base, int stride, int rowbase) {
+    const int l = threadIdx.x & 63;
+    const int r = l & 31, h = l >> 5;
+    const uint8_t* p = base + (rowbase + r) * stride;
+    v8i out;
+    if (FMT == MXC_E4M3) {
+        const v4i a = *(const v4i*)(p + 16 * h);
+        const v4i b = *(const v4i*)(p + 32 + 16 * h);
+        out[0] = a[0]; out[1] = a[1]; out[2] = a[2]; out[3] = a[3];
+        out[4] = b[0]; out[5] = b[1]; out[6] = b[2]; out[7] = b[3];
+    } else {
+        const v4i a = *(const v4i*)(p + 16 * h);
+        out[0] = a[0]; out[1] = a[1]; out[2] = a[2]; out[3] = a[3];
+        out[4] = out[5] = out[6] = out[7] = 0;
+    }
+    return out;
+}
+
+// ============================================================ fwd / dgrad
+struct ConvArgs {
+    Conv cv;
+    const uint8_t* wc;  // weight codes / scales
+    const uint8_t* ws;
+    const uint8_t* bc;  // activation operand: X (fwd) or G_Y (dgrad)
+    const uint8_t* bs;
+    float* out;
+    int layout;
+    int M;              // real output channels (cout for fwd, cin for dgrad)
+    int mtiles, ctiles;
+    int hs, wsrc, cps, ncbs;  // activation operand: spatial size, padded channels, blocks
+    int kcb;                  // channel blocks along K
+    int hout, wout;           // output spatial size
+};
+
+template <int FMT, bool DG, int UNIT>
+__global__ __launch_bounds__(NT) void conv_kernel(ConvArgs p) {
+    constexpr int EB = FMT == MXC_E4M3 ? 8 : 4;     // element bits
+    constexpr int ROWB = 32 * EB / 8;               // bytes of one 32-element block row
+    constexpr int BSTR = BN * EB / 8 + 16;          // B: K-major row stride
+    constexpr int B_BYTES = 64 * BSTR;
+    constexpr int ASTR = DG ? 2 * ROWB + 16 : BM * EB / 8 + 16;
+    constexpr int A_BYTES = DG ? BM * ASTR : 64 * ASTR;
+    constexpr int NU_B = BN * EB / (32 * UNIT);     // B copy units per thread per step
+    constexpr int AUNITS = 128 * ROWB / 16;          // A copy units (16 B) per step
+    __shared__ __attribute__((aligned(16))) uint8_t lds_a[2][A_BYTES];
+    __shared__ __attribute__((aligned(16))) uint8_t lds_b[2][B_BYTES];
+    __shared__ int sc_a[2][2][2];                    // [buf][block][row block]
+    __shared__ uint8_t sc_b[2][2][BN];               // [buf][block][pixel slot]
+    __shared__ int slot_g[BN], slot_y[BN], slot_x[BN];
+
+    const Conv& cv = p.cv;
+    const int tid = threadIdx.x;
+    const int bn = cv.x.bn;
+    const int nps = BN / bn;                         // pixel slots per tile
+    const int rb = bn * EB / 8;                      // bytes of one row of an activation block
+    const int parts = rb / UNIT;
+
+    // ---- which tile: XCD-aware (tiles sharing columns land on one XCD)
+    const int ntile = p.mtiles * p.ctiles;
+    const int per_xcd = (gridDim.x + 7) / 8;
+    const int lin = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+    if (lin >= ntile) return;
+    const int mt = lin % p.mtiles, ct = lin / p.mtiles;
+
+    // ---- phase (dgrad) and the taps that reach it
+    int ry = 0, rx = 0, kh0 = 0, kw0 = 0, nvh = cv.kh, nvw = cv.kw, gh = cv.ho, gw = cv.wo;
+    if (DG) {
+        const int ph_id = blockIdx.y;
+        ry = ph_id / cv.sw; rx = ph_id % cv.sw;
+        kh0 = (ry + cv.ph) % cv.sh; kw0 = (rx + cv.pw) % cv.sw;
+        nvh = kh0 < cv.kh ? (cv.kh - kh0 + cv.sh - 1) / cv.sh : 0;
+        nvw = kw0 < cv.kw ? (cv.kw - kw0 + cv.sw - 1) / cv.sw : 0;
+        gh = ry < cv.h ? (cv.h - ry + cv.sh - 1) / cv.sh : 0;
+        gw = rx < cv.w ? (cv.w - rx + cv.sw - 1) / cv.sw : 0;
+    }
+    const int pph = gh * gw;                          // output pixels in this phase
+    const int ng = cv.x.ng;
+    if ((long)ct * BN >= (long)ng * pph * bn) return;
+    const int nkb = nvh * nvw * p.kcb;                // K blocks
+    const int nsteps = (nkb + 1) / 2;
+
+    // ---- pixel slots of this column tile
+    for (int s = tid; s < nps; s += NT) {
+        const long q = (long)ct * nps + s;            // (group, pixel) index
+        const int g = (int)(q / (pph > 0 ? pph : 1)), pp = pph > 0 ? (int)(q % pph) : 0;
+        slot_g[s] = (pph > 0 && g < ng) ? g : -1;
+        slot_y[s] = pph > 0 ? pp / gw : 0;
+        slot_x[s] = pph > 0 ? pp % gw : 0;
+    }
+    __syncthreads();
+
+    // tap index -> (kh, kw) and the source-pixel offset of the tap
+    const int tsh = DG ? cv.sh : 1, tsw = DG ? cv.sw : 1;
+    auto tap_of = [&](int ti, int& kh, int& kw) {
+        kh = kh0 + (ti / nvw) * tsh;
+        kw = kw0 + (ti % nvw) * tsw;
+    };
+
+    typename Vec<UNIT>::T rb_regs[NU_B];
+    uint4 ra;
+    uint8_t rsb = 0;
+    int rsa = 0;
+
+    auto load_step = [&](int s) {
+        // B: units ordered (block, slot, k, part) so lanes walk contiguous bytes
+#pragma unroll
+        for (int i = 0; i < NU_B; i++) {
+            const int u = tid + NT * i;
+            const int part = u % parts;
+            const int r1 = u / parts;
+            const int k = r1 & 31;
+            const int r2 = r1 >> 5;
+            const int ps = r2 % nps;
+            const int blk = r2 / nps;
+            const int b = 2 * s + blk;
+            typename Vec<UNIT>::T v = vzero<UNIT>();
+            const int g = slot_g[ps];
+            if (b < nkb && g >= 0) {
+                const int ti = b / p.kcb, kc = b % p.kcb;
+                int kh, kw;
+                tap_of(ti, kh, kw);
+                int sy, sx;
+                if (DG) {
+                    sy = slot_y[ps] + (ry + cv.ph - kh) / cv.sh;
+                    sx = slot_x[ps] + (rx + cv.pw - kw) / cv.sw;
+                } else {
+                    sy = slot_y[ps] * cv.sh + kh - cv.ph;
+                    sx = slot_x[ps] * cv.sw + kw - cv.pw;
+                }
+                if (sy >= 0 && sy < p.hs && sx >= 0 && sx < p.wsrc) {
+                    const size_t off = ((((size_t)g * p.hs + sy) * p.wsrc + sx) * p.cps + 32 * kc) *
+                                           (size_t)bn * EB / 8 + (size_t)k * rb + part * UNIT;
+                    v = *(const typename Vec<UNIT>::T*)(p.bc + off);
+                }
+            }
+            rb_regs[i] = v;
+        }
+        // B scales: one per (block, slot)
+        if (tid < 2 * nps) {
+            const int blk = tid / nps, ps = tid % nps, b = 2 * s + blk;
+            const int g = slot_g[ps];
+            uint8_t sc = 0;
+            if (b < nkb && g >= 0) {
+                const int ti = b / p.kcb, kc = b % p.kcb;
+                int kh, kw;
+                tap_of(ti, kh, kw);
+                int sy, sx;
+                if (DG) {
+                    sy = slot_y[ps] + (ry + cv.ph - kh) / cv.sh;
+                    sx = slot_x[ps] + (rx + cv.pw - kw) / cv.sw;
+                } else {
+                    sy = slot_y[ps] * cv.sh + kh - cv.ph;
+                    sx = slot_x[ps] * cv.sw + kw - cv.pw;
+                }
+                if (sy >= 0 && sy < p.hs && sx >= 0 && sx < p.wsrc)
+                    sc = p.bs[(((size_t)g * p.hs + sy) * p.wsrc + sx) * p.ncbs + kc];
+            }
+            rsb = sc;
+        }
+        // A: weight blocks; units ordered (block, row block, k, part)
+        ra = make_uint4(0, 0, 0, 0);
+        if (tid < AUNITS) {
+            const int u = tid;
+            const int part = u % (ROWB / 16);
+            const int r1 = u / (ROWB / 16);
+            const int k = r1 & 31;
+            const int mb = (r1 >> 5) & 1;
+            const int blk = r1 >> 6;
+            const int b = 2 * s + blk;
+            if (b < nkb) {
+                const int ti = b / p.kcb, kc = b % p.kcb;
+                int kh, kw;
+                tap_of(ti, kh, kw);
+                const int rowblk = 2 * mt + mb;       // block of output rows
+                const int cob = DG ? kc : rowblk, cib = DG ? rowblk : kc;
+                if (cob < cv.wt.np / 32 && cib < cv.wt.ncb) {
+                    const size_t off = ((((size_t)cob * cv.kh + kh) * cv.kw + kw) * cv.wt.cp + 32 * cib) *
+                                           (size_t)32 * EB / 8 + (size_t)k * ROWB + part * 16;
+                    ra = *(const uint4*)(p.wc + off);
+                }
+            }
+        }
+        if (tid < 4) {
+            const int blk = tid >> 1, mb = tid & 1, b = 2 * s + blk;
+            int sc = 0;
+            if (b < nkb) {
+                const int ti = b / p.kcb, kc = b % p.kcb;
+                int kh, kw;
+                tap_of(ti, kh, kw);
+                const int rowblk = 2 * mt + mb;
+                const int cob = DG ? kc : rowblk, cib = DG ? rowblk : kc;
+                if (cob < cv.wt.np / 32 && cib < cv.wt.ncb)
+                    sc = p.ws[(((size_t)cob * cv.kh + kh) * cv.kw + kw) * cv.wt.ncb + cib];
+            }
+            rsa = sc;
+        }
+    };
+
+    auto store_step = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < NU_B; i++) {
+            const int u = tid + NT * i;
+            const int part = u % parts;
+            const int r1 = u / parts;
+            const int k = r1 & 31;
+            const int r2 = r1 >> 5;
+            const int ps = r2 % nps;
+            const int blk = r2 / nps;
+            *(typename Vec<UNIT>::T*)&lds_b[buf][(blk * 32 + k) * BSTR + ps * rb + part * UNIT] = rb_regs[i];
+        }
+        if (tid < 2 * nps) sc_b[buf][tid / nps][tid % nps] = rsb;
+        if (tid < AUNITS) {
+            const int u = tid;
+            const int part = u % (ROWB / 16);
+            const int r1 = u / (ROWB / 16);
+            const int k = r1 & 31;
+            const int mb = (r1 >> 5) & 1;
+            const int blk = r1 >> 6;
+            const int off = DG ? (mb * 32 + k) * ASTR + blk * ROWB + part * 16
+                               : (blk * 32 + k) * ASTR + mb * ROWB + part * 16;
+            *(uint4*)&lds_a[buf][off] = ra;
+        }
+        if (tid < 4) sc_a[buf][tid >> 1][tid & 1] = rsa;
+    };
+
+    const int wave = tid >> 6, lane = tid & 63;
+    const int wm = wave & 1, wn = wave >> 1;
+    v16f acc[2];
+    for (int c = 0; c < 2; c++)
+        for (int e = 0; e < 16; e++) acc[c][e] = 0.0f;
+
+    if (nsteps > 0) {
+        load_step(0);
+        store_step(0);
+    }
+    __syncthreads();
+    for (int s = 0; s < nsteps; s++) {
+        const int buf = s & 1;
+        if (s + 1 < nsteps) load_step(s + 1);
+        const v8i af = DG ? frag_rows<FMT>(lds_a[buf], ASTR, 32 * wm)
+                          : frag_tr<FMT>(lds_a[buf], ASTR, 32 * wm);
+        const int h = lane >> 5;
+        const int sa = sc_a[buf][h][wm];
+#pragma unroll
+        for (int c = 0; c < 2; c++) {
+            const int colbase = 64 * wn + 32 * c;
+            const v8i bf = frag_tr<FMT>(lds_b[buf], BSTR, colbase);
+            const int sb = sc_b[buf][h][(colbase + (lane & 31)) / bn];
+            acc[c] = mfma_mx<FMT>(af, bf, acc[c], sa, sb);
+        }
+        if (s + 1 < nsteps) store_step(buf ^ 1);
+        __syncthreads();
+    }
+
+    // ---- epilogue: D(row, col) of lane l, value e: col = l%32,
+    //      row = 8*(e/4) + 4*(l/32) + e%4
+#pragma unroll
+    for (int c = 0; c < 2; c++) {
+        const int col = 64 * wn + 32 * c + (lane & 31);
+        const int ps = col / bn, j = col % bn;
+        const int g = slot_g[ps];
+        if (g < 0) continue;
+        const int oy = DG ? ry + cv.sh * slot_y[ps] : slot_y[ps];
+        const int ox = DG ? rx + cv.sw * slot_x[ps] : slot_x[ps];
+        const int n = g * bn + j;
+#pragma unroll
+        for (int e = 0; e < 16; e++) {
+            const int m = BM * mt + 32 * wm + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+            if (m >= p.M) continue;
+            size_t o;
+            if (p.layout == MXC_CBF)
+                o = ((((size_t)g * p.hout + oy) * p.wout + ox) * p.M + m) * bn + j;
+            else
+                o = (((size_t)n * p.M + m) * p.hout + oy) * p.wout + ox;
+            p.out[o] = acc[c][e];
+        }
+    }
+}
+
+template <bool DG, int FMT>
+int launch_conv_u(const ConvArgs& a, dim3 grid, hipStream_t s) {
+    const int rb = a.cv.x.bn * (FMT == MXC_E4M3 ? 8 : 4) / 8;
+    const int unit = rb >= 16 ? 16 : rb;
+    switch (unit) {
+        case 16: hipLaunchKernelGGL((conv_kernel<FMT, DG, 16>), grid, dim3(NT), 0, s, a); break;
+        case 8:  hipLaunchKernelGGL((conv_kernel<FMT, DG, 8>), grid, dim3(NT), 0, s, a); break;
+        case 4:  hipLaunchKernelGGL((conv_kernel<FMT, DG, 4>), grid, dim3(NT), 0, s, a); break;
+        case 2:  hipLaunchKernelGGL((conv_kernel<FMT, DG, 2>), grid, dim3(NT), 0, s, a); break;
+        default: hipLaunchKernelGGL((conv_kernel<FMT, DG, 1>), grid, dim3(NT), 0, s, a); break;
+    }
+    return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
+}
+
+int launch_conv(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const void* bc,
+                const uint8_t* bs, float* out, int layout, hipStream_t s) {
+    ConvArgs a;
+    a.cv = cv;
+    a.wc = (const uint8_t*)wc; a.ws = ws; a.bc = (const uint8_t*)bc; a.bs = bs;
+    a.out = out; a.layout = layout;
+    const Geom& src = dg ? cv.gy : cv.x;
+    a.hs = src.h; a.wsrc = src.w; a.cps = src.cp; a.ncbs = src.ncb;
+    a.kcb = dg ? cv.wt.np / 32 : cv.wt.ncb;
+    a.M = dg ? cv.cin : cv.cout;
+    a.hout = dg ? cv.h : cv.ho;
+    a.wout = dg ? cv.w : cv.wo;
+    a.mtiles = (a.M + BM - 1) / BM;
+    // largest phase grid sets the number of column tiles
+    long maxp = 0;
+    const int nph = dg ? cv.sh * cv.sw : 1;
+    for (int ph = 0; ph < nph; ph++) {
+        const int ry = dg ? ph / cv.sw : 0, rx = dg ? ph % cv.sw : 0;
+        const long gh = dg ? (ry < cv.h ? (cv.h - ry + cv.sh - 1) / cv.sh : 0) : cv.ho;
+        const long gw = dg ? (rx < cv.w ? (cv.w - rx + cv.sw - 1) / cv.sw : 0) : cv.wo;
+        if (gh * gw > maxp) maxp = gh * gw;
+    }
+    const long ctiles = ((long)cv.x.ng * maxp * cv.x.bn + BN - 1) / BN;
+    const long ntile = ctiles * a.mtiles;
+    if (ntile > 0x7FFFFFF0L) return MXC_ERR_SHAPE;
+    a.ctiles = (int)ctiles;
+    const unsigned gx = (unsigned)((ntile + 7) / 8 * 8);
+    const dim3 grid(gx, nph);
+    if (cv.fmt == MXC_E4M3)
+        return dg ? launch_conv_u<true, MXC_E4M3>(a, grid, s) : launch_conv_u<false, MXC_E4M3>(a, grid, s);
+    return dg ? launch_conv_u<true, MXC_E2M1>(a, grid, s) : launch_conv_u<false, MXC_E2M1>(a, grid, s);
+}
+
+// ============================================================ wgrad
+struct WgradArgs {
+    Conv cv;
+    const uint8_t* gc;  // G_Y codes / scales
+    const uint8_t* gs;
+    const uint8_t* xc;  // X codes / scales
+    const uint8_t* xs;
+    float* part;        // [splits][Cout_p][ntot] partial sums
+    int ntot;           // columns: Kh*Kw*Cin_p, column = tap*Cin_p + ci
+    int mtiles, ctiles, splits, kbps;   // K blocks per split (even)
+};
+
+template <int FMT, int UNIT>
+__global__ __launch_bounds__(NT) void wgrad_kernel(WgradArgs p) {
+    constexpr int EB = FMT == MXC_E4M3 ? 8 : 4;
+    constexpr int ROWB = 32 * EB / 8;
+    constexpr int STR = 2 * ROWB + 16;
+    __shared__ __attribute__((aligned(16))) uint8_t lds_a[2][BM * STR];
+    __shared__ __attribute__((aligned(16))) uint8_t lds_b[2][BN * STR];
+    __shared__ int sc_a[2][2][2];
+    __shared__ int sc_b[2][2][4];
+
+    const Conv& cv = p.cv;
+    const int tid = threadIdx.x;
+    const int bn = cv.x.bn;
+    const int rb = bn * EB / 8;                  // real bytes of a block row
+    const int parts = rb / UNIT;
+    const int npix = cv.ho * cv.wo;
+    const int nkb = cv.x.ng * npix;              // K blocks: (group, output pixel)
+
+    const int ntile = p.mtiles * p.ctiles * p.splits;
+    const int per_xcd = (gridDim.x + 7) / 8;
+    const int lin = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+    if (lin >= ntile) return;
+    const int mt = lin % p.mtiles;
+    const int r0 = lin / p.mtiles;
+    const int ct = r0 % p.ctiles, sp = r0 / p.ctiles;
+    const int kb0 = sp * p.kbps;
+    const int kb1 = min(nkb, kb0 + p.kbps);
+    const int nsteps = kb1 > kb0 ? (kb1 - kb0 + 1) / 2 : 0;
+
+    // rows shorter than a block are zero-padded once; loads never touch the pad
+    if (rb < ROWB) {
+        for (int i = tid; i < 2 * BM * STR / 4; i += NT) ((uint32_t*)lds_a)[i] = 0;
+        for (int i = tid; i < 2 * BN * STR / 4; i += NT) ((uint32_t*)lds_b)[i] = 0;
+        __syncthreads();
+    }
+
+    // column block cbk (0..3) of this tile -> (tap, ci block)
+    const int cinb = cv.x.ncb;
+    // a block row is either split into 16-byte units (at most 2: 32 FP8 codes)
+    // or moved as one smaller unit, so A has <= 2*BM*2 = NT units, B <= 2*NT
+    constexpr int NUA = 1;
+    constexpr int NUB = 2;
+    typename Vec<UNIT>::T ra[NUA], rbv[NUB];
+    int rs = 0;
+
+    // A units: (block, row, part); B units: (block, column, part); only the
+    // real bytes of each row are loaded.
+    auto load_step = [&](int s) {
+#pragma unroll
+        for (int i = 0; i < NUA; i++) {
+            const int u = tid + NT * i;
+            typename Vec<UNIT>::T v = vzero<UNIT>();
+            if (u < 2 * BM * parts) {
+                const int part = u % parts, r1 = u / parts;
+                const int row = r1 % BM, blk = r1 / BM;
+                const int b = kb0 + 2 * s + blk;
+                const int co = BM * mt + row;
+                if (b < kb1 && co < cv.gy.cp) {
+                    const int g = b / npix, pix = b % npix;
+                    const size_t off = (((size_t)g * npix + pix) * cv.gy.cp + co) * (size_t)rb + part * UNIT;
+                    v = *(const typename Vec<UNIT>::T*)(p.gc + off);
+                }
+            }
+            ra[i] = v;
+        }
+#pragma unroll
+        for (int i = 0; i < NUB; i++) {
+            const int u = tid + NT * i;
+            typename Vec<UNIT>::T v = vzero<UNIT>();
+            if (u < 2 * BN * parts) {
+                const int part = u % parts, r1 = u / parts;
+                const int col = r1 % BN, blk = r1 / BN;
+                const int b = kb0 + 2 * s + blk;
+                const int gcol = BN * ct + col;
+                const int tap = gcol / cv.x.cp, ci = gcol % cv.x.cp;
+                if (b < kb1 && tap < cv.kh * cv.kw) {
+                    const int g = b / npix, pix = b % npix;
+                    const int oh = pix / cv.wo, ow = pix % cv.wo;
+                    const int ih = oh * cv.sh + tap / cv.kw - cv.ph, iw = ow * cv.sw + tap % cv.kw - cv.pw;
+                    if (ih >= 0 && ih < cv.h && iw >= 0 && iw < cv.w) {
+                        const size_t off = ((((size_t)g * cv.h + ih) * cv.w + iw) * cv.x.cp + ci) * (size_t)rb +
+                                           part * UNIT;
+                        v = *(const typename Vec<UNIT>::T*)(p.xc + off);
+                    }
+                }
+            }
+            rbv[i] = v;
+        }
+        // scales: 4 for A (block x row block), 8 for B (block x column block)
+        rs = 0;
+        if (tid < 4) {
+            const int blk = tid >> 1, mb = tid & 1, b = kb0 + 2 * s + blk;
+            const int cob = 2 * mt + mb;
+            if (b < kb1 && cob < cv.gy.ncb) rs = p.gs[(size_t)b * cv.gy.ncb + cob];
+        } else if (tid < 12) {
+            const int t = tid - 4, blk = t >> 2, cbk = t & 3, b = kb0 + 2 * s + blk;
+            const int gcb = 4 * ct + cbk;                 // global column block
+            const int tap = gcb / cinb, cib = gcb % cinb;
+            if (b < kb1 && tap < cv.kh * cv.kw) {
+                const int g = b / npix, pix = b % npix;
+                const int oh = pix / cv.wo, ow = pix % cv.wo;
+                const int ih = oh * cv.sh + tap / cv.kw - cv.ph, iw = ow * cv.sw + tap % cv.kw - cv.pw;
+                if (ih >= 0 && ih < cv.h && iw >= 0 && iw < cv.w)
+                    rs = p.xs[(((size_t)g * cv.h + ih) * cv.w + iw) * cinb + cib];
+            }
+        }
+    };
+
+    auto store_step = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < NUA; i++) {
+            const int u = tid + NT * i;
+            if (u < 2 * BM * parts) {
+                const int part = u % parts, r1 = u / parts;
+                const int row = r1 % BM, blk = r1 / BM;
+                *(typename Vec<UNIT>::T*)&lds_a[buf][row * STR + blk * ROWB + part * UNIT] = ra[i];
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < NUB; i++) {
+            const int u = tid + NT * i;
+            if (u < 2 * BN * parts) {
+                const int part = u % parts, r1 = u / parts;
+                const int col = r1 % BN, blk = r1 / BN;
+                *(typename Vec<UNIT>::T*)&lds_b[buf][col * STR + blk * ROWB + part * UNIT] = rbv[i];
+            }
+        }
+        if (tid < 4) sc_a[buf][tid >> 1][tid & 1] = rs;
+        else if (tid < 12) sc_b[buf][(tid - 4) >> 2][(tid - 4) & 3] = rs;
+    };
+
+    const int wave = tid >> 6, lane = tid & 63;
+    const int wm = wave & 1, wn = wave >> 1;
+    v16f acc[2];
+    for (int c = 0; c < 2; c++)
+        for (int e = 0; e < 16; e++) acc[c][e] = 0.0f;
+
+    if (nsteps > 0) {
+        load_step(0);
+        store_step(0);
+    }
+    __syncthreads();
+    for (int s = 0; s < nsteps; s++) {
+        const int buf = s & 1;
+        if (s + 1 < nsteps) load_step(s + 1);
+        const int h = lane >> 5;
+        const v8i af = frag_rows<FMT>(lds_a[buf], STR, 32 * wm);
+        const int sa = sc_a[buf][h][wm];
+#pragma unroll
+        for (int c = 0; c < 2; c++) {
+            const v8i bf = frag_rows<FMT>(lds_b[buf], STR, 64 * wn + 32 * c);
+            const int sb = sc_b[buf][h][2 * wn + c];
+            acc[c] = mfma_mx<FMT>(af, bf, acc[c], sa, sb);
+        }
+        if (s + 1 < nsteps) store_step(buf ^ 1);
+        __syncthreads();
+    }
+
+    // partial tile -> workspace [split][Cout_p][ntot]
+#pragma unroll
+    for (int c = 0; c < 2; c++) {
+        const int col = BN * ct + 64 * wn + 32 * c + (lane & 31);
+        if (col >= p.ntot) continue;
+#pragma unroll
+        for (int e = 0; e < 16; e++) {
+            const int m = BM * mt + 32 * wm + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+            if (m >= cv.gy.cp) continue;
+            p.part[((size_t)sp * cv.gy.cp + m) * p.ntot + col] = acc[c][e];
+        }
+    }
+}
+
+// G_W[co][ci][kh][kw] = sum over splits of the partial (co, tap*Cin_p + ci).
+__global__ __launch_bounds__(256) void wgrad_reduce(const float* __restrict__ part, float* __restrict__ gw,
+                                                    Conv cv, int ntot, int splits) {
+    const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;   // over (co, tap, ci) real
+    const int taps = cv.kh * cv.kw;
+    const long total = (long)cv.cout * taps * cv.cin;
+    if (i >= total) return;
+    const int ci = (int)(i % cv.cin);
+    const long r = i / cv.cin;
+    const int tap = (int)(r % taps);
+    const int co = (int)(r / taps);
+    const size_t col = (size_t)tap * cv.x.cp + ci;
+    float s = 0.0f;
+    for (int k = 0; k < splits; k++) s += part[((size_t)k * cv.gy.cp + co) * ntot + col];
+    gw[(((size_t)co * cv.cin + ci) * cv.kh + tap / cv.kw) * cv.kw + tap % cv.kw] = s;
+}
+
+struct WgradPlan {
+    int mtiles, ctiles, splits, kbps, ntot;
+};
+
+WgradPlan wgrad_plan(const Conv& cv) {
+    WgradPlan pl;
+    pl.ntot = cv.kh * cv.kw * cv.x.cp;
+    pl.mtiles = (cv.gy.cp + BM - 1) / BM;
+    pl.ctiles = (pl.ntot + BN - 1) / BN;
+    const long nkb = (long)cv.x.ng * cv.ho * cv.wo;
+    const long tiles = (long)pl.mtiles * pl.ctiles;
+    const long target = 1024;                    // workgroups to fill 256 CUs
+    long splits = (target + tiles - 1) / tiles;
+    const long max_splits = (nkb + 15) / 16;     // at least 8 K steps per split
+    if (splits > max_splits) splits = max_splits;
+    if (splits < 1) splits = 1;
+    long kbps = (nkb + splits - 1) / splits;
+    kbps = (kbps + 1) / 2 * 2;
+    splits = (nkb + kbps - 1) / kbps;
+    pl.splits = (int)splits;
+    pl.kbps = (int)kbps;
+    return pl;
+}
+
+template <int FMT>
+int launch_wgrad_f(const WgradArgs& a, dim3 grid, hipStream_t s) {
+    const int rb = a.cv.x.bn * (FMT == MXC_E4M3 ? 8 : 4) / 8;
+    const int unit = rb >= 16 ? 16 : rb;
+    switch (unit) {
+        case 16: hipLaunchKernelGGL((wgrad_kernel<FMT, 16>), grid, dim3(NT), 0, s, a); break;
+        case 8:  hipLaunchKernelGGL((wgrad_kernel<FMT, 8>), grid, dim3(NT), 0, s, a); break;
+        case 4:  hipLaunchKernelGGL((wgrad_kernel<FMT, 4>), grid, dim3(NT), 0, s, a); break;
+        case 2:  hipLaunchKernelGGL((wgrad_kernel<FMT, 2>), grid, dim3(NT), 0, s, a); break;
+        default: hipLaunchKernelGGL((wgrad_kernel<FMT, 1>), grid, dim3(NT), 0, s, a); break;
+    }
+    return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
+}
+
+}  // namespace
+
+int launch_fwd(const Conv& cv, const void* wc, const uint8_t* ws, const void* xc, const uint8_t* xs,
+               float* y, int layout, hipStream_t s) {
+    return launch_conv(cv, false, wc, ws, xc, xs, y, layout, s);
+}
+
+int launch_dgrad(const Conv& cv, const void* wc, const uint8_t* ws, const void* gc, const uint8_t* gs,
+                 float* gx, int layout, hipStream_t s) {
+    return launch_conv(cv, true, wc, ws, gc, gs, gx, layout, s);
+}
+
+size_t wgrad_workspace(const Conv& cv) {
+    const WgradPlan pl = wgrad_plan(cv);
+    return (size_t)pl.splits * cv.gy.cp * pl.ntot * sizeof(float);
+}
+
+int launch_wgrad(const Conv& cv, const void* gc, const uint8_t* gs, const void* xc, const uint8_t* xs,
+                 float* gw, void* ws, hipStream_t s) {
+    const WgradPlan pl = wgrad_plan(cv);
+    WgradArgs a;
+    a.cv = cv;
+    a.gc = (const uint8_t*)gc; a.gs = gs; a.xc = (const uint8_t*)xc; a.xs = xs;
+    a.part = (float*)ws;
+    a.ntot = pl.ntot; a.mtiles = pl.mtiles; a.ctiles = pl.ctiles; a.splits = pl.splits; a.kbps = pl.kbps;
+    const long ntile = (long)pl.mtiles * pl.ctiles * pl.splits;
+    if (ntile > 0x7FFFFFF0L) return MXC_ERR_SHAPE;
+    const dim3 grid((unsigned)((ntile + 7) / 8 * 8));
+    int rc = cv.fmt == MXC_E4M3 ? launch_wgrad_f<MXC_E4M3>(a, grid, s) : launch_wgrad_f<MXC_E2M1>(a, grid, s);
+    if (rc) return rc;
+    const long total = (long)cv.cout * cv.kh * cv.kw * cv.cin;
+    hipLaunchKernelGGL(wgrad_reduce, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, (const float*)ws, gw,
+                       cv, pl.ntot, pl.splits);
+    return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
+}
+
+}  // namespace mxc

@@ -1,0 +1,145 @@
+// mx_internal.h -- geometry and device helpers shared by the gfx950 kernels
+// and the host-side argument checks of the C ABI.  Internal to the library.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+#include "../../include/mxconv.h"
+
+namespace mxc {
+
+// ---------------------------------------------------------------- geometry
+// MX tensor: logical (n, c, h, w); codes [np/bn][h][w][cp][bn], scales
+// [np/bn][h][w][cp/32] (see mxconv.h).
+struct Geom {
+    int n, c, h, w;
+    int bn, np, cp, ng, ncb;  // batch block, padded batch, padded channels, groups, channel blocks
+    int bits;                 // 8 or 4
+};
+
+// Returns MXC_OK or an error code.
+int geom_init(Geom* g, int role, int fmt, int n, int c, int h, int w);
+
+static inline size_t geom_codes_bytes(const Geom& g) {
+    size_t e = (size_t)g.np * g.h * g.w * g.cp;
+    return g.bits == 8 ? e : e / 2;
+}
+static inline size_t geom_scales_bytes(const Geom& g) {
+    return (size_t)g.ng * g.h * g.w * g.ncb;
+}
+
+struct Conv {
+    int n, cin, cout, h, w, kh, kw, sh, sw, ph, pw, ho, wo;
+    int fmt, bits;
+    Geom x;   // X  (n, cin, h, w), role ACT
+    Geom gy;  // G_Y (n, cout, ho, wo), role ACT
+    Geom wt;  // W  (cout, cin, kh, kw), role WEIGHT
+};
+
+int conv_init(Conv* cv, const mxc_conv* p, int fmt);
+
+// ---------------------------------------------------------------- launchers
+int launch_quantize(const void* src, int dtype, int layout, const Geom& g, int fmt,
+                    void* codes, uint8_t* scales, hipStream_t s);
+int launch_im2col(const Conv& cv, const void* xc, const uint8_t* xs, void* cc, uint8_t* cs,
+                  hipStream_t s);
+int launch_fwd(const Conv& cv, const void* wc, const uint8_t* ws, const void* xc,
+               const uint8_t* xs, float* y, int layout, hipStream_t s);
+int launch_dgrad(const Conv& cv, const void* wc, const uint8_t* ws, const void* gc,
+                 const uint8_t* gs, float* gx, int layout, hipStream_t s);
+size_t wgrad_workspace(const Conv& cv);
+int launch_wgrad(const Conv& cv, const void* gc, const uint8_t* gs, const void* xc,
+                 const uint8_t* xs, float* gw, void* ws, hipStream_t s);
+
+}  // namespace mxc
+
+// ---------------------------------------------------------------- device side
+#if defined(__HIPCC__)
+namespace mxc {
+
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v2i __attribute__((ext_vector_type(2)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) v2i lds_v2i;
+
+// Largest |x| bit pattern of a block -> E8M0 code (0xFF if any element was
+// NaN/inf).  floor(log2) comes from the exponent field, or from the
+// leading-zero count for an fp32 subnormal.
+template <int EMAX>
+__device__ __forceinline__ uint32_t scale_code_from_bits(uint32_t amax_bits) {
+    if (amax_bits >= 0x7F800000u) return 0xFFu;
+    if (amax_bits == 0u) return 0u;
+    int e = (amax_bits >= 0x00800000u) ? (int)(amax_bits >> 23) - 127
+                                       : (31 - __clz((int)amax_bits)) - 149;
+    int s = e - EMAX;
+    s = s < -127 ? -127 : (s > 127 ? 127 : s);
+    return (uint32_t)(s + 127);
+}
+
+// 2^-s as a float for s = code - 127 in [-127, 126] (always exact).
+__device__ __forceinline__ float inv_scale(uint32_t code) {
+    int s = (int)code - 127;
+    return __uint_as_float((uint32_t)(127 - s) << 23);
+}
+
+// Round v (already divided by the block scale, |v| < 2^(emax+1)) to FP8 E4M3:
+// nearest-even on the integer bit pattern, saturating at 448, sign kept.
+__device__ __forceinline__ uint32_t enc_e4m3(float v) {
+    uint32_t u = __float_as_uint(v);
+    uint32_t sign = (u >> 24) & 0x80u;
+    uint32_t a = u & 0x7FFFFFFFu;
+    uint32_t code;
+    if (a >= 0x43E00000u) {                     // >= 448
+        code = 0x7Eu;
+    } else if (a < 0x3C800000u) {               // < 2^-6: subnormal, quantum 2^-9
+        code = (uint32_t)__builtin_rintf(__uint_as_float(a) * 512.0f);
+    } else {                                    // drop 20 mantissa bits, ties to even
+        uint32_t r = a + 0x7FFFFu + ((a >> 20) & 1u);
+        code = (r >> 20) - (120u << 3);
+    }
+    return sign | code;
+}
+
+// Round v (|v| < 8) to FP4 E2M1: nearest-even, saturating at 6, sign kept.
+__device__ __forceinline__ uint32_t enc_e2m1(float v) {
+    uint32_t u = __float_as_uint(v);
+    uint32_t sign = (u >> 28) & 0x8u;
+    uint32_t a = u & 0x7FFFFFFFu;
+    uint32_t code;
+    if (a >= 0x40C00000u) {                     // >= 6
+        code = 0x7u;
+    } else if (a < 0x3F800000u) {               // < 1: subnormal, quantum 0.5
+        code = (uint32_t)__builtin_rintf(__uint_as_float(a) * 2.0f);
+    } else {                                    // drop 22 mantissa bits, ties to even
+        uint32_t r = a + 0x1FFFFFu + ((a >> 22) & 1u);
+        code = (r >> 22) - (126u << 1);
+    }
+    return sign | code;
+}
+
+// One block-scaled MFMA: D(32x32) += A(32 x 64) B(64 x 32) with one E8M0
+// scale per (row, 32-wide K block).  Operand fragment of lane l (row l%32,
+// half h = l/32):
+//   FP8: bytes 0..15  = K-block 0 elements [16h, 16h+16)
+//        bytes 16..31 = K-block 1 elements [16h, 16h+16)
+//   FP4: bytes 0..15  = K-block h, all 32 elements (nibble k = element k)
+//   scale operand: E8M0 of (row l%32, K-block h) in the low byte.
+template <int FMT>
+__device__ __forceinline__ v16f mfma_mx(v8i a, v8i b, v16f c, int sa, int sb) {
+    return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, FMT == MXC_E4M3 ? 0 : 4,
+                                                           FMT == MXC_E4M3 ? 0 : 4, 0, sa, 0, sb);
+}
+
+// LDS transposing reads (16-lane groups).
+//  tr8: lane i gets byte (i%8) of the 8-byte chunks addressed by lanes 2q + i/8, q = 0..7.
+//  tr4: lane i gets nibble i of the chunks addressed by lanes q, q = 0..15.
+__device__ __forceinline__ v2i lds_tr8(const uint8_t* p) {
+    return __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i*)(p));
+}
+__device__ __forceinline__ v2i lds_tr4(const uint8_t* p) {
+    return __builtin_amdgcn_ds_read_tr4_b64_v2i32((lds_v2i*)(p));
+}
+
+}  // namespace mxc
+#endif

@@ -1,0 +1,175 @@
+// mxconv_abi.cpp -- the C ABI of include/mxconv.h: host-side validation,
+// size helpers and dispatch to the gfx950 kernels.  Every argument check runs
+// on the host before anything is enqueued.
+#include "mx_internal.h"
+
+namespace mxc {
+
+int geom_init(Geom* g, int role, int fmt, int n, int c, int h, int w) {
+    if (fmt != MXC_E4M3 && fmt != MXC_E2M1) return MXC_ERR_ARG;
+    if (role != MXC_ACT && role != MXC_WEIGHT) return MXC_ERR_ARG;
+    if (n <= 0 || c <= 0 || h <= 0 || w <= 0) return MXC_ERR_ARG;
+    g->n = n; g->c = c; g->h = h; g->w = w;
+    g->bits = fmt == MXC_E4M3 ? 8 : 4;
+    g->cp = (c + 31) / 32 * 32;
+    g->ncb = g->cp / 32;
+    if (role == MXC_WEIGHT) {
+        g->bn = 32;
+        g->np = (n + 31) / 32 * 32;
+    } else {
+        if (n >= 32) {
+            if (n % 32) return MXC_ERR_SHAPE;
+            g->bn = 32;
+        } else {
+            if (32 % n) return MXC_ERR_SHAPE;
+            g->bn = n;
+        }
+        g->np = n;
+        if (fmt == MXC_E2M1 && g->bn < 2) return MXC_ERR_SHAPE;
+    }
+    g->ng = g->np / g->bn;
+    // sizes addressed with 32-bit pixel / block indices inside kernels
+    if ((long long)g->ng * h * w * g->ncb > 0x7FFFFFFFLL) return MXC_ERR_SHAPE;
+    return MXC_OK;
+}
+
+int conv_init(Conv* cv, const mxc_conv* p, int fmt) {
+    if (fmt != MXC_E4M3 && fmt != MXC_E2M1) return MXC_ERR_ARG;
+    if (p->n <= 0 || p->cin <= 0 || p->cout <= 0 || p->h <= 0 || p->w <= 0 || p->kh <= 0 ||
+        p->kw <= 0 || p->sh <= 0 || p->sw <= 0 || p->ph < 0 || p->pw < 0)
+        return MXC_ERR_ARG;
+    cv->n = p->n; cv->cin = p->cin; cv->cout = p->cout; cv->h = p->h; cv->w = p->w;
+    cv->kh = p->kh; cv->kw = p->kw; cv->sh = p->sh; cv->sw = p->sw; cv->ph = p->ph; cv->pw = p->pw;
+    if (p->h + 2 * p->ph < p->kh || p->w + 2 * p->pw < p->kw) return MXC_ERR_SHAPE;
+    cv->ho = (p->h + 2 * p->ph - p->kh) / p->sh + 1;
+    cv->wo = (p->w + 2 * p->pw - p->kw) / p->sw + 1;
+    cv->fmt = fmt;
+    cv->bits = fmt == MXC_E4M3 ? 8 : 4;
+    int rc;
+    if ((rc = geom_init(&cv->x, MXC_ACT, fmt, p->n, p->cin, p->h, p->w))) return rc;
+    if ((rc = geom_init(&cv->gy, MXC_ACT, fmt, p->n, p->cout, cv->ho, cv->wo))) return rc;
+    if ((rc = geom_init(&cv->wt, MXC_WEIGHT, fmt, p->cout, p->cin, p->kh, p->kw))) return rc;
+    return MXC_OK;
+}
+
+}  // namespace mxc
+
+using namespace mxc;
+
+static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+extern "C" {
+
+size_t mxconv_codes_bytes(int role, int fmt, int n, int c, int h, int w) {
+    Geom g;
+    return geom_init(&g, role, fmt, n, c, h, w) ? 0 : geom_codes_bytes(g);
+}
+
+size_t mxconv_scales_bytes(int role, int fmt, int n, int c, int h, int w) {
+    Geom g;
+    return geom_init(&g, role, fmt, n, c, h, w) ? 0 : geom_scales_bytes(g);
+}
+
+int mxconv_out_size(const mxc_conv* p, int* ho, int* wo) {
+    if (!p || !ho || !wo) return MXC_ERR_NULL;
+    Conv cv;
+    int rc = conv_init(&cv, p, MXC_E4M3);
+    if (rc) return rc;
+    *ho = cv.ho; *wo = cv.wo;
+    return MXC_OK;
+}
+
+size_t mxconv_im2col_codes_bytes(const mxc_conv* p, int fmt) {
+    Conv cv;
+    if (!p || conv_init(&cv, p, fmt)) return 0;
+    return (size_t)cv.x.ng * cv.ho * cv.wo * cv.kh * cv.kw * cv.x.cp * cv.x.bn * cv.bits / 8;
+}
+
+size_t mxconv_im2col_scales_bytes(const mxc_conv* p, int fmt) {
+    Conv cv;
+    if (!p || conv_init(&cv, p, fmt)) return 0;
+    return (size_t)cv.x.ng * cv.ho * cv.wo * cv.kh * cv.kw * cv.x.ncb;
+}
+
+size_t mxconv_wgrad_workspace_bytes(const mxc_conv* p, int fmt) {
+    Conv cv;
+    if (!p || conv_init(&cv, p, fmt)) return 0;
+    return wgrad_workspace(cv);
+}
+
+int mxconv_quantize(const void* src, int dtype, int layout, int role, int fmt, int n, int c,
+                    int h, int w, void* codes, uint8_t* scales, void* stream) {
+    if (!src || !codes || !scales) return MXC_ERR_NULL;
+    if (dtype != MXC_F32 && dtype != MXC_BF16) return MXC_ERR_ARG;
+    if (layout != MXC_NCHW && layout != MXC_NHWC && layout != MXC_CBF) return MXC_ERR_ARG;
+    if (layout == MXC_CBF && role != MXC_ACT) return MXC_ERR_ARG;
+    Geom g;
+    int rc = geom_init(&g, role, fmt, n, c, h, w);
+    if (rc) return rc;
+    if (!aligned16(src) || !aligned16(codes) || !aligned16(scales)) return MXC_ERR_ALIGN;
+    return launch_quantize(src, dtype, layout, g, fmt, codes, scales, (hipStream_t)stream);
+}
+
+int mxconv_im2col_cbf(const mxc_conv* p, int fmt, const void* xc, const uint8_t* xs, void* cc,
+                      uint8_t* cs, void* stream) {
+    if (!p || !xc || !xs || !cc || !cs) return MXC_ERR_NULL;
+    Conv cv;
+    int rc = conv_init(&cv, p, fmt);
+    if (rc) return rc;
+    if (!aligned16(xc) || !aligned16(xs) || !aligned16(cc) || !aligned16(cs)) return MXC_ERR_ALIGN;
+    return launch_im2col(cv, xc, xs, cc, cs, (hipStream_t)stream);
+}
+
+int mxconv_fwd(const mxc_conv* p, int fmt, const void* wc, const uint8_t* ws, const void* xc,
+               const uint8_t* xs, float* y, int y_layout, void* stream) {
+    if (!p || !wc || !ws || !xc || !xs || !y) return MXC_ERR_NULL;
+    if (y_layout != MXC_NCHW && y_layout != MXC_CBF) return MXC_ERR_ARG;
+    Conv cv;
+    int rc = conv_init(&cv, p, fmt);
+    if (rc) return rc;
+    if (!aligned16(wc) || !aligned16(ws) || !aligned16(xc) || !aligned16(xs) || !aligned16(y))
+        return MXC_ERR_ALIGN;
+    return launch_fwd(cv, wc, ws, xc, xs, y, y_layout, (hipStream_t)stream);
+}
+
+int mxconv_dgrad(const mxc_conv* p, int fmt, const void* wc, const uint8_t* ws, const void* gc,
+                 const uint8_t* gs, float* gx, int gx_layout, void* stream) {
+    if (!p || !wc || !ws || !gc || !gs || !gx) return MXC_ERR_NULL;
+    if (gx_layout != MXC_NCHW && gx_layout != MXC_CBF) return MXC_ERR_ARG;
+    Conv cv;
+    int rc = conv_init(&cv, p, fmt);
+    if (rc) return rc;
+    if (!aligned16(wc) || !aligned16(ws) || !aligned16(gc) || !aligned16(gs) || !aligned16(gx))
+        return MXC_ERR_ALIGN;
+    return launch_dgrad(cv, wc, ws, gc, gs, gx, gx_layout, (hipStream_t)stream);
+}
+
+int mxconv_wgrad(const mxc_conv* p, int fmt, const void* gc, const uint8_t* gs, const void* xc,
+                 const uint8_t* xs, float* gw, void* workspace, size_t ws_bytes, void* stream) {
+    if (!p || !gc || !gs || !xc || !xs || !gw) return MXC_ERR_NULL;
+    Conv cv;
+    int rc = conv_init(&cv, p, fmt);
+    if (rc) return rc;
+    const size_t need = wgrad_workspace(cv);
+    if (need && (!workspace || ws_bytes < need)) return MXC_ERR_WORKSPACE;
+    if (!aligned16(gc) || !aligned16(gs) || !aligned16(xc) || !aligned16(xs) || !aligned16(gw) ||
+        (need && !aligned16(workspace)))
+        return MXC_ERR_ALIGN;
+    return launch_wgrad(cv, gc, gs, xc, xs, gw, workspace, (hipStream_t)stream);
+}
+
+const char* mxconv_strerror(int code) {
+    switch (code) {
+        case MXC_OK: return "ok";
+        case MXC_ERR_NULL: return "a required pointer is NULL";
+        case MXC_ERR_ARG: return "bad enum value or non-positive size";
+        case MXC_ERR_SHAPE: return "unsupported shape (batch must divide 32 or be a multiple of 32; "
+                                   "E2M1 needs at least 2 samples per block; output must be non-empty)";
+        case MXC_ERR_ALIGN: return "device pointer not 16-byte aligned";
+        case MXC_ERR_HIP: return "HIP launch error";
+        case MXC_ERR_WORKSPACE: return "workspace missing or too small";
+        default: return "unknown error";
+    }
+}
+
+}  // extern "C"

@@ -1,0 +1,197 @@
+"""ctypes binding of libmxconv.so (include/mxconv.h).
+
+Argument marshalling only: output tensors are allocated with torch on the
+caller's device, pointers and the current HIP stream are passed through, and
+every step runs in the library's HIP kernels.  A missing library raises; there
+is no fallback path.
+"""
+import ctypes
+import os
+
+import torch
+
+E4M3, E2M1 = 0, 1
+F32, BF16 = 0, 1
+NCHW, NHWC, CBF = 0, 1, 2
+ACT, WEIGHT = 0, 1
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmxconv.so")
+_lib = None
+
+
+class MxconvError(RuntimeError):
+    pass
+
+
+class MxcConv(ctypes.Structure):
+    _fields_ = [(k, ctypes.c_int32) for k in
+                ("n", "cin", "cout", "h", "w", "kh", "kw", "sh", "sw", "ph", "pw")]
+
+
+def lib():
+    """Load the in-tree library (built by paper_2609_28358_amd.build)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise MxconvError(f"{LIB_PATH} is missing: build it with "
+                          "`python -m paper_2609_28358_amd.build` (no CPU fallback exists)")
+    L = ctypes.CDLL(LIB_PATH)
+    P, i32, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+    CP = ctypes.POINTER(MxcConv)
+    sigs = {
+        "mxconv_codes_bytes": (sz, [i32] * 6),
+        "mxconv_scales_bytes": (sz, [i32] * 6),
+        "mxconv_out_size": (i32, [CP, ctypes.POINTER(i32), ctypes.POINTER(i32)]),
+        "mxconv_im2col_codes_bytes": (sz, [CP, i32]),
+        "mxconv_im2col_scales_bytes": (sz, [CP, i32]),
+        "mxconv_wgrad_workspace_bytes": (sz, [CP, i32]),
+        "mxconv_quantize": (i32, [P, i32, i32, i32, i32, i32, i32, i32, i32, P, P, P]),
+        "mxconv_im2col_cbf": (i32, [CP, i32, P, P, P, P, P]),
+        "mxconv_fwd": (i32, [CP, i32, P, P, P, P, P, i32, P]),
+        "mxconv_dgrad": (i32, [CP, i32, P, P, P, P, P, i32, P]),
+        "mxconv_wgrad": (i32, [CP, i32, P, P, P, P, P, P, sz, P]),
+        "mxconv_strerror": (ctypes.c_char_p, [i32]),
+    }
+    for name, (res, args) in sigs.items():
+        fn = getattr(L, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = L
+    return L
+
+
+def strerror(rc):
+    return lib().mxconv_strerror(rc).decode()
+
+
+def _check(rc, what):
+    if rc != 0:
+        raise MxconvError(f"{what}: {strerror(rc)} (code {rc})")
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def conv_struct(cv):
+    return MxcConv(*[int(cv[k]) for k in ("n", "cin", "cout", "h", "w", "kh", "kw", "sh", "sw", "ph", "pw")])
+
+
+def codes_bytes(role, fmt, n, c, h, w):
+    return lib().mxconv_codes_bytes(role, fmt, n, c, h, w)
+
+
+def scales_bytes(role, fmt, n, c, h, w):
+    return lib().mxconv_scales_bytes(role, fmt, n, c, h, w)
+
+
+def out_size(cv):
+    ho, wo = ctypes.c_int(), ctypes.c_int()
+    _check(lib().mxconv_out_size(ctypes.byref(conv_struct(cv)), ctypes.byref(ho), ctypes.byref(wo)),
+           "out_size")
+    return ho.value, wo.value
+
+
+def wgrad_workspace_bytes(cv, fmt):
+    return lib().mxconv_wgrad_workspace_bytes(ctypes.byref(conv_struct(cv)), fmt)
+
+
+class MxTensor:
+    """Codes and E8M0 scales of one quantized tensor (device uint8 tensors)."""
+
+    def __init__(self, codes, scales, role, fmt, shape):
+        self.codes, self.scales, self.role, self.fmt, self.shape = codes, scales, role, fmt, tuple(shape)
+
+    @staticmethod
+    def empty(role, fmt, shape, device):
+        n, c, h, w = shape
+        nb = codes_bytes(role, fmt, n, c, h, w)
+        ns = scales_bytes(role, fmt, n, c, h, w)
+        if nb == 0:
+            raise MxconvError(f"invalid MX tensor geometry {shape} role {role} fmt {fmt}")
+        return MxTensor(torch.empty(nb, dtype=torch.uint8, device=device),
+                        torch.empty(ns, dtype=torch.uint8, device=device), role, fmt, shape)
+
+
+def quantize(src, role, fmt, layout=NCHW, shape=None, out=None, stream=None):
+    """Quantize `src` (fp32 or bf16 device tensor) once.  `shape` is the
+    logical (n, c, h, w); it defaults to src.shape for NCHW."""
+    if shape is None:
+        if layout == NHWC:
+            n, h, w, c = src.shape
+            shape = (n, c, h, w)
+        elif layout == NCHW:
+            shape = tuple(src.shape)
+        else:
+            raise ValueError("shape is required for the CBF layout")
+    dtype = {torch.float32: F32, torch.bfloat16: BF16}.get(src.dtype)
+    if dtype is None:
+        raise MxconvError(f"unsupported dtype {src.dtype}")
+    if not src.is_contiguous():
+        raise MxconvError("src must be contiguous")
+    if out is None:
+        out = MxTensor.empty(role, fmt, shape, src.device)
+    _check(lib().mxconv_quantize(_ptr(src), dtype, layout, role, fmt, *[int(v) for v in shape],
+                                 _ptr(out.codes), _ptr(out.scales), _stream(stream)), "mxconv_quantize")
+    return out
+
+
+def im2col_cbf(cv, x, stream=None):
+    c = conv_struct(cv)
+    nb = lib().mxconv_im2col_codes_bytes(ctypes.byref(c), x.fmt)
+    ns = lib().mxconv_im2col_scales_bytes(ctypes.byref(c), x.fmt)
+    codes = torch.empty(nb, dtype=torch.uint8, device=x.codes.device)
+    scales = torch.empty(ns, dtype=torch.uint8, device=x.codes.device)
+    _check(lib().mxconv_im2col_cbf(ctypes.byref(c), x.fmt, _ptr(x.codes), _ptr(x.scales), _ptr(codes),
+                                   _ptr(scales), _stream(stream)), "mxconv_im2col_cbf")
+    return codes, scales
+
+
+def _out(shape, layout, bn, device, out):
+    n, c, h, w = shape
+    if out is not None:
+        return out
+    if layout == CBF:
+        return torch.empty((n // bn, h, w, c, bn), dtype=torch.float32, device=device)
+    return torch.empty((n, c, h, w), dtype=torch.float32, device=device)
+
+
+def batch_block(n):
+    return 32 if n >= 32 else n
+
+
+def fwd(cv, w, x, layout=NCHW, out=None, stream=None):
+    ho, wo = out_size(cv)
+    y = _out((cv["n"], cv["cout"], ho, wo), layout, batch_block(cv["n"]), x.codes.device, out)
+    _check(lib().mxconv_fwd(ctypes.byref(conv_struct(cv)), x.fmt, _ptr(w.codes), _ptr(w.scales),
+                            _ptr(x.codes), _ptr(x.scales), _ptr(y), layout, _stream(stream)), "mxconv_fwd")
+    return y
+
+
+def dgrad(cv, w, gy, layout=NCHW, out=None, stream=None):
+    gx = _out((cv["n"], cv["cin"], cv["h"], cv["w"]), layout, batch_block(cv["n"]), gy.codes.device, out)
+    _check(lib().mxconv_dgrad(ctypes.byref(conv_struct(cv)), gy.fmt, _ptr(w.codes), _ptr(w.scales),
+                              _ptr(gy.codes), _ptr(gy.scales), _ptr(gx), layout, _stream(stream)),
+           "mxconv_dgrad")
+    return gx
+
+
+def wgrad(cv, gy, x, out=None, workspace=None, stream=None):
+    gw = out if out is not None else torch.empty((cv["cout"], cv["cin"], cv["kh"], cv["kw"]),
+                                                 dtype=torch.float32, device=x.codes.device)
+    need = wgrad_workspace_bytes(cv, x.fmt)
+    if workspace is None and need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=x.codes.device)
+    wsz = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(lib().mxconv_wgrad(ctypes.byref(conv_struct(cv)), x.fmt, _ptr(gy.codes), _ptr(gy.scales),
+                              _ptr(x.codes), _ptr(x.scales), _ptr(gw), _ptr(workspace), wsz,
+                              _stream(stream)), "mxconv_wgrad")
+    return gw

@@ -1,0 +1,113 @@
+"""The C ABI on the host (no GPU): the library loads, exports every entry
+point include/mxconv.h declares, sizes match the stated layouts, and every
+argument error is reported before anything is launched.  Calls here either
+fail validation or are pure size queries; none reaches a kernel."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import oracle
+from paper_2609_28358_amd import mxconv as mx
+from paper_2609_28358_amd import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "mxconv.h")).read()
+    return sorted(set(re.findall(r"\b(mxconv_\w+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = mx.lib()
+    names = _declared()
+    assert len(names) >= 12
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_sizes_match_layout_and_oracle():
+    for role in (mx.ACT, mx.WEIGHT):
+        for fmt in (mx.E4M3, mx.E2M1):
+            for shape in [(32, 64, 56, 56), (2, 32, 8, 8), (16, 3, 640, 640), (64, 100, 3, 5),
+                          (256, 64, 3, 3), (20, 33, 1, 1)]:
+                n, c, h, w = shape
+                if role == mx.ACT and not (n % 32 == 0 or 32 % n == 0):
+                    continue
+                assert mx.codes_bytes(role, fmt, *shape) == oracle.codes_bytes(role, fmt, *shape)
+                assert mx.scales_bytes(role, fmt, *shape) == oracle.scales_bytes(role, fmt, *shape)
+    # [N/Bn][H][W][Cp][Bn] codes, [N/Bn][H][W][Cp/32] scales
+    assert mx.codes_bytes(mx.ACT, mx.E4M3, 32, 64, 56, 56) == 32 * 64 * 56 * 56
+    assert mx.codes_bytes(mx.ACT, mx.E2M1, 16, 3, 640, 640) == 16 * 32 * 640 * 640 // 2
+    assert mx.scales_bytes(mx.ACT, mx.E4M3, 16, 3, 640, 640) == 640 * 640
+    assert mx.codes_bytes(mx.WEIGHT, mx.E4M3, 20, 33, 3, 3) == 32 * 64 * 9
+
+
+def test_conv_sizes():
+    for cv in (synth.conv_dict(32, 64, 64, 56, 56, 3, 1, 1), synth.conv_dict(32, 128, 256, 28, 28, 3, 2, 1),
+               dict(n=8, cin=33, cout=20, h=9, w=7, kh=3, kw=2, sh=2, sw=1, ph=1, pw=0)):
+        assert mx.out_size(cv) == synth.out_hw(cv) == oracle.conv_out(cv)
+        c = mx.conv_struct(cv)
+        for fmt in (0, 1):
+            assert mx.lib().mxconv_im2col_codes_bytes(ctypes.byref(c), fmt) == oracle.load().o_im2col_codes_bytes(
+                oracle._ptr(oracle._conv_params(cv)), fmt)
+            assert mx.wgrad_workspace_bytes(cv, fmt) > 0
+
+
+P = ctypes.c_void_p
+GOOD = P(0x10000)        # 16-byte aligned, never dereferenced: validation fails first
+ODD = P(0x10001)
+
+
+def test_quantize_errors():
+    L = mx.lib()
+    q = L.mxconv_quantize
+    assert q(None, 0, 0, 0, 0, 32, 32, 4, 4, GOOD, GOOD, None) == -1
+    assert q(GOOD, 0, 0, 0, 0, 32, 32, 4, 4, None, GOOD, None) == -1
+    assert q(GOOD, 2, 0, 0, 0, 32, 32, 4, 4, GOOD, GOOD, None) == -2     # dtype
+    assert q(GOOD, 0, 3, 0, 0, 32, 32, 4, 4, GOOD, GOOD, None) == -2     # layout
+    assert q(GOOD, 0, 0, 2, 0, 32, 32, 4, 4, GOOD, GOOD, None) == -2     # role
+    assert q(GOOD, 0, 0, 0, 2, 32, 32, 4, 4, GOOD, GOOD, None) == -2     # fmt
+    assert q(GOOD, 0, 2, 1, 0, 32, 32, 4, 4, GOOD, GOOD, None) == -2     # CBF weights
+    assert q(GOOD, 0, 0, 0, 0, 0, 32, 4, 4, GOOD, GOOD, None) == -2      # empty
+    assert q(GOOD, 0, 0, 0, 0, 32, -1, 4, 4, GOOD, GOOD, None) == -2
+    assert q(GOOD, 0, 0, 0, 0, 48, 32, 4, 4, GOOD, GOOD, None) == -3     # batch rule
+    assert q(GOOD, 0, 0, 0, 0, 3, 32, 4, 4, GOOD, GOOD, None) == -3
+    assert q(GOOD, 0, 0, 0, 1, 1, 32, 4, 4, GOOD, GOOD, None) == -3      # E2M1 with one sample
+    assert q(ODD, 0, 0, 0, 0, 32, 32, 4, 4, GOOD, GOOD, None) == -4
+    assert q(GOOD, 0, 0, 0, 0, 32, 32, 4, 4, GOOD, ODD, None) == -4
+
+
+def test_gemm_and_im2col_errors():
+    L = mx.lib()
+    cv = mx.conv_struct(synth.conv_dict(32, 64, 64, 8, 8, 3, 1, 1))
+    r = ctypes.byref(cv)
+    for fn in (L.mxconv_fwd, L.mxconv_dgrad):
+        assert fn(None, 0, GOOD, GOOD, GOOD, GOOD, GOOD, 0, None) == -1
+        assert fn(r, 0, GOOD, None, GOOD, GOOD, GOOD, 0, None) == -1
+        assert fn(r, 5, GOOD, GOOD, GOOD, GOOD, GOOD, 0, None) == -2
+        assert fn(r, 0, GOOD, GOOD, GOOD, GOOD, GOOD, 1, None) == -2     # NHWC output not offered
+        assert fn(r, 0, ODD, GOOD, GOOD, GOOD, GOOD, 0, None) == -4
+        assert fn(r, 0, GOOD, GOOD, GOOD, GOOD, ODD, 2, None) == -4
+    assert L.mxconv_im2col_cbf(r, 0, GOOD, None, GOOD, GOOD, None) == -1
+    assert L.mxconv_im2col_cbf(r, 0, GOOD, GOOD, ODD, GOOD, None) == -4
+    need = mx.wgrad_workspace_bytes(synth.conv_dict(32, 64, 64, 8, 8, 3, 1, 1), 0)
+    assert L.mxconv_wgrad(r, 0, GOOD, GOOD, GOOD, GOOD, GOOD, None, 0, None) == -6
+    assert L.mxconv_wgrad(r, 0, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, need - 1, None) == -6
+    assert L.mxconv_wgrad(r, 0, GOOD, GOOD, GOOD, GOOD, GOOD, ODD, need, None) == -4
+    bad = [dict(n=32, cin=64, cout=64, h=8, w=8, kh=3, kw=3, sh=0, sw=1, ph=1, pw=1),
+           dict(n=32, cin=64, cout=64, h=8, w=8, kh=3, kw=3, sh=1, sw=1, ph=-1, pw=1)]
+    for b in bad:
+        assert L.mxconv_fwd(ctypes.byref(mx.conv_struct(b)), 0, GOOD, GOOD, GOOD, GOOD, GOOD, 0, None) == -2
+    small = mx.conv_struct(dict(n=32, cin=64, cout=64, h=2, w=8, kh=5, kw=3, sh=1, sw=1, ph=1, pw=1))
+    assert L.mxconv_fwd(ctypes.byref(small), 0, GOOD, GOOD, GOOD, GOOD, GOOD, 0, None) == -3
+    odd_batch = mx.conv_struct(synth.conv_dict(24, 64, 64, 8, 8, 3, 1, 1))
+    assert L.mxconv_dgrad(ctypes.byref(odd_batch), 0, GOOD, GOOD, GOOD, GOOD, GOOD, 0, None) == -3
+
+
+def test_strerror_covers_codes():
+    for rc in range(0, -7, -1):
+        assert mx.strerror(rc) and mx.strerror(rc) != "unknown error"
+    assert mx.strerror(-99) == "unknown error"

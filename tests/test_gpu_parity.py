@@ -1,0 +1,274 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Codes and scales must match bit for bit.  GEMM outputs are compared with
+the oracle's fp64 results element by element: |gpu - oracle| <= 1e-5 * S,
+S = sum_k |a_k b_k| (the oracle's sum of absolute products, the error scale
+of an fp32 accumulation), for MXFP4; for MXFP8 the bound adds 2^-10 * G for
+the FP8 MFMA's grouped, truncating product alignment (see mx_tolerance.py).
+An output whose products are all zero must be exactly zero.  Inputs come from
+the seeded generators in paper_2609_28358_amd.synth.
+"""
+import numpy as np
+import pytest
+import torch
+
+import mx_tolerance as mxt
+import oracle
+from paper_2609_28358_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-5
+
+
+@pytest.fixture(scope="module")
+def mx():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_28358_amd import mxconv
+    mxconv.lib()
+    return mxconv
+
+
+DEV = "cuda:0"
+
+
+def _qcheck(mx, t, role, fmt, layout, shape, src_for_gpu=None):
+    """Quantize on both sides; GPU gets `src_for_gpu` (same values, maybe a
+    different layout or bf16), the oracle gets the fp32 NCHW tensor `t`."""
+    g = mx.quantize((src_for_gpu if src_for_gpu is not None else t).to(DEV), role, fmt, layout=layout,
+                    shape=shape)
+    torch.cuda.synchronize()
+    ref = oracle.quantize(t.float().numpy(), oracle.NCHW, role, fmt, *shape)
+    gc, gs = g.codes.cpu().numpy(), g.scales.cpu().numpy()
+    assert np.array_equal(gs, ref[1]), f"scales differ at {np.flatnonzero(gs != ref[1])[:8]}"
+    assert np.array_equal(gc, ref[0]), f"codes differ at {np.flatnonzero(gc != ref[0])[:8]}"
+    return g
+
+
+Q_SHAPES = [(32, 64, 7, 9), (2, 32, 8, 8), (16, 3, 5, 6), (64, 40, 3, 3), (1, 100, 4, 5),
+            (8, 33, 1, 1), (4, 96, 2, 17), (32, 32, 1, 300)]
+
+
+@pytest.mark.parametrize("fmt", [0, 1], ids=["e4m3", "e2m1"])
+@pytest.mark.parametrize("shape", Q_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_quantize_nchw_f32(mx, fmt, shape):
+    if fmt == 1 and shape[0] == 1:
+        pytest.skip("E2M1 needs two samples per block")
+    t = synth.normal(shape, 1.0, 11 + shape[0]) * torch.exp(synth.normal(shape, 2.0, 5))
+    _qcheck(mx, t, mx.ACT, fmt, mx.NCHW, shape)
+
+
+@pytest.mark.parametrize("fmt", [0, 1], ids=["e4m3", "e2m1"])
+@pytest.mark.parametrize("layout", ["nhwc", "cbf", "bf16"])
+def test_quantize_layouts_and_bf16(mx, fmt, layout):
+    for shape in [(32, 64, 5, 7), (16, 40, 3, 4), (64, 35, 2, 3)]:
+        t = synth.silu_normal(shape, 3)
+        if layout == "nhwc":
+            _qcheck(mx, t, mx.ACT, fmt, mx.NHWC, shape, t.permute(0, 2, 3, 1).contiguous())
+        elif layout == "cbf":
+            _qcheck(mx, t, mx.ACT, fmt, mx.CBF, shape, synth.nchw_to_cbf(t, synth.batch_block(shape[0])))
+        else:
+            tb = t.to(torch.bfloat16)
+            _qcheck(mx, tb.float(), mx.ACT, fmt, mx.NCHW, shape, tb)
+
+
+@pytest.mark.parametrize("fmt", [0, 1], ids=["e4m3", "e2m1"])
+def test_quantize_weights(mx, fmt):
+    for shape in [(64, 64, 3, 3), (20, 48, 3, 3), (256, 64, 1, 1), (16, 3, 3, 3), (33, 70, 5, 2)]:
+        t = synth.kaiming(*shape, seed=shape[0])
+        _qcheck(mx, t, mx.WEIGHT, fmt, mx.NCHW, shape)
+
+
+@pytest.mark.parametrize("fmt", [0, 1], ids=["e4m3", "e2m1"])
+def test_quantize_edge_values(mx, fmt):
+    shape = (32, 64, 2, 4)
+    t = synth.normal(shape, 1.0, 9)
+    t[:, :32, 0, 0] = 0.0                                 # all-zero block
+    t[:, 32:, 0, 0] = -0.0                                # negative zeros
+    t[3, 5, 0, 1] = float("inf")                          # non-finite blocks
+    t[4, 40, 0, 1] = float("nan")
+    t[:, :32, 0, 2] = 2.0 ** -140                         # fp32 subnormals
+    t[7, 3, 0, 2] = -(2.0 ** -149)
+    t[:, 32:, 0, 2] = 3.0e38                              # near the fp32 maximum
+    t[:, :32, 0, 3] = 448.0 * 1.0625                      # saturation and ties
+    t[0, 0, 0, 3] = 1.75 * 2 ** 8
+    t[:, :32, 1, 0] = torch.tensor([1.0625, 1.1875, 0.75, 1.25, 2.5, 5.0, 1.75, 3.5]).repeat(4)[:32]
+    t[:, 32:, 1, 1] = 2.0 ** -10
+    _qcheck(mx, t, mx.ACT, fmt, mx.NCHW, shape)
+
+
+def test_quantize_golden_blocks(mx):
+    """The hand-worked blocks of tests/golden through the GPU kernel."""
+    from test_oracle_pins import _golden_blocks, _code_at
+    for name, fmt, vals, scale, codes in _golden_blocks():
+        x = torch.zeros((32, 32, 1, 1))
+        for i, v in enumerate(vals):
+            x[i, 0, 0, 0] = v
+        g = mx.quantize(x.to(DEV), mx.ACT, fmt)
+        torch.cuda.synchronize()
+        c, s = g.codes.cpu().numpy(), g.scales.cpu().numpy()
+        assert s.tolist() == [scale], name
+        assert [_code_at(c, fmt, i) for i in range(len(vals))] == codes, name
+
+
+# ------------------------------------------------------------------ im2col
+IM_CONVS = [synth.conv_dict(2, 32, 32, 8, 8, 3, 1, 1), synth.conv_dict(32, 64, 64, 9, 7, 3, 2, 1),
+            dict(n=16, cin=40, cout=8, h=6, w=5, kh=3, kw=2, sh=1, sw=2, ph=1, pw=0),
+            synth.conv_dict(64, 32, 32, 4, 4, 1, 1, 0)]
+
+
+@pytest.mark.parametrize("fmt", [0, 1], ids=["e4m3", "e2m1"])
+@pytest.mark.parametrize("ci", range(len(IM_CONVS)))
+def test_im2col(mx, fmt, ci):
+    cv = IM_CONVS[ci]
+    x = synth.silu_normal((cv["n"], cv["cin"], cv["h"], cv["w"]), 4)
+    qx = mx.quantize(x.to(DEV), mx.ACT, fmt)
+    cc, cs = mx.im2col_cbf(cv, qx)
+    torch.cuda.synchronize()
+    ox = oracle.quantize(x.numpy(), oracle.NCHW, oracle.ACT, fmt, *x.shape)
+    rc, rs = oracle.im2col_cbf(cv, fmt, *ox)
+    assert np.array_equal(cs.cpu().numpy(), rs) and np.array_equal(cc.cpu().numpy(), rc)
+
+
+# ------------------------------------------------------------------ GEMMs
+def _err(got, ref, sabs, gbound=None):
+    """Largest |gpu - oracle| as a fraction of the allowed error (<= 1 passes)."""
+    got = got.astype(np.float64)
+    zero = sabs == 0
+    assert np.all(got[zero] == 0), "outputs with no non-zero products must be exactly 0"
+    tol = TOL * sabs
+    if gbound is not None:
+        tol = tol + 2.0 ** -10 * gbound
+    nz = ~zero
+    return float(np.max(np.abs(got[nz] - ref[nz]) / tol[nz])) if nz.any() else 0.0
+
+
+def _all_idx(*dims):
+    return np.stack(np.meshgrid(*[np.arange(d) for d in dims], indexing="ij"), -1).reshape(-1, len(dims))
+
+
+def _exps(o, cv, fmt):
+    ho, wo = synth.out_hw(cv)
+    shapes = {"x": (cv["n"], cv["cin"], cv["h"], cv["w"]), "w": (cv["cout"], cv["cin"], cv["kh"], cv["kw"]),
+              "gy": (cv["n"], cv["cout"], ho, wo)}
+    out = {}
+    for k, role in (("x", oracle.ACT), ("w", oracle.WEIGHT), ("gy", oracle.ACT)):
+        d = oracle.dequant(*o[k], role, fmt, *shapes[k])
+        out[k] = mxt.elem_exponents(d, o[k][1], role, fmt, shapes[k])
+    return out
+
+
+def _layer(mx, cv, fmt, seed, kind="sweep"):
+    x, w, gy = synth.layer_inputs(cv, seed, kind=kind)
+    q = {k: mx.quantize(t.to(DEV), role, fmt) for k, t, role in
+         (("x", x, mx.ACT), ("w", w, mx.WEIGHT), ("gy", gy, mx.ACT))}
+    o = {k: oracle.quantize(t.numpy(), oracle.NCHW, role, fmt, *t.shape) for k, t, role in
+         (("x", x, oracle.ACT), ("w", w, oracle.WEIGHT), ("gy", gy, oracle.ACT))}
+    torch.cuda.synchronize()
+    for k in q:   # the GEMMs below see identical operands on both sides
+        assert np.array_equal(q[k].codes.cpu().numpy(), o[k][0])
+        assert np.array_equal(q[k].scales.cpu().numpy(), o[k][1])
+    return q, o
+
+
+GEMM_CONVS = [
+    synth.conv_dict(2, 32, 32, 8, 8, 3, 1, 1),                # the small single-layer case
+    synth.conv_dict(32, 64, 64, 12, 10, 3, 1, 1),
+    synth.conv_dict(32, 64, 96, 9, 9, 1, 1, 0),
+    synth.conv_dict(32, 64, 48, 11, 9, 3, 2, 1),
+    synth.conv_dict(16, 3, 16, 13, 12, 3, 2, 1),              # 3-channel input, Bn = 16
+    dict(n=8, cin=33, cout=20, h=9, w=7, kh=3, kw=2, sh=2, sw=1, ph=1, pw=0),
+    synth.conv_dict(64, 32, 128, 6, 5, 3, 1, 1),              # two batch groups
+    synth.conv_dict(4, 40, 70, 10, 11, 5, 2, 2),
+    synth.conv_dict(1, 64, 32, 7, 7, 3, 1, 1),                # one sample (E4M3 only)
+    synth.conv_dict(32, 128, 64, 8, 8, 1, 2, 0),              # 1x1 stride 2: a phase with no taps
+]
+
+
+def _ids(c):
+    return f"n{c['n']}_{c['cin']}to{c['cout']}_{c['h']}x{c['w']}_k{c['kh']}{c['kw']}_s{c['sh']}{c['sw']}"
+
+
+@pytest.mark.parametrize("fmt", [0, 1], ids=["e4m3", "e2m1"])
+@pytest.mark.parametrize("cv", GEMM_CONVS, ids=_ids)
+@pytest.mark.parametrize("layout", ["nchw", "cbf"])
+def test_gemms(mx, fmt, cv, layout):
+    if fmt == 1 and cv["n"] == 1:
+        pytest.skip("E2M1 needs two samples per block")
+    lay = mx.NCHW if layout == "nchw" else mx.CBF
+    q, o = _layer(mx, cv, fmt, 7, kind="unit")
+    bn = synth.batch_block(cv["n"])
+    ho, wo = synth.out_hw(cv)
+    y = mx.fwd(cv, q["w"], q["x"], layout=lay)
+    gx = mx.dgrad(cv, q["w"], q["gy"], layout=lay)
+    gw = mx.wgrad(cv, q["gy"], q["x"])
+    torch.cuda.synchronize()
+    if lay == mx.CBF:
+        y = synth.cbf_to_nchw(y.cpu(), cv["n"], cv["cout"], ho, wo, bn)
+        gx = synth.cbf_to_nchw(gx.cpu(), cv["n"], cv["cin"], cv["h"], cv["w"], bn)
+    ry, sy = oracle.fwd(cv, fmt, o["w"], o["x"])
+    rgx, sgx = oracle.dgrad(cv, fmt, o["w"], o["gy"])
+    rgw, sgw = oracle.wgrad(cv, fmt, o["gy"], o["x"])
+    gy_, ggx, ggw = None, None, None
+    if fmt == 0:
+        e = _exps(o, cv, fmt)
+        gy_ = mxt.fwd_bound(cv, e["x"], e["w"], _all_idx(*ry.shape)).reshape(ry.shape)
+        ggx = mxt.dgrad_bound(cv, e["gy"], e["w"], _all_idx(*rgx.shape)).reshape(rgx.shape)
+        ggw = mxt.wgrad_bound(cv, e["gy"], e["x"], _all_idx(*rgw.shape)).reshape(rgw.shape)
+    e = (_err(y.cpu().numpy(), ry, sy, gy_), _err(gx.cpu().numpy(), rgx, sgx, ggx),
+         _err(gw.cpu().numpy(), rgw, sgw, ggw))
+    assert max(e) <= 1.0, f"fwd/dgrad/wgrad error / allowed = {e}"
+
+
+def test_nonfinite_block_propagates(mx):
+    cv = synth.conv_dict(32, 32, 32, 4, 4, 3, 1, 1)
+    x, w, gy = synth.layer_inputs(cv, 3, kind="unit")
+    x[0, 0, 1, 1] = float("inf")
+    qx = mx.quantize(x.to(DEV), mx.ACT, mx.E4M3)
+    qw = mx.quantize(w.to(DEV), mx.WEIGHT, mx.E4M3)
+    y = mx.fwd(cv, qw, qx).cpu()
+    # the non-finite block feeds output pixels (0..2, 0..2) of all samples only
+    assert torch.isnan(y[:, :, 0:3, 0:3]).all()
+    assert torch.isfinite(y[:, :, 3:, :]).all() and torch.isfinite(y[:, :, :, 3:]).all()
+
+
+# ------------------------------------------------------------------ full-size layers
+@pytest.mark.parametrize("fmt", [0, 1], ids=["e4m3", "e2m1"])
+@pytest.mark.parametrize("li", range(len(synth.SWEEP_LAYERS)), ids=[n for n, _ in synth.SWEEP_LAYERS])
+def test_sweep_layer_full_size(mx, fmt, li):
+    """The benchmark's layers at full size, in the launch configuration the
+    benchmark times (CBF activations in and out): codes bit-exact everywhere,
+    GEMM outputs checked on 2048 seeded samples each by direct dot products."""
+    name, cv = synth.SWEEP_LAYERS[li]
+    x, w, gy = synth.layer_inputs(cv, 1000 + li, kind="sweep")
+    bn = 32
+    ho, wo = synth.out_hw(cv)
+    qx = mx.quantize(synth.nchw_to_cbf(x, bn).to(DEV), mx.ACT, fmt, layout=mx.CBF, shape=tuple(x.shape))
+    qw = mx.quantize(w.to(DEV), mx.WEIGHT, fmt)
+    qg = mx.quantize(synth.nchw_to_cbf(gy, bn).to(DEV), mx.ACT, fmt, layout=mx.CBF, shape=tuple(gy.shape))
+    y = mx.fwd(cv, qw, qx, layout=mx.CBF)
+    gx = mx.dgrad(cv, qw, qg, layout=mx.CBF)
+    gw = mx.wgrad(cv, qg, qx)
+    torch.cuda.synchronize()
+    o = {}
+    for k, t, role, q in (("x", x, oracle.ACT, qx), ("w", w, oracle.WEIGHT, qw), ("gy", gy, oracle.ACT, qg)):
+        o[k] = oracle.quantize(t.numpy(), oracle.NCHW, role, fmt, *t.shape)
+        assert np.array_equal(q.scales.cpu().numpy(), o[k][1]), f"{k} scales"
+        assert np.array_equal(q.codes.cpu().numpy(), o[k][0]), f"{k} codes"
+    rng = np.random.default_rng(li)
+    y = synth.cbf_to_nchw(y.cpu(), cv["n"], cv["cout"], ho, wo, bn).numpy()
+    gx = synth.cbf_to_nchw(gx.cpu(), cv["n"], cv["cin"], cv["h"], cv["w"], bn).numpy()
+    gw = gw.cpu().numpy()
+    S = 2048
+    ex = _exps(o, cv, fmt) if fmt == 0 else None
+    idx = np.stack([rng.integers(0, d, S) for d in (cv["n"], cv["cout"], ho, wo)], 1)
+    r, s = oracle.fwd_at(cv, fmt, o["w"], o["x"], idx)
+    ey = _err(y[tuple(idx.T)], r, s, mxt.fwd_bound(cv, ex["x"], ex["w"], idx) if ex else None)
+    idx = np.stack([rng.integers(0, d, S) for d in (cv["n"], cv["cin"], cv["h"], cv["w"])], 1)
+    r, s = oracle.dgrad_at(cv, fmt, o["w"], o["gy"], idx)
+    egx = _err(gx[tuple(idx.T)], r, s, mxt.dgrad_bound(cv, ex["gy"], ex["w"], idx) if ex else None)
+    idx = np.stack([rng.integers(0, d, S // 8) for d in (cv["cout"], cv["cin"], cv["kh"], cv["kw"])], 1)
+    r, s = oracle.wgrad_at(cv, fmt, o["gy"], o["x"], idx)
+    egw = _err(gw[tuple(idx.T)], r, s, mxt.wgrad_bound(cv, ex["gy"], ex["x"], idx) if ex else None)
+    assert max(ey, egx, egw) <= 1.0, (ey, egx, egw)
