@@ -1,0 +1,245 @@
+#!/usr/bin/env python3
+"""Benchmark of the quantize-once MX convolution hot path on one MI355X.
+
+One step = one pass of the whole path over the layer sweep (batch 32, inputs
+resident in HBM): for each layer
+    3x3 s1 p1 64->64 at 56x56,  1x1 64->256 at 56x56,  3x3 s2 p1 128->256 at 28x28
+and each format (MXFP8 E4M3, MXFP4 E2M1): quantize X, W and G_Y once
+(activations arrive channel-batch-first in fp32, weights OIHW fp32), the
+explicit CBF im2col of X, then the forward, input-gradient and
+weight-gradient GEMMs.  Activations are SiLU(N(0,1)), weights Kaiming-normal,
+gradients N(0, 1e-3), all seeded.
+
+`value` is the conv fwd+bwd GEMM throughput of the whole step: the three
+GEMMs' algorithmic flops (2 N Cout Ho Wo Cin Kh Kw each, real channels) over
+the step's wall time, quantize and im2col included.  Every op is also timed
+with HIP events on the stream it runs on; the op taking the most time per
+step gets the `roofline` object, and all ops are listed in `ops`.
+
+    python bench.py [--steps K] [--warmup W] [--no-cpu-baseline]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_GBS = 8000.0                                   # MI355X HBM3E
+MFMA_TFLOPS = {0: 5000.0, 1: 10100.0}              # dense MXFP8 / MXFP4
+FMT_NAME = {0: "mxfp8", 1: "mxfp4"}
+
+
+def layer_numbers(cv, fmt, mx):
+    """Algorithmic flops and bytes of each op of one layer step."""
+    from paper_2609_28358_amd import synth
+    n, ci, co, kh, kw = cv["n"], cv["cin"], cv["cout"], cv["kh"], cv["kw"]
+    ho, wo = synth.out_hw(cv)
+    flops = 2.0 * n * co * ho * wo * ci * kh * kw
+
+    def mxb(role, nn, c, h, w):
+        return mx.codes_bytes(role, fmt, nn, c, h, w) + mx.scales_bytes(role, fmt, nn, c, h, w)
+
+    X = mxb(mx.ACT, n, ci, cv["h"], cv["w"])
+    W = mxb(mx.WEIGHT, co, ci, kh, kw)
+    G = mxb(mx.ACT, n, co, ho, wo)
+    import ctypes
+    c = mx.conv_struct(cv)
+    XC = (mx.lib().mxconv_im2col_codes_bytes(ctypes.byref(c), fmt) +
+          mx.lib().mxconv_im2col_scales_bytes(ctypes.byref(c), fmt))
+    return {
+        "quant_x": (0.0, 4.0 * n * ci * cv["h"] * cv["w"] + X),
+        "quant_w": (0.0, 4.0 * co * ci * kh * kw + W),
+        "quant_gy": (0.0, 4.0 * n * co * ho * wo + G),
+        "im2col": (0.0, X + XC),
+        "fwd": (flops, W + X + 4.0 * n * co * ho * wo),
+        "dgrad": (flops, W + G + 4.0 * n * ci * cv["h"] * cv["w"]),
+        "wgrad": (flops, G + X + 4.0 * co * ci * kh * kw),
+    }
+
+
+def cpu_baseline():
+    """The oracle on the benchmark's own workload, once: every layer of the
+    sweep in both formats -- quantize X, W, G_Y, CBF im2col, fwd, dgrad,
+    wgrad in fp64 loops on the host -- i.e. one step on the CPU."""
+    import oracle
+    from paper_2609_28358_amd import synth
+    flops, dt = 0.0, 0.0
+    for li, (name, cv) in enumerate(synth.SWEEP_LAYERS):
+        x, w, gy = synth.layer_inputs(cv, 1000 + li, kind="sweep")
+        xn, wn, gn = x.numpy(), w.numpy(), gy.numpy()
+        ho, wo = synth.out_hw(cv)
+        for fmt in (0, 1):
+            t0 = time.perf_counter()
+            ox = oracle.quantize(xn, oracle.NCHW, oracle.ACT, fmt, *x.shape)
+            ow = oracle.quantize(wn, oracle.NCHW, oracle.WEIGHT, fmt, *w.shape)
+            og = oracle.quantize(gn, oracle.NCHW, oracle.ACT, fmt, *gy.shape)
+            oracle.im2col_cbf(cv, fmt, *ox)
+            oracle.fwd(cv, fmt, ow, ox)
+            oracle.dgrad(cv, fmt, ow, og)
+            oracle.wgrad(cv, fmt, og, ox)
+            dt += time.perf_counter() - t0
+            flops += 3 * 2.0 * cv["n"] * cv["cout"] * ho * wo * cv["cin"] * cv["kh"] * cv["kw"]
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.get_threads(), "kind": "oracle",
+            "sample": f"one full step of the benchmark workload (all three layers, MXFP8 and MXFP4) through "
+                      f"the fp64 oracle: {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--layers", default="all", help="comma list of layer indices (profiling aid)")
+    ap.add_argument("--fmts", default="0,1")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the path has no "
+              f"multi-GPU part)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_28358_amd import mxconv as mx
+    from paper_2609_28358_amd import synth
+    mx.lib()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    layers = list(range(len(synth.SWEEP_LAYERS))) if args.layers == "all" else [int(v) for v in args.layers.split(",")]
+    fmts = [int(v) for v in args.fmts.split(",")]
+    jobs = []
+    for li in layers:
+        name, cv = synth.SWEEP_LAYERS[li]
+        x, w, gy = synth.layer_inputs(cv, 1000 + li, kind="sweep")
+        ho, wo = synth.out_hw(cv)
+        xs, gs = tuple(x.shape), tuple(gy.shape)
+        xd = synth.nchw_to_cbf(x, 32).to(dev)
+        gd = synth.nchw_to_cbf(gy, 32).to(dev)
+        wd = w.to(dev)
+        for fmt in fmts:
+            j = dict(name=f"{name}/{FMT_NAME[fmt]}", cv=cv, fmt=fmt, x=xd, w=wd, gy=gd, xs=xs, gs=gs,
+                     qx=mx.MxTensor.empty(mx.ACT, fmt, xs, dev), qw=mx.MxTensor.empty(mx.WEIGHT, fmt, tuple(w.shape), dev),
+                     qg=mx.MxTensor.empty(mx.ACT, fmt, gs, dev),
+                     y=torch.empty((cv["n"] // 32, ho, wo, cv["cout"], 32), dtype=torch.float32, device=dev),
+                     gx=torch.empty((cv["n"] // 32, cv["h"], cv["w"], cv["cin"], 32), dtype=torch.float32, device=dev),
+                     gw=torch.empty(tuple(w.shape), dtype=torch.float32, device=dev),
+                     ws=torch.empty(max(1, mx.wgrad_workspace_bytes(cv, fmt)), dtype=torch.uint8, device=dev),
+                     nums=layer_numbers(cv, fmt, mx))
+            jobs.append(j)
+
+    stream = torch.cuda.current_stream()
+    OPS = ("quant_x", "quant_w", "quant_gy", "im2col", "fwd", "dgrad", "wgrad")
+
+    def run_op(j, op):
+        cv, fmt = j["cv"], j["fmt"]
+        if op == "quant_x":
+            mx.quantize(j["x"], mx.ACT, fmt, layout=mx.CBF, shape=j["xs"], out=j["qx"])
+        elif op == "quant_w":
+            mx.quantize(j["w"], mx.WEIGHT, fmt, out=j["qw"])
+        elif op == "quant_gy":
+            mx.quantize(j["gy"], mx.ACT, fmt, layout=mx.CBF, shape=j["gs"], out=j["qg"])
+        elif op == "fwd":
+            mx.fwd(cv, j["qw"], j["qx"], layout=mx.CBF, out=j["y"])
+        elif op == "dgrad":
+            mx.dgrad(cv, j["qw"], j["qg"], layout=mx.CBF, out=j["gx"])
+        else:
+            mx.wgrad(cv, j["qg"], j["qx"], out=j["gw"], workspace=j["ws"])
+
+    # the explicit im2col output is written into a preallocated buffer too
+    import ctypes
+    for j in jobs:
+        c = mx.conv_struct(j["cv"])
+        j["col"] = (torch.empty(mx.lib().mxconv_im2col_codes_bytes(ctypes.byref(c), j["fmt"]), dtype=torch.uint8, device=dev),
+                    torch.empty(mx.lib().mxconv_im2col_scales_bytes(ctypes.byref(c), j["fmt"]), dtype=torch.uint8, device=dev))
+
+    def run_im2col(j):
+        c = mx.conv_struct(j["cv"])
+        rc = mx.lib().mxconv_im2col_cbf(ctypes.byref(c), j["fmt"], mx._ptr(j["qx"].codes), mx._ptr(j["qx"].scales),
+                                        mx._ptr(j["col"][0]), mx._ptr(j["col"][1]), mx._stream(None))
+        if rc:
+            raise mx.MxconvError(mx.strerror(rc))
+
+    def step(events=None):
+        for j in jobs:
+            for op in OPS:
+                key = (j["name"], op)
+                if events is not None and key in events:
+                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    e0.record(stream)
+                    run_im2col(j) if op == "im2col" else run_op(j, op)
+                    e1.record(stream)
+                    events[key].append((e0, e1))
+                else:
+                    run_im2col(j) if op == "im2col" else run_op(j, op)
+
+    # warmup, then one instrumented pass to find each op's time
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    probe = {(j["name"], op): [] for j in jobs for op in OPS}
+    for _ in range(3):
+        step(probe)
+    torch.cuda.synchronize()
+    op_ms = {k: sum(a.elapsed_time(b) for a, b in v) / len(v) for k, v in probe.items()}
+    dom = max(op_ms, key=op_ms.get)
+
+    # timed region: K steps, events only around the dominant op's launches
+    live = {dom: []}
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(live)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    dom_ms = sum(a.elapsed_time(b) for a, b in live[dom]) / len(live[dom])
+
+    gemm_flops = sum(j["nums"][op][0] for j in jobs for op in ("fwd", "dgrad", "wgrad"))
+    value = gemm_flops / (ms_step * 1e-3) / 1e12
+
+    def roof(job, op, ms):
+        fl, by = job["nums"][op]
+        fmt = job["fmt"]
+        ai = fl / by if by else 0.0
+        hbm_bound = fl == 0 or ai * HBM_GBS * 1e9 < MFMA_TFLOPS[fmt] * 1e12
+        if hbm_bound:
+            ach = by / (ms * 1e-3) / 1e9
+            return {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_GBS, "unit": "GB/s",
+                    "frac": round(ach / HBM_GBS, 4)}
+        ach = fl / (ms * 1e-3) / 1e12
+        return {"bound": "mfma", "achieved": round(ach, 1), "peak": MFMA_TFLOPS[fmt], "unit": "TFLOP/s",
+                "frac": round(ach / MFMA_TFLOPS[fmt], 4)}
+
+    jmap = {j["name"]: j for j in jobs}
+    rl = roof(jmap[dom[0]], dom[1], dom_ms)
+    rl.update({"kernel": f"{dom[1]} {dom[0]}", "ms": round(dom_ms, 4), "traffic": None})
+    ops = {}
+    for (nm, op), ms in op_ms.items():
+        fl, by = jmap[nm]["nums"][op]
+        r = roof(jmap[nm], op, ms)
+        ops[f"{nm}/{op}"] = {"ms": round(ms, 4), "tflops": round(fl / (ms * 1e-3) / 1e12, 2) if fl else None,
+                             "gbps": round(by / (ms * 1e-3) / 1e9, 1), "bound": r["bound"], "frac": r["frac"]}
+
+    out = {
+        "metric": "conv fwd+bwd TFLOPS (MXFP8/MXFP4) + quantize/im2col HBM GB/s, % of roofline",
+        "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "mxfp8+mxfp4 (fp32 accumulate)", "data": "synthetic",
+        "config": {"workload": "conv layer sweep, batch 32: 3x3 s1 64->64 56x56, 1x1 64->256 56x56, "
+                               "3x3 s2 128->256 28x28; each in MXFP8 and MXFP4; quantize x3 + im2col + fwd + "
+                               "dgrad + wgrad per layer",
+                   "global_batch": 32, "layers": [n for n, _ in synth.SWEEP_LAYERS], "formats": ["mxfp8", "mxfp4"],
+                   "parallelism": "single GPU"},
+        "roofline": rl,
+        "ops": ops,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline()
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

@@ -196,27 +196,26 @@ __global__ __launch_bounds__(NT) void conv_kernel(ConvArgs p) {
             const int ps = r2 % nps;
             const int blk = r2 / nps;
             const int b = 2 * s + blk;
-            typename Vec<UNIT>::T v = vzero<UNIT>();
+            // every load is issued (out-of-range ones read offset 0 and are
+            // zeroed), so all of a step's loads are in flight together
             const int g = slot_g[ps];
-            if (b < nkb && g >= 0) {
-                const int ti = b / p.kcb, kc = b % p.kcb;
-                int kh, kw;
-                tap_of(ti, kh, kw);
-                int sy, sx;
-                if (DG) {
-                    sy = slot_y[ps] + (ry + cv.ph - kh) / cv.sh;
-                    sx = slot_x[ps] + (rx + cv.pw - kw) / cv.sw;
-                } else {
-                    sy = slot_y[ps] * cv.sh + kh - cv.ph;
-                    sx = slot_x[ps] * cv.sw + kw - cv.pw;
-                }
-                if (sy >= 0 && sy < p.hs && sx >= 0 && sx < p.wsrc) {
-                    const size_t off = ((((size_t)g * p.hs + sy) * p.wsrc + sx) * p.cps + 32 * kc) *
-                                           (size_t)bn * EB / 8 + (size_t)k * rb + part * UNIT;
-                    v = *(const typename Vec<UNIT>::T*)(p.bc + off);
-                }
+            const int bb = min(b, nkb - 1);
+            const int ti = bb / p.kcb, kc = bb % p.kcb;
+            int kh, kw;
+            tap_of(ti, kh, kw);
+            int sy, sx;
+            if (DG) {
+                sy = slot_y[ps] + (ry + cv.ph - kh) / cv.sh;
+                sx = slot_x[ps] + (rx + cv.pw - kw) / cv.sw;
+            } else {
+                sy = slot_y[ps] * cv.sh + kh - cv.ph;
+                sx = slot_x[ps] * cv.sw + kw - cv.pw;
             }
-            rb_regs[i] = v;
+            const bool ok = b < nkb && g >= 0 && sy >= 0 && sy < p.hs && sx >= 0 && sx < p.wsrc;
+            const size_t off = ((((size_t)max(g, 0) * p.hs + sy) * p.wsrc + sx) * p.cps + 32 * kc) *
+                                   (size_t)bn * EB / 8 + (size_t)k * rb + part * UNIT;
+            const typename Vec<UNIT>::T v = *(const typename Vec<UNIT>::T*)(p.bc + (ok ? off : 0));
+            rb_regs[i] = ok ? v : vzero<UNIT>();
         }
         // B scales: one per (block, slot)
         if (tid < 2 * nps) {
@@ -250,18 +249,17 @@ __global__ __launch_bounds__(NT) void conv_kernel(ConvArgs p) {
             const int mb = (r1 >> 5) & 1;
             const int blk = r1 >> 6;
             const int b = 2 * s + blk;
-            if (b < nkb) {
-                const int ti = b / p.kcb, kc = b % p.kcb;
-                int kh, kw;
-                tap_of(ti, kh, kw);
-                const int rowblk = 2 * mt + mb;       // block of output rows
-                const int cob = DG ? kc : rowblk, cib = DG ? rowblk : kc;
-                if (cob < cv.wt.np / 32 && cib < cv.wt.ncb) {
-                    const size_t off = ((((size_t)cob * cv.kh + kh) * cv.kw + kw) * cv.wt.cp + 32 * cib) *
-                                           (size_t)32 * EB / 8 + (size_t)k * ROWB + part * 16;
-                    ra = *(const uint4*)(p.wc + off);
-                }
-            }
+            const int bb = min(b, nkb - 1);
+            const int ti = bb / p.kcb, kc = bb % p.kcb;
+            int kh, kw;
+            tap_of(ti, kh, kw);
+            const int rowblk = 2 * mt + mb;           // block of output rows
+            const int cob = DG ? kc : rowblk, cib = DG ? rowblk : kc;
+            const bool ok = b < nkb && cob < cv.wt.np / 32 && cib < cv.wt.ncb;
+            const size_t off = ((((size_t)cob * cv.kh + kh) * cv.kw + kw) * cv.wt.cp + 32 * cib) *
+                                   (size_t)32 * EB / 8 + (size_t)k * ROWB + part * 16;
+            const uint4 v = *(const uint4*)(p.wc + (ok ? off : 0));
+            ra = ok ? v : make_uint4(0, 0, 0, 0);
         }
         if (tid < 4) {
             const int blk = tid >> 1, mb = tid & 1, b = 2 * s + blk;
@@ -470,42 +468,34 @@ __global__ __launch_bounds__(NT) void wgrad_kernel(WgradArgs p) {
 #pragma unroll
         for (int i = 0; i < NUA; i++) {
             const int u = tid + NT * i;
-            typename Vec<UNIT>::T v = vzero<UNIT>();
-            if (u < 2 * BM * parts) {
-                const int part = u % parts, r1 = u / parts;
-                const int row = r1 % BM, blk = r1 / BM;
-                const int b = kb0 + 2 * s + blk;
-                const int co = BM * mt + row;
-                if (b < kb1 && co < cv.gy.cp) {
-                    const int g = b / npix, pix = b % npix;
-                    const size_t off = (((size_t)g * npix + pix) * cv.gy.cp + co) * (size_t)rb + part * UNIT;
-                    v = *(const typename Vec<UNIT>::T*)(p.gc + off);
-                }
-            }
-            ra[i] = v;
+            const int part = u % parts, r1 = u / parts;
+            const int row = r1 % BM, blk = r1 / BM;
+            const int b = kb0 + 2 * s + blk;
+            const int co = BM * mt + row;
+            const bool ok = u < 2 * BM * parts && b < kb1 && co < cv.gy.cp;
+            const int bb = min(b, nkb - 1);
+            const int g = bb / npix, pix = bb % npix;
+            const size_t off = (((size_t)g * npix + pix) * cv.gy.cp + co) * (size_t)rb + part * UNIT;
+            const typename Vec<UNIT>::T v = *(const typename Vec<UNIT>::T*)(p.gc + (ok ? off : 0));
+            ra[i] = ok ? v : vzero<UNIT>();
         }
 #pragma unroll
         for (int i = 0; i < NUB; i++) {
             const int u = tid + NT * i;
-            typename Vec<UNIT>::T v = vzero<UNIT>();
-            if (u < 2 * BN * parts) {
-                const int part = u % parts, r1 = u / parts;
-                const int col = r1 % BN, blk = r1 / BN;
-                const int b = kb0 + 2 * s + blk;
-                const int gcol = BN * ct + col;
-                const int tap = gcol / cv.x.cp, ci = gcol % cv.x.cp;
-                if (b < kb1 && tap < cv.kh * cv.kw) {
-                    const int g = b / npix, pix = b % npix;
-                    const int oh = pix / cv.wo, ow = pix % cv.wo;
-                    const int ih = oh * cv.sh + tap / cv.kw - cv.ph, iw = ow * cv.sw + tap % cv.kw - cv.pw;
-                    if (ih >= 0 && ih < cv.h && iw >= 0 && iw < cv.w) {
-                        const size_t off = ((((size_t)g * cv.h + ih) * cv.w + iw) * cv.x.cp + ci) * (size_t)rb +
-                                           part * UNIT;
-                        v = *(const typename Vec<UNIT>::T*)(p.xc + off);
-                    }
-                }
-            }
-            rbv[i] = v;
+            const int part = u % parts, r1 = u / parts;
+            const int col = r1 % BN, blk = r1 / BN;
+            const int b = kb0 + 2 * s + blk;
+            const int gcol = BN * ct + col;
+            const int tap = gcol / cv.x.cp, ci = gcol % cv.x.cp;
+            const int bb = min(b, nkb - 1);
+            const int g = bb / npix, pix = bb % npix;
+            const int oh = pix / cv.wo, ow = pix % cv.wo;
+            const int ih = oh * cv.sh + tap / cv.kw - cv.ph, iw = ow * cv.sw + tap % cv.kw - cv.pw;
+            const bool ok = u < 2 * BN * parts && b < kb1 && tap < cv.kh * cv.kw && ih >= 0 && ih < cv.h &&
+                            iw >= 0 && iw < cv.w;
+            const size_t off = ((((size_t)g * cv.h + ih) * cv.w + iw) * cv.x.cp + ci) * (size_t)rb + part * UNIT;
+            const typename Vec<UNIT>::T v = *(const typename Vec<UNIT>::T*)(p.xc + (ok ? off : 0));
+            rbv[i] = ok ? v : vzero<UNIT>();
         }
         // scales: 4 for A (block x row block), 8 for B (block x column block)
         rs = 0;
@@ -592,6 +582,7 @@ __global__ __launch_bounds__(NT) void wgrad_kernel(WgradArgs p) {
 }
 
 // G_W[co][ci][kh][kw] = sum over splits of the partial (co, tap*Cin_p + ci).
+// Four independent partial sums keep several split loads in flight.
 __global__ __launch_bounds__(256) void wgrad_reduce(const float* __restrict__ part, float* __restrict__ gw,
                                                     Conv cv, int ntot, int splits) {
     const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;   // over (co, tap, ci) real
@@ -603,9 +594,18 @@ __global__ __launch_bounds__(256) void wgrad_reduce(const float* __restrict__ pa
     const int tap = (int)(r % taps);
     const int co = (int)(r / taps);
     const size_t col = (size_t)tap * cv.x.cp + ci;
-    float s = 0.0f;
-    for (int k = 0; k < splits; k++) s += part[((size_t)k * cv.gy.cp + co) * ntot + col];
-    gw[(((size_t)co * cv.cin + ci) * cv.kh + tap / cv.kw) * cv.kw + tap % cv.kw] = s;
+    const size_t stride = (size_t)cv.gy.cp * ntot;
+    const float* q = part + (size_t)co * ntot + col;
+    float s0 = 0.0f, s1 = 0.0f, s2 = 0.0f, s3 = 0.0f;
+    int k = 0;
+    for (; k + 4 <= splits; k += 4) {
+        s0 += __ldg(q + (size_t)k * stride);
+        s1 += __ldg(q + (size_t)(k + 1) * stride);
+        s2 += __ldg(q + (size_t)(k + 2) * stride);
+        s3 += __ldg(q + (size_t)(k + 3) * stride);
+    }
+    for (; k < splits; k++) s0 += __ldg(q + (size_t)k * stride);
+    gw[(((size_t)co * cv.cin + ci) * cv.kh + tap / cv.kw) * cv.kw + tap % cv.kw] = (s0 + s1) + (s2 + s3);
 }
 
 struct WgradPlan {

@@ -21,26 +21,39 @@ namespace mxc {
 namespace {
 
 constexpr int QT = 256;            // threads per workgroup
-constexpr int SLABS_PER_WG = 4;    // consecutive slabs per workgroup
 
 __device__ __forceinline__ int swz(int u) { return ((u >> 5) ^ (u >> 1)) & 7; }
 
-template <int DTYPE>
-__device__ __forceinline__ float load_elem(const void* src, size_t i) {
-    if (DTYPE == MXC_F32) return __ldg((const float*)src + i);
-    uint32_t b = (uint32_t)__ldg((const unsigned short*)src + i);
-    return __uint_as_float(b << 16);
+// Four consecutive source elements as floats (bf16 widened exactly).
+template <int DTYPE, int VEC>
+__device__ __forceinline__ float4 load4(const void* src, size_t i) {
+    if (VEC == 4) {
+        if (DTYPE == MXC_F32) return __ldg((const float4*)((const float*)src + i));
+        const uint2 b = __ldg((const uint2*)((const unsigned short*)src + i));
+        return make_float4(__uint_as_float(b.x << 16), __uint_as_float(b.x & 0xFFFF0000u),
+                           __uint_as_float(b.y << 16), __uint_as_float(b.y & 0xFFFF0000u));
+    }
+    float v;
+    if (DTYPE == MXC_F32) v = __ldg((const float*)src + i);
+    else v = __uint_as_float((uint32_t)__ldg((const unsigned short*)src + i) << 16);
+    return make_float4(v, 0.0f, 0.0f, 0.0f);
 }
 
-template <int LAYOUT, int DTYPE, int FMT>
+// VEC = 4: every thread moves 8 runs of 4 consecutive elements along the
+// source's contiguous dimension (16-byte loads); VEC = 1: 32 single elements.
+// All loads of a slab are issued before any is consumed (addresses of
+// out-of-range elements are clamped to the tensor's first element and the
+// value replaced by zero), so each thread has its whole slab share in flight.
+template <int LAYOUT, int DTYPE, int FMT, int VEC>
 __global__ __launch_bounds__(QT) void quantize_kernel(const void* __restrict__ src, Geom g,
                                                       uint8_t* __restrict__ codes,
                                                       uint8_t* __restrict__ scales,
-                                                      int nslabs, int pixblocks) {
+                                                      int nslabs, int pixblocks, int slabs_per_wg) {
     __shared__ __attribute__((aligned(16))) float slab[QT * 32];
     const int tid = threadIdx.x;
     const int bn = g.bn, tt = QT / bn;
     const int hw = g.h * g.w;
+    constexpr int NL = 32 / VEC;              // loads per thread per slab
 
     // XCD-aware order: workgroups are dealt round-robin to the 8 XCDs, so give
     // each XCD a contiguous range of slabs (neighbouring pixel blocks share
@@ -48,10 +61,9 @@ __global__ __launch_bounds__(QT) void quantize_kernel(const void* __restrict__ s
     const int nwg = gridDim.x;
     const int per_xcd = (nwg + 7) / 8;
     const int wg = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-    if (wg >= nwg) return;
 
-    for (int it = 0; it < SLABS_PER_WG; it++) {
-        const int slab_id = wg * SLABS_PER_WG + it;
+    for (int it = 0; it < slabs_per_wg; it++) {
+        const int slab_id = wg * slabs_per_wg + it;
         if (slab_id >= nslabs) return;
         const int pb = slab_id % pixblocks;
         const int rest = slab_id / pixblocks;
@@ -59,10 +71,12 @@ __global__ __launch_bounds__(QT) void quantize_kernel(const void* __restrict__ s
         const int ng = rest / g.ncb;
         const int p0 = pb * tt;
 
-        // ---- 1. load into the slab (code order, swizzled chunks)
-#pragma unroll 8
-        for (int r = 0; r < 32; r++) {
-            const int e = tid + QT * r;
+        // ---- 1. load (all loads first), then store into the slab in code order
+        float4 v[NL];
+        int ci0[NL];
+#pragma unroll
+        for (int r = 0; r < NL; r++) {
+            const int e = (tid + QT * r) * VEC;
             int pl, cl, j;
             if (LAYOUT == MXC_NCHW) {
                 pl = e % tt; const int r1 = e / tt; cl = r1 & 31; j = r1 >> 5;
@@ -72,17 +86,28 @@ __global__ __launch_bounds__(QT) void quantize_kernel(const void* __restrict__ s
                 j = e % bn; const int r1 = e / bn; cl = r1 & 31; pl = r1 >> 5;
             }
             const int pix = p0 + pl, c = cb * 32 + cl, n = ng * bn + j;
-            float v = 0.0f;
-            if (pix < hw && c < g.c && n < g.n) {
-                size_t gi;
-                if (LAYOUT == MXC_NCHW)      gi = ((size_t)n * g.c + c) * hw + pix;
-                else if (LAYOUT == MXC_NHWC) gi = ((size_t)n * hw + pix) * g.c + c;
-                else                         gi = (((size_t)ng * hw + pix) * g.c + c) * bn + j;
-                v = load_elem<DTYPE>(src, gi);
+            const bool ok = pix < hw && c < g.c && n < g.n;
+            size_t gi;
+            if (LAYOUT == MXC_NCHW)      gi = ((size_t)n * g.c + c) * hw + pix;
+            else if (LAYOUT == MXC_NHWC) gi = ((size_t)n * hw + pix) * g.c + c;
+            else                         gi = (((size_t)ng * hw + pix) * g.c + c) * bn + j;
+            v[r] = load4<DTYPE, VEC>(src, ok ? gi : 0);
+            if (!ok) v[r] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            ci0[r] = (pl * 32 + cl) * bn + j;          // canonical index of the first element
+        }
+#pragma unroll
+        for (int r = 0; r < NL; r++) {
+            const float x4[4] = {v[r].x, v[r].y, v[r].z, v[r].w};
+#pragma unroll
+            for (int q = 0; q < VEC; q++) {
+                // the q-th element steps along the contiguous dimension
+                int ci;
+                if (LAYOUT == MXC_NCHW)      ci = ci0[r] + q * 32 * bn;
+                else if (LAYOUT == MXC_NHWC) ci = ci0[r] + q * bn;
+                else                         ci = ci0[r] + q;
+                const int u = ci >> 5, k = ci & 31;
+                slab[u * 32 + ((((k >> 2) ^ swz(u))) << 2) + (k & 3)] = x4[q];
             }
-            const int ci = (pl * 32 + cl) * bn + j;      // canonical index in the slab
-            const int u = ci >> 5, k = ci & 31;
-            slab[u * 32 + ((((k >> 2) ^ swz(u))) << 2) + (k & 3)] = v;
         }
         __syncthreads();
 
@@ -143,13 +168,26 @@ __global__ __launch_bounds__(QT) void quantize_kernel(const void* __restrict__ s
 template <int LAYOUT, int DTYPE, int FMT>
 int launch_q(const void* src, const Geom& g, void* codes, uint8_t* scales, hipStream_t s) {
     const int tt = QT / g.bn;
-    const int pixblocks = (g.h * g.w + tt - 1) / tt;
+    const int hw = g.h * g.w;
+    const int pixblocks = (hw + tt - 1) / tt;
     const long nslabs = (long)g.ng * g.ncb * pixblocks;
-    if (nslabs > 0x7FFFFFFFL / SLABS_PER_WG) return MXC_ERR_SHAPE;
-    const int nwg = (int)((nslabs + SLABS_PER_WG - 1) / SLABS_PER_WG);
+    // 16-byte loads need runs of 4 along the contiguous dimension that never
+    // straddle a row: pixels (NCHW), channels (NHWC) or samples (CBF)
+    bool vec4;
+    if (LAYOUT == MXC_NCHW)      vec4 = hw % 4 == 0 && tt % 4 == 0;
+    else if (LAYOUT == MXC_NHWC) vec4 = g.c % 4 == 0;
+    else                         vec4 = g.bn % 4 == 0;
+    // NCHW: neighbouring pixel blocks share cache lines, keep a few together
+    const int spw = LAYOUT == MXC_NCHW ? 2 : 1;
+    if (nslabs > 0x7FFFFFFFL / spw) return MXC_ERR_SHAPE;
+    const int nwg = (int)((nslabs + spw - 1) / spw);
     const int grid = (nwg + 7) / 8 * 8;     // whole rounds over the 8 XCDs
-    hipLaunchKernelGGL((quantize_kernel<LAYOUT, DTYPE, FMT>), dim3(grid), dim3(QT), 0, s, src, g,
-                       (uint8_t*)codes, scales, (int)nslabs, pixblocks);
+    if (vec4)
+        hipLaunchKernelGGL((quantize_kernel<LAYOUT, DTYPE, FMT, 4>), dim3(grid), dim3(QT), 0, s, src, g,
+                           (uint8_t*)codes, scales, (int)nslabs, pixblocks, spw);
+    else
+        hipLaunchKernelGGL((quantize_kernel<LAYOUT, DTYPE, FMT, 1>), dim3(grid), dim3(QT), 0, s, src, g,
+                           (uint8_t*)codes, scales, (int)nslabs, pixblocks, spw);
     return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
 }
 
