@@ -31,6 +31,7 @@ namespace {
 constexpr int BM = 64;    // output rows per workgroup (2 MFMA row blocks)
 constexpr int BN = 128;   // output columns per workgroup (4 MFMA column blocks)
 constexpr int NT = 256;   // 4 waves: wave w owns rows 32*(w&1), columns 64*(w>>1)
+constexpr int SP = 4;     // streamed wgrad: pixel blocks per stage
 
 template <int UNIT> struct Vec;
 template <> struct Vec<16> { typedef uint4 T; };
@@ -612,6 +613,8 @@ struct WgradPlan {
     int mtiles, ctiles, splits, kbps, ntot;
 };
 
+bool wstream_ok(const Conv& cv);
+
 WgradPlan wgrad_plan(const Conv& cv) {
     WgradPlan pl;
     pl.ntot = cv.kh * cv.kw * cv.x.cp;
@@ -619,13 +622,18 @@ WgradPlan wgrad_plan(const Conv& cv) {
     pl.ctiles = (pl.ntot + BN - 1) / BN;
     const long nkb = (long)cv.x.ng * cv.ho * cv.wo;
     const long tiles = (long)pl.mtiles * pl.ctiles;
-    const long target = 1024;                    // workgroups to fill 256 CUs
+    // enough workgroups for the 256 CUs, but long enough K ranges that the
+    // partial sums stay small next to the operands
+    const bool streamed = wstream_ok(cv);
+    const long target = streamed ? 512 : 1024;
+    const long min_kb = streamed ? 32 : 16;
+    const long gran = streamed ? SP : 2;
     long splits = (target + tiles - 1) / tiles;
-    const long max_splits = (nkb + 15) / 16;     // at least 8 K steps per split
+    const long max_splits = (nkb + min_kb - 1) / min_kb;
     if (splits > max_splits) splits = max_splits;
     if (splits < 1) splits = 1;
     long kbps = (nkb + splits - 1) / splits;
-    kbps = (kbps + 1) / 2 * 2;
+    kbps = (kbps + gran - 1) / gran * gran;
     splits = (nkb + kbps - 1) / kbps;
     pl.splits = (int)splits;
     pl.kbps = (int)kbps;
@@ -646,15 +654,626 @@ int launch_wgrad_f(const WgradArgs& a, dim3 grid, hipStream_t s) {
     return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
 }
 
+
+// ============================================================ streamed kernels
+// Used when a block row is at least 8 bytes (FP8 Bn >= 8, FP4 Bn >= 16).  LDS
+// holds whole blocks ("tile-major": a block is 32 rows x Bn codes, exactly as
+// stored), streamed in by global_load_lds_dwordx4: every lane moves 16 bytes
+// from its own global address to LDS base + 16*lane, so one wave instruction
+// fills 1 KB and nothing passes through registers.  Taps in the padding read a
+// zero block.  Two stages are double-buffered: the next stage's loads are in
+// flight while the current stage's MFMAs run.
+
+__device__ __attribute__((aligned(16))) uint8_t g_zero_block[1024];
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// 16 bytes per lane from gsrc into lds_base + 16 * lane.
+__device__ __forceinline__ void lds_dma16(const void* gsrc, uint8_t* lds_base) {
+    __builtin_amdgcn_global_load_lds(gsrc, (lds_void*)lds_base, 16, 0, 0);
+}
+
+__device__ __forceinline__ void wait_dma() {
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this wave's LDS DMA has landed
+}
+
+struct StreamArgs {
+    Conv cv;
+    const uint8_t* wc;
+    const uint8_t* ws;
+    const uint8_t* bc;
+    const uint8_t* bs;
+    float* out;
+    int layout;
+    int M;                     // real output channels
+    int mtiles;
+    int P;                     // output pixels per tile (BN / Bn), along one output row
+    int kcb;                   // channel blocks along K
+    int hs, wsrc, cps, ncbs;   // activation operand geometry
+    int hout, wout;            // output spatial size
+    int ctiles_max;            // column tiles of the largest phase
+    int a_bytes, b_bytes, stage_bytes;   // per-stage LDS regions (A, B, + scales)
+};
+
+// fwd / dgrad: one stage = one kernel row (its taps) x two channel blocks.
+// B holds the halo of source pixels the row's taps read for the tile's P
+// output pixels: [block][halo column] blocks; A holds the weight blocks
+// [tap][block][row block].
+//
+// Address arithmetic is kept off the critical path: Bn is a template
+// parameter (pixel / sample splits are shifts), every lane builds the
+// stage-invariant part of its DMA source offsets once, and a stage only adds
+// one delta per operand.  Offsets are 32-bit (tensors below 4 GB).
+constexpr int NDMA = 8;        // DMA instructions per wave per stage (<= 32 KB stages)
+
+template <int FMT, bool DG, int BNS>
+__global__ __launch_bounds__(NT) void conv_stream_kernel(StreamArgs p) {
+    constexpr int EB = FMT == MXC_E4M3 ? 8 : 4;
+    constexpr int TA = 32 * 32 * EB / 8;              // bytes of a weight block
+    constexpr int RB = BNS * EB / 8;                  // bytes of an activation block row
+    constexpr int TB = 32 * RB;                       // bytes of an activation block
+    constexpr int P = BN / BNS;                       // output pixels per tile
+    constexpr int LOGB = BNS == 32 ? 5 : BNS == 16 ? 4 : 3;
+    extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+    const Conv& cv = p.cv;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+
+    // ---- tile: XCD-aware linear order over (column tile, row tile)
+    const int ntile = p.mtiles * p.ctiles_max;
+    const int per_xcd = (gridDim.x + 7) / 8;
+    const int lin = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+    if (lin >= ntile) return;
+    const int mt = lin % p.mtiles, ct = lin / p.mtiles;
+
+    // ---- phase and the taps that reach it (fwd: one phase, all taps)
+    int ry = 0, rx = 0, kh0 = 0, kw0 = 0, nvh = cv.kh, nvw = cv.kw, gh = cv.ho, gw = cv.wo;
+    if (DG) {
+        ry = blockIdx.y / cv.sw; rx = blockIdx.y % cv.sw;
+        kh0 = (ry + cv.ph) % cv.sh; kw0 = (rx + cv.pw) % cv.sw;
+        nvh = kh0 < cv.kh ? (cv.kh - kh0 + cv.sh - 1) / cv.sh : 0;
+        nvw = kw0 < cv.kw ? (cv.kw - kw0 + cv.sw - 1) / cv.sw : 0;
+        gh = ry < cv.h ? (cv.h - ry + cv.sh - 1) / cv.sh : 0;
+        gw = rx < cv.w ? (cv.w - rx + cv.sw - 1) / cv.sw : 0;
+    }
+    const int nseg = (gw + P - 1) / P;
+    const int tiles = cv.x.ng * gh * nseg;
+    if (ct >= tiles) return;
+    const int seg = ct % nseg;
+    const int r0 = ct / nseg;
+    const int oyr = r0 % gh, g = r0 / gh;
+    const int b0 = seg * P;
+
+    const int CS = DG ? 1 : cv.sw;
+    const int ntw = nvw;
+    const int HC = (P - 1) * CS + ntw;
+    const int cbase = DG ? b0 + (rx + cv.pw - (kw0 + cv.sw * (ntw - 1))) / cv.sw : b0 * cv.sw - cv.pw;
+    const int nkk = (p.kcb + 1) / 2;
+    const int nstage = ntw > 0 ? nkk * nvh : 0;
+    const int a_pieces = ntw * 4 * TA / 16;
+    const int b_pieces = 2 * HC * TB / 16;
+    const int a_ins = (a_pieces + 63) / 64, b_ins = (b_pieces + 63) / 64;
+
+    // strides (bytes) of the stored tensors
+    const uint32_t w_kc = DG ? (uint32_t)cv.kh * cv.kw * cv.wt.cp * 32 * EB / 8 : (uint32_t)TA;   // per K block
+    const uint32_t w_kh = (uint32_t)cv.kw * cv.wt.cp * 32 * EB / 8;
+    const uint32_t x_row = (uint32_t)p.wsrc * p.cps * RB;
+    const uint32_t x_kc = 32u * RB;
+
+    // ---- per-lane DMA descriptors (stage-invariant)
+    uint32_t d_off[NDMA];     // invariant source offset
+    uint32_t d_zero[NDMA];    // offset inside the zero block
+    int d_info[NDMA];         // bit0: B piece, bit1: block 1, bit2: invariant-valid, bit3: lane active
+#pragma unroll
+    for (int k = 0; k < NDMA; k++) {
+        const int ins = wave + 4 * k;
+        d_off[k] = 0; d_zero[k] = 0; d_info[k] = 0;
+        if (ins >= a_ins + b_ins) continue;
+        const bool isA = ins < a_ins;
+        const int pc = (isA ? ins : ins - a_ins) * 64 + lane;
+        if (isA) {
+            const int t = pc / (4 * TA / 16), rem = pc % (4 * TA / 16);
+            const int blk = rem / (2 * TA / 16), mb = (rem / (TA / 16)) & 1;
+            const int within = (pc % (TA / 16)) * 16;
+            const int rowblk = 2 * mt + mb;
+            const int kw = DG ? kw0 + cv.sw * t : t;
+            const bool ok = DG ? rowblk < cv.wt.ncb : rowblk < cv.wt.np / 32;
+            const int cob = DG ? 0 : rowblk, cib = DG ? rowblk : 0;
+            d_off[k] = ((((uint32_t)cob * cv.kh) * cv.kw + kw) * cv.wt.cp + 32 * cib) * (uint32_t)(32 * EB / 8) +
+                       (uint32_t)blk * w_kc + within;
+            d_zero[k] = within;
+            d_info[k] = (blk << 1) | (ok ? 4 : 0) | (pc < a_pieces ? 8 : 0);
+        } else {
+            const int tile = pc / (TB / 16), within = (pc % (TB / 16)) * 16;
+            const int blk = tile / HC, hc = tile % HC;
+            const int sx = cbase + hc;
+            const bool ok = sx >= 0 && sx < p.wsrc;
+            d_off[k] = ((uint32_t)g * p.hs * p.wsrc + (ok ? sx : 0)) * (uint32_t)p.cps * RB +
+                       (uint32_t)blk * x_kc + within;
+            d_zero[k] = within;
+            d_info[k] = 1 | (blk << 1) | (ok ? 4 : 0) | (pc < b_pieces ? 8 : 0);
+        }
+    }
+    // scale descriptors: threads [0, ntw*4) A scales, [ntw*4, ntw*4 + 2*HC) B scales
+    const int na = ntw * 4;
+    uint32_t s_off = 0;
+    int s_info = 0;
+    if (tid < na) {
+        const int t = tid >> 2, blk = (tid >> 1) & 1, mb = tid & 1;
+        const int rowblk = 2 * mt + mb, kw = DG ? kw0 + cv.sw * t : t;
+        const bool ok = DG ? rowblk < cv.wt.ncb : rowblk < cv.wt.np / 32;
+        const int cob = DG ? 0 : rowblk, cib = DG ? rowblk : 0;
+        s_off = (((uint32_t)cob * cv.kh) * cv.kw + kw) * cv.wt.ncb + cib +
+                (uint32_t)blk * (DG ? (uint32_t)cv.kh * cv.kw * cv.wt.ncb : 1u);
+        s_info = (blk << 1) | (ok ? 4 : 0) | 8;
+    } else if (tid < na + 2 * HC) {
+        const int q = tid - na, blk = q / HC, hc = q % HC;
+        const int sx = cbase + hc;
+        const bool ok = sx >= 0 && sx < p.wsrc;
+        s_off = ((uint32_t)g * p.hs * p.wsrc + (ok ? sx : 0)) * p.ncbs + blk;
+        s_info = 1 | (blk << 1) | (ok ? 4 : 0) | 8;
+    }
+
+    int sreg = 0;
+    auto issue = [&](int st, int buf) {
+        uint8_t* base = smem + buf * p.stage_bytes;
+        const int kk = st / nvh, ri = st % nvh;
+        const int kh = DG ? kh0 + cv.sh * ri : ri;
+        const int sy = DG ? oyr + (ry + cv.ph - kh) / cv.sh : oyr * cv.sh + kh - cv.ph;
+        const bool row_ok = sy >= 0 && sy < p.hs;
+        const bool blk1_ok = 2 * kk + 1 < p.kcb;
+        const uint32_t add_a = (uint32_t)kh * w_kh + (uint32_t)(2 * kk) * w_kc;
+        const uint32_t add_b = (uint32_t)(row_ok ? sy : 0) * x_row + (uint32_t)(2 * kk) * x_kc;
+#pragma unroll
+        for (int k = 0; k < NDMA; k++) {
+            const int ins = wave + 4 * k;
+            if (ins >= a_ins + b_ins) break;
+            const int info = d_info[k];
+            const bool isB = info & 1;
+            const bool ok = (info & 4) && ((info & 2) == 0 || blk1_ok) && (!isB || row_ok);
+            const uint8_t* src = ok ? (isB ? p.bc + d_off[k] + add_b : p.wc + d_off[k] + add_a)
+                                    : g_zero_block + d_zero[k];
+            uint8_t* dst = isB ? base + p.a_bytes + (ins - a_ins) * 1024 : base + ins * 1024;
+            if (info & 8) lds_dma16(src, dst);
+        }
+        sreg = 0;
+        if (s_info & 8) {
+            const bool isB = s_info & 1;
+            const bool ok = (s_info & 4) && ((s_info & 2) == 0 || blk1_ok) && (!isB || row_ok);
+            const uint32_t o = isB ? s_off + (uint32_t)(row_ok ? sy : 0) * p.wsrc * p.ncbs + 2 * kk
+                                   : s_off + (uint32_t)kh * cv.kw * cv.wt.ncb +
+                                         (uint32_t)(2 * kk) * (DG ? (uint32_t)cv.kh * cv.kw * cv.wt.ncb : 1u);
+            sreg = ok ? (isB ? p.bs[o] : p.ws[o]) : 0;
+        }
+    };
+    auto store_scales = [&](int buf) {
+        if (s_info & 8) smem[buf * p.stage_bytes + p.a_bytes + p.b_bytes + tid] = (uint8_t)sreg;
+    };
+
+    const int wm = wave & 1, wn = wave >> 1;
+    const int h = lane >> 5;
+    // per-lane fragment addresses (bytes from the stage base)
+    const int i16 = lane & 15, gi = lane >> 4, cg = gi & 1, hh = gi >> 1;
+    int a_lane;                       // A: offset inside a weight block
+    if (DG) a_lane = FMT == MXC_E4M3 ? (lane & 31) * 32 + 16 * h : (lane & 31) * 16;
+    else    a_lane = FMT == MXC_E4M3 ? (16 * hh + (i16 >> 1)) * 32 + 16 * cg + 8 * (i16 & 1)
+                                     : i16 * 16 + 8 * cg;
+    int b_lane[2], b_hc[2], s_hc[2];
+#pragma unroll
+    for (int c = 0; c < 2; c++) {
+        const int colbase = 64 * wn + 32 * c;
+        const int col = FMT == MXC_E4M3 ? colbase + 16 * cg + 8 * (i16 & 1) : colbase + 16 * cg;
+        const int pix = col >> LOGB, jb = (col & (BNS - 1)) * EB / 8;
+        b_hc[c] = pix * CS;
+        b_lane[c] = FMT == MXC_E4M3 ? (16 * hh + (i16 >> 1)) * RB + jb : i16 * RB + jb;
+        s_hc[c] = ((colbase + (lane & 31)) >> LOGB) * CS;
+    }
+
+    v16f acc[2];
+    for (int c = 0; c < 2; c++)
+        for (int e = 0; e < 16; e++) acc[c][e] = 0.0f;
+
+    if (nstage > 0) {
+        issue(0, 0);
+        wait_dma();
+        store_scales(0);
+    }
+    __syncthreads();
+    for (int st = 0; st < nstage; st++) {
+        const int buf = st & 1;
+        if (st + 1 < nstage) issue(st + 1, buf ^ 1);
+        const uint8_t* A = smem + buf * p.stage_bytes;
+        const uint8_t* B = A + p.a_bytes;
+        const uint8_t* SC = B + p.b_bytes;
+        for (int t = 0; t < ntw; t++) {
+            const int co = DG ? ntw - 1 - t : t;         // halo column offset of this tap
+            const uint8_t* a0 = A + ((t * 2 + 0) * 2 + wm) * TA + a_lane;
+            const uint8_t* a1 = a0 + 2 * TA;
+            v8i af;
+            if (DG) {
+                if (FMT == MXC_E4M3) {
+                    const v4i x0 = *(const v4i*)a0;
+                    const v4i x1 = *(const v4i*)a1;
+                    af[0] = x0[0]; af[1] = x0[1]; af[2] = x0[2]; af[3] = x0[3];
+                    af[4] = x1[0]; af[5] = x1[1]; af[6] = x1[2]; af[7] = x1[3];
+                } else {
+                    const v4i x0 = *(const v4i*)(h ? a1 : a0);
+                    af[0] = x0[0]; af[1] = x0[1]; af[2] = x0[2]; af[3] = x0[3];
+                    af[4] = af[5] = af[6] = af[7] = 0;
+                }
+            } else {
+                if (FMT == MXC_E4M3) {
+#pragma unroll
+                    for (int blk = 0; blk < 2; blk++)
+#pragma unroll
+                        for (int hf = 0; hf < 2; hf++) {
+                            const v2i v = lds_tr8((blk ? a1 : a0) + hf * 8 * 32);
+                            af[4 * blk + 2 * hf] = v[0];
+                            af[4 * blk + 2 * hf + 1] = v[1];
+                        }
+                } else {
+                    const uint8_t* ab = hh ? a1 : a0;
+#pragma unroll
+                    for (int hf = 0; hf < 2; hf++) {
+                        const v2i v = lds_tr4(ab + hf * 16 * 16);
+                        af[2 * hf] = v[0];
+                        af[2 * hf + 1] = v[1];
+                    }
+                    af[4] = af[5] = af[6] = af[7] = 0;
+                }
+            }
+            const int sa = SC[(t * 2 + h) * 2 + wm];
+#pragma unroll
+            for (int c = 0; c < 2; c++) {
+                v8i bf;
+                const int hc = b_hc[c] + co;
+                if (FMT == MXC_E4M3) {
+                    const uint8_t* tb = B + hc * TB + b_lane[c];
+#pragma unroll
+                    for (int blk = 0; blk < 2; blk++)
+#pragma unroll
+                        for (int hf = 0; hf < 2; hf++) {
+                            const v2i v = lds_tr8(tb + blk * HC * TB + hf * 8 * RB);
+                            bf[4 * blk + 2 * hf] = v[0];
+                            bf[4 * blk + 2 * hf + 1] = v[1];
+                        }
+                } else {
+                    const uint8_t* tb = B + (hh * HC + hc) * TB + b_lane[c];
+#pragma unroll
+                    for (int hf = 0; hf < 2; hf++) {
+                        const v2i v = lds_tr4(tb + hf * 16 * RB);
+                        bf[2 * hf] = v[0];
+                        bf[2 * hf + 1] = v[1];
+                    }
+                    bf[4] = bf[5] = bf[6] = bf[7] = 0;
+                }
+                const int sb = SC[ntw * 4 + h * HC + s_hc[c] + co];
+                acc[c] = mfma_mx<FMT>(af, bf, acc[c], sa, sb);
+            }
+        }
+        if (st + 1 < nstage) {
+            wait_dma();
+            store_scales(buf ^ 1);
+        }
+        __syncthreads();
+    }
+
+    // ---- epilogue: lane's column is fixed; rows step by 1 / 8
+    const int oy = DG ? ry + cv.sh * oyr : oyr;
+#pragma unroll
+    for (int c = 0; c < 2; c++) {
+        const int col = 64 * wn + 32 * c + (lane & 31);
+        const int pix = col >> LOGB, j = col & (BNS - 1);
+        const int ox_g = b0 + pix;
+        if (ox_g >= gw) continue;
+        const int ox = DG ? rx + cv.sw * ox_g : ox_g;
+        const int m0 = BM * mt + 32 * wm + 4 * h;
+        size_t o0, mstride;
+        if (p.layout == MXC_CBF) {
+            o0 = ((((size_t)g * p.hout + oy) * p.wout + ox) * p.M + m0) * BNS + j;
+            mstride = BNS;
+        } else {
+            o0 = (((size_t)(g * BNS + j) * p.M + m0) * p.hout + oy) * p.wout + ox;
+            mstride = (size_t)p.hout * p.wout;
+        }
+#pragma unroll
+        for (int e = 0; e < 16; e++) {
+            const int dm = 8 * (e >> 2) + (e & 3);
+            if (m0 + dm < p.M) p.out[o0 + dm * mstride] = acc[c][e];
+        }
+    }
+}
+
+// transposing reads need 8 consecutive FP8 samples / 16 consecutive FP4 samples
+// of one block row, i.e. rows of at least 8 bytes
+bool stream_ok(const Conv& cv) { return cv.x.bn * cv.bits >= 64; }
+
+int launch_conv_stream(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const void* bc,
+                       const uint8_t* bs, float* out, int layout, hipStream_t s) {
+    StreamArgs a;
+    a.cv = cv;
+    a.wc = (const uint8_t*)wc; a.ws = ws; a.bc = (const uint8_t*)bc; a.bs = bs;
+    a.out = out; a.layout = layout;
+    const Geom& src = dg ? cv.gy : cv.x;
+    a.hs = src.h; a.wsrc = src.w; a.cps = src.cp; a.ncbs = src.ncb;
+    a.kcb = dg ? cv.wt.np / 32 : cv.wt.ncb;
+    a.M = dg ? cv.cin : cv.cout;
+    a.hout = dg ? cv.h : cv.ho;
+    a.wout = dg ? cv.w : cv.wo;
+    a.mtiles = (a.M + BM - 1) / BM;
+    a.P = BN / cv.x.bn;
+    const int EB = cv.bits;
+    const int TA = 32 * 32 * EB / 8, TB = 32 * cv.x.bn * EB / 8;
+    // LDS: the largest stage over the phases
+    long maxtiles = 0;
+    int max_ntw = 0, max_hc = 0;
+    const int nph = dg ? cv.sh * cv.sw : 1;
+    for (int ph = 0; ph < nph; ph++) {
+        const int ry = dg ? ph / cv.sw : 0, rx = dg ? ph % cv.sw : 0;
+        const int kw0 = dg ? (rx + cv.pw) % cv.sw : 0;
+        const int nvw = dg ? (kw0 < cv.kw ? (cv.kw - kw0 + cv.sw - 1) / cv.sw : 0) : cv.kw;
+        const long gh = dg ? (ry < cv.h ? (cv.h - ry + cv.sh - 1) / cv.sh : 0) : cv.ho;
+        const long gw = dg ? (rx < cv.w ? (cv.w - rx + cv.sw - 1) / cv.sw : 0) : cv.wo;
+        const long tiles = (long)cv.x.ng * gh * ((gw + a.P - 1) / a.P);
+        if (tiles > maxtiles) maxtiles = tiles;
+        const int hcv = (a.P - 1) * (dg ? 1 : cv.sw) + nvw;
+        if (nvw > max_ntw) max_ntw = nvw;
+        if (hcv > max_hc) max_hc = hcv;
+    }
+    a.a_bytes = max_ntw * 4 * TA;
+    a.b_bytes = 2 * max_hc * TB;
+    // each wave issues at most NDMA 1 KB DMA instructions per stage
+    if ((a.a_bytes + 1023) / 1024 + (a.b_bytes + 1023) / 1024 > 4 * NDMA)
+        return launch_conv(cv, dg, wc, ws, bc, bs, out, layout, s);
+    a.stage_bytes = (a.a_bytes + a.b_bytes + max_ntw * 4 + 2 * max_hc + 15) / 16 * 16;
+    const size_t lds = 2 * (size_t)a.stage_bytes;
+    if (lds > 64 * 1024) return launch_conv(cv, dg, wc, ws, bc, bs, out, layout, s);
+    const long ntile = maxtiles * a.mtiles;
+    if (ntile > 0x7FFFFFF0L) return MXC_ERR_SHAPE;
+    a.ctiles_max = (int)maxtiles;
+    const dim3 grid((unsigned)((ntile + 7) / 8 * 8), nph);
+#define MXC_LAUNCH_CS(F, D, B) hipLaunchKernelGGL((conv_stream_kernel<F, D, B>), grid, dim3(NT), lds, s, a)
+    const int bn = cv.x.bn;
+    if (cv.fmt == MXC_E4M3) {
+        if (bn == 32)      { if (dg) MXC_LAUNCH_CS(MXC_E4M3, true, 32); else MXC_LAUNCH_CS(MXC_E4M3, false, 32); }
+        else if (bn == 16) { if (dg) MXC_LAUNCH_CS(MXC_E4M3, true, 16); else MXC_LAUNCH_CS(MXC_E4M3, false, 16); }
+        else               { if (dg) MXC_LAUNCH_CS(MXC_E4M3, true, 8);  else MXC_LAUNCH_CS(MXC_E4M3, false, 8); }
+    } else {
+        if (bn == 32)      { if (dg) MXC_LAUNCH_CS(MXC_E2M1, true, 32); else MXC_LAUNCH_CS(MXC_E2M1, false, 32); }
+        else               { if (dg) MXC_LAUNCH_CS(MXC_E2M1, true, 16); else MXC_LAUNCH_CS(MXC_E2M1, false, 16); }
+    }
+#undef MXC_LAUNCH_CS
+    return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
+}
+
+
+// wgrad: output tile BM x BN as in wgrad_kernel; one stage = SP pixel blocks
+// (SP/2 MFMA K steps).  LDS blocks are full 32 x 32-element MFMA blocks; a
+// batch block shorter than 32 samples is padded with zero pieces.
+struct WStreamArgs {
+    Conv cv;
+    const uint8_t* gc;
+    const uint8_t* gs;
+    const uint8_t* xc;
+    const uint8_t* xs;
+    float* part;
+    int ntot, mtiles, ctiles, splits, kbps;   // kbps: K blocks per split, a multiple of SP
+};
+
+template <int FMT>
+__global__ __launch_bounds__(NT) void wgrad_stream_kernel(WStreamArgs p) {
+    constexpr int EB = FMT == MXC_E4M3 ? 8 : 4;
+    constexpr int ROWB = 32 * EB / 8;                  // bytes of a 32-element row
+    constexpr int TT = 32 * ROWB;                      // bytes of an LDS block
+    constexpr int A_BYTES = SP * 2 * TT, B_BYTES = SP * 4 * TT;
+    constexpr int STAGE = A_BYTES + B_BYTES + 32;      // + scales (SP*2 + SP*4 bytes)
+    __shared__ __attribute__((aligned(16))) uint8_t smem[2 * STAGE];
+    const Conv& cv = p.cv;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int bn = cv.x.bn;
+    const int rb = bn * EB / 8;                        // real bytes of a row (>= 16)
+    const int npix = cv.ho * cv.wo;
+    const int nkb = cv.x.ng * npix;
+    const int cinb = cv.x.ncb, taps = cv.kh * cv.kw;
+
+    const int ntile = p.mtiles * p.ctiles * p.splits;
+    const int per_xcd = (gridDim.x + 7) / 8;
+    const int lin = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+    if (lin >= ntile) return;
+    const int mt = lin % p.mtiles;
+    const int r0 = lin / p.mtiles;
+    const int ct = r0 % p.ctiles, sp = r0 / p.ctiles;
+    const int kb0 = sp * p.kbps;
+    const int kb1 = min(nkb, kb0 + p.kbps);
+    const int nstage = kb1 > kb0 ? (kb1 - kb0 + SP - 1) / SP : 0;
+
+    // ---- per-lane DMA descriptors.  An LDS block is 1 KB (FP8) or 512 B (FP4),
+    // so one 1 KB instruction carries blocks of a single pixel slot pi; the
+    // stage only supplies that slot's K block (group, output pixel).
+    constexpr int PT = TT / 16;
+    constexpr int NINS = (A_BYTES + B_BYTES) / 1024;    // instructions per stage
+    constexpr int NK = NINS / 4;                        // per wave
+    static_assert(NINS % 4 == 0, "stage must split evenly over 4 waves");
+    const uint32_t gy_pix = (uint32_t)cv.gy.cp * rb;    // bytes of one G_Y pixel (all blocks)
+    const uint32_t x_pix = (uint32_t)cv.x.cp * rb;
+    uint32_t d_off[NK];
+    int d_pi[NK], d_kh[NK], d_kw[NK], d_ok[NK], d_b[NK];
+#pragma unroll
+    for (int k = 0; k < NK; k++) {
+        const int ins = wave + 4 * k;
+        const int pc = ins * 64 + lane;
+        const int tile = pc / PT, within = (pc % PT) * 16;
+        const int row = within / ROWB, byte = within % ROWB;
+        d_b[k] = tile >= SP * 2;
+        if (!d_b[k]) {
+            const int pi = tile >> 1, mb = tile & 1, cob = 2 * mt + mb;
+            d_pi[k] = pi; d_kh[k] = 0; d_kw[k] = 0;
+            d_ok[k] = byte < rb && cob < cv.gy.ncb;
+            d_off[k] = (uint32_t)(32 * cob + row) * rb + byte;
+        } else {
+            const int t2 = tile - SP * 2, pi = t2 >> 2, cbk = t2 & 3;
+            const int gcb = 4 * ct + cbk, tap = gcb / cinb, cib = gcb % cinb;
+            d_pi[k] = pi; d_kh[k] = tap / cv.kw; d_kw[k] = tap % cv.kw;
+            d_ok[k] = byte < rb && tap < taps;
+            d_off[k] = (uint32_t)(32 * cib + row) * rb + byte;
+        }
+    }
+    // scale descriptors: threads [0, 2*SP) G_Y scales, [2*SP, 6*SP) X scales
+    int s_pi = 0, s_kh = 0, s_kw = 0, s_ok = 0, s_idx = 0;
+    if (tid < SP * 2) {
+        const int mb = tid & 1, cob = 2 * mt + mb;
+        s_pi = tid >> 1; s_ok = cob < cv.gy.ncb; s_idx = cob;
+    } else if (tid < SP * 6) {
+        const int t2 = tid - SP * 2, cbk = t2 & 3;
+        const int gcb = 4 * ct + cbk, tap = gcb / cinb;
+        s_pi = t2 >> 2; s_ok = tap < taps; s_kh = tap / cv.kw; s_kw = tap % cv.kw; s_idx = gcb % cinb;
+    }
+
+    int sreg = 0;
+    auto issue = [&](int st, int buf) {
+        uint8_t* base = smem + buf * STAGE;
+        const int bst = kb0 + st * SP;
+        // positions (group, oh, ow) of the stage's SP K blocks (wave-uniform)
+        int pg[SP], poh[SP], pw[SP];
+        {
+            const int g0 = bst / npix, px = bst % npix;
+            int gg = g0, oh = px / cv.wo, ow = px % cv.wo;
+#pragma unroll
+            for (int i = 0; i < SP; i++) {
+                pg[i] = gg; poh[i] = oh; pw[i] = ow;
+                ow++;
+                const bool wrap = ow == cv.wo;
+                ow = wrap ? 0 : ow;
+                oh += wrap ? 1 : 0;
+                const bool wrap2 = oh == cv.ho;
+                oh = wrap2 ? 0 : oh;
+                gg += wrap2 ? 1 : 0;
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < NK; k++) {
+            const int ins = wave + 4 * k;
+            const int pi = d_pi[k];
+            const int b = bst + pi;
+            const int gg = pi == 0 ? pg[0] : pi == 1 ? pg[1] : pi == 2 ? pg[2] : pg[3];
+            const int oh = pi == 0 ? poh[0] : pi == 1 ? poh[1] : pi == 2 ? poh[2] : poh[3];
+            const int ow = pi == 0 ? pw[0] : pi == 1 ? pw[1] : pi == 2 ? pw[2] : pw[3];
+            bool ok = d_ok[k] && b < kb1;
+            uint32_t off;
+            const uint8_t* src;
+            if (!d_b[k]) {
+                off = (uint32_t)b * gy_pix + d_off[k];
+                src = p.gc;
+            } else {
+                const int ih = oh * cv.sh + d_kh[k] - cv.ph, iw = ow * cv.sw + d_kw[k] - cv.pw;
+                ok = ok && ih >= 0 && ih < cv.h && iw >= 0 && iw < cv.w;
+                off = (((uint32_t)gg * cv.h + ih) * cv.w + iw) * x_pix + d_off[k];
+                src = p.xc;
+            }
+            // a piece invalid in this stage reads the zero block at its offset
+            // inside the block (< 1 KB), never at its tensor offset
+            lds_dma16(ok ? src + off : g_zero_block + (lane & (PT - 1)) * 16, base + ins * 1024);
+        }
+        sreg = 0;
+        if (tid < SP * 6) {
+            const int pi = s_pi, b = bst + pi;
+            const int gg = pi == 0 ? pg[0] : pi == 1 ? pg[1] : pi == 2 ? pg[2] : pg[3];
+            const int oh = pi == 0 ? poh[0] : pi == 1 ? poh[1] : pi == 2 ? poh[2] : poh[3];
+            const int ow = pi == 0 ? pw[0] : pi == 1 ? pw[1] : pi == 2 ? pw[2] : pw[3];
+            if (tid < SP * 2) {
+                if (s_ok && b < kb1) sreg = p.gs[(size_t)b * cv.gy.ncb + s_idx];
+            } else {
+                const int ih = oh * cv.sh + s_kh - cv.ph, iw = ow * cv.sw + s_kw - cv.pw;
+                if (s_ok && b < kb1 && ih >= 0 && ih < cv.h && iw >= 0 && iw < cv.w)
+                    sreg = p.xs[(((size_t)gg * cv.h + ih) * cv.w + iw) * cinb + s_idx];
+            }
+        }
+    };
+    auto store_scales = [&](int buf) {
+        if (tid < SP * 6) smem[buf * STAGE + A_BYTES + B_BYTES + tid] = (uint8_t)sreg;
+    };
+
+    const int wm = wave & 1, wn = wave >> 1, h = lane >> 5, r = lane & 31;
+    v16f acc[2];
+    for (int c = 0; c < 2; c++)
+        for (int e = 0; e < 16; e++) acc[c][e] = 0.0f;
+
+    if (nstage > 0) {
+        issue(0, 0);
+        wait_dma();
+        store_scales(0);
+    }
+    __syncthreads();
+    for (int st = 0; st < nstage; st++) {
+        const int buf = st & 1;
+        if (st + 1 < nstage) issue(st + 1, buf ^ 1);
+        const uint8_t* A = smem + buf * STAGE;
+        const uint8_t* B = A + A_BYTES;
+        const uint8_t* SC = B + B_BYTES;
+#pragma unroll
+        for (int ks = 0; ks < SP / 2; ks++) {
+            v8i af;
+            if (FMT == MXC_E4M3) {
+                const v4i x0 = *(const v4i*)(A + ((2 * ks) * 2 + wm) * TT + r * ROWB + 16 * h);
+                const v4i x1 = *(const v4i*)(A + ((2 * ks + 1) * 2 + wm) * TT + r * ROWB + 16 * h);
+                af[0] = x0[0]; af[1] = x0[1]; af[2] = x0[2]; af[3] = x0[3];
+                af[4] = x1[0]; af[5] = x1[1]; af[6] = x1[2]; af[7] = x1[3];
+            } else {
+                const v4i x0 = *(const v4i*)(A + ((2 * ks + h) * 2 + wm) * TT + r * ROWB);
+                af[0] = x0[0]; af[1] = x0[1]; af[2] = x0[2]; af[3] = x0[3];
+                af[4] = af[5] = af[6] = af[7] = 0;
+            }
+            const int sa = SC[(2 * ks + h) * 2 + wm];
+#pragma unroll
+            for (int c = 0; c < 2; c++) {
+                const int cbk = 2 * wn + c;
+                v8i bf;
+                if (FMT == MXC_E4M3) {
+                    const v4i y0 = *(const v4i*)(B + ((2 * ks) * 4 + cbk) * TT + r * ROWB + 16 * h);
+                    const v4i y1 = *(const v4i*)(B + ((2 * ks + 1) * 4 + cbk) * TT + r * ROWB + 16 * h);
+                    bf[0] = y0[0]; bf[1] = y0[1]; bf[2] = y0[2]; bf[3] = y0[3];
+                    bf[4] = y1[0]; bf[5] = y1[1]; bf[6] = y1[2]; bf[7] = y1[3];
+                } else {
+                    const v4i y0 = *(const v4i*)(B + ((2 * ks + h) * 4 + cbk) * TT + r * ROWB);
+                    bf[0] = y0[0]; bf[1] = y0[1]; bf[2] = y0[2]; bf[3] = y0[3];
+                    bf[4] = bf[5] = bf[6] = bf[7] = 0;
+                }
+                const int sb = SC[SP * 2 + (2 * ks + h) * 4 + cbk];
+                acc[c] = mfma_mx<FMT>(af, bf, acc[c], sa, sb);
+            }
+        }
+        if (st + 1 < nstage) {
+            wait_dma();
+            store_scales(buf ^ 1);
+        }
+        __syncthreads();
+    }
+
+#pragma unroll
+    for (int c = 0; c < 2; c++) {
+        const int col = BN * ct + 64 * wn + 32 * c + (lane & 31);
+        if (col >= p.ntot) continue;
+#pragma unroll
+        for (int e = 0; e < 16; e++) {
+            const int m = BM * mt + 32 * wm + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+            if (m >= cv.gy.cp) continue;
+            p.part[((size_t)sp * cv.gy.cp + m) * p.ntot + col] = acc[c][e];
+        }
+    }
+}
+
+bool wstream_ok(const Conv& cv) { return cv.x.bn * cv.bits >= 128; }   // rows of >= 16 bytes
+
 }  // namespace
 
 int launch_fwd(const Conv& cv, const void* wc, const uint8_t* ws, const void* xc, const uint8_t* xs,
                float* y, int layout, hipStream_t s) {
+    if (stream_ok(cv)) return launch_conv_stream(cv, false, wc, ws, xc, xs, y, layout, s);
     return launch_conv(cv, false, wc, ws, xc, xs, y, layout, s);
 }
 
 int launch_dgrad(const Conv& cv, const void* wc, const uint8_t* ws, const void* gc, const uint8_t* gs,
                  float* gx, int layout, hipStream_t s) {
+    if (stream_ok(cv)) return launch_conv_stream(cv, true, wc, ws, gc, gs, gx, layout, s);
     return launch_conv(cv, true, wc, ws, gc, gs, gx, layout, s);
 }
 
@@ -674,7 +1293,18 @@ int launch_wgrad(const Conv& cv, const void* gc, const uint8_t* gs, const void* 
     const long ntile = (long)pl.mtiles * pl.ctiles * pl.splits;
     if (ntile > 0x7FFFFFF0L) return MXC_ERR_SHAPE;
     const dim3 grid((unsigned)((ntile + 7) / 8 * 8));
-    int rc = cv.fmt == MXC_E4M3 ? launch_wgrad_f<MXC_E4M3>(a, grid, s) : launch_wgrad_f<MXC_E2M1>(a, grid, s);
+    int rc;
+    if (wstream_ok(cv)) {
+        WStreamArgs w;
+        w.cv = cv;
+        w.gc = a.gc; w.gs = gs; w.xc = a.xc; w.xs = xs; w.part = a.part;
+        w.ntot = pl.ntot; w.mtiles = pl.mtiles; w.ctiles = pl.ctiles; w.splits = pl.splits; w.kbps = pl.kbps;
+        if (cv.fmt == MXC_E4M3) hipLaunchKernelGGL((wgrad_stream_kernel<MXC_E4M3>), grid, dim3(NT), 0, s, w);
+        else                    hipLaunchKernelGGL((wgrad_stream_kernel<MXC_E2M1>), grid, dim3(NT), 0, s, w);
+        rc = hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
+    } else {
+        rc = cv.fmt == MXC_E4M3 ? launch_wgrad_f<MXC_E4M3>(a, grid, s) : launch_wgrad_f<MXC_E2M1>(a, grid, s);
+    }
     if (rc) return rc;
     const long total = (long)cv.cout * cv.kh * cv.kw * cv.cin;
     hipLaunchKernelGGL(wgrad_reduce, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, (const float*)ws, gw,

@@ -11,8 +11,8 @@
 //      XOR-swizzled per unit to spread banks);
 //   2. each thread takes one unit: max |x| over its 32 elements, then over the
 //      Bn lanes that share the block (xor shuffles);
-//   3. scale code from the exponent bits, elements encoded with integer
-//      round-to-nearest-even, codes stored as 16-byte vectors.
+//   3. scale code from the exponent bits; elements scaled by 2^-s (exact) and
+//      encoded with the hardware converts, codes stored as 16-byte vectors.
 // Traffic: 4 (or 2) bytes read and 1 (or 1/2) byte written per element, plus
 // one scale byte per block; HBM-bound.
 #include "mx_internal.h"
@@ -97,6 +97,12 @@ __global__ __launch_bounds__(QT) void quantize_kernel(const void* __restrict__ s
         }
 #pragma unroll
         for (int r = 0; r < NL; r++) {
+            if (LAYOUT == MXC_CBF && VEC == 4) {
+                // four consecutive samples: one 16-byte chunk of the slab
+                const int u = ci0[r] >> 5, k = ci0[r] & 31;
+                *(float4*)&slab[u * 32 + (((k >> 2) ^ swz(u)) << 2)] = v[r];
+                continue;
+            }
             const float x4[4] = {v[r].x, v[r].y, v[r].z, v[r].w};
 #pragma unroll
             for (int q = 0; q < VEC; q++) {
@@ -141,25 +147,14 @@ __global__ __launch_bounds__(QT) void quantize_kernel(const void* __restrict__ s
         if (FMT == MXC_E4M3) {
             uint32_t w[8];
 #pragma unroll
-            for (int q = 0; q < 8; q++) {
-                uint32_t c0 = enc_e4m3(x[q].x * inv), c1 = enc_e4m3(x[q].y * inv);
-                uint32_t c2 = enc_e4m3(x[q].z * inv), c3 = enc_e4m3(x[q].w * inv);
-                w[q] = bad ? 0u : (c0 | (c1 << 8) | (c2 << 16) | (c3 << 24));
-            }
+            for (int q = 0; q < 8; q++) w[q] = bad ? 0u : pack4_e4m3(x[q], inv);
             uint4* dst = (uint4*)(codes + e0);
             dst[0] = make_uint4(w[0], w[1], w[2], w[3]);
             dst[1] = make_uint4(w[4], w[5], w[6], w[7]);
         } else {
             uint32_t w[4];
 #pragma unroll
-            for (int q = 0; q < 4; q++) {
-                const float4 a = x[2 * q], b = x[2 * q + 1];
-                uint32_t t = enc_e2m1(a.x * inv) | (enc_e2m1(a.y * inv) << 4) |
-                             (enc_e2m1(a.z * inv) << 8) | (enc_e2m1(a.w * inv) << 12) |
-                             (enc_e2m1(b.x * inv) << 16) | (enc_e2m1(b.y * inv) << 20) |
-                             (enc_e2m1(b.z * inv) << 24) | (enc_e2m1(b.w * inv) << 28);
-                w[q] = bad ? 0u : t;
-            }
+            for (int q = 0; q < 4; q++) w[q] = bad ? 0u : pack8_e2m1(x[2 * q], x[2 * q + 1], inv);
             *(uint4*)(codes + e0 / 2) = make_uint4(w[0], w[1], w[2], w[3]);
         }
     }

@@ -183,6 +183,10 @@ GEMM_CONVS = [
     synth.conv_dict(4, 40, 70, 10, 11, 5, 2, 2),
     synth.conv_dict(1, 64, 32, 7, 7, 3, 1, 1),                # one sample (E4M3 only)
     synth.conv_dict(32, 128, 64, 8, 8, 1, 2, 0),              # 1x1 stride 2: a phase with no taps
+    synth.conv_dict(32, 32, 40, 13, 11, 5, 2, 2),             # 5x5 stride 2, odd sizes
+    dict(n=32, cin=48, cout=96, h=10, w=9, kh=7, kw=3, sh=2, sw=1, ph=3, pw=1),
+    synth.conv_dict(8, 64, 32, 6, 19, 3, 1, 1),               # Bn = 8: a tile spans 16 pixels
+    synth.conv_dict(32, 16, 24, 9, 11, 7, 1, 3),              # 7x7: stages too big for the stream path
 ]
 
 
