@@ -70,6 +70,9 @@ def load():
         "o_dgrad_at": (i32, [P, i32, P, P, P, P, P, i64, P, P]),
         "o_wgrad_at": (i32, [P, i32, P, P, P, P, P, i64, P, P]),
         "o_quantize_1d": (i32, [P, i64, i64, i32, i32, P, P]),
+        "o_dequant_1d": (i32, [P, P, i64, i64, i32, i32, P]),
+        "o_naive_im2col": (i32, [P, P, P]),
+        "o_naive_col2im": (i32, [P, P, P]),
         "o_counter_get": (i64, []),
         "o_counter_reset": (None, []),
         "o_set_threads": (None, [i32]),
@@ -263,6 +266,66 @@ def quantize_1d(m, direction, fmt):
     _check(lib.o_quantize_1d(_ptr(m), rows, cols, direction, fmt, _ptr(codes), _ptr(scales)),
            "quantize_1d")
     return codes, scales
+
+
+def dequant_1d(codes, scales, rows, cols, direction, fmt):
+    """Fake quantization of a quantize_1d result: fp64 [rows][cols]."""
+    out = np.zeros((rows, cols), dtype=np.float64)
+    _check(load().o_dequant_1d(_ptr(np.ascontiguousarray(codes)), _ptr(np.ascontiguousarray(scales)),
+                               rows, cols, direction, fmt, _ptr(out)), "dequant_1d")
+    return out
+
+
+def naive_im2col(conv, x_nhwc):
+    """fp32 im2col of an NHWC tensor: [P][K], P = (n, ho, wo), K = (kh, kw, ci)."""
+    p = _conv_params(conv)
+    ho, wo = conv_out(conv)
+    x = np.ascontiguousarray(x_nhwc, dtype=np.float32)
+    col = np.zeros((conv["n"] * ho * wo, conv["kh"] * conv["kw"] * conv["cin"]), dtype=np.float32)
+    _check(load().o_naive_im2col(_ptr(p), _ptr(x), _ptr(col)), "naive_im2col")
+    return col
+
+
+def naive_col2im(conv, gcol):
+    """Scatter-add of a [P][K] fp64 matrix back to an NHWC tensor."""
+    p = _conv_params(conv)
+    g = np.ascontiguousarray(gcol, dtype=np.float64)
+    gx = np.zeros((conv["n"], conv["h"], conv["w"], conv["cin"]), dtype=np.float64)
+    _check(load().o_naive_col2im(_ptr(p), _ptr(g), _ptr(gx)), "naive_col2im")
+    return gx
+
+
+def _fake_1d(m, direction, fmt):
+    m = np.ascontiguousarray(m, dtype=np.float32)
+    codes, scales = quantize_1d(m, direction, fmt)
+    return dequant_1d(codes, scales, m.shape[0], m.shape[1], direction, fmt)
+
+
+# The naive comparator's three GEMMs (Sec. III-C / Table I baseline), in the
+# channels-last GEMM form: X, G_Y and G_X are NHWC, W and G_W are OHWI
+# ([Cout][K]).  Each operand is quantized with 1-D blocks along its GEMM's
+# contraction dimension, so every tensor is quantized twice per step.  Each
+# returns (result, sum of absolute products) in fp64.
+def naive_fwd(conv, fmt, x_nhwc, w_ohwi):
+    """Y [P][Cout] = X'[P][K] W[Cout][K]^T, X' and W blocked along K."""
+    a = _fake_1d(naive_im2col(conv, x_nhwc), 0, fmt)
+    b = _fake_1d(np.asarray(w_ohwi, dtype=np.float32).reshape(conv["cout"], -1), 0, fmt)
+    return a @ b.T, np.abs(a) @ np.abs(b).T
+
+
+def naive_dgrad(conv, fmt, gy_nhwc, w_ohwi):
+    """G_X' [P][K] = G_Y[P][Cout] W[Cout][K], both blocked along Cout; then col2im."""
+    cout = conv["cout"]
+    a = _fake_1d(np.asarray(gy_nhwc, dtype=np.float32).reshape(-1, cout), 0, fmt)
+    b = _fake_1d(np.asarray(w_ohwi, dtype=np.float32).reshape(cout, -1), 1, fmt)
+    return naive_col2im(conv, a @ b), naive_col2im(conv, np.abs(a) @ np.abs(b))
+
+
+def naive_wgrad(conv, fmt, gy_nhwc, x_nhwc):
+    """G_W [Cout][K] = G_Y[P][Cout]^T X'[P][K], both blocked along P."""
+    a = _fake_1d(np.asarray(gy_nhwc, dtype=np.float32).reshape(-1, conv["cout"]), 1, fmt)
+    b = _fake_1d(naive_im2col(conv, x_nhwc), 1, fmt)
+    return a.T @ b, np.abs(a).T @ np.abs(b)
 
 
 def counter_get():

@@ -30,6 +30,9 @@
  *                         at sizes where the full GEMMs are too slow.
  *   o_quantize_1d         the naive comparator's quantizer: 1-D blocks of 32
  *                         along one matrix direction (Sec. III-C, Dacapo).
+ *   o_dequant_1d          its fake quantization.
+ *   o_naive_im2col /      the naive comparator's fp32 im2col (channels-last
+ *   o_naive_col2im          GEMM form) and the col2im scatter-add back.
  *
  * Readings of the paper that this file fixes (the paper uses NVFP with 8x8
  * blocks; the build uses OCP MX):
@@ -806,5 +809,84 @@ int o_quantize_1d(const float *m, int64_t rows, int64_t cols, int dir, int fmt,
         }
     }
     o_quantized_count += rows * cols;
+    return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* naive comparator (Sec. III-C; the baseline column of Table I): the  */
+/* full-precision im2col comes first and every GEMM operand is then    */
+/* quantized with 1-D blocks of 32 along its contraction dimension     */
+/* ------------------------------------------------------------------ */
+
+/* Fake quantization of a matrix quantized by o_quantize_1d (same layouts:
+ * codes in the matrix's own row-major order, scales [rows][ceil(cols/32)]
+ * for dir 0 and [ceil(rows/32)][cols] for dir 1). */
+int o_dequant_1d(const uint8_t *codes, const uint8_t *scales, int64_t rows, int64_t cols,
+                 int dir, int fmt, double *out)
+{
+    o_fmt f;
+    if (fmt_get(fmt, &f)) return -2;
+    if (rows <= 0 || cols <= 0 || (dir != 0 && dir != 1)) return -2;
+    int64_t nbc = (cols + 31) / 32;
+    for (int64_t r = 0; r < rows; r++)
+        for (int64_t c = 0; c < cols; c++) {
+            int64_t bi = dir == 0 ? r * nbc + c / 32 : (r / 32) * cols + c;
+            int64_t pos = r * cols + c;
+            out[pos] = o_decode(get_code(codes, f.bits, pos), fmt) * o_scale_value(scales[bi]);
+        }
+    return 0;
+}
+
+/* fp32 im2col in channels-last GEMM form: col[p][k] with p = (n, ho, wo)
+ * and k = (kh, kw, ci), x in NHWC.  col[p][k] = x[n][ho*sh+kh-ph][wo*sw+kw-pw][ci],
+ * zero where the tap falls into the padding. */
+int o_naive_im2col(const int *p, const float *x, float *col)
+{
+    o_conv cv;
+    int rc = conv_init(&cv, p);
+    if (rc) return rc;
+    int64_t K = (int64_t)cv.kh * cv.kw * cv.cin;
+    for (int nn = 0; nn < cv.n; nn++)
+        for (int oh = 0; oh < cv.ho; oh++)
+            for (int ow = 0; ow < cv.wo; ow++) {
+                int64_t row = ((int64_t)nn * cv.ho + oh) * cv.wo + ow;
+                for (int a = 0; a < cv.kh; a++)
+                    for (int b = 0; b < cv.kw; b++)
+                        for (int ci = 0; ci < cv.cin; ci++) {
+                            int ih = oh * cv.sh + a - cv.ph, iw = ow * cv.sw + b - cv.pw;
+                            int inside = ih >= 0 && ih < cv.h && iw >= 0 && iw < cv.w;
+                            int64_t k = ((int64_t)a * cv.kw + b) * cv.cin + ci;
+                            col[row * K + k] = inside ? x[(((int64_t)nn * cv.h + ih) * cv.w + iw) * cv.cin + ci]
+                                                      : 0.0f;
+                        }
+            }
+    return 0;
+}
+
+/* col2im: G_X[n][h][w][ci] (NHWC) = sum of gcol[p][k] over every (p, k) that
+ * o_naive_im2col reads from (n, h, w, ci) -- the scatter-add that turns
+ * G_X' back into G_X (Sec. IV-B). */
+int o_naive_col2im(const int *p, const double *gcol, double *gx)
+{
+    o_conv cv;
+    int rc = conv_init(&cv, p);
+    if (rc) return rc;
+    int64_t K = (int64_t)cv.kh * cv.kw * cv.cin;
+    int64_t nx = (int64_t)cv.n * cv.h * cv.w * cv.cin;
+    for (int64_t i = 0; i < nx; i++) gx[i] = 0.0;
+    for (int nn = 0; nn < cv.n; nn++)
+        for (int oh = 0; oh < cv.ho; oh++)
+            for (int ow = 0; ow < cv.wo; ow++) {
+                int64_t row = ((int64_t)nn * cv.ho + oh) * cv.wo + ow;
+                for (int a = 0; a < cv.kh; a++)
+                    for (int b = 0; b < cv.kw; b++) {
+                        int ih = oh * cv.sh + a - cv.ph, iw = ow * cv.sw + b - cv.pw;
+                        if (ih < 0 || ih >= cv.h || iw < 0 || iw >= cv.w) continue;
+                        for (int ci = 0; ci < cv.cin; ci++) {
+                            int64_t k = ((int64_t)a * cv.kw + b) * cv.cin + ci;
+                            gx[(((int64_t)nn * cv.h + ih) * cv.w + iw) * cv.cin + ci] += gcol[row * K + k];
+                        }
+                    }
+            }
     return 0;
 }

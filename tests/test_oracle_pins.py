@@ -476,3 +476,153 @@ def test_quantize_1d_blocks_follow_direction():
         ref = torch.clamp(torch.from_numpy(m.astype(np.float64) / 2.0 ** s), -448, 448)
         ref = ref.to(torch.float8_e4m3fn).view(torch.uint8).numpy()
         assert np.array_equal(codes.reshape(70, 45), ref)
+
+
+# ---------------------------------------------------------------- naive comparator
+def _nhwc(t):
+    return np.ascontiguousarray(t.permute(0, 2, 3, 1).numpy())
+
+
+def _ohwi(w):
+    return np.ascontiguousarray(w.permute(0, 2, 3, 1).reshape(w.shape[0], -1).numpy())
+
+
+def _int_tensor(shape, seed, lo=-4, hi=4):
+    """Small integers: exact under every 1-D block scale of E4M3 and E2M1."""
+    g = torch.Generator().manual_seed(seed)
+    return torch.randint(lo, hi + 1, shape, generator=g).to(torch.float64)
+
+
+@pytest.mark.parametrize("cv", CONVS, ids=lambda c: f"n{c['n']}c{c['cin']}k{c['kh']}{c['kw']}s{c['sh']}")
+def test_naive_im2col_matches_unfold(cv):
+    """The comparator's fp32 im2col is F.unfold with K reordered to (kh, kw, ci)."""
+    n, cin, kh, kw = cv["n"], cv["cin"], cv["kh"], cv["kw"]
+    x = torch.from_numpy(_rand_tensor((n, cin, cv["h"], cv["w"]), 41))
+    ho, wo = synth.out_hw(cv)
+    col = oracle.naive_im2col(cv, _nhwc(x))
+    u = F.unfold(x, (kh, kw), padding=(cv["ph"], cv["pw"]), stride=(cv["sh"], cv["sw"]))
+    ref = u.reshape(n, cin, kh, kw, ho * wo).permute(0, 4, 2, 3, 1).reshape(n * ho * wo, kh * kw * cin)
+    assert np.array_equal(col, ref.numpy())
+
+
+@pytest.mark.parametrize("cv", CONVS, ids=lambda c: f"n{c['n']}c{c['cin']}k{c['kh']}{c['kw']}s{c['sh']}")
+def test_naive_col2im_matches_fold(cv):
+    """col2im is F.fold (the adjoint of unfold) with the same K order."""
+    n, cin, kh, kw = cv["n"], cv["cin"], cv["kh"], cv["kw"]
+    ho, wo = synth.out_hw(cv)
+    g = np.random.default_rng(5).standard_normal((n * ho * wo, kh * kw * cin))
+    gx = oracle.naive_col2im(cv, g)
+    u = torch.from_numpy(g).reshape(n, ho * wo, kh, kw, cin).permute(0, 4, 2, 3, 1).reshape(n, cin * kh * kw, -1)
+    ref = F.fold(u, (cv["h"], cv["w"]), (kh, kw), padding=(cv["ph"], cv["pw"]), stride=(cv["sh"], cv["sw"]))
+    assert np.allclose(gx, ref.permute(0, 2, 3, 1).numpy(), rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("fmt", [oracle.E4M3, oracle.E2M1])
+def test_dequant_1d_inverts_quantize_1d(fmt):
+    """Values on the grid come back unchanged through quantize_1d/dequant_1d
+    in both directions (each block carries its own power-of-two factor, so a
+    scale read from the wrong block shows), and quantize_1d is idempotent."""
+    rows, cols = 70, 45
+    r, c = np.meshgrid(np.arange(rows), np.arange(cols), indexing="ij")
+    base = _int_tensor((rows, cols), 8).numpy()
+    for d in (0, 1):
+        blk = (r + c // 32) if d == 0 else (r // 32 + c)
+        m = (base * np.exp2(blk % 7 - 3)).astype(np.float32)
+        codes, scales = oracle.quantize_1d(m, d, fmt)
+        assert np.array_equal(oracle.dequant_1d(codes, scales, rows, cols, d, fmt), m)
+        x = _rand_tensor((rows, cols), 9 + d)
+        codes, scales = oracle.quantize_1d(x, d, fmt)
+        dq = oracle.dequant_1d(codes, scales, rows, cols, d, fmt).astype(np.float32)
+        c2, s2 = oracle.quantize_1d(dq, d, fmt)
+        assert np.array_equal(codes, c2) and np.array_equal(scales, s2)
+
+
+def _torch_layer(cv, x, w, gy):
+    st, pd = (cv["sh"], cv["sw"]), (cv["ph"], cv["pw"])
+    y = F.conv2d(x, w, stride=st, padding=pd)
+    gx = torch.nn.grad.conv2d_input(x.shape, w, gy, stride=st, padding=pd)
+    gw = torch.nn.grad.conv2d_weight(x, w.shape, gy, stride=st, padding=pd)
+    return y, gx, gw
+
+
+@pytest.mark.parametrize("fmt", [oracle.E4M3, oracle.E2M1])
+@pytest.mark.parametrize("cv", CONVS[:4], ids=lambda c: f"n{c['n']}c{c['cin']}k{c['kh']}{c['kw']}s{c['sh']}")
+def test_naive_gemms_on_lossless_inputs_match_torch(fmt, cv):
+    """On small-integer inputs every 1-D quantization is the identity, so the
+    comparator's fwd / dgrad / wgrad equal torch's fp64 convolutions."""
+    ho, wo = synth.out_hw(cv)
+    x = _int_tensor((cv["n"], cv["cin"], cv["h"], cv["w"]), 21)
+    w = _int_tensor((cv["cout"], cv["cin"], cv["kh"], cv["kw"]), 22)
+    gy = _int_tensor((cv["n"], cv["cout"], ho, wo), 23)
+    y_ref, gx_ref, gw_ref = _torch_layer(cv, x, w, gy)
+    y, _ = oracle.naive_fwd(cv, fmt, _nhwc(x), _ohwi(w))
+    assert np.array_equal(y, _nhwc(y_ref).reshape(-1, cv["cout"]))
+    gx, _ = oracle.naive_dgrad(cv, fmt, _nhwc(gy), _ohwi(w))
+    assert np.array_equal(gx, _nhwc(gx_ref))
+    gw, _ = oracle.naive_wgrad(cv, fmt, _nhwc(gy), _nhwc(x))
+    assert np.array_equal(gw, _ohwi(gw_ref))
+
+
+@pytest.mark.parametrize("fmt", [oracle.E4M3, oracle.E2M1])
+def test_naive_gemms_block_along_their_contraction(fmt):
+    """One huge element flushes the small ones of its own 1-D block to zero;
+    which ones that are shows the direction each GEMM blocks its operand in:
+    W along K for fwd and along Cout for dgrad, G_Y along P for wgrad."""
+    cv = synth.conv_dict(2, 64, 64, 6, 6, 3, 1, 1)
+    ho, wo = synth.out_hw(cv)
+    x = _int_tensor((2, 64, 6, 6), 31, 1, 4)
+    w = _int_tensor((64, 64, 3, 3), 32, 1, 4)
+    gy = _int_tensor((2, 64, ho, wo), 33, 1, 4)
+    co0, ci0, a0, b0 = 37, 45, 1, 2
+    big = 2.0 ** 20
+    wb = w.clone()
+    wb[co0, ci0, a0, b0] = big
+    k0 = (a0 * 3 + b0) * 64 + ci0
+    # fwd: W blocked along K -> same row co0, K block of k0
+    wf = wb.permute(0, 2, 3, 1).reshape(64, -1).clone()
+    kb = k0 // 32 * 32
+    keep = wf[co0, k0].item()
+    wf[co0, kb:kb + 32] = 0.0
+    wf[co0, k0] = keep
+    w_fwd = wf.reshape(64, 3, 3, 64).permute(0, 3, 1, 2)
+    y, _ = oracle.naive_fwd(cv, fmt, _nhwc(x), _ohwi(wb))
+    y_ref = F.conv2d(x, w_fwd, padding=1)
+    assert np.array_equal(y, _nhwc(y_ref).reshape(-1, 64))
+    # dgrad: W blocked along Cout -> same column k0, Cout block of co0
+    wd = wb.permute(0, 2, 3, 1).reshape(64, -1).clone()
+    cb = co0 // 32 * 32
+    wd[cb:cb + 32, k0] = 0.0
+    wd[co0, k0] = big
+    w_dg = wd.reshape(64, 3, 3, 64).permute(0, 3, 1, 2)
+    gx, _ = oracle.naive_dgrad(cv, fmt, _nhwc(gy), _ohwi(wb))
+    gx_ref = torch.nn.grad.conv2d_input(x.shape, w_dg, gy, padding=1)
+    assert np.array_equal(gx, _nhwc(gx_ref))
+    # wgrad: G_Y blocked along P = (n, ho, wo) -> same channel, P block of p0
+    n0, oh0, ow0, cg = 1, 2, 3, 17
+    gyb = gy.clone()
+    gyb[n0, cg, oh0, ow0] = big
+    gf = gyb.permute(0, 2, 3, 1).reshape(-1, 64).clone()
+    p0 = (n0 * ho + oh0) * wo + ow0
+    pb = p0 // 32 * 32
+    gf[pb:pb + 32, cg] = 0.0
+    gf[p0, cg] = big
+    gy_wg = gf.reshape(2, ho, wo, 64).permute(0, 3, 1, 2)
+    gw, _ = oracle.naive_wgrad(cv, fmt, _nhwc(gyb), _nhwc(x))
+    gw_ref = torch.nn.grad.conv2d_weight(x, w.shape, gy_wg, padding=1)
+    assert np.array_equal(gw, _ohwi(gw_ref))
+
+
+def test_naive_step_quantizes_each_tensor_twice():
+    """A comparator step (fwd, dgrad, wgrad) quantizes 2|X'| + 2|W| + 2|G_Y|
+    elements; at 3x3 s1 p1 that is Table I's baseline count."""
+    t1 = _table1()
+    cv = synth.conv_dict(32, 32, 32, 8, 8, 3, 1, 1)
+    x, w, gy = synth.layer_inputs(cv, 1, kind="unit")
+    xn, wn, gn = _nhwc(x), _ohwi(w), _nhwc(gy)
+    oracle.counter_reset()
+    oracle.naive_fwd(cv, oracle.E4M3, xn, wn)
+    oracle.naive_dgrad(cv, oracle.E4M3, gn, wn)
+    oracle.naive_wgrad(cv, oracle.E4M3, gn, xn)
+    total = oracle.counter_get()
+    dac = t1["Dacapo"]
+    assert total == dac[0] * x.numel() + dac[1] * w.numel() + dac[2] * gy.numel()
