@@ -783,6 +783,10 @@ int o_quantize_1d(const float *m, int64_t rows, int64_t cols, int dir, int fmt,
     if (rows <= 0 || cols <= 0 || (dir != 0 && dir != 1)) return -2;
     int64_t nbr = dir == 0 ? rows : (rows + 31) / 32;
     int64_t nbc = dir == 0 ? (cols + 31) / 32 : cols;
+    /* codes are produced one per element and packed afterwards: two FP4
+     * codes of different blocks can share a byte */
+    uint8_t *one = (uint8_t *)malloc((size_t)(rows * cols));
+    if (!one) return -1;
     fesetround(FE_TONEAREST);
     #pragma omp parallel for schedule(static)
     for (int64_t bi = 0; bi < nbr * nbc; bi++) {
@@ -805,9 +809,11 @@ int o_quantize_1d(const float *m, int64_t rows, int64_t cols, int dir, int fmt,
         scales[bi] = (uint8_t)scode;
         for (int t = 0; t < cnt; t++) {
             int code = nonfinite ? 0 : o_encode(ldexp((double)m[pos[t]], -(scode - 127)), fmt);
-            put_code(codes, f.bits, pos[t], code);
+            one[pos[t]] = (uint8_t)code;
         }
     }
+    for (int64_t i = 0; i < rows * cols; i++) put_code(codes, f.bits, i, one[i]);
+    free(one);
     o_quantized_count += rows * cols;
     return 0;
 }
