@@ -191,6 +191,81 @@ int mxconv_wgrad(const mxc_conv* cv, int fmt,
                  const void* x_codes, const uint8_t* x_scales,
                  float* gw, void* workspace, size_t ws_bytes, void* stream);
 
+/* ------------------------------------------------------------------ a6 */
+/* Naive comparator (the baseline of Sec. III-C and Table I): the im2col is
+ * done in full precision first, and every GEMM operand is then quantized
+ * with 1-D blocks of 32 elements along that GEMM's contraction dimension --
+ * so X', W and G_Y are each quantized twice per step, once per GEMM they
+ * enter.  Same element formats and scale rule as above; only the block shape
+ * and the data flow differ.  It exists to be measured against, not used.
+ *
+ * Matrices are in channels-last GEMM form: P = n*Ho*Wo output positions
+ * ordered (n, ho, wo); K = kh*kw*cin ordered (kh, kw, ci).  X, G_Y and G_X
+ * are NHWC fp32 (G_Y is then [P][cout]); W and G_W are OHWI fp32, i.e.
+ * [cout][K].
+ *
+ * Line matrix: the output of mxconv_naive_quantize_1d.  A matrix blocked
+ * along one dimension of length L is stored with that dimension contiguous:
+ *   codes  [lines][Lp]     (FP4: two per byte, even element in the low nibble)
+ *   scales [lines][Lp/32]
+ * Lp = L rounded up to a multiple of 64 (padding codes and scales are 0). */
+
+/* Bytes of a line matrix of `lines` lines of length `len`; 0 if invalid. */
+size_t mxconv_naive_codes_bytes(int64_t lines, int64_t len, int fmt);
+size_t mxconv_naive_scales_bytes(int64_t lines, int64_t len);
+
+/* fp32 im2col: col[p][k] = x[n][ho*sh+kh-ph][wo*sw+kw-pw][ci], 0 in the
+ * padding (Eq. (1) unrolled into the GEMM of Sec. II-C).
+ *   x    device fp32, NHWC (n, h, w, cin).
+ *   col  device fp32, [P][K], written.
+ * Errors: NULL, ARG, SHAPE, ALIGN, HIP. */
+int mxconv_naive_im2col_f32(const mxc_conv* cv, const float* x, float* col, void* stream);
+
+/* 1-D quantization of a row-major fp32 matrix src[rows][cols].
+ *   dir 0: blocks of 32 along each row    -> lines = rows, L = cols;
+ *   dir 1: blocks of 32 down each column  -> lines = cols, L = rows (the
+ *          output is the transposed line matrix).
+ *   codes   device, mxconv_naive_codes_bytes(lines, L, fmt) bytes, written.
+ *   scales  device, mxconv_naive_scales_bytes(lines, L) bytes, written.
+ * Errors: NULL, ARG, ALIGN, HIP. */
+int mxconv_naive_quantize_1d(const float* src, int64_t rows, int64_t cols, int dir, int fmt,
+                             void* codes, uint8_t* scales, void* stream);
+
+/* Forward GEMM Y[P][cout] = X'[P][K] W[cout][K]^T (Sec. II-C), both operands
+ * blocked along K:
+ *   col_codes / col_scales  X' quantized with dir 0 (lines P, length K);
+ *   w_codes / w_scales      W (OHWI as [cout][K]) quantized with dir 0;
+ *   y                       device fp32 [P][cout] (= NHWC), written.
+ * Errors: NULL, ARG, SHAPE, ALIGN, HIP. */
+int mxconv_naive_fwd(const mxc_conv* cv, int fmt,
+                     const void* col_codes, const uint8_t* col_scales,
+                     const void* w_codes, const uint8_t* w_scales,
+                     float* y, void* stream);
+
+/* Input gradient: G_X'[P][K] = G_Y[P][cout] W[cout][K] (Sec. II-C), both
+ * blocked along cout, then col2im (sum over the taps that read each input
+ * element):
+ *   gy_codes / gy_scales  G_Y ([P][cout]) quantized with dir 0;
+ *   wt_codes / wt_scales  W ([cout][K]) quantized with dir 1 (lines K);
+ *   gcol                  device fp32 [P][K] scratch for G_X';
+ *   gx                    device fp32 NHWC (n, h, w, cin), written.
+ * Errors: NULL, ARG, SHAPE, ALIGN, HIP. */
+int mxconv_naive_dgrad(const mxc_conv* cv, int fmt,
+                       const void* gy_codes, const uint8_t* gy_scales,
+                       const void* wt_codes, const uint8_t* wt_scales,
+                       float* gcol, float* gx, void* stream);
+
+/* Weight gradient: G_W[cout][K] = G_Y[P][cout]^T X'[P][K] (Sec. II-C), both
+ * blocked along P:
+ *   gyt_codes / gyt_scales  G_Y ([P][cout]) quantized with dir 1 (lines cout);
+ *   xt_codes / xt_scales    X' ([P][K]) quantized with dir 1 (lines K);
+ *   gw                      device fp32 [cout][K] (= OHWI), written.
+ * Errors: NULL, ARG, SHAPE, ALIGN, HIP. */
+int mxconv_naive_wgrad(const mxc_conv* cv, int fmt,
+                       const void* gyt_codes, const uint8_t* gyt_scales,
+                       const void* xt_codes, const uint8_t* xt_scales,
+                       float* gw, void* stream);
+
 /* Human-readable text for a return code (static storage). */
 const char* mxconv_strerror(int code);
 

@@ -51,6 +51,19 @@ size_t wgrad_workspace(const Conv& cv);
 int launch_wgrad(const Conv& cv, const void* gc, const uint8_t* gs, const void* xc,
                  const uint8_t* xs, float* gw, void* ws, hipStream_t s);
 
+// naive comparator (naive.hip): a line matrix stores each 1-D-blocked line
+// zero-padded to a multiple of 64 elements (one K step of the MFMA)
+static inline long long naive_line_len(long long len) { return (len + 63) / 64 * 64; }
+int launch_naive_im2col(const Conv& cv, const float* x, float* col, hipStream_t s);
+int launch_naive_q1d(const float* src, long long rows, long long cols, int dir, int fmt, void* codes,
+                     uint8_t* scales, hipStream_t s);
+int launch_naive_fwd(const Conv& cv, const void* cc, const uint8_t* cs, const void* wc,
+                     const uint8_t* ws, float* y, hipStream_t s);
+int launch_naive_dgrad(const Conv& cv, const void* gc, const uint8_t* gs, const void* wtc,
+                       const uint8_t* wts, float* gcol, float* gx, hipStream_t s);
+int launch_naive_wgrad(const Conv& cv, const void* gtc, const uint8_t* gts, const void* xtc,
+                       const uint8_t* xts, float* gw, hipStream_t s);
+
 }  // namespace mxc
 
 // ---------------------------------------------------------------- device side

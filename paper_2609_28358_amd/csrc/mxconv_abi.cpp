@@ -158,6 +158,69 @@ int mxconv_wgrad(const mxc_conv* p, int fmt, const void* gc, const uint8_t* gs, 
     return launch_wgrad(cv, gc, gs, xc, xs, gw, workspace, (hipStream_t)stream);
 }
 
+size_t mxconv_naive_codes_bytes(int64_t lines, int64_t len, int fmt) {
+    if (lines <= 0 || len <= 0 || (fmt != MXC_E4M3 && fmt != MXC_E2M1)) return 0;
+    const long long lp = naive_line_len(len);
+    return (size_t)lines * lp * (fmt == MXC_E4M3 ? 8 : 4) / 8;
+}
+
+size_t mxconv_naive_scales_bytes(int64_t lines, int64_t len) {
+    if (lines <= 0 || len <= 0) return 0;
+    return (size_t)lines * (naive_line_len(len) / 32);
+}
+
+int mxconv_naive_im2col_f32(const mxc_conv* p, const float* x, float* col, void* stream) {
+    if (!p || !x || !col) return MXC_ERR_NULL;
+    Conv cv;
+    int rc = conv_init(&cv, p, MXC_E4M3);
+    if (rc) return rc;
+    if (!aligned16(x) || !aligned16(col)) return MXC_ERR_ALIGN;
+    return launch_naive_im2col(cv, x, col, (hipStream_t)stream);
+}
+
+int mxconv_naive_quantize_1d(const float* src, int64_t rows, int64_t cols, int dir, int fmt,
+                             void* codes, uint8_t* scales, void* stream) {
+    if (!src || !codes || !scales) return MXC_ERR_NULL;
+    if (rows <= 0 || cols <= 0 || (dir != 0 && dir != 1) || (fmt != MXC_E4M3 && fmt != MXC_E2M1))
+        return MXC_ERR_ARG;
+    if (!aligned16(src) || !aligned16(codes) || !aligned16(scales)) return MXC_ERR_ALIGN;
+    return launch_naive_q1d(src, rows, cols, dir, fmt, codes, scales, (hipStream_t)stream);
+}
+
+int mxconv_naive_fwd(const mxc_conv* p, int fmt, const void* cc, const uint8_t* cs, const void* wc,
+                     const uint8_t* ws, float* y, void* stream) {
+    if (!p || !cc || !cs || !wc || !ws || !y) return MXC_ERR_NULL;
+    Conv cv;
+    int rc = conv_init(&cv, p, fmt);
+    if (rc) return rc;
+    if (!aligned16(cc) || !aligned16(cs) || !aligned16(wc) || !aligned16(ws) || !aligned16(y))
+        return MXC_ERR_ALIGN;
+    return launch_naive_fwd(cv, cc, cs, wc, ws, y, (hipStream_t)stream);
+}
+
+int mxconv_naive_dgrad(const mxc_conv* p, int fmt, const void* gc, const uint8_t* gs,
+                       const void* wtc, const uint8_t* wts, float* gcol, float* gx, void* stream) {
+    if (!p || !gc || !gs || !wtc || !wts || !gcol || !gx) return MXC_ERR_NULL;
+    Conv cv;
+    int rc = conv_init(&cv, p, fmt);
+    if (rc) return rc;
+    if (!aligned16(gc) || !aligned16(gs) || !aligned16(wtc) || !aligned16(wts) || !aligned16(gcol) ||
+        !aligned16(gx))
+        return MXC_ERR_ALIGN;
+    return launch_naive_dgrad(cv, gc, gs, wtc, wts, gcol, gx, (hipStream_t)stream);
+}
+
+int mxconv_naive_wgrad(const mxc_conv* p, int fmt, const void* gtc, const uint8_t* gts,
+                       const void* xtc, const uint8_t* xts, float* gw, void* stream) {
+    if (!p || !gtc || !gts || !xtc || !xts || !gw) return MXC_ERR_NULL;
+    Conv cv;
+    int rc = conv_init(&cv, p, fmt);
+    if (rc) return rc;
+    if (!aligned16(gtc) || !aligned16(gts) || !aligned16(xtc) || !aligned16(xts) || !aligned16(gw))
+        return MXC_ERR_ALIGN;
+    return launch_naive_wgrad(cv, gtc, gts, xtc, xts, gw, (hipStream_t)stream);
+}
+
 const char* mxconv_strerror(int code) {
     switch (code) {
         case MXC_OK: return "ok";

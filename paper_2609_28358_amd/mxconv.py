@@ -38,7 +38,7 @@ def lib():
         raise MxconvError(f"{LIB_PATH} is missing: build it with "
                           "`python -m paper_2609_28358_amd.build` (no CPU fallback exists)")
     L = ctypes.CDLL(LIB_PATH)
-    P, i32, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+    P, i32, i64, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_size_t
     CP = ctypes.POINTER(MxcConv)
     sigs = {
         "mxconv_codes_bytes": (sz, [i32] * 6),
@@ -52,6 +52,13 @@ def lib():
         "mxconv_fwd": (i32, [CP, i32, P, P, P, P, P, i32, P]),
         "mxconv_dgrad": (i32, [CP, i32, P, P, P, P, P, i32, P]),
         "mxconv_wgrad": (i32, [CP, i32, P, P, P, P, P, P, sz, P]),
+        "mxconv_naive_codes_bytes": (sz, [i64, i64, i32]),
+        "mxconv_naive_scales_bytes": (sz, [i64, i64]),
+        "mxconv_naive_im2col_f32": (i32, [CP, P, P, P]),
+        "mxconv_naive_quantize_1d": (i32, [P, i64, i64, i32, i32, P, P, P]),
+        "mxconv_naive_fwd": (i32, [CP, i32, P, P, P, P, P, P]),
+        "mxconv_naive_dgrad": (i32, [CP, i32, P, P, P, P, P, P, P]),
+        "mxconv_naive_wgrad": (i32, [CP, i32, P, P, P, P, P, P]),
         "mxconv_strerror": (ctypes.c_char_p, [i32]),
     }
     for name, (res, args) in sigs.items():
@@ -194,4 +201,75 @@ def wgrad(cv, gy, x, out=None, workspace=None, stream=None):
     _check(lib().mxconv_wgrad(ctypes.byref(conv_struct(cv)), x.fmt, _ptr(gy.codes), _ptr(gy.scales),
                               _ptr(x.codes), _ptr(x.scales), _ptr(gw), _ptr(workspace), wsz,
                               _stream(stream)), "mxconv_wgrad")
+    return gw
+
+
+# ---------------------------------------------------------------- naive comparator
+# Channels-last GEMM form: P = n*Ho*Wo positions (n, ho, wo), K = kh*kw*cin
+# (kh, kw, ci); X, G_Y, G_X NHWC fp32; W, G_W OHWI fp32 ([cout][K]).
+class LineMatrix:
+    """A 1-D-blocked matrix: codes [lines][Lp] and scales [lines][Lp/32]."""
+
+    def __init__(self, codes, scales, fmt, lines, length):
+        self.codes, self.scales, self.fmt, self.lines, self.length = codes, scales, fmt, lines, length
+
+
+def naive_im2col_f32(cv, x, out=None, stream=None):
+    ho, wo = out_size(cv)
+    col = out if out is not None else torch.empty((cv["n"] * ho * wo, cv["kh"] * cv["kw"] * cv["cin"]),
+                                                  dtype=torch.float32, device=x.device)
+    _check(lib().mxconv_naive_im2col_f32(ctypes.byref(conv_struct(cv)), _ptr(x), _ptr(col), _stream(stream)),
+           "mxconv_naive_im2col_f32")
+    return col
+
+
+def naive_quantize_1d(m, direction, fmt, out=None, stream=None):
+    """Quantize a contiguous fp32 [rows][cols] device matrix with 1-D blocks
+    of 32 along its rows (direction 0) or columns (direction 1)."""
+    rows, cols = m.shape
+    lines, length = (rows, cols) if direction == 0 else (cols, rows)
+    if out is None:
+        nb = lib().mxconv_naive_codes_bytes(lines, length, fmt)
+        ns = lib().mxconv_naive_scales_bytes(lines, length)
+        if nb == 0:
+            raise MxconvError(f"invalid line matrix {lines} x {length}")
+        out = LineMatrix(torch.empty(nb, dtype=torch.uint8, device=m.device),
+                         torch.empty(ns, dtype=torch.uint8, device=m.device), fmt, lines, length)
+    if m.dtype != torch.float32 or not m.is_contiguous():
+        raise MxconvError("naive_quantize_1d needs a contiguous fp32 matrix")
+    _check(lib().mxconv_naive_quantize_1d(_ptr(m), rows, cols, direction, fmt, _ptr(out.codes),
+                                          _ptr(out.scales), _stream(stream)), "mxconv_naive_quantize_1d")
+    return out
+
+
+def naive_fwd(cv, col_q, w_q, out=None, stream=None):
+    ho, wo = out_size(cv)
+    y = out if out is not None else torch.empty((cv["n"] * ho * wo, cv["cout"]), dtype=torch.float32,
+                                                device=col_q.codes.device)
+    _check(lib().mxconv_naive_fwd(ctypes.byref(conv_struct(cv)), col_q.fmt, _ptr(col_q.codes),
+                                  _ptr(col_q.scales), _ptr(w_q.codes), _ptr(w_q.scales), _ptr(y),
+                                  _stream(stream)), "mxconv_naive_fwd")
+    return y
+
+
+def naive_dgrad(cv, gy_q, wt_q, gcol=None, out=None, stream=None):
+    ho, wo = out_size(cv)
+    dev = gy_q.codes.device
+    if gcol is None:
+        gcol = torch.empty((cv["n"] * ho * wo, cv["kh"] * cv["kw"] * cv["cin"]), dtype=torch.float32,
+                           device=dev)
+    gx = out if out is not None else torch.empty((cv["n"], cv["h"], cv["w"], cv["cin"]),
+                                                 dtype=torch.float32, device=dev)
+    _check(lib().mxconv_naive_dgrad(ctypes.byref(conv_struct(cv)), gy_q.fmt, _ptr(gy_q.codes),
+                                    _ptr(gy_q.scales), _ptr(wt_q.codes), _ptr(wt_q.scales), _ptr(gcol),
+                                    _ptr(gx), _stream(stream)), "mxconv_naive_dgrad")
+    return gx
+
+
+def naive_wgrad(cv, gyt_q, xt_q, out=None, stream=None):
+    gw = out if out is not None else torch.empty((cv["cout"], cv["kh"] * cv["kw"] * cv["cin"]),
+                                                 dtype=torch.float32, device=gyt_q.codes.device)
+    _check(lib().mxconv_naive_wgrad(ctypes.byref(conv_struct(cv)), gyt_q.fmt, _ptr(gyt_q.codes),
+                                    _ptr(gyt_q.scales), _ptr(xt_q.codes), _ptr(xt_q.scales), _ptr(gw),
+                                    _stream(stream)), "mxconv_naive_wgrad")
     return gw

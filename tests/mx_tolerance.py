@@ -112,3 +112,29 @@ def wgrad_bound(cv, eg, ex, idx):
         E = E.reshape(n // bn, bn // gs, gs, ho * wo).max(2)                   # group max over samples
         out[i] = np.exp2(E).sum()
     return out
+
+
+def elem_exponents_1d(d, scales, direction, fmt):
+    """Per-element e(v) of a dequantized 1-D-blocked matrix d [rows][cols]
+    with scales in the layout of the oracle's quantize_1d."""
+    rows, cols = d.shape
+    r = np.arange(rows)[:, None]
+    c = np.arange(cols)[None, :]
+    blk = r * ((cols + 31) // 32) + c // 32 if direction == 0 else (r // 32) * cols + c
+    s = scales.astype(np.int64)[blk] - 127
+    with np.errstate(divide="ignore"):
+        e = np.floor(np.log2(np.abs(d)))
+    e = np.maximum(e, s + EMIN[fmt])
+    return np.where(d == 0, -np.inf, e)
+
+
+def nt_group_bound(EA, EB, gsize=8):
+    """G[m][n] = sum over groups of gsize consecutive k of
+    2^max_k (EA[m][k] + EB[n][k]), for C = A B^T contracted over k."""
+    M, K = EA.shape
+    N = EB.shape[0]
+    out = np.zeros((M, N))
+    for g in range(0, K, gsize):
+        s = EA[:, g:g + gsize][:, None, :] + EB[:, g:g + gsize][None, :, :]
+        out += np.exp2(s.max(-1))
+    return out

@@ -111,3 +111,38 @@ def test_strerror_covers_codes():
     for rc in range(0, -7, -1):
         assert mx.strerror(rc) and mx.strerror(rc) != "unknown error"
     assert mx.strerror(-99) == "unknown error"
+
+
+def test_naive_sizes():
+    L = mx.lib()
+    # line matrices: lines x (length rounded up to 64), one scale per 32
+    assert L.mxconv_naive_codes_bytes(100, 576, mx.E4M3) == 100 * 576
+    assert L.mxconv_naive_codes_bytes(100, 27, mx.E4M3) == 100 * 64
+    assert L.mxconv_naive_codes_bytes(100, 65, mx.E2M1) == 100 * 128 // 2
+    assert L.mxconv_naive_scales_bytes(100, 65) == 100 * 4
+    assert L.mxconv_naive_codes_bytes(0, 5, mx.E4M3) == 0
+    assert L.mxconv_naive_codes_bytes(5, 5, 2) == 0
+    assert L.mxconv_naive_scales_bytes(5, -1) == 0
+
+
+def test_naive_errors():
+    L = mx.lib()
+    c = ctypes.byref(mx.conv_struct(synth.conv_dict(32, 64, 64, 8, 8, 3, 1, 1)))
+    bad = ctypes.byref(mx.conv_struct(synth.conv_dict(48, 64, 64, 8, 8, 3, 1, 1)))   # batch rule
+    assert L.mxconv_naive_im2col_f32(None, GOOD, GOOD, None) == -1
+    assert L.mxconv_naive_im2col_f32(c, GOOD, None, None) == -1
+    assert L.mxconv_naive_im2col_f32(bad, GOOD, GOOD, None) == -3
+    assert L.mxconv_naive_im2col_f32(c, ODD, GOOD, None) == -4
+    q = L.mxconv_naive_quantize_1d
+    assert q(None, 4, 4, 0, 0, GOOD, GOOD, None) == -1
+    assert q(GOOD, 0, 4, 0, 0, GOOD, GOOD, None) == -2
+    assert q(GOOD, 4, 4, 2, 0, GOOD, GOOD, None) == -2
+    assert q(GOOD, 4, 4, 0, 5, GOOD, GOOD, None) == -2
+    assert q(GOOD, 4, 4, 1, 0, GOOD, ODD, None) == -4
+    for fn, extra in ((L.mxconv_naive_fwd, ()), (L.mxconv_naive_dgrad, (GOOD,)), (L.mxconv_naive_wgrad, ())):
+        args = [GOOD] * 4 + list(extra) + [GOOD]
+        assert fn(None, 0, *args, None) == -1
+        assert fn(c, 0, None, *args[1:], None) == -1
+        assert fn(c, 3, *args, None) == -2
+        assert fn(bad, 0, *args, None) == -3
+        assert fn(c, 0, *args[:-1], ODD, None) == -4
