@@ -60,6 +60,31 @@ def layer_numbers(cv, fmt, mx):
     }
 
 
+def naive_numbers(cv, fmt, mx):
+    """Algorithmic bytes of one layer step of the naive comparator, and the
+    elements it quantizes (X' twice, W twice, G_Y twice)."""
+    from paper_2609_28358_amd import synth
+    n, ci, co, kh, kw = cv["n"], cv["cin"], cv["cout"], cv["kh"], cv["kw"]
+    ho, wo = synth.out_hw(cv)
+    P, K = n * ho * wo, kh * kw * ci
+    L = mx.lib()
+
+    def line(lines, length):
+        return L.mxconv_naive_codes_bytes(lines, length, fmt) + L.mxconv_naive_scales_bytes(lines, length)
+
+    nx, ny, nw = n * ci * cv["h"] * cv["w"], P * co, co * K
+    by = {
+        "im2col_f32": 4.0 * nx + 4.0 * P * K,
+        "quant_col_k": 4.0 * P * K + line(P, K), "quant_col_p": 4.0 * P * K + line(K, P),
+        "quant_w_k": 4.0 * nw + line(co, K), "quant_w_co": 4.0 * nw + line(K, co),
+        "quant_gy_co": 4.0 * ny + line(P, co), "quant_gy_p": 4.0 * ny + line(co, P),
+        "fwd": line(P, K) + line(co, K) + 4.0 * ny,
+        "dgrad": line(P, co) + line(K, co) + 4.0 * P * K + 4.0 * P * K + 4.0 * nx,   # GEMM + col2im
+        "wgrad": line(co, P) + line(K, P) + 4.0 * nw,
+    }
+    return by, 2 * P * K + 2 * nw + 2 * ny
+
+
 def cpu_baseline():
     """The oracle on the benchmark's own workload, once: every layer of the
     sweep in both formats -- quantize X, W, G_Y, CBF im2col, fwd, dgrad,
@@ -87,12 +112,75 @@ def cpu_baseline():
                       f"the fp64 oracle: {dt:.1f} s"}
 
 
+def naive_leg(jobs, op_ms, mx, synth, dev, stream, reps=3):
+    """Run the naive comparator once per (layer, format) on the same inputs
+    (outside the timed region) and report its time, algorithmic bytes and
+    quantized elements beside the method's.  The method's bytes are its
+    quantize x3 + fwd + dgrad + wgrad (the GEMMs take the im2col implicitly)."""
+    import torch
+    res = {}
+    shared = {}
+    for j in jobs:
+        cv, fmt = j["cv"], j["fmt"]
+        ho, wo = synth.out_hw(cv)
+        P, K, co = cv["n"] * ho * wo, cv["kh"] * cv["kw"] * cv["cin"], cv["cout"]
+        key = j["name"].split("/")[0]
+        if key not in shared:
+            x = synth.cbf_to_nchw(j["x"].cpu(), cv["n"], cv["cin"], cv["h"], cv["w"], 32)
+            gy = synth.cbf_to_nchw(j["gy"].cpu(), cv["n"], co, ho, wo, 32)
+            shared = {key: dict(
+                x=x.permute(0, 2, 3, 1).contiguous().to(dev),
+                gy=gy.permute(0, 2, 3, 1).reshape(P, co).contiguous().to(dev),
+                w=j["w"].permute(0, 2, 3, 1).reshape(co, K).contiguous(),
+                col=torch.empty((P, K), dtype=torch.float32, device=dev),
+                gcol=torch.empty((P, K), dtype=torch.float32, device=dev),
+                y=torch.empty((P, co), dtype=torch.float32, device=dev),
+                gx=torch.empty((cv["n"], cv["h"], cv["w"], cv["cin"]), dtype=torch.float32, device=dev),
+                gw=torch.empty((co, K), dtype=torch.float32, device=dev))}
+        b = shared[key]
+
+        def naive_step():
+            mx.naive_im2col_f32(cv, b["x"], out=b["col"])
+            qc0 = mx.naive_quantize_1d(b["col"], 0, fmt)
+            qw0 = mx.naive_quantize_1d(b["w"], 0, fmt)
+            mx.naive_fwd(cv, qc0, qw0, out=b["y"])
+            qg0 = mx.naive_quantize_1d(b["gy"], 0, fmt)
+            qw1 = mx.naive_quantize_1d(b["w"], 1, fmt)
+            mx.naive_dgrad(cv, qg0, qw1, gcol=b["gcol"], out=b["gx"])
+            qg1 = mx.naive_quantize_1d(b["gy"], 1, fmt)
+            qc1 = mx.naive_quantize_1d(b["col"], 1, fmt)
+            mx.naive_wgrad(cv, qg1, qc1, out=b["gw"])
+
+        naive_step()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            naive_step()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms_naive = e0.elapsed_time(e1) / reps
+        nby, nq = naive_numbers(cv, fmt, mx)
+        ours_ops = ("quant_x", "quant_w", "quant_gy", "fwd", "dgrad", "wgrad")
+        oby = sum(j["nums"][op][1] for op in ours_ops)
+        ms_ours = sum(op_ms[(j["name"], op)] for op in ours_ops)
+        nx = cv["n"] * cv["cin"] * cv["h"] * cv["w"]
+        oq = nx + co * K + P * co
+        res[j["name"]] = {"bytes_naive": round(sum(nby.values())), "bytes_ours": round(oby),
+                          "bytes_ratio": round(sum(nby.values()) / oby, 2),
+                          "ms_naive": round(ms_naive, 4), "ms_ours": round(ms_ours, 4),
+                          "speedup": round(ms_naive / ms_ours, 2),
+                          "quantized_naive": nq, "quantized_ours": oq}
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-naive", action="store_true", help="skip the naive comparator leg")
     ap.add_argument("--layers", default="all", help="comma list of layer indices (profiling aid)")
     ap.add_argument("--fmts", default="0,1")
     args = ap.parse_args()
@@ -197,6 +285,8 @@ def main():
     ms_step = (t1 - t0) * 1e3 / args.steps
     dom_ms = sum(a.elapsed_time(b) for a, b in live[dom]) / len(live[dom])
 
+    naive = {} if args.no_naive else naive_leg(jobs, op_ms, mx, synth, dev, stream)
+
     gemm_flops = sum(j["nums"][op][0] for j in jobs for op in ("fwd", "dgrad", "wgrad"))
     value = gemm_flops / (ms_step * 1e-3) / 1e12
 
@@ -236,6 +326,8 @@ def main():
         "roofline": rl,
         "ops": ops,
     }
+    if naive:
+        out["vs_naive"] = naive
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline()
     print(json.dumps(out))
