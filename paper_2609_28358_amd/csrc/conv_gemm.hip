@@ -1267,12 +1267,16 @@ bool wstream_ok(const Conv& cv) { return cv.x.bn * cv.bits >= 128; }   // rows o
 
 int launch_fwd(const Conv& cv, const void* wc, const uint8_t* ws, const void* xc, const uint8_t* xs,
                float* y, int layout, hipStream_t s) {
+    const int rc = launch_conv_lean(cv, false, wc, ws, xc, xs, y, layout, s);
+    if (rc != 1) return rc;
     if (stream_ok(cv)) return launch_conv_stream(cv, false, wc, ws, xc, xs, y, layout, s);
     return launch_conv(cv, false, wc, ws, xc, xs, y, layout, s);
 }
 
 int launch_dgrad(const Conv& cv, const void* wc, const uint8_t* ws, const void* gc, const uint8_t* gs,
                  float* gx, int layout, hipStream_t s) {
+    const int rc = launch_conv_lean(cv, true, wc, ws, gc, gs, gx, layout, s);
+    if (rc != 1) return rc;
     if (stream_ok(cv)) return launch_conv_stream(cv, true, wc, ws, gc, gs, gx, layout, s);
     return launch_conv(cv, true, wc, ws, gc, gs, gx, layout, s);
 }

@@ -1,0 +1,412 @@
+// conv_lean.hip -- a3 / a4 for the common layer shapes: forward (Sec. II-C,
+// Y_f = W_f X') and stride-1 input gradient (G_X' = W_f^T G_Yf folded back by
+// col2im, computed as a gather) on MX-CBF operands with a batch block of 32,
+// kernel width 1 or 3 and column stride 1 or 2 (forward; any row stride).
+//
+// One workgroup (4 waves) computes a tile of BM = 64*WGM output channels x
+// PX = 8/WGM output pixels of one output row x 32 samples; each wave owns
+// 64 channels x 2 pixels (2 x 2 MFMAs of 32 x 32 x 64 per tap and K step).
+// The K loop runs over stages (kernel row, pair of 32-channel blocks).  A
+// stage holds, in LDS, the weight blocks of its kernel row ([tap][block]
+// [row block]) and the source pixels its taps reach in that row (the halo:
+// [block][pixel]), both as whole stored blocks.  They are streamed with
+// global_load_lds (16 bytes per lane straight into LDS): each wave
+// instruction moves one 1 KB slice; every lane's source offset is fixed for
+// the tile and a stage adds one uniform delta; padding taps and missing
+// blocks read a zero block through a select, not a branch.  Stages are
+// double-buffered: the next stage streams in while the current one computes.
+// The fragments of each source pixel are read from LDS once per stage and
+// reused by every tap that reaches it.
+#include "mx_internal.h"
+
+namespace mxc {
+namespace {
+
+constexpr int LT = 256;
+
+__device__ __attribute__((aligned(16))) uint8_t g_zero_lean[1024];
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+__device__ __forceinline__ void dma16(const void* gsrc, uint8_t* lds_base) {
+    __builtin_amdgcn_global_load_lds(gsrc, (lds_void_t*)lds_base, 16, 0, 0);
+}
+
+struct LeanArgs {
+    const uint8_t* wc;        // weight codes / scales
+    const uint8_t* ws;
+    const uint8_t* sc;        // source activation codes / scales (X or G_Y)
+    const uint8_t* ss;
+    float* out;
+    int layout;
+    int M;                    // real output channels
+    int mtiles, nseg;         // row tiles, pixel segments per output row
+    int hout, wout;           // output spatial size
+    int hsrc, wsrc;           // source spatial size
+    int kh, sh, ph, pw;       // kernel rows, row stride, padding
+    int kcb;                  // 32-channel blocks of the source (K blocks per tap)
+    int w_rowblocks;          // valid 32-row blocks of the weight operand
+    int w_cp;                 // weight Cin_p
+    int w_ncb;                // weight scale blocks per tap (Cin_p / 32)
+    int w_nco;                // weight Cout_p / 32
+    int x_ncb;                // source scale blocks per pixel
+    int ntiles;
+    int stage_bytes, a_bytes, b_bytes, nq;
+};
+
+template <int FMT, bool DG, int KW, int S, int WGM>
+__global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
+    constexpr int EB = FMT == MXC_E4M3 ? 8 : 4;
+    constexpr int TB = 32 * 32 * EB / 8;            // bytes of one stored block (weights and activations)
+    constexpr int RB = 32 * EB / 8;                 // bytes of one channel row of an activation block
+    constexpr int RBW = 2 * WGM;                    // 32-row blocks per tile
+    constexpr int PX = 8 / WGM;                     // output pixels per tile
+    constexpr int HP = DG ? PX + KW - 1 : (PX - 1) * S + KW;   // halo pixels
+    constexpr int NA = KW * 2 * RBW;                // weight blocks per stage
+    constexpr int NB = 2 * HP;                      // activation blocks per stage
+    constexpr int BPI = 1024 / TB;                  // blocks per wave instruction
+    constexpr int NQ = (NA + NB + 4 * BPI - 1) / (4 * BPI);   // DMA instructions per thread per stage
+    constexpr int ND = S + KW;                      // distinct halo pixels of a wave (2 pixels)
+    constexpr int NSA = KW * 2 * RBW;               // weight scales per stage
+    constexpr int NSB = 2 * HP;                     // activation scales per stage
+    static_assert(NSA + NSB <= LT, "scale staging needs one thread per scale");
+    static_assert(!DG || S == 1, "the gather form of dgrad is stride 1 here");
+    extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+    // ---- tile (XCD-aware: consecutive tiles -- same output row -- on one XCD)
+    const int per_xcd = (gridDim.x + 7) / 8;
+    const int lin = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+    if (lin >= p.ntiles) return;
+    const int mt = lin % p.mtiles;
+    int r = lin / p.mtiles;
+    const int seg = r % p.nseg;
+    r /= p.nseg;
+    const int y = r % p.hout, g = r / p.hout;
+    const int x0 = seg * PX;
+    const int cbase = DG ? x0 + p.pw - (KW - 1) : x0 * S - p.pw;   // first halo column
+
+    // ---- strides (bytes)
+    const uint32_t w_tap = (uint32_t)p.w_cp * RB;                  // one tap of one 32-Cout block
+    const uint32_t w_cob = (uint32_t)p.kh * KW * w_tap;            // one 32-Cout block
+    const uint32_t x_pix = (uint32_t)p.kcb * TB;                   // one source pixel
+    const uint32_t x_row = (uint32_t)p.wsrc * x_pix;
+
+    // ---- per-lane DMA pieces: instruction q of this wave moves LDS slice
+    // (4q + wave) of the stage; its block(s) and this lane's 16 bytes
+    uint32_t off[NQ];
+    uint32_t flg[NQ];        // bit0 tile-valid, bit1 K block 1, bit2 activation block
+#pragma unroll
+    for (int q = 0; q < NQ; q++) {
+        const int slice = 4 * q + wave;
+        const int blk = slice * BPI + (BPI == 2 ? (lane >> 5) : 0);
+        const int within = (BPI == 2 ? (lane & 31) : lane) * 16;
+        off[q] = within;
+        flg[q] = 0;
+        if (blk < NA) {
+            // [tap t][K half kb][row block rb]
+            const int rb = blk % RBW, kb = (blk / RBW) & 1, t = blk / (2 * RBW);
+            const int rowblk = mt * RBW + rb;
+            if (DG) {   // rows = input channels (block rowblk of Cin_p), K = output channels
+                off[q] += (uint32_t)kb * w_cob + (uint32_t)t * w_tap + (uint32_t)rowblk * TB;
+            } else {    // rows = output channels (32-Cout block rowblk), K = input channels
+                off[q] += (uint32_t)rowblk * w_cob + (uint32_t)t * w_tap + (uint32_t)kb * TB;
+            }
+            flg[q] = (rowblk < p.w_rowblocks ? 1u : 0u) | (uint32_t)kb << 1;
+        } else if (blk < NA + NB) {
+            // [K half kb][halo pixel hc]
+            const int b = blk - NA, kb = b / HP, hc = b % HP;
+            const int col = cbase + hc;
+            const bool ok = col >= 0 && col < p.wsrc;
+            off[q] += (uint32_t)(ok ? col : 0) * x_pix + (uint32_t)kb * TB;
+            flg[q] = (ok ? 1u : 0u) | (uint32_t)kb << 1 | 4u;
+        }
+    }
+    // scale staging: threads [0, NSA) weight scales [t][kb][rb], [NSA, NSA+NSB) halo scales [kb][hc]
+    uint32_t s_off = 0, s_flg = 0;
+    if (tid < NSA) {
+        const int rb = tid % RBW, kb = (tid / RBW) & 1, t = tid / (2 * RBW);
+        const int rowblk = mt * RBW + rb;
+        if (DG) s_off = ((uint32_t)kb * p.kh * KW + t) * p.w_ncb + rowblk;
+        else    s_off = ((uint32_t)rowblk * p.kh * KW + t) * p.w_ncb + kb;
+        s_flg = (rowblk < p.w_rowblocks ? 1u : 0u) | (uint32_t)kb << 1 | 8u;
+    } else if (tid < NSA + NSB) {
+        const int q = tid - NSA, kb = q / HP, hc = q % HP;
+        const int col = cbase + hc;
+        const bool ok = col >= 0 && col < p.wsrc;
+        s_off = (uint32_t)(ok ? col : 0) * p.x_ncb + kb;
+        s_flg = (ok ? 1u : 0u) | (uint32_t)kb << 1 | 4u | 8u;
+    }
+
+    const int nkk = (p.kcb + 1) / 2;
+    const int nstage = p.kh * nkk;
+    const uint8_t* const zero = g_zero_lean;
+    uint32_t sreg = 0;
+
+    // stage st = (kernel row kh, K pair kk): issue its loads into buffer buf
+    auto issue = [&](int st, int buf) {
+        const int kk = st % nkk, kh = st / nkk;
+        const int sy = DG ? y + p.ph - kh : y * p.sh + kh - p.ph;
+        const bool row_ok = sy >= 0 && sy < p.hsrc;
+        const bool kb1_ok = 2 * kk + 1 < p.kcb;
+        const uint8_t* abase = p.wc + (DG ? (uint32_t)(2 * kk) * w_cob : (uint32_t)(2 * kk) * TB) +
+                               (uint32_t)kh * KW * w_tap;
+        const uint8_t* bbase = p.sc + ((uint32_t)g * p.hsrc + (row_ok ? sy : 0)) * x_row + (uint32_t)(2 * kk) * TB;
+        uint8_t* lds = smem + buf * p.stage_bytes;
+#pragma unroll
+        for (int q = 0; q < NQ; q++) {
+            const uint32_t f = flg[q];
+            const bool isb = f & 4u;
+            const bool ok = (f & 1u) && (!(f & 2u) || kb1_ok) && (!isb || row_ok);
+            const uint8_t* src = (isb ? bbase : abase) + off[q];
+            dma16(ok ? src : zero + (off[q] & (TB - 1)), lds + (4 * q + wave) * 1024);
+        }
+        sreg = 0;
+        if (s_flg & 8u) {
+            const bool isb = s_flg & 4u;
+            const bool ok = (s_flg & 1u) && (!(s_flg & 2u) || kb1_ok) && (!isb || row_ok);
+            const uint32_t o = isb ? s_off + ((uint32_t)g * p.hsrc + (row_ok ? sy : 0)) * p.wsrc * p.x_ncb + 2 * kk
+                                   : s_off + (uint32_t)kh * KW * p.w_ncb +
+                                         (DG ? (uint32_t)(2 * kk) * p.kh * KW * p.w_ncb : (uint32_t)(2 * kk));
+            const uint8_t v = (isb ? p.ss : p.ws)[ok ? o : 0u];   // index 0 is always in bounds
+            sreg = ok ? v : 0u;
+        }
+    };
+    auto store_scales = [&](int buf) {
+        if (s_flg & 8u) smem[buf * p.stage_bytes + p.a_bytes + p.b_bytes + tid] = (uint8_t)sreg;
+    };
+
+    // ---- wave geometry and per-lane fragment offsets
+    const int wm = wave % WGM, wn = wave / WGM;       // 64-row group, pixel pair
+    const int h = lane >> 5, i16 = lane & 15, gi = lane >> 4, cg = gi & 1, hh = gi >> 1;
+    int a_lane;
+    if (DG) a_lane = FMT == MXC_E4M3 ? (lane & 31) * 32 + 16 * h : (lane & 31) * 16;
+    else    a_lane = FMT == MXC_E4M3 ? (16 * hh + (i16 >> 1)) * 32 + 16 * cg + 8 * (i16 & 1) : i16 * 16 + 8 * cg;
+    const int b_lane = FMT == MXC_E4M3 ? (16 * hh + (i16 >> 1)) * RB + 16 * cg + 8 * (i16 & 1)
+                                       : i16 * RB + 8 * cg;
+    const int hbase = DG ? 2 * wn : 2 * wn * S;       // first halo pixel of the wave
+
+    v16f acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; i++)
+#pragma unroll
+        for (int j = 0; j < 2; j++)
+#pragma unroll
+            for (int e = 0; e < 16; e++) acc[i][j][e] = 0.0f;
+
+    if (nstage > 0) {
+        issue(0, 0);
+        __builtin_amdgcn_s_waitcnt(0x0F70);
+        store_scales(0);
+    }
+    __syncthreads();
+    for (int st = 0; st < nstage; st++) {
+        const int buf = st & 1;
+        if (st + 1 < nstage) issue(st + 1, buf ^ 1);
+        const uint8_t* A = smem + buf * p.stage_bytes;
+        const uint8_t* B = A + p.a_bytes;
+        const uint8_t* SC = B + p.b_bytes;
+
+        // fragments of the wave's ND halo pixels (both K halves)
+        v8i bf[ND];
+        int sb[ND];
+#pragma unroll
+        for (int d = 0; d < ND; d++) {
+            const int hc = hbase + d;
+            if (FMT == MXC_E4M3) {
+                const uint8_t* tb = B + hc * TB + b_lane;
+#pragma unroll
+                for (int kb = 0; kb < 2; kb++)
+#pragma unroll
+                    for (int hf = 0; hf < 2; hf++) {
+                        const v2i v = lds_tr8(tb + kb * HP * TB + hf * 8 * RB);
+                        bf[d][4 * kb + 2 * hf] = v[0];
+                        bf[d][4 * kb + 2 * hf + 1] = v[1];
+                    }
+            } else {
+                const uint8_t* tb = B + (hh * HP + hc) * TB + b_lane;
+#pragma unroll
+                for (int hf = 0; hf < 2; hf++) {
+                    const v2i v = lds_tr4(tb + hf * 16 * RB);
+                    bf[d][2 * hf] = v[0];
+                    bf[d][2 * hf + 1] = v[1];
+                }
+                bf[d][4] = bf[d][5] = bf[d][6] = bf[d][7] = 0;
+            }
+            sb[d] = SC[NSA + h * HP + hc];
+        }
+#pragma unroll
+        for (int t = 0; t < KW; t++) {
+            v8i af[2];
+            int sa[2];
+#pragma unroll
+            for (int rb = 0; rb < 2; rb++) {
+                const int rbi = 2 * wm + rb;
+                const uint8_t* a0 = A + ((t * 2 + 0) * RBW + rbi) * TB + a_lane;
+                const uint8_t* a1 = a0 + RBW * TB;
+                if (DG) {
+                    if (FMT == MXC_E4M3) {
+                        const v4i u0 = *(const v4i*)a0;
+                        const v4i u1 = *(const v4i*)a1;
+                        af[rb][0] = u0[0]; af[rb][1] = u0[1]; af[rb][2] = u0[2]; af[rb][3] = u0[3];
+                        af[rb][4] = u1[0]; af[rb][5] = u1[1]; af[rb][6] = u1[2]; af[rb][7] = u1[3];
+                    } else {
+                        const v4i u0 = *(const v4i*)(h ? a1 : a0);
+                        af[rb][0] = u0[0]; af[rb][1] = u0[1]; af[rb][2] = u0[2]; af[rb][3] = u0[3];
+                        af[rb][4] = af[rb][5] = af[rb][6] = af[rb][7] = 0;
+                    }
+                } else {
+                    if (FMT == MXC_E4M3) {
+#pragma unroll
+                        for (int kb = 0; kb < 2; kb++)
+#pragma unroll
+                            for (int hf = 0; hf < 2; hf++) {
+                                const v2i v = lds_tr8((kb ? a1 : a0) + hf * 8 * 32);
+                                af[rb][4 * kb + 2 * hf] = v[0];
+                                af[rb][4 * kb + 2 * hf + 1] = v[1];
+                            }
+                    } else {
+                        const uint8_t* ab = hh ? a1 : a0;
+#pragma unroll
+                        for (int hf = 0; hf < 2; hf++) {
+                            const v2i v = lds_tr4(ab + hf * 16 * 16);
+                            af[rb][2 * hf] = v[0];
+                            af[rb][2 * hf + 1] = v[1];
+                        }
+                        af[rb][4] = af[rb][5] = af[rb][6] = af[rb][7] = 0;
+                    }
+                }
+                sa[rb] = SC[(t * 2 + h) * RBW + rbi];
+            }
+#pragma unroll
+            for (int cn = 0; cn < 2; cn++) {
+                const int d = DG ? cn + (KW - 1 - t) : cn * S + t;
+#pragma unroll
+                for (int rb = 0; rb < 2; rb++)
+                    acc[rb][cn] = mfma_mx<FMT>(af[rb], bf[d], acc[rb][cn], sa[rb], sb[d]);
+            }
+        }
+        if (st + 1 < nstage) {
+            __builtin_amdgcn_s_waitcnt(0x0F70);     // this wave's loads of the next stage have landed
+            store_scales(buf ^ 1);
+        }
+        __syncthreads();
+    }
+
+    // ---- epilogue: lane column = sample (lane % 32) of pixel x0 + 2 wn + cn;
+    // rows step by 1 within groups of 4 and by 8 between groups
+    const int mrow = mt * 64 * WGM + 64 * wm + 4 * h;
+    const bool rows_full = mrow + 59 < p.M;           // the wave's last row is mrow + 59
+    const int n = lane & 31;
+#pragma unroll
+    for (int cn = 0; cn < 2; cn++) {
+        const int x = x0 + 2 * wn + cn;
+        if (x >= p.wout) continue;
+        size_t o0, ms;
+        if (p.layout == MXC_CBF) {
+            o0 = ((((size_t)g * p.hout + y) * p.wout + x) * p.M + mrow) * 32 + n;
+            ms = 32;
+        } else {
+            o0 = (((size_t)(g * 32 + n) * p.M + mrow) * p.hout + y) * p.wout + x;
+            ms = (size_t)p.hout * p.wout;
+        }
+        float* out = p.out + o0;
+#pragma unroll
+        for (int rb = 0; rb < 2; rb++)
+#pragma unroll
+            for (int e = 0; e < 16; e++) {
+                const int dm = 32 * rb + 8 * (e >> 2) + (e & 3);
+                if (rows_full || mrow + dm < p.M) out[dm * ms] = acc[rb][cn][e];
+            }
+    }
+}
+
+template <int FMT, bool DG, int KW, int S, int WGM>
+int launch_lean_t(const LeanArgs& a, hipStream_t s) {
+    const size_t lds = 2 * (size_t)a.stage_bytes;
+    static bool attr = false;
+    if (lds > 65536 && !attr) {
+        if (hipFuncSetAttribute((const void*)conv_lean_kernel<FMT, DG, KW, S, WGM>,
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+            return MXC_ERR_HIP;
+        attr = true;
+    }
+    const int grid = (a.ntiles + 7) / 8 * 8;
+    hipLaunchKernelGGL((conv_lean_kernel<FMT, DG, KW, S, WGM>), dim3(grid), dim3(LT), lds, s, a);
+    return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
+}
+
+template <int FMT, bool DG, int KW, int S>
+int launch_lean_w(const LeanArgs& a, int wgm, hipStream_t s) {
+    if (wgm == 4) return launch_lean_t<FMT, DG, KW, S, 4>(a, s);
+    if (wgm == 2) return launch_lean_t<FMT, DG, KW, S, 2>(a, s);
+    return launch_lean_t<FMT, DG, KW, S, 1>(a, s);
+}
+
+template <int FMT, bool DG>
+int launch_lean_f(const LeanArgs& a, int kw, int sw, int wgm, hipStream_t s) {
+    if constexpr (DG) {
+        (void)sw;
+        return kw == 3 ? launch_lean_w<FMT, DG, 3, 1>(a, wgm, s) : launch_lean_w<FMT, DG, 1, 1>(a, wgm, s);
+    } else {
+        if (kw == 3) return sw == 2 ? launch_lean_w<FMT, DG, 3, 2>(a, wgm, s) : launch_lean_w<FMT, DG, 3, 1>(a, wgm, s);
+        return sw == 2 ? launch_lean_w<FMT, DG, 1, 2>(a, wgm, s) : launch_lean_w<FMT, DG, 1, 1>(a, wgm, s);
+    }
+}
+
+}  // namespace
+
+// Returns 1 when the layer is outside this kernel's shapes (the caller then
+// uses the general kernels), else an MXC_* code.
+int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const void* sc,
+                     const uint8_t* ss, float* out, int layout, hipStream_t s) {
+    if (cv.x.bn != 32) return 1;
+    if (cv.kw != 1 && cv.kw != 3) return 1;
+    if (dg ? (cv.sh != 1 || cv.sw != 1) : (cv.sw != 1 && cv.sw != 2)) return 1;
+    LeanArgs a;
+    a.wc = (const uint8_t*)wc; a.ws = ws; a.sc = (const uint8_t*)sc; a.ss = ss;
+    a.out = out; a.layout = layout;
+    a.M = dg ? cv.cin : cv.cout;
+    const Geom& src = dg ? cv.gy : cv.x;
+    a.hsrc = src.h; a.wsrc = src.w;
+    a.hout = dg ? cv.h : cv.ho;
+    a.wout = dg ? cv.w : cv.wo;
+    a.kh = cv.kh; a.sh = cv.sh; a.ph = cv.ph; a.pw = cv.pw;
+    a.kcb = src.ncb;
+    a.w_rowblocks = dg ? cv.wt.ncb : cv.wt.np / 32;
+    a.w_cp = cv.wt.cp; a.w_ncb = cv.wt.ncb; a.w_nco = cv.wt.np / 32;
+    a.x_ncb = src.ncb;
+    if (dg && a.w_nco != src.ncb) return 1;
+    // rows per tile: as many 64-row groups as the output channels fill, up to 4
+    const int mp = (a.M + 63) / 64;
+    const int wgm = mp >= 4 ? 4 : (mp >= 2 ? 2 : 1);
+    const int px = 8 / wgm;
+    a.mtiles = (a.M + 64 * wgm - 1) / (64 * wgm);
+    a.nseg = (a.wout + px - 1) / px;
+    const long long nt = (long long)a.mtiles * a.nseg * a.hout * src.ng;
+    if (nt <= 0 || nt > 0x7FFFFFF0LL) return 1;
+    a.ntiles = (int)nt;
+    const int tb = cv.bits == 8 ? 1024 : 512;
+    const int hp = dg ? px + cv.kw - 1 : (px - 1) * cv.sw + cv.kw;
+    const int na = cv.kw * 2 * 2 * wgm, nb = 2 * hp;
+    const int bpi = 1024 / tb;
+    a.nq = (na + nb + 4 * bpi - 1) / (4 * bpi);
+    a.a_bytes = na * tb;
+    a.b_bytes = nb * tb;
+    // DMA slices cover nq * 4 KB; scales follow the blocks
+    const int blocks_bytes = a.nq * 4096;
+    a.stage_bytes = blocks_bytes + 256;
+    if (a.a_bytes + a.b_bytes > blocks_bytes) return MXC_ERR_HIP;
+    // scales sit right after the blocks region
+    a.b_bytes = blocks_bytes - a.a_bytes;
+    if (2 * (size_t)a.stage_bytes > 160 * 1024) return 1;
+    if (cv.fmt == MXC_E4M3)
+        return dg ? launch_lean_f<MXC_E4M3, true>(a, cv.kw, cv.sw, wgm, s)
+                  : launch_lean_f<MXC_E4M3, false>(a, cv.kw, cv.sw, wgm, s);
+    return dg ? launch_lean_f<MXC_E2M1, true>(a, cv.kw, cv.sw, wgm, s)
+              : launch_lean_f<MXC_E2M1, false>(a, cv.kw, cv.sw, wgm, s);
+}
+
+}  // namespace mxc

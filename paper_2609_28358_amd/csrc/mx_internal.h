@@ -47,6 +47,10 @@ int launch_fwd(const Conv& cv, const void* wc, const uint8_t* ws, const void* xc
                const uint8_t* xs, float* y, int layout, hipStream_t s);
 int launch_dgrad(const Conv& cv, const void* wc, const uint8_t* ws, const void* gc,
                  const uint8_t* gs, float* gx, int layout, hipStream_t s);
+// fwd / stride-1 dgrad for batch block 32 and kernel width 1 or 3
+// (conv_lean.hip); returns 1 when the layer is outside those shapes
+int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const void* sc,
+                     const uint8_t* ss, float* out, int layout, hipStream_t s);
 size_t wgrad_workspace(const Conv& cv);
 int launch_wgrad(const Conv& cv, const void* gc, const uint8_t* gs, const void* xc,
                  const uint8_t* xs, float* gw, void* ws, hipStream_t s);

@@ -187,6 +187,9 @@ GEMM_CONVS = [
     dict(n=32, cin=48, cout=96, h=10, w=9, kh=7, kw=3, sh=2, sw=1, ph=3, pw=1),
     synth.conv_dict(8, 64, 32, 6, 19, 3, 1, 1),               # Bn = 8: a tile spans 16 pixels
     synth.conv_dict(32, 16, 24, 9, 11, 7, 1, 3),              # 7x7: stages too big for the stream path
+    synth.conv_dict(32, 32, 256, 5, 6, 3, 1, 1),              # 256 output channels: 4 row groups per tile
+    synth.conv_dict(32, 256, 64, 6, 7, 1, 1, 0),              # 1x1 with 256 input channels (dgrad rows)
+    synth.conv_dict(32, 96, 200, 7, 9, 3, 2, 1),              # ragged channels at stride 2
 ]
 
 
