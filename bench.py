@@ -12,9 +12,12 @@ gradients N(0, 1e-3), all seeded.
 
 `value` is the conv fwd+bwd GEMM throughput of the whole step: the three
 GEMMs' algorithmic flops (2 N Cout Ho Wo Cin Kh Kw each, real channels) over
-the step's wall time, quantize and im2col included.  Every op is also timed
-with HIP events on the stream it runs on; the op taking the most time per
-step gets the `roofline` object, and all ops are listed in `ops`.
+the step's wall time, quantize and im2col included.  The timed step is
+replayed from HIP graphs (captured once after warm-up), so it measures GPU
+time, not Python launch cost.  Every op is also timed alone with HIP events
+on the stream it runs on; the op taking the most time per step gets the
+`roofline` object (its time measured again inside the timed region), and all
+ops are listed in `ops`.
 
     python bench.py [--steps K] [--warmup W] [--no-cpu-baseline]
 """
@@ -28,6 +31,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_GBS = 8000.0                                   # MI355X HBM3E
+SPIN_CYCLES = 100000                               # GPU spin ahead of a timed eager launch
 MFMA_TFLOPS = {0: 5000.0, 1: 10100.0}              # dense MXFP8 / MXFP4
 FMT_NAME = {0: "mxfp8", 1: "mxfp4"}
 
@@ -154,6 +158,7 @@ def naive_leg(jobs, op_ms, mx, synth, dev, stream, reps=3):
         naive_step()
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(SPIN_CYCLES)
         e0.record(stream)
         for _ in range(reps):
             naive_step()
@@ -250,40 +255,73 @@ def main():
         if rc:
             raise mx.MxconvError(mx.strerror(rc))
 
-    def step(events=None):
-        for j in jobs:
-            for op in OPS:
-                key = (j["name"], op)
-                if events is not None and key in events:
-                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                    e0.record(stream)
-                    run_im2col(j) if op == "im2col" else run_op(j, op)
-                    e1.record(stream)
-                    events[key].append((e0, e1))
-                else:
-                    run_im2col(j) if op == "im2col" else run_op(j, op)
+    seq = [(j, op) for j in jobs for op in OPS]
 
-    # warmup, then one instrumented pass to find each op's time
+    def run(j, op):
+        run_im2col(j) if op == "im2col" else run_op(j, op)
+
+    def step():
+        for j, op in seq:
+            run(j, op)
+
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    probe = {(j["name"], op): [] for j in jobs for op in OPS}
-    for _ in range(3):
-        step(probe)
-    torch.cuda.synchronize()
-    op_ms = {k: sum(a.elapsed_time(b) for a, b in v) / len(v) for k, v in probe.items()}
-    dom = max(op_ms, key=op_ms.get)
 
-    # timed region: K steps, events only around the dominant op's launches
-    live = {dom: []}
+    # Per-op GPU time: each op alone, behind a GPU spin so that the event pair
+    # brackets the kernel(s) and not the host's launch latency.
+    def op_time(j, op, reps=5):
+        marks = []
+        for _ in range(reps):
+            torch.cuda._sleep(SPIN_CYCLES)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            run(j, op)
+            e1.record(stream)
+            marks.append((e0, e1))
+        torch.cuda.synchronize()
+        return sum(a.elapsed_time(b) for a, b in marks) / reps
+
+    op_ms = {(j["name"], op): op_time(j, op) for j, op in seq}
+    dom = max(op_ms, key=op_ms.get)
+    di = [(j["name"], op) for j, op in seq].index(dom)
+
+    # The step is launched as HIP graphs (one per stretch: the ops before the
+    # dominant one, the dominant op, the ops after it), so host-side launch
+    # cost does not enter the step time; HIP events recorded between the
+    # graph launches time the dominant op inside the timed region.
+    graphs = []
+    for part in (seq[:di], seq[di:di + 1], seq[di + 1:]):
+        if not part:
+            graphs.append(None)
+            continue
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for j, op in part:
+                run(j, op)
+        graphs.append(g)
+    for _ in range(2):
+        for g in graphs:
+            if g is not None:
+                g.replay()
     torch.cuda.synchronize()
+
+    marks = []
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        step(live)
+        if graphs[0] is not None:
+            graphs[0].replay()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        graphs[1].replay()
+        e1.record(stream)
+        if graphs[2] is not None:
+            graphs[2].replay()
+        marks.append((e0, e1))
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_step = (t1 - t0) * 1e3 / args.steps
-    dom_ms = sum(a.elapsed_time(b) for a, b in live[dom]) / len(live[dom])
+    dom_ms = sum(a.elapsed_time(b) for a, b in marks) / len(marks)
 
     naive = {} if args.no_naive else naive_leg(jobs, op_ms, mx, synth, dev, stream)
 

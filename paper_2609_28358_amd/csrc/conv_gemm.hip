@@ -1282,12 +1282,23 @@ int launch_dgrad(const Conv& cv, const void* wc, const uint8_t* ws, const void* 
 }
 
 size_t wgrad_workspace(const Conv& cv) {
+    const int ls = wgrad_lean_splits(cv);
+    if (ls > 0) return ls > 1 ? (size_t)ls * cv.gy.cp * cv.kh * cv.kw * cv.x.cp * sizeof(float) : 0;
     const WgradPlan pl = wgrad_plan(cv);
     return (size_t)pl.splits * cv.gy.cp * pl.ntot * sizeof(float);
 }
 
 int launch_wgrad(const Conv& cv, const void* gc, const uint8_t* gs, const void* xc, const uint8_t* xs,
                  float* gw, void* ws, hipStream_t s) {
+    const int ls = wgrad_lean_splits(cv);
+    if (ls > 0) {
+        const int rc = launch_wgrad_lean(cv, gc, gs, xc, xs, ls > 1 ? (float*)ws : gw, ls, s);
+        if (rc || ls == 1) return rc;
+        const long total = (long)cv.cout * cv.kh * cv.kw * cv.cin;
+        hipLaunchKernelGGL(wgrad_reduce, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s,
+                           (const float*)ws, gw, cv, cv.kh * cv.kw * cv.x.cp, ls);
+        return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
+    }
     const WgradPlan pl = wgrad_plan(cv);
     WgradArgs a;
     a.cv = cv;

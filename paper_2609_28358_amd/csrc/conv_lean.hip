@@ -16,7 +16,9 @@
 // blocks read a zero block through a select, not a branch.  Stages are
 // double-buffered: the next stage streams in while the current one computes.
 // The fragments of each source pixel are read from LDS once per stage and
-// reused by every tap that reaches it.
+// reused by every tap that reaches it.  The MFMAs compute the transposed
+// tile (samples x channels) so that each lane ends up holding four
+// consecutive samples of one channel: one 16-byte store in the CBF layout.
 #include "mx_internal.h"
 
 namespace mxc {
@@ -284,8 +286,8 @@ __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
             for (int cn = 0; cn < 2; cn++) {
                 const int d = DG ? cn + (KW - 1 - t) : cn * S + t;
 #pragma unroll
-                for (int rb = 0; rb < 2; rb++)
-                    acc[rb][cn] = mfma_mx<FMT>(af[rb], bf[d], acc[rb][cn], sa[rb], sb[d]);
+                for (int rb = 0; rb < 2; rb++)   // transposed product: rows = samples, columns = channels
+                    acc[rb][cn] = mfma_mx<FMT>(bf[d], af[rb], acc[rb][cn], sb[d], sa[rb]);
             }
         }
         if (st + 1 < nstage) {
@@ -295,31 +297,41 @@ __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
         __syncthreads();
     }
 
-    // ---- epilogue: lane column = sample (lane % 32) of pixel x0 + 2 wn + cn;
-    // rows step by 1 within groups of 4 and by 8 between groups
-    const int mrow = mt * 64 * WGM + 64 * wm + 4 * h;
-    const bool rows_full = mrow + 59 < p.M;           // the wave's last row is mrow + 59
-    const int n = lane & 31;
+    // ---- epilogue.  The tile was computed transposed: in acc[rb][cn] lane l
+    // holds output channel 32 rb + l % 32 of the wave's 64, and samples
+    // 8 (e / 4) + 4 (l / 32) + e % 4 -- four consecutive samples per group of
+    // 4 registers, i.e. one 16-byte run of the CBF output.
+    const int m = mt * 64 * WGM + 64 * wm + (lane & 31);
 #pragma unroll
     for (int cn = 0; cn < 2; cn++) {
         const int x = x0 + 2 * wn + cn;
         if (x >= p.wout) continue;
-        size_t o0, ms;
         if (p.layout == MXC_CBF) {
-            o0 = ((((size_t)g * p.hout + y) * p.wout + x) * p.M + mrow) * 32 + n;
-            ms = 32;
-        } else {
-            o0 = (((size_t)(g * 32 + n) * p.M + mrow) * p.hout + y) * p.wout + x;
-            ms = (size_t)p.hout * p.wout;
-        }
-        float* out = p.out + o0;
+            float* px = p.out + (((size_t)g * p.hout + y) * p.wout + x) * p.M * 32;
 #pragma unroll
-        for (int rb = 0; rb < 2; rb++)
+            for (int rb = 0; rb < 2; rb++) {
+                const int mm = m + 32 * rb;
+                if (mm >= p.M) continue;
+                float* o = px + (size_t)mm * 32 + 4 * h;
 #pragma unroll
-            for (int e = 0; e < 16; e++) {
-                const int dm = 32 * rb + 8 * (e >> 2) + (e & 3);
-                if (rows_full || mrow + dm < p.M) out[dm * ms] = acc[rb][cn][e];
+                for (int e4 = 0; e4 < 4; e4++)
+                    *(float4*)(o + 8 * e4) = make_float4(acc[rb][cn][4 * e4], acc[rb][cn][4 * e4 + 1],
+                                                         acc[rb][cn][4 * e4 + 2], acc[rb][cn][4 * e4 + 3]);
             }
+        } else {
+            const size_t hw = (size_t)p.hout * p.wout;
+            float* px = p.out + (size_t)y * p.wout + x;
+#pragma unroll
+            for (int rb = 0; rb < 2; rb++) {
+                const int mm = m + 32 * rb;
+                if (mm >= p.M) continue;
+#pragma unroll
+                for (int e = 0; e < 16; e++) {
+                    const int n = 8 * (e >> 2) + 4 * h + (e & 3);
+                    px[((size_t)(g * 32 + n) * p.M + mm) * hw] = acc[rb][cn][e];
+                }
+            }
+        }
     }
 }
 

@@ -39,7 +39,7 @@ struct Conv {
 int conv_init(Conv* cv, const mxc_conv* p, int fmt);
 
 // ---------------------------------------------------------------- launchers
-int launch_quantize(const void* src, int dtype, int layout, const Geom& g, int fmt,
+int launch_quantize(const void* src, int dtype, int layout, int role, const Geom& g, int fmt,
                     void* codes, uint8_t* scales, hipStream_t s);
 int launch_im2col(const Conv& cv, const void* xc, const uint8_t* xs, void* cc, uint8_t* cs,
                   hipStream_t s);
@@ -51,6 +51,12 @@ int launch_dgrad(const Conv& cv, const void* wc, const uint8_t* ws, const void* 
 // (conv_lean.hip); returns 1 when the layer is outside those shapes
 int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const void* sc,
                      const uint8_t* ss, float* out, int layout, hipStream_t s);
+// weight gradient for batch block 32 (wgrad_lean.hip): number of K splits
+// (0: not applicable); with more than one split the partial tiles go to the
+// workspace and are reduced by the caller
+int wgrad_lean_splits(const Conv& cv);
+int launch_wgrad_lean(const Conv& cv, const void* gc, const uint8_t* gs, const void* xc, const uint8_t* xs,
+                      float* dst, int splits, hipStream_t s);
 size_t wgrad_workspace(const Conv& cv);
 int launch_wgrad(const Conv& cv, const void* gc, const uint8_t* gs, const void* xc,
                  const uint8_t* xs, float* gw, void* ws, hipStream_t s);
@@ -129,6 +135,14 @@ __device__ __forceinline__ uint32_t pack8_e2m1(float4 x, float4 y, float inv) {
     q = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(q, y.x * inv, y.y * inv, 1.0f, 2);
     q = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(q, y.z * inv, y.w * inv, 1.0f, 3);
     return q;
+}
+
+// four consecutive elements -> four E2M1 codes in 16 bits (first element in the low nibble)
+__device__ __forceinline__ unsigned short pack4_e2m1(float4 x, float inv) {
+    uint32_t q = 0;
+    q = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(q, x.x * inv, x.y * inv, 1.0f, 0);
+    q = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(q, x.z * inv, x.w * inv, 1.0f, 1);
+    return (unsigned short)q;
 }
 
 // One block-scaled MFMA: D(32x32) += A(32 x 64) B(64 x 32) with one E8M0

@@ -107,7 +107,7 @@ int mxconv_quantize(const void* src, int dtype, int layout, int role, int fmt, i
     int rc = geom_init(&g, role, fmt, n, c, h, w);
     if (rc) return rc;
     if (!aligned16(src) || !aligned16(codes) || !aligned16(scales)) return MXC_ERR_ALIGN;
-    return launch_quantize(src, dtype, layout, g, fmt, codes, scales, (hipStream_t)stream);
+    return launch_quantize(src, dtype, layout, role, g, fmt, codes, scales, (hipStream_t)stream);
 }
 
 int mxconv_im2col_cbf(const mxc_conv* p, int fmt, const void* xc, const uint8_t* xs, void* cc,

@@ -15,6 +15,10 @@
 //      encoded with the hardware converts, codes stored as 16-byte vectors.
 // Traffic: 4 (or 2) bytes read and 1 (or 1/2) byte written per element, plus
 // one scale byte per block; HBM-bound.
+//
+// CBF sources with Bn = 32 and OIHW weights skip the slab: their blocks need
+// no transposition, so one wave quantizes one block straight from its
+// registers (quantize_block_kernel).
 #include "mx_internal.h"
 
 namespace mxc {
@@ -160,6 +164,92 @@ __global__ __launch_bounds__(QT) void quantize_kernel(const void* __restrict__ s
     }
 }
 
+// One wave per 32 x 32 block, for the two sources whose blocks need no
+// transposition: a CBF activation with Bn = 32 (a block is 1024 contiguous
+// source elements in code order) and OIHW weights (a block is a gather of
+// 32 Cout x 32 Cin at one tap).  Block index b = scale index; its codes are
+// the 1024 elements at b * 1024.  Lane l holds the four element runs
+// [256 q + 4 l, 256 q + 4 l + 4), q = 0..3, so every load and store
+// instruction of the wave covers one contiguous range.
+// SRC 0: CBF activation, SRC 1: NCHW-ordered weights (n = Cout).
+template <int SRC, int DTYPE, int FMT>
+__global__ __launch_bounds__(QT) void quantize_block_kernel(const void* __restrict__ src, Geom g,
+                                                            uint8_t* __restrict__ codes,
+                                                            uint8_t* __restrict__ scales, int nblocks) {
+    const int lane = threadIdx.x & 63;
+    const int blk = blockIdx.x * (QT / 64) + (threadIdx.x >> 6);
+    if (blk >= nblocks) return;
+    const int cb = blk % g.ncb, rest = blk / g.ncb;          // rest = (group, pixel) or (Cout block, tap)
+    const int j = 4 * (lane & 7);                            // first sample (output channel) of the run
+    float4 x[4];
+    if (SRC == 0) {
+#pragma unroll
+        for (int q = 0; q < 4; q++) {
+            const int c = cb * 32 + 8 * q + (lane >> 3);
+            const bool ok = c < g.c;
+            const size_t i = ((size_t)rest * g.c + (ok ? c : 0)) * 32 + j;
+            if (DTYPE == MXC_F32) {
+                x[q] = __ldg((const float4*)((const float*)src + i));
+            } else {
+                const uint2 b = __ldg((const uint2*)((const unsigned short*)src + i));
+                x[q] = make_float4(__uint_as_float(b.x << 16), __uint_as_float(b.x & 0xFFFF0000u),
+                                   __uint_as_float(b.y << 16), __uint_as_float(b.y & 0xFFFF0000u));
+            }
+            if (!ok) x[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+    } else {
+        const int hw = g.h * g.w;
+        const int cob = rest / hw, tap = rest % hw;
+        float v[16];
+#pragma unroll
+        for (int k = 0; k < 16; k++) {
+            const int c = cb * 32 + 8 * (k >> 2) + (lane >> 3);
+            const int n = cob * 32 + j + (k & 3);
+            const bool ok = c < g.c && n < g.n;
+            const size_t i = ok ? ((size_t)n * g.c + c) * hw + tap : 0;
+            v[k] = DTYPE == MXC_F32 ? __ldg((const float*)src + i)
+                                    : __uint_as_float((uint32_t)__ldg((const unsigned short*)src + i) << 16);
+            if (!ok) v[k] = 0.0f;
+        }
+#pragma unroll
+        for (int q = 0; q < 4; q++) x[q] = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+    }
+    uint32_t m = 0;
+#pragma unroll
+    for (int q = 0; q < 4; q++) {
+        m = max(m, __float_as_uint(x[q].x) & 0x7FFFFFFFu);
+        m = max(m, __float_as_uint(x[q].y) & 0x7FFFFFFFu);
+        m = max(m, __float_as_uint(x[q].z) & 0x7FFFFFFFu);
+        m = max(m, __float_as_uint(x[q].w) & 0x7FFFFFFFu);
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off));
+    constexpr int EMAX = FMT == MXC_E4M3 ? 8 : 2;
+    const uint32_t sc = scale_code_from_bits<EMAX>(m);
+    if (lane == 0) scales[blk] = (uint8_t)sc;
+    const float inv = inv_scale(sc);
+    const bool bad = sc == 0xFFu;
+    if (FMT == MXC_E4M3) {
+        uint32_t* d = (uint32_t*)(codes + (size_t)blk * 1024) + lane;
+#pragma unroll
+        for (int q = 0; q < 4; q++) d[64 * q] = bad ? 0u : pack4_e4m3(x[q], inv);
+    } else {
+        unsigned short* d = (unsigned short*)(codes + (size_t)blk * 512) + lane;
+#pragma unroll
+        for (int q = 0; q < 4; q++) d[64 * q] = bad ? (unsigned short)0 : pack4_e2m1(x[q], inv);
+    }
+}
+
+template <int SRC, int DTYPE, int FMT>
+int launch_qb(const void* src, const Geom& g, void* codes, uint8_t* scales, hipStream_t s) {
+    const long long nb = (long long)g.ng * g.h * g.w * g.ncb;
+    if (nb > 0x7FFFFFFFLL - 4) return MXC_ERR_SHAPE;
+    const int grid = (int)((nb + 3) / 4);
+    hipLaunchKernelGGL((quantize_block_kernel<SRC, DTYPE, FMT>), dim3(grid), dim3(QT), 0, s, src, g,
+                       (uint8_t*)codes, scales, (int)nb);
+    return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
+}
+
 template <int LAYOUT, int DTYPE, int FMT>
 int launch_q(const void* src, const Geom& g, void* codes, uint8_t* scales, hipStream_t s) {
     const int tt = QT / g.bn;
@@ -202,8 +292,22 @@ int launch_q_dt(const void* src, int dtype, const Geom& g, int fmt, void* codes,
 
 }  // namespace
 
-int launch_quantize(const void* src, int dtype, int layout, const Geom& g, int fmt, void* codes,
+int launch_quantize(const void* src, int dtype, int layout, int role, const Geom& g, int fmt, void* codes,
                     uint8_t* scales, hipStream_t s) {
+    // blocks that are contiguous (CBF, Bn = 32) or a small gather (weights): one wave per block
+    const int blocksrc = (layout == MXC_CBF && g.bn == 32) ? 0 : (role == MXC_WEIGHT && layout == MXC_NCHW) ? 1 : -1;
+    if (blocksrc >= 0) {
+#define QB(S, D, F) return launch_qb<S, D, F>(src, g, codes, scales, s)
+        if (blocksrc == 0) {
+            if (dtype == MXC_F32) { if (fmt == MXC_E4M3) QB(0, MXC_F32, MXC_E4M3); QB(0, MXC_F32, MXC_E2M1); }
+            if (fmt == MXC_E4M3) QB(0, MXC_BF16, MXC_E4M3);
+            QB(0, MXC_BF16, MXC_E2M1);
+        }
+        if (dtype == MXC_F32) { if (fmt == MXC_E4M3) QB(1, MXC_F32, MXC_E4M3); QB(1, MXC_F32, MXC_E2M1); }
+        if (fmt == MXC_E4M3) QB(1, MXC_BF16, MXC_E4M3);
+        QB(1, MXC_BF16, MXC_E2M1);
+#undef QB
+    }
     switch (layout) {
         case MXC_NCHW: return launch_q_dt<MXC_NCHW>(src, dtype, g, fmt, codes, scales, s);
         case MXC_NHWC: return launch_q_dt<MXC_NHWC>(src, dtype, g, fmt, codes, scales, s);

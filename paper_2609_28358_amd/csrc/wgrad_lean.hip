@@ -1,0 +1,223 @@
+// wgrad_lean.hip -- a5 for batch block 32: G_Wf = G_Yf X'^T (Sec. II-C,
+// Sec. IV-B), contracted over (output pixel, sample).
+//
+// With Bn = 32 the contraction runs along the samples of a block row, which
+// the CBF layout stores contiguously: a G_Y block is [32 Cout][32 samples]
+// and the X block of a tap's input pixel is [32 Cin][32 samples].  So both
+// MFMA operands are read straight from memory into registers, 16 bytes per
+// lane, with no LDS staging and no transposition: one 32 x 32 x 64 MFMA
+// contracts the 32 samples of two consecutive output pixels (K block 0 =
+// pixel P0, K block 1 = pixel P1), each K block with its own E8M0 scales.
+// Taps that fall into the padding read a zero block.
+//
+// Work split: a tile is 64 Cout x 64 Cin at one tap; each wave of a
+// workgroup accumulates the tile over its own range of pixel pairs, the four
+// waves are summed through LDS, and the workgroup writes one partial tile
+// ([split][Cout_p][tap * Cin_p + ci], reduced by wgrad_reduce) or, with a
+// single split, the final OIHW values.  The next pixel pair's fragments are
+// loaded while the current pair's MFMAs run.
+#include "mx_internal.h"
+
+namespace mxc {
+namespace {
+
+constexpr int WT = 256;
+
+__device__ __attribute__((aligned(16))) uint8_t g_zero_wl[64];
+
+struct WLArgs {
+    const uint8_t* gc;
+    const uint8_t* gs;
+    const uint8_t* xc;
+    const uint8_t* xs;
+    float* dst;
+    int direct;                    // 1: dst is G_W (OIHW); 0: partial tiles
+    int cout, cin, kh, kw, sh, sw, ph, pw, ho, wo, h, w;
+    int gy_ncb, x_ncb, gy_cp, x_cp, ntot;
+    int npix, npairs;              // output pixels (all batch groups), pixel pairs
+    int cot, cit, ntiles;          // 64-row / 64-column tile counts, tiles
+    int ppw;                       // pixel pairs per wave
+};
+
+template <int FMT>
+__global__ __launch_bounds__(WT) void wgrad_lean_kernel(WLArgs p) {
+    constexpr int EB = FMT == MXC_E4M3 ? 8 : 4;
+    constexpr int RB = 32 * EB / 8;               // bytes of one block row (32 samples)
+    constexpr int TB = 32 * RB;                   // bytes of one block
+    __shared__ float red[4][64 * 64];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int tile = blockIdx.x % p.ntiles, split = blockIdx.x / p.ntiles;
+    const int tap = tile / (p.cot * p.cit);
+    const int rc = tile % (p.cot * p.cit);
+    const int cop = rc / p.cit, cip = rc % p.cit;
+    const int th = tap / p.kw, tw = tap % p.kw;
+    const int r = lane & 31, hf = lane >> 5;
+
+    // lane offsets inside one pixel's codes, and block validity
+    uint32_t a_off[2], b_off[2];
+    bool a_ok[2], b_ok[2];
+#pragma unroll
+    for (int i = 0; i < 2; i++) {
+        const int cob = 2 * cop + i, cib = 2 * cip + i;
+        a_ok[i] = cob < p.gy_ncb;
+        b_ok[i] = cib < p.x_ncb;
+        a_off[i] = (uint32_t)(a_ok[i] ? cob : 0) * TB + r * RB + (FMT == MXC_E4M3 ? 16 * hf : 0);
+        b_off[i] = (uint32_t)(b_ok[i] ? cib : 0) * TB + r * RB + (FMT == MXC_E4M3 ? 16 * hf : 0);
+    }
+    const uint32_t gy_pix = (uint32_t)p.gy_ncb * TB, x_pix = (uint32_t)p.x_ncb * TB;
+
+    v16f acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; i++)
+#pragma unroll
+        for (int j = 0; j < 2; j++)
+#pragma unroll
+            for (int e = 0; e < 16; e++) acc[i][j][e] = 0.0f;
+
+    const int wid = split * 4 + wave;
+    const int q0 = wid * p.ppw;
+    const int q1 = min(p.npairs, q0 + p.ppw);
+
+    // operands of pair q (pixels 2q, 2q + 1)
+    struct Ops {
+        v8i a[2], b[2];
+        int sa[2], sb[2];
+    };
+    auto load = [&](int q, Ops& o) {
+        int pg[2];                 // pixel index (or -1) of K block 0 / 1
+        int qpix[2];               // tap's input pixel (or -1)
+#pragma unroll
+        for (int k = 0; k < 2; k++) {
+            const int P = 2 * q + k;
+            pg[k] = P < p.npix ? P : -1;
+            qpix[k] = -1;
+            if (pg[k] >= 0) {
+                const int ox = P % p.wo, t = P / p.wo;
+                const int oy = t % p.ho, g = t / p.ho;
+                const int iy = oy * p.sh + th - p.ph, ix = ox * p.sw + tw - p.pw;
+                if (iy >= 0 && iy < p.h && ix >= 0 && ix < p.w) qpix[k] = (g * p.h + iy) * p.w + ix;
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < 2; i++) {
+            if (FMT == MXC_E4M3) {
+                v4i u[2], v[2];
+#pragma unroll
+                for (int k = 0; k < 2; k++) {
+                    const uint8_t* ap = (pg[k] >= 0 && a_ok[i]) ? p.gc + (size_t)pg[k] * gy_pix + a_off[i] : g_zero_wl;
+                    const uint8_t* bp = (qpix[k] >= 0 && b_ok[i]) ? p.xc + (size_t)qpix[k] * x_pix + b_off[i] : g_zero_wl;
+                    u[k] = *(const v4i*)ap;
+                    v[k] = *(const v4i*)bp;
+                }
+#pragma unroll
+                for (int e = 0; e < 4; e++) {
+                    o.a[i][e] = u[0][e]; o.a[i][4 + e] = u[1][e];
+                    o.b[i][e] = v[0][e]; o.b[i][4 + e] = v[1][e];
+                }
+            } else {
+                const int P = pg[hf], Q = qpix[hf];
+                const uint8_t* ap = (P >= 0 && a_ok[i]) ? p.gc + (size_t)P * gy_pix + a_off[i] : g_zero_wl;
+                const uint8_t* bp = (Q >= 0 && b_ok[i]) ? p.xc + (size_t)Q * x_pix + b_off[i] : g_zero_wl;
+                const v4i u = *(const v4i*)ap, v = *(const v4i*)bp;
+#pragma unroll
+                for (int e = 0; e < 4; e++) {
+                    o.a[i][e] = u[e]; o.a[i][4 + e] = 0;
+                    o.b[i][e] = v[e]; o.b[i][4 + e] = 0;
+                }
+            }
+            // scale of (row, K block hf): the pixel of this lane's half
+            const int P = pg[hf], Q = qpix[hf];
+            const int cob = 2 * cop + i, cib = 2 * cip + i;
+            const uint8_t sa = p.gs[(P >= 0 && a_ok[i]) ? (size_t)P * p.gy_ncb + cob : 0];
+            const uint8_t sb = p.xs[(Q >= 0 && b_ok[i]) ? (size_t)Q * p.x_ncb + cib : 0];
+            o.sa[i] = (P >= 0 && a_ok[i]) ? sa : 0;
+            o.sb[i] = (Q >= 0 && b_ok[i]) ? sb : 0;
+        }
+    };
+
+    if (q0 < q1) {
+        Ops cur, nxt;
+        load(q0, cur);
+        for (int q = q0; q < q1; q++) {
+            if (q + 1 < q1) load(q + 1, nxt);
+#pragma unroll
+            for (int i = 0; i < 2; i++)
+#pragma unroll
+                for (int j = 0; j < 2; j++)
+                    acc[i][j] = mfma_mx<FMT>(cur.a[i], cur.b[j], acc[i][j], cur.sa[i], cur.sb[j]);
+            cur = nxt;
+        }
+    }
+
+    // ---- sum the four waves' tiles, then write
+#pragma unroll
+    for (int i = 0; i < 2; i++)
+#pragma unroll
+        for (int j = 0; j < 2; j++)
+#pragma unroll
+            for (int e = 0; e < 16; e++) {
+                const int row = 32 * i + 8 * (e >> 2) + 4 * hf + (e & 3);
+                red[wave][row * 64 + 32 * j + r] = acc[i][j][e];
+            }
+    __syncthreads();
+#pragma unroll 4
+    for (int k = 0; k < 16; k++) {
+        const int idx = tid + WT * k;
+        const int row = idx >> 6, col = idx & 63;
+        const float v = (red[0][idx] + red[1][idx]) + (red[2][idx] + red[3][idx]);
+        const int co = cop * 64 + row, ci = cip * 64 + col;
+        if (p.direct) {
+            if (co < p.cout && ci < p.cin)
+                p.dst[(((size_t)co * p.cin + ci) * p.kh + th) * p.kw + tw] = v;
+        } else if (co < p.gy_cp && ci < p.x_cp) {
+            p.dst[((size_t)split * p.gy_cp + co) * p.ntot + (size_t)tap * p.x_cp + ci] = v;
+        }
+    }
+}
+
+}  // namespace
+
+// Splits of the lean weight-gradient kernel for this layer, or 0 when it does
+// not apply (batch block below 32).
+int wgrad_lean_splits(const Conv& cv) {
+    if (cv.x.bn != 32) return 0;
+    const long npix = (long)cv.x.ng * cv.ho * cv.wo;
+    const long npairs = (npix + 1) / 2;
+    const long ntiles = (long)cv.kh * cv.kw * ((cv.gy.ncb + 1) / 2) * ((cv.x.ncb + 1) / 2);
+    if (npix > 0x3FFFFFFFL || ntiles > 0x7FFFFFL) return 0;
+    // about two workgroups per CU, each wave with at least 8 pixel pairs
+    long splits = 512 / ntiles;
+    const long cap = npairs / (4 * 8);
+    if (splits > cap) splits = cap;
+    if (splits < 1) splits = 1;
+    return (int)splits;
+}
+
+int launch_wgrad_lean(const Conv& cv, const void* gc, const uint8_t* gs, const void* xc, const uint8_t* xs,
+                      float* dst, int splits, hipStream_t s) {
+    WLArgs a;
+    a.gc = (const uint8_t*)gc; a.gs = gs; a.xc = (const uint8_t*)xc; a.xs = xs;
+    a.dst = dst;
+    a.direct = splits == 1;
+    a.cout = cv.cout; a.cin = cv.cin; a.kh = cv.kh; a.kw = cv.kw; a.sh = cv.sh; a.sw = cv.sw;
+    a.ph = cv.ph; a.pw = cv.pw; a.ho = cv.ho; a.wo = cv.wo; a.h = cv.h; a.w = cv.w;
+    a.gy_ncb = cv.gy.ncb; a.x_ncb = cv.x.ncb; a.gy_cp = cv.gy.cp; a.x_cp = cv.x.cp;
+    a.ntot = cv.kh * cv.kw * cv.x.cp;
+    a.npix = cv.x.ng * cv.ho * cv.wo;
+    a.npairs = (a.npix + 1) / 2;
+    a.cot = (cv.gy.ncb + 1) / 2; a.cit = (cv.x.ncb + 1) / 2;
+    a.ntiles = cv.kh * cv.kw * a.cot * a.cit;
+    const int waves = splits * 4;
+    a.ppw = (a.npairs + waves - 1) / waves;
+    const long grid = (long)a.ntiles * splits;
+    if (grid > 0x7FFFFFFFL) return MXC_ERR_SHAPE;
+    if (cv.fmt == MXC_E4M3)
+        hipLaunchKernelGGL(wgrad_lean_kernel<MXC_E4M3>, dim3((unsigned)grid), dim3(WT), 0, s, a);
+    else
+        hipLaunchKernelGGL(wgrad_lean_kernel<MXC_E2M1>, dim3((unsigned)grid), dim3(WT), 0, s, a);
+    return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
+}
+
+}  // namespace mxc

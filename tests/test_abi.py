@@ -93,10 +93,15 @@ def test_gemm_and_im2col_errors():
         assert fn(r, 0, GOOD, GOOD, GOOD, GOOD, ODD, 2, None) == -4
     assert L.mxconv_im2col_cbf(r, 0, GOOD, None, GOOD, GOOD, None) == -1
     assert L.mxconv_im2col_cbf(r, 0, GOOD, GOOD, ODD, GOOD, None) == -4
-    need = mx.wgrad_workspace_bytes(synth.conv_dict(32, 64, 64, 8, 8, 3, 1, 1), 0)
-    assert L.mxconv_wgrad(r, 0, GOOD, GOOD, GOOD, GOOD, GOOD, None, 0, None) == -6
-    assert L.mxconv_wgrad(r, 0, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, need - 1, None) == -6
-    assert L.mxconv_wgrad(r, 0, GOOD, GOOD, GOOD, GOOD, GOOD, ODD, need, None) == -4
+    # a layer large enough to split the weight-gradient contraction: it needs a
+    # workspace, so these calls must fail validation (never reach a kernel)
+    big = synth.conv_dict(32, 64, 64, 56, 56, 3, 1, 1)
+    rb = ctypes.byref(mx.conv_struct(big))
+    need = mx.wgrad_workspace_bytes(big, 0)
+    assert need > 0
+    assert L.mxconv_wgrad(rb, 0, GOOD, GOOD, GOOD, GOOD, GOOD, None, 0, None) == -6
+    assert L.mxconv_wgrad(rb, 0, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, need - 1, None) == -6
+    assert L.mxconv_wgrad(rb, 0, GOOD, GOOD, GOOD, GOOD, GOOD, ODD, need, None) == -4
     bad = [dict(n=32, cin=64, cout=64, h=8, w=8, kh=3, kw=3, sh=0, sw=1, ph=1, pw=1),
            dict(n=32, cin=64, cout=64, h=8, w=8, kh=3, kw=3, sh=1, sw=1, ph=-1, pw=1)]
     for b in bad:
