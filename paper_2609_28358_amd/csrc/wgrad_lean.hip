@@ -14,8 +14,8 @@
 // workgroup accumulates the tile over its own range of pixel pairs, the four
 // waves are summed through LDS, and the workgroup writes one partial tile
 // ([split][Cout_p][tap * Cin_p + ci], reduced by wgrad_reduce) or, with a
-// single split, the final OIHW values.  The next pixel pair's fragments are
-// loaded while the current pair's MFMAs run.
+// single split, the final OIHW values.  Pixel pairs are processed in
+// batches whose loads are all issued before the first MFMA.
 #include "mx_internal.h"
 
 namespace mxc {
@@ -85,13 +85,13 @@ __global__ __launch_bounds__(WT) void wgrad_lean_kernel(WLArgs p) {
         v8i a[2], b[2];
         int sa[2], sb[2];
     };
-    auto load = [&](int q, Ops& o) {
+    auto load = [&](int q, bool live, Ops& o) {
         int pg[2];                 // pixel index (or -1) of K block 0 / 1
         int qpix[2];               // tap's input pixel (or -1)
 #pragma unroll
         for (int k = 0; k < 2; k++) {
             const int P = 2 * q + k;
-            pg[k] = P < p.npix ? P : -1;
+            pg[k] = live && P < p.npix ? P : -1;
             qpix[k] = -1;
             if (pg[k] >= 0) {
                 const int ox = P % p.wo, t = P / p.wo;
@@ -137,18 +137,21 @@ __global__ __launch_bounds__(WT) void wgrad_lean_kernel(WLArgs p) {
         }
     };
 
-    if (q0 < q1) {
-        Ops cur, nxt;
-        load(q0, cur);
-        for (int q = q0; q < q1; q++) {
-            if (q + 1 < q1) load(q + 1, nxt);
+    // batches of PB pairs: all loads of a batch are in flight together (the
+    // loop is bound by memory latency, not by the MFMAs); pairs past the
+    // wave's range get a zero G_Y operand and add nothing
+    constexpr int PB = 4;
+    for (int q = q0; q < q1; q += PB) {
+        Ops o[PB];
+#pragma unroll
+        for (int b = 0; b < PB; b++) load(q + b, q + b < q1, o[b]);
+#pragma unroll
+        for (int b = 0; b < PB; b++)
 #pragma unroll
             for (int i = 0; i < 2; i++)
 #pragma unroll
                 for (int j = 0; j < 2; j++)
-                    acc[i][j] = mfma_mx<FMT>(cur.a[i], cur.b[j], acc[i][j], cur.sa[i], cur.sb[j]);
-            cur = nxt;
-        }
+                    acc[i][j] = mfma_mx<FMT>(o[b].a[i], o[b].b[j], acc[i][j], o[b].sa[i], o[b].sb[j]);
     }
 
     // ---- sum the four waves' tiles, then write
