@@ -13,11 +13,12 @@ gradients N(0, 1e-3), all seeded.
 `value` is the conv fwd+bwd GEMM throughput of the whole step: the three
 GEMMs' algorithmic flops (2 N Cout Ho Wo Cin Kh Kw each, real channels) over
 the step's wall time, quantize and im2col included.  The timed step is
-replayed from HIP graphs (captured once after warm-up), so it measures GPU
-time, not Python launch cost.  Every op is also timed alone with HIP events
-on the stream it runs on; the op taking the most time per step gets the
-`roofline` object (its time measured again inside the timed region), and all
-ops are listed in `ops`.
+replayed from one HIP graph (captured once after warm-up), so it measures
+GPU time, not Python launch cost.  Every op is also timed alone with HIP
+events on the stream it runs on (behind a GPU spin, so the host's launch
+latency is excluded); the op taking the most time per step gets the
+`roofline` object, its time measured again over K launches right after the
+timed region, and all ops are listed in `ops`.
 
     python bench.py [--steps K] [--warmup W] [--no-cpu-baseline]
 """
@@ -62,6 +63,52 @@ def layer_numbers(cv, fmt, mx):
         "dgrad": (flops, W + G + 4.0 * n * ci * cv["h"] * cv["w"]),
         "wgrad": (flops, G + X + 4.0 * co * ci * kh * kw),
     }
+
+
+PMC_SUMMARY = os.path.join(ROOT, "profiles", "op_traffic_pmc.md")
+COPY_BYTES = 256 << 20                             # calibration copy of the counter pass
+
+
+def source_digest():
+    """Digest of the HIP sources: counter figures taken from an older build
+    no longer describe the kernels and are not reported."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2609_28358_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()[:16]
+
+
+def counter_traffic(op_key):
+    """HBM bytes per launch of `op_key` ("layer/format/op") from the committed
+    counter summary: FETCH_SIZE and WRITE_SIZE (KiB per dispatch, summed over
+    the op's kernels), each scaled by the factor the same counter gives for a
+    copy of known size.  None if there is no summary, the op is missing, or the
+    sources changed since the counters were taken."""
+    if not os.path.exists(PMC_SUMMARY):
+        return None
+    digest, fetch_f, write_f, rows = None, None, None, {}
+    with open(PMC_SUMMARY) as f:
+        for line in f:
+            t = line.strip()
+            if t.startswith("source digest:"):
+                digest = t.split(":", 1)[1].strip().strip("`")
+            elif t.startswith("fetch factor:"):
+                fetch_f = float(t.split(":", 1)[1])
+            elif t.startswith("write factor:"):
+                write_f = float(t.split(":", 1)[1])
+            elif t.startswith("|") and "/" in t:
+                c = [x.strip() for x in t.strip("|").split("|")]
+                try:
+                    rows[c[0]] = (float(c[2]), float(c[3]))
+                except (ValueError, IndexError):
+                    pass
+    if digest != source_digest() or fetch_f is None or write_f is None or op_key not in rows:
+        return None
+    fk, wk = rows[op_key]
+    return round((fk * fetch_f + wk * write_f) * 1024.0)
 
 
 def naive_numbers(cv, fmt, mx):
@@ -186,6 +233,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-naive", action="store_true", help="skip the naive comparator leg")
+    ap.add_argument("--pmc-pass", action="store_true",
+                    help="counter-collection pass: every op once in step order, then a copy of known size")
     ap.add_argument("--layers", default="all", help="comma list of layer indices (profiling aid)")
     ap.add_argument("--fmts", default="0,1")
     args = ap.parse_args()
@@ -268,6 +317,21 @@ def main():
         step()
     torch.cuda.synchronize()
 
+    if args.pmc_pass:
+        # one eager launch per op, separated, then the calibration copy; the
+        # counter summary maps dispatches to ops in this order
+        for j, op in seq:
+            run(j, op)
+            torch.cuda.synchronize()
+        src = torch.empty(COPY_BYTES, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"pmc_pass": [f"{j['name']}/{op}" for j, op in seq], "copy_bytes": COPY_BYTES,
+                          "source_digest": source_digest()}))
+        return
+
     # Per-op GPU time: each op alone, behind a GPU spin so that the event pair
     # brackets the kernel(s) and not the host's launch latency.
     def op_time(j, op, reps=5):
@@ -284,44 +348,27 @@ def main():
 
     op_ms = {(j["name"], op): op_time(j, op) for j, op in seq}
     dom = max(op_ms, key=op_ms.get)
-    di = [(j["name"], op) for j, op in seq].index(dom)
 
-    # The step is launched as HIP graphs (one per stretch: the ops before the
-    # dominant one, the dominant op, the ops after it), so host-side launch
-    # cost does not enter the step time; HIP events recorded between the
-    # graph launches time the dominant op inside the timed region.
-    graphs = []
-    for part in (seq[:di], seq[di:di + 1], seq[di + 1:]):
-        if not part:
-            graphs.append(None)
-            continue
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):
-            for j, op in part:
-                run(j, op)
-        graphs.append(g)
+    # The step is launched as one HIP graph (captured once), so host-side
+    # launch cost does not enter the step time.
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
     for _ in range(2):
-        for g in graphs:
-            if g is not None:
-                g.replay()
+        graph.replay()
     torch.cuda.synchronize()
 
-    marks = []
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        if graphs[0] is not None:
-            graphs[0].replay()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        graphs[1].replay()
-        e1.record(stream)
-        if graphs[2] is not None:
-            graphs[2].replay()
-        marks.append((e0, e1))
+        graph.replay()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_step = (t1 - t0) * 1e3 / args.steps
-    dom_ms = sum(a.elapsed_time(b) for a, b in marks) / len(marks)
+
+    # The dominant op again, K launches on its stream, each bracketed by HIP
+    # events behind a GPU spin: kernel time plus its launch, no host latency.
+    dj = next(j for j, op in seq if (j["name"], op) == dom)
+    dom_ms = op_time(dj, dom[1], reps=args.steps)
 
     naive = {} if args.no_naive else naive_leg(jobs, op_ms, mx, synth, dev, stream)
 
@@ -343,7 +390,8 @@ def main():
 
     jmap = {j["name"]: j for j in jobs}
     rl = roof(jmap[dom[0]], dom[1], dom_ms)
-    rl.update({"kernel": f"{dom[1]} {dom[0]}", "ms": round(dom_ms, 4), "traffic": None})
+    rl.update({"kernel": f"{dom[1]} {dom[0]}", "ms": round(dom_ms, 4),
+               "traffic": counter_traffic(f"{dom[0]}/{dom[1]}")})
     ops = {}
     for (nm, op), ms in op_ms.items():
         fl, by = jmap[nm]["nums"][op]

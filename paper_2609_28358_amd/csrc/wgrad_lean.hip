@@ -37,6 +37,7 @@ struct WLArgs {
     int npix, npairs;              // output pixels (all batch groups), pixel pairs
     int cot, cit, ntiles;          // 64-row / 64-column tile counts, tiles
     int ppw;                       // pixel pairs per wave
+    int nsplit;
 };
 
 template <int FMT>
@@ -48,7 +49,13 @@ __global__ __launch_bounds__(WT) void wgrad_lean_kernel(WLArgs p) {
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int tile = blockIdx.x % p.ntiles, split = blockIdx.x / p.ntiles;
+    // XCD-aware order: workgroups are dealt round-robin to the 8 XCDs; give
+    // each XCD a contiguous range of (split, tile), so the tiles (taps, channel
+    // blocks) that read the same pixels share that XCD's L2
+    const int per_xcd = (gridDim.x + 7) / 8;
+    const int lin = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+    if (lin >= p.ntiles * p.nsplit) return;
+    const int tile = lin % p.ntiles, split = lin / p.ntiles;
     const int tap = tile / (p.cot * p.cit);
     const int rc = tile % (p.cot * p.cit);
     const int cop = rc / p.cit, cip = rc % p.cit;
@@ -214,7 +221,8 @@ int launch_wgrad_lean(const Conv& cv, const void* gc, const uint8_t* gs, const v
     a.ntiles = cv.kh * cv.kw * a.cot * a.cit;
     const int waves = splits * 4;
     a.ppw = (a.npairs + waves - 1) / waves;
-    const long grid = (long)a.ntiles * splits;
+    a.nsplit = splits;
+    const long grid = ((long)a.ntiles * splits + 7) / 8 * 8;
     if (grid > 0x7FFFFFFFL) return MXC_ERR_SHAPE;
     if (cv.fmt == MXC_E4M3)
         hipLaunchKernelGGL(wgrad_lean_kernel<MXC_E4M3>, dim3((unsigned)grid), dim3(WT), 0, s, a);
