@@ -42,6 +42,13 @@ def build(verbose=False):
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr}")
+    # a kernel instantiation the host pass dropped shows up as an undefined
+    # symbol only when the library is loaded: load it here, not on the GPU machine
+    import ctypes
+    try:
+        ctypes.CDLL(tmp)
+    except OSError as e:
+        raise RuntimeError(f"built library does not load: {e}")
     os.replace(tmp, LIB)
     if verbose:
         print("built", LIB)

@@ -583,30 +583,37 @@ __global__ __launch_bounds__(NT) void wgrad_kernel(WgradArgs p) {
 }
 
 // G_W[co][ci][kh][kw] = sum over splits of the partial (co, tap*Cin_p + ci).
-// Four independent partial sums keep several split loads in flight.
+// A workgroup takes 64 consecutive partial columns; its four waves each sum
+// every fourth split (eight loads in flight per lane), and the four sums are
+// added in a fixed order through LDS, so the result does not depend on timing.
 __global__ __launch_bounds__(256) void wgrad_reduce(const float* __restrict__ part, float* __restrict__ gw,
                                                     Conv cv, int ntot, int splits) {
-    const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;   // over (co, tap, ci) real
-    const int taps = cv.kh * cv.kw;
-    const long total = (long)cv.cout * taps * cv.cin;
-    if (i >= total) return;
-    const int ci = (int)(i % cv.cin);
-    const long r = i / cv.cin;
-    const int tap = (int)(r % taps);
-    const int co = (int)(r / taps);
-    const size_t col = (size_t)tap * cv.x.cp + ci;
+    __shared__ float red[4][64];
+    const int lane = threadIdx.x & 63, quarter = threadIdx.x >> 6;
+    const long i = (long)blockIdx.x * 64 + lane;                  // over (co, col) of the partial layout
+    const long total = (long)cv.cout * ntot;
+    const bool live = i < total;
+    const int co = live ? (int)(i / ntot) : 0;
+    const int col = live ? (int)(i % ntot) : 0;
     const size_t stride = (size_t)cv.gy.cp * ntot;
     const float* q = part + (size_t)co * ntot + col;
-    float s0 = 0.0f, s1 = 0.0f, s2 = 0.0f, s3 = 0.0f;
-    int k = 0;
-    for (; k + 4 <= splits; k += 4) {
-        s0 += __ldg(q + (size_t)k * stride);
-        s1 += __ldg(q + (size_t)(k + 1) * stride);
-        s2 += __ldg(q + (size_t)(k + 2) * stride);
-        s3 += __ldg(q + (size_t)(k + 3) * stride);
+    float acc = 0.0f;
+    int k = quarter;
+    for (; k + 28 < splits; k += 32) {
+        float v[8];
+#pragma unroll
+        for (int j = 0; j < 8; j++) v[j] = __ldg(q + (size_t)(k + 4 * j) * stride);
+#pragma unroll
+        for (int j = 0; j < 8; j++) acc += v[j];
     }
-    for (; k < splits; k++) s0 += __ldg(q + (size_t)k * stride);
-    gw[(((size_t)co * cv.cin + ci) * cv.kh + tap / cv.kw) * cv.kw + tap % cv.kw] = (s0 + s1) + (s2 + s3);
+    for (; k < splits; k += 4) acc += __ldg(q + (size_t)k * stride);
+    red[quarter][lane] = acc;
+    __syncthreads();
+    if (quarter != 0 || !live) return;
+    const float sum = (red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane]);
+    const int tap = col / cv.x.cp, ci = col % cv.x.cp;
+    if (ci < cv.cin)
+        gw[(((size_t)co * cv.cin + ci) * cv.kh + tap / cv.kw) * cv.kw + tap % cv.kw] = sum;
 }
 
 struct WgradPlan {
@@ -1294,8 +1301,8 @@ int launch_wgrad(const Conv& cv, const void* gc, const uint8_t* gs, const void* 
     if (ls > 0) {
         const int rc = launch_wgrad_lean(cv, gc, gs, xc, xs, ls > 1 ? (float*)ws : gw, ls, s);
         if (rc || ls == 1) return rc;
-        const long total = (long)cv.cout * cv.kh * cv.kw * cv.cin;
-        hipLaunchKernelGGL(wgrad_reduce, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s,
+        const long cols = (long)cv.cout * cv.kh * cv.kw * cv.x.cp;
+        hipLaunchKernelGGL(wgrad_reduce, dim3((unsigned)((cols + 63) / 64)), dim3(256), 0, s,
                            (const float*)ws, gw, cv, cv.kh * cv.kw * cv.x.cp, ls);
         return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
     }
@@ -1321,8 +1328,8 @@ int launch_wgrad(const Conv& cv, const void* gc, const uint8_t* gs, const void* 
         rc = cv.fmt == MXC_E4M3 ? launch_wgrad_f<MXC_E4M3>(a, grid, s) : launch_wgrad_f<MXC_E2M1>(a, grid, s);
     }
     if (rc) return rc;
-    const long total = (long)cv.cout * cv.kh * cv.kw * cv.cin;
-    hipLaunchKernelGGL(wgrad_reduce, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, (const float*)ws, gw,
+    const long cols = (long)cv.cout * pl.ntot;
+    hipLaunchKernelGGL(wgrad_reduce, dim3((unsigned)((cols + 63) / 64)), dim3(256), 0, s, (const float*)ws, gw,
                        cv, pl.ntot, pl.splits);
     return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
 }

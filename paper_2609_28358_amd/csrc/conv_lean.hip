@@ -13,8 +13,11 @@
 // global_load_lds (16 bytes per lane straight into LDS): each wave
 // instruction moves one 1 KB slice; every lane's source offset is fixed for
 // the tile and a stage adds one uniform delta; padding taps and missing
-// blocks read a zero block through a select, not a branch.  Stages are
-// double-buffered: the next stage streams in while the current one computes.
+// blocks read a zero block through a select, not a branch.  The E8M0
+// scales of a stage stream the same way, one byte per lane.  Stages rotate
+// through a ring of 2 to 4 LDS buffers: while one stage computes, the next
+// ones stream in (the host picks the ring depth from the LDS left per
+// workgroup at the layer's occupancy).
 // The fragments of each source pixel are read from LDS once per stage and
 // reused by every tap that reaches it.  The MFMAs compute the transposed
 // tile (samples x channels) so that each lane ends up holding four
@@ -28,11 +31,11 @@ constexpr int LT = 256;
 
 __device__ __attribute__((aligned(16))) uint8_t g_zero_lean[1024];
 
-typedef __attribute__((address_space(3))) void lds_void_t;
-
-__device__ __forceinline__ void dma16(const void* gsrc, uint8_t* lds_base) {
-    __builtin_amdgcn_global_load_lds(gsrc, (lds_void_t*)lds_base, 16, 0, 0);
-}
+// LDS of one stage: NQ 4 KB groups of DMA slices (weight blocks, then halo
+// blocks), then 1 KB of scale entries (entry e at byte 4 e: one dword per
+// lane of the one-byte copies).
+constexpr int SCALE_REGION = 1024;
+constexpr int LDS_MAX = 160 * 1024;       // LDS of one CU
 
 struct LeanArgs {
     const uint8_t* wc;        // weight codes / scales
@@ -54,6 +57,7 @@ struct LeanArgs {
     int x_ncb;                // source scale blocks per pixel
     int ntiles;
     int stage_bytes, a_bytes, b_bytes, nq;
+    int nbuf;                 // ring depth, 2..4
 };
 
 template <int FMT, bool DG, int KW, int S, int WGM>
@@ -72,6 +76,7 @@ __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
     constexpr int NSA = KW * 2 * RBW;               // weight scales per stage
     constexpr int NSB = 2 * HP;                     // activation scales per stage
     static_assert(NSA + NSB <= LT, "scale staging needs one thread per scale");
+    static_assert(2 * (NQ + 1) <= 63, "two stages in flight must fit the vmcnt counter");
     static_assert(!DG || S == 1, "the gather form of dgrad is stride 1 here");
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 
@@ -126,7 +131,8 @@ __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
             flg[q] = (ok ? 1u : 0u) | (uint32_t)kb << 1 | 4u;
         }
     }
-    // scale staging: threads [0, NSA) weight scales [t][kb][rb], [NSA, NSA+NSB) halo scales [kb][hc]
+    // scale entries: thread e copies entry e; [0, NSA) weight scales
+    // [t][kb][rb], [NSA, NSA+NSB) halo scales [kb][hc], the rest zero
     uint32_t s_off = 0, s_flg = 0;
     if (tid < NSA) {
         const int rb = tid % RBW, kb = (tid / RBW) & 1, t = tid / (2 * RBW);
@@ -145,9 +151,9 @@ __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
     const int nkk = (p.kcb + 1) / 2;
     const int nstage = p.kh * nkk;
     const uint8_t* const zero = g_zero_lean;
-    uint32_t sreg = 0;
 
-    // stage st = (kernel row kh, K pair kk): issue its loads into buffer buf
+    // stage st = (kernel row kh, K pair kk): issue its copies into buffer
+    // buf.  Every wave issues exactly NQ + 1 copies per stage.
     auto issue = [&](int st, int buf) {
         const int kk = st % nkk, kh = st / nkk;
         const int sy = DG ? y + p.ph - kh : y * p.sh + kh - p.ph;
@@ -156,28 +162,21 @@ __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
         const uint8_t* abase = p.wc + (DG ? (uint32_t)(2 * kk) * w_cob : (uint32_t)(2 * kk) * TB) +
                                (uint32_t)kh * KW * w_tap;
         const uint8_t* bbase = p.sc + ((uint32_t)g * p.hsrc + (row_ok ? sy : 0)) * x_row + (uint32_t)(2 * kk) * TB;
-        uint8_t* lds = smem + buf * p.stage_bytes;
+        const uint8_t* lds = smem + buf * p.stage_bytes;
 #pragma unroll
         for (int q = 0; q < NQ; q++) {
             const uint32_t f = flg[q];
             const bool isb = f & 4u;
             const bool ok = (f & 1u) && (!(f & 2u) || kb1_ok) && (!isb || row_ok);
             const uint8_t* src = (isb ? bbase : abase) + off[q];
-            dma16(ok ? src : zero + (off[q] & (TB - 1)), lds + (4 * q + wave) * 1024);
+            dma16_async(ok ? src : zero + (off[q] & (TB - 1)), lds_addr(lds + (4 * q + wave) * 1024));
         }
-        sreg = 0;
-        if (s_flg & 8u) {
-            const bool isb = s_flg & 4u;
-            const bool ok = (s_flg & 1u) && (!(s_flg & 2u) || kb1_ok) && (!isb || row_ok);
-            const uint32_t o = isb ? s_off + ((uint32_t)g * p.hsrc + (row_ok ? sy : 0)) * p.wsrc * p.x_ncb + 2 * kk
-                                   : s_off + (uint32_t)kh * KW * p.w_ncb +
-                                         (DG ? (uint32_t)(2 * kk) * p.kh * KW * p.w_ncb : (uint32_t)(2 * kk));
-            const uint8_t v = (isb ? p.ss : p.ws)[ok ? o : 0u];   // index 0 is always in bounds
-            sreg = ok ? v : 0u;
-        }
-    };
-    auto store_scales = [&](int buf) {
-        if (s_flg & 8u) smem[buf * p.stage_bytes + p.a_bytes + p.b_bytes + tid] = (uint8_t)sreg;
+        const bool isb = s_flg & 4u;
+        const bool ok = (s_flg & 8u) && (s_flg & 1u) && (!(s_flg & 2u) || kb1_ok) && (!isb || row_ok);
+        const uint32_t o = isb ? s_off + ((uint32_t)g * p.hsrc + (row_ok ? sy : 0)) * p.wsrc * p.x_ncb + 2 * kk
+                               : s_off + (uint32_t)kh * KW * p.w_ncb +
+                                     (DG ? (uint32_t)(2 * kk) * p.kh * KW * p.w_ncb : (uint32_t)(2 * kk));
+        dma1_async(ok ? (isb ? p.ss : p.ws) + o : zero, lds_addr(lds + p.nq * 4096 + wave * 256));
     };
 
     // ---- wave geometry and per-lane fragment offsets
@@ -198,18 +197,20 @@ __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
 #pragma unroll
             for (int e = 0; e < 16; e++) acc[i][j][e] = 0.0f;
 
-    if (nstage > 0) {
-        issue(0, 0);
-        __builtin_amdgcn_s_waitcnt(0x0F70);
-        store_scales(0);
-    }
-    __syncthreads();
+    // ring of nbuf buffers: stages st + 1 .. st + nbuf - 2 are in flight
+    // while stage st computes; the barrier after the wait both publishes
+    // stage st and frees the buffer of stage st - 1 for the next copy
+    const int nbuf = p.nbuf;
+    for (int j = 0; j < nbuf - 1 && j < nstage; j++) issue(j, j);
+    int buf = 0;
     for (int st = 0; st < nstage; st++) {
-        const int buf = st & 1;
-        if (st + 1 < nstage) issue(st + 1, buf ^ 1);
+        vm_wait_stage<NQ + 1>(min(nbuf - 2, nstage - 1 - st));
+        __syncthreads();
+        if (st + nbuf - 1 < nstage) issue(st + nbuf - 1, buf == 0 ? nbuf - 1 : buf - 1);
         const uint8_t* A = smem + buf * p.stage_bytes;
         const uint8_t* B = A + p.a_bytes;
-        const uint8_t* SC = B + p.b_bytes;
+        const uint8_t* SC = A + p.nq * 4096;
+        buf = buf + 1 == nbuf ? 0 : buf + 1;
 
         // fragments of the wave's ND halo pixels (both K halves)
         v8i bf[ND];
@@ -237,7 +238,7 @@ __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
                 }
                 bf[d][4] = bf[d][5] = bf[d][6] = bf[d][7] = 0;
             }
-            sb[d] = SC[NSA + h * HP + hc];
+            sb[d] = SC[4 * (NSA + h * HP + hc)];
         }
 #pragma unroll
         for (int t = 0; t < KW; t++) {
@@ -280,7 +281,7 @@ __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
                         af[rb][4] = af[rb][5] = af[rb][6] = af[rb][7] = 0;
                     }
                 }
-                sa[rb] = SC[(t * 2 + h) * RBW + rbi];
+                sa[rb] = SC[4 * ((t * 2 + h) * RBW + rbi)];
             }
 #pragma unroll
             for (int cn = 0; cn < 2; cn++) {
@@ -290,18 +291,19 @@ __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
                     acc[rb][cn] = mfma_mx<FMT>(bf[d], af[rb], acc[rb][cn], sb[d], sa[rb]);
             }
         }
-        if (st + 1 < nstage) {
-            __builtin_amdgcn_s_waitcnt(0x0F70);     // this wave's loads of the next stage have landed
-            store_scales(buf ^ 1);
-        }
-        __syncthreads();
     }
 
     // ---- epilogue.  The tile was computed transposed: in acc[rb][cn] lane l
     // holds output channel 32 rb + l % 32 of the wave's 64, and samples
     // 8 (e / 4) + 4 (l / 32) + e % 4 -- four consecutive samples per group of
-    // 4 registers, i.e. one 16-byte run of the CBF output.
+    // 4 registers.  In the CBF output the 32 channels of one (rb, cn) are one
+    // contiguous 4 KB run, so each wave passes them through 4 KB of LDS
+    // (16-byte chunks XOR-swizzled by row against bank conflicts) and writes
+    // them back as four fully contiguous 1 KB stores.
     const int m = mt * 64 * WGM + 64 * wm + (lane & 31);
+    if (p.layout == MXC_CBF) __syncthreads();           // every wave is done with the stage buffers
+    uint8_t* const ep = smem + wave * 4096;
+    const int er = lane >> 3, ec = lane & 7;            // read-back: row er + 8 i, chunk ec
 #pragma unroll
     for (int cn = 0; cn < 2; cn++) {
         const int x = x0 + 2 * wn + cn;
@@ -310,13 +312,21 @@ __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
             float* px = p.out + (((size_t)g * p.hout + y) * p.wout + x) * p.M * 32;
 #pragma unroll
             for (int rb = 0; rb < 2; rb++) {
-                const int mm = m + 32 * rb;
-                if (mm >= p.M) continue;
-                float* o = px + (size_t)mm * 32 + 4 * h;
+                const int m0 = mt * 64 * WGM + 64 * wm + 32 * rb;
+                if (m0 >= p.M) continue;
+                const int r = lane & 31;
 #pragma unroll
                 for (int e4 = 0; e4 < 4; e4++)
-                    *(float4*)(o + 8 * e4) = make_float4(acc[rb][cn][4 * e4], acc[rb][cn][4 * e4 + 1],
-                                                         acc[rb][cn][4 * e4 + 2], acc[rb][cn][4 * e4 + 3]);
+                    *(float4*)(ep + r * 128 + (((2 * e4 + h) ^ (r & 7)) << 4)) =
+                        make_float4(acc[rb][cn][4 * e4], acc[rb][cn][4 * e4 + 1],
+                                    acc[rb][cn][4 * e4 + 2], acc[rb][cn][4 * e4 + 3]);
+                float* o = px + (size_t)m0 * 32;
+#pragma unroll
+                for (int i = 0; i < 4; i++) {
+                    const int row = er + 8 * i;
+                    const float4 v = *(const float4*)(ep + row * 128 + ((ec ^ (row & 7)) << 4));
+                    if (m0 + row < p.M) *(float4*)(o + row * 32 + 4 * ec) = v;
+                }
             }
         } else {
             const size_t hw = (size_t)p.hout * p.wout;
@@ -336,12 +346,14 @@ __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
 }
 
 template <int FMT, bool DG, int KW, int S, int WGM>
-int launch_lean_t(const LeanArgs& a, hipStream_t s) {
-    const size_t lds = 2 * (size_t)a.stage_bytes;
+int launch_lean_t(const LeanArgs& a, int nbufs_used, hipStream_t s) {
+    // the stage ring, and at least the 4 x 4 KB the epilogue stages through
+    size_t lds = (size_t)nbufs_used * a.stage_bytes;
+    if (lds < 4 * 4096) lds = 4 * 4096;
     static bool attr = false;
     if (lds > 65536 && !attr) {
         if (hipFuncSetAttribute((const void*)conv_lean_kernel<FMT, DG, KW, S, WGM>,
-                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+                                hipFuncAttributeMaxDynamicSharedMemorySize, LDS_MAX) != hipSuccess)
             return MXC_ERR_HIP;
         attr = true;
     }
@@ -351,20 +363,20 @@ int launch_lean_t(const LeanArgs& a, hipStream_t s) {
 }
 
 template <int FMT, bool DG, int KW, int S>
-int launch_lean_w(const LeanArgs& a, int wgm, hipStream_t s) {
-    if (wgm == 4) return launch_lean_t<FMT, DG, KW, S, 4>(a, s);
-    if (wgm == 2) return launch_lean_t<FMT, DG, KW, S, 2>(a, s);
-    return launch_lean_t<FMT, DG, KW, S, 1>(a, s);
+int launch_lean_w(const LeanArgs& a, int wgm, int nb, hipStream_t s) {
+    if (wgm == 4) return launch_lean_t<FMT, DG, KW, S, 4>(a, nb, s);
+    if (wgm == 2) return launch_lean_t<FMT, DG, KW, S, 2>(a, nb, s);
+    return launch_lean_t<FMT, DG, KW, S, 1>(a, nb, s);
 }
 
 template <int FMT, bool DG>
-int launch_lean_f(const LeanArgs& a, int kw, int sw, int wgm, hipStream_t s) {
+int launch_lean_f(const LeanArgs& a, int kw, int sw, int wgm, int nb, hipStream_t s) {
     if constexpr (DG) {
         (void)sw;
-        return kw == 3 ? launch_lean_w<FMT, DG, 3, 1>(a, wgm, s) : launch_lean_w<FMT, DG, 1, 1>(a, wgm, s);
+        return kw == 3 ? launch_lean_w<FMT, DG, 3, 1>(a, wgm, nb, s) : launch_lean_w<FMT, DG, 1, 1>(a, wgm, nb, s);
     } else {
-        if (kw == 3) return sw == 2 ? launch_lean_w<FMT, DG, 3, 2>(a, wgm, s) : launch_lean_w<FMT, DG, 3, 1>(a, wgm, s);
-        return sw == 2 ? launch_lean_w<FMT, DG, 1, 2>(a, wgm, s) : launch_lean_w<FMT, DG, 1, 1>(a, wgm, s);
+        if (kw == 3) return sw == 2 ? launch_lean_w<FMT, DG, 3, 2>(a, wgm, nb, s) : launch_lean_w<FMT, DG, 3, 1>(a, wgm, nb, s);
+        return sw == 2 ? launch_lean_w<FMT, DG, 1, 2>(a, wgm, nb, s) : launch_lean_w<FMT, DG, 1, 1>(a, wgm, nb, s);
     }
 }
 
@@ -391,9 +403,11 @@ int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws,
     a.w_cp = cv.wt.cp; a.w_ncb = cv.wt.ncb; a.w_nco = cv.wt.np / 32;
     a.x_ncb = src.ncb;
     if (dg && a.w_nco != src.ncb) return 1;
-    // rows per tile: as many 64-row groups as the output channels fill, up to 4
+    // rows per tile: the choice that streams the fewest bytes per stage for
+    // the same 48 MFMAs -- 64 rows x 8 pixels at column stride 1; at stride 2
+    // the halo of 8 pixels is wide, 128 rows x 4 pixels is cheaper
     const int mp = (a.M + 63) / 64;
-    const int wgm = mp >= 4 ? 4 : (mp >= 2 ? 2 : 1);
+    const int wgm = (!dg && cv.sw == 2 && mp >= 2) ? 2 : 1;
     const int px = 8 / wgm;
     a.mtiles = (a.M + 64 * wgm - 1) / (64 * wgm);
     a.nseg = (a.wout + px - 1) / px;
@@ -407,18 +421,26 @@ int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws,
     a.nq = (na + nb + 4 * bpi - 1) / (4 * bpi);
     a.a_bytes = na * tb;
     a.b_bytes = nb * tb;
-    // DMA slices cover nq * 4 KB; scales follow the blocks
+    // DMA slices cover nq * 4 KB; the scale entries follow
     const int blocks_bytes = a.nq * 4096;
-    a.stage_bytes = blocks_bytes + 256;
     if (a.a_bytes + a.b_bytes > blocks_bytes) return MXC_ERR_HIP;
-    // scales sit right after the blocks region
     a.b_bytes = blocks_bytes - a.a_bytes;
-    if (2 * (size_t)a.stage_bytes > 160 * 1024) return 1;
+    a.stage_bytes = blocks_bytes + SCALE_REGION;
+    const int nstage = cv.kh * ((a.kcb + 1) / 2);
+    if (2 * a.stage_bytes > LDS_MAX || nstage < 1) return 1;
+    // ring depth: the workgroups that share a CU at this grid size split its
+    // LDS; each takes as many stage buffers (2..4) as fit in its share
+    const int per_cu = (int)((nt + 255) / 256);
+    int nbuf = 2;
+    for (int b = 4; b > 2; b--)
+        if ((long)per_cu * b * a.stage_bytes <= LDS_MAX) { nbuf = b; break; }
+    a.nbuf = nbuf;
+    const int used = nbuf < nstage ? nbuf : nstage;
     if (cv.fmt == MXC_E4M3)
-        return dg ? launch_lean_f<MXC_E4M3, true>(a, cv.kw, cv.sw, wgm, s)
-                  : launch_lean_f<MXC_E4M3, false>(a, cv.kw, cv.sw, wgm, s);
-    return dg ? launch_lean_f<MXC_E2M1, true>(a, cv.kw, cv.sw, wgm, s)
-              : launch_lean_f<MXC_E2M1, false>(a, cv.kw, cv.sw, wgm, s);
+        return dg ? launch_lean_f<MXC_E4M3, true>(a, cv.kw, cv.sw, wgm, used, s)
+                  : launch_lean_f<MXC_E4M3, false>(a, cv.kw, cv.sw, wgm, used, s);
+    return dg ? launch_lean_f<MXC_E2M1, true>(a, cv.kw, cv.sw, wgm, used, s)
+              : launch_lean_f<MXC_E2M1, false>(a, cv.kw, cv.sw, wgm, used, s);
 }
 
 }  // namespace mxc

@@ -158,6 +158,40 @@ __device__ __forceinline__ v16f mfma_mx(v8i a, v8i b, v16f c, int sa, int sb) {
                                                            FMT == MXC_E4M3 ? 0 : 4, 0, sa, 0, sb);
 }
 
+// Asynchronous global -> LDS copies (global_load_lds).  Every lane supplies
+// its own source address; the LDS destination is the wave-uniform base in M0
+// plus 16 * lane for the 16-byte form, plus 4 * lane for the one-byte form
+// (the byte is zero-extended to the lane's dword).  They are issued as inline
+// assembly, so the compiler does not track them: left to itself it waits for
+// every outstanding copy before any LDS read, which serialises a multi-stage
+// pipeline.  The caller waits with vm_wait<N>() -- N = the vector-memory
+// operations of this wave that may still be in flight, counted in issue
+// order -- before the barrier that publishes the data to the other waves.
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
+
+__device__ __forceinline__ uint32_t lds_addr(const uint8_t* p) {
+    return (uint32_t)(uintptr_t)(const lds_u8*)p;
+}
+__device__ __forceinline__ void dma16_async(const void* gsrc, uint32_t lds) {
+    asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(gsrc), "{m0}"(lds) : "memory");
+}
+__device__ __forceinline__ void dma1_async(const void* gsrc, uint32_t lds) {
+    asm volatile("global_load_lds_ubyte %0, off" ::"v"(gsrc), "{m0}"(lds) : "memory");
+}
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+    static_assert(N >= 0 && N <= 63, "vmcnt holds 6 bits");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+// Wait for a stage when `later` stages of PER operations each were issued
+// after it (later in 0..2).
+template <int PER>
+__device__ __forceinline__ void vm_wait_stage(int later) {
+    if (later <= 0) vm_wait<0>();
+    else if (later == 1) vm_wait<PER>();
+    else vm_wait<2 * PER>();
+}
+
 // LDS transposing reads (16-lane groups).
 //  tr8: lane i gets byte (i%8) of the 8-byte chunks addressed by lanes 2q + i/8, q = 0..7.
 //  tr4: lane i gets nibble i of the chunks addressed by lanes q, q = 0..15.
