@@ -1,7 +1,16 @@
 // conv_lean.hip -- a3 / a4 for the common layer shapes: forward (Sec. II-C,
-// Y_f = W_f X') and stride-1 input gradient (G_X' = W_f^T G_Yf folded back by
-// col2im, computed as a gather) on MX-CBF operands with a batch block of 32,
-// kernel width 1 or 3 and column stride 1 or 2 (forward; any row stride).
+// Y_f = W_f X') and input gradient (G_X' = W_f^T G_Yf folded back by col2im,
+// computed as a gather) on MX-CBF operands with a batch block of 32, kernel
+// width 1 or 3; forward with column stride 1 or 2 (any row stride), input
+// gradient with stride 1 or 2 x 2.
+//
+// Stride-2 input gradient: the output pixels split into four phases (row
+// parity ry, column parity rx).  A phase only meets the taps whose offset has
+// its parity, kh = kh0 + 2 i and kw = kw0 + 2 j, and its pixel (ry + 2 yi,
+// rx + 2 xi) reads G_Y at row yi + (ry + ph - kh) / 2 and column
+// xi + (rx + pw - kw) / 2: on the phase's own pixel grid that is a stride-1
+// gather with ceil((K - k0) / 2) taps per dimension, which is the stride-1
+// kernel with a smaller kernel.  One launch covers the four phases.
 //
 // One workgroup (4 waves) computes a tile of BM = 64*WGM output channels x
 // PX = 8/WGM output pixels of one output row x 32 samples; each wave owns
@@ -45,7 +54,7 @@ struct LeanArgs {
     float* out;
     int layout;
     int M;                    // real output channels
-    int mtiles, nseg;         // row tiles, pixel segments per output row
+    int mtiles;               // row tiles
     int hout, wout;           // output spatial size
     int hsrc, wsrc;           // source spatial size
     int kh, sh, ph, pw;       // kernel rows, row stride, padding
@@ -56,48 +65,64 @@ struct LeanArgs {
     int w_nco;                // weight Cout_p / 32
     int x_ncb;                // source scale blocks per pixel
     int ntiles;
-    int stage_bytes, a_bytes, b_bytes, nq;
+    int stage_bytes;          // bytes between stage buffers
     int nbuf;                 // ring depth, 2..4
+    int kwf;                  // full kernel width
+    int pofs[5];              // stride-2 input gradient: first tile of each phase (ry, rx) = 00, 01, 10, 11
 };
 
+// Taps and output pixel grid of one phase; the stride-1 kernels use the
+// trivial phase (every tap, every pixel).
+struct Phase {
+    int ry, rx;               // output row / column parity
+    int kh0, nvh;             // first kernel row, kernel rows
+    int kw0;                  // first kernel column
+    int gh, gw;               // output rows / columns of the phase
+    int c0;                   // G_Y column of phase column 0 for kernel column kw0
+    int r0;                   // G_Y row of phase row 0 for kernel row kh0
+};
+
+// One tile.  DG with S = 2 is a phase of the stride-2 input gradient and KW
+// its taps per row (the halo is then a stride-1 one on the phase grid).
 template <int FMT, bool DG, int KW, int S, int WGM>
-__global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
+__device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phase& f) {
     constexpr int EB = FMT == MXC_E4M3 ? 8 : 4;
     constexpr int TB = 32 * 32 * EB / 8;            // bytes of one stored block (weights and activations)
     constexpr int RB = 32 * EB / 8;                 // bytes of one channel row of an activation block
     constexpr int RBW = 2 * WGM;                    // 32-row blocks per tile
     constexpr int PX = 8 / WGM;                     // output pixels per tile
-    constexpr int HP = DG ? PX + KW - 1 : (PX - 1) * S + KW;   // halo pixels
+    constexpr int CS = DG ? 1 : S;                  // halo columns per output pixel step
+    constexpr int DS = DG ? S : 1;                  // tap step of a phase (stride-2 input gradient)
+    constexpr int HP = (PX - 1) * CS + KW;          // halo pixels
     constexpr int NA = KW * 2 * RBW;                // weight blocks per stage
     constexpr int NB = 2 * HP;                      // activation blocks per stage
     constexpr int BPI = 1024 / TB;                  // blocks per wave instruction
     constexpr int NQ = (NA + NB + 4 * BPI - 1) / (4 * BPI);   // DMA instructions per thread per stage
-    constexpr int ND = S + KW;                      // distinct halo pixels of a wave (2 pixels)
+    constexpr int ND = CS + KW;                     // distinct halo pixels of a wave (2 pixels)
     constexpr int NSA = KW * 2 * RBW;               // weight scales per stage
     constexpr int NSB = 2 * HP;                     // activation scales per stage
     static_assert(NSA + NSB <= LT, "scale staging needs one thread per scale");
     static_assert(2 * (NQ + 1) <= 63, "two stages in flight must fit the vmcnt counter");
-    static_assert(!DG || S == 1, "the gather form of dgrad is stride 1 here");
+    static_assert(S == 1 || S == 2, "stride 1 or 2");
+    constexpr int A_BYTES = NA * TB;
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
-    // ---- tile (XCD-aware: consecutive tiles -- same output row -- on one XCD)
-    const int per_xcd = (gridDim.x + 7) / 8;
-    const int lin = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-    if (lin >= p.ntiles) return;
+    // ---- tile: (row tile, pixel segment, output row of the phase, group)
+    const int nseg = (f.gw + PX - 1) / PX;
     const int mt = lin % p.mtiles;
     int r = lin / p.mtiles;
-    const int seg = r % p.nseg;
-    r /= p.nseg;
-    const int y = r % p.hout, g = r / p.hout;
-    const int x0 = seg * PX;
-    const int cbase = DG ? x0 + p.pw - (KW - 1) : x0 * S - p.pw;   // first halo column
+    const int seg = r % nseg;
+    r /= nseg;
+    const int yi = r % f.gh, g = r / f.gh;
+    const int x0 = seg * PX;                                       // first pixel on the phase grid
+    const int cbase = DG ? x0 + f.c0 - (KW - 1) : x0 * S - p.pw;   // first halo column
 
     // ---- strides (bytes)
     const uint32_t w_tap = (uint32_t)p.w_cp * RB;                  // one tap of one 32-Cout block
-    const uint32_t w_cob = (uint32_t)p.kh * KW * w_tap;            // one 32-Cout block
+    const uint32_t w_cob = (uint32_t)p.kh * p.kwf * w_tap;         // one 32-Cout block
     const uint32_t x_pix = (uint32_t)p.kcb * TB;                   // one source pixel
     const uint32_t x_row = (uint32_t)p.wsrc * x_pix;
 
@@ -117,7 +142,7 @@ __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
             const int rb = blk % RBW, kb = (blk / RBW) & 1, t = blk / (2 * RBW);
             const int rowblk = mt * RBW + rb;
             if (DG) {   // rows = input channels (block rowblk of Cin_p), K = output channels
-                off[q] += (uint32_t)kb * w_cob + (uint32_t)t * w_tap + (uint32_t)rowblk * TB;
+                off[q] += (uint32_t)kb * w_cob + (uint32_t)(f.kw0 + DS * t) * w_tap + (uint32_t)rowblk * TB;
             } else {    // rows = output channels (32-Cout block rowblk), K = input channels
                 off[q] += (uint32_t)rowblk * w_cob + (uint32_t)t * w_tap + (uint32_t)kb * TB;
             }
@@ -137,8 +162,8 @@ __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
     if (tid < NSA) {
         const int rb = tid % RBW, kb = (tid / RBW) & 1, t = tid / (2 * RBW);
         const int rowblk = mt * RBW + rb;
-        if (DG) s_off = ((uint32_t)kb * p.kh * KW + t) * p.w_ncb + rowblk;
-        else    s_off = ((uint32_t)rowblk * p.kh * KW + t) * p.w_ncb + kb;
+        if (DG) s_off = ((uint32_t)kb * p.kh * p.kwf + f.kw0 + DS * t) * p.w_ncb + rowblk;
+        else    s_off = ((uint32_t)rowblk * p.kh * p.kwf + t) * p.w_ncb + kb;
         s_flg = (rowblk < p.w_rowblocks ? 1u : 0u) | (uint32_t)kb << 1 | 8u;
     } else if (tid < NSA + NSB) {
         const int q = tid - NSA, kb = q / HP, hc = q % HP;
@@ -149,18 +174,25 @@ __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
     }
 
     const int nkk = (p.kcb + 1) / 2;
-    const int nstage = p.kh * nkk;
+    const int nstage = f.nvh * nkk;
     const uint8_t* const zero = g_zero_lean;
+    // both scale tensors in scalar registers: a per-lane choice between the
+    // two argument fields would otherwise be made by a vector load from the
+    // argument block, whose wait would also drain every copy in flight
+    const uint8_t* wsp = p.ws;
+    const uint8_t* ssp = p.ss;
+    asm("" : "+s"(wsp), "+s"(ssp));
 
     // stage st = (kernel row kh, K pair kk): issue its copies into buffer
     // buf.  Every wave issues exactly NQ + 1 copies per stage.
     auto issue = [&](int st, int buf) {
-        const int kk = st % nkk, kh = st / nkk;
-        const int sy = DG ? y + p.ph - kh : y * p.sh + kh - p.ph;
+        const int kk = st % nkk, ki = st / nkk;
+        const int kh = f.kh0 + DS * ki;
+        const int sy = DG ? yi + f.r0 - ki : yi * p.sh + kh - p.ph;
         const bool row_ok = sy >= 0 && sy < p.hsrc;
         const bool kb1_ok = 2 * kk + 1 < p.kcb;
         const uint8_t* abase = p.wc + (DG ? (uint32_t)(2 * kk) * w_cob : (uint32_t)(2 * kk) * TB) +
-                               (uint32_t)kh * KW * w_tap;
+                               (uint32_t)kh * p.kwf * w_tap;
         const uint8_t* bbase = p.sc + ((uint32_t)g * p.hsrc + (row_ok ? sy : 0)) * x_row + (uint32_t)(2 * kk) * TB;
         const uint8_t* lds = smem + buf * p.stage_bytes;
 #pragma unroll
@@ -174,9 +206,9 @@ __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
         const bool isb = s_flg & 4u;
         const bool ok = (s_flg & 8u) && (s_flg & 1u) && (!(s_flg & 2u) || kb1_ok) && (!isb || row_ok);
         const uint32_t o = isb ? s_off + ((uint32_t)g * p.hsrc + (row_ok ? sy : 0)) * p.wsrc * p.x_ncb + 2 * kk
-                               : s_off + (uint32_t)kh * KW * p.w_ncb +
-                                     (DG ? (uint32_t)(2 * kk) * p.kh * KW * p.w_ncb : (uint32_t)(2 * kk));
-        dma1_async(ok ? (isb ? p.ss : p.ws) + o : zero, lds_addr(lds + p.nq * 4096 + wave * 256));
+                               : s_off + (uint32_t)kh * p.kwf * p.w_ncb +
+                                     (DG ? (uint32_t)(2 * kk) * p.kh * p.kwf * p.w_ncb : (uint32_t)(2 * kk));
+        dma1_async(ok ? (isb ? ssp : wsp) + o : zero, lds_addr(lds + NQ * 4096 + wave * 256));
     };
 
     // ---- wave geometry and per-lane fragment offsets
@@ -187,7 +219,7 @@ __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
     else    a_lane = FMT == MXC_E4M3 ? (16 * hh + (i16 >> 1)) * 32 + 16 * cg + 8 * (i16 & 1) : i16 * 16 + 8 * cg;
     const int b_lane = FMT == MXC_E4M3 ? (16 * hh + (i16 >> 1)) * RB + 16 * cg + 8 * (i16 & 1)
                                        : i16 * RB + 8 * cg;
-    const int hbase = DG ? 2 * wn : 2 * wn * S;       // first halo pixel of the wave
+    const int hbase = 2 * wn * CS;                    // first halo pixel of the wave
 
     v16f acc[2][2];
 #pragma unroll
@@ -208,8 +240,8 @@ __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
         __syncthreads();
         if (st + nbuf - 1 < nstage) issue(st + nbuf - 1, buf == 0 ? nbuf - 1 : buf - 1);
         const uint8_t* A = smem + buf * p.stage_bytes;
-        const uint8_t* B = A + p.a_bytes;
-        const uint8_t* SC = A + p.nq * 4096;
+        const uint8_t* B = A + A_BYTES;
+        const uint8_t* SC = A + NQ * 4096;
         buf = buf + 1 == nbuf ? 0 : buf + 1;
 
         // fragments of the wave's ND halo pixels (both K halves)
@@ -285,7 +317,7 @@ __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
             }
 #pragma unroll
             for (int cn = 0; cn < 2; cn++) {
-                const int d = DG ? cn + (KW - 1 - t) : cn * S + t;
+                const int d = DG ? cn + (KW - 1 - t) : cn * CS + t;
 #pragma unroll
                 for (int rb = 0; rb < 2; rb++)   // transposed product: rows = samples, columns = channels
                     acc[rb][cn] = mfma_mx<FMT>(bf[d], af[rb], acc[rb][cn], sb[d], sa[rb]);
@@ -304,10 +336,12 @@ __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
     if (p.layout == MXC_CBF) __syncthreads();           // every wave is done with the stage buffers
     uint8_t* const ep = smem + wave * 4096;
     const int er = lane >> 3, ec = lane & 7;            // read-back: row er + 8 i, chunk ec
+    const int y = f.ry + DS * yi;
 #pragma unroll
     for (int cn = 0; cn < 2; cn++) {
-        const int x = x0 + 2 * wn + cn;
-        if (x >= p.wout) continue;
+        const int xi = x0 + 2 * wn + cn;
+        if (xi >= f.gw) continue;
+        const int x = f.rx + DS * xi;
         if (p.layout == MXC_CBF) {
             float* px = p.out + (((size_t)g * p.hout + y) * p.wout + x) * p.M * 32;
 #pragma unroll
@@ -346,20 +380,70 @@ __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
 }
 
 template <int FMT, bool DG, int KW, int S, int WGM>
-int launch_lean_t(const LeanArgs& a, int nbufs_used, hipStream_t s) {
-    // the stage ring, and at least the 4 x 4 KB the epilogue stages through
-    size_t lds = (size_t)nbufs_used * a.stage_bytes;
-    if (lds < 4 * 4096) lds = 4 * 4096;
-    static bool attr = false;
+__global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
+    // XCD-aware order: consecutive tiles (same output row) on one XCD
+    const int per_xcd = (gridDim.x + 7) / 8;
+    const int lin = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+    if (lin >= p.ntiles) return;
+    Phase f;
+    f.ry = 0; f.rx = 0; f.kh0 = 0; f.nvh = p.kh; f.kw0 = 0;
+    f.gh = p.hout; f.gw = p.wout; f.c0 = p.pw; f.r0 = p.ph;
+    lean_tile<FMT, DG, KW, S, WGM>(p, lin, f);
+}
+
+// Stride-2 input gradient for kernel width KWF (1 or 3): the four phases in
+// one launch, tiles of phase (ry, rx) at [pofs[2 ry + rx], pofs[2 ry + rx + 1]).
+template <int FMT, int KWF, int WGM>
+__global__ __launch_bounds__(LT) void conv_lean_dg2_kernel(LeanArgs p) {
+    const int per_xcd = (gridDim.x + 7) / 8;
+    int lin = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+    if (lin >= p.pofs[4]) return;
+    int ph = 0;
+    while (ph < 3 && lin >= p.pofs[ph + 1]) ph++;
+    lin -= p.pofs[ph];
+    Phase f;
+    f.ry = ph >> 1; f.rx = ph & 1;
+    f.kh0 = (f.ry + p.ph) & 1;
+    f.kw0 = (f.rx + p.pw) & 1;
+    f.nvh = f.kh0 < p.kh ? (p.kh - f.kh0 + 1) / 2 : 0;
+    const int nvw = f.kw0 < KWF ? (KWF - f.kw0 + 1) / 2 : 0;
+    if (nvw == 0) f.nvh = 0;                       // no tap reaches the phase: its pixels are zero
+    f.gh = (p.hout - f.ry + 1) / 2; f.gw = (p.wout - f.rx + 1) / 2;
+    f.c0 = (f.rx + p.pw - f.kw0) / 2; f.r0 = (f.ry + p.ph - f.kh0) / 2;
+    if (KWF == 3 && nvw == 2) lean_tile<FMT, true, 2, 2, WGM>(p, lin, f);
+    else                      lean_tile<FMT, true, 1, 2, WGM>(p, lin, f);
+}
+
+// LDS bytes of one launch: the stage ring, and at least the 4 x 4 KB the
+// epilogue stages through.
+inline size_t lean_lds(const LeanArgs& a, int nbufs_used) {
+    const size_t lds = (size_t)nbufs_used * a.stage_bytes;
+    return lds < 4 * 4096 ? 4 * 4096 : lds;
+}
+
+template <typename K>
+int lean_launch(K kernel, bool& attr, const LeanArgs& a, int ntiles, size_t lds, hipStream_t s) {
     if (lds > 65536 && !attr) {
-        if (hipFuncSetAttribute((const void*)conv_lean_kernel<FMT, DG, KW, S, WGM>,
-                                hipFuncAttributeMaxDynamicSharedMemorySize, LDS_MAX) != hipSuccess)
+        if (hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, LDS_MAX) !=
+            hipSuccess)
             return MXC_ERR_HIP;
         attr = true;
     }
-    const int grid = (a.ntiles + 7) / 8 * 8;
-    hipLaunchKernelGGL((conv_lean_kernel<FMT, DG, KW, S, WGM>), dim3(grid), dim3(LT), lds, s, a);
+    const int grid = (ntiles + 7) / 8 * 8;
+    hipLaunchKernelGGL(kernel, dim3(grid), dim3(LT), lds, s, a);
     return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
+}
+
+template <int FMT, bool DG, int KW, int S, int WGM>
+int launch_lean_t(const LeanArgs& a, int nbufs_used, hipStream_t s) {
+    static bool attr = false;
+    return lean_launch(conv_lean_kernel<FMT, DG, KW, S, WGM>, attr, a, a.ntiles, lean_lds(a, nbufs_used), s);
+}
+
+template <int FMT, int KWF>
+int launch_lean_dg2(const LeanArgs& a, int nbufs_used, hipStream_t s) {
+    static bool attr = false;
+    return lean_launch(conv_lean_dg2_kernel<FMT, KWF, 1>, attr, a, a.pofs[4], lean_lds(a, nbufs_used), s);
 }
 
 template <int FMT, bool DG, int KW, int S>
@@ -372,7 +456,7 @@ int launch_lean_w(const LeanArgs& a, int wgm, int nb, hipStream_t s) {
 template <int FMT, bool DG>
 int launch_lean_f(const LeanArgs& a, int kw, int sw, int wgm, int nb, hipStream_t s) {
     if constexpr (DG) {
-        (void)sw;
+        if (sw == 2) return kw == 3 ? launch_lean_dg2<FMT, 3>(a, nb, s) : launch_lean_dg2<FMT, 1>(a, nb, s);
         return kw == 3 ? launch_lean_w<FMT, DG, 3, 1>(a, wgm, nb, s) : launch_lean_w<FMT, DG, 1, 1>(a, wgm, nb, s);
     } else {
         if (kw == 3) return sw == 2 ? launch_lean_w<FMT, DG, 3, 2>(a, wgm, nb, s) : launch_lean_w<FMT, DG, 3, 1>(a, wgm, nb, s);
@@ -388,7 +472,10 @@ int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws,
                      const uint8_t* ss, float* out, int layout, hipStream_t s) {
     if (cv.x.bn != 32) return 1;
     if (cv.kw != 1 && cv.kw != 3) return 1;
-    if (dg ? (cv.sh != 1 || cv.sw != 1) : (cv.sw != 1 && cv.sw != 2)) return 1;
+    // input gradient: stride 1, or 2 in both directions (phases); forward:
+    // column stride 1 or 2, any row stride
+    const bool dg2 = dg && cv.sh == 2 && cv.sw == 2;
+    if (dg ? !(dg2 || (cv.sh == 1 && cv.sw == 1)) : (cv.sw != 1 && cv.sw != 2)) return 1;
     LeanArgs a;
     a.wc = (const uint8_t*)wc; a.ws = ws; a.sc = (const uint8_t*)sc; a.ss = ss;
     a.out = out; a.layout = layout;
@@ -398,6 +485,7 @@ int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws,
     a.hout = dg ? cv.h : cv.ho;
     a.wout = dg ? cv.w : cv.wo;
     a.kh = cv.kh; a.sh = cv.sh; a.ph = cv.ph; a.pw = cv.pw;
+    a.kwf = cv.kw;
     a.kcb = src.ncb;
     a.w_rowblocks = dg ? cv.wt.ncb : cv.wt.np / 32;
     a.w_cp = cv.wt.cp; a.w_ncb = cv.wt.ncb; a.w_nco = cv.wt.np / 32;
@@ -410,23 +498,33 @@ int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws,
     const int wgm = (!dg && cv.sw == 2 && mp >= 2) ? 2 : 1;
     const int px = 8 / wgm;
     a.mtiles = (a.M + 64 * wgm - 1) / (64 * wgm);
-    a.nseg = (a.wout + px - 1) / px;
-    const long long nt = (long long)a.mtiles * a.nseg * a.hout * src.ng;
+    long long nt = 0;
+    for (int i = 0; i < 5; i++) a.pofs[i] = 0;
+    if (dg2) {
+        // tiles of the four phases (ry, rx); their pixel grids are the
+        // output rows / columns of that parity
+        for (int ph = 0; ph < 4; ph++) {
+            const int gh = (a.hout - (ph >> 1) + 1) / 2, gw = (a.wout - (ph & 1) + 1) / 2;
+            nt += (long long)a.mtiles * ((gw + px - 1) / px) * gh * src.ng;
+            if (nt > 0x7FFFFFF0LL) return 1;
+            a.pofs[ph + 1] = (int)nt;
+        }
+    } else {
+        nt = (long long)a.mtiles * ((a.wout + px - 1) / px) * a.hout * src.ng;
+    }
     if (nt <= 0 || nt > 0x7FFFFFF0LL) return 1;
     a.ntiles = (int)nt;
+    // stage layout: DMA slices of the weight blocks, then the halo blocks,
+    // rounded to whole 4 KB groups, then the scale entries; at stride 2 the
+    // widest phase has (kw + 1) / 2 taps per row
     const int tb = cv.bits == 8 ? 1024 : 512;
-    const int hp = dg ? px + cv.kw - 1 : (px - 1) * cv.sw + cv.kw;
-    const int na = cv.kw * 2 * 2 * wgm, nb = 2 * hp;
+    const int kwt = dg2 ? (cv.kw + 1) / 2 : cv.kw;
+    const int hp = dg ? px + kwt - 1 : (px - 1) * cv.sw + cv.kw;
+    const int na = kwt * 2 * 2 * wgm, nb = 2 * hp;
     const int bpi = 1024 / tb;
-    a.nq = (na + nb + 4 * bpi - 1) / (4 * bpi);
-    a.a_bytes = na * tb;
-    a.b_bytes = nb * tb;
-    // DMA slices cover nq * 4 KB; the scale entries follow
-    const int blocks_bytes = a.nq * 4096;
-    if (a.a_bytes + a.b_bytes > blocks_bytes) return MXC_ERR_HIP;
-    a.b_bytes = blocks_bytes - a.a_bytes;
-    a.stage_bytes = blocks_bytes + SCALE_REGION;
-    const int nstage = cv.kh * ((a.kcb + 1) / 2);
+    const int nq = (na + nb + 4 * bpi - 1) / (4 * bpi);
+    a.stage_bytes = nq * 4096 + SCALE_REGION;
+    const int nstage = (dg2 ? (cv.kh + 1) / 2 : cv.kh) * ((a.kcb + 1) / 2);
     if (2 * a.stage_bytes > LDS_MAX || nstage < 1) return 1;
     // ring depth: the workgroups that share a CU at this grid size split its
     // LDS; each takes as many stage buffers (2..4) as fit in its share
