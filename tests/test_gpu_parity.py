@@ -74,6 +74,19 @@ def test_quantize_layouts_and_bf16(mx, fmt, layout):
 
 
 @pytest.mark.parametrize("fmt", [0, 1], ids=["e4m3", "e2m1"])
+@pytest.mark.parametrize("bf16", [False, True], ids=["f32", "bf16"])
+def test_quantize_cbf_medium(mx, fmt, bf16):
+    """CBF activations of a few thousand blocks, with ragged channels and two
+    batch groups, fp32 and bf16 sources."""
+    for shape in [(32, 70, 41, 37), (64, 64, 40, 29), (32, 100, 61, 47)]:
+        t = synth.silu_normal(shape, 7)
+        if bf16:
+            t = t.to(torch.bfloat16).float()
+        src = synth.nchw_to_cbf(t, 32)
+        _qcheck(mx, t, mx.ACT, fmt, mx.CBF, shape, src.to(torch.bfloat16) if bf16 else src)
+
+
+@pytest.mark.parametrize("fmt", [0, 1], ids=["e4m3", "e2m1"])
 def test_quantize_weights(mx, fmt):
     for shape in [(64, 64, 3, 3), (20, 48, 3, 3), (256, 64, 1, 1), (16, 3, 3, 3), (33, 70, 5, 2)]:
         t = synth.kaiming(*shape, seed=shape[0])
