@@ -14,11 +14,16 @@ gradients N(0, 1e-3), all seeded.
 GEMMs' algorithmic flops (2 N Cout Ho Wo Cin Kh Kw each, real channels) over
 the step's wall time, quantize and im2col included.  The timed step is
 replayed from one HIP graph (captured once after warm-up), so it measures
-GPU time, not Python launch cost.  Every op is also timed alone with HIP
-events on the stream it runs on (behind a GPU spin, so the host's launch
-latency is excluded); the op taking the most time per step gets the
-`roofline` object, its time measured again over K launches right after the
-timed region, and all ops are listed in `ops`.
+GPU time, not Python launch cost.
+
+Per op, two times are reported in `ops`: `ms`, the op's kernel time in
+steady state -- a HIP graph of K back-to-back launches of the op, replayed on
+the stream its kernels run on and bracketed by HIP events (median of
+rounds); quantize launches rotate over enough copies of their fp32 source
+that it is read from HBM, not from the 256 MB last-level cache -- and
+`ms_alone`, one eager launch bracketed by HIP events behind a GPU spin
+(launch and event overhead included).  The op with the largest `ms` gets the
+`roofline` object.
 
     python bench.py [--steps K] [--warmup W] [--no-cpu-baseline]
 """
@@ -275,14 +280,14 @@ def main():
     stream = torch.cuda.current_stream()
     OPS = ("quant_x", "quant_w", "quant_gy", "im2col", "fwd", "dgrad", "wgrad")
 
-    def run_op(j, op):
+    def run_op(j, op, src=None):
         cv, fmt = j["cv"], j["fmt"]
         if op == "quant_x":
-            mx.quantize(j["x"], mx.ACT, fmt, layout=mx.CBF, shape=j["xs"], out=j["qx"])
+            mx.quantize(j["x"] if src is None else src, mx.ACT, fmt, layout=mx.CBF, shape=j["xs"], out=j["qx"])
         elif op == "quant_w":
             mx.quantize(j["w"], mx.WEIGHT, fmt, out=j["qw"])
         elif op == "quant_gy":
-            mx.quantize(j["gy"], mx.ACT, fmt, layout=mx.CBF, shape=j["gs"], out=j["qg"])
+            mx.quantize(j["gy"] if src is None else src, mx.ACT, fmt, layout=mx.CBF, shape=j["gs"], out=j["qg"])
         elif op == "fwd":
             mx.fwd(cv, j["qw"], j["qx"], layout=mx.CBF, out=j["y"])
         elif op == "dgrad":
@@ -347,7 +352,6 @@ def main():
         return sum(a.elapsed_time(b) for a, b in marks) / reps
 
     op_ms = {(j["name"], op): op_time(j, op) for j, op in seq}
-    dom = max(op_ms, key=op_ms.get)
 
     # The step is launched as one HIP graph (captured once), so host-side
     # launch cost does not enter the step time.
@@ -365,10 +369,38 @@ def main():
     t1 = time.perf_counter()
     ms_step = (t1 - t0) * 1e3 / args.steps
 
-    # The dominant op again, K launches on its stream, each bracketed by HIP
-    # events behind a GPU spin: kernel time plus its launch, no host latency.
-    dj = next(j for j, op in seq if (j["name"], op) == dom)
-    dom_ms = op_time(dj, dom[1], reps=args.steps)
+    # Steady-state kernel time of every op: a graph of back-to-back launches,
+    # replayed.  Quantize sources rotate over copies totalling more than the
+    # last-level cache, so that they come from HBM as they do in the step.
+    def replay_ms(g, reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    import statistics
+    LLC_BYTES = 256 << 20
+    steady = {}
+    for j, op in seq:
+        srcs = [None]
+        if op in ("quant_x", "quant_gy"):
+            base = j["x"] if op == "quant_x" else j["gy"]
+            ncopy = min(48, -(-(LLC_BYTES + (64 << 20)) // (base.numel() * base.element_size())))
+            srcs = [base] + [base.clone() for _ in range(ncopy - 1)]
+        kl = max(12, len(srcs))
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for k in range(kl):
+                run_op(j, op, srcs[k % len(srcs)]) if op != "im2col" else run_im2col(j)
+        g.replay()
+        torch.cuda.synchronize()
+        steady[(j["name"], op)] = statistics.median(replay_ms(g, 3) for _ in range(3)) / kl
+        del g, srcs
+    dom = max(steady, key=steady.get)
+    dom_ms = steady[dom]
 
     naive = {} if args.no_naive else naive_leg(jobs, op_ms, mx, synth, dev, stream)
 
@@ -391,12 +423,14 @@ def main():
     jmap = {j["name"]: j for j in jobs}
     rl = roof(jmap[dom[0]], dom[1], dom_ms)
     rl.update({"kernel": f"{dom[1]} {dom[0]}", "ms": round(dom_ms, 4),
+               "ms_alone": round(op_ms[dom], 4),
                "traffic": counter_traffic(f"{dom[0]}/{dom[1]}")})
     ops = {}
-    for (nm, op), ms in op_ms.items():
+    for (nm, op), ms in steady.items():
         fl, by = jmap[nm]["nums"][op]
         r = roof(jmap[nm], op, ms)
-        ops[f"{nm}/{op}"] = {"ms": round(ms, 4), "tflops": round(fl / (ms * 1e-3) / 1e12, 2) if fl else None,
+        ops[f"{nm}/{op}"] = {"ms": round(ms, 4), "ms_alone": round(op_ms[(nm, op)], 4),
+                             "tflops": round(fl / (ms * 1e-3) / 1e12, 2) if fl else None,
                              "gbps": round(by / (ms * 1e-3) / 1e9, 1), "bound": r["bound"], "frac": r["frac"]}
 
     out = {
@@ -411,6 +445,7 @@ def main():
                    "parallelism": "single GPU"},
         "roofline": rl,
         "ops": ops,
+        "ops_sum_ms": round(sum(steady.values()), 4),
     }
     if naive:
         out["vs_naive"] = naive
