@@ -13,8 +13,8 @@
 // kernel with a smaller kernel.  One launch covers the four phases.
 //
 // One workgroup (4 waves) computes a tile of BM = 64*WGM output channels x
-// PX = 8/WGM output pixels of one output row x 32 samples; each wave owns
-// 64 channels x 2 pixels (2 x 2 MFMAs of 32 x 32 x 64 per tap and K step).
+// PX = 4*PW/WGM output pixels of one output row x 32 samples; each wave owns
+// 64 channels x PW pixels (2 x PW MFMAs of 32 x 32 x 64 per tap and K step).
 // The K loop runs over stages (kernel row, pair of 32-channel blocks).  A
 // stage holds, in LDS, the weight blocks of its kernel row ([tap][block]
 // [row block]) and the source pixels its taps reach in that row (the halo:
@@ -84,13 +84,15 @@ struct Phase {
 
 // One tile.  DG with S = 2 is a phase of the stride-2 input gradient and KW
 // its taps per row (the halo is then a stride-1 one on the phase grid).
-template <int FMT, bool DG, int KW, int S, int WGM>
+// Each wave owns 64 channels x PW pixels (PW = 2, or 1 for layers with few
+// tiles: twice the workgroups, so more waves stream and store at once).
+template <int FMT, bool DG, int KW, int S, int WGM, int PW>
 __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phase& f) {
     constexpr int EB = FMT == MXC_E4M3 ? 8 : 4;
     constexpr int TB = 32 * 32 * EB / 8;            // bytes of one stored block (weights and activations)
     constexpr int RB = 32 * EB / 8;                 // bytes of one channel row of an activation block
     constexpr int RBW = 2 * WGM;                    // 32-row blocks per tile
-    constexpr int PX = 8 / WGM;                     // output pixels per tile
+    constexpr int PX = PW * 4 / WGM;                // output pixels per tile
     constexpr int CS = DG ? 1 : S;                  // halo columns per output pixel step
     constexpr int DS = DG ? S : 1;                  // tap step of a phase (stride-2 input gradient)
     constexpr int HP = (PX - 1) * CS + KW;          // halo pixels
@@ -98,7 +100,7 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
     constexpr int NB = 2 * HP;                      // activation blocks per stage
     constexpr int BPI = 1024 / TB;                  // blocks per wave instruction
     constexpr int NQ = (NA + NB + 4 * BPI - 1) / (4 * BPI);   // DMA instructions per thread per stage
-    constexpr int ND = CS + KW;                     // distinct halo pixels of a wave (2 pixels)
+    constexpr int ND = (PW - 1) * CS + KW;          // distinct halo pixels of a wave
     constexpr int NSA = KW * 2 * RBW;               // weight scales per stage
     constexpr int NSB = 2 * HP;                     // activation scales per stage
     static_assert(NSA + NSB <= LT, "scale staging needs one thread per scale");
@@ -219,13 +221,13 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
     else    a_lane = FMT == MXC_E4M3 ? (16 * hh + (i16 >> 1)) * 32 + 16 * cg + 8 * (i16 & 1) : i16 * 16 + 8 * cg;
     const int b_lane = FMT == MXC_E4M3 ? (16 * hh + (i16 >> 1)) * RB + 16 * cg + 8 * (i16 & 1)
                                        : i16 * RB + 8 * cg;
-    const int hbase = 2 * wn * CS;                    // first halo pixel of the wave
+    const int hbase = PW * wn * CS;                   // first halo pixel of the wave
 
-    v16f acc[2][2];
+    v16f acc[2][PW];
 #pragma unroll
     for (int i = 0; i < 2; i++)
 #pragma unroll
-        for (int j = 0; j < 2; j++)
+        for (int j = 0; j < PW; j++)
 #pragma unroll
             for (int e = 0; e < 16; e++) acc[i][j][e] = 0.0f;
 
@@ -316,7 +318,7 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                 sa[rb] = SC[4 * ((t * 2 + h) * RBW + rbi)];
             }
 #pragma unroll
-            for (int cn = 0; cn < 2; cn++) {
+            for (int cn = 0; cn < PW; cn++) {
                 const int d = DG ? cn + (KW - 1 - t) : cn * CS + t;
 #pragma unroll
                 for (int rb = 0; rb < 2; rb++)   // transposed product: rows = samples, columns = channels
@@ -338,8 +340,8 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
     const int er = lane >> 3, ec = lane & 7;            // read-back: row er + 8 i, chunk ec
     const int y = f.ry + DS * yi;
 #pragma unroll
-    for (int cn = 0; cn < 2; cn++) {
-        const int xi = x0 + 2 * wn + cn;
+    for (int cn = 0; cn < PW; cn++) {
+        const int xi = x0 + PW * wn + cn;
         if (xi >= f.gw) continue;
         const int x = f.rx + DS * xi;
         if (p.layout == MXC_CBF) {
@@ -379,7 +381,7 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
     }
 }
 
-template <int FMT, bool DG, int KW, int S, int WGM>
+template <int FMT, bool DG, int KW, int S, int WGM, int PW>
 __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
     // XCD-aware order: consecutive tiles (same output row) on one XCD
     const int per_xcd = (gridDim.x + 7) / 8;
@@ -388,12 +390,12 @@ __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
     Phase f;
     f.ry = 0; f.rx = 0; f.kh0 = 0; f.nvh = p.kh; f.kw0 = 0;
     f.gh = p.hout; f.gw = p.wout; f.c0 = p.pw; f.r0 = p.ph;
-    lean_tile<FMT, DG, KW, S, WGM>(p, lin, f);
+    lean_tile<FMT, DG, KW, S, WGM, PW>(p, lin, f);
 }
 
 // Stride-2 input gradient for kernel width KWF (1 or 3): the four phases in
 // one launch, tiles of phase (ry, rx) at [pofs[2 ry + rx], pofs[2 ry + rx + 1]).
-template <int FMT, int KWF, int WGM>
+template <int FMT, int KWF, int WGM, int PW>
 __global__ __launch_bounds__(LT) void conv_lean_dg2_kernel(LeanArgs p) {
     const int per_xcd = (gridDim.x + 7) / 8;
     int lin = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
@@ -410,8 +412,8 @@ __global__ __launch_bounds__(LT) void conv_lean_dg2_kernel(LeanArgs p) {
     if (nvw == 0) f.nvh = 0;                       // no tap reaches the phase: its pixels are zero
     f.gh = (p.hout - f.ry + 1) / 2; f.gw = (p.wout - f.rx + 1) / 2;
     f.c0 = (f.rx + p.pw - f.kw0) / 2; f.r0 = (f.ry + p.ph - f.kh0) / 2;
-    if (KWF == 3 && nvw == 2) lean_tile<FMT, true, 2, 2, WGM>(p, lin, f);
-    else                      lean_tile<FMT, true, 1, 2, WGM>(p, lin, f);
+    if (KWF == 3 && nvw == 2) lean_tile<FMT, true, 2, 2, WGM, PW>(p, lin, f);
+    else                      lean_tile<FMT, true, 1, 2, WGM, PW>(p, lin, f);
 }
 
 // LDS bytes of one launch: the stage ring, and at least the 4 x 4 KB the
@@ -434,33 +436,38 @@ int lean_launch(K kernel, bool& attr, const LeanArgs& a, int ntiles, size_t lds,
     return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
 }
 
-template <int FMT, bool DG, int KW, int S, int WGM>
+template <int FMT, bool DG, int KW, int S, int WGM, int PW>
 int launch_lean_t(const LeanArgs& a, int nbufs_used, hipStream_t s) {
     static bool attr = false;
-    return lean_launch(conv_lean_kernel<FMT, DG, KW, S, WGM>, attr, a, a.ntiles, lean_lds(a, nbufs_used), s);
+    return lean_launch(conv_lean_kernel<FMT, DG, KW, S, WGM, PW>, attr, a, a.ntiles, lean_lds(a, nbufs_used), s);
 }
 
-template <int FMT, int KWF>
+template <int FMT, int KWF, int PW>
 int launch_lean_dg2(const LeanArgs& a, int nbufs_used, hipStream_t s) {
     static bool attr = false;
-    return lean_launch(conv_lean_dg2_kernel<FMT, KWF, 1>, attr, a, a.pofs[4], lean_lds(a, nbufs_used), s);
+    return lean_launch(conv_lean_dg2_kernel<FMT, KWF, 1, PW>, attr, a, a.pofs[4], lean_lds(a, nbufs_used), s);
 }
 
+// (WGM, PW) in use: (1, 1), (1, 2), (2, 2), (4, 2)
 template <int FMT, bool DG, int KW, int S>
-int launch_lean_w(const LeanArgs& a, int wgm, int nb, hipStream_t s) {
-    if (wgm == 4) return launch_lean_t<FMT, DG, KW, S, 4>(a, nb, s);
-    if (wgm == 2) return launch_lean_t<FMT, DG, KW, S, 2>(a, nb, s);
-    return launch_lean_t<FMT, DG, KW, S, 1>(a, nb, s);
+int launch_lean_w(const LeanArgs& a, int wgm, int pw, int nb, hipStream_t s) {
+    if (wgm == 4) return launch_lean_t<FMT, DG, KW, S, 4, 2>(a, nb, s);
+    if (wgm == 2) return launch_lean_t<FMT, DG, KW, S, 2, 2>(a, nb, s);
+    return pw == 1 ? launch_lean_t<FMT, DG, KW, S, 1, 1>(a, nb, s) : launch_lean_t<FMT, DG, KW, S, 1, 2>(a, nb, s);
 }
 
 template <int FMT, bool DG>
-int launch_lean_f(const LeanArgs& a, int kw, int sw, int wgm, int nb, hipStream_t s) {
+int launch_lean_f(const LeanArgs& a, int kw, int sw, int wgm, int pw, int nb, hipStream_t s) {
     if constexpr (DG) {
-        if (sw == 2) return kw == 3 ? launch_lean_dg2<FMT, 3>(a, nb, s) : launch_lean_dg2<FMT, 1>(a, nb, s);
-        return kw == 3 ? launch_lean_w<FMT, DG, 3, 1>(a, wgm, nb, s) : launch_lean_w<FMT, DG, 1, 1>(a, wgm, nb, s);
+        if (sw == 2) {
+            if (kw == 3) return pw == 1 ? launch_lean_dg2<FMT, 3, 1>(a, nb, s) : launch_lean_dg2<FMT, 3, 2>(a, nb, s);
+            return pw == 1 ? launch_lean_dg2<FMT, 1, 1>(a, nb, s) : launch_lean_dg2<FMT, 1, 2>(a, nb, s);
+        }
+        return kw == 3 ? launch_lean_w<FMT, DG, 3, 1>(a, wgm, pw, nb, s) : launch_lean_w<FMT, DG, 1, 1>(a, wgm, pw, nb, s);
     } else {
-        if (kw == 3) return sw == 2 ? launch_lean_w<FMT, DG, 3, 2>(a, wgm, nb, s) : launch_lean_w<FMT, DG, 3, 1>(a, wgm, nb, s);
-        return sw == 2 ? launch_lean_w<FMT, DG, 1, 2>(a, wgm, nb, s) : launch_lean_w<FMT, DG, 1, 1>(a, wgm, nb, s);
+        if (kw == 3) return sw == 2 ? launch_lean_w<FMT, DG, 3, 2>(a, wgm, pw, nb, s)
+                                    : launch_lean_w<FMT, DG, 3, 1>(a, wgm, pw, nb, s);
+        return sw == 2 ? launch_lean_w<FMT, DG, 1, 2>(a, wgm, pw, nb, s) : launch_lean_w<FMT, DG, 1, 1>(a, wgm, pw, nb, s);
     }
 }
 
@@ -495,23 +502,31 @@ int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws,
     // the same 48 MFMAs -- 64 rows x 8 pixels at column stride 1; at stride 2
     // the halo of 8 pixels is wide, 128 rows x 4 pixels is cheaper
     const int mp = (a.M + 63) / 64;
-    const int wgm = (!dg && cv.sw == 2 && mp >= 2) ? 2 : 1;
-    const int px = 8 / wgm;
-    a.mtiles = (a.M + 64 * wgm - 1) / (64 * wgm);
-    long long nt = 0;
-    for (int i = 0; i < 5; i++) a.pofs[i] = 0;
-    if (dg2) {
-        // tiles of the four phases (ry, rx); their pixel grids are the
-        // output rows / columns of that parity
+    int wgm = (!dg && cv.sw == 2 && mp >= 2) ? 2 : 1;
+    int pw = 2;
+    // tiles of a tile shape; for the stride-2 input gradient, per phase
+    // (ry, rx), whose pixel grids are the output rows / columns of that parity
+    auto count = [&](int wgm_, int pw_, bool fill) -> long long {
+        const int px_ = pw_ * 4 / wgm_;
+        const long long mt = (a.M + 64 * wgm_ - 1) / (64 * wgm_);
+        if (!dg2) return mt * ((a.wout + px_ - 1) / px_) * a.hout * src.ng;
+        long long t = 0;
         for (int ph = 0; ph < 4; ph++) {
             const int gh = (a.hout - (ph >> 1) + 1) / 2, gw = (a.wout - (ph & 1) + 1) / 2;
-            nt += (long long)a.mtiles * ((gw + px - 1) / px) * gh * src.ng;
-            if (nt > 0x7FFFFFF0LL) return 1;
-            a.pofs[ph + 1] = (int)nt;
+            t += mt * ((gw + px_ - 1) / px_) * gh * src.ng;
+            if (fill) a.pofs[ph + 1] = t <= 0x7FFFFFF0LL ? (int)t : 0;
         }
-    } else {
-        nt = (long long)a.mtiles * ((a.wout + px - 1) / px) * a.hout * src.ng;
-    }
+        return t;
+    };
+    // a layer whose tiles would leave a quarter of the CUs idle takes one
+    // pixel per wave instead: twice the workgroups, more waves streaming
+    // operands and storing results at once (measured: faster below ~200
+    // tiles, slower from ~400)
+    if (count(wgm, pw, false) < 192) { wgm = 1; pw = 1; }
+    const int px = pw * 4 / wgm;
+    a.mtiles = (a.M + 64 * wgm - 1) / (64 * wgm);
+    for (int i = 0; i < 5; i++) a.pofs[i] = 0;
+    const long long nt = count(wgm, pw, true);
     if (nt <= 0 || nt > 0x7FFFFFF0LL) return 1;
     a.ntiles = (int)nt;
     // stage layout: DMA slices of the weight blocks, then the halo blocks,
@@ -535,10 +550,10 @@ int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws,
     a.nbuf = nbuf;
     const int used = nbuf < nstage ? nbuf : nstage;
     if (cv.fmt == MXC_E4M3)
-        return dg ? launch_lean_f<MXC_E4M3, true>(a, cv.kw, cv.sw, wgm, used, s)
-                  : launch_lean_f<MXC_E4M3, false>(a, cv.kw, cv.sw, wgm, used, s);
-    return dg ? launch_lean_f<MXC_E2M1, true>(a, cv.kw, cv.sw, wgm, used, s)
-              : launch_lean_f<MXC_E2M1, false>(a, cv.kw, cv.sw, wgm, used, s);
+        return dg ? launch_lean_f<MXC_E4M3, true>(a, cv.kw, cv.sw, wgm, pw, used, s)
+                  : launch_lean_f<MXC_E4M3, false>(a, cv.kw, cv.sw, wgm, pw, used, s);
+    return dg ? launch_lean_f<MXC_E2M1, true>(a, cv.kw, cv.sw, wgm, pw, used, s)
+              : launch_lean_f<MXC_E2M1, false>(a, cv.kw, cv.sw, wgm, pw, used, s);
 }
 
 }  // namespace mxc
