@@ -85,6 +85,7 @@ typedef enum { MXC_E4M3 = 0, MXC_E2M1 = 1 } mxc_fmt;
 typedef enum { MXC_F32 = 0, MXC_BF16 = 1 } mxc_dtype;
 typedef enum { MXC_NCHW = 0, MXC_NHWC = 1, MXC_CBF = 2 } mxc_layout;
 typedef enum { MXC_ACT = 0, MXC_WEIGHT = 1 } mxc_role;
+typedef enum { MXC_FN_NONE = 0, MXC_FN_RELU = 1, MXC_FN_SILU = 2 } mxc_fn;   /* activation function */
 
 /* One convolution layer: batch n, channels cin -> cout, input h x w,
  * kernel kh x kw, stride sh, sw, zero padding ph, pw. */
@@ -265,6 +266,47 @@ int mxconv_naive_wgrad(const mxc_conv* cv, int fmt,
                        const void* gyt_codes, const uint8_t* gyt_scales,
                        const void* xt_codes, const uint8_t* xt_scales,
                        float* gw, void* stream);
+
+/* ------------------------------------------------------------------ f1 */
+/* Fused quantizing epilogues.  In the paper's training step a layer's output
+ * is still on chip when it is quantized for the next use, and only the MX
+ * codes go off chip (Sec. V, DRAM simulation; Sec. IV-B: every tensor is
+ * quantized once).  Here the forward and input-gradient kernels quantize
+ * their output tile in the epilogue: one 32-channel x 32-sample output tile
+ * at one pixel is exactly one MX block of the next consumer's operand, so
+ * the block maximum, E8M0 scale and codes are formed in registers with the
+ * rule of mxconv_quantize (role MXC_ACT) and no fp32 tensor is written.
+ *
+ * Forward: Y = fn(W * X), fn in mxc_fn (MXC_FN_NONE, MXC_FN_RELU, or
+ * MXC_FN_SILU y / (1 + exp(-y))), quantized into the MX-CBF tensor of
+ * (n, cout, Ho, Wo):
+ *   y_codes / y_scales  device, mxconv_codes_bytes / mxconv_scales_bytes(
+ *                       MXC_ACT, out_fmt, n, cout, Ho, Wo) bytes, written.
+ *   y_act               NULL, or device fp32 n x cout x Ho x Wo in CBF
+ *                       layout: receives the values that were quantized.
+ * Input gradient: G_Z = (W^T * G_Y) . fn'(z), the gradient at the
+ * pre-activation z of this layer's input X = fn(z) (fn' = 1 for
+ * MXC_FN_NONE, [z > 0] for ReLU, s (1 + z (1 - s)) with s = 1 / (1 +
+ * exp(-z)) for SiLU), quantized into the MX-CBF tensor of (n, cin, h, w) --
+ * the G_Y operand of the layer before:
+ *   z                   device fp32 n x cin x h x w in CBF layout; may be
+ *                       NULL for MXC_FN_NONE.
+ *   gx_codes / gx_scales, gx_act  as above for (n, cin, h, w).
+ * The fused kernels cover batch block 32 (n a multiple of 32), kernel width
+ * 1 or 3, forward column stride 1 or 2, input-gradient stride 1x1 or 2x2;
+ * other layers return MXC_ERR_SHAPE (use mxconv_fwd / mxconv_dgrad and
+ * mxconv_quantize).
+ * Errors: NULL, ARG, SHAPE, ALIGN, HIP. */
+int mxconv_fwd_quant(const mxc_conv* cv, int fmt,
+                     const void* w_codes, const uint8_t* w_scales,
+                     const void* x_codes, const uint8_t* x_scales,
+                     int fn, int out_fmt, void* y_codes, uint8_t* y_scales,
+                     float* y_act, void* stream);
+int mxconv_dgrad_quant(const mxc_conv* cv, int fmt,
+                       const void* w_codes, const uint8_t* w_scales,
+                       const void* gy_codes, const uint8_t* gy_scales,
+                       int fn, const float* z, int out_fmt,
+                       void* gx_codes, uint8_t* gx_scales, float* gx_act, void* stream);
 
 /* Human-readable text for a return code (static storage). */
 const char* mxconv_strerror(int code);

@@ -334,3 +334,36 @@ def counter_get():
 
 def counter_reset():
     load().o_counter_reset()
+
+
+# ---------------------------------------------------------------- fused epilogues
+FN_NONE, FN_RELU, FN_SILU = 0, 1, 2
+
+
+def act_fn(y, fn):
+    """The activation between two convolutions, in fp64: identity, ReLU
+    (y if y > 0 else 0; the ResNets of Sec. VI) or SiLU y / (1 + exp(-y))
+    (the YOLO networks of Sec. VI).  The fused forward epilogue quantizes
+    act_fn(Y) as the next layer's X, once (Sec. IV-B, Sec. V)."""
+    y = np.asarray(y, dtype=np.float64)
+    if fn == FN_NONE:
+        return y.copy()
+    if fn == FN_RELU:
+        return np.where(y > 0, y, 0.0)
+    with np.errstate(over="ignore"):
+        return y / (1.0 + np.exp(-y))
+
+
+def act_grad(z, fn):
+    """Derivative of act_fn at the pre-activation z, in fp64: 1, [z > 0], or
+    for SiLU s (1 + z (1 - s)) with s = 1 / (1 + exp(-z)).  The fused
+    input-gradient epilogue quantizes G_X * act_grad(z) as the previous
+    layer's G_Y."""
+    z = np.asarray(z, dtype=np.float64)
+    if fn == FN_NONE:
+        return np.ones_like(z)
+    if fn == FN_RELU:
+        return (z > 0).astype(np.float64)
+    with np.errstate(over="ignore"):
+        s = 1.0 / (1.0 + np.exp(-z))
+    return s * (1.0 + z * (1.0 - s))

@@ -40,6 +40,17 @@ constexpr int LT = 256;
 
 __device__ __attribute__((aligned(16))) uint8_t g_zero_lean[1024];
 
+// Activation (forward epilogue) and its derivative (input-gradient epilogue).
+__device__ __forceinline__ float fn_apply(int fn, float y) {
+    if (fn == MXC_FN_RELU) return y > 0.0f ? y : 0.0f;
+    return y / (1.0f + expf(-y));                               // SiLU
+}
+__device__ __forceinline__ float fn_grad(int fn, float z) {
+    if (fn == MXC_FN_RELU) return z > 0.0f ? 1.0f : 0.0f;
+    const float s = 1.0f / (1.0f + expf(-z));                   // SiLU' = s (1 + z (1 - s))
+    return s * (1.0f + z * (1.0f - s));
+}
+
 // LDS of one stage: NQ 4 KB groups of DMA slices (weight blocks, then halo
 // blocks), then 1 KB of scale entries (entry e at byte 4 e: one dword per
 // lane of the one-byte copies).
@@ -69,6 +80,15 @@ struct LeanArgs {
     int nbuf;                 // ring depth, 2..4
     int kwf;                  // full kernel width
     int pofs[5];              // stride-2 input gradient: first tile of each phase (ry, rx) = 00, 01, 10, 11
+    // fused quantizing epilogue (qcodes != NULL): the output tile, after the
+    // activation (forward) or the activation's derivative at zpre (input
+    // gradient), is quantized into the MX-CBF tensor (qcodes, qscales) of
+    // format qfmt with q_ncb 32-channel blocks per pixel; `out`, if not NULL,
+    // receives the fp32 values that were quantized (CBF layout)
+    uint8_t* qcodes;
+    uint8_t* qscales;
+    int qfmt, q_ncb, fn;
+    const float* zpre;
 };
 
 // Taps and output pixel grid of one phase; the stride-1 kernels use the
@@ -335,10 +355,79 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
     // (16-byte chunks XOR-swizzled by row against bank conflicts) and writes
     // them back as four fully contiguous 1 KB stores.
     const int m = mt * 64 * WGM + 64 * wm + (lane & 31);
-    if (p.layout == MXC_CBF) __syncthreads();           // every wave is done with the stage buffers
+    if (p.layout == MXC_CBF && !p.qcodes) __syncthreads();   // every wave is done with the stage buffers
     uint8_t* const ep = smem + wave * 4096;
     const int er = lane >> 3, ec = lane & 7;            // read-back: row er + 8 i, chunk ec
     const int y = f.ry + DS * yi;
+    if (p.qcodes) {
+        // ---- fused quantizing epilogue: acc[rb][cn] is one whole MX block of
+        // the output (32 channels x 32 samples at one pixel); lane l holds
+        // channel l % 32 and samples 8 (e / 4) + 4 (l / 32) + e % 4
+        const int r = lane & 31;
+#pragma unroll
+        for (int cn = 0; cn < PW; cn++) {
+            const int xi = x0 + PW * wn + cn;
+            if (xi >= f.gw) continue;
+            const size_t pix = ((size_t)g * p.hout + y) * p.wout + (f.rx + DS * xi);
+#pragma unroll
+            for (int rb = 0; rb < 2; rb++) {
+                const int cb = mt * 2 * WGM + 2 * wm + rb;
+                if (cb >= p.q_ncb) continue;
+                const int c = cb * 32 + r;
+                const bool real = c < p.M;
+                float v[16];
+#pragma unroll
+                for (int e = 0; e < 16; e++) v[e] = acc[rb][cn][e];
+                if (p.fn != MXC_FN_NONE) {
+                    if (DG) {
+                        const float* zp = p.zpre + (pix * p.M + (real ? c : 0)) * 32 + 4 * h;
+#pragma unroll
+                        for (int e4 = 0; e4 < 4; e4++) {
+                            const float4 z = real ? *(const float4*)(zp + 8 * e4) : make_float4(0.f, 0.f, 0.f, 0.f);
+                            v[4 * e4] *= fn_grad(p.fn, z.x);
+                            v[4 * e4 + 1] *= fn_grad(p.fn, z.y);
+                            v[4 * e4 + 2] *= fn_grad(p.fn, z.z);
+                            v[4 * e4 + 3] *= fn_grad(p.fn, z.w);
+                        }
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 16; e++) v[e] = fn_apply(p.fn, v[e]);
+                    }
+                }
+                if (p.out && real) {
+                    float* o = p.out + (pix * p.M + c) * 32 + 4 * h;
+#pragma unroll
+                    for (int e4 = 0; e4 < 4; e4++)
+                        *(float4*)(o + 8 * e4) = make_float4(v[4 * e4], v[4 * e4 + 1], v[4 * e4 + 2], v[4 * e4 + 3]);
+                }
+                uint32_t m = 0;
+#pragma unroll
+                for (int e = 0; e < 16; e++) m = max(m, __float_as_uint(v[e]) & 0x7FFFFFFFu);
+#pragma unroll
+                for (int off = 32; off >= 1; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off));
+                const bool q8 = p.qfmt == MXC_E4M3;
+                const uint32_t sc = q8 ? scale_code_from_bits<8>(m) : scale_code_from_bits<2>(m);
+                const float inv = inv_scale(sc);
+                const bool bad = sc == 0xFFu;
+                if (lane == 0) p.qscales[pix * p.q_ncb + cb] = (uint8_t)sc;
+                if (q8) {
+                    uint8_t* blk = p.qcodes + (pix * p.q_ncb + cb) * 1024 + r * 32 + 4 * h;
+#pragma unroll
+                    for (int e4 = 0; e4 < 4; e4++)
+                        *(uint32_t*)(blk + 8 * e4) =
+                            bad ? 0u : pack4_e4m3(make_float4(v[4 * e4], v[4 * e4 + 1], v[4 * e4 + 2], v[4 * e4 + 3]), inv);
+                } else {
+                    uint8_t* blk = p.qcodes + (pix * p.q_ncb + cb) * 512 + r * 16 + 2 * h;
+#pragma unroll
+                    for (int e4 = 0; e4 < 4; e4++)
+                        *(unsigned short*)(blk + 4 * e4) =
+                            bad ? (unsigned short)0
+                                : pack4_e2m1(make_float4(v[4 * e4], v[4 * e4 + 1], v[4 * e4 + 2], v[4 * e4 + 3]), inv);
+                }
+            }
+        }
+        return;
+    }
 #pragma unroll
     for (int cn = 0; cn < PW; cn++) {
         const int xi = x0 + PW * wn + cn;
@@ -476,7 +565,7 @@ int launch_lean_f(const LeanArgs& a, int kw, int sw, int wgm, int pw, int nb, hi
 // Returns 1 when the layer is outside this kernel's shapes (the caller then
 // uses the general kernels), else an MXC_* code.
 int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const void* sc,
-                     const uint8_t* ss, float* out, int layout, hipStream_t s) {
+                     const uint8_t* ss, float* out, int layout, hipStream_t s, const FusedEpi* q) {
     if (cv.x.bn != 32) return 1;
     if (cv.kw != 1 && cv.kw != 3) return 1;
     // input gradient: stride 1, or 2 in both directions (phases); forward:
@@ -487,6 +576,12 @@ int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws,
     a.wc = (const uint8_t*)wc; a.ws = ws; a.sc = (const uint8_t*)sc; a.ss = ss;
     a.out = out; a.layout = layout;
     a.M = dg ? cv.cin : cv.cout;
+    a.qcodes = q ? (uint8_t*)q->codes : nullptr;
+    a.qscales = q ? q->scales : nullptr;
+    a.qfmt = q ? q->fmt : 0;
+    a.q_ncb = (a.M + 31) / 32;
+    a.fn = q ? q->fn : MXC_FN_NONE;
+    a.zpre = q ? q->z : nullptr;
     const Geom& src = dg ? cv.gy : cv.x;
     a.hsrc = src.h; a.wsrc = src.w;
     a.hout = dg ? cv.h : cv.ho;

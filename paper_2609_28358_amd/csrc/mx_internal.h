@@ -47,10 +47,21 @@ int launch_fwd(const Conv& cv, const void* wc, const uint8_t* ws, const void* xc
                const uint8_t* xs, float* y, int layout, hipStream_t s);
 int launch_dgrad(const Conv& cv, const void* wc, const uint8_t* ws, const void* gc,
                  const uint8_t* gs, float* gx, int layout, hipStream_t s);
-// fwd / stride-1 dgrad for batch block 32 and kernel width 1 or 3
-// (conv_lean.hip); returns 1 when the layer is outside those shapes
+// Fused quantizing epilogue of fwd / dgrad: the output, after the activation
+// fn (fwd) or times its derivative at z (dgrad), quantized into MX-CBF codes
+// and scales of format fmt.
+struct FusedEpi {
+    void* codes;
+    uint8_t* scales;
+    int fmt, fn;
+    const float* z;
+};
+// fwd / dgrad for batch block 32 and kernel width 1 or 3 (conv_lean.hip);
+// returns 1 when the layer is outside those shapes.  With q, the output is
+// quantized in the epilogue (out, if not NULL, gets the fp32 values that were
+// quantized, CBF layout).
 int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const void* sc,
-                     const uint8_t* ss, float* out, int layout, hipStream_t s);
+                     const uint8_t* ss, float* out, int layout, hipStream_t s, const FusedEpi* q = nullptr);
 // weight gradient for batch block 32 (wgrad_lean.hip): number of K splits
 // (0: not applicable); with more than one split the partial tiles go to the
 // workspace and are reduced by the caller

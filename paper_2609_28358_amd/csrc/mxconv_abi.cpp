@@ -158,6 +158,50 @@ int mxconv_wgrad(const mxc_conv* p, int fmt, const void* gc, const uint8_t* gs, 
     return launch_wgrad(cv, gc, gs, xc, xs, gw, workspace, (hipStream_t)stream);
 }
 
+namespace {
+// the fused kernels' shapes: batch block 32 (so the output tensor is also in
+// blocks of 32 samples), kernel width 1 or 3, the strides the lean kernels run
+bool fused_shape(const Conv& cv, bool dg) {
+    if (cv.x.bn != 32 || (cv.kw != 1 && cv.kw != 3)) return false;
+    return dg ? ((cv.sh == 1 && cv.sw == 1) || (cv.sh == 2 && cv.sw == 2)) : (cv.sw == 1 || cv.sw == 2);
+}
+}  // namespace
+
+int mxconv_fwd_quant(const mxc_conv* p, int fmt, const void* wc, const uint8_t* ws, const void* xc,
+                     const uint8_t* xs, int fn, int out_fmt, void* yc, uint8_t* ysc, float* y_act,
+                     void* stream) {
+    if (!p || !wc || !ws || !xc || !xs || !yc || !ysc) return MXC_ERR_NULL;
+    if (fn < MXC_FN_NONE || fn > MXC_FN_SILU || (out_fmt != MXC_E4M3 && out_fmt != MXC_E2M1)) return MXC_ERR_ARG;
+    Conv cv;
+    int rc = conv_init(&cv, p, fmt);
+    if (rc) return rc;
+    if (!fused_shape(cv, false)) return MXC_ERR_SHAPE;
+    if (!aligned16(wc) || !aligned16(ws) || !aligned16(xc) || !aligned16(xs) || !aligned16(yc) ||
+        !aligned16(ysc) || (y_act && !aligned16(y_act)))
+        return MXC_ERR_ALIGN;
+    FusedEpi q{yc, ysc, out_fmt, fn, nullptr};
+    rc = launch_conv_lean(cv, false, wc, ws, xc, xs, y_act, MXC_CBF, (hipStream_t)stream, &q);
+    return rc == 1 ? MXC_ERR_SHAPE : rc;
+}
+
+int mxconv_dgrad_quant(const mxc_conv* p, int fmt, const void* wc, const uint8_t* ws, const void* gc,
+                       const uint8_t* gs, int fn, const float* z, int out_fmt, void* gxc, uint8_t* gxs,
+                       float* gx_act, void* stream) {
+    if (!p || !wc || !ws || !gc || !gs || !gxc || !gxs) return MXC_ERR_NULL;
+    if (fn < MXC_FN_NONE || fn > MXC_FN_SILU || (out_fmt != MXC_E4M3 && out_fmt != MXC_E2M1)) return MXC_ERR_ARG;
+    if (fn != MXC_FN_NONE && !z) return MXC_ERR_NULL;
+    Conv cv;
+    int rc = conv_init(&cv, p, fmt);
+    if (rc) return rc;
+    if (!fused_shape(cv, true)) return MXC_ERR_SHAPE;
+    if (!aligned16(wc) || !aligned16(ws) || !aligned16(gc) || !aligned16(gs) || !aligned16(gxc) ||
+        !aligned16(gxs) || (gx_act && !aligned16(gx_act)) || (fn != MXC_FN_NONE && !aligned16(z)))
+        return MXC_ERR_ALIGN;
+    FusedEpi q{gxc, gxs, out_fmt, fn, z};
+    rc = launch_conv_lean(cv, true, wc, ws, gc, gs, gx_act, MXC_CBF, (hipStream_t)stream, &q);
+    return rc == 1 ? MXC_ERR_SHAPE : rc;
+}
+
 size_t mxconv_naive_codes_bytes(int64_t lines, int64_t len, int fmt) {
     if (lines <= 0 || len <= 0 || (fmt != MXC_E4M3 && fmt != MXC_E2M1)) return 0;
     const long long lp = naive_line_len(len);

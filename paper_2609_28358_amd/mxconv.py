@@ -14,6 +14,7 @@ E4M3, E2M1 = 0, 1
 F32, BF16 = 0, 1
 NCHW, NHWC, CBF = 0, 1, 2
 ACT, WEIGHT = 0, 1
+FN_NONE, FN_RELU, FN_SILU = 0, 1, 2
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libmxconv.so")
@@ -52,6 +53,8 @@ def lib():
         "mxconv_fwd": (i32, [CP, i32, P, P, P, P, P, i32, P]),
         "mxconv_dgrad": (i32, [CP, i32, P, P, P, P, P, i32, P]),
         "mxconv_wgrad": (i32, [CP, i32, P, P, P, P, P, P, sz, P]),
+        "mxconv_fwd_quant": (i32, [CP, i32, P, P, P, P, i32, i32, P, P, P, P]),
+        "mxconv_dgrad_quant": (i32, [CP, i32, P, P, P, P, i32, P, i32, P, P, P, P]),
         "mxconv_naive_codes_bytes": (sz, [i64, i64, i32]),
         "mxconv_naive_scales_bytes": (sz, [i64, i64]),
         "mxconv_naive_im2col_f32": (i32, [CP, P, P, P]),
@@ -202,6 +205,33 @@ def wgrad(cv, gy, x, out=None, workspace=None, stream=None):
                               _ptr(x.codes), _ptr(x.scales), _ptr(gw), _ptr(workspace), wsz,
                               _stream(stream)), "mxconv_wgrad")
     return gw
+
+
+def fwd_quant(cv, w, x, fn=FN_NONE, out_fmt=None, out=None, act_out=None, stream=None):
+    """Forward with the quantizing epilogue: MX codes of fn(W * X) for
+    (n, cout, Ho, Wo); `act_out` (CBF fp32, optional) receives the values
+    that were quantized.  Returns the MxTensor."""
+    ho, wo = out_size(cv)
+    out_fmt = x.fmt if out_fmt is None else out_fmt
+    shape = (cv["n"], cv["cout"], ho, wo)
+    y = out if out is not None else MxTensor.empty(ACT, out_fmt, shape, x.codes.device)
+    _check(lib().mxconv_fwd_quant(ctypes.byref(conv_struct(cv)), x.fmt, _ptr(w.codes), _ptr(w.scales),
+                                  _ptr(x.codes), _ptr(x.scales), fn, out_fmt, _ptr(y.codes), _ptr(y.scales),
+                                  _ptr(act_out), _stream(stream)), "mxconv_fwd_quant")
+    return y
+
+
+def dgrad_quant(cv, w, gy, fn=FN_NONE, z=None, out_fmt=None, out=None, act_out=None, stream=None):
+    """Input gradient with the quantizing epilogue: MX codes of
+    (W^T * G_Y) . fn'(z) for (n, cin, h, w); z is the CBF fp32 pre-activation
+    of this layer's input (not needed for FN_NONE)."""
+    out_fmt = gy.fmt if out_fmt is None else out_fmt
+    shape = (cv["n"], cv["cin"], cv["h"], cv["w"])
+    g = out if out is not None else MxTensor.empty(ACT, out_fmt, shape, gy.codes.device)
+    _check(lib().mxconv_dgrad_quant(ctypes.byref(conv_struct(cv)), gy.fmt, _ptr(w.codes), _ptr(w.scales),
+                                    _ptr(gy.codes), _ptr(gy.scales), fn, _ptr(z), out_fmt, _ptr(g.codes),
+                                    _ptr(g.scales), _ptr(act_out), _stream(stream)), "mxconv_dgrad_quant")
+    return g
 
 
 # ---------------------------------------------------------------- naive comparator

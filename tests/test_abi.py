@@ -151,3 +151,35 @@ def test_naive_errors():
         assert fn(c, 3, *args, None) == -2
         assert fn(bad, 0, *args, None) == -3
         assert fn(c, 0, *args[:-1], ODD, None) == -4
+
+
+def test_fused_errors():
+    """mxconv_fwd_quant / mxconv_dgrad_quant: every call below fails validation."""
+    L = mx.lib()
+    c = ctypes.byref(mx.conv_struct(synth.conv_dict(32, 64, 64, 8, 8, 3, 1, 1)))
+    c16 = ctypes.byref(mx.conv_struct(synth.conv_dict(16, 64, 64, 8, 8, 3, 1, 1)))       # batch block 16
+    c5 = ctypes.byref(mx.conv_struct(synth.conv_dict(32, 64, 64, 8, 8, 5, 1, 2)))        # kernel width 5
+    c21 = ctypes.byref(mx.conv_struct(dict(n=32, cin=64, cout=64, h=8, w=8, kh=3, kw=3, sh=2, sw=1, ph=1, pw=1)))
+    f = L.mxconv_fwd_quant          # (cv, fmt, wc, ws, xc, xs, fn, out_fmt, yc, ys, y_act, stream)
+    assert f(None, 0, GOOD, GOOD, GOOD, GOOD, 0, 0, GOOD, GOOD, None, None) == -1
+    assert f(c, 0, GOOD, GOOD, GOOD, GOOD, 0, 0, None, GOOD, None, None) == -1
+    assert f(c, 0, GOOD, GOOD, GOOD, None, 0, 0, GOOD, GOOD, None, None) == -1
+    assert f(c, 0, GOOD, GOOD, GOOD, GOOD, 3, 0, GOOD, GOOD, None, None) == -2      # activation
+    assert f(c, 0, GOOD, GOOD, GOOD, GOOD, -1, 0, GOOD, GOOD, None, None) == -2
+    assert f(c, 0, GOOD, GOOD, GOOD, GOOD, 0, 2, GOOD, GOOD, None, None) == -2      # output format
+    assert f(c, 7, GOOD, GOOD, GOOD, GOOD, 0, 0, GOOD, GOOD, None, None) == -2      # operand format
+    assert f(c16, 0, GOOD, GOOD, GOOD, GOOD, 0, 0, GOOD, GOOD, None, None) == -3
+    assert f(c5, 0, GOOD, GOOD, GOOD, GOOD, 0, 0, GOOD, GOOD, None, None) == -3
+    assert f(c, 0, GOOD, GOOD, GOOD, GOOD, 0, 0, ODD, GOOD, None, None) == -4
+    assert f(c, 0, GOOD, GOOD, GOOD, GOOD, 2, 1, GOOD, GOOD, ODD, None) == -4
+    d = L.mxconv_dgrad_quant        # (cv, fmt, wc, ws, gc, gs, fn, z, out_fmt, gxc, gxs, gx_act, stream)
+    assert d(None, 0, GOOD, GOOD, GOOD, GOOD, 0, None, 0, GOOD, GOOD, None, None) == -1
+    assert d(c, 0, GOOD, GOOD, GOOD, GOOD, 1, None, 0, GOOD, GOOD, None, None) == -1   # ReLU needs z
+    assert d(c, 0, GOOD, GOOD, GOOD, GOOD, 2, None, 0, GOOD, GOOD, None, None) == -1   # SiLU needs z
+    assert d(c, 0, GOOD, GOOD, GOOD, GOOD, 0, None, 0, None, GOOD, None, None) == -1
+    assert d(c, 0, GOOD, GOOD, GOOD, GOOD, 4, GOOD, 0, GOOD, GOOD, None, None) == -2
+    assert d(c, 0, GOOD, GOOD, GOOD, GOOD, 1, GOOD, 3, GOOD, GOOD, None, None) == -2
+    assert d(c21, 0, GOOD, GOOD, GOOD, GOOD, 0, None, 0, GOOD, GOOD, None, None) == -3  # stride 2x1
+    assert d(c16, 0, GOOD, GOOD, GOOD, GOOD, 1, GOOD, 0, GOOD, GOOD, None, None) == -3
+    assert d(c, 0, GOOD, GOOD, GOOD, GOOD, 1, ODD, 0, GOOD, GOOD, None, None) == -4
+    assert d(c, 0, GOOD, GOOD, GOOD, GOOD, 0, None, 0, GOOD, GOOD, ODD, None) == -4

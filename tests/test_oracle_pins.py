@@ -626,3 +626,32 @@ def test_naive_step_quantizes_each_tensor_twice():
     total = oracle.counter_get()
     dac = t1["Dacapo"]
     assert total == dac[0] * x.numel() + dac[1] * w.numel() + dac[2] * gy.numel()
+
+
+# ------------------------------------------------------------ fused-epilogue activations
+def test_act_fn_special_values():
+    y = np.array([-3.0, -0.0, 0.0, 0.5, 2.0, 40.0, -40.0])
+    assert np.array_equal(oracle.act_fn(y, oracle.FN_NONE), y)
+    r = oracle.act_fn(y, oracle.FN_RELU)
+    assert np.array_equal(r, [0, 0, 0, 0.5, 2.0, 40.0, 0]) and not np.signbit(r[1])
+    s = oracle.act_fn(y, oracle.FN_SILU)
+    assert s[2] == 0 and abs(s[3] - 0.5 / (1 + np.exp(-0.5))) < 1e-15
+    assert abs(s[5] - 40.0) < 1e-15 and abs(s[6]) < 1e-15          # y and 0 far out on either side
+    assert abs(oracle.act_fn(np.array([-1e4]), oracle.FN_SILU)[0]) == 0.0   # exp overflow gives -0
+
+
+def test_act_grad_is_the_derivative():
+    # central differences of act_fn, away from ReLU's kink
+    rng = np.random.default_rng(5)
+    z = rng.normal(0, 3, 2000)
+    z = z[np.abs(z) > 1e-3]
+    h = 1e-6
+    for fn in (oracle.FN_NONE, oracle.FN_RELU, oracle.FN_SILU):
+        fd = (oracle.act_fn(z + h, fn) - oracle.act_fn(z - h, fn)) / (2 * h)
+        assert np.max(np.abs(fd - oracle.act_grad(z, fn))) < 1e-7, fn
+    g = oracle.act_grad(np.array([0.0, 50.0, -50.0]), oracle.FN_SILU)
+    assert g[0] == 0.5 and abs(g[1] - 1) < 1e-15 and abs(g[2]) < 1e-15
+    # SiLU' stays in [-0.1, 1.1]: the Lipschitz constant the fused tests use
+    zz = np.linspace(-20, 20, 200001)
+    gg = oracle.act_grad(zz, oracle.FN_SILU)
+    assert gg.max() < 1.1 and gg.min() > -0.1
