@@ -29,6 +29,7 @@ that it is read from HBM, not from the 256 MB last-level cache -- and
 """
 import argparse
 import json
+import math
 import os
 import sys
 import time
@@ -238,6 +239,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-naive", action="store_true", help="skip the naive comparator leg")
+    ap.add_argument("--no-fused", action="store_true", help="skip the fused-epilogue leg")
     ap.add_argument("--pmc-pass", action="store_true",
                     help="counter-collection pass: every op once in step order, then a copy of known size")
     ap.add_argument("--layers", default="all", help="comma list of layer indices (profiling aid)")
@@ -404,6 +406,54 @@ def main():
 
     naive = {} if args.no_naive else naive_leg(jobs, op_ms, mx, synth, dev, stream)
 
+    # Fused quantizing epilogues (outside the step): the forward with its
+    # output quantized in the epilogue (after SiLU, or none) against the
+    # forward writing fp32 followed by a quantize of that output; the input
+    # gradient likewise (SiLU' mask at a pre-activation z, or none).
+    def steady_ms(fn, kl=12):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(kl):
+                fn()
+        g.replay()
+        torch.cuda.synchronize()
+        r = statistics.median(replay_ms(g, 3) for _ in range(3)) / kl
+        del g
+        return r
+
+    fused = {}
+    if not args.no_fused:
+        for j in jobs:
+            cv, fmt = j["cv"], j["fmt"]
+            ho, wo = synth.out_hw(cv)
+            ysh, xsh = (cv["n"], cv["cout"], ho, wo), (cv["n"], cv["cin"], cv["h"], cv["w"])
+            yq = mx.MxTensor.empty(mx.ACT, fmt, ysh, dev)
+            gq = mx.MxTensor.empty(mx.ACT, fmt, xsh, dev)
+            z = j["x"]                                   # a CBF fp32 tensor of X's shape
+            t = {
+                "fwd_quant_silu": steady_ms(lambda: mx.fwd_quant(cv, j["qw"], j["qx"], fn=mx.FN_SILU, out=yq)),
+                "fwd_quant": steady_ms(lambda: mx.fwd_quant(cv, j["qw"], j["qx"], out=yq)),
+                "fwd_then_quantize": steady_ms(lambda: (run_op(j, "fwd"), mx.quantize(
+                    j["y"], mx.ACT, fmt, layout=mx.CBF, shape=ysh, out=yq))),
+                "dgrad_quant_silu": steady_ms(lambda: mx.dgrad_quant(cv, j["qw"], j["qg"], fn=mx.FN_SILU, z=z,
+                                                                     out=gq)),
+                "dgrad_quant": steady_ms(lambda: mx.dgrad_quant(cv, j["qw"], j["qg"], out=gq)),
+                "dgrad_then_quantize": steady_ms(lambda: (run_op(j, "dgrad"), mx.quantize(
+                    j["gx"], mx.ACT, fmt, layout=mx.CBF, shape=xsh, out=gq))),
+            }
+            W = mx.codes_bytes(mx.WEIGHT, fmt, *j["w"].shape) + mx.scales_bytes(mx.WEIGHT, fmt, *j["w"].shape)
+            Xq = mx.codes_bytes(mx.ACT, fmt, *xsh) + mx.scales_bytes(mx.ACT, fmt, *xsh)
+            Yq = mx.codes_bytes(mx.ACT, fmt, *ysh) + mx.scales_bytes(mx.ACT, fmt, *ysh)
+            ny, nx = 4.0 * math.prod(ysh), 4.0 * math.prod(xsh)
+            fl = j["nums"]["fwd"][0]
+            fused[j["name"]] = {k + "_ms": round(v, 4) for k, v in t.items()}
+            fused[j["name"]].update({
+                "fwd_bytes_fused": round(W + Xq + Yq), "fwd_bytes_unfused": round(W + Xq + 2 * ny + Yq),
+                "dgrad_bytes_fused": round(W + Yq + Xq), "dgrad_bytes_unfused": round(W + Yq + 2 * nx + Xq),
+                "fwd_quant_tflops": round(fl / (t["fwd_quant"] * 1e-3) / 1e12, 1),
+                "fwd_speedup": round(t["fwd_then_quantize"] / t["fwd_quant"], 2),
+                "dgrad_speedup": round(t["dgrad_then_quantize"] / t["dgrad_quant"], 2)})
+
     gemm_flops = sum(j["nums"][op][0] for j in jobs for op in ("fwd", "dgrad", "wgrad"))
     value = gemm_flops / (ms_step * 1e-3) / 1e12
 
@@ -449,6 +499,8 @@ def main():
     }
     if naive:
         out["vs_naive"] = naive
+    if fused:
+        out["fused_epilogues"] = fused
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline()
     print(json.dumps(out))

@@ -41,13 +41,19 @@ constexpr int LT = 256;
 __device__ __attribute__((aligned(16))) uint8_t g_zero_lean[1024];
 
 // Activation (forward epilogue) and its derivative (input-gradient epilogue).
+// SiLU uses the hardware exp2 and reciprocal (about 1 ulp each): the
+// logistic s(y) = 1 / (1 + 2^(-y log2 e)); exp2 overflows to +inf for very
+// negative y, where s = 0 and SiLU = -0.
+__device__ __forceinline__ float logistic(float y) {
+    return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-y * 1.4426950408889634f));
+}
 __device__ __forceinline__ float fn_apply(int fn, float y) {
     if (fn == MXC_FN_RELU) return y > 0.0f ? y : 0.0f;
-    return y / (1.0f + expf(-y));                               // SiLU
+    return y * logistic(y);                                     // SiLU
 }
 __device__ __forceinline__ float fn_grad(int fn, float z) {
     if (fn == MXC_FN_RELU) return z > 0.0f ? 1.0f : 0.0f;
-    const float s = 1.0f / (1.0f + expf(-z));                   // SiLU' = s (1 + z (1 - s))
+    const float s = logistic(z);                                // SiLU' = s (1 + z (1 - s))
     return s * (1.0f + z * (1.0f - s));
 }
 
@@ -362,7 +368,11 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
     if (p.qcodes) {
         // ---- fused quantizing epilogue: acc[rb][cn] is one whole MX block of
         // the output (32 channels x 32 samples at one pixel); lane l holds
-        // channel l % 32 and samples 8 (e / 4) + 4 (l / 32) + e % 4
+        // channel l % 32 and samples 8 (e / 4) + 4 (l / 32) + e % 4.  The
+        // codes are assembled in 1 KB of LDS per wave in stored order and
+        // written as one contiguous run (16 or 8 bytes per lane).
+        __syncthreads();                                 // every wave is done with the stage buffers
+        uint8_t* const ep = smem + wave * 1024;
         const int r = lane & 31;
 #pragma unroll
         for (int cn = 0; cn < PW; cn++) {
@@ -403,26 +413,27 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                 uint32_t m = 0;
 #pragma unroll
                 for (int e = 0; e < 16; e++) m = max(m, __float_as_uint(v[e]) & 0x7FFFFFFFu);
-#pragma unroll
-                for (int off = 32; off >= 1; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off));
+                m = wave_max_u32(m);
                 const bool q8 = p.qfmt == MXC_E4M3;
                 const uint32_t sc = q8 ? scale_code_from_bits<8>(m) : scale_code_from_bits<2>(m);
                 const float inv = inv_scale(sc);
                 const bool bad = sc == 0xFFu;
                 if (lane == 0) p.qscales[pix * p.q_ncb + cb] = (uint8_t)sc;
                 if (q8) {
-                    uint8_t* blk = p.qcodes + (pix * p.q_ncb + cb) * 1024 + r * 32 + 4 * h;
 #pragma unroll
                     for (int e4 = 0; e4 < 4; e4++)
-                        *(uint32_t*)(blk + 8 * e4) =
+                        *(uint32_t*)(ep + r * 32 + 8 * e4 + 4 * h) =
                             bad ? 0u : pack4_e4m3(make_float4(v[4 * e4], v[4 * e4 + 1], v[4 * e4 + 2], v[4 * e4 + 3]), inv);
+                    const uint4 run = *(const uint4*)(ep + lane * 16);
+                    *(uint4*)(p.qcodes + (pix * p.q_ncb + cb) * 1024 + lane * 16) = run;
                 } else {
-                    uint8_t* blk = p.qcodes + (pix * p.q_ncb + cb) * 512 + r * 16 + 2 * h;
 #pragma unroll
                     for (int e4 = 0; e4 < 4; e4++)
-                        *(unsigned short*)(blk + 4 * e4) =
+                        *(unsigned short*)(ep + r * 16 + 4 * e4 + 2 * h) =
                             bad ? (unsigned short)0
                                 : pack4_e2m1(make_float4(v[4 * e4], v[4 * e4 + 1], v[4 * e4 + 2], v[4 * e4 + 3]), inv);
+                    const uint2 run = *(const uint2*)(ep + lane * 8);
+                    *(uint2*)(p.qcodes + (pix * p.q_ncb + cb) * 512 + lane * 8) = run;
                 }
             }
         }

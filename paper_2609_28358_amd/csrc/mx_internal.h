@@ -203,6 +203,24 @@ __device__ __forceinline__ void vm_wait_stage(int later) {
     else vm_wait<2 * PER>();
 }
 
+// Maximum of a 32-bit value over the 64 lanes of a wave, returned to every
+// lane: DPP swaps within quads (lanes 1032 and 2301 orders), a mirror within
+// each 8 and each 16 lanes (after which every lane of a 16-lane row holds the
+// row's maximum), then the four row maxima read as scalars.  No LDS traffic
+// and no waits, unlike a shuffle through ds_bpermute.  The whole wave must be
+// active.
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t m) {
+    m = max(m, (uint32_t)__builtin_amdgcn_mov_dpp((int)m, 0xB1, 0xF, 0xF, false));   // quad_perm 1,0,3,2
+    m = max(m, (uint32_t)__builtin_amdgcn_mov_dpp((int)m, 0x4E, 0xF, 0xF, false));   // quad_perm 2,3,0,1
+    m = max(m, (uint32_t)__builtin_amdgcn_mov_dpp((int)m, 0x141, 0xF, 0xF, false));  // row_half_mirror
+    m = max(m, (uint32_t)__builtin_amdgcn_mov_dpp((int)m, 0x140, 0xF, 0xF, false));  // row_mirror
+    const uint32_t a = (uint32_t)__builtin_amdgcn_readlane((int)m, 0);
+    const uint32_t b = (uint32_t)__builtin_amdgcn_readlane((int)m, 16);
+    const uint32_t c = (uint32_t)__builtin_amdgcn_readlane((int)m, 32);
+    const uint32_t d = (uint32_t)__builtin_amdgcn_readlane((int)m, 48);
+    return max(max(a, b), max(c, d));
+}
+
 // LDS transposing reads (16-lane groups).
 //  tr8: lane i gets byte (i%8) of the 8-byte chunks addressed by lanes 2q + i/8, q = 0..7.
 //  tr4: lane i gets nibble i of the chunks addressed by lanes q, q = 0..15.

@@ -222,8 +222,7 @@ __global__ __launch_bounds__(QT) void quantize_block_kernel(const void* __restri
         m = max(m, __float_as_uint(x[q].z) & 0x7FFFFFFFu);
         m = max(m, __float_as_uint(x[q].w) & 0x7FFFFFFFu);
     }
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off));
+    m = wave_max_u32(m);
     constexpr int EMAX = FMT == MXC_E4M3 ? 8 : 2;
     const uint32_t sc = scale_code_from_bits<EMAX>(m);
     if (lane == 0) scales[blk] = (uint8_t)sc;
