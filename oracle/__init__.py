@@ -23,7 +23,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "mxoracle.c")
 _LIB = os.path.join(_HERE, "libmxoracle.so")
 
-E4M3, E2M1 = 0, 1
+E4M3, E2M1, E2M3, E3M2 = 0, 1, 2, 3
+BITS = {E4M3: 8, E2M1: 4, E2M3: 6, E3M2: 6}
 NCHW, NHWC, CBF = 0, 1, 2
 ACT, WEIGHT = 0, 1
 
@@ -60,15 +61,15 @@ def load():
         "o_im2col_cbf": (i32, [P, i32, P, P, P, P]),
         "o_im2col_codes_bytes": (i64, [P, i32]),
         "o_im2col_scales_bytes": (i64, [P, i32]),
-        "o_fwd": (i32, [P, i32, P, P, P, P, P, P]),
-        "o_wgrad": (i32, [P, i32, P, P, P, P, P, P]),
-        "o_dgrad": (i32, [P, i32, P, P, P, P, P, P]),
+        "o_fwd": (i32, [P, i32, i32, P, P, P, P, P, P]),
+        "o_wgrad": (i32, [P, i32, i32, P, P, P, P, P, P]),
+        "o_dgrad": (i32, [P, i32, i32, P, P, P, P, P, P]),
         "o_direct_fwd": (i32, [P, P, P, P]),
         "o_direct_dgrad": (i32, [P, P, P, P]),
         "o_direct_wgrad": (i32, [P, P, P, P]),
-        "o_fwd_at": (i32, [P, i32, P, P, P, P, P, i64, P, P]),
-        "o_dgrad_at": (i32, [P, i32, P, P, P, P, P, i64, P, P]),
-        "o_wgrad_at": (i32, [P, i32, P, P, P, P, P, i64, P, P]),
+        "o_fwd_at": (i32, [P, i32, i32, P, P, P, P, P, i64, P, P]),
+        "o_dgrad_at": (i32, [P, i32, i32, P, P, P, P, P, i64, P, P]),
+        "o_wgrad_at": (i32, [P, i32, i32, P, P, P, P, P, i64, P, P]),
         "o_quantize_1d": (i32, [P, i64, i64, i32, i32, P, P]),
         "o_dequant_1d": (i32, [P, P, i64, i64, i32, i32, P]),
         "o_naive_im2col": (i32, [P, P, P]),
@@ -174,29 +175,40 @@ def im2col_cbf(conv, fmt, xcodes, xscales):
     return cc, cs
 
 
+def _fmts(fmt):
+    """One element format for both operands, or a pair (first operand's,
+    second operand's), in the argument order of the call."""
+    if isinstance(fmt, (tuple, list)):
+        return int(fmt[0]), int(fmt[1])
+    return int(fmt), int(fmt)
+
+
 def _gemm(name, conv, fmt, a, b, shape):
     lib = load()
     p = _conv_params(conv)
     out = np.zeros(shape, dtype=np.float64)
     sabs = np.zeros(shape, dtype=np.float64)
     (ac, as_), (bc, bs) = a, b
-    _check(getattr(lib, name)(_ptr(p), fmt, _ptr(np.ascontiguousarray(ac)),
+    _check(getattr(lib, name)(_ptr(p), *_fmts(fmt), _ptr(np.ascontiguousarray(ac)),
                               _ptr(np.ascontiguousarray(as_)), _ptr(np.ascontiguousarray(bc)),
                               _ptr(np.ascontiguousarray(bs)), _ptr(out), _ptr(sabs)), name)
     return out, sabs
 
 
 def fwd(conv, fmt, w, x):
-    """w, x: (codes, scales) pairs.  Returns (Y NCHW fp64, sum|products|)."""
+    """w, x: (codes, scales) pairs; fmt: one format, or (W's, X's).
+    Returns (Y NCHW fp64, sum|products|)."""
     ho, wo = conv_out(conv)
     return _gemm("o_fwd", conv, fmt, w, x, (conv["n"], conv["cout"], ho, wo))
 
 
 def dgrad(conv, fmt, w, gy):
+    """fmt: one format, or (W's, G_Y's)."""
     return _gemm("o_dgrad", conv, fmt, w, gy, (conv["n"], conv["cin"], conv["h"], conv["w"]))
 
 
 def wgrad(conv, fmt, gy, x):
+    """fmt: one format, or (G_Y's, X's)."""
     return _gemm("o_wgrad", conv, fmt, gy, x, (conv["cout"], conv["cin"], conv["kh"], conv["kw"]))
 
 
@@ -207,7 +219,7 @@ def _at(name, conv, fmt, a, b, idx):
     out = np.zeros(len(idx), dtype=np.float64)
     sabs = np.zeros(len(idx), dtype=np.float64)
     (ac, as_), (bc, bs) = a, b
-    _check(getattr(lib, name)(_ptr(p), fmt, _ptr(np.ascontiguousarray(ac)),
+    _check(getattr(lib, name)(_ptr(p), *_fmts(fmt), _ptr(np.ascontiguousarray(ac)),
                               _ptr(np.ascontiguousarray(as_)), _ptr(np.ascontiguousarray(bc)),
                               _ptr(np.ascontiguousarray(bs)), _ptr(idx), len(idx), _ptr(out),
                               _ptr(sabs)), name)
@@ -257,7 +269,7 @@ def quantize_1d(m, direction, fmt):
     lib = load()
     m = np.ascontiguousarray(m, dtype=np.float32)
     rows, cols = m.shape
-    bits = 8 if fmt == E4M3 else 4
+    bits = BITS[fmt]
     codes = np.zeros((rows * cols * bits + 7) // 8, dtype=np.uint8)
     if direction == 0:
         scales = np.zeros(rows * ((cols + 31) // 32), dtype=np.uint8)

@@ -10,9 +10,12 @@
  * Everything here is a plain, slow, obviously-correct definition written
  * in fp64 loops (OpenMP only splits the outermost loop of the big ones):
  *
- *   o_encode / o_decode   one element to/from FP8 E4M3 or FP4 E2M1 (OCP MX
- *                         element formats; the paper's number formats are
- *                         introduced in Sec. II-D and Sec. III-A).
+ *   o_encode / o_decode   one element to/from FP8 E4M3, FP4 E2M1, FP6 E2M3
+ *                         or FP6 E3M2 (OCP MX element formats; the paper's
+ *                         number formats are introduced in Sec. II-D and
+ *                         Sec. III-A, its FP6 variants in Sec. V: E3M2
+ *                         activations for MicroQonv+, E2M3 for the "-6"
+ *                         methods).
  *   o_quantize            microscaling quantizer, Sec. III-A Eqs. (4)-(6) in
  *                         its OCP-MX form: one E8M0 power-of-two scale per
  *                         square block (Sec. IV-B), elements rounded to
@@ -24,7 +27,9 @@
  *   o_fwd / o_wgrad /     the three GEMMs of Sec. IV-B,
  *   o_dgrad                 Y_f = W_f X',  G_Wf = G_Yf X'^T,  G_X' = W_f^T G_Yf,
  *                         on dequantized operands, with the reordering back to
- *                         NCHW/OIHW (a col2im scatter-add for G_X').
+ *                         NCHW/OIHW (a col2im scatter-add for G_X').  Each
+ *                         operand carries its own element format (MicroQonv+
+ *                         pairs FP4 weights and gradients with FP6 activations).
  *   o_direct_*            brute-force definitions of Eqs. (1)-(3).
  *   o_*_at                single outputs of Eqs. (1)-(3), for sampled checks
  *                         at sizes where the full GEMMs are too slow.
@@ -37,15 +42,22 @@
  * Readings of the paper that this file fixes (the paper uses NVFP with 8x8
  * blocks; the build uses OCP MX):
  *   - scale code = clamp(floor(log2 amax) - emax, -127, 127) + 127 where
- *     emax is 8 for E4M3 and 2 for E2M1; amax == 0 gives code 0; a block
- *     holding a NaN or infinity gets code 0xFF and all-zero element codes.
+ *     emax is 8 for E4M3, 2 for E2M1 and E2M3, 4 for E3M2; amax == 0 gives
+ *     code 0; a block holding a NaN or infinity gets code 0xFF and all-zero
+ *     element codes.
  *   - elements: x * 2^-s rounded to nearest, ties to even, magnitudes above
- *     the format maximum saturate (448 or 6); the sign of zero is kept.
+ *     the format maximum saturate (448, 6, 7.5 or 28); the sign of zero is
+ *     kept.
  *   - block = 32 channels x Bn batch samples at one pixel, Bn = min(32, N);
  *     for weights 32 input channels x 32 output channels at one tap.
  *   - code layout [N/Bn][H][W][Cp][Bn] (Bn fastest), scales
  *     [N/Bn][H][W][Cp/32]; FP4 packs two consecutive codes per byte, the
  *     even one in the low nibble.  Cp = C rounded up to 32; padding is +0.
+ *   - FP6 codes are packed as one little-endian bit string: the code at
+ *     linear position p occupies bits 6p .. 6p+5 (bit 0 = least significant
+ *     bit of byte 0), so 32 samples of one channel take 24 bytes.  The same
+ *     rule with 4 bits is the FP4 nibble order above.  FP6 activations need
+ *     Bn >= 4 so that every channel row starts on a byte.
  */
 #include <math.h>
 #include <stdint.h>
@@ -56,7 +68,7 @@
 #include <omp.h>
 #endif
 
-enum { O_E4M3 = 0, O_E2M1 = 1 };
+enum { O_E4M3 = 0, O_E2M1 = 1, O_E2M3 = 2, O_E3M2 = 3 };
 enum { O_NCHW = 0, O_NHWC = 1, O_CBF = 2 };
 enum { O_ACT = 0, O_WEIGHT = 1 };
 
@@ -80,6 +92,16 @@ static int fmt_get(int fmt, o_fmt *f)
     if (fmt == O_E2M1) {
         f->bits = 4; f->mbits = 1; f->bias = 1; f->emax = 2;
         f->maxval = 6.0; f->min_normal = 1.0; f->quantum = 0.5;
+        return 0;
+    }
+    if (fmt == O_E2M3) {                /* max 2^2 * 1.875, no inf / NaN */
+        f->bits = 6; f->mbits = 3; f->bias = 1; f->emax = 2;
+        f->maxval = 7.5; f->min_normal = 1.0; f->quantum = 0.125;
+        return 0;
+    }
+    if (fmt == O_E3M2) {                /* max 2^4 * 1.75, no inf / NaN */
+        f->bits = 6; f->mbits = 2; f->bias = 3; f->emax = 4;
+        f->maxval = 28.0; f->min_normal = 0.25; f->quantum = 0.0625;
         return 0;
     }
     return -2;
@@ -171,6 +193,7 @@ static int geom_init(o_geom *g, int role, int fmt, int n, int c, int h, int w)
         }
         g->np = n;
         if (fmt == O_E2M1 && g->bn == 1) return -3;
+        if (f.bits == 6 && g->bn < 4) return -3;
     } else {
         return -2;
     }
@@ -182,7 +205,7 @@ int64_t o_codes_bytes(int role, int fmt, int n, int c, int h, int w)
     o_geom g;
     if (geom_init(&g, role, fmt, n, c, h, w)) return -1;
     int64_t elems = (int64_t)g.np * g.h * g.w * g.cp;
-    return g.bits == 8 ? elems : elems / 2;
+    return elems * g.bits / 8;
 }
 
 int64_t o_scales_bytes(int role, int fmt, int n, int c, int h, int w)
@@ -206,6 +229,15 @@ static int64_t scale_pos(const o_geom *g, int nb, int hh, int ww, int cb)
 static void put_code(uint8_t *codes, int bits, int64_t pos, int code)
 {
     if (bits == 8) { codes[pos] = (uint8_t)code; return; }
+    if (bits == 6) {                    /* bit string, bit 6*pos + t = bit t of the code */
+        for (int t = 0; t < 6; t++) {
+            int64_t bit = 6 * pos + t;
+            uint8_t m = (uint8_t)(1u << (bit & 7));
+            if ((code >> t) & 1) codes[bit >> 3] |= m;
+            else codes[bit >> 3] &= (uint8_t)~m;
+        }
+        return;
+    }
     uint8_t *b = &codes[pos >> 1];
     if (pos & 1) *b = (uint8_t)((*b & 0x0F) | (code << 4));
     else         *b = (uint8_t)((*b & 0xF0) | (code & 0x0F));
@@ -214,6 +246,14 @@ static void put_code(uint8_t *codes, int bits, int64_t pos, int code)
 static int get_code(const uint8_t *codes, int bits, int64_t pos)
 {
     if (bits == 8) return codes[pos];
+    if (bits == 6) {
+        int code = 0;
+        for (int t = 0; t < 6; t++) {
+            int64_t bit = 6 * pos + t;
+            code |= ((codes[bit >> 3] >> (bit & 7)) & 1) << t;
+        }
+        return code;
+    }
     uint8_t b = codes[pos >> 1];
     return (pos & 1) ? (b >> 4) : (b & 0x0F);
 }
@@ -466,18 +506,20 @@ static double *build_gyf(const o_conv *cv, int fmt, const uint8_t *gcodes, const
     return gf;
 }
 
-/* Forward: Y_f = W_f X', reordered to Y[n][co][ho][wo].  sabs (optional)
- * receives sum_k |W_f[co][k] X'[k][col]|, the scale of the rounding error. */
-int o_fwd(const int *p, int fmt, const uint8_t *wcodes, const uint8_t *wscales,
+/* Forward: Y_f = W_f X', reordered to Y[n][co][ho][wo]; W in element format
+ * wfmt, X in xfmt.  sabs (optional) receives sum_k |W_f[co][k] X'[k][col]|,
+ * the scale of the rounding error. */
+int o_fwd(const int *p, int wfmt, int xfmt, const uint8_t *wcodes, const uint8_t *wscales,
           const uint8_t *xcodes, const uint8_t *xscales, double *y, double *sabs)
 {
     o_conv cv;
     o_geom g;
     int rc = conv_init(&cv, p);
     if (rc) return rc;
-    if ((rc = geom_init(&g, O_ACT, fmt, cv.n, cv.cin, cv.h, cv.w))) return rc;
-    double *xcol = build_xcol(&cv, fmt, xcodes, xscales);
-    double *wf = build_wf(&cv, fmt, wcodes, wscales);
+    if ((rc = geom_init(&g, O_ACT, xfmt, cv.n, cv.cin, cv.h, cv.w))) return rc;
+    if ((rc = geom_init(&g, O_WEIGHT, wfmt, cv.cout, cv.cin, cv.kh, cv.kw))) return rc;
+    double *xcol = build_xcol(&cv, xfmt, xcodes, xscales);
+    double *wf = build_wf(&cv, wfmt, wcodes, wscales);
     int64_t K = (int64_t)cv.kh * cv.kw * cv.cin, NC = (int64_t)cv.ho * cv.wo * cv.n;
     #pragma omp parallel for schedule(dynamic)
     for (int co = 0; co < cv.cout; co++) {
@@ -504,17 +546,19 @@ int o_fwd(const int *p, int fmt, const uint8_t *wcodes, const uint8_t *wscales,
     return 0;
 }
 
-/* Weight gradient: G_Wf = G_Yf X'^T, reordered to G_W[co][ci][kh][kw]. */
-int o_wgrad(const int *p, int fmt, const uint8_t *gcodes, const uint8_t *gscales,
+/* Weight gradient: G_Wf = G_Yf X'^T, reordered to G_W[co][ci][kh][kw]; G_Y in
+ * element format gfmt, X in xfmt. */
+int o_wgrad(const int *p, int gfmt, int xfmt, const uint8_t *gcodes, const uint8_t *gscales,
             const uint8_t *xcodes, const uint8_t *xscales, double *gw, double *sabs)
 {
     o_conv cv;
     o_geom g;
     int rc = conv_init(&cv, p);
     if (rc) return rc;
-    if ((rc = geom_init(&g, O_ACT, fmt, cv.n, cv.cin, cv.h, cv.w))) return rc;
-    double *xcol = build_xcol(&cv, fmt, xcodes, xscales);
-    double *gf = build_gyf(&cv, fmt, gcodes, gscales);
+    if ((rc = geom_init(&g, O_ACT, xfmt, cv.n, cv.cin, cv.h, cv.w))) return rc;
+    if ((rc = geom_init(&g, O_ACT, gfmt, cv.n, cv.cout, cv.ho, cv.wo))) return rc;
+    double *xcol = build_xcol(&cv, xfmt, xcodes, xscales);
+    double *gf = build_gyf(&cv, gfmt, gcodes, gscales);
     int64_t K = (int64_t)cv.kh * cv.kw * cv.cin, NC = (int64_t)cv.ho * cv.wo * cv.n;
     #pragma omp parallel for schedule(dynamic) collapse(2)
     for (int co = 0; co < cv.cout; co++)
@@ -537,17 +581,19 @@ int o_wgrad(const int *p, int fmt, const uint8_t *gcodes, const uint8_t *gscales
 }
 
 /* Input gradient: G_X' = W_f^T G_Yf, then the col2im scatter-add that turns
- * the (Kh Kw Cin) x (Ho Wo N) matrix back into G_X[n][ci][h][w]. */
-int o_dgrad(const int *p, int fmt, const uint8_t *wcodes, const uint8_t *wscales,
+ * the (Kh Kw Cin) x (Ho Wo N) matrix back into G_X[n][ci][h][w]; W in element
+ * format wfmt, G_Y in gfmt. */
+int o_dgrad(const int *p, int wfmt, int gfmt, const uint8_t *wcodes, const uint8_t *wscales,
             const uint8_t *gcodes, const uint8_t *gscales, double *gx, double *sabs)
 {
     o_conv cv;
     o_geom g;
     int rc = conv_init(&cv, p);
     if (rc) return rc;
-    if ((rc = geom_init(&g, O_ACT, fmt, cv.n, cv.cout, cv.ho, cv.wo))) return rc;
-    double *wf = build_wf(&cv, fmt, wcodes, wscales);
-    double *gf = build_gyf(&cv, fmt, gcodes, gscales);
+    if ((rc = geom_init(&g, O_ACT, gfmt, cv.n, cv.cout, cv.ho, cv.wo))) return rc;
+    if ((rc = geom_init(&g, O_WEIGHT, wfmt, cv.cout, cv.cin, cv.kh, cv.kw))) return rc;
+    double *wf = build_wf(&cv, wfmt, wcodes, wscales);
+    double *gf = build_gyf(&cv, gfmt, gcodes, gscales);
     int64_t K = (int64_t)cv.kh * cv.kw * cv.cin, NC = (int64_t)cv.ho * cv.wo * cv.n;
     double *gcol = (double *)malloc(sizeof(double) * (size_t)(K * NC));
     double *scol = (double *)malloc(sizeof(double) * (size_t)(K * NC));
@@ -678,7 +724,7 @@ static double mx_elem(const uint8_t *codes, const uint8_t *scales, const o_geom 
 }
 
 /* idx: cnt x 4 ints (n, co, ho, wo); out/sabs: cnt doubles */
-int o_fwd_at(const int *p, int fmt, const uint8_t *wcodes, const uint8_t *wscales,
+int o_fwd_at(const int *p, int wfmt, int xfmt, const uint8_t *wcodes, const uint8_t *wscales,
              const uint8_t *xcodes, const uint8_t *xscales, const int *idx, int64_t cnt,
              double *out, double *sabs)
 {
@@ -686,8 +732,8 @@ int o_fwd_at(const int *p, int fmt, const uint8_t *wcodes, const uint8_t *wscale
     o_geom gw, gx;
     int rc = conv_init(&cv, p);
     if (rc) return rc;
-    if ((rc = geom_init(&gw, O_WEIGHT, fmt, cv.cout, cv.cin, cv.kh, cv.kw))) return rc;
-    if ((rc = geom_init(&gx, O_ACT, fmt, cv.n, cv.cin, cv.h, cv.w))) return rc;
+    if ((rc = geom_init(&gw, O_WEIGHT, wfmt, cv.cout, cv.cin, cv.kh, cv.kw))) return rc;
+    if ((rc = geom_init(&gx, O_ACT, xfmt, cv.n, cv.cin, cv.h, cv.w))) return rc;
     #pragma omp parallel for schedule(dynamic)
     for (int64_t i = 0; i < cnt; i++) {
         int nn = idx[4 * i], co = idx[4 * i + 1], oh = idx[4 * i + 2], ow = idx[4 * i + 3];
@@ -697,8 +743,8 @@ int o_fwd_at(const int *p, int fmt, const uint8_t *wcodes, const uint8_t *wscale
                 for (int b = 0; b < cv.kw; b++) {
                     int ih = oh * cv.sh + a - cv.ph, iw = ow * cv.sw + b - cv.pw;
                     if (ih < 0 || ih >= cv.h || iw < 0 || iw >= cv.w) continue;
-                    double t = mx_elem(wcodes, wscales, &gw, fmt, co, ci, a, b) *
-                               mx_elem(xcodes, xscales, &gx, fmt, nn, ci, ih, iw);
+                    double t = mx_elem(wcodes, wscales, &gw, wfmt, co, ci, a, b) *
+                               mx_elem(xcodes, xscales, &gx, xfmt, nn, ci, ih, iw);
                     s += t; sa += fabs(t);
                 }
         out[i] = s; sabs[i] = sa;
@@ -707,7 +753,7 @@ int o_fwd_at(const int *p, int fmt, const uint8_t *wcodes, const uint8_t *wscale
 }
 
 /* idx: cnt x 4 ints (n, ci, h, w) */
-int o_dgrad_at(const int *p, int fmt, const uint8_t *wcodes, const uint8_t *wscales,
+int o_dgrad_at(const int *p, int wfmt, int gfmt, const uint8_t *wcodes, const uint8_t *wscales,
                const uint8_t *gcodes, const uint8_t *gscales, const int *idx, int64_t cnt,
                double *out, double *sabs)
 {
@@ -715,8 +761,8 @@ int o_dgrad_at(const int *p, int fmt, const uint8_t *wcodes, const uint8_t *wsca
     o_geom gw, gg;
     int rc = conv_init(&cv, p);
     if (rc) return rc;
-    if ((rc = geom_init(&gw, O_WEIGHT, fmt, cv.cout, cv.cin, cv.kh, cv.kw))) return rc;
-    if ((rc = geom_init(&gg, O_ACT, fmt, cv.n, cv.cout, cv.ho, cv.wo))) return rc;
+    if ((rc = geom_init(&gw, O_WEIGHT, wfmt, cv.cout, cv.cin, cv.kh, cv.kw))) return rc;
+    if ((rc = geom_init(&gg, O_ACT, gfmt, cv.n, cv.cout, cv.ho, cv.wo))) return rc;
     #pragma omp parallel for schedule(dynamic)
     for (int64_t i = 0; i < cnt; i++) {
         int nn = idx[4 * i], ci = idx[4 * i + 1], ih = idx[4 * i + 2], iw = idx[4 * i + 3];
@@ -728,8 +774,8 @@ int o_dgrad_at(const int *p, int fmt, const uint8_t *wcodes, const uint8_t *wsca
                     if (th < 0 || tw < 0 || th % cv.sh || tw % cv.sw) continue;
                     int oh = th / cv.sh, ow = tw / cv.sw;
                     if (oh >= cv.ho || ow >= cv.wo) continue;
-                    double t = mx_elem(wcodes, wscales, &gw, fmt, co, ci, a, b) *
-                               mx_elem(gcodes, gscales, &gg, fmt, nn, co, oh, ow);
+                    double t = mx_elem(wcodes, wscales, &gw, wfmt, co, ci, a, b) *
+                               mx_elem(gcodes, gscales, &gg, gfmt, nn, co, oh, ow);
                     s += t; sa += fabs(t);
                 }
         out[i] = s; sabs[i] = sa;
@@ -738,7 +784,7 @@ int o_dgrad_at(const int *p, int fmt, const uint8_t *wcodes, const uint8_t *wsca
 }
 
 /* idx: cnt x 4 ints (co, ci, kh, kw) */
-int o_wgrad_at(const int *p, int fmt, const uint8_t *gcodes, const uint8_t *gscales,
+int o_wgrad_at(const int *p, int gfmt, int xfmt, const uint8_t *gcodes, const uint8_t *gscales,
                const uint8_t *xcodes, const uint8_t *xscales, const int *idx, int64_t cnt,
                double *out, double *sabs)
 {
@@ -746,8 +792,8 @@ int o_wgrad_at(const int *p, int fmt, const uint8_t *gcodes, const uint8_t *gsca
     o_geom gx, gg;
     int rc = conv_init(&cv, p);
     if (rc) return rc;
-    if ((rc = geom_init(&gx, O_ACT, fmt, cv.n, cv.cin, cv.h, cv.w))) return rc;
-    if ((rc = geom_init(&gg, O_ACT, fmt, cv.n, cv.cout, cv.ho, cv.wo))) return rc;
+    if ((rc = geom_init(&gx, O_ACT, xfmt, cv.n, cv.cin, cv.h, cv.w))) return rc;
+    if ((rc = geom_init(&gg, O_ACT, gfmt, cv.n, cv.cout, cv.ho, cv.wo))) return rc;
     #pragma omp parallel for schedule(dynamic)
     for (int64_t i = 0; i < cnt; i++) {
         int co = idx[4 * i], ci = idx[4 * i + 1], a = idx[4 * i + 2], b = idx[4 * i + 3];
@@ -757,8 +803,8 @@ int o_wgrad_at(const int *p, int fmt, const uint8_t *gcodes, const uint8_t *gsca
                 for (int ow = 0; ow < cv.wo; ow++) {
                     int ih = oh * cv.sh + a - cv.ph, iw = ow * cv.sw + b - cv.pw;
                     if (ih < 0 || ih >= cv.h || iw < 0 || iw >= cv.w) continue;
-                    double t = mx_elem(gcodes, gscales, &gg, fmt, nn, co, oh, ow) *
-                               mx_elem(xcodes, xscales, &gx, fmt, nn, ci, ih, iw);
+                    double t = mx_elem(gcodes, gscales, &gg, gfmt, nn, co, oh, ow) *
+                               mx_elem(xcodes, xscales, &gx, xfmt, nn, ci, ih, iw);
                     s += t; sa += fabs(t);
                 }
         out[i] = s; sabs[i] = sa;

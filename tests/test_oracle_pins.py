@@ -19,9 +19,12 @@ import oracle
 from paper_2609_28358_amd import synth
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
-FMTS = {"E4M3": oracle.E4M3, "E2M1": oracle.E2M1}
-EMAX = {oracle.E4M3: 8, oracle.E2M1: 2}
-MAXV = {oracle.E4M3: 448.0, oracle.E2M1: 6.0}
+FMTS = {"E4M3": oracle.E4M3, "E2M1": oracle.E2M1, "E2M3": oracle.E2M3, "E3M2": oracle.E3M2}
+ALL_FMTS = [oracle.E4M3, oracle.E2M1, oracle.E2M3, oracle.E3M2]
+# OCP MX element formats: emax, largest finite magnitude, code width
+EMAX = {oracle.E4M3: 8, oracle.E2M1: 2, oracle.E2M3: 2, oracle.E3M2: 4}
+MAXV = {oracle.E4M3: 448.0, oracle.E2M1: 6.0, oracle.E2M3: 7.5, oracle.E3M2: 28.0}
+BITS = {oracle.E4M3: 8, oracle.E2M1: 4, oracle.E2M3: 6, oracle.E3M2: 6}
 
 
 def _parse_num(t):
@@ -46,8 +49,15 @@ def _golden_blocks():
 
 
 def _code_at(codes, fmt, pos):
+    """Stated code packing (a spec, not the method): FP8 one byte per code,
+    FP4 two per byte (even position low), FP6 a little-endian bit string
+    with the code at position p in bits 6p .. 6p+5."""
     if fmt == oracle.E4M3:
         return int(codes[pos])
+    if BITS[fmt] == 6:
+        bit = 6 * pos
+        word = int(codes[bit // 8]) | (int(codes[bit // 8 + 1]) << 8 if bit // 8 + 1 < len(codes) else 0)
+        return (word >> (bit % 8)) & 0x3F
     b = int(codes[pos // 2])
     return (b >> 4) if pos % 2 else (b & 0xF)
 
@@ -75,7 +85,18 @@ def _grid(fmt):
         u = torch.arange(0, 0x7F, dtype=torch.uint8)       # 0x7F is NaN
         v = u.view(torch.float8_e4m3fn).double()
         return list(zip(u.tolist(), v.tolist()))
-    mags = [0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0]         # E2M1 by definition
+    if fmt == oracle.E2M1:
+        mags = [0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0]     # E2M1 by definition
+    elif fmt == oracle.E2M3:                                 # OCP MX FP6 E2M3, codes 0..31
+        mags = [0.0, 0.125, 0.25, 0.375, 0.5, 0.625, 0.75, 0.875,
+                1.0, 1.125, 1.25, 1.375, 1.5, 1.625, 1.75, 1.875,
+                2.0, 2.25, 2.5, 2.75, 3.0, 3.25, 3.5, 3.75,
+                4.0, 4.5, 5.0, 5.5, 6.0, 6.5, 7.0, 7.5]
+    else:                                                    # OCP MX FP6 E3M2, codes 0..31
+        mags = [0.0, 0.0625, 0.125, 0.1875, 0.25, 0.3125, 0.375, 0.4375,
+                0.5, 0.625, 0.75, 0.875, 1.0, 1.25, 1.5, 1.75,
+                2.0, 2.5, 3.0, 3.5, 4.0, 5.0, 6.0, 7.0,
+                8.0, 10.0, 12.0, 14.0, 16.0, 20.0, 24.0, 28.0]
     return list(enumerate(mags))
 
 
@@ -88,11 +109,24 @@ def _brute_encode(v, fmt):
     if len(cands) > 1:
         cands = [c for c in cands if c % 2 == 0]            # tie -> even code
     assert len(cands) == 1
-    bits = 8 if fmt == oracle.E4M3 else 4
-    return cands[0] | (sign << (bits - 1))
+    return cands[0] | (sign << (BITS[fmt] - 1))
 
 
-@pytest.mark.parametrize("fmt", [oracle.E4M3, oracle.E2M1])
+def test_fp6_grids_match_published_limits():
+    """The FP6 value lists against the OCP MX figures: largest normal, smallest
+    normal, largest and smallest subnormal, 32 distinct magnitudes each."""
+    limits = {oracle.E2M3: (7.5, 1.0, 0.875, 0.125), oracle.E3M2: (28.0, 0.25, 0.1875, 0.0625)}
+    for fmt, (mx, mn, sub_hi, sub_lo) in limits.items():
+        g = [v for _, v in _grid(fmt)]
+        assert len(set(g)) == 32 and g == sorted(g)
+        assert g[-1] == mx == MAXV[fmt] and g[1] == sub_lo
+        normals = [v for v in g if v >= mn]
+        assert normals[0] == mn and max(v for v in g if v < mn) == sub_hi
+        # top binade of the format is [2^emax, 2^(emax+1))
+        assert 2.0 ** EMAX[fmt] <= mx < 2.0 ** (EMAX[fmt] + 1)
+
+
+@pytest.mark.parametrize("fmt", ALL_FMTS)
 def test_encode_matches_brute_force(fmt):
     grid = [g for _, g in _grid(fmt)]
     pts = set()
@@ -120,11 +154,11 @@ def test_encode_e4m3_matches_torch_cast():
     assert got == ref.tolist()
 
 
-@pytest.mark.parametrize("fmt", [oracle.E4M3, oracle.E2M1])
+@pytest.mark.parametrize("fmt", ALL_FMTS)
 def test_decode_matches_format_grid(fmt):
     for code, val in _grid(fmt):
         assert oracle.decode(code, fmt) == val
-        neg = code | (0x80 if fmt == oracle.E4M3 else 0x8)
+        neg = code | (1 << (BITS[fmt] - 1))
         assert oracle.decode(neg, fmt) == -val
 
 
@@ -135,7 +169,7 @@ def _rand_tensor(shape, seed, spread=6.0):
     return (rng.standard_normal(shape) * mag).astype(np.float32)
 
 
-@pytest.mark.parametrize("fmt", [oracle.E4M3, oracle.E2M1])
+@pytest.mark.parametrize("fmt", ALL_FMTS)
 def test_scale_puts_block_max_in_top_binade(fmt):
     n, c, h, w = 32, 64, 3, 2
     x = _rand_tensor((n, c, h, w), 3)
@@ -150,7 +184,7 @@ def test_scale_puts_block_max_in_top_binade(fmt):
                 assert 2.0 ** EMAX[fmt] <= scaled < 2.0 ** (EMAX[fmt] + 1)
 
 
-@pytest.mark.parametrize("fmt", [oracle.E4M3, oracle.E2M1])
+@pytest.mark.parametrize("fmt", ALL_FMTS)
 def test_dequant_error_bound(fmt):
     """|x - deq(q(x))| <= half a quantum of x's binade, except clipping in
     the block's top binade (amax above the format maximum saturates)."""
@@ -158,8 +192,8 @@ def test_dequant_error_bound(fmt):
     x = _rand_tensor((n, c, h, w), 5).astype(np.float64)
     codes, scales = oracle.quantize(x.astype(np.float32), oracle.NCHW, oracle.ACT, fmt, n, c, h, w)
     d = oracle.dequant(codes, scales, oracle.ACT, fmt, n, c, h, w)
-    mbits = 3 if fmt == oracle.E4M3 else 1
-    minexp = -6 if fmt == oracle.E4M3 else 0
+    mbits = {oracle.E4M3: 3, oracle.E2M1: 1, oracle.E2M3: 3, oracle.E3M2: 2}[fmt]
+    minexp = {oracle.E4M3: -6, oracle.E2M1: 0, oracle.E2M3: 0, oracle.E3M2: -2}[fmt]
     for hh in range(h):
         for ww in range(w):
             s = int(scales[hh * w + ww]) - 127
@@ -174,7 +208,7 @@ def test_dequant_error_bound(fmt):
                     assert abs(v - d[i, cc, hh, ww] / 2.0 ** s) <= half_q
 
 
-@pytest.mark.parametrize("fmt", [oracle.E4M3, oracle.E2M1])
+@pytest.mark.parametrize("fmt", ALL_FMTS)
 def test_quantizer_invariants(fmt):
     n, c, h, w = 32, 40, 2, 3                      # ragged channels: padded to 64
     x = _rand_tensor((n, c, h, w), 9)
@@ -201,9 +235,11 @@ def _pos(n, c, h, w, bn, H, W, Cp):
     return ((((n // bn) * H + h) * W + w) * Cp + c) * bn + n % bn
 
 
-@pytest.mark.parametrize("fmt", [oracle.E4M3, oracle.E2M1])
-@pytest.mark.parametrize("N", [2, 16, 64])
+@pytest.mark.parametrize("fmt", ALL_FMTS)
+@pytest.mark.parametrize("N", [2, 4, 16, 64])
 def test_layout_single_element(fmt, N):
+    if BITS[fmt] == 6 and N < 4:
+        pytest.skip("FP6 activations need Bn >= 4")
     C, H, W = 40, 3, 5
     Cp, bn = 64, min(32, N)
     rng = np.random.default_rng(N)
@@ -214,17 +250,17 @@ def test_layout_single_element(fmt, N):
         x[n, c, h, w] = -1.0
         codes, scales = oracle.quantize(x, oracle.NCHW, oracle.ACT, fmt, N, C, H, W)
         pos = _pos(n, c, h, w, bn, H, W, Cp)
-        # -1.0 alone: scale 2^-emax, element -2^emax = -256 (0xF8) or -4 (0xE)
-        top = 0xF8 if fmt == oracle.E4M3 else 0xE
-        nz = [i for i in range(len(codes) * (1 if fmt == oracle.E4M3 else 2))
-              if _code_at(codes, fmt, i)]
+        # -1.0 alone: scale 2^-emax, element -2^emax = -256 (0xF8), -4 (E2M1
+        # 0xE, E2M3 0x38) or -16 (E3M2 0x3C)
+        top = {oracle.E4M3: 0xF8, oracle.E2M1: 0xE, oracle.E2M3: 0x38, oracle.E3M2: 0x3C}[fmt]
+        nz = [i for i in range(len(codes) * 8 // BITS[fmt]) if _code_at(codes, fmt, i)]
         assert nz == [pos] and _code_at(codes, fmt, pos) == top
         spos = (((n // bn) * H + h) * W + w) * (Cp // 32) + c // 32
         assert [i for i, s in enumerate(scales) if s] == [spos]
         assert scales[spos] == 127 - EMAX[fmt]
 
 
-@pytest.mark.parametrize("fmt", [oracle.E4M3, oracle.E2M1])
+@pytest.mark.parametrize("fmt", ALL_FMTS)
 def test_source_layouts_agree(fmt):
     N, C, H, W = 64, 40, 3, 4
     x = torch.from_numpy(_rand_tensor((N, C, H, W), 21))
@@ -260,6 +296,27 @@ def test_bad_batch_rejected():
         assert oracle.codes_bytes(oracle.ACT, oracle.E4M3, n, 32, 1, 1) < 0
     assert oracle.codes_bytes(oracle.ACT, oracle.E2M1, 1, 32, 1, 1) < 0
     assert oracle.codes_bytes(oracle.ACT, oracle.E4M3, 1, 32, 1, 1) == 32
+    for fmt in (oracle.E2M3, oracle.E3M2):
+        assert oracle.codes_bytes(oracle.ACT, fmt, 2, 32, 1, 1) < 0
+        assert oracle.codes_bytes(oracle.ACT, fmt, 4, 32, 1, 1) == 4 * 32 * 6 // 8
+        assert oracle.codes_bytes(oracle.ACT, fmt, 64, 40, 2, 3) == 64 * 64 * 6 * 6 // 8
+
+
+def test_fp6_bit_string_packing_hand_worked():
+    """Four E2M3 samples of one channel holding codes 1, 2, 3, 4 (values
+    0.125 .. 0.5 under scale 2^0, set by a 7.5 elsewhere in the block).
+    Bit string: 000001 | 000010 | 000011 | 000100, least significant first:
+    byte 0 = 01 + (10 << 6) = 0x81, byte 1 = 0000 + (0011 << 4) = 0x30,
+    byte 2 = 00 + (000100 << 2) = 0x10."""
+    x = np.zeros((4, 32, 1, 1), dtype=np.float32)
+    x[:, 0, 0, 0] = [0.125, 0.25, 0.375, 0.5]
+    x[0, 5, 0, 0] = 7.5
+    codes, scales = oracle.quantize(x, oracle.NCHW, oracle.ACT, oracle.E2M3, 4, 32, 1, 1)
+    assert scales.tolist() == [127] and len(codes) == 96
+    assert codes[:3].tolist() == [0x81, 0x30, 0x10]
+    # channel 5 row starts at byte 15; sample 0 holds 7.5 = 0x1F
+    assert codes[15] == 0x1F and codes[16:18].tolist() == [0, 0]
+    assert int(np.count_nonzero(codes)) == 4
 
 
 # ---------------------------------------------------------------- im2col
@@ -283,11 +340,13 @@ def _unfold_as_tensor(x, cv):
     return u.reshape(n, c, ho * wo * cv["kh"] * cv["kw"], 1).contiguous()
 
 
-@pytest.mark.parametrize("fmt", [oracle.E4M3, oracle.E2M1])
+@pytest.mark.parametrize("fmt", ALL_FMTS)
 @pytest.mark.parametrize("cv", CONVS, ids=lambda c: f"n{c['n']}c{c['cin']}k{c['kh']}{c['kw']}s{c['sh']}")
 def test_im2col_commutes_with_quantize(fmt, cv):
     """quantize(im2col(X)) == im2col_cbf(quantize(X)), bit for bit (Sec. IV-B:
     quantizing X_{Cin,N} keeps its blocks whole through the CBF im2col)."""
+    if BITS[fmt] == 6 and cv["n"] < 4:
+        pytest.skip("FP6 activations need Bn >= 4")
     x = torch.from_numpy(_rand_tensor((cv["n"], cv["cin"], cv["h"], cv["w"]), 31))
     q = oracle.quantize(x.numpy(), oracle.NCHW, oracle.ACT, fmt, cv["n"], cv["cin"], cv["h"], cv["w"])
     col = oracle.im2col_cbf(cv, fmt, *q)
@@ -322,15 +381,34 @@ def test_im2col_index_map_brute_force():
 
 # ---------------------------------------------------------------- GEMMs
 def _quantized_layer(cv, fmt, seed):
+    """fmt: one format for W, X and G_Y, or a (W, X, G_Y) triple."""
+    fw, fx, fg = fmt if isinstance(fmt, tuple) else (fmt, fmt, fmt)
     x, w, gy = synth.layer_inputs(cv, seed, kind="unit")
     ho, wo = synth.out_hw(cv)
-    qx = oracle.quantize(x.numpy(), oracle.NCHW, oracle.ACT, fmt, cv["n"], cv["cin"], cv["h"], cv["w"])
-    qw = oracle.quantize(w.numpy(), oracle.NCHW, oracle.WEIGHT, fmt, cv["cout"], cv["cin"], cv["kh"], cv["kw"])
-    qg = oracle.quantize(gy.numpy(), oracle.NCHW, oracle.ACT, fmt, cv["n"], cv["cout"], ho, wo)
-    xd = oracle.dequant(*qx, oracle.ACT, fmt, cv["n"], cv["cin"], cv["h"], cv["w"])
-    wd = oracle.dequant(*qw, oracle.WEIGHT, fmt, cv["cout"], cv["cin"], cv["kh"], cv["kw"])
-    gd = oracle.dequant(*qg, oracle.ACT, fmt, cv["n"], cv["cout"], ho, wo)
+    qx = oracle.quantize(x.numpy(), oracle.NCHW, oracle.ACT, fx, cv["n"], cv["cin"], cv["h"], cv["w"])
+    qw = oracle.quantize(w.numpy(), oracle.NCHW, oracle.WEIGHT, fw, cv["cout"], cv["cin"], cv["kh"], cv["kw"])
+    qg = oracle.quantize(gy.numpy(), oracle.NCHW, oracle.ACT, fg, cv["n"], cv["cout"], ho, wo)
+    xd = oracle.dequant(*qx, oracle.ACT, fx, cv["n"], cv["cin"], cv["h"], cv["w"])
+    wd = oracle.dequant(*qw, oracle.WEIGHT, fw, cv["cout"], cv["cin"], cv["kh"], cv["kw"])
+    gd = oracle.dequant(*qg, oracle.ACT, fg, cv["n"], cv["cout"], ho, wo)
     return qx, qw, qg, xd, wd, gd
+
+
+# (W, X, G_Y) element formats: the single-format methods, MicroQonv+ (FP6
+# E3M2 activations, FP4 weights and gradients) and an all-E2M3 "-6" layer
+LAYER_FMTS = [oracle.E4M3, oracle.E2M1, (oracle.E2M1, oracle.E3M2, oracle.E2M1),
+              (oracle.E2M3, oracle.E2M3, oracle.E2M3)]
+
+
+def _pairs(fmt):
+    """Per-call format pairs (fwd: W, X; dgrad: W, G_Y; wgrad: G_Y, X)."""
+    fw, fx, fg = fmt if isinstance(fmt, tuple) else (fmt, fmt, fmt)
+    return (fw, fx), (fw, fg), (fg, fx)
+
+
+def _fmt_id(f):
+    names = {v: k for k, v in FMTS.items()}
+    return "-".join(names[t] for t in f) if isinstance(f, tuple) else names[f]
 
 
 def _close(a, b, s):
@@ -338,15 +416,18 @@ def _close(a, b, s):
     return np.max(np.abs(a - b) / scale) <= 1e-12
 
 
-@pytest.mark.parametrize("fmt", [oracle.E4M3, oracle.E2M1])
+@pytest.mark.parametrize("fmt", LAYER_FMTS, ids=_fmt_id)
 @pytest.mark.parametrize("cv", CONVS, ids=lambda c: f"n{c['n']}c{c['cin']}k{c['kh']}{c['kw']}s{c['sh']}")
 def test_gemms_match_torch_fp64(fmt, cv):
+    if isinstance(fmt, tuple) and cv["n"] < 4:
+        pytest.skip("FP6 activations need Bn >= 4")
     qx, qw, qg, xd, wd, gd = _quantized_layer(cv, fmt, 5)
+    pf, pd_, pw = _pairs(fmt)
     st, pd = (cv["sh"], cv["sw"]), (cv["ph"], cv["pw"])
     X, Wt, G = map(torch.from_numpy, (xd, wd, gd))
-    y, sy = oracle.fwd(cv, fmt, qw, qx)
-    gx, sgx = oracle.dgrad(cv, fmt, qw, qg)
-    gw, sgw = oracle.wgrad(cv, fmt, qg, qx)
+    y, sy = oracle.fwd(cv, pf, qw, qx)
+    gx, sgx = oracle.dgrad(cv, pd_, qw, qg)
+    gw, sgw = oracle.wgrad(cv, pw, qg, qx)
     y_ref = F.conv2d(X, Wt, stride=st, padding=pd).numpy()
     gx_ref = torch.nn.grad.conv2d_input(X.shape, Wt, G, stride=st, padding=pd).numpy()
     gw_ref = torch.nn.grad.conv2d_weight(X, Wt.shape, G, stride=st, padding=pd).numpy()
@@ -359,35 +440,41 @@ def test_gemms_match_torch_fp64(fmt, cv):
     assert np.allclose(sgw, sgw_ref, rtol=1e-12, atol=0)
 
 
+@pytest.mark.parametrize("fmt", [oracle.E4M3, (oracle.E2M1, oracle.E3M2, oracle.E2M1)], ids=_fmt_id)
 @pytest.mark.parametrize("cv", CONVS[:4], ids=lambda c: f"n{c['n']}c{c['cin']}k{c['kh']}{c['kw']}s{c['sh']}")
-def test_gemms_match_direct_definitions(cv):
-    fmt = oracle.E4M3
+def test_gemms_match_direct_definitions(cv, fmt):
+    if isinstance(fmt, tuple) and cv["n"] < 4:
+        pytest.skip("FP6 activations need Bn >= 4")
     qx, qw, qg, xd, wd, gd = _quantized_layer(cv, fmt, 6)
-    y, sy = oracle.fwd(cv, fmt, qw, qx)
-    gx, sgx = oracle.dgrad(cv, fmt, qw, qg)
-    gw, sgw = oracle.wgrad(cv, fmt, qg, qx)
+    pf, pd_, pw = _pairs(fmt)
+    y, sy = oracle.fwd(cv, pf, qw, qx)
+    gx, sgx = oracle.dgrad(cv, pd_, qw, qg)
+    gw, sgw = oracle.wgrad(cv, pw, qg, qx)
     assert _close(y, oracle.direct_fwd(cv, wd, xd), sy)
     assert _close(gx, oracle.direct_dgrad(cv, wd, gd), sgx)
     assert _close(gw, oracle.direct_wgrad(cv, gd, xd), sgw)
 
 
+@pytest.mark.parametrize("fmt", [oracle.E2M1, (oracle.E2M3, oracle.E3M2, oracle.E2M1)], ids=_fmt_id)
 @pytest.mark.parametrize("cv", CONVS[:4], ids=lambda c: f"n{c['n']}c{c['cin']}k{c['kh']}{c['kw']}s{c['sh']}")
-def test_single_output_routines_match_full(cv):
-    fmt = oracle.E2M1
+def test_single_output_routines_match_full(cv, fmt):
+    if isinstance(fmt, tuple) and cv["n"] < 4:
+        pytest.skip("FP6 activations need Bn >= 4")
     qx, qw, qg, xd, wd, gd = _quantized_layer(cv, fmt, 8)
+    pf, pd_, pw = _pairs(fmt)
     ho, wo = synth.out_hw(cv)
     rng = np.random.default_rng(0)
-    y, sy = oracle.fwd(cv, fmt, qw, qx)
+    y, sy = oracle.fwd(cv, pf, qw, qx)
     idx = np.stack([rng.integers(0, d, 50) for d in (cv["n"], cv["cout"], ho, wo)], 1)
-    v, s = oracle.fwd_at(cv, fmt, qw, qx, idx)
+    v, s = oracle.fwd_at(cv, pf, qw, qx, idx)
     assert _close(v, y[tuple(idx.T)], s) and np.allclose(s, sy[tuple(idx.T)], rtol=1e-12)
-    gx, sgx = oracle.dgrad(cv, fmt, qw, qg)
+    gx, sgx = oracle.dgrad(cv, pd_, qw, qg)
     idx = np.stack([rng.integers(0, d, 50) for d in (cv["n"], cv["cin"], cv["h"], cv["w"])], 1)
-    v, s = oracle.dgrad_at(cv, fmt, qw, qg, idx)
+    v, s = oracle.dgrad_at(cv, pd_, qw, qg, idx)
     assert _close(v, gx[tuple(idx.T)], s) and np.allclose(s, sgx[tuple(idx.T)], rtol=1e-12)
-    gw, sgw = oracle.wgrad(cv, fmt, qg, qx)
+    gw, sgw = oracle.wgrad(cv, pw, qg, qx)
     idx = np.stack([rng.integers(0, d, 50) for d in (cv["cout"], cv["cin"], cv["kh"], cv["kw"])], 1)
-    v, s = oracle.wgrad_at(cv, fmt, qg, qx, idx)
+    v, s = oracle.wgrad_at(cv, pw, qg, qx, idx)
     assert _close(v, gw[tuple(idx.T)], s) and np.allclose(s, sgw[tuple(idx.T)], rtol=1e-12)
 
 
@@ -400,16 +487,18 @@ def test_pointwise_conv_is_a_matmul():
     assert _close(y, ref, sy)
 
 
-def test_lossless_inputs_reproduce_plain_convolution():
+@pytest.mark.parametrize("fmt", [oracle.E4M3, (oracle.E2M1, oracle.E3M2, oracle.E2M1),
+                                 (oracle.E2M3, oracle.E2M3, oracle.E2M3)], ids=_fmt_id)
+def test_lossless_inputs_reproduce_plain_convolution(fmt):
     """Inputs already on the MX grid pass through quantization unchanged, so
     the MX convolution equals torch's fp64 convolution of the raw inputs."""
     cv = synth.conv_dict(32, 32, 32, 6, 6, 3, 1, 1)
-    fmt = oracle.E4M3
+    fw, fx, _ = fmt if isinstance(fmt, tuple) else (fmt, fmt, fmt)
     qx, qw, qg, xd, wd, gd = _quantized_layer(cv, fmt, 12)
     # xd, wd are exactly representable; quantize them again from fp32
-    qx2 = oracle.quantize(xd.astype(np.float32), oracle.NCHW, oracle.ACT, fmt, 32, 32, 6, 6)
-    qw2 = oracle.quantize(wd.astype(np.float32), oracle.NCHW, oracle.WEIGHT, fmt, 32, 32, 3, 3)
-    y, sy = oracle.fwd(cv, fmt, qw2, qx2)
+    qx2 = oracle.quantize(xd.astype(np.float32), oracle.NCHW, oracle.ACT, fx, 32, 32, 6, 6)
+    qw2 = oracle.quantize(wd.astype(np.float32), oracle.NCHW, oracle.WEIGHT, fw, 32, 32, 3, 3)
+    y, sy = oracle.fwd(cv, (fw, fx), qw2, qx2)
     ref = F.conv2d(torch.from_numpy(xd), torch.from_numpy(wd), padding=1).numpy()
     assert _close(y, ref, sy)
 
