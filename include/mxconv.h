@@ -16,12 +16,33 @@
  *             1 byte per element.
  *   MXC_E2M1: FP4 E2M1 elements (max 6), two per byte, the element at the
  *             even position in the low nibble.
+ *   MXC_E2M3, MXC_E3M2: FP6 elements (OCP: E2M3 bias 1, max 7.5; E3M2 bias 3,
+ *             max 28; no inf or NaN), packed as one little-endian bit string:
+ *             the element at position p occupies bits 6p .. 6p+5 (bit 0 =
+ *             least significant bit of byte 0), so 32 samples take 24 bytes.
+ *             Sec. V's MicroQonv+ keeps activations in E3M2 with FP4
+ *             weights and gradients; its "-6" methods use E2M3 throughout.
+ *             FP6 code buffers end with 16 bytes of slack that the library
+ *             may read but never writes (included in mxconv_codes_bytes).
  *   Scales: one E8M0 byte per block, value 2^(code-127); 0xFF marks a block
  *   that held a NaN or infinity.
  *
+ * Operand formats of the GEMM entry points (fwd, dgrad, wgrad and the fused
+ * forms): `fmt` is either one format for both MX operands, or
+ * MXC_PAIR(first, second) naming the format of each, in the order the call
+ * takes them (fwd: W, X; dgrad: W, G_Y; wgrad: G_Y, X).  Supported: E4M3,
+ * E2M1 and E2M3 alone, and MXC_PAIR(MXC_E2M1, MXC_E3M2) (MicroQonv+: FP4
+ * weights or gradients against E3M2 activations); anything else returns
+ * MXC_ERR_ARG.  (E3M2 against E3M2 is left out: the matrix cores do not sum
+ * those products exactly.)  The FP6 forms run on the batch-block-32 kernels
+ * (n a multiple of 32; fwd and dgrad: kernel width 1 or 3, fwd column
+ * stride 1 or 2, dgrad stride 1x1 or 2x2); other layers return
+ * MXC_ERR_SHAPE.
+ *
  * Quantization rule (per block, the OCP-MX reading of Sec. III-A Eqs. (4)-(6)):
- *   s = clamp(floor(log2 max|x|) - emax, -127, 127), emax = 8 (E4M3) or 2
- *   (E2M1); scale code = s + 127 (code 0 when the block is all zero);
+ *   s = clamp(floor(log2 max|x|) - emax, -127, 127), emax = 8 (E4M3), 2
+ *   (E2M1, E2M3) or 4 (E3M2); scale code = s + 127 (code 0 when the block
+ *   is all zero);
  *   element = x * 2^-s rounded to nearest, ties to even, saturating to the
  *   largest finite element; the sign of zero is kept; a non-finite block
  *   gets scale 0xFF and all-zero element codes.
@@ -35,7 +56,7 @@
  * samples are contiguous; Sec. IV-B's square blocks along Cin and N).
  *   role MXC_ACT:    Bn = 32 if n >= 32 (n must be a multiple of 32),
  *                    else Bn = n (n must divide 32); Np = n.
- *                    E2M1 needs Bn >= 2.
+ *                    E2M1 needs Bn >= 2, E2M3 and E3M2 Bn >= 4.
  *   role MXC_WEIGHT: Bn = 32, Np = n rounded up to 32, i.e. a block is
  *                    32 Cin x 32 Cout at one tap (Sec. IV-B: W_f is blocked
  *                    along Cin and Cout).
@@ -81,7 +102,9 @@ extern "C" {
 #define MXC_ERR_HIP       (-5)  /* the HIP runtime reported a launch error */
 #define MXC_ERR_WORKSPACE (-6)  /* workspace missing or smaller than required */
 
-typedef enum { MXC_E4M3 = 0, MXC_E2M1 = 1 } mxc_fmt;
+typedef enum { MXC_E4M3 = 0, MXC_E2M1 = 1, MXC_E2M3 = 2, MXC_E3M2 = 3 } mxc_fmt;
+/* Different formats for the two MX operands of a GEMM entry point. */
+#define MXC_PAIR(first, second) (0x10 | ((first) << 2) | (second))
 typedef enum { MXC_F32 = 0, MXC_BF16 = 1 } mxc_dtype;
 typedef enum { MXC_NCHW = 0, MXC_NHWC = 1, MXC_CBF = 2 } mxc_layout;
 typedef enum { MXC_ACT = 0, MXC_WEIGHT = 1 } mxc_role;
@@ -281,7 +304,8 @@ int mxconv_naive_wgrad(const mxc_conv* cv, int fmt,
  * MXC_FN_SILU y / (1 + exp(-y))), quantized into the MX-CBF tensor of
  * (n, cout, Ho, Wo):
  *   y_codes / y_scales  device, mxconv_codes_bytes / mxconv_scales_bytes(
- *                       MXC_ACT, out_fmt, n, cout, Ho, Wo) bytes, written.
+ *                       MXC_ACT, out_fmt, n, cout, Ho, Wo) bytes, written
+ *                       (out_fmt any mxc_fmt; FP6 slack not written).
  *   y_act               NULL, or device fp32 n x cout x Ho x Wo in CBF
  *                       layout: receives the values that were quantized.
  * Input gradient: G_Z = (W^T * G_Y) . fn'(z), the gradient at the

@@ -1270,12 +1270,17 @@ __global__ __launch_bounds__(NT) void wgrad_stream_kernel(WStreamArgs p) {
 
 bool wstream_ok(const Conv& cv) { return cv.x.bn * cv.bits >= 128; }   // rows of >= 16 bytes
 
+// the general kernels above run one format for both operands, FP8 or FP4;
+// FP6 and mixed pairs run only on the batch-block-32 kernels
+bool general_fmt(const Conv& cv) { return cv.fmt == MXC_E4M3 || cv.fmt == MXC_E2M1; }
+
 }  // namespace
 
 int launch_fwd(const Conv& cv, const void* wc, const uint8_t* ws, const void* xc, const uint8_t* xs,
                float* y, int layout, hipStream_t s) {
     const int rc = launch_conv_lean(cv, false, wc, ws, xc, xs, y, layout, s);
     if (rc != 1) return rc;
+    if (!general_fmt(cv)) return MXC_ERR_SHAPE;
     if (stream_ok(cv)) return launch_conv_stream(cv, false, wc, ws, xc, xs, y, layout, s);
     return launch_conv(cv, false, wc, ws, xc, xs, y, layout, s);
 }
@@ -1284,6 +1289,7 @@ int launch_dgrad(const Conv& cv, const void* wc, const uint8_t* ws, const void* 
                  float* gx, int layout, hipStream_t s) {
     const int rc = launch_conv_lean(cv, true, wc, ws, gc, gs, gx, layout, s);
     if (rc != 1) return rc;
+    if (!general_fmt(cv)) return MXC_ERR_SHAPE;
     if (stream_ok(cv)) return launch_conv_stream(cv, true, wc, ws, gc, gs, gx, layout, s);
     return launch_conv(cv, true, wc, ws, gc, gs, gx, layout, s);
 }
@@ -1291,6 +1297,7 @@ int launch_dgrad(const Conv& cv, const void* wc, const uint8_t* ws, const void* 
 size_t wgrad_workspace(const Conv& cv) {
     const int ls = wgrad_lean_splits(cv);
     if (ls > 0) return ls > 1 ? (size_t)ls * cv.gy.cp * cv.kh * cv.kw * cv.x.cp * sizeof(float) : 0;
+    if (!general_fmt(cv)) return 0;
     const WgradPlan pl = wgrad_plan(cv);
     return (size_t)pl.splits * cv.gy.cp * pl.ntot * sizeof(float);
 }
@@ -1306,6 +1313,7 @@ int launch_wgrad(const Conv& cv, const void* gc, const uint8_t* gs, const void* 
                            (const float*)ws, gw, cv, cv.kh * cv.kw * cv.x.cp, ls);
         return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
     }
+    if (!general_fmt(cv)) return MXC_ERR_SHAPE;
     const WgradPlan pl = wgrad_plan(cv);
     WgradArgs a;
     a.cv = cv;

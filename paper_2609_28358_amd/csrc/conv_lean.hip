@@ -112,11 +112,29 @@ struct Phase {
 // its taps per row (the halo is then a stride-1 one on the phase grid).
 // Each wave owns 64 channels x PW pixels (PW = 2, or 1 for layers with few
 // tiles: twice the workgroups, so more waves stream and store at once).
-template <int FMT, bool DG, int KW, int S, int WGM, int PW>
+//
+// Element formats: FW of the weights, FX of the source activation.  A stored
+// block is 32 rows x 32 codes: 1024 bytes (FP8), 768 (FP6) or 512 (FP4).  In
+// LDS an FP8 or FP4 block keeps its stored layout; an FP6 block takes 1 KB,
+// each 12-byte half row (16 codes) at the start of its own 16-byte slot --
+// the alignment the 6-bit transposing read needs.  One wave copy
+// instruction moves 1 KB of LDS: two FP4 blocks, or one FP8 block, or one
+// FP6 block with lane j reading the 16 bytes at 12 j (the last 4 of them
+// belong to the next half row and are never read back).
+template <int F> struct LdsBlock {
+    static constexpr int TBG = 32 * 32 * fmt_bits(F) / 8;        // stored block bytes
+    static constexpr int TBL = F == MXC_E2M1 ? 512 : 1024;       // LDS block bytes
+    static constexpr int BPI = 1024 / TBL;                       // blocks per copy instruction
+    static constexpr int STEP = fmt_bits(F) == 6 ? 12 : 16;      // source bytes between lanes
+};
+
+template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW>
 __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phase& f) {
-    constexpr int EB = FMT == MXC_E4M3 ? 8 : 4;
-    constexpr int TB = 32 * 32 * EB / 8;            // bytes of one stored block (weights and activations)
-    constexpr int RB = 32 * EB / 8;                 // bytes of one channel row of an activation block
+    typedef LdsBlock<FW> BW;
+    typedef LdsBlock<FX> BX;
+    constexpr int TBW = BW::TBG, TBX = BX::TBG;     // stored block bytes (weights, activations)
+    constexpr int RBW_G = 32 * fmt_bits(FW) / 8;    // stored bytes of one 32-code row of a weight block
+    constexpr int RB = 32 * fmt_bits(FX) / 8;       // stored bytes of one channel row of an activation block
     constexpr int RBW = 2 * WGM;                    // 32-row blocks per tile
     constexpr int PX = PW * 4 / WGM;                // output pixels per tile
     constexpr int CS = DG ? 1 : S;                  // halo columns per output pixel step
@@ -124,15 +142,17 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
     constexpr int HP = (PX - 1) * CS + KW;          // halo pixels
     constexpr int NA = KW * 2 * RBW;                // weight blocks per stage
     constexpr int NB = 2 * HP;                      // activation blocks per stage
-    constexpr int BPI = 1024 / TB;                  // blocks per wave instruction
-    constexpr int NQ = (NA + NB + 4 * BPI - 1) / (4 * BPI);   // DMA instructions per thread per stage
+    constexpr int NSW = NA / BW::BPI;               // weight slices (1 KB) per stage
+    constexpr int NSX = NB / BX::BPI;               // activation slices per stage
+    constexpr int NQ = (NSW + NSX + 3) / 4;         // DMA instructions per thread per stage
     constexpr int ND = (PW - 1) * CS + KW;          // distinct halo pixels of a wave
     constexpr int NSA = KW * 2 * RBW;               // weight scales per stage
     constexpr int NSB = 2 * HP;                     // activation scales per stage
+    static_assert(NA % BW::BPI == 0 && NB % BX::BPI == 0, "whole slices");
     static_assert(NSA + NSB <= LT, "scale staging needs one thread per scale");
     static_assert(2 * (NQ + 1) <= 63, "two stages in flight must fit the vmcnt counter");
     static_assert(S == 1 || S == 2, "stride 1 or 2");
-    constexpr int A_BYTES = NA * TB;
+    constexpr int A_BYTES = NSW * 1024;
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -149,38 +169,41 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
     const int cbase = DG ? x0 + f.c0 - (KW - 1) : x0 * S - p.pw;   // first halo column
 
     // ---- strides (bytes)
-    const uint32_t w_tap = (uint32_t)p.w_cp * RB;                  // one tap of one 32-Cout block
+    const uint32_t w_tap = (uint32_t)p.w_cp * RBW_G;               // one tap of one 32-Cout block
     const uint32_t w_cob = (uint32_t)p.kh * p.kwf * w_tap;         // one 32-Cout block
-    const uint32_t x_pix = (uint32_t)p.kcb * TB;                   // one source pixel
+    const uint32_t x_pix = (uint32_t)p.kcb * TBX;                  // one source pixel
     const uint32_t x_row = (uint32_t)p.wsrc * x_pix;
 
     // ---- per-lane DMA pieces: instruction q of this wave moves LDS slice
     // (4q + wave) of the stage; its block(s) and this lane's 16 bytes
+    const uint32_t in_w = (uint32_t)(BW::BPI == 2 ? (lane & 31) : lane) * BW::STEP;   // lane offset in a block
+    const uint32_t in_x = (uint32_t)(BX::BPI == 2 ? (lane & 31) : lane) * BX::STEP;
     uint32_t off[NQ];
     uint32_t flg[NQ];        // bit0 tile-valid, bit1 K block 1, bit2 activation block
 #pragma unroll
     for (int q = 0; q < NQ; q++) {
         const int slice = 4 * q + wave;
-        const int blk = slice * BPI + (BPI == 2 ? (lane >> 5) : 0);
-        const int within = (BPI == 2 ? (lane & 31) : lane) * 16;
-        off[q] = within;
         flg[q] = 0;
-        if (blk < NA) {
+        off[q] = 0;
+        if (slice < NSW) {
             // [tap t][K half kb][row block rb]
+            const int blk = slice * BW::BPI + (BW::BPI == 2 ? (lane >> 5) : 0);
             const int rb = blk % RBW, kb = (blk / RBW) & 1, t = blk / (2 * RBW);
             const int rowblk = mt * RBW + rb;
             if (DG) {   // rows = input channels (block rowblk of Cin_p), K = output channels
-                off[q] += (uint32_t)kb * w_cob + (uint32_t)(f.kw0 + DS * t) * w_tap + (uint32_t)rowblk * TB;
+                off[q] = (uint32_t)kb * w_cob + (uint32_t)(f.kw0 + DS * t) * w_tap + (uint32_t)rowblk * TBW;
             } else {    // rows = output channels (32-Cout block rowblk), K = input channels
-                off[q] += (uint32_t)rowblk * w_cob + (uint32_t)t * w_tap + (uint32_t)kb * TB;
+                off[q] = (uint32_t)rowblk * w_cob + (uint32_t)t * w_tap + (uint32_t)kb * TBW;
             }
+            off[q] += in_w;
             flg[q] = (rowblk < p.w_rowblocks ? 1u : 0u) | (uint32_t)kb << 1;
-        } else if (blk < NA + NB) {
+        } else if (slice < NSW + NSX) {
             // [K half kb][halo pixel hc]
-            const int b = blk - NA, kb = b / HP, hc = b % HP;
+            const int b = (slice - NSW) * BX::BPI + (BX::BPI == 2 ? (lane >> 5) : 0);
+            const int kb = b / HP, hc = b % HP;
             const int col = cbase + hc;
             const bool ok = col >= 0 && col < p.wsrc;
-            off[q] += (uint32_t)(ok ? col : 0) * x_pix + (uint32_t)kb * TB;
+            off[q] = (uint32_t)(ok ? col : 0) * x_pix + (uint32_t)kb * TBX + in_x;
             flg[q] = (ok ? 1u : 0u) | (uint32_t)kb << 1 | 4u;
         }
     }
@@ -219,9 +242,9 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
         const int sy = DG ? yi + f.r0 - ki : yi * p.sh + kh - p.ph;
         const bool row_ok = sy >= 0 && sy < p.hsrc;
         const bool kb1_ok = 2 * kk + 1 < p.kcb;
-        const uint8_t* abase = p.wc + (DG ? (uint32_t)(2 * kk) * w_cob : (uint32_t)(2 * kk) * TB) +
+        const uint8_t* abase = p.wc + (DG ? (uint32_t)(2 * kk) * w_cob : (uint32_t)(2 * kk) * TBW) +
                                (uint32_t)kh * p.kwf * w_tap;
-        const uint8_t* bbase = p.sc + ((uint32_t)g * p.hsrc + (row_ok ? sy : 0)) * x_row + (uint32_t)(2 * kk) * TB;
+        const uint8_t* bbase = p.sc + ((uint32_t)g * p.hsrc + (row_ok ? sy : 0)) * x_row + (uint32_t)(2 * kk) * TBX;
         const uint8_t* lds = smem + buf * p.stage_bytes;
 #pragma unroll
         for (int q = 0; q < NQ; q++) {
@@ -229,7 +252,7 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
             const bool isb = f & 4u;
             const bool ok = (f & 1u) && (!(f & 2u) || kb1_ok) && (!isb || row_ok);
             const uint8_t* src = (isb ? bbase : abase) + off[q];
-            dma16_async(ok ? src : zero + (off[q] & (TB - 1)), lds_addr(lds + (4 * q + wave) * 1024));
+            dma16_async(ok ? src : zero + (isb ? in_x : in_w), lds_addr(lds + (4 * q + wave) * 1024));
         }
         const bool isb = s_flg & 4u;
         const bool ok = (s_flg & 8u) && (s_flg & 1u) && (!(s_flg & 2u) || kb1_ok) && (!isb || row_ok);
@@ -242,11 +265,13 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
     // ---- wave geometry and per-lane fragment offsets
     const int wm = wave % WGM, wn = wave / WGM;       // 64-row group, pixel pair
     const int h = lane >> 5, i16 = lane & 15, gi = lane >> 4, cg = gi & 1, hh = gi >> 1;
+    // FP6 in LDS: half row (row k, half c) in the 16-byte slot 2 k + c
     int a_lane;
-    if (DG) a_lane = FMT == MXC_E4M3 ? (lane & 31) * 32 + 16 * h : (lane & 31) * 16;
-    else    a_lane = FMT == MXC_E4M3 ? (16 * hh + (i16 >> 1)) * 32 + 16 * cg + 8 * (i16 & 1) : i16 * 16 + 8 * cg;
-    const int b_lane = FMT == MXC_E4M3 ? (16 * hh + (i16 >> 1)) * RB + 16 * cg + 8 * (i16 & 1)
-                                       : i16 * RB + 8 * cg;
+    if (DG) a_lane = FW == MXC_E4M3 ? (lane & 31) * 32 + 16 * h : fmt_bits(FW) == 6 ? (lane & 31) * 32 : (lane & 31) * 16;
+    else    a_lane = FW == MXC_E4M3 ? (16 * hh + (i16 >> 1)) * 32 + 16 * cg + 8 * (i16 & 1)
+                   : fmt_bits(FW) == 6 ? 32 * i16 + 16 * cg : i16 * 16 + 8 * cg;
+    const int b_lane = FX == MXC_E4M3 ? (16 * hh + (i16 >> 1)) * RB + 16 * cg + 8 * (i16 & 1)
+                     : fmt_bits(FX) == 6 ? 32 * i16 + 16 * cg : i16 * RB + 8 * cg;
     const int hbase = PW * wn * CS;                   // first halo pixel of the wave
 
     v16f acc[2][PW];
@@ -278,18 +303,25 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
 #pragma unroll
         for (int d = 0; d < ND; d++) {
             const int hc = hbase + d;
-            if (FMT == MXC_E4M3) {
-                const uint8_t* tb = B + hc * TB + b_lane;
+            if (FX == MXC_E4M3) {
+                const uint8_t* tb = B + hc * BX::TBL + b_lane;
 #pragma unroll
                 for (int kb = 0; kb < 2; kb++)
 #pragma unroll
                     for (int hf = 0; hf < 2; hf++) {
-                        const v2i v = lds_tr8(tb + kb * HP * TB + hf * 8 * RB);
+                        const v2i v = lds_tr8(tb + kb * HP * BX::TBL + hf * 8 * RB);
                         bf[d][4 * kb + 2 * hf] = v[0];
                         bf[d][4 * kb + 2 * hf + 1] = v[1];
                     }
+            } else if (fmt_bits(FX) == 6) {
+                // channels 0..15, then 16..31, of this lane's sample
+                const uint8_t* tb = B + (hh * HP + hc) * BX::TBL + b_lane;
+                const v3i lo = lds_tr6(tb), hi = lds_tr6(tb + 512);
+                bf[d][0] = lo[0]; bf[d][1] = lo[1]; bf[d][2] = lo[2];
+                bf[d][3] = hi[0]; bf[d][4] = hi[1]; bf[d][5] = hi[2];
+                bf[d][6] = bf[d][7] = 0;
             } else {
-                const uint8_t* tb = B + (hh * HP + hc) * TB + b_lane;
+                const uint8_t* tb = B + (hh * HP + hc) * BX::TBL + b_lane;
 #pragma unroll
                 for (int hf = 0; hf < 2; hf++) {
                     const v2i v = lds_tr4(tb + hf * 16 * RB);
@@ -307,21 +339,29 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
 #pragma unroll
             for (int rb = 0; rb < 2; rb++) {
                 const int rbi = 2 * wm + rb;
-                const uint8_t* a0 = A + ((t * 2 + 0) * RBW + rbi) * TB + a_lane;
-                const uint8_t* a1 = a0 + RBW * TB;
+                const uint8_t* a0 = A + ((t * 2 + 0) * RBW + rbi) * BW::TBL + a_lane;
+                const uint8_t* a1 = a0 + RBW * BW::TBL;
                 if (DG) {
-                    if (FMT == MXC_E4M3) {
+                    if (FW == MXC_E4M3) {
                         const v4i u0 = *(const v4i*)a0;
                         const v4i u1 = *(const v4i*)a1;
                         af[rb][0] = u0[0]; af[rb][1] = u0[1]; af[rb][2] = u0[2]; af[rb][3] = u0[3];
                         af[rb][4] = u1[0]; af[rb][5] = u1[1]; af[rb][6] = u1[2]; af[rb][7] = u1[3];
+                    } else if (fmt_bits(FW) == 6) {
+                        // the lane's row: 12 bytes from each of its two slots
+                        const uint8_t* ar = h ? a1 : a0;
+                        const v3i u0 = *(const v3i*)ar;
+                        const v3i u1 = *(const v3i*)(ar + 16);
+                        af[rb][0] = u0[0]; af[rb][1] = u0[1]; af[rb][2] = u0[2];
+                        af[rb][3] = u1[0]; af[rb][4] = u1[1]; af[rb][5] = u1[2];
+                        af[rb][6] = af[rb][7] = 0;
                     } else {
                         const v4i u0 = *(const v4i*)(h ? a1 : a0);
                         af[rb][0] = u0[0]; af[rb][1] = u0[1]; af[rb][2] = u0[2]; af[rb][3] = u0[3];
                         af[rb][4] = af[rb][5] = af[rb][6] = af[rb][7] = 0;
                     }
                 } else {
-                    if (FMT == MXC_E4M3) {
+                    if (FW == MXC_E4M3) {
 #pragma unroll
                         for (int kb = 0; kb < 2; kb++)
 #pragma unroll
@@ -330,6 +370,12 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                                 af[rb][4 * kb + 2 * hf] = v[0];
                                 af[rb][4 * kb + 2 * hf + 1] = v[1];
                             }
+                    } else if (fmt_bits(FW) == 6) {
+                        const uint8_t* ab = hh ? a1 : a0;
+                        const v3i lo = lds_tr6(ab), hi = lds_tr6(ab + 512);
+                        af[rb][0] = lo[0]; af[rb][1] = lo[1]; af[rb][2] = lo[2];
+                        af[rb][3] = hi[0]; af[rb][4] = hi[1]; af[rb][5] = hi[2];
+                        af[rb][6] = af[rb][7] = 0;
                     } else {
                         const uint8_t* ab = hh ? a1 : a0;
 #pragma unroll
@@ -348,7 +394,7 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                 const int d = DG ? cn + (KW - 1 - t) : cn * CS + t;
 #pragma unroll
                 for (int rb = 0; rb < 2; rb++)   // transposed product: rows = samples, columns = channels
-                    acc[rb][cn] = mfma_mx<FMT>(bf[d], af[rb], acc[rb][cn], sb[d], sa[rb]);
+                    acc[rb][cn] = mfma_mx<FX, FW>(bf[d], af[rb], acc[rb][cn], sb[d], sa[rb]);
             }
         }
     }
@@ -414,12 +460,36 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
 #pragma unroll
                 for (int e = 0; e < 16; e++) m = max(m, __float_as_uint(v[e]) & 0x7FFFFFFFu);
                 m = wave_max_u32(m);
-                const bool q8 = p.qfmt == MXC_E4M3;
-                const uint32_t sc = q8 ? scale_code_from_bits<8>(m) : scale_code_from_bits<2>(m);
+                const bool q8 = p.qfmt == MXC_E4M3, q6 = p.qfmt == MXC_E2M3 || p.qfmt == MXC_E3M2;
+                const uint32_t sc = q8 ? scale_code_from_bits<8>(m)
+                                  : p.qfmt == MXC_E3M2 ? scale_code_from_bits<4>(m) : scale_code_from_bits<2>(m);
                 const float inv = inv_scale(sc);
                 const bool bad = sc == 0xFFu;
                 if (lane == 0) p.qscales[pix * p.q_ncb + cb] = (uint8_t)sc;
-                if (q8) {
+                if (q6) {
+                    // the lane's four runs of four samples: 16 codes in 96 bits,
+                    // run e4 (samples 8 e4 + 4 h ..) in bits 24 e4 .. 24 e4 + 23,
+                    // stored at byte 6 e4 + 3 h of the channel's 24-byte row
+                    float4 xv[4];
+#pragma unroll
+                    for (int e4 = 0; e4 < 4; e4++) xv[e4] = make_float4(v[4 * e4], v[4 * e4 + 1], v[4 * e4 + 2], v[4 * e4 + 3]);
+                    const v6i w = p.qfmt == MXC_E2M3 ? pack16_fp6<MXC_E2M3>(xv, inv) : pack16_fp6<MXC_E3M2>(xv, inv);
+                    const uint32_t w0 = bad ? 0u : (uint32_t)w[0], w1 = bad ? 0u : (uint32_t)w[1],
+                                   w2 = bad ? 0u : (uint32_t)w[2];
+                    const uint32_t run[4] = {w0 & 0xFFFFFFu, (w0 >> 24) | ((w1 & 0xFFFFu) << 8),
+                                             (w1 >> 16) | ((w2 & 0xFFu) << 16), w2 >> 8};
+#pragma unroll
+                    for (int e4 = 0; e4 < 4; e4++) {
+                        uint8_t* d = ep + r * 24 + 6 * e4 + 3 * h;
+                        d[0] = (uint8_t)run[e4];
+                        d[1] = (uint8_t)(run[e4] >> 8);
+                        d[2] = (uint8_t)(run[e4] >> 16);
+                    }
+                    if (lane < 48) {
+                        const uint4 chunk = *(const uint4*)(ep + lane * 16);
+                        *(uint4*)(p.qcodes + (pix * p.q_ncb + cb) * 768 + lane * 16) = chunk;
+                    }
+                } else if (q8) {
 #pragma unroll
                     for (int e4 = 0; e4 < 4; e4++)
                         *(uint32_t*)(ep + r * 32 + 8 * e4 + 4 * h) =
@@ -481,7 +551,7 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
     }
 }
 
-template <int FMT, bool DG, int KW, int S, int WGM, int PW>
+template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW>
 __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
     // XCD-aware order: consecutive tiles (same output row) on one XCD
     const int per_xcd = (gridDim.x + 7) / 8;
@@ -490,12 +560,12 @@ __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
     Phase f;
     f.ry = 0; f.rx = 0; f.kh0 = 0; f.nvh = p.kh; f.kw0 = 0;
     f.gh = p.hout; f.gw = p.wout; f.c0 = p.pw; f.r0 = p.ph;
-    lean_tile<FMT, DG, KW, S, WGM, PW>(p, lin, f);
+    lean_tile<FW, FX, DG, KW, S, WGM, PW>(p, lin, f);
 }
 
 // Stride-2 input gradient for kernel width KWF (1 or 3): the four phases in
 // one launch, tiles of phase (ry, rx) at [pofs[2 ry + rx], pofs[2 ry + rx + 1]).
-template <int FMT, int KWF, int WGM, int PW>
+template <int FW, int FX, int KWF, int WGM, int PW>
 __global__ __launch_bounds__(LT) void conv_lean_dg2_kernel(LeanArgs p) {
     const int per_xcd = (gridDim.x + 7) / 8;
     int lin = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
@@ -512,8 +582,8 @@ __global__ __launch_bounds__(LT) void conv_lean_dg2_kernel(LeanArgs p) {
     if (nvw == 0) f.nvh = 0;                       // no tap reaches the phase: its pixels are zero
     f.gh = (p.hout - f.ry + 1) / 2; f.gw = (p.wout - f.rx + 1) / 2;
     f.c0 = (f.rx + p.pw - f.kw0) / 2; f.r0 = (f.ry + p.ph - f.kh0) / 2;
-    if (KWF == 3 && nvw == 2) lean_tile<FMT, true, 2, 2, WGM, PW>(p, lin, f);
-    else                      lean_tile<FMT, true, 1, 2, WGM, PW>(p, lin, f);
+    if (KWF == 3 && nvw == 2) lean_tile<FW, FX, true, 2, 2, WGM, PW>(p, lin, f);
+    else                      lean_tile<FW, FX, true, 1, 2, WGM, PW>(p, lin, f);
 }
 
 // LDS bytes of one launch: the stage ring, and at least the 4 x 4 KB the
@@ -536,39 +606,44 @@ int lean_launch(K kernel, bool& attr, const LeanArgs& a, int ntiles, size_t lds,
     return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
 }
 
-template <int FMT, bool DG, int KW, int S, int WGM, int PW>
+template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW>
 int launch_lean_t(const LeanArgs& a, int nbufs_used, hipStream_t s) {
     static bool attr = false;
-    return lean_launch(conv_lean_kernel<FMT, DG, KW, S, WGM, PW>, attr, a, a.ntiles, lean_lds(a, nbufs_used), s);
+    return lean_launch(conv_lean_kernel<FW, FX, DG, KW, S, WGM, PW>, attr, a, a.ntiles, lean_lds(a, nbufs_used), s);
 }
 
-template <int FMT, int KWF, int PW>
+template <int FW, int FX, int KWF, int PW>
 int launch_lean_dg2(const LeanArgs& a, int nbufs_used, hipStream_t s) {
     static bool attr = false;
-    return lean_launch(conv_lean_dg2_kernel<FMT, KWF, 1, PW>, attr, a, a.pofs[4], lean_lds(a, nbufs_used), s);
+    return lean_launch(conv_lean_dg2_kernel<FW, FX, KWF, 1, PW>, attr, a, a.pofs[4], lean_lds(a, nbufs_used), s);
 }
 
 // (WGM, PW) in use: (1, 1), (1, 2), (2, 2), (4, 2)
-template <int FMT, bool DG, int KW, int S>
+template <int FW, int FX, bool DG, int KW, int S>
 int launch_lean_w(const LeanArgs& a, int wgm, int pw, int nb, hipStream_t s) {
-    if (wgm == 4) return launch_lean_t<FMT, DG, KW, S, 4, 2>(a, nb, s);
-    if (wgm == 2) return launch_lean_t<FMT, DG, KW, S, 2, 2>(a, nb, s);
-    return pw == 1 ? launch_lean_t<FMT, DG, KW, S, 1, 1>(a, nb, s) : launch_lean_t<FMT, DG, KW, S, 1, 2>(a, nb, s);
+    if (wgm == 4) return launch_lean_t<FW, FX, DG, KW, S, 4, 2>(a, nb, s);
+    if (wgm == 2) return launch_lean_t<FW, FX, DG, KW, S, 2, 2>(a, nb, s);
+    return pw == 1 ? launch_lean_t<FW, FX, DG, KW, S, 1, 1>(a, nb, s) : launch_lean_t<FW, FX, DG, KW, S, 1, 2>(a, nb, s);
 }
 
-template <int FMT, bool DG>
+template <int FW, int FX, bool DG>
 int launch_lean_f(const LeanArgs& a, int kw, int sw, int wgm, int pw, int nb, hipStream_t s) {
     if constexpr (DG) {
         if (sw == 2) {
-            if (kw == 3) return pw == 1 ? launch_lean_dg2<FMT, 3, 1>(a, nb, s) : launch_lean_dg2<FMT, 3, 2>(a, nb, s);
-            return pw == 1 ? launch_lean_dg2<FMT, 1, 1>(a, nb, s) : launch_lean_dg2<FMT, 1, 2>(a, nb, s);
+            if (kw == 3) return pw == 1 ? launch_lean_dg2<FW, FX, 3, 1>(a, nb, s) : launch_lean_dg2<FW, FX, 3, 2>(a, nb, s);
+            return pw == 1 ? launch_lean_dg2<FW, FX, 1, 1>(a, nb, s) : launch_lean_dg2<FW, FX, 1, 2>(a, nb, s);
         }
-        return kw == 3 ? launch_lean_w<FMT, DG, 3, 1>(a, wgm, pw, nb, s) : launch_lean_w<FMT, DG, 1, 1>(a, wgm, pw, nb, s);
+        return kw == 3 ? launch_lean_w<FW, FX, DG, 3, 1>(a, wgm, pw, nb, s) : launch_lean_w<FW, FX, DG, 1, 1>(a, wgm, pw, nb, s);
     } else {
-        if (kw == 3) return sw == 2 ? launch_lean_w<FMT, DG, 3, 2>(a, wgm, pw, nb, s)
-                                    : launch_lean_w<FMT, DG, 3, 1>(a, wgm, pw, nb, s);
-        return sw == 2 ? launch_lean_w<FMT, DG, 1, 2>(a, wgm, pw, nb, s) : launch_lean_w<FMT, DG, 1, 1>(a, wgm, pw, nb, s);
+        if (kw == 3) return sw == 2 ? launch_lean_w<FW, FX, DG, 3, 2>(a, wgm, pw, nb, s)
+                                    : launch_lean_w<FW, FX, DG, 3, 1>(a, wgm, pw, nb, s);
+        return sw == 2 ? launch_lean_w<FW, FX, DG, 1, 2>(a, wgm, pw, nb, s) : launch_lean_w<FW, FX, DG, 1, 1>(a, wgm, pw, nb, s);
     }
+}
+
+template <int FW, int FX>
+int launch_lean_dir(const LeanArgs& a, bool dg, int kw, int sw, int wgm, int pw, int nb, hipStream_t s) {
+    return dg ? launch_lean_f<FW, FX, true>(a, kw, sw, wgm, pw, nb, s) : launch_lean_f<FW, FX, false>(a, kw, sw, wgm, pw, nb, s);
 }
 
 }  // namespace
@@ -638,12 +713,12 @@ int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws,
     // stage layout: DMA slices of the weight blocks, then the halo blocks,
     // rounded to whole 4 KB groups, then the scale entries; at stride 2 the
     // widest phase has (kw + 1) / 2 taps per row
-    const int tb = cv.bits == 8 ? 1024 : 512;
+    // (weights: format fa; source: fb; FP4 blocks take half a 1 KB slice)
+    const int bpiw = cv.fa == MXC_E2M1 ? 2 : 1, bpix = cv.fb == MXC_E2M1 ? 2 : 1;
     const int kwt = dg2 ? (cv.kw + 1) / 2 : cv.kw;
     const int hp = dg ? px + kwt - 1 : (px - 1) * cv.sw + cv.kw;
     const int na = kwt * 2 * 2 * wgm, nb = 2 * hp;
-    const int bpi = 1024 / tb;
-    const int nq = (na + nb + 4 * bpi - 1) / (4 * bpi);
+    const int nq = (na / bpiw + nb / bpix + 3) / 4;
     a.stage_bytes = nq * 4096 + SCALE_REGION;
     const int nstage = (dg2 ? (cv.kh + 1) / 2 : cv.kh) * ((a.kcb + 1) / 2);
     if (2 * a.stage_bytes > LDS_MAX || nstage < 1) return 1;
@@ -655,11 +730,15 @@ int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws,
         if ((long)per_cu * b * a.stage_bytes <= LDS_MAX) { nbuf = b; break; }
     a.nbuf = nbuf;
     const int used = nbuf < nstage ? nbuf : nstage;
-    if (cv.fmt == MXC_E4M3)
-        return dg ? launch_lean_f<MXC_E4M3, true>(a, cv.kw, cv.sw, wgm, pw, used, s)
-                  : launch_lean_f<MXC_E4M3, false>(a, cv.kw, cv.sw, wgm, pw, used, s);
-    return dg ? launch_lean_f<MXC_E2M1, true>(a, cv.kw, cv.sw, wgm, pw, used, s)
-              : launch_lean_f<MXC_E2M1, false>(a, cv.kw, cv.sw, wgm, pw, used, s);
+    if (cv.fa == MXC_E4M3 && cv.fb == MXC_E4M3)
+        return launch_lean_dir<MXC_E4M3, MXC_E4M3>(a, dg, cv.kw, cv.sw, wgm, pw, used, s);
+    if (cv.fa == MXC_E2M1 && cv.fb == MXC_E2M1)
+        return launch_lean_dir<MXC_E2M1, MXC_E2M1>(a, dg, cv.kw, cv.sw, wgm, pw, used, s);
+    if (cv.fa == MXC_E2M3 && cv.fb == MXC_E2M3)
+        return launch_lean_dir<MXC_E2M3, MXC_E2M3>(a, dg, cv.kw, cv.sw, wgm, pw, used, s);
+    if (cv.fa == MXC_E2M1 && cv.fb == MXC_E3M2)
+        return launch_lean_dir<MXC_E2M1, MXC_E3M2>(a, dg, cv.kw, cv.sw, wgm, pw, used, s);
+    return MXC_ERR_ARG;
 }
 
 }  // namespace mxc

@@ -44,7 +44,7 @@ __global__ __launch_bounds__(256) void im2col_kernel(const uint4* __restrict__ s
 
 int launch_im2col(const Conv& cv, const void* xc, const uint8_t* xs, void* cc, uint8_t* cs,
                   hipStream_t s) {
-    const long run_bytes = (long)cv.x.cp * cv.x.bn * cv.bits / 8;   // multiple of 32
+    const long run_bytes = (long)cv.x.cp * cv.x.bn * cv.x.bits / 8;   // a multiple of 16 (FP6: Bn >= 4)
     const int run16 = (int)(run_bytes / 16);
     const long row = (long)cv.wo * run16;            // chunks of one output row, one tap
     const long rows = (long)cv.x.ng * cv.ho;

@@ -14,15 +14,25 @@ namespace mxc {
 struct Geom {
     int n, c, h, w;
     int bn, np, cp, ng, ncb;  // batch block, padded batch, padded channels, groups, channel blocks
-    int bits;                 // 8 or 4
+    int fmt, bits;            // element format; bits 8 (E4M3), 6 (E2M3, E3M2) or 4 (E2M1)
 };
+
+// Element bits, exponent of the largest power of two below the maximum
+// (OCP emax), and the format selector of the block-scaled MFMA.
+constexpr int fmt_bits(int f) { return f == MXC_E4M3 ? 8 : f == MXC_E2M1 ? 4 : 6; }
+constexpr int fmt_emax(int f) { return f == MXC_E4M3 ? 8 : f == MXC_E3M2 ? 4 : 2; }
+constexpr int fmt_mfma(int f) { return f == MXC_E4M3 ? 0 : f == MXC_E2M3 ? 2 : f == MXC_E3M2 ? 3 : 4; }
+// FP6 blocks are copied into LDS 16 bytes per 12-byte half row, so a copy
+// reads up to 4 bytes past the last block: FP6 code buffers end with this
+// much read-only slack.
+constexpr size_t FP6_SLACK = 16;
 
 // Returns MXC_OK or an error code.
 int geom_init(Geom* g, int role, int fmt, int n, int c, int h, int w);
 
 static inline size_t geom_codes_bytes(const Geom& g) {
     size_t e = (size_t)g.np * g.h * g.w * g.cp;
-    return g.bits == 8 ? e : e / 2;
+    return e * g.bits / 8 + (g.bits == 6 ? FP6_SLACK : 0);
 }
 static inline size_t geom_scales_bytes(const Geom& g) {
     return (size_t)g.ng * g.h * g.w * g.ncb;
@@ -30,13 +40,18 @@ static inline size_t geom_scales_bytes(const Geom& g) {
 
 struct Conv {
     int n, cin, cout, h, w, kh, kw, sh, sw, ph, pw, ho, wo;
-    int fmt, bits;
+    int fmt, bits;   // the common format of the call's two operands (-1, 0: mixed)
+    int fa, fb;      // formats of the GEMM's first operand (W; G_Y for wgrad) and second (X or G_Y)
     Geom x;   // X  (n, cin, h, w), role ACT
     Geom gy;  // G_Y (n, cout, ho, wo), role ACT
     Geom wt;  // W  (cout, cin, kh, kw), role WEIGHT
 };
 
-int conv_init(Conv* cv, const mxc_conv* p, int fmt);
+// Which GEMM a call runs: the first and second operand of its format pair
+// are (W, X) for the forward, (W, G_Y) for the input gradient and (G_Y, X)
+// for the weight gradient.  CONV_ONE: a single format for every operand.
+enum { CONV_ONE = 0, CONV_FWD = 1, CONV_DGRAD = 2, CONV_WGRAD = 3 };
+int conv_init(Conv* cv, const mxc_conv* p, int fmt, int op = CONV_ONE);
 
 // ---------------------------------------------------------------- launchers
 int launch_quantize(const void* src, int dtype, int layout, int role, const Geom& g, int fmt,
@@ -148,6 +163,43 @@ __device__ __forceinline__ uint32_t pack8_e2m1(float4 x, float4 y, float inv) {
     return q;
 }
 
+// FP6 (E2M3 / E3M2): v_cvt_scalef32_2xpk16_{fp6,bf6}_f32 converts 32 floats
+// into one 192-bit string of codes, rounding to nearest even, saturating at
+// the format maximum and keeping the sign of zero (checked against the
+// reference rule on MI355X); it interleaves its two sources (code 2i from
+// the first, 2i + 1 from the second), so the even elements go first.
+typedef int v6i __attribute__((ext_vector_type(6)));
+template <int FMT>
+__device__ __forceinline__ v6i cvt32_fp6(const v16f& even, const v16f& odd) {
+    if constexpr (FMT == MXC_E2M3) return __builtin_amdgcn_cvt_scalef32_2xpk16_fp6_f32(even, odd, 1.0f);
+    else return __builtin_amdgcn_cvt_scalef32_2xpk16_bf6_f32(even, odd, 1.0f);
+}
+// 32 consecutive elements (x[0..7]) -> 24 bytes of codes
+template <int FMT>
+__device__ __forceinline__ v6i pack32_fp6(const float4* x, float inv) {
+    v16f a, b;
+#pragma unroll
+    for (int q = 0; q < 8; q++) {
+        a[2 * q] = x[q].x * inv; b[2 * q] = x[q].y * inv;
+        a[2 * q + 1] = x[q].z * inv; b[2 * q + 1] = x[q].w * inv;
+    }
+    return cvt32_fp6<FMT>(a, b);
+}
+// 16 consecutive elements (x[0..3]) -> 12 bytes of codes (the first three
+// dwords of the result)
+template <int FMT>
+__device__ __forceinline__ v6i pack16_fp6(const float4* x, float inv) {
+    v16f a, b;
+#pragma unroll
+    for (int q = 0; q < 4; q++) {
+        a[2 * q] = x[q].x * inv; b[2 * q] = x[q].y * inv;
+        a[2 * q + 1] = x[q].z * inv; b[2 * q + 1] = x[q].w * inv;
+    }
+#pragma unroll
+    for (int i = 8; i < 16; i++) { a[i] = 0.0f; b[i] = 0.0f; }
+    return cvt32_fp6<FMT>(a, b);
+}
+
 // four consecutive elements -> four E2M1 codes in 16 bits (first element in the low nibble)
 __device__ __forceinline__ unsigned short pack4_e2m1(float4 x, float inv) {
     uint32_t q = 0;
@@ -163,10 +215,13 @@ __device__ __forceinline__ unsigned short pack4_e2m1(float4 x, float inv) {
 //        bytes 16..31 = K-block 1 elements [16h, 16h+16)
 //   FP4: bytes 0..15  = K-block h, all 32 elements (nibble k = element k)
 //   scale operand: E8M0 of (row l%32, K-block h) in the low byte.
-template <int FMT>
+//   FP6: bytes 0..23  = K-block h, all 32 elements as a bit string (element
+//        k in bits 6k .. 6k+5), bytes 24..31 unused.
+// The two operands may have different formats (FA for a, FB for b).
+template <int FA, int FB = FA>
 __device__ __forceinline__ v16f mfma_mx(v8i a, v8i b, v16f c, int sa, int sb) {
-    return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, FMT == MXC_E4M3 ? 0 : 4,
-                                                           FMT == MXC_E4M3 ? 0 : 4, 0, sa, 0, sb);
+    constexpr int ca = fmt_mfma(FA), cb = fmt_mfma(FB);
+    return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, ca, cb, 0, sa, 0, sb);
 }
 
 // Asynchronous global -> LDS copies (global_load_lds).  Every lane supplies
@@ -229,6 +284,14 @@ __device__ __forceinline__ v2i lds_tr8(const uint8_t* p) {
 }
 __device__ __forceinline__ v2i lds_tr4(const uint8_t* p) {
     return __builtin_amdgcn_ds_read_tr4_b64_v2i32((lds_v2i*)(p));
+}
+//  tr6: lane i gets 6-bit element i of the 12-byte chunks addressed by lanes
+//       q, q = 0..15, as element q of its 96-bit result.  Every chunk address
+//       must be 16-byte aligned (the low four bits are ignored).
+typedef int v3i __attribute__((ext_vector_type(3)));
+typedef __attribute__((address_space(3))) v3i lds_v3i;
+__device__ __forceinline__ v3i lds_tr6(const uint8_t* p) {
+    return __builtin_amdgcn_ds_read_tr6_b96_v3i32((lds_v3i*)(p));
 }
 
 }  // namespace mxc

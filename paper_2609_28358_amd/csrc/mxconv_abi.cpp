@@ -5,12 +5,15 @@
 
 namespace mxc {
 
+static bool fmt_ok(int fmt) { return fmt >= MXC_E4M3 && fmt <= MXC_E3M2; }
+
 int geom_init(Geom* g, int role, int fmt, int n, int c, int h, int w) {
-    if (fmt != MXC_E4M3 && fmt != MXC_E2M1) return MXC_ERR_ARG;
+    if (!fmt_ok(fmt)) return MXC_ERR_ARG;
     if (role != MXC_ACT && role != MXC_WEIGHT) return MXC_ERR_ARG;
     if (n <= 0 || c <= 0 || h <= 0 || w <= 0) return MXC_ERR_ARG;
     g->n = n; g->c = c; g->h = h; g->w = w;
-    g->bits = fmt == MXC_E4M3 ? 8 : 4;
+    g->fmt = fmt;
+    g->bits = fmt_bits(fmt);
     g->cp = (c + 31) / 32 * 32;
     g->ncb = g->cp / 32;
     if (role == MXC_WEIGHT) {
@@ -26,6 +29,7 @@ int geom_init(Geom* g, int role, int fmt, int n, int c, int h, int w) {
         }
         g->np = n;
         if (fmt == MXC_E2M1 && g->bn < 2) return MXC_ERR_SHAPE;
+        if (g->bits == 6 && g->bn < 4) return MXC_ERR_SHAPE;   // whole bytes per channel row
     }
     g->ng = g->np / g->bn;
     // sizes addressed with 32-bit pixel / block indices inside kernels
@@ -33,8 +37,21 @@ int geom_init(Geom* g, int role, int fmt, int n, int c, int h, int w) {
     return MXC_OK;
 }
 
-int conv_init(Conv* cv, const mxc_conv* p, int fmt) {
-    if (fmt != MXC_E4M3 && fmt != MXC_E2M1) return MXC_ERR_ARG;
+// The format pairs the GEMM kernels are built for.
+static bool pair_ok(int fa, int fb) {
+    if (fa == fb) return fa == MXC_E4M3 || fa == MXC_E2M1 || fa == MXC_E2M3;
+    return fa == MXC_E2M1 && fb == MXC_E3M2;
+}
+
+int conv_init(Conv* cv, const mxc_conv* p, int fmt, int op) {
+    int f1 = fmt, f2 = fmt;
+    if (op != CONV_ONE) {
+        if ((fmt & ~0x1F) != 0) return MXC_ERR_ARG;
+        if (fmt & 0x10) { f1 = (fmt >> 2) & 3; f2 = fmt & 3; }
+        if (!fmt_ok(f1) || !fmt_ok(f2) || !pair_ok(f1, f2)) return MXC_ERR_ARG;
+    } else if (!fmt_ok(fmt)) {
+        return MXC_ERR_ARG;
+    }
     if (p->n <= 0 || p->cin <= 0 || p->cout <= 0 || p->h <= 0 || p->w <= 0 || p->kh <= 0 ||
         p->kw <= 0 || p->sh <= 0 || p->sw <= 0 || p->ph < 0 || p->pw < 0)
         return MXC_ERR_ARG;
@@ -43,12 +60,19 @@ int conv_init(Conv* cv, const mxc_conv* p, int fmt) {
     if (p->h + 2 * p->ph < p->kh || p->w + 2 * p->pw < p->kw) return MXC_ERR_SHAPE;
     cv->ho = (p->h + 2 * p->ph - p->kh) / p->sh + 1;
     cv->wo = (p->w + 2 * p->pw - p->kw) / p->sw + 1;
-    cv->fmt = fmt;
-    cv->bits = fmt == MXC_E4M3 ? 8 : 4;
+    // formats of X, G_Y and W (an operand the call does not read takes the
+    // format of one it does, for its geometry only)
+    int fx = f1, fg = f1, fw = f1;
+    if (op == CONV_FWD) { fw = f1; fx = f2; fg = f2; }
+    else if (op == CONV_DGRAD) { fw = f1; fg = f2; fx = f2; }
+    else if (op == CONV_WGRAD) { fg = f1; fx = f2; fw = f1; }
+    cv->fa = f1; cv->fb = f2;
+    cv->fmt = f1 == f2 ? f1 : -1;
+    cv->bits = f1 == f2 ? fmt_bits(f1) : 0;
     int rc;
-    if ((rc = geom_init(&cv->x, MXC_ACT, fmt, p->n, p->cin, p->h, p->w))) return rc;
-    if ((rc = geom_init(&cv->gy, MXC_ACT, fmt, p->n, p->cout, cv->ho, cv->wo))) return rc;
-    if ((rc = geom_init(&cv->wt, MXC_WEIGHT, fmt, p->cout, p->cin, p->kh, p->kw))) return rc;
+    if ((rc = geom_init(&cv->x, MXC_ACT, fx, p->n, p->cin, p->h, p->w))) return rc;
+    if ((rc = geom_init(&cv->gy, MXC_ACT, fg, p->n, p->cout, cv->ho, cv->wo))) return rc;
+    if ((rc = geom_init(&cv->wt, MXC_WEIGHT, fw, p->cout, p->cin, p->kh, p->kw))) return rc;
     return MXC_OK;
 }
 
@@ -82,7 +106,8 @@ int mxconv_out_size(const mxc_conv* p, int* ho, int* wo) {
 size_t mxconv_im2col_codes_bytes(const mxc_conv* p, int fmt) {
     Conv cv;
     if (!p || conv_init(&cv, p, fmt)) return 0;
-    return (size_t)cv.x.ng * cv.ho * cv.wo * cv.kh * cv.kw * cv.x.cp * cv.x.bn * cv.bits / 8;
+    return (size_t)cv.x.ng * cv.ho * cv.wo * cv.kh * cv.kw * cv.x.cp * cv.x.bn * cv.x.bits / 8 +
+           (cv.x.bits == 6 ? FP6_SLACK : 0);
 }
 
 size_t mxconv_im2col_scales_bytes(const mxc_conv* p, int fmt) {
@@ -93,7 +118,7 @@ size_t mxconv_im2col_scales_bytes(const mxc_conv* p, int fmt) {
 
 size_t mxconv_wgrad_workspace_bytes(const mxc_conv* p, int fmt) {
     Conv cv;
-    if (!p || conv_init(&cv, p, fmt)) return 0;
+    if (!p || conv_init(&cv, p, fmt, CONV_WGRAD)) return 0;
     return wgrad_workspace(cv);
 }
 
@@ -125,7 +150,7 @@ int mxconv_fwd(const mxc_conv* p, int fmt, const void* wc, const uint8_t* ws, co
     if (!p || !wc || !ws || !xc || !xs || !y) return MXC_ERR_NULL;
     if (y_layout != MXC_NCHW && y_layout != MXC_CBF) return MXC_ERR_ARG;
     Conv cv;
-    int rc = conv_init(&cv, p, fmt);
+    int rc = conv_init(&cv, p, fmt, CONV_FWD);
     if (rc) return rc;
     if (!aligned16(wc) || !aligned16(ws) || !aligned16(xc) || !aligned16(xs) || !aligned16(y))
         return MXC_ERR_ALIGN;
@@ -137,7 +162,7 @@ int mxconv_dgrad(const mxc_conv* p, int fmt, const void* wc, const uint8_t* ws, 
     if (!p || !wc || !ws || !gc || !gs || !gx) return MXC_ERR_NULL;
     if (gx_layout != MXC_NCHW && gx_layout != MXC_CBF) return MXC_ERR_ARG;
     Conv cv;
-    int rc = conv_init(&cv, p, fmt);
+    int rc = conv_init(&cv, p, fmt, CONV_DGRAD);
     if (rc) return rc;
     if (!aligned16(wc) || !aligned16(ws) || !aligned16(gc) || !aligned16(gs) || !aligned16(gx))
         return MXC_ERR_ALIGN;
@@ -148,7 +173,7 @@ int mxconv_wgrad(const mxc_conv* p, int fmt, const void* gc, const uint8_t* gs, 
                  const uint8_t* xs, float* gw, void* workspace, size_t ws_bytes, void* stream) {
     if (!p || !gc || !gs || !xc || !xs || !gw) return MXC_ERR_NULL;
     Conv cv;
-    int rc = conv_init(&cv, p, fmt);
+    int rc = conv_init(&cv, p, fmt, CONV_WGRAD);
     if (rc) return rc;
     const size_t need = wgrad_workspace(cv);
     if (need && (!workspace || ws_bytes < need)) return MXC_ERR_WORKSPACE;
@@ -171,9 +196,9 @@ int mxconv_fwd_quant(const mxc_conv* p, int fmt, const void* wc, const uint8_t* 
                      const uint8_t* xs, int fn, int out_fmt, void* yc, uint8_t* ysc, float* y_act,
                      void* stream) {
     if (!p || !wc || !ws || !xc || !xs || !yc || !ysc) return MXC_ERR_NULL;
-    if (fn < MXC_FN_NONE || fn > MXC_FN_SILU || (out_fmt != MXC_E4M3 && out_fmt != MXC_E2M1)) return MXC_ERR_ARG;
+    if (fn < MXC_FN_NONE || fn > MXC_FN_SILU || !fmt_ok(out_fmt)) return MXC_ERR_ARG;
     Conv cv;
-    int rc = conv_init(&cv, p, fmt);
+    int rc = conv_init(&cv, p, fmt, CONV_FWD);
     if (rc) return rc;
     if (!fused_shape(cv, false)) return MXC_ERR_SHAPE;
     if (!aligned16(wc) || !aligned16(ws) || !aligned16(xc) || !aligned16(xs) || !aligned16(yc) ||
@@ -188,10 +213,10 @@ int mxconv_dgrad_quant(const mxc_conv* p, int fmt, const void* wc, const uint8_t
                        const uint8_t* gs, int fn, const float* z, int out_fmt, void* gxc, uint8_t* gxs,
                        float* gx_act, void* stream) {
     if (!p || !wc || !ws || !gc || !gs || !gxc || !gxs) return MXC_ERR_NULL;
-    if (fn < MXC_FN_NONE || fn > MXC_FN_SILU || (out_fmt != MXC_E4M3 && out_fmt != MXC_E2M1)) return MXC_ERR_ARG;
+    if (fn < MXC_FN_NONE || fn > MXC_FN_SILU || !fmt_ok(out_fmt)) return MXC_ERR_ARG;
     if (fn != MXC_FN_NONE && !z) return MXC_ERR_NULL;
     Conv cv;
-    int rc = conv_init(&cv, p, fmt);
+    int rc = conv_init(&cv, p, fmt, CONV_DGRAD);
     if (rc) return rc;
     if (!fused_shape(cv, true)) return MXC_ERR_SHAPE;
     if (!aligned16(wc) || !aligned16(ws) || !aligned16(gc) || !aligned16(gs) || !aligned16(gxc) ||
@@ -234,6 +259,7 @@ int mxconv_naive_quantize_1d(const float* src, int64_t rows, int64_t cols, int d
 int mxconv_naive_fwd(const mxc_conv* p, int fmt, const void* cc, const uint8_t* cs, const void* wc,
                      const uint8_t* ws, float* y, void* stream) {
     if (!p || !cc || !cs || !wc || !ws || !y) return MXC_ERR_NULL;
+    if (fmt != MXC_E4M3 && fmt != MXC_E2M1) return MXC_ERR_ARG;   // the comparator runs MXFP8 / MXFP4
     Conv cv;
     int rc = conv_init(&cv, p, fmt);
     if (rc) return rc;
@@ -245,6 +271,7 @@ int mxconv_naive_fwd(const mxc_conv* p, int fmt, const void* cc, const uint8_t* 
 int mxconv_naive_dgrad(const mxc_conv* p, int fmt, const void* gc, const uint8_t* gs,
                        const void* wtc, const uint8_t* wts, float* gcol, float* gx, void* stream) {
     if (!p || !gc || !gs || !wtc || !wts || !gcol || !gx) return MXC_ERR_NULL;
+    if (fmt != MXC_E4M3 && fmt != MXC_E2M1) return MXC_ERR_ARG;   // the comparator runs MXFP8 / MXFP4
     Conv cv;
     int rc = conv_init(&cv, p, fmt);
     if (rc) return rc;
@@ -257,6 +284,7 @@ int mxconv_naive_dgrad(const mxc_conv* p, int fmt, const void* gc, const uint8_t
 int mxconv_naive_wgrad(const mxc_conv* p, int fmt, const void* gtc, const uint8_t* gts,
                        const void* xtc, const uint8_t* xts, float* gw, void* stream) {
     if (!p || !gtc || !gts || !xtc || !xts || !gw) return MXC_ERR_NULL;
+    if (fmt != MXC_E4M3 && fmt != MXC_E2M1) return MXC_ERR_ARG;   // the comparator runs MXFP8 / MXFP4
     Conv cv;
     int rc = conv_init(&cv, p, fmt);
     if (rc) return rc;
@@ -271,7 +299,8 @@ const char* mxconv_strerror(int code) {
         case MXC_ERR_NULL: return "a required pointer is NULL";
         case MXC_ERR_ARG: return "bad enum value or non-positive size";
         case MXC_ERR_SHAPE: return "unsupported shape (batch must divide 32 or be a multiple of 32; "
-                                   "E2M1 needs at least 2 samples per block; output must be non-empty)";
+                                   "E2M1 needs at least 2 samples per block, FP6 at least 4; output must be non-empty; "
+                                   "FP6 GEMMs need batch block 32 and the lean kernels' shapes)";
         case MXC_ERR_ALIGN: return "device pointer not 16-byte aligned";
         case MXC_ERR_HIP: return "HIP launch error";
         case MXC_ERR_WORKSPACE: return "workspace missing or too small";

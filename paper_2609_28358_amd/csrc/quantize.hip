@@ -13,8 +13,8 @@
 //      Bn lanes that share the block (xor shuffles);
 //   3. scale code from the exponent bits; elements scaled by 2^-s (exact) and
 //      encoded with the hardware converts, codes stored as 16-byte vectors.
-// Traffic: 4 (or 2) bytes read and 1 (or 1/2) byte written per element, plus
-// one scale byte per block; HBM-bound.
+// Traffic: 4 (or 2) bytes read and 1, 3/4 or 1/2 byte written per element
+// (FP8, FP6, FP4), plus one scale byte per block; HBM-bound.
 //
 // CBF sources with Bn = 32 and OIHW weights skip the slab: their blocks need
 // no transposition, so one wave quantizes one block straight from its
@@ -139,8 +139,7 @@ __global__ __launch_bounds__(QT) void quantize_kernel(const void* __restrict__ s
         const int pl = u / bn, part = u % bn;      // pixel in slab, unit within the block
         const int pix = p0 + pl;
         if (pix >= hw) continue;
-        constexpr int EMAX = FMT == MXC_E4M3 ? 8 : 2;
-        const uint32_t sc = scale_code_from_bits<EMAX>(m);
+        const uint32_t sc = scale_code_from_bits<fmt_emax(FMT)>(m);
         const size_t blk = ((size_t)ng * hw + pix) * g.ncb + cb;
         if (part == 0) scales[blk] = (uint8_t)sc;
         const float inv = inv_scale(sc);
@@ -155,6 +154,13 @@ __global__ __launch_bounds__(QT) void quantize_kernel(const void* __restrict__ s
             uint4* dst = (uint4*)(codes + e0);
             dst[0] = make_uint4(w[0], w[1], w[2], w[3]);
             dst[1] = make_uint4(w[4], w[5], w[6], w[7]);
+        } else if constexpr (fmt_bits(FMT) == 6) {
+            // 32 codes = 24 bytes at byte 3/4 e0 (a multiple of 24)
+            const v6i w = pack32_fp6<FMT>(x, inv);
+            uint2* dst = (uint2*)(codes + e0 / 4 * 3);
+            dst[0] = bad ? make_uint2(0, 0) : make_uint2(w[0], w[1]);
+            dst[1] = bad ? make_uint2(0, 0) : make_uint2(w[2], w[3]);
+            dst[2] = bad ? make_uint2(0, 0) : make_uint2(w[4], w[5]);
         } else {
             uint32_t w[4];
 #pragma unroll
@@ -172,6 +178,65 @@ __global__ __launch_bounds__(QT) void quantize_kernel(const void* __restrict__ s
 // [256 q + 4 l, 256 q + 4 l + 4), q = 0..3, so every load and store
 // instruction of the wave covers one contiguous range.
 // SRC 0: CBF activation, SRC 1: NCHW-ordered weights (n = Cout).
+// FP6 (768-byte blocks): lane l holds the 16 consecutive elements [16 l,
+// 16 l + 16) -- half a channel row -- and writes their 12 bytes of codes, so
+// the wave's store is one contiguous 768-byte run.
+template <int SRC, int DTYPE, int FMT>
+__device__ __forceinline__ void quantize_block_fp6(const void* __restrict__ src, const Geom& g,
+                                                   uint8_t* __restrict__ codes, uint8_t* __restrict__ scales,
+                                                   int blk, int lane) {
+    const int cb = blk % g.ncb, rest = blk / g.ncb;
+    const int c = cb * 32 + (lane >> 1);                     // channel (input channel) of the half row
+    const int j0 = 16 * (lane & 1);                          // first sample (output channel)
+    float4 x[4];
+    if (SRC == 0) {
+        const bool ok = c < g.c;
+        const size_t i0 = ((size_t)rest * g.c + (ok ? c : 0)) * 32 + j0;
+#pragma unroll
+        for (int q = 0; q < 4; q++) {
+            if (DTYPE == MXC_F32) {
+                x[q] = __ldg((const float4*)((const float*)src + i0 + 4 * q));
+            } else {
+                const uint2 b = __ldg((const uint2*)((const unsigned short*)src + i0 + 4 * q));
+                x[q] = make_float4(__uint_as_float(b.x << 16), __uint_as_float(b.x & 0xFFFF0000u),
+                                   __uint_as_float(b.y << 16), __uint_as_float(b.y & 0xFFFF0000u));
+            }
+            if (!ok) x[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+    } else {
+        const int hw = g.h * g.w;
+        const int cob = rest / hw, tap = rest % hw;
+        float v[16];
+#pragma unroll
+        for (int k = 0; k < 16; k++) {
+            const int n = cob * 32 + j0 + k;
+            const bool ok = c < g.c && n < g.n;
+            const size_t i = ok ? ((size_t)n * g.c + c) * hw + tap : 0;
+            v[k] = DTYPE == MXC_F32 ? __ldg((const float*)src + i)
+                                    : __uint_as_float((uint32_t)__ldg((const unsigned short*)src + i) << 16);
+            if (!ok) v[k] = 0.0f;
+        }
+#pragma unroll
+        for (int q = 0; q < 4; q++) x[q] = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+    }
+    uint32_t m = 0;
+#pragma unroll
+    for (int q = 0; q < 4; q++) {
+        m = max(m, __float_as_uint(x[q].x) & 0x7FFFFFFFu);
+        m = max(m, __float_as_uint(x[q].y) & 0x7FFFFFFFu);
+        m = max(m, __float_as_uint(x[q].z) & 0x7FFFFFFFu);
+        m = max(m, __float_as_uint(x[q].w) & 0x7FFFFFFFu);
+    }
+    m = wave_max_u32(m);
+    const uint32_t sc = scale_code_from_bits<fmt_emax(FMT)>(m);
+    if (lane == 0) scales[blk] = (uint8_t)sc;
+    const bool bad = sc == 0xFFu;
+    const v6i w = pack16_fp6<FMT>(x, inv_scale(sc));
+    v3i out;
+    out[0] = bad ? 0 : w[0]; out[1] = bad ? 0 : w[1]; out[2] = bad ? 0 : w[2];
+    *(v3i*)(codes + (size_t)blk * 768 + 12 * lane) = out;
+}
+
 template <int SRC, int DTYPE, int FMT>
 __global__ __launch_bounds__(QT) void quantize_block_kernel(const void* __restrict__ src, Geom g,
                                                             uint8_t* __restrict__ codes,
@@ -179,6 +244,10 @@ __global__ __launch_bounds__(QT) void quantize_block_kernel(const void* __restri
     const int lane = threadIdx.x & 63;
     const int blk = blockIdx.x * (QT / 64) + (threadIdx.x >> 6);
     if (blk >= nblocks) return;
+    if constexpr (fmt_bits(FMT) == 6) {
+        quantize_block_fp6<SRC, DTYPE, FMT>(src, g, codes, scales, blk, lane);
+        return;
+    }
     const int cb = blk % g.ncb, rest = blk / g.ncb;          // rest = (group, pixel) or (Cout block, tap)
     const int j = 4 * (lane & 7);                            // first sample (output channel) of the run
     float4 x[4];
@@ -223,8 +292,7 @@ __global__ __launch_bounds__(QT) void quantize_block_kernel(const void* __restri
         m = max(m, __float_as_uint(x[q].w) & 0x7FFFFFFFu);
     }
     m = wave_max_u32(m);
-    constexpr int EMAX = FMT == MXC_E4M3 ? 8 : 2;
-    const uint32_t sc = scale_code_from_bits<EMAX>(m);
+    const uint32_t sc = scale_code_from_bits<fmt_emax(FMT)>(m);
     if (lane == 0) scales[blk] = (uint8_t)sc;
     const float inv = inv_scale(sc);
     const bool bad = sc == 0xFFu;
@@ -278,8 +346,22 @@ int launch_q(const void* src, const Geom& g, void* codes, uint8_t* scales, hipSt
 template <int LAYOUT, int DTYPE>
 int launch_q_fmt(const void* src, const Geom& g, int fmt, void* codes, uint8_t* scales,
                  hipStream_t s) {
-    return fmt == MXC_E4M3 ? launch_q<LAYOUT, DTYPE, MXC_E4M3>(src, g, codes, scales, s)
-                           : launch_q<LAYOUT, DTYPE, MXC_E2M1>(src, g, codes, scales, s);
+    switch (fmt) {
+        case MXC_E4M3: return launch_q<LAYOUT, DTYPE, MXC_E4M3>(src, g, codes, scales, s);
+        case MXC_E2M3: return launch_q<LAYOUT, DTYPE, MXC_E2M3>(src, g, codes, scales, s);
+        case MXC_E3M2: return launch_q<LAYOUT, DTYPE, MXC_E3M2>(src, g, codes, scales, s);
+        default:       return launch_q<LAYOUT, DTYPE, MXC_E2M1>(src, g, codes, scales, s);
+    }
+}
+
+template <int SRC, int DTYPE>
+int launch_qb_fmt(const void* src, const Geom& g, int fmt, void* codes, uint8_t* scales, hipStream_t s) {
+    switch (fmt) {
+        case MXC_E4M3: return launch_qb<SRC, DTYPE, MXC_E4M3>(src, g, codes, scales, s);
+        case MXC_E2M3: return launch_qb<SRC, DTYPE, MXC_E2M3>(src, g, codes, scales, s);
+        case MXC_E3M2: return launch_qb<SRC, DTYPE, MXC_E3M2>(src, g, codes, scales, s);
+        default:       return launch_qb<SRC, DTYPE, MXC_E2M1>(src, g, codes, scales, s);
+    }
 }
 
 template <int LAYOUT>
@@ -295,18 +377,12 @@ int launch_quantize(const void* src, int dtype, int layout, int role, const Geom
                     uint8_t* scales, hipStream_t s) {
     // blocks that are contiguous (CBF, Bn = 32) or a small gather (weights): one wave per block
     const int blocksrc = (layout == MXC_CBF && g.bn == 32) ? 0 : (role == MXC_WEIGHT && layout == MXC_NCHW) ? 1 : -1;
-    if (blocksrc >= 0) {
-#define QB(S, D, F) return launch_qb<S, D, F>(src, g, codes, scales, s)
-        if (blocksrc == 0) {
-            if (dtype == MXC_F32) { if (fmt == MXC_E4M3) QB(0, MXC_F32, MXC_E4M3); QB(0, MXC_F32, MXC_E2M1); }
-            if (fmt == MXC_E4M3) QB(0, MXC_BF16, MXC_E4M3);
-            QB(0, MXC_BF16, MXC_E2M1);
-        }
-        if (dtype == MXC_F32) { if (fmt == MXC_E4M3) QB(1, MXC_F32, MXC_E4M3); QB(1, MXC_F32, MXC_E2M1); }
-        if (fmt == MXC_E4M3) QB(1, MXC_BF16, MXC_E4M3);
-        QB(1, MXC_BF16, MXC_E2M1);
-#undef QB
-    }
+    if (blocksrc == 0)
+        return dtype == MXC_F32 ? launch_qb_fmt<0, MXC_F32>(src, g, fmt, codes, scales, s)
+                                : launch_qb_fmt<0, MXC_BF16>(src, g, fmt, codes, scales, s);
+    if (blocksrc == 1)
+        return dtype == MXC_F32 ? launch_qb_fmt<1, MXC_F32>(src, g, fmt, codes, scales, s)
+                                : launch_qb_fmt<1, MXC_BF16>(src, g, fmt, codes, scales, s);
     switch (layout) {
         case MXC_NCHW: return launch_q_dt<MXC_NCHW>(src, dtype, g, fmt, codes, scales, s);
         case MXC_NHWC: return launch_q_dt<MXC_NHWC>(src, dtype, g, fmt, codes, scales, s);

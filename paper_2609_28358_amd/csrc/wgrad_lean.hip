@@ -4,8 +4,9 @@
 // With Bn = 32 the contraction runs along the samples of a block row, which
 // the CBF layout stores contiguously: a G_Y block is [32 Cout][32 samples]
 // and the X block of a tap's input pixel is [32 Cin][32 samples].  So both
-// MFMA operands are read straight from memory into registers, 16 bytes per
-// lane, with no LDS staging and no transposition: one 32 x 32 x 64 MFMA
+// MFMA operands are read straight from memory into registers (16 bytes per
+// lane; an FP6 row is 24 bytes), with no LDS staging and no transposition:
+// G_Y and X may have different element formats.  One 32 x 32 x 64 MFMA
 // contracts the 32 samples of two consecutive output pixels (K block 0 =
 // pixel P0, K block 1 = pixel P1), each K block with its own E8M0 scales.
 // Taps that fall into the padding read a zero block.
@@ -40,11 +41,34 @@ struct WLArgs {
     int nsplit;
 };
 
-template <int FMT>
+// One operand's fragment for a K step: K block 0 from pixel row p0, K block
+// 1 from p1 (rows already offset to this lane's row; zero block if invalid).
+// FP8: 16 bytes of each (the lane's half of the row); FP4 and FP6: the whole
+// row of the lane's own K block (ph = p0 or p1 by lane half).
+template <int F>
+__device__ __forceinline__ v8i row_frag(const uint8_t* p0, const uint8_t* p1, const uint8_t* ph) {
+    v8i o;
+    if constexpr (F == MXC_E4M3) {
+        const v4i u = *(const v4i*)p0, v = *(const v4i*)p1;
+#pragma unroll
+        for (int e = 0; e < 4; e++) { o[e] = u[e]; o[4 + e] = v[e]; }
+    } else if constexpr (fmt_bits(F) == 6) {
+        const v2i a = *(const v2i*)ph, b = *(const v2i*)(ph + 8), c = *(const v2i*)(ph + 16);
+        o[0] = a[0]; o[1] = a[1]; o[2] = b[0]; o[3] = b[1]; o[4] = c[0]; o[5] = c[1];
+        o[6] = o[7] = 0;
+    } else {
+        const v4i u = *(const v4i*)ph;
+#pragma unroll
+        for (int e = 0; e < 4; e++) { o[e] = u[e]; o[4 + e] = 0; }
+    }
+    return o;
+}
+
+template <int FA, int FB>
 __global__ __launch_bounds__(WT) void wgrad_lean_kernel(WLArgs p) {
-    constexpr int EB = FMT == MXC_E4M3 ? 8 : 4;
-    constexpr int RB = 32 * EB / 8;               // bytes of one block row (32 samples)
-    constexpr int TB = 32 * RB;                   // bytes of one block
+    constexpr int RBA = 32 * fmt_bits(FA) / 8;    // bytes of one block row (32 samples): G_Y
+    constexpr int RBB = 32 * fmt_bits(FB) / 8;    // X
+    constexpr int TBA = 32 * RBA, TBB = 32 * RBB; // bytes of one block
     __shared__ float red[4][64 * 64];
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -70,10 +94,10 @@ __global__ __launch_bounds__(WT) void wgrad_lean_kernel(WLArgs p) {
         const int cob = 2 * cop + i, cib = 2 * cip + i;
         a_ok[i] = cob < p.gy_ncb;
         b_ok[i] = cib < p.x_ncb;
-        a_off[i] = (uint32_t)(a_ok[i] ? cob : 0) * TB + r * RB + (FMT == MXC_E4M3 ? 16 * hf : 0);
-        b_off[i] = (uint32_t)(b_ok[i] ? cib : 0) * TB + r * RB + (FMT == MXC_E4M3 ? 16 * hf : 0);
+        a_off[i] = (uint32_t)(a_ok[i] ? cob : 0) * TBA + r * RBA + (FA == MXC_E4M3 ? 16 * hf : 0);
+        b_off[i] = (uint32_t)(b_ok[i] ? cib : 0) * TBB + r * RBB + (FB == MXC_E4M3 ? 16 * hf : 0);
     }
-    const uint32_t gy_pix = (uint32_t)p.gy_ncb * TB, x_pix = (uint32_t)p.x_ncb * TB;
+    const uint32_t gy_pix = (uint32_t)p.gy_ncb * TBA, x_pix = (uint32_t)p.x_ncb * TBB;
 
     v16f acc[2][2];
 #pragma unroll
@@ -109,31 +133,15 @@ __global__ __launch_bounds__(WT) void wgrad_lean_kernel(WLArgs p) {
         }
 #pragma unroll
         for (int i = 0; i < 2; i++) {
-            if (FMT == MXC_E4M3) {
-                v4i u[2], v[2];
+            const uint8_t* ap[2];
+            const uint8_t* bp[2];
 #pragma unroll
-                for (int k = 0; k < 2; k++) {
-                    const uint8_t* ap = (pg[k] >= 0 && a_ok[i]) ? p.gc + (size_t)pg[k] * gy_pix + a_off[i] : g_zero_wl;
-                    const uint8_t* bp = (qpix[k] >= 0 && b_ok[i]) ? p.xc + (size_t)qpix[k] * x_pix + b_off[i] : g_zero_wl;
-                    u[k] = *(const v4i*)ap;
-                    v[k] = *(const v4i*)bp;
-                }
-#pragma unroll
-                for (int e = 0; e < 4; e++) {
-                    o.a[i][e] = u[0][e]; o.a[i][4 + e] = u[1][e];
-                    o.b[i][e] = v[0][e]; o.b[i][4 + e] = v[1][e];
-                }
-            } else {
-                const int P = pg[hf], Q = qpix[hf];
-                const uint8_t* ap = (P >= 0 && a_ok[i]) ? p.gc + (size_t)P * gy_pix + a_off[i] : g_zero_wl;
-                const uint8_t* bp = (Q >= 0 && b_ok[i]) ? p.xc + (size_t)Q * x_pix + b_off[i] : g_zero_wl;
-                const v4i u = *(const v4i*)ap, v = *(const v4i*)bp;
-#pragma unroll
-                for (int e = 0; e < 4; e++) {
-                    o.a[i][e] = u[e]; o.a[i][4 + e] = 0;
-                    o.b[i][e] = v[e]; o.b[i][4 + e] = 0;
-                }
+            for (int k = 0; k < 2; k++) {
+                ap[k] = (pg[k] >= 0 && a_ok[i]) ? p.gc + (size_t)pg[k] * gy_pix + a_off[i] : g_zero_wl;
+                bp[k] = (qpix[k] >= 0 && b_ok[i]) ? p.xc + (size_t)qpix[k] * x_pix + b_off[i] : g_zero_wl;
             }
+            o.a[i] = row_frag<FA>(ap[0], ap[1], ap[hf]);
+            o.b[i] = row_frag<FB>(bp[0], bp[1], bp[hf]);
             // scale of (row, K block hf): the pixel of this lane's half
             const int P = pg[hf], Q = qpix[hf];
             const int cob = 2 * cop + i, cib = 2 * cip + i;
@@ -158,7 +166,7 @@ __global__ __launch_bounds__(WT) void wgrad_lean_kernel(WLArgs p) {
             for (int i = 0; i < 2; i++)
 #pragma unroll
                 for (int j = 0; j < 2; j++)
-                    acc[i][j] = mfma_mx<FMT>(o[b].a[i], o[b].b[j], acc[i][j], o[b].sa[i], o[b].sb[j]);
+                    acc[i][j] = mfma_mx<FA, FB>(o[b].a[i], o[b].b[j], acc[i][j], o[b].sa[i], o[b].sb[j]);
     }
 
     // ---- sum the four waves' tiles, then write
@@ -224,10 +232,12 @@ int launch_wgrad_lean(const Conv& cv, const void* gc, const uint8_t* gs, const v
     a.nsplit = splits;
     const long grid = ((long)a.ntiles * splits + 7) / 8 * 8;
     if (grid > 0x7FFFFFFFL) return MXC_ERR_SHAPE;
-    if (cv.fmt == MXC_E4M3)
-        hipLaunchKernelGGL(wgrad_lean_kernel<MXC_E4M3>, dim3((unsigned)grid), dim3(WT), 0, s, a);
-    else
-        hipLaunchKernelGGL(wgrad_lean_kernel<MXC_E2M1>, dim3((unsigned)grid), dim3(WT), 0, s, a);
+    const dim3 gd((unsigned)grid);
+    if (cv.fa == MXC_E4M3 && cv.fb == MXC_E4M3)      hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E4M3, MXC_E4M3>), gd, dim3(WT), 0, s, a);
+    else if (cv.fa == MXC_E2M1 && cv.fb == MXC_E2M1) hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E2M1, MXC_E2M1>), gd, dim3(WT), 0, s, a);
+    else if (cv.fa == MXC_E2M3 && cv.fb == MXC_E2M3) hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E2M3, MXC_E2M3>), gd, dim3(WT), 0, s, a);
+    else if (cv.fa == MXC_E2M1 && cv.fb == MXC_E3M2) hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E2M1, MXC_E3M2>), gd, dim3(WT), 0, s, a);
+    else return MXC_ERR_ARG;
     return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
 }
 

@@ -10,7 +10,7 @@ import os
 
 import torch
 
-E4M3, E2M1 = 0, 1
+E4M3, E2M1, E2M3, E3M2 = 0, 1, 2, 3
 F32, BF16 = 0, 1
 NCHW, NHWC, CBF = 0, 1, 2
 ACT, WEIGHT = 0, 1
@@ -70,6 +70,12 @@ def lib():
         fn.argtypes = args
     _lib = L
     return L
+
+
+def pair(first, second):
+    """The `fmt` argument of a GEMM entry point whose two MX operands have
+    these formats (first, second in the call's argument order)."""
+    return first if first == second else 0x10 | (first << 2) | second
 
 
 def strerror(rc):
@@ -181,14 +187,14 @@ def batch_block(n):
 def fwd(cv, w, x, layout=NCHW, out=None, stream=None):
     ho, wo = out_size(cv)
     y = _out((cv["n"], cv["cout"], ho, wo), layout, batch_block(cv["n"]), x.codes.device, out)
-    _check(lib().mxconv_fwd(ctypes.byref(conv_struct(cv)), x.fmt, _ptr(w.codes), _ptr(w.scales),
+    _check(lib().mxconv_fwd(ctypes.byref(conv_struct(cv)), pair(w.fmt, x.fmt), _ptr(w.codes), _ptr(w.scales),
                             _ptr(x.codes), _ptr(x.scales), _ptr(y), layout, _stream(stream)), "mxconv_fwd")
     return y
 
 
 def dgrad(cv, w, gy, layout=NCHW, out=None, stream=None):
     gx = _out((cv["n"], cv["cin"], cv["h"], cv["w"]), layout, batch_block(cv["n"]), gy.codes.device, out)
-    _check(lib().mxconv_dgrad(ctypes.byref(conv_struct(cv)), gy.fmt, _ptr(w.codes), _ptr(w.scales),
+    _check(lib().mxconv_dgrad(ctypes.byref(conv_struct(cv)), pair(w.fmt, gy.fmt), _ptr(w.codes), _ptr(w.scales),
                               _ptr(gy.codes), _ptr(gy.scales), _ptr(gx), layout, _stream(stream)),
            "mxconv_dgrad")
     return gx
@@ -197,11 +203,11 @@ def dgrad(cv, w, gy, layout=NCHW, out=None, stream=None):
 def wgrad(cv, gy, x, out=None, workspace=None, stream=None):
     gw = out if out is not None else torch.empty((cv["cout"], cv["cin"], cv["kh"], cv["kw"]),
                                                  dtype=torch.float32, device=x.codes.device)
-    need = wgrad_workspace_bytes(cv, x.fmt)
+    need = wgrad_workspace_bytes(cv, pair(gy.fmt, x.fmt))
     if workspace is None and need:
         workspace = torch.empty(need, dtype=torch.uint8, device=x.codes.device)
     wsz = workspace.numel() * workspace.element_size() if workspace is not None else 0
-    _check(lib().mxconv_wgrad(ctypes.byref(conv_struct(cv)), x.fmt, _ptr(gy.codes), _ptr(gy.scales),
+    _check(lib().mxconv_wgrad(ctypes.byref(conv_struct(cv)), pair(gy.fmt, x.fmt), _ptr(gy.codes), _ptr(gy.scales),
                               _ptr(x.codes), _ptr(x.scales), _ptr(gw), _ptr(workspace), wsz,
                               _stream(stream)), "mxconv_wgrad")
     return gw
@@ -215,7 +221,7 @@ def fwd_quant(cv, w, x, fn=FN_NONE, out_fmt=None, out=None, act_out=None, stream
     out_fmt = x.fmt if out_fmt is None else out_fmt
     shape = (cv["n"], cv["cout"], ho, wo)
     y = out if out is not None else MxTensor.empty(ACT, out_fmt, shape, x.codes.device)
-    _check(lib().mxconv_fwd_quant(ctypes.byref(conv_struct(cv)), x.fmt, _ptr(w.codes), _ptr(w.scales),
+    _check(lib().mxconv_fwd_quant(ctypes.byref(conv_struct(cv)), pair(w.fmt, x.fmt), _ptr(w.codes), _ptr(w.scales),
                                   _ptr(x.codes), _ptr(x.scales), fn, out_fmt, _ptr(y.codes), _ptr(y.scales),
                                   _ptr(act_out), _stream(stream)), "mxconv_fwd_quant")
     return y
@@ -228,7 +234,7 @@ def dgrad_quant(cv, w, gy, fn=FN_NONE, z=None, out_fmt=None, out=None, act_out=N
     out_fmt = gy.fmt if out_fmt is None else out_fmt
     shape = (cv["n"], cv["cin"], cv["h"], cv["w"])
     g = out if out is not None else MxTensor.empty(ACT, out_fmt, shape, gy.codes.device)
-    _check(lib().mxconv_dgrad_quant(ctypes.byref(conv_struct(cv)), gy.fmt, _ptr(w.codes), _ptr(w.scales),
+    _check(lib().mxconv_dgrad_quant(ctypes.byref(conv_struct(cv)), pair(w.fmt, gy.fmt), _ptr(w.codes), _ptr(w.scales),
                                     _ptr(gy.codes), _ptr(gy.scales), fn, _ptr(z), out_fmt, _ptr(g.codes),
                                     _ptr(g.scales), _ptr(act_out), _stream(stream)), "mxconv_dgrad_quant")
     return g

@@ -30,19 +30,24 @@ def test_library_exports_every_declared_symbol():
 
 def test_sizes_match_layout_and_oracle():
     for role in (mx.ACT, mx.WEIGHT):
-        for fmt in (mx.E4M3, mx.E2M1):
+        for fmt in (mx.E4M3, mx.E2M1, mx.E2M3, mx.E3M2):
             for shape in [(32, 64, 56, 56), (2, 32, 8, 8), (16, 3, 640, 640), (64, 100, 3, 5),
-                          (256, 64, 3, 3), (20, 33, 1, 1)]:
+                          (256, 64, 3, 3), (20, 33, 1, 1), (4, 40, 3, 3)]:
                 n, c, h, w = shape
                 if role == mx.ACT and not (n % 32 == 0 or 32 % n == 0):
                     continue
-                assert mx.codes_bytes(role, fmt, *shape) == oracle.codes_bytes(role, fmt, *shape)
+                slack = 16 if fmt in (mx.E2M3, mx.E3M2) else 0     # FP6 read slack
+                if role == mx.ACT and fmt in (mx.E2M3, mx.E3M2) and n < 4:
+                    assert mx.codes_bytes(role, fmt, *shape) == 0 and oracle.codes_bytes(role, fmt, *shape) < 0
+                    continue
+                assert mx.codes_bytes(role, fmt, *shape) == oracle.codes_bytes(role, fmt, *shape) + slack
                 assert mx.scales_bytes(role, fmt, *shape) == oracle.scales_bytes(role, fmt, *shape)
     # [N/Bn][H][W][Cp][Bn] codes, [N/Bn][H][W][Cp/32] scales
     assert mx.codes_bytes(mx.ACT, mx.E4M3, 32, 64, 56, 56) == 32 * 64 * 56 * 56
     assert mx.codes_bytes(mx.ACT, mx.E2M1, 16, 3, 640, 640) == 16 * 32 * 640 * 640 // 2
     assert mx.scales_bytes(mx.ACT, mx.E4M3, 16, 3, 640, 640) == 640 * 640
     assert mx.codes_bytes(mx.WEIGHT, mx.E4M3, 20, 33, 3, 3) == 32 * 64 * 9
+    assert mx.codes_bytes(mx.ACT, mx.E3M2, 32, 64, 56, 56) == 32 * 64 * 56 * 56 * 3 // 4 + 16
 
 
 def test_conv_sizes():
@@ -50,10 +55,12 @@ def test_conv_sizes():
                dict(n=8, cin=33, cout=20, h=9, w=7, kh=3, kw=2, sh=2, sw=1, ph=1, pw=0)):
         assert mx.out_size(cv) == synth.out_hw(cv) == oracle.conv_out(cv)
         c = mx.conv_struct(cv)
-        for fmt in (0, 1):
+        for fmt in (0, 1, 2, 3):
+            slack = 16 if fmt >= 2 else 0
             assert mx.lib().mxconv_im2col_codes_bytes(ctypes.byref(c), fmt) == oracle.load().o_im2col_codes_bytes(
-                oracle._ptr(oracle._conv_params(cv)), fmt)
-            assert mx.wgrad_workspace_bytes(cv, fmt) > 0
+                oracle._ptr(oracle._conv_params(cv)), fmt) + slack
+            if fmt < 2 or cv["n"] % 32 == 0:
+                assert mx.wgrad_workspace_bytes(cv, fmt if fmt != 3 else mx.pair(1, 3)) > 0
 
 
 P = ctypes.c_void_p
@@ -69,7 +76,10 @@ def test_quantize_errors():
     assert q(GOOD, 2, 0, 0, 0, 32, 32, 4, 4, GOOD, GOOD, None) == -2     # dtype
     assert q(GOOD, 0, 3, 0, 0, 32, 32, 4, 4, GOOD, GOOD, None) == -2     # layout
     assert q(GOOD, 0, 0, 2, 0, 32, 32, 4, 4, GOOD, GOOD, None) == -2     # role
-    assert q(GOOD, 0, 0, 0, 2, 32, 32, 4, 4, GOOD, GOOD, None) == -2     # fmt
+    assert q(GOOD, 0, 0, 0, 4, 32, 32, 4, 4, GOOD, GOOD, None) == -2     # fmt
+    assert q(GOOD, 0, 0, 0, mx.pair(1, 3), 32, 32, 4, 4, GOOD, GOOD, None) == -2   # no pairs here
+    assert q(GOOD, 0, 0, 0, 2, 2, 32, 4, 4, GOOD, GOOD, None) == -3      # FP6 with two samples
+    assert q(GOOD, 0, 0, 0, 3, 4, 32, 4, 4, GOOD, ODD, None) == -4       # FP6 with four: accepted
     assert q(GOOD, 0, 2, 1, 0, 32, 32, 4, 4, GOOD, GOOD, None) == -2     # CBF weights
     assert q(GOOD, 0, 0, 0, 0, 0, 32, 4, 4, GOOD, GOOD, None) == -2      # empty
     assert q(GOOD, 0, 0, 0, 0, 32, -1, 4, 4, GOOD, GOOD, None) == -2
@@ -166,7 +176,9 @@ def test_fused_errors():
     assert f(c, 0, GOOD, GOOD, GOOD, None, 0, 0, GOOD, GOOD, None, None) == -1
     assert f(c, 0, GOOD, GOOD, GOOD, GOOD, 3, 0, GOOD, GOOD, None, None) == -2      # activation
     assert f(c, 0, GOOD, GOOD, GOOD, GOOD, -1, 0, GOOD, GOOD, None, None) == -2
-    assert f(c, 0, GOOD, GOOD, GOOD, GOOD, 0, 2, GOOD, GOOD, None, None) == -2      # output format
+    assert f(c, 0, GOOD, GOOD, GOOD, GOOD, 0, 4, GOOD, GOOD, None, None) == -2      # output format
+    assert f(c, mx.pair(1, 3), GOOD, GOOD, GOOD, GOOD, 0, 3, ODD, GOOD, None, None) == -4   # MicroQonv+ accepted
+    assert f(c, mx.pair(3, 3), GOOD, GOOD, GOOD, GOOD, 0, 3, GOOD, GOOD, None, None) == -2
     assert f(c, 7, GOOD, GOOD, GOOD, GOOD, 0, 0, GOOD, GOOD, None, None) == -2      # operand format
     assert f(c16, 0, GOOD, GOOD, GOOD, GOOD, 0, 0, GOOD, GOOD, None, None) == -3
     assert f(c5, 0, GOOD, GOOD, GOOD, GOOD, 0, 0, GOOD, GOOD, None, None) == -3
@@ -178,8 +190,42 @@ def test_fused_errors():
     assert d(c, 0, GOOD, GOOD, GOOD, GOOD, 2, None, 0, GOOD, GOOD, None, None) == -1   # SiLU needs z
     assert d(c, 0, GOOD, GOOD, GOOD, GOOD, 0, None, 0, None, GOOD, None, None) == -1
     assert d(c, 0, GOOD, GOOD, GOOD, GOOD, 4, GOOD, 0, GOOD, GOOD, None, None) == -2
-    assert d(c, 0, GOOD, GOOD, GOOD, GOOD, 1, GOOD, 3, GOOD, GOOD, None, None) == -2
+    assert d(c, 0, GOOD, GOOD, GOOD, GOOD, 1, GOOD, 5, GOOD, GOOD, None, None) == -2
+    assert d(c, 2, GOOD, GOOD, GOOD, GOOD, 1, GOOD, 2, GOOD, GOOD, ODD, None) == -4
     assert d(c21, 0, GOOD, GOOD, GOOD, GOOD, 0, None, 0, GOOD, GOOD, None, None) == -3  # stride 2x1
     assert d(c16, 0, GOOD, GOOD, GOOD, GOOD, 1, GOOD, 0, GOOD, GOOD, None, None) == -3
     assert d(c, 0, GOOD, GOOD, GOOD, GOOD, 1, ODD, 0, GOOD, GOOD, None, None) == -4
     assert d(c, 0, GOOD, GOOD, GOOD, GOOD, 0, None, 0, GOOD, GOOD, ODD, None) == -4
+
+
+def test_fp6_format_pairs():
+    """The GEMM entry points take one format or MXC_PAIR(first, second); only
+    the pairs the kernels are built for pass validation (misaligned outputs
+    then stop the accepted ones before any launch)."""
+    L = mx.lib()
+    r = ctypes.byref(mx.conv_struct(synth.conv_dict(32, 64, 64, 8, 8, 3, 1, 1)))
+    accepted = [0, 1, 2, mx.pair(1, 3), 0x10 | (2 << 2) | 2]
+    refused = [3, mx.pair(3, 3), mx.pair(0, 1), mx.pair(1, 2), mx.pair(3, 1), 0x20, 0x10 | 15, 4, -1]
+    for fn in (L.mxconv_fwd, L.mxconv_dgrad):
+        for f in accepted:
+            assert fn(r, f, GOOD, GOOD, GOOD, GOOD, ODD, 0, None) == -4, f
+        for f in refused:
+            assert fn(r, f, GOOD, GOOD, GOOD, GOOD, GOOD, 0, None) == -2, f
+    for f in accepted:
+        assert L.mxconv_wgrad(r, f, GOOD, GOOD, GOOD, GOOD, ODD, None, 0, None) == -4, f
+    for f in refused:
+        assert L.mxconv_wgrad(r, f, GOOD, GOOD, GOOD, GOOD, GOOD, None, 0, None) == -2, f
+    # im2col and the size queries take a single format
+    assert L.mxconv_im2col_cbf(r, mx.pair(1, 3), GOOD, GOOD, GOOD, GOOD, None) == -2
+    assert L.mxconv_im2col_codes_bytes(r, mx.pair(1, 3)) == 0
+    # FP6 runs only on the batch-block-32 kernels: other layers are refused
+    # (after validation, with nothing launched)
+    for cvd in (synth.conv_dict(32, 64, 64, 8, 8, 5, 1, 2), synth.conv_dict(16, 64, 64, 8, 8, 3, 1, 1)):
+        rr = ctypes.byref(mx.conv_struct(cvd))
+        for f in (2, mx.pair(1, 3)):
+            assert L.mxconv_fwd(rr, f, GOOD, GOOD, GOOD, GOOD, GOOD, 0, None) == -3
+            assert L.mxconv_dgrad(rr, f, GOOD, GOOD, GOOD, GOOD, GOOD, 0, None) == -3
+    r16 = ctypes.byref(mx.conv_struct(synth.conv_dict(16, 64, 64, 8, 8, 3, 1, 1)))
+    assert L.mxconv_wgrad(r16, 2, GOOD, GOOD, GOOD, GOOD, GOOD, None, 0, None) == -3
+    # the naive comparator stays MXFP8 / MXFP4
+    assert L.mxconv_naive_fwd(r, 2, GOOD, GOOD, GOOD, GOOD, GOOD, None) == -2
