@@ -41,6 +41,11 @@ HBM_GBS = 8000.0                                   # MI355X HBM3E
 SPIN_CYCLES = 100000                               # GPU spin ahead of a timed eager launch
 MFMA_TFLOPS = {0: 5000.0, 1: 10100.0}              # dense MXFP8 / MXFP4
 FMT_NAME = {0: "mxfp8", 1: "mxfp4"}
+# FP6 methods of Sec. V as (W, X, G_Y) element formats: MicroQonv+ keeps
+# activations in E3M2 with FP4 weights and gradients; the "-6" methods use
+# E2M3 throughout
+FP6_METHODS = {"microqonv_plus": (1, 3, 1), "microqonv_6": (2, 2, 2)}
+FP6_SLACK = 16                                     # read slack at the end of an FP6 code buffer
 
 
 def layer_numbers(cv, fmt, mx):
@@ -240,6 +245,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-naive", action="store_true", help="skip the naive comparator leg")
     ap.add_argument("--no-fused", action="store_true", help="skip the fused-epilogue leg")
+    ap.add_argument("--no-fp6", action="store_true", help="skip the FP6-method leg")
     ap.add_argument("--pmc-pass", action="store_true",
                     help="counter-collection pass: every op once in step order, then a copy of known size")
     ap.add_argument("--layers", default="all", help="comma list of layer indices (profiling aid)")
@@ -454,6 +460,68 @@ def main():
                 "fwd_speedup": round(t["fwd_then_quantize"] / t["fwd_quant"], 2),
                 "dgrad_speedup": round(t["dgrad_then_quantize"] / t["dgrad_quant"], 2)})
 
+    # FP6 methods (outside the step): the same layers and ops with the FP6
+    # operand formats, timed like `ops` (steady state, quantize sources
+    # rotated through HBM), against the MXFP4 layer of the step.
+    fp6 = {}
+    if not args.no_fp6:
+        def mxbytes(role, f, shape):
+            b = mx.codes_bytes(role, f, *shape) + mx.scales_bytes(role, f, *shape)
+            return b - (FP6_SLACK if f in (2, 3) else 0)
+
+        def rotated(base):
+            ncopy = min(48, -(-(LLC_BYTES + (64 << 20)) // (base.numel() * base.element_size())))
+            return [base] + [base.clone() for _ in range(ncopy - 1)]
+
+        seen = set()
+        for j in jobs:
+            cv = j["cv"]
+            lname = j["name"].split("/")[0]
+            if lname in seen:
+                continue
+            seen.add(lname)
+            ho, wo = synth.out_hw(cv)
+            wsh = tuple(j["w"].shape)
+            xsrc, gsrc = rotated(j["x"]), rotated(j["gy"])
+            fl = j["nums"]["fwd"][0]
+            for meth, (fw, fx, fg) in FP6_METHODS.items():
+                qx = mx.MxTensor.empty(mx.ACT, fx, j["xs"], dev)
+                qw = mx.MxTensor.empty(mx.WEIGHT, fw, wsh, dev)
+                qg = mx.MxTensor.empty(mx.ACT, fg, j["gs"], dev)
+                wsb = torch.empty(max(1, mx.wgrad_workspace_bytes(cv, mx.pair(fg, fx))), dtype=torch.uint8, device=dev)
+                it = {"x": 0, "g": 0}
+
+                def qxr():
+                    it["x"] += 1
+                    mx.quantize(xsrc[it["x"] % len(xsrc)], mx.ACT, fx, layout=mx.CBF, shape=j["xs"], out=qx)
+
+                def qgr():
+                    it["g"] += 1
+                    mx.quantize(gsrc[it["g"] % len(gsrc)], mx.ACT, fg, layout=mx.CBF, shape=j["gs"], out=qg)
+
+                qxr(); qgr(); mx.quantize(j["w"], mx.WEIGHT, fw, out=qw)
+                kq = max(12, len(xsrc), len(gsrc))
+                t = {"quant_x": steady_ms(qxr, kq),
+                     "quant_w": steady_ms(lambda: mx.quantize(j["w"], mx.WEIGHT, fw, out=qw)),
+                     "quant_gy": steady_ms(qgr, kq)}
+                qxr(); qgr()
+                t["fwd"] = steady_ms(lambda: mx.fwd(cv, qw, qx, layout=mx.CBF, out=j["y"]))
+                t["dgrad"] = steady_ms(lambda: mx.dgrad(cv, qw, qg, layout=mx.CBF, out=j["gx"]))
+                t["wgrad"] = steady_ms(lambda: mx.wgrad(cv, qg, qx, out=j["gw"], workspace=wsb))
+                X, W, G = mxbytes(mx.ACT, fx, j["xs"]), mxbytes(mx.WEIGHT, fw, wsh), mxbytes(mx.ACT, fg, j["gs"])
+                fp4 = sum(steady[(f"{lname}/mxfp4", op)] for op in t if (f"{lname}/mxfp4", op) in steady)
+                r = {k + "_ms": round(v, 4) for k, v in t.items()}
+                r.update({"fwd_tflops": round(fl / (t["fwd"] * 1e-3) / 1e12, 1),
+                          "dgrad_tflops": round(fl / (t["dgrad"] * 1e-3) / 1e12, 1),
+                          "wgrad_tflops": round(fl / (t["wgrad"] * 1e-3) / 1e12, 1),
+                          "quant_x_gbps": round((4.0 * math.prod(j["xs"]) + X) / (t["quant_x"] * 1e-3) / 1e9, 1),
+                          "x_bytes": X, "w_bytes": W, "gy_bytes": G,
+                          "layer_ms": round(sum(t.values()), 4)})
+                if fp4:
+                    r["layer_ms_vs_mxfp4"] = round(sum(t.values()) / fp4, 3)
+                fp6[f"{lname}/{meth}"] = r
+            del xsrc, gsrc
+
     gemm_flops = sum(j["nums"][op][0] for j in jobs for op in ("fwd", "dgrad", "wgrad"))
     value = gemm_flops / (ms_step * 1e-3) / 1e12
 
@@ -501,6 +569,8 @@ def main():
         out["vs_naive"] = naive
     if fused:
         out["fused_epilogues"] = fused
+    if fp6:
+        out["fp6_methods"] = fp6
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline()
     print(json.dumps(out))
