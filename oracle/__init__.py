@@ -56,6 +56,10 @@ def load():
         "o_codes_bytes": (i64, [i32, i32, i32, i32, i32, i32]),
         "o_scales_bytes": (i64, [i32, i32, i32, i32, i32, i32]),
         "o_quantize": (i32, [P, i32, i32, i32, i32, i32, i32, i32, P, P]),
+        "o_quantize_sr": (i32, [P, i32, i32, i32, i32, i32, i32, i32, ctypes.c_uint64, P, P]),
+        "o_philox4x32_10": (None, [P, P, P]),
+        "o_sr_bits": (ctypes.c_uint, [ctypes.c_uint64, i64]),
+        "o_encode_sr": (i32, [dbl, i32, ctypes.c_uint]),
         "o_dequant": (i32, [P, P, i32, i32, i32, i32, i32, i32, P]),
         "o_conv_out": (i32, [P, P, P]),
         "o_im2col_cbf": (i32, [P, i32, P, P, P, P]),
@@ -144,6 +148,38 @@ def quantize(src, layout, role, fmt, n, c, h, w):
     _check(lib.o_quantize(_ptr(src), layout, role, fmt, n, c, h, w, _ptr(codes), _ptr(scales)),
            "quantize")
     return codes, scales
+
+
+def quantize_sr(src, layout, role, fmt, n, c, h, w, seed):
+    """quantize() with stochastic rounding of the elements under `seed`."""
+    lib = load()
+    src = np.ascontiguousarray(src, dtype=np.float32)
+    nb = lib.o_codes_bytes(role, fmt, n, c, h, w)
+    ns = lib.o_scales_bytes(role, fmt, n, c, h, w)
+    if nb < 0:
+        raise ValueError("bad geometry")
+    codes = np.zeros(nb, dtype=np.uint8)
+    scales = np.zeros(ns, dtype=np.uint8)
+    _check(lib.o_quantize_sr(_ptr(src), layout, role, fmt, n, c, h, w, int(seed) & (2 ** 64 - 1),
+                             _ptr(codes), _ptr(scales)), "quantize_sr")
+    return codes, scales
+
+
+def philox4x32_10(ctr, key):
+    """Philox4x32-10 of a 4-word counter under a 2-word key."""
+    c = np.ascontiguousarray(ctr, dtype=np.uint32)
+    k = np.ascontiguousarray(key, dtype=np.uint32)
+    out = np.zeros(4, dtype=np.uint32)
+    load().o_philox4x32_10(_ptr(c), _ptr(k), _ptr(out))
+    return out
+
+
+def sr_bits(seed, pos):
+    return load().o_sr_bits(int(seed) & (2 ** 64 - 1), int(pos))
+
+
+def encode_sr(v, fmt, r):
+    return load().o_encode_sr(float(v), fmt, int(r))
 
 
 def dequant(codes, scales, role, fmt, n, c, h, w):

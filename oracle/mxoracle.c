@@ -22,6 +22,10 @@
  *                         nearest-even with saturation.
  *   o_dequant             fake quantization: element value times the block
  *                         scale (Sec. III-A, below Eq. (6)).
+ *   o_quantize_sr         the same quantizer with stochastic rounding of the
+ *                         elements, the option Eq. (6) offers and Sec. III-A
+ *                         applies to gradients; random bits from
+ *                         o_philox4x32_10 (Salmon et al., SC'11).
  *   o_im2col_cbf          channel-batch-first im2col applied to MX codes
  *                         (Sec. IV-A; Fig. 3).
  *   o_fwd / o_wgrad /     the three GEMMs of Sec. IV-B,
@@ -53,6 +57,14 @@
  *   - code layout [N/Bn][H][W][Cp][Bn] (Bn fastest), scales
  *     [N/Bn][H][W][Cp/32]; FP4 packs two consecutive codes per byte, the
  *     even one in the low nibble.  Cp = C rounded up to 32; padding is +0.
+ *   - stochastic rounding (o_encode_sr): with lo <= |x| < hi the two
+ *     neighbouring grid values and frac = (|x| - lo) / (hi - lo), the element
+ *     becomes hi when r < frac * 2^16 for its 16 random bits r, else lo;
+ *     grid values stay exact, magnitudes at or above the format maximum
+ *     saturate, the scale rule is unchanged.  The bits of the code at linear
+ *     position p: Philox4x32-10 with key (seed mod 2^32, seed / 2^32) and
+ *     counter (p / 8 mod 2^32, p / 2^40, 0, 0) gives four words w0..w3;
+ *     j = p mod 8 selects bits 16 (j mod 2) .. 16 (j mod 2) + 15 of w[j / 2].
  *   - FP6 codes are packed as one little-endian bit string: the code at
  *     linear position p occupies bits 6p .. 6p+5 (bit 0 = least significant
  *     bit of byte 0), so 32 samples of one channel take 24 bytes.  The same
@@ -166,6 +178,65 @@ int o_scale_code(double amax, int fmt)
     if (s < -127) s = -127;
     if (s > 127) s = 127;
     return s + 127;
+}
+
+/* Philox4x32-10 (Salmon, Moraes, Dror, Shaw, "Parallel random numbers: as
+ * easy as 1, 2, 3", SC'11): ten rounds of two 32x32->64-bit products mixed
+ * with the key, the key advanced by the Weyl constants between rounds. */
+void o_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4])
+{
+    uint32_t c0 = ctr[0], c1 = ctr[1], c2 = ctr[2], c3 = ctr[3];
+    uint32_t k0 = key[0], k1 = key[1];
+    for (int round = 0; round < 10; round++) {
+        if (round > 0) { k0 += 0x9E3779B9u; k1 += 0xBB67AE85u; }
+        uint64_t p0 = (uint64_t)0xD2511F53u * c0;
+        uint64_t p1 = (uint64_t)0xCD9E8D57u * c2;
+        uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0;
+        uint32_t n1 = (uint32_t)p1;
+        uint32_t n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
+        uint32_t n3 = (uint32_t)p0;
+        c0 = n0; c1 = n1; c2 = n2; c3 = n3;
+    }
+    out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+/* The 16 random bits of code position pos (see the header). */
+unsigned o_sr_bits(uint64_t seed, int64_t pos)
+{
+    uint64_t q = (uint64_t)pos >> 3;
+    uint32_t ctr[4] = {(uint32_t)q, (uint32_t)(q >> 32), 0u, 0u};
+    uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+    uint32_t w[4];
+    o_philox4x32_10(ctr, key, w);
+    int j = (int)(pos & 7);
+    return (w[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
+}
+
+/* Stochastic rounding of v (already divided by the block scale) to the
+ * element format, with the 16 random bits r. */
+int o_encode_sr(double v, int fmt, unsigned r)
+{
+    o_fmt f;
+    if (fmt_get(fmt, &f)) return -1;
+    int neg = signbit(v) ? 1 : 0;
+    double a = fabs(v);
+    double pick;
+    if (a >= f.maxval) {
+        pick = f.maxval;
+    } else {
+        double q;                                       /* grid spacing at a */
+        if (a < f.min_normal) {
+            q = f.quantum;
+        } else {
+            int e2;
+            frexp(a, &e2);                              /* a in [2^(e2-1), 2^e2) */
+            q = ldexp(1.0, e2 - 1 - f.mbits);
+        }
+        double lo = floor(a / q) * q;                   /* exact: q is a power of two */
+        double frac = (a - lo) / q;                     /* in [0, 1), exact */
+        pick = ((double)r < frac * 65536.0) ? lo + q : lo;
+    }
+    return o_encode(neg ? -pick : pick, fmt);           /* pick is on the grid */
 }
 
 /* ------------------------------------------------------------------ */
@@ -297,8 +368,27 @@ int o_get_threads(void)
  * src: logical (n, c, h, w) tensor in `layout` (weights: OIHW, i.e. NCHW
  * with n = Cout, c = Cin).  codes/scales sized by o_codes_bytes/o_scales_bytes.
  * Returns 0, or a negative error. */
+static int quantize_impl(const float *src, int layout, int role, int fmt,
+                         int n, int c, int h, int w, int sr, uint64_t seed,
+                         uint8_t *codes, uint8_t *scales);
+
 int o_quantize(const float *src, int layout, int role, int fmt,
                int n, int c, int h, int w, uint8_t *codes, uint8_t *scales)
+{
+    return quantize_impl(src, layout, role, fmt, n, c, h, w, 0, 0, codes, scales);
+}
+
+/* As o_quantize, with every element rounded stochastically (Eq. (6)'s
+ * stochastic option) under `seed`. */
+int o_quantize_sr(const float *src, int layout, int role, int fmt,
+                  int n, int c, int h, int w, uint64_t seed, uint8_t *codes, uint8_t *scales)
+{
+    return quantize_impl(src, layout, role, fmt, n, c, h, w, 1, seed, codes, scales);
+}
+
+static int quantize_impl(const float *src, int layout, int role, int fmt,
+                         int n, int c, int h, int w, int sr, uint64_t seed,
+                         uint8_t *codes, uint8_t *scales)
 {
     o_geom g;
     o_fmt f;
@@ -334,8 +424,11 @@ int o_quantize(const float *src, int layout, int role, int fmt,
         int s = scode - 127;
         for (int ci = 0; ci < 32; ci++) {
             for (int j = 0; j < g.bn; j++) {
-                int code = nonfinite ? 0 : o_encode(ldexp(vals[ci][j], -s), fmt);
-                put_code(codes, g.bits, code_pos(&g, nb, hh, ww, cb * 32 + ci, j), code);
+                int64_t pos = code_pos(&g, nb, hh, ww, cb * 32 + ci, j);
+                int code = nonfinite ? 0
+                         : sr ? o_encode_sr(ldexp(vals[ci][j], -s), fmt, o_sr_bits(seed, pos))
+                              : o_encode(ldexp(vals[ci][j], -s), fmt);
+                put_code(codes, g.bits, pos, code);
             }
         }
     }

@@ -744,3 +744,108 @@ def test_act_grad_is_the_derivative():
     zz = np.linspace(-20, 20, 200001)
     gg = oracle.act_grad(zz, oracle.FN_SILU)
     assert gg.max() < 1.1 and gg.min() > -0.1
+
+
+# ---------------------------------------------------------------- stochastic rounding
+def test_philox_known_answers():
+    """The counter-based generator against its published known-answer vectors."""
+    rows = 0
+    with open(os.path.join(GOLDEN, "philox4x32_10_kat.txt")) as f:
+        for line in f:
+            if not line.strip() or line.startswith("#"):
+                continue
+            ctr, key, out = [[int(v, 16) for v in part.split()] for part in line.split("|")]
+            assert oracle.philox4x32_10(ctr, key).tolist() == out
+            rows += 1
+    assert rows == 3
+
+
+def test_sr_bits_follow_the_stated_counter_mapping():
+    """Position p takes half (p mod 2) of word (p mod 8) / 2 of the generator
+    at counter (p / 8 low, p / 8 high, 0, 0), key = the seed's two halves."""
+    for seed in (0, 12345, 2 ** 63 + 977):
+        key = [seed & 0xFFFFFFFF, seed >> 32]
+        for base in (0, 8 * 1000, 8 * (2 ** 33 + 5)):
+            q = base // 8
+            w = oracle.philox4x32_10([q & 0xFFFFFFFF, q >> 32, 0, 0], key)
+            halves = [(int(w[j // 2]) >> (16 * (j % 2))) & 0xFFFF for j in range(8)]
+            assert [oracle.sr_bits(seed, base + j) for j in range(8)] == halves
+
+
+@pytest.mark.parametrize("fmt", ALL_FMTS)
+def test_sr_picks_a_neighbour(fmt):
+    """Every stochastic result is one of the two grid values around |x| (by
+    enumeration of the grid), the sign is kept, grid values stay exact for
+    any random bits, and magnitudes at or above the maximum saturate."""
+    grid = [g for _, g in _grid(fmt)]
+    rng = np.random.default_rng(fmt + 40)
+    top = MAXV[fmt]
+    for v in np.concatenate([rng.random(400) * top, rng.random(200) * grid[2] * 2]):
+        lo = max(g for g in grid if g <= v)
+        hi = min([g for g in grid if g > v] or [top])
+        for r in rng.integers(0, 65536, 6):
+            for s in (v, -v):
+                d = oracle.decode(oracle.encode_sr(s, fmt, int(r)), fmt)
+                assert abs(d) in (lo, hi) and (d == 0 or math.copysign(1, d) == math.copysign(1, s))
+    for g in grid:
+        for r in (0, 1, 12345, 65535):
+            assert oracle.decode(oracle.encode_sr(g, fmt, r), fmt) == g
+            assert oracle.decode(oracle.encode_sr(-g, fmt, r), fmt) == -g
+    for v in (top * 1.01, top * 3, 1e30):
+        assert oracle.decode(oracle.encode_sr(v, fmt, 0), fmt) == top
+
+
+@pytest.mark.parametrize("fmt", ALL_FMTS)
+def test_sr_is_exactly_unbiased(fmt):
+    """Over all 2^16 values of the random bits, x rounds up exactly
+    ceil(frac * 2^16) times; when frac is a multiple of 2^-16 the mean of the
+    rounded values is x itself."""
+    grid = [g for _, g in _grid(fmt)]
+    m = len(grid) // 2
+    cases = [(grid[3], grid[4], 12345 / 65536), (grid[1], grid[2], 0.5), (grid[-3], grid[-2], 1 / 65536),
+             (grid[-2], grid[-1], 0.7), (grid[m], grid[m + 1], 0.25 + 3 / 65536)]
+    for lo, hi, frac in cases:
+        x = lo + frac * (hi - lo)
+        ups = sum(oracle.decode(oracle.encode_sr(x, fmt, r), fmt) == hi for r in range(65536))
+        assert ups == math.ceil(frac * 65536)
+        if (frac * 65536).is_integer():
+            assert lo + ups / 65536 * (hi - lo) == x
+
+
+@pytest.mark.parametrize("fmt", [oracle.E4M3, oracle.E2M1, oracle.E3M2])
+def test_quantize_sr_tensor(fmt):
+    """The tensor quantizer with stochastic rounding: scales are the
+    round-to-nearest ones; every element is a neighbour of its exact scaled
+    value; the same seed reproduces the codes and another seed changes them;
+    and the mean over 256 seeds of the dequantized tensor approaches x within
+    four standard errors of the rounding noise (which is at most half a
+    quantum per element)."""
+    n, c, h, w = 32, 40, 2, 3
+    x = _rand_tensor((n, c, h, w), 13)
+    rc, rs = oracle.quantize(x, oracle.NCHW, oracle.ACT, fmt, n, c, h, w)
+    c1, s1 = oracle.quantize_sr(x, oracle.NCHW, oracle.ACT, fmt, n, c, h, w, 7)
+    c1b, _ = oracle.quantize_sr(x, oracle.NCHW, oracle.ACT, fmt, n, c, h, w, 7)
+    c2, s2 = oracle.quantize_sr(x, oracle.NCHW, oracle.ACT, fmt, n, c, h, w, 8)
+    assert np.array_equal(s1, rs) and np.array_equal(s2, rs)
+    assert np.array_equal(c1, c1b) and not np.array_equal(c1, c2)
+    xd = x.astype(np.float64)
+    acc = np.zeros_like(xd)
+    seeds = 256
+    for seed in range(seeds):
+        cs, ss = oracle.quantize_sr(x, oracle.NCHW, oracle.ACT, fmt, n, c, h, w, 1000 + seed)
+        acc += oracle.dequant(cs, ss, oracle.ACT, fmt, n, c, h, w)
+    mean = acc / seeds
+    # block scales, and the grid spacing q around each scaled element (from
+    # the enumerated grid): the rounding noise has standard deviation <= q / 2
+    sc = np.zeros_like(xd)
+    for hh in range(h):
+        for ww in range(w):
+            for cb in range(2):
+                sc[:, cb * 32:(cb + 1) * 32, hh, ww] = 2.0 ** (int(rs[(hh * w + ww) * 2 + cb]) - 127)
+    grid = np.array([g for _, g in _grid(fmt)])
+    a = np.abs(xd) / sc
+    ok = a < MAXV[fmt]                      # saturated elements are not unbiased
+    k = np.clip(np.searchsorted(grid, a, side="right"), 1, len(grid) - 1)
+    q = (grid[k] - grid[k - 1]) * sc
+    bound = 4 * (q / 2) / np.sqrt(seeds)
+    assert np.all(np.abs(mean - xd)[ok] <= bound[ok])
