@@ -149,6 +149,23 @@ int mxconv_quantize(const void* src, int dtype, int layout, int role, int fmt,
                     int n, int c, int h, int w,
                     void* codes, uint8_t* scales, void* stream);
 
+/* Quantize with stochastic rounding of the elements (Eq. (6) allows
+ * round-to-nearest or stochastic rounding; Sec. III-A rounds gradients
+ * stochastically and activations and weights to nearest).  Same arguments,
+ * layout and scales as mxconv_quantize; each element becomes the upper of
+ * its two neighbouring grid values lo <= |x| 2^-s < hi when r < frac * 2^16,
+ * frac = (|x| 2^-s - lo) / (hi - lo), else the lower (sign kept; grid values
+ * are exact; magnitudes at or above the format maximum saturate).  r: the 16
+ * random bits of the code's linear position p in the code array: Philox4x32-10
+ * (Salmon et al., SC'11) with key (seed mod 2^32, seed / 2^32) and counter
+ * (p / 8 mod 2^32, p / 2^35, 0, 0) gives words w0..w3, and j = p mod 8 takes
+ * bits 16 (j mod 2) .. 16 (j mod 2) + 15 of w[j / 2].  The same seed and
+ * tensor always give the same codes, whatever the source layout.
+ * Errors: as mxconv_quantize. */
+int mxconv_quantize_sr(const void* src, int dtype, int layout, int role, int fmt,
+                       int n, int c, int h, int w, uint64_t seed,
+                       void* codes, uint8_t* scales, void* stream);
+
 /* ------------------------------------------------------------------ a2 */
 /* Channel-batch-first im2col on MX codes (Sec. IV-A, X'_{Cin,N}): for every
  * output pixel (ho, wo) and tap (kh, kw), the block of the input pixel

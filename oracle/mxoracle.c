@@ -63,7 +63,7 @@
  *     grid values stay exact, magnitudes at or above the format maximum
  *     saturate, the scale rule is unchanged.  The bits of the code at linear
  *     position p: Philox4x32-10 with key (seed mod 2^32, seed / 2^32) and
- *     counter (p / 8 mod 2^32, p / 2^40, 0, 0) gives four words w0..w3;
+ *     counter (p / 8 mod 2^32, p / 2^35, 0, 0) gives four words w0..w3;
  *     j = p mod 8 selects bits 16 (j mod 2) .. 16 (j mod 2) + 15 of w[j / 2].
  *   - FP6 codes are packed as one little-endian bit string: the code at
  *     linear position p occupies bits 6p .. 6p+5 (bit 0 = least significant

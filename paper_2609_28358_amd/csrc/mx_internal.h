@@ -54,8 +54,9 @@ enum { CONV_ONE = 0, CONV_FWD = 1, CONV_DGRAD = 2, CONV_WGRAD = 3 };
 int conv_init(Conv* cv, const mxc_conv* p, int fmt, int op = CONV_ONE);
 
 // ---------------------------------------------------------------- launchers
+// seed != NULL: elements rounded stochastically with that Philox key
 int launch_quantize(const void* src, int dtype, int layout, int role, const Geom& g, int fmt,
-                    void* codes, uint8_t* scales, hipStream_t s);
+                    void* codes, uint8_t* scales, hipStream_t s, const uint64_t* seed = nullptr);
 int launch_im2col(const Conv& cv, const void* xc, const uint8_t* xs, void* cc, uint8_t* cs,
                   hipStream_t s);
 int launch_fwd(const Conv& cv, const void* wc, const uint8_t* ws, const void* xc,
@@ -198,6 +199,76 @@ __device__ __forceinline__ v6i pack16_fp6(const float4* x, float inv) {
 #pragma unroll
     for (int i = 8; i < 16; i++) { a[i] = 0.0f; b[i] = 0.0f; }
     return cvt32_fp6<FMT>(a, b);
+}
+
+// ---------------------------------------------------------------- stochastic rounding
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of two
+// 32x32 -> 64-bit products mixed with the key, the key advanced by the Weyl
+// constants between rounds.
+__device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+    for (int round = 0; round < 10; round++) {
+        if (round > 0) { k0 += 0x9E3779B9u; k1 += 0xBB67AE85u; }
+        const uint64_t p0 = (uint64_t)0xD2511F53u * c.x;
+        const uint64_t p1 = (uint64_t)0xCD9E8D57u * c.z;
+        c = make_uint4((uint32_t)(p1 >> 32) ^ c.y ^ k0, (uint32_t)p1, (uint32_t)(p0 >> 32) ^ c.w ^ k1, (uint32_t)p0);
+    }
+    return c;
+}
+// The 16-bit random words of the eight code positions 8 q .. 8 q + 7:
+// position 8 q + j takes half (j mod 2) of word j / 2 at counter (q, 0, 0).
+__device__ __forceinline__ uint4 sr_words(uint64_t q, uint32_t k0, uint32_t k1) {
+    return philox4x32_10(make_uint4((uint32_t)q, (uint32_t)(q >> 32), 0u, 0u), k0, k1);
+}
+__device__ __forceinline__ uint32_t sr_half(const uint4& w, int j) {
+    const uint32_t v = (j >> 1) == 0 ? w.x : (j >> 1) == 1 ? w.y : (j >> 1) == 2 ? w.z : w.w;
+    return (j & 1) ? v >> 16 : v & 0xFFFFu;
+}
+
+template <int F> struct FmtSR;
+template <> struct FmtSR<MXC_E4M3> { static constexpr int MB = 3, BIAS = 7; static constexpr uint32_t MAXB = 0x43E00000u, MAXC = 0x7Eu; };
+template <> struct FmtSR<MXC_E2M1> { static constexpr int MB = 1, BIAS = 1; static constexpr uint32_t MAXB = 0x40C00000u, MAXC = 0x7u; };
+template <> struct FmtSR<MXC_E2M3> { static constexpr int MB = 3, BIAS = 1; static constexpr uint32_t MAXB = 0x40F00000u, MAXC = 0x1Fu; };
+template <> struct FmtSR<MXC_E3M2> { static constexpr int MB = 2, BIAS = 3; static constexpr uint32_t MAXB = 0x41E00000u, MAXC = 0x1Fu; };
+
+// Stochastic rounding of one finite element x of a block with scale 2^s
+// (inv = 2^-s) under 16 random bits r: with lo <= |x| 2^-s < hi the
+// neighbouring grid values, the code of hi when r < frac * 2^16, frac =
+// (|x| 2^-s - lo) / (hi - lo), else of lo; at or above the format maximum,
+// the maximum.  The decision is taken in integers on the bits of x itself
+// (|x| = M 2^(ex - 23)), so a scaled value below the fp32 range still rounds
+// exactly: |x| 2^-s / 2^(te - MB) = M 2^-k with te the scaled value's binade
+// (at least the format's smallest), and frac = (M mod 2^k) / 2^k.
+template <int FMT>
+__device__ __forceinline__ uint32_t encode_sr(float x, int s, float inv, uint32_t r) {
+    typedef FmtSR<FMT> F;
+    constexpr int MB = F::MB, BIAS = F::BIAS, EMIN = 1 - BIAS;
+    const uint32_t b = __float_as_uint(x), ab = b & 0x7FFFFFFFu;
+    const uint32_t scaled = __float_as_uint(x * inv) & 0x7FFFFFFFu;   // exact unless far below the maximum
+    uint32_t code;
+    if (scaled >= F::MAXB) {
+        code = F::MAXC;
+    } else if (ab == 0u) {
+        code = 0u;
+    } else {
+        const uint32_t fe = ab >> 23;
+        const uint32_t M = fe ? ((ab & 0x7FFFFFu) | 0x800000u) : ab;
+        const int ex = fe ? (int)fe - 127 : -126;
+        const int fl = fe ? ex : (31 - __clz((int)ab)) - 149;       // floor(log2 |x|)
+        const int te = max(fl - s, EMIN);
+        const int k = 23 + te - MB - ex + s;                          // >= 13 for any block scale
+        uint32_t mlo;
+        bool up;
+        if (k >= 32) {
+            mlo = 0u;
+            up = k > 40 ? r == 0u : ((uint64_t)r << k) < ((uint64_t)M << 16);
+        } else {
+            mlo = M >> k;
+            up = ((uint64_t)r << k) < ((uint64_t)(M & ((1u << k) - 1u)) << 16);
+        }
+        code = (uint32_t)(((te + BIAS) << MB) + (int)(mlo + (up ? 1u : 0u)) - (1 << MB));
+    }
+    return code | ((b >> 31) << (fmt_bits(FMT) - 1));
 }
 
 // four consecutive elements -> four E2M1 codes in 16 bits (first element in the low nibble)

@@ -135,6 +135,19 @@ int mxconv_quantize(const void* src, int dtype, int layout, int role, int fmt, i
     return launch_quantize(src, dtype, layout, role, g, fmt, codes, scales, (hipStream_t)stream);
 }
 
+int mxconv_quantize_sr(const void* src, int dtype, int layout, int role, int fmt, int n, int c,
+                       int h, int w, uint64_t seed, void* codes, uint8_t* scales, void* stream) {
+    if (!src || !codes || !scales) return MXC_ERR_NULL;
+    if (dtype != MXC_F32 && dtype != MXC_BF16) return MXC_ERR_ARG;
+    if (layout != MXC_NCHW && layout != MXC_NHWC && layout != MXC_CBF) return MXC_ERR_ARG;
+    if (layout == MXC_CBF && role != MXC_ACT) return MXC_ERR_ARG;
+    Geom g;
+    int rc = geom_init(&g, role, fmt, n, c, h, w);
+    if (rc) return rc;
+    if (!aligned16(src) || !aligned16(codes) || !aligned16(scales)) return MXC_ERR_ALIGN;
+    return launch_quantize(src, dtype, layout, role, g, fmt, codes, scales, (hipStream_t)stream, &seed);
+}
+
 int mxconv_im2col_cbf(const mxc_conv* p, int fmt, const void* xc, const uint8_t* xs, void* cc,
                       uint8_t* cs, void* stream) {
     if (!p || !xc || !xs || !cc || !cs) return MXC_ERR_NULL;

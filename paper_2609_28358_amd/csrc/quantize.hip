@@ -48,11 +48,63 @@ __device__ __forceinline__ float4 load4(const void* src, size_t i) {
 // All loads of a slab are issued before any is consumed (addresses of
 // out-of-range elements are clamped to the tensor's first element and the
 // value replaced by zero), so each thread has its whole slab share in flight.
-template <int LAYOUT, int DTYPE, int FMT, int VEC>
+__device__ __forceinline__ float comp(const float4& v, int t) {
+    return t == 0 ? v.x : t == 1 ? v.y : t == 2 ? v.z : v.w;
+}
+
+// Codes of 32 consecutive elements (x[0..7]) at code position e0 (a multiple
+// of 8) by stochastic rounding, written at their place in the code array.
+template <int FMT>
+__device__ __forceinline__ void store_sr32(uint8_t* __restrict__ codes, size_t e0, const float4* x, int s,
+                                           float inv, bool bad, uint32_t k0, uint32_t k1) {
+    uint32_t cd[32];
+#pragma unroll
+    for (int g8 = 0; g8 < 4; g8++) {
+        const uint4 w = sr_words((uint64_t)(e0 >> 3) + g8, k0, k1);
+#pragma unroll
+        for (int j = 0; j < 8; j++) {
+            const int k = 8 * g8 + j;
+            cd[k] = bad ? 0u : encode_sr<FMT>(comp(x[k >> 2], k & 3), s, inv, sr_half(w, j));
+        }
+    }
+    if constexpr (FMT == MXC_E4M3) {
+        uint32_t w[8];
+#pragma unroll
+        for (int q = 0; q < 8; q++) w[q] = cd[4 * q] | cd[4 * q + 1] << 8 | cd[4 * q + 2] << 16 | cd[4 * q + 3] << 24;
+        uint4* dst = (uint4*)(codes + e0);
+        dst[0] = make_uint4(w[0], w[1], w[2], w[3]);
+        dst[1] = make_uint4(w[4], w[5], w[6], w[7]);
+    } else if constexpr (fmt_bits(FMT) == 6) {
+        uint32_t w[6] = {0u, 0u, 0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int k = 0; k < 32; k++) {
+            const int bit = 6 * k;
+            w[bit >> 5] |= cd[k] << (bit & 31);
+            if ((bit & 31) > 26) w[(bit >> 5) + 1] |= cd[k] >> (32 - (bit & 31));
+        }
+        uint2* dst = (uint2*)(codes + e0 / 4 * 3);
+        dst[0] = make_uint2(w[0], w[1]);
+        dst[1] = make_uint2(w[2], w[3]);
+        dst[2] = make_uint2(w[4], w[5]);
+    } else {
+        uint32_t w[4];
+#pragma unroll
+        for (int q = 0; q < 4; q++) {
+            uint32_t v = 0u;
+#pragma unroll
+            for (int t = 0; t < 8; t++) v |= cd[8 * q + t] << (4 * t);
+            w[q] = v;
+        }
+        *(uint4*)(codes + e0 / 2) = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+}
+
+template <int LAYOUT, int DTYPE, int FMT, int VEC, bool SR>
 __global__ __launch_bounds__(QT) void quantize_kernel(const void* __restrict__ src, Geom g,
                                                       uint8_t* __restrict__ codes,
                                                       uint8_t* __restrict__ scales,
-                                                      int nslabs, int pixblocks, int slabs_per_wg) {
+                                                      int nslabs, int pixblocks, int slabs_per_wg,
+                                                      uint32_t k0, uint32_t k1) {
     __shared__ __attribute__((aligned(16))) float slab[QT * 32];
     const int tid = threadIdx.x;
     const int bn = g.bn, tt = QT / bn;
@@ -147,7 +199,9 @@ __global__ __launch_bounds__(QT) void quantize_kernel(const void* __restrict__ s
         const size_t e0 = (((size_t)ng * hw + pix) * g.cp + cb * 32) * bn + part * 32;
 
         // ---- 3. encode and store
-        if (FMT == MXC_E4M3) {
+        if constexpr (SR) {
+            store_sr32<FMT>(codes, e0, x, (int)sc - 127, inv, bad, k0, k1);
+        } else if (FMT == MXC_E4M3) {
             uint32_t w[8];
 #pragma unroll
             for (int q = 0; q < 8; q++) w[q] = bad ? 0u : pack4_e4m3(x[q], inv);
@@ -181,10 +235,12 @@ __global__ __launch_bounds__(QT) void quantize_kernel(const void* __restrict__ s
 // FP6 (768-byte blocks): lane l holds the 16 consecutive elements [16 l,
 // 16 l + 16) -- half a channel row -- and writes their 12 bytes of codes, so
 // the wave's store is one contiguous 768-byte run.
-template <int SRC, int DTYPE, int FMT>
-__device__ __forceinline__ void quantize_block_fp6(const void* __restrict__ src, const Geom& g,
-                                                   uint8_t* __restrict__ codes, uint8_t* __restrict__ scales,
-                                                   int blk, int lane) {
+// The same layout serves stochastic rounding in every format (positions
+// 16 l .. 16 l + 15 take their random bits from two generator calls).
+template <int SRC, int DTYPE, int FMT, bool SR>
+__device__ __forceinline__ void quantize_block16(const void* __restrict__ src, const Geom& g,
+                                                 uint8_t* __restrict__ codes, uint8_t* __restrict__ scales,
+                                                 int blk, int lane, uint32_t k0, uint32_t k1) {
     const int cb = blk % g.ncb, rest = blk / g.ncb;
     const int c = cb * 32 + (lane >> 1);                     // channel (input channel) of the half row
     const int j0 = 16 * (lane & 1);                          // first sample (output channel)
@@ -231,21 +287,59 @@ __device__ __forceinline__ void quantize_block_fp6(const void* __restrict__ src,
     const uint32_t sc = scale_code_from_bits<fmt_emax(FMT)>(m);
     if (lane == 0) scales[blk] = (uint8_t)sc;
     const bool bad = sc == 0xFFu;
-    const v6i w = pack16_fp6<FMT>(x, inv_scale(sc));
-    v3i out;
-    out[0] = bad ? 0 : w[0]; out[1] = bad ? 0 : w[1]; out[2] = bad ? 0 : w[2];
-    *(v3i*)(codes + (size_t)blk * 768 + 12 * lane) = out;
+    const float inv = inv_scale(sc);
+    if constexpr (!SR) {
+        const v6i w = pack16_fp6<FMT>(x, inv);
+        v3i out;
+        out[0] = bad ? 0 : w[0]; out[1] = bad ? 0 : w[1]; out[2] = bad ? 0 : w[2];
+        *(v3i*)(codes + (size_t)blk * 768 + 12 * lane) = out;
+    } else {
+        uint32_t cd[16];
+        const uint64_t q0 = (uint64_t)blk * 128 + 2 * lane;       // (1024 blk + 16 lane) / 8
+#pragma unroll
+        for (int g8 = 0; g8 < 2; g8++) {
+            const uint4 w = sr_words(q0 + g8, k0, k1);
+#pragma unroll
+            for (int j = 0; j < 8; j++) {
+                const int k = 8 * g8 + j;
+                cd[k] = bad ? 0u : encode_sr<FMT>(comp(x[k >> 2], k & 3), (int)sc - 127, inv, sr_half(w, j));
+            }
+        }
+        if constexpr (FMT == MXC_E4M3) {
+            uint32_t w[4];
+#pragma unroll
+            for (int q = 0; q < 4; q++) w[q] = cd[4 * q] | cd[4 * q + 1] << 8 | cd[4 * q + 2] << 16 | cd[4 * q + 3] << 24;
+            *(uint4*)(codes + (size_t)blk * 1024 + 16 * lane) = make_uint4(w[0], w[1], w[2], w[3]);
+        } else if constexpr (fmt_bits(FMT) == 6) {
+            uint32_t w[3] = {0u, 0u, 0u};
+#pragma unroll
+            for (int k = 0; k < 16; k++) {
+                const int bit = 6 * k;
+                w[bit >> 5] |= cd[k] << (bit & 31);
+                if ((bit & 31) > 26) w[(bit >> 5) + 1] |= cd[k] >> (32 - (bit & 31));
+            }
+            v3i out;
+            out[0] = (int)w[0]; out[1] = (int)w[1]; out[2] = (int)w[2];
+            *(v3i*)(codes + (size_t)blk * 768 + 12 * lane) = out;
+        } else {
+            uint32_t w[2] = {0u, 0u};
+#pragma unroll
+            for (int k = 0; k < 16; k++) w[k >> 3] |= cd[k] << (4 * (k & 7));
+            *(uint2*)(codes + (size_t)blk * 512 + 8 * lane) = make_uint2(w[0], w[1]);
+        }
+    }
 }
 
-template <int SRC, int DTYPE, int FMT>
+template <int SRC, int DTYPE, int FMT, bool SR>
 __global__ __launch_bounds__(QT) void quantize_block_kernel(const void* __restrict__ src, Geom g,
                                                             uint8_t* __restrict__ codes,
-                                                            uint8_t* __restrict__ scales, int nblocks) {
+                                                            uint8_t* __restrict__ scales, int nblocks,
+                                                            uint32_t k0, uint32_t k1) {
     const int lane = threadIdx.x & 63;
     const int blk = blockIdx.x * (QT / 64) + (threadIdx.x >> 6);
     if (blk >= nblocks) return;
-    if constexpr (fmt_bits(FMT) == 6) {
-        quantize_block_fp6<SRC, DTYPE, FMT>(src, g, codes, scales, blk, lane);
+    if constexpr (SR || fmt_bits(FMT) == 6) {
+        quantize_block16<SRC, DTYPE, FMT, SR>(src, g, codes, scales, blk, lane, k0, k1);
         return;
     }
     const int cb = blk % g.ncb, rest = blk / g.ncb;          // rest = (group, pixel) or (Cout block, tap)
@@ -307,18 +401,20 @@ __global__ __launch_bounds__(QT) void quantize_block_kernel(const void* __restri
     }
 }
 
-template <int SRC, int DTYPE, int FMT>
-int launch_qb(const void* src, const Geom& g, void* codes, uint8_t* scales, hipStream_t s) {
+template <int SRC, int DTYPE, int FMT, bool SR>
+int launch_qb(const void* src, const Geom& g, void* codes, uint8_t* scales, hipStream_t s, uint32_t k0,
+              uint32_t k1) {
     const long long nb = (long long)g.ng * g.h * g.w * g.ncb;
     if (nb > 0x7FFFFFFFLL - 4) return MXC_ERR_SHAPE;
     const int grid = (int)((nb + 3) / 4);
-    hipLaunchKernelGGL((quantize_block_kernel<SRC, DTYPE, FMT>), dim3(grid), dim3(QT), 0, s, src, g,
-                       (uint8_t*)codes, scales, (int)nb);
+    hipLaunchKernelGGL((quantize_block_kernel<SRC, DTYPE, FMT, SR>), dim3(grid), dim3(QT), 0, s, src, g,
+                       (uint8_t*)codes, scales, (int)nb, k0, k1);
     return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
 }
 
-template <int LAYOUT, int DTYPE, int FMT>
-int launch_q(const void* src, const Geom& g, void* codes, uint8_t* scales, hipStream_t s) {
+template <int LAYOUT, int DTYPE, int FMT, bool SR>
+int launch_q(const void* src, const Geom& g, void* codes, uint8_t* scales, hipStream_t s, uint32_t k0,
+             uint32_t k1) {
     const int tt = QT / g.bn;
     const int hw = g.h * g.w;
     const int pixblocks = (hw + tt - 1) / tt;
@@ -335,58 +431,64 @@ int launch_q(const void* src, const Geom& g, void* codes, uint8_t* scales, hipSt
     const int nwg = (int)((nslabs + spw - 1) / spw);
     const int grid = (nwg + 7) / 8 * 8;     // whole rounds over the 8 XCDs
     if (vec4)
-        hipLaunchKernelGGL((quantize_kernel<LAYOUT, DTYPE, FMT, 4>), dim3(grid), dim3(QT), 0, s, src, g,
-                           (uint8_t*)codes, scales, (int)nslabs, pixblocks, spw);
+        hipLaunchKernelGGL((quantize_kernel<LAYOUT, DTYPE, FMT, 4, SR>), dim3(grid), dim3(QT), 0, s, src, g,
+                           (uint8_t*)codes, scales, (int)nslabs, pixblocks, spw, k0, k1);
     else
-        hipLaunchKernelGGL((quantize_kernel<LAYOUT, DTYPE, FMT, 1>), dim3(grid), dim3(QT), 0, s, src, g,
-                           (uint8_t*)codes, scales, (int)nslabs, pixblocks, spw);
+        hipLaunchKernelGGL((quantize_kernel<LAYOUT, DTYPE, FMT, 1, SR>), dim3(grid), dim3(QT), 0, s, src, g,
+                           (uint8_t*)codes, scales, (int)nslabs, pixblocks, spw, k0, k1);
     return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
 }
 
-template <int LAYOUT, int DTYPE>
-int launch_q_fmt(const void* src, const Geom& g, int fmt, void* codes, uint8_t* scales,
-                 hipStream_t s) {
-    switch (fmt) {
-        case MXC_E4M3: return launch_q<LAYOUT, DTYPE, MXC_E4M3>(src, g, codes, scales, s);
-        case MXC_E2M3: return launch_q<LAYOUT, DTYPE, MXC_E2M3>(src, g, codes, scales, s);
-        case MXC_E3M2: return launch_q<LAYOUT, DTYPE, MXC_E3M2>(src, g, codes, scales, s);
-        default:       return launch_q<LAYOUT, DTYPE, MXC_E2M1>(src, g, codes, scales, s);
+// format and rounding dispatch: F(LAUNCHER, FMT, SR) expands to one launch
+#define MXC_FMT_SR_SWITCH(CALL)                                          \
+    switch (fmt) {                                                       \
+        case MXC_E4M3: return sr ? CALL(MXC_E4M3, true) : CALL(MXC_E4M3, false); \
+        case MXC_E2M3: return sr ? CALL(MXC_E2M3, true) : CALL(MXC_E2M3, false); \
+        case MXC_E3M2: return sr ? CALL(MXC_E3M2, true) : CALL(MXC_E3M2, false); \
+        default:       return sr ? CALL(MXC_E2M1, true) : CALL(MXC_E2M1, false); \
     }
+
+template <int LAYOUT, int DTYPE>
+int launch_q_fmt(const void* src, const Geom& g, int fmt, bool sr, void* codes, uint8_t* scales,
+                 hipStream_t s, uint32_t k0, uint32_t k1) {
+#define Q_CALL(F, R) launch_q<LAYOUT, DTYPE, F, R>(src, g, codes, scales, s, k0, k1)
+    MXC_FMT_SR_SWITCH(Q_CALL)
+#undef Q_CALL
 }
 
 template <int SRC, int DTYPE>
-int launch_qb_fmt(const void* src, const Geom& g, int fmt, void* codes, uint8_t* scales, hipStream_t s) {
-    switch (fmt) {
-        case MXC_E4M3: return launch_qb<SRC, DTYPE, MXC_E4M3>(src, g, codes, scales, s);
-        case MXC_E2M3: return launch_qb<SRC, DTYPE, MXC_E2M3>(src, g, codes, scales, s);
-        case MXC_E3M2: return launch_qb<SRC, DTYPE, MXC_E3M2>(src, g, codes, scales, s);
-        default:       return launch_qb<SRC, DTYPE, MXC_E2M1>(src, g, codes, scales, s);
-    }
+int launch_qb_fmt(const void* src, const Geom& g, int fmt, bool sr, void* codes, uint8_t* scales, hipStream_t s,
+                  uint32_t k0, uint32_t k1) {
+#define QB_CALL(F, R) launch_qb<SRC, DTYPE, F, R>(src, g, codes, scales, s, k0, k1)
+    MXC_FMT_SR_SWITCH(QB_CALL)
+#undef QB_CALL
 }
 
 template <int LAYOUT>
-int launch_q_dt(const void* src, int dtype, const Geom& g, int fmt, void* codes,
-                uint8_t* scales, hipStream_t s) {
-    return dtype == MXC_F32 ? launch_q_fmt<LAYOUT, MXC_F32>(src, g, fmt, codes, scales, s)
-                            : launch_q_fmt<LAYOUT, MXC_BF16>(src, g, fmt, codes, scales, s);
+int launch_q_dt(const void* src, int dtype, const Geom& g, int fmt, bool sr, void* codes,
+                uint8_t* scales, hipStream_t s, uint32_t k0, uint32_t k1) {
+    return dtype == MXC_F32 ? launch_q_fmt<LAYOUT, MXC_F32>(src, g, fmt, sr, codes, scales, s, k0, k1)
+                            : launch_q_fmt<LAYOUT, MXC_BF16>(src, g, fmt, sr, codes, scales, s, k0, k1);
 }
 
 }  // namespace
 
 int launch_quantize(const void* src, int dtype, int layout, int role, const Geom& g, int fmt, void* codes,
-                    uint8_t* scales, hipStream_t s) {
+                    uint8_t* scales, hipStream_t s, const uint64_t* seed) {
+    const bool sr = seed != nullptr;
+    const uint32_t k0 = sr ? (uint32_t)*seed : 0u, k1 = sr ? (uint32_t)(*seed >> 32) : 0u;
     // blocks that are contiguous (CBF, Bn = 32) or a small gather (weights): one wave per block
     const int blocksrc = (layout == MXC_CBF && g.bn == 32) ? 0 : (role == MXC_WEIGHT && layout == MXC_NCHW) ? 1 : -1;
     if (blocksrc == 0)
-        return dtype == MXC_F32 ? launch_qb_fmt<0, MXC_F32>(src, g, fmt, codes, scales, s)
-                                : launch_qb_fmt<0, MXC_BF16>(src, g, fmt, codes, scales, s);
+        return dtype == MXC_F32 ? launch_qb_fmt<0, MXC_F32>(src, g, fmt, sr, codes, scales, s, k0, k1)
+                                : launch_qb_fmt<0, MXC_BF16>(src, g, fmt, sr, codes, scales, s, k0, k1);
     if (blocksrc == 1)
-        return dtype == MXC_F32 ? launch_qb_fmt<1, MXC_F32>(src, g, fmt, codes, scales, s)
-                                : launch_qb_fmt<1, MXC_BF16>(src, g, fmt, codes, scales, s);
+        return dtype == MXC_F32 ? launch_qb_fmt<1, MXC_F32>(src, g, fmt, sr, codes, scales, s, k0, k1)
+                                : launch_qb_fmt<1, MXC_BF16>(src, g, fmt, sr, codes, scales, s, k0, k1);
     switch (layout) {
-        case MXC_NCHW: return launch_q_dt<MXC_NCHW>(src, dtype, g, fmt, codes, scales, s);
-        case MXC_NHWC: return launch_q_dt<MXC_NHWC>(src, dtype, g, fmt, codes, scales, s);
-        default:       return launch_q_dt<MXC_CBF>(src, dtype, g, fmt, codes, scales, s);
+        case MXC_NCHW: return launch_q_dt<MXC_NCHW>(src, dtype, g, fmt, sr, codes, scales, s, k0, k1);
+        case MXC_NHWC: return launch_q_dt<MXC_NHWC>(src, dtype, g, fmt, sr, codes, scales, s, k0, k1);
+        default:       return launch_q_dt<MXC_CBF>(src, dtype, g, fmt, sr, codes, scales, s, k0, k1);
     }
 }
 

@@ -49,6 +49,7 @@ def lib():
         "mxconv_im2col_scales_bytes": (sz, [CP, i32]),
         "mxconv_wgrad_workspace_bytes": (sz, [CP, i32]),
         "mxconv_quantize": (i32, [P, i32, i32, i32, i32, i32, i32, i32, i32, P, P, P]),
+        "mxconv_quantize_sr": (i32, [P, i32, i32, i32, i32, i32, i32, i32, i32, ctypes.c_uint64, P, P, P]),
         "mxconv_im2col_cbf": (i32, [CP, i32, P, P, P, P, P]),
         "mxconv_fwd": (i32, [CP, i32, P, P, P, P, P, i32, P]),
         "mxconv_dgrad": (i32, [CP, i32, P, P, P, P, P, i32, P]),
@@ -137,9 +138,7 @@ class MxTensor:
                         torch.empty(ns, dtype=torch.uint8, device=device), role, fmt, shape)
 
 
-def quantize(src, role, fmt, layout=NCHW, shape=None, out=None, stream=None):
-    """Quantize `src` (fp32 or bf16 device tensor) once.  `shape` is the
-    logical (n, c, h, w); it defaults to src.shape for NCHW."""
+def _quant_args(src, layout, shape):
     if shape is None:
         if layout == NHWC:
             n, h, w, c = src.shape
@@ -153,10 +152,27 @@ def quantize(src, role, fmt, layout=NCHW, shape=None, out=None, stream=None):
         raise MxconvError(f"unsupported dtype {src.dtype}")
     if not src.is_contiguous():
         raise MxconvError("src must be contiguous")
+    return dtype, tuple(int(v) for v in shape)
+
+
+def quantize(src, role, fmt, layout=NCHW, shape=None, out=None, stream=None):
+    """Quantize `src` (fp32 or bf16 device tensor) once.  `shape` is the
+    logical (n, c, h, w); it defaults to src.shape for NCHW."""
+    dtype, shape = _quant_args(src, layout, shape)
     if out is None:
         out = MxTensor.empty(role, fmt, shape, src.device)
-    _check(lib().mxconv_quantize(_ptr(src), dtype, layout, role, fmt, *[int(v) for v in shape],
+    _check(lib().mxconv_quantize(_ptr(src), dtype, layout, role, fmt, *shape,
                                  _ptr(out.codes), _ptr(out.scales), _stream(stream)), "mxconv_quantize")
+    return out
+
+
+def quantize_sr(src, role, fmt, seed, layout=NCHW, shape=None, out=None, stream=None):
+    """quantize() with stochastic rounding of the elements under `seed`."""
+    dtype, shape = _quant_args(src, layout, shape)
+    if out is None:
+        out = MxTensor.empty(role, fmt, shape, src.device)
+    _check(lib().mxconv_quantize_sr(_ptr(src), dtype, layout, role, fmt, *shape, int(seed) & (2 ** 64 - 1),
+                                    _ptr(out.codes), _ptr(out.scales), _stream(stream)), "mxconv_quantize_sr")
     return out
 
 

@@ -229,3 +229,16 @@ def test_fp6_format_pairs():
     assert L.mxconv_wgrad(r16, 2, GOOD, GOOD, GOOD, GOOD, GOOD, None, 0, None) == -3
     # the naive comparator stays MXFP8 / MXFP4
     assert L.mxconv_naive_fwd(r, 2, GOOD, GOOD, GOOD, GOOD, GOOD, None) == -2
+
+
+def test_quantize_sr_errors():
+    L = mx.lib()
+    q = L.mxconv_quantize_sr      # (src, dtype, layout, role, fmt, n, c, h, w, seed, codes, scales, stream)
+    assert q(None, 0, 0, 0, 0, 32, 32, 4, 4, 1, GOOD, GOOD, None) == -1
+    assert q(GOOD, 0, 0, 0, 0, 32, 32, 4, 4, 1, GOOD, None, None) == -1
+    assert q(GOOD, 2, 0, 0, 0, 32, 32, 4, 4, 1, GOOD, GOOD, None) == -2
+    assert q(GOOD, 0, 2, 1, 0, 32, 32, 4, 4, 1, GOOD, GOOD, None) == -2
+    assert q(GOOD, 0, 0, 0, 4, 32, 32, 4, 4, 1, GOOD, GOOD, None) == -2
+    assert q(GOOD, 0, 0, 0, 0, 48, 32, 4, 4, 1, GOOD, GOOD, None) == -3
+    assert q(GOOD, 0, 0, 0, 3, 2, 32, 4, 4, 1, GOOD, GOOD, None) == -3
+    assert q(GOOD, 0, 0, 0, 3, 32, 32, 4, 4, 2 ** 64 - 1, ODD, GOOD, None) == -4
