@@ -246,6 +246,7 @@ def main():
     ap.add_argument("--no-naive", action="store_true", help="skip the naive comparator leg")
     ap.add_argument("--no-fused", action="store_true", help="skip the fused-epilogue leg")
     ap.add_argument("--no-fp6", action="store_true", help="skip the FP6-method leg")
+    ap.add_argument("--no-sr", action="store_true", help="skip the stochastic-rounding leg")
     ap.add_argument("--pmc-pass", action="store_true",
                     help="counter-collection pass: every op once in step order, then a copy of known size")
     ap.add_argument("--layers", default="all", help="comma list of layer indices (profiling aid)")
@@ -522,6 +523,33 @@ def main():
                 fp6[f"{lname}/{meth}"] = r
             del xsrc, gsrc
 
+    # Stochastic rounding (outside the step): the gradient quantize with
+    # Eq. (6)'s stochastic option against the round-to-nearest one of the
+    # step, same source rotation.
+    sr = {}
+    if not args.no_sr:
+        for j in jobs:
+            fmt = j["fmt"]
+            gsrc = [j["gy"]] + [j["gy"].clone() for _ in range(min(48, -(-(LLC_BYTES + (64 << 20)) // (
+                j["gy"].numel() * j["gy"].element_size()))) - 1)]
+            it = [0]
+
+            def qsr():
+                it[0] += 1
+                mx.quantize_sr(gsrc[it[0] % len(gsrc)], mx.ACT, fmt, 7 + it[0], layout=mx.CBF, shape=j["gs"],
+                               out=j["qg"])
+
+            t_sr = steady_ms(qsr, max(12, len(gsrc)))
+            t_rn = steady[(j["name"], "quant_gy")]
+            by = j["nums"]["quant_gy"][1]
+            sr[j["name"]] = {"quant_gy_sr_ms": round(t_sr, 4), "quant_gy_ms": round(t_rn, 4),
+                             "sr_gbps": round(by / (t_sr * 1e-3) / 1e9, 1), "sr_over_rn": round(t_sr / t_rn, 3)}
+            del gsrc
+        # leave the step's G_Y codes as the round-to-nearest quantize made them
+        for j in jobs:
+            run_op(j, "quant_gy")
+        torch.cuda.synchronize()
+
     gemm_flops = sum(j["nums"][op][0] for j in jobs for op in ("fwd", "dgrad", "wgrad"))
     value = gemm_flops / (ms_step * 1e-3) / 1e12
 
@@ -571,6 +599,8 @@ def main():
         out["fused_epilogues"] = fused
     if fp6:
         out["fp6_methods"] = fp6
+    if sr:
+        out["stochastic_rounding"] = sr
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline()
     print(json.dumps(out))

@@ -238,37 +238,64 @@ template <> struct FmtSR<MXC_E3M2> { static constexpr int MB = 2, BIAS = 3; stat
 // the maximum.  The decision is taken in integers on the bits of x itself
 // (|x| = M 2^(ex - 23)), so a scaled value below the fp32 range still rounds
 // exactly: |x| 2^-s / 2^(te - MB) = M 2^-k with te the scaled value's binade
-// (at least the format's smallest), and frac = (M mod 2^k) / 2^k.
+// (at least the format's smallest), lo = (M >> k) quanta, frac = D / 2^k
+// with D = M mod 2^k, and r < frac * 2^16 <=> r < ceil(D 2^(16 - k)).
+// k >= 13 for every block scale; M < 2^24, so shifts are capped at 24.
+// Written without branches: every lane takes the same path.
 template <int FMT>
 __device__ __forceinline__ uint32_t encode_sr(float x, int s, float inv, uint32_t r) {
     typedef FmtSR<FMT> F;
     constexpr int MB = F::MB, BIAS = F::BIAS, EMIN = 1 - BIAS;
     const uint32_t b = __float_as_uint(x), ab = b & 0x7FFFFFFFu;
     const uint32_t scaled = __float_as_uint(x * inv) & 0x7FFFFFFFu;   // exact unless far below the maximum
-    uint32_t code;
-    if (scaled >= F::MAXB) {
-        code = F::MAXC;
-    } else if (ab == 0u) {
-        code = 0u;
-    } else {
-        const uint32_t fe = ab >> 23;
-        const uint32_t M = fe ? ((ab & 0x7FFFFFu) | 0x800000u) : ab;
-        const int ex = fe ? (int)fe - 127 : -126;
-        const int fl = fe ? ex : (31 - __clz((int)ab)) - 149;       // floor(log2 |x|)
-        const int te = max(fl - s, EMIN);
-        const int k = 23 + te - MB - ex + s;                          // >= 13 for any block scale
-        uint32_t mlo;
-        bool up;
-        if (k >= 32) {
-            mlo = 0u;
-            up = k > 40 ? r == 0u : ((uint64_t)r << k) < ((uint64_t)M << 16);
-        } else {
-            mlo = M >> k;
-            up = ((uint64_t)r << k) < ((uint64_t)(M & ((1u << k) - 1u)) << 16);
-        }
-        code = (uint32_t)(((te + BIAS) << MB) + (int)(mlo + (up ? 1u : 0u)) - (1 << MB));
-    }
+    const uint32_t fe = ab >> 23;
+    const uint32_t M = fe ? ((ab & 0x7FFFFFu) | 0x800000u) : ab;
+    const int ex = fe ? (int)fe - 127 : -126;
+    const int fl = fe ? ex : (31 - __clz((int)ab)) - 149;           // floor(log2 |x|)
+    const int te = max(fl - s, EMIN);
+    const int k = 23 + te - MB - ex + s;
+    const int kc = min(k, 24);
+    const uint32_t mlo = M >> kc;
+    const uint32_t D = M & ((1u << kc) - 1u);
+    const int sh = k - 16;                                            // >= -3
+    const int shc = min(sh, 24);
+    const uint32_t t = sh <= 0 ? D << (-sh) : (D + (1u << shc) - 1u) >> shc;
+    const uint32_t up = r < t ? 1u : 0u;
+    uint32_t code = (uint32_t)(((te + BIAS) << MB) - (1 << MB)) + mlo + up;
+    code = scaled >= F::MAXB ? F::MAXC : (ab == 0u ? 0u : code);
     return code | ((b >> 31) << (fmt_bits(FMT) - 1));
+}
+
+// The same decision for a normal fp32 x (or a zero), in fewer operations:
+// the carry out of the low k bits of M + R, R = ((2^16 - 1 - r) << (k - 16))
+// | (2^(k - 16) - 1), is exactly [r < ceil(D 2^(16 - k))], so the rounded
+// magnitude in quanta is (M + R) >> k.  For k > 31 (elements more than 2^8
+// quanta below the grid's first step) the low k - 31 bits of M are folded
+// into a sticky bit first, which leaves the decision unchanged.  An fp32
+// subnormal x (M without its implicit bit) needs encode_sr.
+template <int FMT>
+__device__ __forceinline__ uint32_t encode_sr_normal(float x, int s, float inv, uint32_t r) {
+    typedef FmtSR<FMT> F;
+    constexpr int MB = F::MB, BIAS = F::BIAS, EMIN = 1 - BIAS;
+    const uint32_t b = __float_as_uint(x), ab = b & 0x7FFFFFFFu;
+    const uint32_t scaled = __float_as_uint(x * inv) & 0x7FFFFFFFu;   // exact when at or above the maximum
+    const int ea = (int)(ab >> 23) - 127 - s;                         // binade of |x| 2^-s
+    const int te = max(ea, EMIN);
+    const int k = 23 - MB + te - ea;                                  // >= 20
+    const uint32_t M = (ab & 0x7FFFFFu) | 0x800000u;
+    const int sh2 = min(max(k - 31, 0), 24);
+    const int kk = min(k, 31);
+    const uint32_t Mp = (M >> sh2) + ((M & ((1u << sh2) - 1u)) != 0u ? 1u : 0u);
+    const uint32_t lowm = (1u << (kk - 16)) - 1u;
+    const uint32_t R = ((r ^ 0xFFFFu) << (kk - 16)) | lowm;
+    uint32_t code = (uint32_t)((te + BIAS - 1) << MB) + ((Mp + R) >> kk);
+    code = scaled >= F::MAXB ? F::MAXC : (ab == 0u ? 0u : code);
+    return code | ((b >> 31) << (fmt_bits(FMT) - 1));
+}
+// Does x need the general path (a non-zero fp32 subnormal)?
+__device__ __forceinline__ bool sr_needs_general(float x) {
+    const uint32_t ab = __float_as_uint(x) & 0x7FFFFFFFu;
+    return ab != 0u && ab < 0x800000u;
 }
 
 // four consecutive elements -> four E2M1 codes in 16 bits (first element in the low nibble)

@@ -52,21 +52,39 @@ __device__ __forceinline__ float comp(const float4& v, int t) {
     return t == 0 ? v.x : t == 1 ? v.y : t == 2 ? v.z : v.w;
 }
 
+// Stochastic codes of N consecutive elements x[0 .. N/4) whose first code
+// position is 8 q0; GEN selects the encoder that also handles fp32 subnormals.
+template <int FMT, int N, bool GEN>
+__device__ __forceinline__ void sr_codes(uint32_t* cd, const float4* x, uint64_t q0, int s, float inv, bool bad,
+                                         uint32_t k0, uint32_t k1) {
+#pragma unroll
+    for (int g8 = 0; g8 < N / 8; g8++) {
+        const uint4 w = sr_words(q0 + g8, k0, k1);
+#pragma unroll
+        for (int j = 0; j < 8; j++) {
+            const int k = 8 * g8 + j;
+            const float xv = comp(x[k >> 2], k & 3);
+            const uint32_t r = sr_half(w, j);
+            const uint32_t c = GEN ? encode_sr<FMT>(xv, s, inv, r) : encode_sr_normal<FMT>(xv, s, inv, r);
+            cd[k] = bad ? 0u : c;
+        }
+    }
+}
+
 // Codes of 32 consecutive elements (x[0..7]) at code position e0 (a multiple
 // of 8) by stochastic rounding, written at their place in the code array.
 template <int FMT>
 __device__ __forceinline__ void store_sr32(uint8_t* __restrict__ codes, size_t e0, const float4* x, int s,
                                            float inv, bool bad, uint32_t k0, uint32_t k1) {
     uint32_t cd[32];
+    bool gen = false;
 #pragma unroll
-    for (int g8 = 0; g8 < 4; g8++) {
-        const uint4 w = sr_words((uint64_t)(e0 >> 3) + g8, k0, k1);
-#pragma unroll
-        for (int j = 0; j < 8; j++) {
-            const int k = 8 * g8 + j;
-            cd[k] = bad ? 0u : encode_sr<FMT>(comp(x[k >> 2], k & 3), s, inv, sr_half(w, j));
-        }
-    }
+    for (int k = 0; k < 32; k++) gen |= sr_needs_general(comp(x[k >> 2], k & 3));
+    // wave-uniform choice: only a wave holding an fp32 subnormal takes the general path
+    if (__builtin_amdgcn_ballot_w64(gen) != 0)
+        sr_codes<FMT, 32, true>(cd, x, (uint64_t)(e0 >> 3), s, inv, bad, k0, k1);
+    else
+        sr_codes<FMT, 32, false>(cd, x, (uint64_t)(e0 >> 3), s, inv, bad, k0, k1);
     if constexpr (FMT == MXC_E4M3) {
         uint32_t w[8];
 #pragma unroll
@@ -296,15 +314,14 @@ __device__ __forceinline__ void quantize_block16(const void* __restrict__ src, c
     } else {
         uint32_t cd[16];
         const uint64_t q0 = (uint64_t)blk * 128 + 2 * lane;       // (1024 blk + 16 lane) / 8
+        bool gen = false;
 #pragma unroll
-        for (int g8 = 0; g8 < 2; g8++) {
-            const uint4 w = sr_words(q0 + g8, k0, k1);
-#pragma unroll
-            for (int j = 0; j < 8; j++) {
-                const int k = 8 * g8 + j;
-                cd[k] = bad ? 0u : encode_sr<FMT>(comp(x[k >> 2], k & 3), (int)sc - 127, inv, sr_half(w, j));
-            }
-        }
+        for (int k = 0; k < 16; k++) gen |= sr_needs_general(comp(x[k >> 2], k & 3));
+        const int s = (int)sc - 127;
+        if (__builtin_amdgcn_ballot_w64(gen) != 0)   // wave-uniform
+            sr_codes<FMT, 16, true>(cd, x, q0, s, inv, bad, k0, k1);
+        else
+            sr_codes<FMT, 16, false>(cd, x, q0, s, inv, bad, k0, k1);
         if constexpr (FMT == MXC_E4M3) {
             uint32_t w[4];
 #pragma unroll
