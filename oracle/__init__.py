@@ -60,6 +60,9 @@ def load():
         "o_philox4x32_10": (None, [P, P, P]),
         "o_sr_bits": (ctypes.c_uint, [ctypes.c_uint64, i64]),
         "o_encode_sr": (i32, [dbl, i32, ctypes.c_uint]),
+        "o_nvfp_scales_bytes": (i64, [i32, i32, i32, i32, i32, i32]),
+        "o_nvfp_quantize": (i32, [P, i32, i32, i32, i32, i32, i32, i32, P, P, P]),
+        "o_nvfp_dequant": (i32, [P, P, ctypes.c_float, i32, i32, i32, i32, i32, i32, P]),
         "o_dequant": (i32, [P, P, i32, i32, i32, i32, i32, i32, P]),
         "o_conv_out": (i32, [P, P, P]),
         "o_im2col_cbf": (i32, [P, i32, P, P, P, P]),
@@ -163,6 +166,29 @@ def quantize_sr(src, layout, role, fmt, n, c, h, w, seed):
     _check(lib.o_quantize_sr(_ptr(src), layout, role, fmt, n, c, h, w, int(seed) & (2 ** 64 - 1),
                              _ptr(codes), _ptr(scales)), "quantize_sr")
     return codes, scales
+
+
+def nvfp_quantize(src, layout, role, fmt, n, c, h, w):
+    """Eqs. (4)-(6) literally: returns (codes, E4M3 block scales, T)."""
+    lib = load()
+    src = np.ascontiguousarray(src, dtype=np.float32)
+    nb = lib.o_codes_bytes(role, fmt, n, c, h, w)
+    ns = lib.o_nvfp_scales_bytes(role, fmt, n, c, h, w)
+    if nb < 0 or ns < 0:
+        raise ValueError("bad geometry")
+    codes = np.zeros(nb, dtype=np.uint8)
+    scales = np.zeros(ns, dtype=np.uint8)
+    t = np.zeros(1, dtype=np.float32)
+    _check(lib.o_nvfp_quantize(_ptr(src), layout, role, fmt, n, c, h, w, _ptr(codes), _ptr(scales), _ptr(t)),
+           "nvfp_quantize")
+    return codes, scales, float(t[0])
+
+
+def nvfp_dequant(codes, scales, tscale, role, fmt, n, c, h, w):
+    out = np.zeros((n, c, h, w), dtype=np.float64)
+    _check(load().o_nvfp_dequant(_ptr(np.ascontiguousarray(codes)), _ptr(np.ascontiguousarray(scales)),
+                                 float(tscale), role, fmt, n, c, h, w, _ptr(out)), "nvfp_dequant")
+    return out
 
 
 def philox4x32_10(ctr, key):

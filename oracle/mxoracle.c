@@ -22,6 +22,10 @@
  *                         nearest-even with saturation.
  *   o_dequant             fake quantization: element value times the block
  *                         scale (Sec. III-A, below Eq. (6)).
+ *   o_nvfp_quantize /     the paper's own two-level format, Eqs. (4)-(6)
+ *   o_nvfp_dequant          literally: a per-tensor scale T, an FP8 E4M3
+ *                         scale per 8x8 square block (Sec. IV-B: B = 64),
+ *                         elements of any of the four element formats.
  *   o_quantize_sr         the same quantizer with stochastic rounding of the
  *                         elements, the option Eq. (6) offers and Sec. III-A
  *                         applies to gradients; random bits from
@@ -65,6 +69,18 @@
  *     position p: Philox4x32-10 with key (seed mod 2^32, seed / 2^32) and
  *     counter (p / 8 mod 2^32, p / 2^35, 0, 0) gives four words w0..w3;
  *     j = p mod 8 selects bits 16 (j mod 2) .. 16 (j mod 2) + 15 of w[j / 2].
+ *   - NVFP (Eqs. (4)-(6)), every step one fp32 operation rounded to nearest
+ *     even (the paper fixes no precision; its simulation runs in fp32):
+ *     T = fl(amax / fl(448 * emax_val)) over the whole tensor (emax_val =
+ *     the element format's largest value); per 8-channel x 8-sample block
+ *     (weights: 8 Cin x 8 Cout) B = CastE4M3(fl(bmax / fl(T * emax_val)))
+ *     with E4M3 rounding to nearest even, saturating at 448; element code =
+ *     encode(fl(x / fl(B * T))) (round to nearest even, saturating).  T = 0
+ *     or B = 0 gives zero codes.  A non-finite element anywhere makes T NaN,
+ *     every block scale the E4M3 NaN code 0x7F and every element code 0.
+ *     Codes use the MX-CBF code layout with Bn a multiple of 8 (n a multiple
+ *     of 32, or 8 or 16); block scales are E4M3 bytes in the layout
+ *     [Np/Bn][H][W][Cp/8][Bn/8].
  *   - FP6 codes are packed as one little-endian bit string: the code at
  *     linear position p occupies bits 6p .. 6p+5 (bit 0 = least significant
  *     bit of byte 0), so 32 samples of one channel take 24 bytes.  The same
@@ -453,6 +469,118 @@ int o_dequant(const uint8_t *codes, const uint8_t *scales, int role, int fmt,
                     int sc = scales[scale_pos(&g, nb, hh, ww, cc / 32)];
                     out[(((int64_t)nn * c + cc) * h + hh) * w + ww] =
                         o_decode(code, fmt) * o_scale_value(sc);
+                }
+    return 0;
+}
+
+/* ------------------------------------------------------------------ */
+/* NVFP, Eqs. (4)-(6) literally                                         */
+/* ------------------------------------------------------------------ */
+static int nvfp_geom(o_geom *g, int role, int fmt, int n, int c, int h, int w)
+{
+    int rc = geom_init(g, role, fmt, n, c, h, w);
+    if (rc) return rc;
+    if (g->bn % 8) return -3;                           /* 8x8 blocks */
+    return 0;
+}
+
+int64_t o_nvfp_scales_bytes(int role, int fmt, int n, int c, int h, int w)
+{
+    o_geom g;
+    if (nvfp_geom(&g, role, fmt, n, c, h, w)) return -1;
+    return (int64_t)(g.np / g.bn) * g.h * g.w * (g.cp / 8) * (g.bn / 8);
+}
+
+static int64_t nvfp_scale_pos(const o_geom *g, int nb, int hh, int ww, int cb8, int sb8)
+{
+    return ((((int64_t)nb * g->h + hh) * g->w + ww) * (g->cp / 8) + cb8) * (g->bn / 8) + sb8;
+}
+
+/* Quantize into NVFP: codes (o_codes_bytes), E4M3 block scales
+ * (o_nvfp_scales_bytes) and the per-tensor scale *tscale. */
+int o_nvfp_quantize(const float *src, int layout, int role, int fmt, int n, int c, int h, int w,
+                    uint8_t *codes, uint8_t *scales, float *tscale)
+{
+    o_geom g;
+    o_fmt f;
+    int rc = nvfp_geom(&g, role, fmt, n, c, h, w);
+    if (rc) return rc;
+    fmt_get(fmt, &f);
+    if (layout < O_NCHW || layout > O_CBF) return -2;
+    if (layout == O_CBF && role != O_ACT) return -2;
+    const float emaxv = (float)f.maxval;
+    /* Eq. (4): the per-tensor scale */
+    float amax = 0.0f;
+    int nonfinite = 0;
+    for (int nn = 0; nn < n; nn++)
+        for (int cc = 0; cc < c; cc++)
+            for (int hh = 0; hh < h; hh++)
+                for (int ww = 0; ww < w; ww++) {
+                    float x = (float)src_at(src, layout, &g, nn, cc, hh, ww);
+                    if (!isfinite(x)) nonfinite = 1;
+                    else if (fabsf(x) > amax) amax = fabsf(x);
+                }
+    volatile float denom_t = 448.0f * emaxv;
+    float T = nonfinite ? NAN : amax / denom_t;
+    *tscale = T;
+    volatile float tm = T * emaxv;                     /* T x max B_ef, rounded to fp32 */
+    int ngroups = g.np / g.bn;
+    for (int nb = 0; nb < ngroups; nb++)
+      for (int hh = 0; hh < g.h; hh++)
+        for (int ww = 0; ww < g.w; ww++)
+          for (int cb8 = 0; cb8 < g.cp / 8; cb8++)
+            for (int sb8 = 0; sb8 < g.bn / 8; sb8++) {
+                float v[8][8];
+                float bmax = 0.0f;
+                for (int i = 0; i < 8; i++)
+                    for (int j = 0; j < 8; j++) {
+                        int nn = nb * g.bn + sb8 * 8 + j, cc = cb8 * 8 + i;
+                        v[i][j] = (nn < g.n && cc < g.c) ? (float)src_at(src, layout, &g, nn, cc, hh, ww) : 0.0f;
+                        if (fabsf(v[i][j]) > bmax) bmax = fabsf(v[i][j]);
+                    }
+                int bcode;
+                float B = 0.0f;
+                if (nonfinite) {
+                    bcode = 0x7F;
+                } else if (T == 0.0f) {
+                    bcode = 0;
+                } else {
+                    volatile float ratio = bmax / tm;     /* Eq. (5), before the cast */
+                    bcode = o_encode((double)ratio, O_E4M3);
+                    B = (float)o_decode(bcode, O_E4M3);
+                }
+                scales[nvfp_scale_pos(&g, nb, hh, ww, cb8, sb8)] = (uint8_t)bcode;
+                volatile float bt = B * T;                /* B_scale x T_scale, rounded to fp32 */
+                for (int i = 0; i < 8; i++)
+                    for (int j = 0; j < 8; j++) {
+                        int code = 0;
+                        if (!nonfinite && bt != 0.0f) {
+                            volatile float q = v[i][j] / bt;   /* Eq. (6), before the rounding */
+                            code = o_encode((double)q, fmt);
+                        }
+                        put_code(codes, g.bits, code_pos(&g, nb, hh, ww, cb8 * 8 + i, sb8 * 8 + j), code);
+                    }
+            }
+    o_quantized_count += (int64_t)g.n * g.c * g.h * g.w;
+    return 0;
+}
+
+/* Fake quantization: code value x B x T, exact in fp64, real-sized NCHW. */
+int o_nvfp_dequant(const uint8_t *codes, const uint8_t *scales, float tscale, int role, int fmt,
+                   int n, int c, int h, int w, double *out)
+{
+    o_geom g;
+    int rc = nvfp_geom(&g, role, fmt, n, c, h, w);
+    if (rc) return rc;
+    for (int nn = 0; nn < n; nn++)
+        for (int cc = 0; cc < c; cc++)
+            for (int hh = 0; hh < h; hh++)
+                for (int ww = 0; ww < w; ww++) {
+                    int nb = nn / g.bn, j = nn % g.bn;
+                    int code = get_code(codes, g.bits, code_pos(&g, nb, hh, ww, cc, j));
+                    int b = scales[nvfp_scale_pos(&g, nb, hh, ww, cc / 8, j / 8)];
+                    out[(((int64_t)nn * c + cc) * h + hh) * w + ww] =
+                        o_decode(code, fmt) * o_decode(b, O_E4M3) * (double)tscale;
                 }
     return 0;
 }

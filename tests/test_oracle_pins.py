@@ -849,3 +849,105 @@ def test_quantize_sr_tensor(fmt):
     q = (grid[k] - grid[k - 1]) * sc
     bound = 4 * (q / 2) / np.sqrt(seeds)
     assert np.all(np.abs(mean - xd)[ok] <= bound[ok])
+
+
+# ---------------------------------------------------------------- NVFP (Eqs. (4)-(6))
+def test_nvfp_hand_worked_blocks():
+    x = np.zeros((8, 16, 1, 1), dtype=np.float32)
+    x[0:3, 0, 0, 0] = [2688.0, 224.0, -1344.0]
+    x[0:5, 8, 0, 0] = [1.1, 0.5, 0.46875, -0.1, 0.05]
+    codes, scales, t = oracle.nvfp_quantize(x, oracle.NCHW, oracle.ACT, oracle.E2M1, 8, 16, 1, 1)
+    rows = []
+    with open(os.path.join(GOLDEN, "nvfp_blocks.txt")) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                rows.append([p.strip() for p in line.split("|")])
+    assert len(rows) == 2
+    for tv, blk, bcode, ecodes in rows:
+        assert t == float(tv)
+        b = int(blk)
+        # scales [Np/Bn][H][W][Cp/8][Bn/8]: Cp = 32 -> 4 channel blocks, Bn = 8 -> 1 sample block
+        assert scales[b] == int(bcode, 16)
+        want = [int(_parse_num(v)) for v in ecodes.split()]
+        # code position of (channel 8 b, sample j) is (8 b) * 8 + j
+        assert [_code_at(codes, oracle.E2M1, 8 * b * 8 + j) for j in range(len(want))] == want
+    assert scales[2:].tolist() == [0, 0]                  # padded channels 16-31
+
+
+@pytest.mark.parametrize("fmt", ALL_FMTS)
+def test_nvfp_block_scale_cast_matches_torch(fmt):
+    """Eq. (5)'s CastE4M3 of every block against torch's float8 E4M3 cast of
+    the same fp32 ratio (after clamping to the E4M3 maximum)."""
+    n, c, h, w = 32, 64, 3, 2
+    x = _rand_tensor((n, c, h, w), 17, spread=4.0)
+    codes, scales, t = oracle.nvfp_quantize(x, oracle.NCHW, oracle.ACT, fmt, n, c, h, w)
+    tm = np.float32(t) * np.float32(MAXV[fmt])
+    ratios = []
+    for hh in range(h):
+        for ww in range(w):
+            for cb8 in range(c // 8):
+                for sb8 in range(n // 32 * 4):
+                    blk = x[sb8 * 8:(sb8 + 1) * 8, cb8 * 8:(cb8 + 1) * 8, hh, ww]
+                    ratios.append(np.float32(np.abs(blk).max()) / tm)
+    ref = torch.clamp(torch.tensor(np.array(ratios, dtype=np.float32)), max=448.0).to(torch.float8_e4m3fn)
+    # oracle order: [H][W][Cp/8][Bn/8] for one batch group
+    assert scales.tolist() == ref.view(torch.uint8).tolist()
+
+
+@pytest.mark.parametrize("fmt", ALL_FMTS)
+def test_nvfp_invariants(fmt):
+    """Power-of-two equivariance (codes and block scales unchanged, T scaled
+    exactly), source layouts agree, and every dequantized element lies
+    within one element-grid step (times B T) of x."""
+    n, c, h, w = 32, 40, 2, 3
+    x = _rand_tensor((n, c, h, w), 19)
+    codes, scales, t = oracle.nvfp_quantize(x, oracle.NCHW, oracle.ACT, fmt, n, c, h, w)
+    for k in (-7, 5):
+        c2, s2, t2 = oracle.nvfp_quantize(x * np.float32(2.0 ** k), oracle.NCHW, oracle.ACT, fmt, n, c, h, w)
+        assert np.array_equal(c2, codes) and np.array_equal(s2, scales) and t2 == t * 2.0 ** k
+    xt = torch.from_numpy(x)
+    for lay, arr in ((oracle.NHWC, xt.permute(0, 2, 3, 1).contiguous().numpy()),
+                     (oracle.CBF, synth.nchw_to_cbf(xt, 32).numpy())):
+        c3, s3, t3 = oracle.nvfp_quantize(arr, lay, oracle.ACT, fmt, n, c, h, w)
+        assert np.array_equal(c3, codes) and np.array_equal(s3, scales) and t3 == t
+    d = oracle.nvfp_dequant(codes, scales, t, oracle.ACT, fmt, n, c, h, w)
+    grid = np.array([g for _, g in _grid(fmt)])
+    bt = np.zeros_like(d)
+    for hh in range(h):
+        for ww in range(w):
+            for cb8 in range(c // 8 + 1):
+                for sb8 in range(4):
+                    sc = float(oracle.decode(int(scales[((hh * w + ww) * 8 + cb8) * 4 + sb8]), oracle.E4M3))
+                    bt[sb8 * 8:(sb8 + 1) * 8, cb8 * 8:(cb8 + 1) * 8, hh, ww] = sc * t
+    a = np.abs(x.astype(np.float64)) / bt
+    k = np.clip(np.searchsorted(grid, a, side="right"), 1, len(grid) - 1)
+    step = (grid[k] - grid[k - 1]) * bt
+    clip = np.maximum(np.abs(x) - MAXV[fmt] * bt, 0)          # E4M3 rounding of B can clip the block max
+    assert np.all(np.abs(d - x) <= step * (1 + 1e-6) + clip)
+
+
+def test_nvfp_special_tensors():
+    z = np.zeros((32, 32, 1, 2), dtype=np.float32)
+    c, s, t = oracle.nvfp_quantize(z, oracle.NCHW, oracle.ACT, oracle.E2M1, 32, 32, 1, 2)
+    assert t == 0.0 and not c.any() and not s.any()
+    z[3, 4, 0, 1] = float("nan")
+    c, s, t = oracle.nvfp_quantize(z + 1, oracle.NCHW, oracle.ACT, oracle.E2M1, 32, 32, 1, 2)
+    assert math.isnan(t) and not c.any() and set(s.tolist()) == {0x7F}
+    assert oracle.load().o_nvfp_scales_bytes(oracle.ACT, oracle.E2M1, 4, 32, 1, 1) < 0   # Bn = 4: no 8x8 blocks
+    assert oracle.load().o_nvfp_scales_bytes(oracle.ACT, oracle.E2M1, 64, 40, 3, 3) == 2 * 9 * 8 * 4
+
+
+@pytest.mark.parametrize("fmt", [oracle.E2M1, oracle.E2M3, oracle.E3M2])
+def test_nvfp_reduces_error_against_e8m0_blocks(fmt):
+    """Sec. III-A: the two-level NVFP scaling has lower quantization error
+    than power-of-two block scales.  Mean squared error of NVFP (8x8 blocks,
+    E4M3 scales) against the E8M0 32x32-block quantizer, on N(0,1)
+    activations and on heavy-tailed gradients."""
+    n, c, h, w = 32, 64, 8, 8
+    for x in (np.random.default_rng(3).standard_normal((n, c, h, w)).astype(np.float32),
+              _rand_tensor((n, c, h, w), 23, spread=3.0)):
+        cn, sn, t = oracle.nvfp_quantize(x, oracle.NCHW, oracle.ACT, fmt, n, c, h, w)
+        mse_nv = np.mean((oracle.nvfp_dequant(cn, sn, t, oracle.ACT, fmt, n, c, h, w) - x) ** 2)
+        cm, sm = oracle.quantize(x, oracle.NCHW, oracle.ACT, fmt, n, c, h, w)
+        mse_mx = np.mean((oracle.dequant(cm, sm, oracle.ACT, fmt, n, c, h, w) - x) ** 2)
+        assert mse_nv < mse_mx
