@@ -166,6 +166,36 @@ int mxconv_quantize_sr(const void* src, int dtype, int layout, int role, int fmt
                        int n, int c, int h, int w, uint64_t seed,
                        void* codes, uint8_t* scales, void* stream);
 
+/* ------------------------------------------------------------------ f4 */
+/* The paper's own two-level NVFP format, Eqs. (4)-(6) literally (Sec.
+ * III-A, with Sec. IV-B's square blocks of B = 64 = 8 x 8):
+ *   T = amax / (448 * emax_val)            per tensor (Eq. (4)), fp32;
+ *   B = CastE4M3(bmax / (T * emax_val))    per 8-channel x 8-sample block
+ *                                          (weights: 8 Cin x 8 Cout at one
+ *                                          tap), E4M3 to nearest even,
+ *                                          saturating at 448 (Eq. (5));
+ *   code = Round(x / (B * T))              to nearest even, saturating
+ *                                          (Eq. (6));
+ * each step one IEEE fp32 operation (divisions correctly rounded), emax_val
+ * the element format's largest value (448, 6, 7.5 or 28).  T = 0 or B = 0
+ * gives zero codes; a non-finite element makes T NaN, every block scale
+ * 0x7F and every code 0.  Dequantized value: code value x B x T.
+ *   codes    device, mxconv_codes_bytes(role, fmt, ...) bytes, the MX-CBF
+ *            code layout.
+ *   scales   device, mxconv_nvfp_scales_bytes(...) E4M3 bytes in the layout
+ *            [Np/Bn][h][w][Cp/8][Bn/8].
+ *   tscale   device, one float: T.
+ *   workspace device, >= mxconv_nvfp_workspace_bytes() bytes, scratch.
+ * The GPU kernels take CBF activations with batch block 32 or OIHW weights
+ * (layout MXC_NCHW, role MXC_WEIGHT); other sources return MXC_ERR_SHAPE.
+ * Two launches on `stream` (per-workgroup maxima, then the quantization).
+ * Errors: NULL, ARG, SHAPE, WORKSPACE, ALIGN, HIP. */
+size_t mxconv_nvfp_scales_bytes(int role, int fmt, int n, int c, int h, int w);
+size_t mxconv_nvfp_workspace_bytes(void);
+int mxconv_nvfp_quantize(const void* src, int dtype, int layout, int role, int fmt,
+                         int n, int c, int h, int w, void* codes, uint8_t* scales,
+                         float* tscale, void* workspace, size_t ws_bytes, void* stream);
+
 /* ------------------------------------------------------------------ a2 */
 /* Channel-batch-first im2col on MX codes (Sec. IV-A, X'_{Cin,N}): for every
  * output pixel (ho, wo) and tap (kh, kw), the block of the input pixel

@@ -59,6 +59,10 @@ int launch_quantize(const void* src, int dtype, int layout, int role, const Geom
                     void* codes, uint8_t* scales, hipStream_t s, const uint64_t* seed = nullptr);
 int launch_im2col(const Conv& cv, const void* xc, const uint8_t* xs, void* cc, uint8_t* cs,
                   hipStream_t s);
+// NVFP (nvfp.hip): partial maxima in the workspace (NVFP_PARTS words at most)
+constexpr int NVFP_PARTS = 1024;
+int launch_nvfp_quantize(const void* src, int dtype, int layout, int role, const Geom& g, int fmt, void* codes,
+                         uint8_t* scales, float* tscale, void* ws, hipStream_t s);
 int launch_fwd(const Conv& cv, const void* wc, const uint8_t* ws, const void* xc,
                const uint8_t* xs, float* y, int layout, hipStream_t s);
 int launch_dgrad(const Conv& cv, const void* wc, const uint8_t* ws, const void* gc,

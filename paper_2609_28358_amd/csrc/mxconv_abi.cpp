@@ -148,6 +148,34 @@ int mxconv_quantize_sr(const void* src, int dtype, int layout, int role, int fmt
     return launch_quantize(src, dtype, layout, role, g, fmt, codes, scales, (hipStream_t)stream, &seed);
 }
 
+size_t mxconv_nvfp_scales_bytes(int role, int fmt, int n, int c, int h, int w) {
+    Geom g;
+    if (geom_init(&g, role, fmt, n, c, h, w) || g.bn % 8) return 0;
+    return (size_t)g.ng * g.h * g.w * (g.cp / 8) * (g.bn / 8);
+}
+
+size_t mxconv_nvfp_workspace_bytes(void) { return (size_t)NVFP_PARTS * sizeof(uint32_t); }
+
+int mxconv_nvfp_quantize(const void* src, int dtype, int layout, int role, int fmt, int n, int c, int h, int w,
+                         void* codes, uint8_t* scales, float* tscale, void* workspace, size_t ws_bytes,
+                         void* stream) {
+    if (!src || !codes || !scales || !tscale) return MXC_ERR_NULL;
+    if (dtype != MXC_F32 && dtype != MXC_BF16) return MXC_ERR_ARG;
+    if (layout != MXC_NCHW && layout != MXC_NHWC && layout != MXC_CBF) return MXC_ERR_ARG;
+    if (layout == MXC_CBF && role != MXC_ACT) return MXC_ERR_ARG;
+    Geom g;
+    int rc = geom_init(&g, role, fmt, n, c, h, w);
+    if (rc) return rc;
+    // the GPU kernels read CBF activations with batch block 32 and OIHW weights
+    if (!((layout == MXC_CBF && role == MXC_ACT && g.bn == 32) || (layout == MXC_NCHW && role == MXC_WEIGHT)))
+        return MXC_ERR_SHAPE;
+    if (!workspace || ws_bytes < mxconv_nvfp_workspace_bytes()) return MXC_ERR_WORKSPACE;
+    if (!aligned16(src) || !aligned16(codes) || !aligned16(scales) || !aligned16(tscale) || !aligned16(workspace))
+        return MXC_ERR_ALIGN;
+    return launch_nvfp_quantize(src, dtype, layout, role, g, fmt, codes, scales, tscale, workspace,
+                                (hipStream_t)stream);
+}
+
 int mxconv_im2col_cbf(const mxc_conv* p, int fmt, const void* xc, const uint8_t* xs, void* cc,
                       uint8_t* cs, void* stream) {
     if (!p || !xc || !xs || !cc || !cs) return MXC_ERR_NULL;

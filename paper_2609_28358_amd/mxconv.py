@@ -50,6 +50,9 @@ def lib():
         "mxconv_wgrad_workspace_bytes": (sz, [CP, i32]),
         "mxconv_quantize": (i32, [P, i32, i32, i32, i32, i32, i32, i32, i32, P, P, P]),
         "mxconv_quantize_sr": (i32, [P, i32, i32, i32, i32, i32, i32, i32, i32, ctypes.c_uint64, P, P, P]),
+        "mxconv_nvfp_scales_bytes": (sz, [i32] * 6),
+        "mxconv_nvfp_workspace_bytes": (sz, []),
+        "mxconv_nvfp_quantize": (i32, [P, i32, i32, i32, i32, i32, i32, i32, i32, P, P, P, P, sz, P]),
         "mxconv_im2col_cbf": (i32, [CP, i32, P, P, P, P, P]),
         "mxconv_fwd": (i32, [CP, i32, P, P, P, P, P, i32, P]),
         "mxconv_dgrad": (i32, [CP, i32, P, P, P, P, P, i32, P]),
@@ -173,6 +176,35 @@ def quantize_sr(src, role, fmt, seed, layout=NCHW, shape=None, out=None, stream=
         out = MxTensor.empty(role, fmt, shape, src.device)
     _check(lib().mxconv_quantize_sr(_ptr(src), dtype, layout, role, fmt, *shape, int(seed) & (2 ** 64 - 1),
                                     _ptr(out.codes), _ptr(out.scales), _stream(stream)), "mxconv_quantize_sr")
+    return out
+
+
+class NvfpTensor:
+    """A tensor in the two-level NVFP format: codes (MX-CBF layout), E4M3
+    block scales, and the per-tensor scale (a one-element float tensor)."""
+
+    def __init__(self, codes, scales, tscale, role, fmt, shape):
+        self.codes, self.scales, self.tscale = codes, scales, tscale
+        self.role, self.fmt, self.shape = role, fmt, tuple(shape)
+
+
+def nvfp_quantize(src, role, fmt, layout=NCHW, shape=None, workspace=None, stream=None):
+    """Eqs. (4)-(6) on the GPU: CBF activations (batch block 32) or OIHW weights."""
+    dtype, shape = _quant_args(src, layout, shape)
+    L = lib()
+    nb = L.mxconv_codes_bytes(role, fmt, *shape)
+    ns = L.mxconv_nvfp_scales_bytes(role, fmt, *shape)
+    if nb == 0 or ns == 0:
+        raise MxconvError(f"invalid NVFP tensor geometry {shape} role {role} fmt {fmt}")
+    out = NvfpTensor(torch.empty(nb, dtype=torch.uint8, device=src.device),
+                     torch.empty(ns, dtype=torch.uint8, device=src.device),
+                     torch.empty(4, dtype=torch.float32, device=src.device), role, fmt, shape)
+    wsb = L.mxconv_nvfp_workspace_bytes()
+    if workspace is None:
+        workspace = torch.empty(wsb, dtype=torch.uint8, device=src.device)
+    _check(L.mxconv_nvfp_quantize(_ptr(src), dtype, layout, role, fmt, *shape, _ptr(out.codes), _ptr(out.scales),
+                                  _ptr(out.tscale), _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                  _stream(stream)), "mxconv_nvfp_quantize")
     return out
 
 

@@ -242,3 +242,20 @@ def test_quantize_sr_errors():
     assert q(GOOD, 0, 0, 0, 0, 48, 32, 4, 4, 1, GOOD, GOOD, None) == -3
     assert q(GOOD, 0, 0, 0, 3, 2, 32, 4, 4, 1, GOOD, GOOD, None) == -3
     assert q(GOOD, 0, 0, 0, 3, 32, 32, 4, 4, 2 ** 64 - 1, ODD, GOOD, None) == -4
+
+
+def test_nvfp_errors():
+    L = mx.lib()
+    q = L.mxconv_nvfp_quantize   # (src, dtype, layout, role, fmt, n, c, h, w, codes, scales, t, ws, ws_bytes, stream)
+    wsb = L.mxconv_nvfp_workspace_bytes()
+    assert wsb >= 1024 * 4
+    assert L.mxconv_nvfp_scales_bytes(0, 1, 64, 40, 3, 3) == oracle.load().o_nvfp_scales_bytes(0, 1, 64, 40, 3, 3)
+    assert L.mxconv_nvfp_scales_bytes(0, 1, 4, 32, 1, 1) == 0                       # Bn = 4: no 8x8 blocks
+    assert q(None, 0, 2, 0, 1, 32, 32, 4, 4, GOOD, GOOD, GOOD, GOOD, wsb, None) == -1
+    assert q(GOOD, 0, 2, 0, 1, 32, 32, 4, 4, GOOD, GOOD, None, GOOD, wsb, None) == -1
+    assert q(GOOD, 0, 2, 0, 9, 32, 32, 4, 4, GOOD, GOOD, GOOD, GOOD, wsb, None) == -2
+    assert q(GOOD, 0, 1, 0, 1, 32, 32, 4, 4, GOOD, GOOD, GOOD, GOOD, wsb, None) == -3   # NHWC: not on the GPU
+    assert q(GOOD, 0, 2, 0, 1, 16, 32, 4, 4, GOOD, GOOD, GOOD, GOOD, wsb, None) == -3   # batch block 16
+    assert q(GOOD, 0, 2, 0, 1, 32, 32, 4, 4, GOOD, GOOD, GOOD, None, 0, None) == -6
+    assert q(GOOD, 0, 2, 0, 1, 32, 32, 4, 4, GOOD, GOOD, GOOD, GOOD, wsb - 1, None) == -6
+    assert q(GOOD, 0, 2, 0, 1, 32, 32, 4, 4, GOOD, GOOD, ODD, GOOD, wsb, None) == -4
