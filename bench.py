@@ -5,9 +5,10 @@ One step = one pass of the whole path over the layer sweep (batch 32, inputs
 resident in HBM): for each layer
     3x3 s1 p1 64->64 at 56x56,  1x1 64->256 at 56x56,  3x3 s2 p1 128->256 at 28x28
 and each format (MXFP8 E4M3, MXFP4 E2M1): quantize X, W and G_Y once
-(activations arrive channel-batch-first in fp32, weights OIHW fp32), the
-explicit CBF im2col of X, then the forward, input-gradient and
-weight-gradient GEMMs.  Activations are SiLU(N(0,1)), weights Kaiming-normal,
+(activations arrive channel-batch-first in fp32, weights OIHW fp32; X and W,
+the forward operands, in one call and one launch), the explicit CBF im2col
+of X, then the forward, input-gradient and weight-gradient GEMMs: 42
+kernels.  Activations are SiLU(N(0,1)), weights Kaiming-normal,
 gradients N(0, 1e-3), all seeded.
 
 `value` is the conv fwd+bwd GEMM throughput of the whole step: the three
@@ -68,6 +69,7 @@ def layer_numbers(cv, fmt, mx):
     return {
         "quant_x": (0.0, 4.0 * n * ci * cv["h"] * cv["w"] + X),
         "quant_w": (0.0, 4.0 * co * ci * kh * kw + W),
+        "quant_xw": (0.0, 4.0 * n * ci * cv["h"] * cv["w"] + X + 4.0 * co * ci * kh * kw + W),
         "quant_gy": (0.0, 4.0 * n * co * ho * wo + G),
         "im2col": (0.0, X + XC),
         "fwd": (flops, W + X + 4.0 * n * co * ho * wo),
@@ -224,7 +226,7 @@ def naive_leg(jobs, op_ms, mx, synth, dev, stream, reps=3):
         torch.cuda.synchronize()
         ms_naive = e0.elapsed_time(e1) / reps
         nby, nq = naive_numbers(cv, fmt, mx)
-        ours_ops = ("quant_x", "quant_w", "quant_gy", "fwd", "dgrad", "wgrad")
+        ours_ops = ("quant_xw", "quant_gy", "fwd", "dgrad", "wgrad")
         oby = sum(j["nums"][op][1] for op in ours_ops)
         ms_ours = sum(op_ms[(j["name"], op)] for op in ours_ops)
         nx = cv["n"] * cv["cin"] * cv["h"] * cv["w"]
@@ -287,11 +289,15 @@ def main():
             jobs.append(j)
 
     stream = torch.cuda.current_stream()
-    OPS = ("quant_x", "quant_w", "quant_gy", "im2col", "fwd", "dgrad", "wgrad")
+    # a layer's forward operands X and W are quantized together (one launch)
+    OPS = ("quant_xw", "quant_gy", "im2col", "fwd", "dgrad", "wgrad")
 
     def run_op(j, op, src=None):
         cv, fmt = j["cv"], j["fmt"]
-        if op == "quant_x":
+        if op == "quant_xw":
+            mx.quantize_multi([(j["x"] if src is None else src, mx.ACT, fmt, mx.CBF, j["xs"], j["qx"]),
+                               (j["w"], mx.WEIGHT, fmt, mx.NCHW, tuple(j["w"].shape), j["qw"])])
+        elif op == "quant_x":
             mx.quantize(j["x"] if src is None else src, mx.ACT, fmt, layout=mx.CBF, shape=j["xs"], out=j["qx"])
         elif op == "quant_w":
             mx.quantize(j["w"], mx.WEIGHT, fmt, out=j["qw"])
@@ -395,8 +401,8 @@ def main():
     steady = {}
     for j, op in seq:
         srcs = [None]
-        if op in ("quant_x", "quant_gy"):
-            base = j["x"] if op == "quant_x" else j["gy"]
+        if op in ("quant_xw", "quant_x", "quant_gy"):
+            base = j["x"] if op in ("quant_xw", "quant_x") else j["gy"]
             ncopy = min(48, -(-(LLC_BYTES + (64 << 20)) // (base.numel() * base.element_size())))
             srcs = [base] + [base.clone() for _ in range(ncopy - 1)]
         kl = max(12, len(srcs))
@@ -585,7 +591,7 @@ def main():
         "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "mxfp8+mxfp4 (fp32 accumulate)", "data": "synthetic",
         "config": {"workload": "conv layer sweep, batch 32: 3x3 s1 64->64 56x56, 1x1 64->256 56x56, "
-                               "3x3 s2 128->256 28x28; each in MXFP8 and MXFP4; quantize x3 + im2col + fwd + "
+                               "3x3 s2 128->256 28x28; each in MXFP8 and MXFP4; quantize X+W (one launch) + G_Y + im2col + fwd + "
                                "dgrad + wgrad per layer",
                    "global_batch": 32, "layers": [n for n, _ in synth.SWEEP_LAYERS], "formats": ["mxfp8", "mxfp4"],
                    "parallelism": "single GPU"},

@@ -149,6 +149,25 @@ int mxconv_quantize(const void* src, int dtype, int layout, int role, int fmt,
                     int n, int c, int h, int w,
                     void* codes, uint8_t* scales, void* stream);
 
+/* Several quantizations in one call, with mxconv_quantize's rule: a layer's
+ * forward operands (X and W), which become available together, are
+ * quantized once each (Sec. IV-C) in a single launch.  Every job is exactly
+ * an mxconv_quantize call (same arguments, same codes and scales); the jobs
+ * that read a channel-batch-first activation with batch block 32 or OIHW
+ * weights share one launch, any other job gets a launch of its own.  The
+ * jobs' outputs must not overlap.
+ *   count  0 .. MXC_QMULTI_MAX;  jobs  host array of count descriptors.
+ * Errors: as mxconv_quantize (checked for every job before anything is
+ * launched), ARG for a count out of range. */
+#define MXC_QMULTI_MAX 8
+typedef struct mxc_qjob {
+    const void* src;
+    int dtype, layout, role, fmt, n, c, h, w;
+    void* codes;
+    uint8_t* scales;
+} mxc_qjob;
+int mxconv_quantize_multi(int count, const mxc_qjob* jobs, void* stream);
+
 /* Quantize with stochastic rounding of the elements (Eq. (6) allows
  * round-to-nearest or stochastic rounding; Sec. III-A rounds gradients
  * stochastically and activations and weights to nearest).  Same arguments,

@@ -59,6 +59,15 @@ int launch_quantize(const void* src, int dtype, int layout, int role, const Geom
                     void* codes, uint8_t* scales, hipStream_t s, const uint64_t* seed = nullptr);
 int launch_im2col(const Conv& cv, const void* xc, const uint8_t* xs, void* cc, uint8_t* cs,
                   hipStream_t s);
+// several quantizations, one launch for those of the one-wave-per-block kind
+struct QuantJob {
+    const void* src;
+    int dtype, layout, role, fmt;
+    Geom g;
+    void* codes;
+    uint8_t* scales;
+};
+int launch_quantize_multi(int count, const QuantJob* jobs, hipStream_t s);
 // NVFP (nvfp.hip): partial maxima in the workspace (NVFP_PARTS words at most)
 constexpr int NVFP_PARTS = 1024;
 int launch_nvfp_quantize(const void* src, int dtype, int layout, int role, const Geom& g, int fmt, void* codes,

@@ -135,6 +135,25 @@ int mxconv_quantize(const void* src, int dtype, int layout, int role, int fmt, i
     return launch_quantize(src, dtype, layout, role, g, fmt, codes, scales, (hipStream_t)stream);
 }
 
+int mxconv_quantize_multi(int count, const mxc_qjob* jobs, void* stream) {
+    if (count < 0 || count > MXC_QMULTI_MAX) return MXC_ERR_ARG;
+    if (count > 0 && !jobs) return MXC_ERR_NULL;
+    QuantJob q[MXC_QMULTI_MAX];
+    for (int i = 0; i < count; i++) {
+        const mxc_qjob& j = jobs[i];
+        if (!j.src || !j.codes || !j.scales) return MXC_ERR_NULL;
+        if (j.dtype != MXC_F32 && j.dtype != MXC_BF16) return MXC_ERR_ARG;
+        if (j.layout != MXC_NCHW && j.layout != MXC_NHWC && j.layout != MXC_CBF) return MXC_ERR_ARG;
+        if (j.layout == MXC_CBF && j.role != MXC_ACT) return MXC_ERR_ARG;
+        const int rc = geom_init(&q[i].g, j.role, j.fmt, j.n, j.c, j.h, j.w);
+        if (rc) return rc;
+        if (!aligned16(j.src) || !aligned16(j.codes) || !aligned16(j.scales)) return MXC_ERR_ALIGN;
+        q[i].src = j.src; q[i].dtype = j.dtype; q[i].layout = j.layout; q[i].role = j.role; q[i].fmt = j.fmt;
+        q[i].codes = j.codes; q[i].scales = j.scales;
+    }
+    return launch_quantize_multi(count, q, (hipStream_t)stream);
+}
+
 int mxconv_quantize_sr(const void* src, int dtype, int layout, int role, int fmt, int n, int c,
                        int h, int w, uint64_t seed, void* codes, uint8_t* scales, void* stream) {
     if (!src || !codes || !scales) return MXC_ERR_NULL;

@@ -348,13 +348,9 @@ __device__ __forceinline__ void quantize_block16(const void* __restrict__ src, c
 }
 
 template <int SRC, int DTYPE, int FMT, bool SR>
-__global__ __launch_bounds__(QT) void quantize_block_kernel(const void* __restrict__ src, Geom g,
-                                                            uint8_t* __restrict__ codes,
-                                                            uint8_t* __restrict__ scales, int nblocks,
-                                                            uint32_t k0, uint32_t k1) {
-    const int lane = threadIdx.x & 63;
-    const int blk = blockIdx.x * (QT / 64) + (threadIdx.x >> 6);
-    if (blk >= nblocks) return;
+__device__ __forceinline__ void quantize_block_body(const void* __restrict__ src, const Geom& g,
+                                                    uint8_t* __restrict__ codes, uint8_t* __restrict__ scales,
+                                                    int blk, int lane, uint32_t k0, uint32_t k1) {
     if constexpr (SR || fmt_bits(FMT) == 6) {
         quantize_block16<SRC, DTYPE, FMT, SR>(src, g, codes, scales, blk, lane, k0, k1);
         return;
@@ -416,6 +412,68 @@ __global__ __launch_bounds__(QT) void quantize_block_kernel(const void* __restri
 #pragma unroll
         for (int q = 0; q < 4; q++) d[64 * q] = bad ? (unsigned short)0 : pack4_e2m1(x[q], inv);
     }
+}
+
+template <int SRC, int DTYPE, int FMT, bool SR>
+__global__ __launch_bounds__(QT) void quantize_block_kernel(const void* __restrict__ src, Geom g,
+                                                            uint8_t* __restrict__ codes,
+                                                            uint8_t* __restrict__ scales, int nblocks,
+                                                            uint32_t k0, uint32_t k1) {
+    const int blk = blockIdx.x * (QT / 64) + (threadIdx.x >> 6);
+    if (blk >= nblocks) return;
+    quantize_block_body<SRC, DTYPE, FMT, SR>(src, g, codes, scales, blk, threadIdx.x & 63, k0, k1);
+}
+
+// Several tensors of the one-wave-per-block kind (CBF activations with
+// Bn = 32, OIHW weights) in one launch: the waves of job i take blocks
+// [blk0_i, blk0_i + nblocks_i).  Each tensor keeps its own source kind,
+// source type and element format; the wave picks the job and the kernel
+// body by a uniform branch.
+struct QJob {
+    const void* src;
+    uint8_t* codes;
+    uint8_t* scales;
+    Geom g;
+    int kind, dtype, fmt;          // kind 0: CBF activation, 1: OIHW weights
+    int blk0, nblocks;
+};
+constexpr int QMULTI_MAX = 8;
+struct QMulti {
+    QJob j[QMULTI_MAX];
+    int count, nblocks;
+};
+
+template <int SRC>
+__device__ __forceinline__ void qmulti_dispatch(const QJob& q, int blk, int lane) {
+#define QM_CASE(D, F) quantize_block_body<SRC, D, F, false>(q.src, q.g, q.codes, q.scales, blk, lane, 0u, 0u)
+    if (q.dtype == MXC_F32) {
+        switch (q.fmt) {
+            case MXC_E4M3: QM_CASE(MXC_F32, MXC_E4M3); break;
+            case MXC_E2M3: QM_CASE(MXC_F32, MXC_E2M3); break;
+            case MXC_E3M2: QM_CASE(MXC_F32, MXC_E3M2); break;
+            default:       QM_CASE(MXC_F32, MXC_E2M1); break;
+        }
+    } else {
+        switch (q.fmt) {
+            case MXC_E4M3: QM_CASE(MXC_BF16, MXC_E4M3); break;
+            case MXC_E2M3: QM_CASE(MXC_BF16, MXC_E2M3); break;
+            case MXC_E3M2: QM_CASE(MXC_BF16, MXC_E3M2); break;
+            default:       QM_CASE(MXC_BF16, MXC_E2M1); break;
+        }
+    }
+#undef QM_CASE
+}
+
+__global__ __launch_bounds__(QT) void quantize_multi_kernel(QMulti m) {
+    // the wave's block index is uniform: keep it (and the job choice) scalar
+    const int blk = __builtin_amdgcn_readfirstlane(blockIdx.x * (QT / 64) + (threadIdx.x >> 6));
+    if (blk >= m.nblocks) return;
+    QJob q = m.j[0];
+#pragma unroll
+    for (int t = 1; t < QMULTI_MAX; t++)
+        if (t < m.count && blk >= m.j[t].blk0) q = m.j[t];
+    if (q.kind == 0) qmulti_dispatch<0>(q, blk - q.blk0, threadIdx.x & 63);
+    else             qmulti_dispatch<1>(q, blk - q.blk0, threadIdx.x & 63);
 }
 
 template <int SRC, int DTYPE, int FMT, bool SR>
@@ -489,6 +547,35 @@ int launch_q_dt(const void* src, int dtype, const Geom& g, int fmt, bool sr, voi
 }
 
 }  // namespace
+
+int launch_quantize_multi(int count, const QuantJob* jobs, hipStream_t s) {
+    QMulti m;
+    int nq = 0;
+    long long nb = 0;
+    for (int i = 0; i < count; i++) {
+        const QuantJob& q = jobs[i];
+        const bool block = (q.layout == MXC_CBF && q.role == MXC_ACT && q.g.bn == 32) ||
+                           (q.layout == MXC_NCHW && q.role == MXC_WEIGHT);
+        const long long qb = (long long)q.g.ng * q.g.h * q.g.w * q.g.ncb;
+        if (!block || nq == QMULTI_MAX || nb + qb > 0x7FFFFFFFLL - 4) {
+            // a tensor of another kind: its own launch
+            const int rc = launch_quantize(q.src, q.dtype, q.layout, q.role, q.g, q.fmt, q.codes, q.scales, s);
+            if (rc) return rc;
+            continue;
+        }
+        QJob& d = m.j[nq++];
+        d.src = q.src; d.codes = (uint8_t*)q.codes; d.scales = q.scales; d.g = q.g;
+        d.kind = q.role == MXC_WEIGHT ? 1 : 0; d.dtype = q.dtype; d.fmt = q.fmt;
+        d.blk0 = (int)nb; d.nblocks = (int)qb;
+        nb += qb;
+    }
+    if (nq == 0) return MXC_OK;
+    m.count = nq;
+    m.nblocks = (int)nb;
+    for (int i = nq; i < QMULTI_MAX; i++) m.j[i] = m.j[nq - 1];
+    hipLaunchKernelGGL(quantize_multi_kernel, dim3((unsigned)((nb + 3) / 4)), dim3(QT), 0, s, m);
+    return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
+}
 
 int launch_quantize(const void* src, int dtype, int layout, int role, const Geom& g, int fmt, void* codes,
                     uint8_t* scales, hipStream_t s, const uint64_t* seed) {

@@ -25,6 +25,16 @@ class MxconvError(RuntimeError):
     pass
 
 
+class MxcQJob(ctypes.Structure):
+    _fields_ = [("src", ctypes.c_void_p)] + [(k, ctypes.c_int32) for k in
+                                           ("dtype", "layout", "role", "fmt", "n", "c", "h", "w")] + \
+               [("codes", ctypes.c_void_p), ("scales", ctypes.c_void_p)]
+
+
+QMULTI_MAX = 8
+FP6_SLACK = 16          # bytes of read slack at the end of an FP6 code buffer
+
+
 class MxcConv(ctypes.Structure):
     _fields_ = [(k, ctypes.c_int32) for k in
                 ("n", "cin", "cout", "h", "w", "kh", "kw", "sh", "sw", "ph", "pw")]
@@ -49,6 +59,7 @@ def lib():
         "mxconv_im2col_scales_bytes": (sz, [CP, i32]),
         "mxconv_wgrad_workspace_bytes": (sz, [CP, i32]),
         "mxconv_quantize": (i32, [P, i32, i32, i32, i32, i32, i32, i32, i32, P, P, P]),
+        "mxconv_quantize_multi": (i32, [i32, ctypes.POINTER(MxcQJob), P]),
         "mxconv_quantize_sr": (i32, [P, i32, i32, i32, i32, i32, i32, i32, i32, ctypes.c_uint64, P, P, P]),
         "mxconv_nvfp_scales_bytes": (sz, [i32] * 6),
         "mxconv_nvfp_workspace_bytes": (sz, []),
@@ -137,8 +148,10 @@ class MxTensor:
         ns = scales_bytes(role, fmt, n, c, h, w)
         if nb == 0:
             raise MxconvError(f"invalid MX tensor geometry {shape} role {role} fmt {fmt}")
-        return MxTensor(torch.empty(nb, dtype=torch.uint8, device=device),
-                        torch.empty(ns, dtype=torch.uint8, device=device), role, fmt, shape)
+        codes = torch.empty(nb, dtype=torch.uint8, device=device)
+        if fmt in (E2M3, E3M2):
+            codes[-FP6_SLACK:].zero_()     # read slack, never written by the library: keep it defined
+        return MxTensor(codes, torch.empty(ns, dtype=torch.uint8, device=device), role, fmt, shape)
 
 
 def _quant_args(src, layout, shape):
@@ -167,6 +180,25 @@ def quantize(src, role, fmt, layout=NCHW, shape=None, out=None, stream=None):
     _check(lib().mxconv_quantize(_ptr(src), dtype, layout, role, fmt, *shape,
                                  _ptr(out.codes), _ptr(out.scales), _stream(stream)), "mxconv_quantize")
     return out
+
+
+def quantize_multi(items, stream=None):
+    """Several quantize() calls in one library call (one launch for the CBF
+    batch-block-32 activations and OIHW weights among them).  items: tuples
+    (src, role, fmt, layout, shape, out); returns the MX tensors."""
+    if len(items) > QMULTI_MAX:
+        raise MxconvError(f"at most {QMULTI_MAX} tensors per call")
+    jobs = (MxcQJob * max(1, len(items)))()
+    outs = []
+    for k, (src, role, fmt, layout, shape, out) in enumerate(items):
+        dtype, shape = _quant_args(src, layout, shape)
+        if out is None:
+            out = MxTensor.empty(role, fmt, shape, src.device)
+        jobs[k] = MxcQJob(src.data_ptr(), dtype, layout, role, fmt, *shape, out.codes.data_ptr(),
+                          out.scales.data_ptr())
+        outs.append(out)
+    _check(lib().mxconv_quantize_multi(len(items), jobs, _stream(stream)), "mxconv_quantize_multi")
+    return outs
 
 
 def quantize_sr(src, role, fmt, seed, layout=NCHW, shape=None, out=None, stream=None):

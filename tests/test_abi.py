@@ -259,3 +259,26 @@ def test_nvfp_errors():
     assert q(GOOD, 0, 2, 0, 1, 32, 32, 4, 4, GOOD, GOOD, GOOD, None, 0, None) == -6
     assert q(GOOD, 0, 2, 0, 1, 32, 32, 4, 4, GOOD, GOOD, GOOD, GOOD, wsb - 1, None) == -6
     assert q(GOOD, 0, 2, 0, 1, 32, 32, 4, 4, GOOD, GOOD, ODD, GOOD, wsb, None) == -4
+
+
+def test_quantize_multi_errors():
+    L = mx.lib()
+    J = mx.MxcQJob
+
+    def job(src=0x10000, dtype=0, layout=2, role=0, fmt=0, n=32, c=32, h=4, w=4, codes=0x10000, scales=0x10000):
+        return J(src, dtype, layout, role, fmt, n, c, h, w, codes, scales)
+
+    def call(*jobs):
+        arr = (J * max(1, len(jobs)))(*jobs)
+        return L.mxconv_quantize_multi(len(jobs), arr, None)
+
+    assert L.mxconv_quantize_multi(9, None, None) == -2
+    assert L.mxconv_quantize_multi(-1, None, None) == -2
+    assert L.mxconv_quantize_multi(2, None, None) == -1
+    assert L.mxconv_quantize_multi(0, None, None) == 0                  # nothing to do
+    # every job is validated before anything is launched
+    assert call(job(), job(src=0)) == -1
+    assert call(job(), job(fmt=7)) == -2
+    assert call(job(), job(layout=2, role=1)) == -2                     # CBF weights
+    assert call(job(), job(n=48)) == -3
+    assert call(job(), job(codes=0x10001)) == -4
