@@ -215,6 +215,33 @@ int mxconv_nvfp_quantize(const void* src, int dtype, int layout, int role, int f
                          int n, int c, int h, int w, void* codes, uint8_t* scales,
                          float* tscale, void* workspace, size_t ws_bytes, void* stream);
 
+/* The three GEMMs on NVFP4 operands (E2M1 codes with E4M3 8x8 block scales
+ * and per-tensor scales, as mxconv_nvfp_quantize writes them): Y = W * X,
+ * G_X = W^T * G_Y, G_W = G_Y * X^T (Eqs. (1)-(3)) of the fake-quantized
+ * tensors code x B x T.  The block-scaled matrix cores take only E8M0 scales
+ * per 32 elements, so the kernels decode each fragment to fp16 (code x B is
+ * exact in fp16), run fp16 MFMAs with fp32 accumulation and multiply the
+ * result by the two per-tensor scales.  Arguments as mxconv_fwd / dgrad /
+ * wgrad, with each operand's E4M3 block scales (mxconv_nvfp_scales_bytes)
+ * and its per-tensor scale (w_t, x_t, gy_t: device floats).  fmt must be
+ * MXC_E2M1 (NVFP4); layers outside the batch-block-32 kernels (kernel width
+ * 1 or 3, forward column stride 1 or 2, input-gradient stride 1x1 or 2x2)
+ * return MXC_ERR_SHAPE.  The weight gradient uses the workspace of
+ * mxconv_wgrad_workspace_bytes(cv, MXC_E2M1).
+ * Errors: NULL, ARG, SHAPE, ALIGN, WORKSPACE, HIP. */
+int mxconv_nvfp_fwd(const mxc_conv* cv, int fmt,
+                    const void* w_codes, const uint8_t* w_scales, const float* w_t,
+                    const void* x_codes, const uint8_t* x_scales, const float* x_t,
+                    float* y, int y_layout, void* stream);
+int mxconv_nvfp_dgrad(const mxc_conv* cv, int fmt,
+                      const void* w_codes, const uint8_t* w_scales, const float* w_t,
+                      const void* gy_codes, const uint8_t* gy_scales, const float* gy_t,
+                      float* gx, int gx_layout, void* stream);
+int mxconv_nvfp_wgrad(const mxc_conv* cv, int fmt,
+                      const void* gy_codes, const uint8_t* gy_scales, const float* gy_t,
+                      const void* x_codes, const uint8_t* x_scales, const float* x_t,
+                      float* gw, void* workspace, size_t ws_bytes, void* stream);
+
 /* ------------------------------------------------------------------ a2 */
 /* Channel-batch-first im2col on MX codes (Sec. IV-A, X'_{Cin,N}): for every
  * output pixel (ho, wo) and tap (kh, kw), the block of the input pixel

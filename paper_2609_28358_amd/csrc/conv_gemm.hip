@@ -1303,10 +1303,11 @@ size_t wgrad_workspace(const Conv& cv) {
 }
 
 int launch_wgrad(const Conv& cv, const void* gc, const uint8_t* gs, const void* xc, const uint8_t* xs,
-                 float* gw, void* ws, hipStream_t s) {
+                 float* gw, void* ws, hipStream_t s, const float* nv_tg, const float* nv_tx) {
     const int ls = wgrad_lean_splits(cv);
+    if (nv_tg && ls == 0) return MXC_ERR_SHAPE;
     if (ls > 0) {
-        const int rc = launch_wgrad_lean(cv, gc, gs, xc, xs, ls > 1 ? (float*)ws : gw, ls, s);
+        const int rc = launch_wgrad_lean(cv, gc, gs, xc, xs, ls > 1 ? (float*)ws : gw, ls, s, nv_tg, nv_tx);
         if (rc || ls == 1) return rc;
         const long cols = (long)cv.cout * cv.kh * cv.kw * cv.x.cp;
         hipLaunchKernelGGL(wgrad_reduce, dim3((unsigned)((cols + 63) / 64)), dim3(256), 0, s,

@@ -95,6 +95,11 @@ struct LeanArgs {
     uint8_t* qscales;
     int qfmt, q_ncb, fn;
     const float* zpre;
+    // NVFP4 operands (the NV kernels): per-tensor scales of W and the source;
+    // the scale arrays ws / ss then hold E4M3 scales per 8x8 block, the 16 of
+    // one 32-row block in 16 consecutive bytes
+    const float* tw;
+    const float* tx;
 };
 
 // Taps and output pixel grid of one phase; the stride-1 kernels use the
@@ -128,8 +133,14 @@ template <int F> struct LdsBlock {
     static constexpr int STEP = fmt_bits(F) == 6 ? 12 : 16;      // source bytes between lanes
 };
 
-template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW>
+// NV: NVFP4 operands (both E2M1 codes with E4M3 8x8 block scales and a
+// per-tensor scale, Eqs. (4)-(6)): a stage also carries the 16 block scales of
+// each 32-row block it holds (4 KB of scale entries instead of 1 KB), the
+// fragments are decoded to fp16 and multiplied on fp16 MFMAs, and the result
+// is multiplied by the two per-tensor scales.
+template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW, bool NV = false>
 __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phase& f) {
+    static_assert(!NV || (FW == MXC_E2M1 && FX == MXC_E2M1), "NVFP4 operands only");
     typedef LdsBlock<FW> BW;
     typedef LdsBlock<FX> BX;
     constexpr int TBW = BW::TBG, TBX = BX::TBG;     // stored block bytes (weights, activations)
@@ -259,7 +270,10 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
         const uint32_t o = isb ? s_off + ((uint32_t)g * p.hsrc + (row_ok ? sy : 0)) * p.wsrc * p.x_ncb + 2 * kk
                                : s_off + (uint32_t)kh * p.kwf * p.w_ncb +
                                      (DG ? (uint32_t)(2 * kk) * p.kh * p.kwf * p.w_ncb : (uint32_t)(2 * kk));
-        dma1_async(ok ? (isb ? ssp : wsp) + o : zero, lds_addr(lds + NQ * 4096 + wave * 256));
+        if constexpr (NV)   // the 16 block scales of the 32-row block: 16 bytes per entry
+            dma16_async(ok ? (isb ? ssp : wsp) + 16 * o : zero, lds_addr(lds + NQ * 4096 + wave * 1024));
+        else
+            dma1_async(ok ? (isb ? ssp : wsp) + o : zero, lds_addr(lds + NQ * 4096 + wave * 256));
     };
 
     // ---- wave geometry and per-lane fragment offsets
@@ -300,6 +314,7 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
         // fragments of the wave's ND halo pixels (both K halves)
         v8i bf[ND];
         int sb[ND];
+        uint32_t bfd[NV ? ND : 1][16];          // NV: decoded to fp16
 #pragma unroll
         for (int d = 0; d < ND; d++) {
             const int hc = hbase + d;
@@ -331,6 +346,14 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                 bf[d][4] = bf[d][5] = bf[d][6] = bf[d][7] = 0;
             }
             sb[d] = SC[4 * (NSA + h * HP + hc)];
+            if constexpr (NV) {
+                // scales of (channel group o, this lane's sample group): byte 4 o + (lane % 32) / 8
+                const uint4 u = *(const uint4*)(SC + 16 * (NSA + h * HP + hc));
+                const int sh = 8 * ((lane & 31) >> 3);
+                const uint32_t s4 = ((u.x >> sh) & 0xFFu) | ((u.y >> sh) & 0xFFu) << 8 |
+                                    ((u.z >> sh) & 0xFFu) << 16 | ((u.w >> sh) & 0xFFu) << 24;
+                nv_decode32(bf[d], s4, bfd[d]);
+            }
         }
 #pragma unroll
         for (int t = 0; t < KW; t++) {
@@ -389,12 +412,32 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                 }
                 sa[rb] = SC[4 * ((t * 2 + h) * RBW + rbi)];
             }
+            uint32_t afd[NV ? 2 : 1][16];
+            if constexpr (NV) {
+#pragma unroll
+                for (int rb = 0; rb < 2; rb++) {
+                    const int rbi = 2 * wm + rb;
+                    const uint4 u = *(const uint4*)(SC + 16 * ((t * 2 + h) * RBW + rbi));
+                    uint32_t s4;
+                    if (DG) {   // rows = input channels: the lane's channel group row, K groups o
+                        const int q8 = (lane & 31) >> 3;
+                        s4 = q8 == 0 ? u.x : q8 == 1 ? u.y : q8 == 2 ? u.z : u.w;
+                    } else {    // columns = output channels: byte 4 o + (lane % 32) / 8
+                        const int sh = 8 * ((lane & 31) >> 3);
+                        s4 = ((u.x >> sh) & 0xFFu) | ((u.y >> sh) & 0xFFu) << 8 |
+                             ((u.z >> sh) & 0xFFu) << 16 | ((u.w >> sh) & 0xFFu) << 24;
+                    }
+                    nv_decode32(af[rb], s4, afd[rb]);
+                }
+            }
 #pragma unroll
             for (int cn = 0; cn < PW; cn++) {
                 const int d = DG ? cn + (KW - 1 - t) : cn * CS + t;
 #pragma unroll
-                for (int rb = 0; rb < 2; rb++)   // transposed product: rows = samples, columns = channels
-                    acc[rb][cn] = mfma_mx<FX, FW>(bf[d], af[rb], acc[rb][cn], sb[d], sa[rb]);
+                for (int rb = 0; rb < 2; rb++) {  // transposed product: rows = samples, columns = channels
+                    if constexpr (NV) acc[rb][cn] = mfma_nv(bfd[d], afd[rb], acc[rb][cn]);
+                    else acc[rb][cn] = mfma_mx<FX, FW>(bf[d], af[rb], acc[rb][cn], sb[d], sa[rb]);
+                }
             }
         }
     }
@@ -406,6 +449,15 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
     // contiguous 4 KB run, so each wave passes them through 4 KB of LDS
     // (16-byte chunks XOR-swizzled by row against bank conflicts) and writes
     // them back as four fully contiguous 1 KB stores.
+    if constexpr (NV) {   // Eq. (6)'s fake-quantized operands carry T_W T_X
+        const float tt = *p.tw * *p.tx;
+#pragma unroll
+        for (int rb = 0; rb < 2; rb++)
+#pragma unroll
+            for (int cn = 0; cn < PW; cn++)
+#pragma unroll
+                for (int e = 0; e < 16; e++) acc[rb][cn][e] *= tt;
+    }
     const int m = mt * 64 * WGM + 64 * wm + (lane & 31);
     if (p.layout == MXC_CBF && !p.qcodes) __syncthreads();   // every wave is done with the stage buffers
     uint8_t* const ep = smem + wave * 4096;
@@ -551,7 +603,7 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
     }
 }
 
-template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW>
+template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW, bool NV = false>
 __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
     // XCD-aware order: consecutive tiles (same output row) on one XCD
     const int per_xcd = (gridDim.x + 7) / 8;
@@ -560,12 +612,12 @@ __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
     Phase f;
     f.ry = 0; f.rx = 0; f.kh0 = 0; f.nvh = p.kh; f.kw0 = 0;
     f.gh = p.hout; f.gw = p.wout; f.c0 = p.pw; f.r0 = p.ph;
-    lean_tile<FW, FX, DG, KW, S, WGM, PW>(p, lin, f);
+    lean_tile<FW, FX, DG, KW, S, WGM, PW, NV>(p, lin, f);
 }
 
 // Stride-2 input gradient for kernel width KWF (1 or 3): the four phases in
 // one launch, tiles of phase (ry, rx) at [pofs[2 ry + rx], pofs[2 ry + rx + 1]).
-template <int FW, int FX, int KWF, int WGM, int PW>
+template <int FW, int FX, int KWF, int WGM, int PW, bool NV = false>
 __global__ __launch_bounds__(LT) void conv_lean_dg2_kernel(LeanArgs p) {
     const int per_xcd = (gridDim.x + 7) / 8;
     int lin = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
@@ -582,8 +634,8 @@ __global__ __launch_bounds__(LT) void conv_lean_dg2_kernel(LeanArgs p) {
     if (nvw == 0) f.nvh = 0;                       // no tap reaches the phase: its pixels are zero
     f.gh = (p.hout - f.ry + 1) / 2; f.gw = (p.wout - f.rx + 1) / 2;
     f.c0 = (f.rx + p.pw - f.kw0) / 2; f.r0 = (f.ry + p.ph - f.kh0) / 2;
-    if (KWF == 3 && nvw == 2) lean_tile<FW, FX, true, 2, 2, WGM, PW>(p, lin, f);
-    else                      lean_tile<FW, FX, true, 1, 2, WGM, PW>(p, lin, f);
+    if (KWF == 3 && nvw == 2) lean_tile<FW, FX, true, 2, 2, WGM, PW, NV>(p, lin, f);
+    else                      lean_tile<FW, FX, true, 1, 2, WGM, PW, NV>(p, lin, f);
 }
 
 // LDS bytes of one launch: the stage ring, and at least the 4 x 4 KB the
@@ -606,44 +658,46 @@ int lean_launch(K kernel, bool& attr, const LeanArgs& a, int ntiles, size_t lds,
     return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
 }
 
-template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW>
+template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW, bool NV = false>
 int launch_lean_t(const LeanArgs& a, int nbufs_used, hipStream_t s) {
     static bool attr = false;
-    return lean_launch(conv_lean_kernel<FW, FX, DG, KW, S, WGM, PW>, attr, a, a.ntiles, lean_lds(a, nbufs_used), s);
+    return lean_launch(conv_lean_kernel<FW, FX, DG, KW, S, WGM, PW, NV>, attr, a, a.ntiles, lean_lds(a, nbufs_used), s);
 }
 
-template <int FW, int FX, int KWF, int PW>
+template <int FW, int FX, int KWF, int PW, bool NV = false>
 int launch_lean_dg2(const LeanArgs& a, int nbufs_used, hipStream_t s) {
     static bool attr = false;
-    return lean_launch(conv_lean_dg2_kernel<FW, FX, KWF, 1, PW>, attr, a, a.pofs[4], lean_lds(a, nbufs_used), s);
+    return lean_launch(conv_lean_dg2_kernel<FW, FX, KWF, 1, PW, NV>, attr, a, a.pofs[4], lean_lds(a, nbufs_used), s);
 }
 
-// (WGM, PW) in use: (1, 1), (1, 2), (2, 2), (4, 2)
-template <int FW, int FX, bool DG, int KW, int S>
+// (WGM, PW) in use: (1, 1), (1, 2), (2, 2), (4, 2); the NV kernels run (1, 1)
+template <int FW, int FX, bool DG, int KW, int S, bool NV = false>
 int launch_lean_w(const LeanArgs& a, int wgm, int pw, int nb, hipStream_t s) {
+    if constexpr (NV) return launch_lean_t<FW, FX, DG, KW, S, 1, 1, true>(a, nb, s);
     if (wgm == 4) return launch_lean_t<FW, FX, DG, KW, S, 4, 2>(a, nb, s);
     if (wgm == 2) return launch_lean_t<FW, FX, DG, KW, S, 2, 2>(a, nb, s);
     return pw == 1 ? launch_lean_t<FW, FX, DG, KW, S, 1, 1>(a, nb, s) : launch_lean_t<FW, FX, DG, KW, S, 1, 2>(a, nb, s);
 }
 
-template <int FW, int FX, bool DG>
+template <int FW, int FX, bool DG, bool NV = false>
 int launch_lean_f(const LeanArgs& a, int kw, int sw, int wgm, int pw, int nb, hipStream_t s) {
     if constexpr (DG) {
         if (sw == 2) {
+            if constexpr (NV) return kw == 3 ? launch_lean_dg2<FW, FX, 3, 1, true>(a, nb, s) : launch_lean_dg2<FW, FX, 1, 1, true>(a, nb, s);
             if (kw == 3) return pw == 1 ? launch_lean_dg2<FW, FX, 3, 1>(a, nb, s) : launch_lean_dg2<FW, FX, 3, 2>(a, nb, s);
             return pw == 1 ? launch_lean_dg2<FW, FX, 1, 1>(a, nb, s) : launch_lean_dg2<FW, FX, 1, 2>(a, nb, s);
         }
-        return kw == 3 ? launch_lean_w<FW, FX, DG, 3, 1>(a, wgm, pw, nb, s) : launch_lean_w<FW, FX, DG, 1, 1>(a, wgm, pw, nb, s);
+        return kw == 3 ? launch_lean_w<FW, FX, DG, 3, 1, NV>(a, wgm, pw, nb, s) : launch_lean_w<FW, FX, DG, 1, 1, NV>(a, wgm, pw, nb, s);
     } else {
-        if (kw == 3) return sw == 2 ? launch_lean_w<FW, FX, DG, 3, 2>(a, wgm, pw, nb, s)
-                                    : launch_lean_w<FW, FX, DG, 3, 1>(a, wgm, pw, nb, s);
-        return sw == 2 ? launch_lean_w<FW, FX, DG, 1, 2>(a, wgm, pw, nb, s) : launch_lean_w<FW, FX, DG, 1, 1>(a, wgm, pw, nb, s);
+        if (kw == 3) return sw == 2 ? launch_lean_w<FW, FX, DG, 3, 2, NV>(a, wgm, pw, nb, s)
+                                    : launch_lean_w<FW, FX, DG, 3, 1, NV>(a, wgm, pw, nb, s);
+        return sw == 2 ? launch_lean_w<FW, FX, DG, 1, 2, NV>(a, wgm, pw, nb, s) : launch_lean_w<FW, FX, DG, 1, 1, NV>(a, wgm, pw, nb, s);
     }
 }
 
-template <int FW, int FX>
+template <int FW, int FX, bool NV = false>
 int launch_lean_dir(const LeanArgs& a, bool dg, int kw, int sw, int wgm, int pw, int nb, hipStream_t s) {
-    return dg ? launch_lean_f<FW, FX, true>(a, kw, sw, wgm, pw, nb, s) : launch_lean_f<FW, FX, false>(a, kw, sw, wgm, pw, nb, s);
+    return dg ? launch_lean_f<FW, FX, true, NV>(a, kw, sw, wgm, pw, nb, s) : launch_lean_f<FW, FX, false, NV>(a, kw, sw, wgm, pw, nb, s);
 }
 
 }  // namespace
@@ -651,7 +705,10 @@ int launch_lean_dir(const LeanArgs& a, bool dg, int kw, int sw, int wgm, int pw,
 // Returns 1 when the layer is outside this kernel's shapes (the caller then
 // uses the general kernels), else an MXC_* code.
 int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const void* sc,
-                     const uint8_t* ss, float* out, int layout, hipStream_t s, const FusedEpi* q) {
+                     const uint8_t* ss, float* out, int layout, hipStream_t s, const FusedEpi* q,
+                     const float* nv_tw, const float* nv_tx) {
+    const bool nv = nv_tw != nullptr;
+    if (nv && (q || cv.fa != MXC_E2M1 || cv.fb != MXC_E2M1)) return MXC_ERR_ARG;
     if (cv.x.bn != 32) return 1;
     if (cv.kw != 1 && cv.kw != 3) return 1;
     // input gradient: stride 1, or 2 in both directions (phases); forward:
@@ -668,6 +725,7 @@ int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws,
     a.q_ncb = (a.M + 31) / 32;
     a.fn = q ? q->fn : MXC_FN_NONE;
     a.zpre = q ? q->z : nullptr;
+    a.tw = nv_tw; a.tx = nv_tx;
     const Geom& src = dg ? cv.gy : cv.x;
     a.hsrc = src.h; a.wsrc = src.w;
     a.hout = dg ? cv.h : cv.ho;
@@ -703,7 +761,7 @@ int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws,
     // pixel per wave instead: twice the workgroups, more waves streaming
     // operands and storing results at once (measured: faster below ~200
     // tiles, slower from ~400)
-    if (count(wgm, pw, false) < 192) { wgm = 1; pw = 1; }
+    if (count(wgm, pw, false) < 192 || nv) { wgm = 1; pw = 1; }
     const int px = pw * 4 / wgm;
     a.mtiles = (a.M + 64 * wgm - 1) / (64 * wgm);
     for (int i = 0; i < 5; i++) a.pofs[i] = 0;
@@ -719,7 +777,7 @@ int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws,
     const int hp = dg ? px + kwt - 1 : (px - 1) * cv.sw + cv.kw;
     const int na = kwt * 2 * 2 * wgm, nb = 2 * hp;
     const int nq = (na / bpiw + nb / bpix + 3) / 4;
-    a.stage_bytes = nq * 4096 + SCALE_REGION;
+    a.stage_bytes = nq * 4096 + (nv ? 4096 : SCALE_REGION);
     const int nstage = (dg2 ? (cv.kh + 1) / 2 : cv.kh) * ((a.kcb + 1) / 2);
     if (2 * a.stage_bytes > LDS_MAX || nstage < 1) return 1;
     // ring depth: the workgroups that share a CU at this grid size split its
@@ -730,6 +788,7 @@ int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws,
         if ((long)per_cu * b * a.stage_bytes <= LDS_MAX) { nbuf = b; break; }
     a.nbuf = nbuf;
     const int used = nbuf < nstage ? nbuf : nstage;
+    if (nv) return launch_lean_dir<MXC_E2M1, MXC_E2M1, true>(a, dg, cv.kw, cv.sw, wgm, pw, used, s);
     if (cv.fa == MXC_E4M3 && cv.fb == MXC_E4M3)
         return launch_lean_dir<MXC_E4M3, MXC_E4M3>(a, dg, cv.kw, cv.sw, wgm, pw, used, s);
     if (cv.fa == MXC_E2M1 && cv.fb == MXC_E2M1)

@@ -89,17 +89,22 @@ struct FusedEpi {
 // returns 1 when the layer is outside those shapes.  With q, the output is
 // quantized in the epilogue (out, if not NULL, gets the fp32 values that were
 // quantized, CBF layout).
+// With nv_tw / nv_tx (device per-tensor scales of W and the source), the
+// operands are NVFP4: E2M1 codes with E4M3 block scales per 8x8 block.
 int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const void* sc,
-                     const uint8_t* ss, float* out, int layout, hipStream_t s, const FusedEpi* q = nullptr);
+                     const uint8_t* ss, float* out, int layout, hipStream_t s, const FusedEpi* q = nullptr,
+                     const float* nv_tw = nullptr, const float* nv_tx = nullptr);
 // weight gradient for batch block 32 (wgrad_lean.hip): number of K splits
 // (0: not applicable); with more than one split the partial tiles go to the
 // workspace and are reduced by the caller
 int wgrad_lean_splits(const Conv& cv);
 int launch_wgrad_lean(const Conv& cv, const void* gc, const uint8_t* gs, const void* xc, const uint8_t* xs,
-                      float* dst, int splits, hipStream_t s);
+                      float* dst, int splits, hipStream_t s, const float* nv_tg = nullptr,
+                      const float* nv_tx = nullptr);
 size_t wgrad_workspace(const Conv& cv);
 int launch_wgrad(const Conv& cv, const void* gc, const uint8_t* gs, const void* xc,
-                 const uint8_t* xs, float* gw, void* ws, hipStream_t s);
+                 const uint8_t* xs, float* gw, void* ws, hipStream_t s, const float* nv_tg = nullptr,
+                 const float* nv_tx = nullptr);
 
 // naive comparator (naive.hip): a line matrix stores each 1-D-blocked line
 // zero-padded to a multiple of 64 elements (one K step of the MFMA)
@@ -309,6 +314,49 @@ __device__ __forceinline__ uint32_t encode_sr_normal(float x, int s, float inv, 
 __device__ __forceinline__ bool sr_needs_general(float x) {
     const uint32_t ab = __float_as_uint(x) & 0x7FFFFFFFu;
     return ab != 0u && ab < 0x800000u;
+}
+
+// ---------------------------------------------------------------- NVFP4 operands
+// The block-scaled matrix cores take E8M0 scales per 32 K elements; an NVFP
+// block scale is E4M3 per 8 elements.  A code times its E4M3 scale has at most
+// six significant bits and lies in [2^-10, 2688], so it is exact in fp16: the
+// GEMMs decode NVFP4 fragments to fp16 (code x B) and run fp16 MFMAs.  The
+// scaled converts apply only the power of two of their scale operand
+// (measured), so B = 2^E M is split: 2^E goes to the convert, the mantissa
+// factor M (1 + m/8, or m for a subnormal B) is one packed fp16 multiply.
+typedef _Float16 v2h __attribute__((ext_vector_type(2)));
+typedef _Float16 v8h __attribute__((ext_vector_type(8)));
+
+// 32 E2M1 codes (f[0..3], element k in nibble k) and the E4M3 scales of
+// their four groups of 8 (byte g of s4) -> 32 fp16 values in out[0..15]
+// (element k in half k).
+__device__ __forceinline__ void nv_decode32(const v8i& f, uint32_t s4, uint32_t* out) {
+#pragma unroll
+    for (int g = 0; g < 4; g++) {
+        const uint32_t sg = (s4 >> (8 * g)) & 0xFFu;
+        const uint32_t e = (sg >> 3) & 0xFu, m = sg & 7u;
+        const float pw = __uint_as_float(e ? (e + 120u) << 23 : (127u - 9u) << 23);   // 2^(e-7), or 2^-9
+        const _Float16 mh = e ? (_Float16)(1.0f + 0.125f * (float)m) : (_Float16)(float)m;
+        const v2h mm = {mh, mh};
+        const uint32_t src = (uint32_t)f[g];
+#define NVD(SEL) { const v2h v = __builtin_bit_cast(v2h, __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(src, pw, SEL)) * mm; \
+                   out[4 * g + SEL] = __builtin_bit_cast(uint32_t, v); }
+        NVD(0) NVD(1) NVD(2) NVD(3)
+#undef NVD
+    }
+}
+
+// D += A B over the 64 K elements of two decoded fragments: four fp16 MFMAs,
+// instruction t taking elements 8t .. 8t+7 of each lane's 32 (the same K
+// relabelling on both operands, so the sum is unchanged).
+__device__ __forceinline__ v16f mfma_nv(const uint32_t* a, const uint32_t* b, v16f c) {
+#pragma unroll
+    for (int t = 0; t < 4; t++) {
+        v4i av = {(int)a[4 * t], (int)a[4 * t + 1], (int)a[4 * t + 2], (int)a[4 * t + 3]};
+        v4i bv = {(int)b[4 * t], (int)b[4 * t + 1], (int)b[4 * t + 2], (int)b[4 * t + 3]};
+        c = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(v8h, av), __builtin_bit_cast(v8h, bv), c, 0, 0, 0);
+    }
+    return c;
 }
 
 // four consecutive elements -> four E2M1 codes in 16 bits (first element in the low nibble)

@@ -39,6 +39,11 @@ struct WLArgs {
     int cot, cit, ntiles;          // 64-row / 64-column tile counts, tiles
     int ppw;                       // pixel pairs per wave
     int nsplit;
+    // NVFP4 operands: gs / xs hold E4M3 scales per 8x8 block ([pixel][Cp/8][4]:
+    // a row's four sample groups in four consecutive bytes); tg, tx the
+    // per-tensor scales
+    const float* tg;
+    const float* tx;
 };
 
 // One operand's fragment for a K step: K block 0 from pixel row p0, K block
@@ -64,8 +69,11 @@ __device__ __forceinline__ v8i row_frag(const uint8_t* p0, const uint8_t* p1, co
     return o;
 }
 
-template <int FA, int FB>
+// NV: NVFP4 operands, decoded to fp16 per fragment and multiplied on fp16
+// MFMAs (the 8-sample groups of a row each have their own E4M3 scale).
+template <int FA, int FB, bool NV = false>
 __global__ __launch_bounds__(WT) void wgrad_lean_kernel(WLArgs p) {
+    static_assert(!NV || (FA == MXC_E2M1 && FB == MXC_E2M1), "NVFP4 operands only");
     constexpr int RBA = 32 * fmt_bits(FA) / 8;    // bytes of one block row (32 samples): G_Y
     constexpr int RBB = 32 * fmt_bits(FB) / 8;    // X
     constexpr int TBA = 32 * RBA, TBB = 32 * RBB; // bytes of one block
@@ -115,6 +123,7 @@ __global__ __launch_bounds__(WT) void wgrad_lean_kernel(WLArgs p) {
     struct Ops {
         v8i a[2], b[2];
         int sa[2], sb[2];
+        uint32_t na[2], nb[2];     // NV: the four E4M3 scales of the lane's row
     };
     auto load = [&](int q, bool live, Ops& o) {
         int pg[2];                 // pixel index (or -1) of K block 0 / 1
@@ -149,24 +158,55 @@ __global__ __launch_bounds__(WT) void wgrad_lean_kernel(WLArgs p) {
             const uint8_t sb = p.xs[(Q >= 0 && b_ok[i]) ? (size_t)Q * p.x_ncb + cib : 0];
             o.sa[i] = (P >= 0 && a_ok[i]) ? sa : 0;
             o.sb[i] = (Q >= 0 && b_ok[i]) ? sb : 0;
+            if constexpr (NV) {
+                const uint32_t* ga = (const uint32_t*)p.gs;
+                const uint32_t* xa = (const uint32_t*)p.xs;
+                const uint32_t va = ga[(P >= 0 && a_ok[i]) ? ((size_t)P * (p.gy_cp / 8) + cob * 4 + (r >> 3)) : 0];
+                const uint32_t vb = xa[(Q >= 0 && b_ok[i]) ? ((size_t)Q * (p.x_cp / 8) + cib * 4 + (r >> 3)) : 0];
+                o.na[i] = (P >= 0 && a_ok[i]) ? va : 0u;
+                o.nb[i] = (Q >= 0 && b_ok[i]) ? vb : 0u;
+            }
         }
     };
 
     // batches of PB pairs: all loads of a batch are in flight together (the
     // loop is bound by memory latency, not by the MFMAs); pairs past the
     // wave's range get a zero G_Y operand and add nothing
-    constexpr int PB = 4;
+    constexpr int PB = NV ? 2 : 4;
     for (int q = q0; q < q1; q += PB) {
         Ops o[PB];
 #pragma unroll
         for (int b = 0; b < PB; b++) load(q + b, q + b < q1, o[b]);
 #pragma unroll
-        for (int b = 0; b < PB; b++)
+        for (int b = 0; b < PB; b++) {
+            if constexpr (NV) {
+                uint32_t ad[2][16], bd[2][16];
 #pragma unroll
-            for (int i = 0; i < 2; i++)
+                for (int i = 0; i < 2; i++) {
+                    nv_decode32(o[b].a[i], o[b].na[i], ad[i]);
+                    nv_decode32(o[b].b[i], o[b].nb[i], bd[i]);
+                }
 #pragma unroll
-                for (int j = 0; j < 2; j++)
-                    acc[i][j] = mfma_mx<FA, FB>(o[b].a[i], o[b].b[j], acc[i][j], o[b].sa[i], o[b].sb[j]);
+                for (int i = 0; i < 2; i++)
+#pragma unroll
+                    for (int j = 0; j < 2; j++) acc[i][j] = mfma_nv(ad[i], bd[j], acc[i][j]);
+            } else {
+#pragma unroll
+                for (int i = 0; i < 2; i++)
+#pragma unroll
+                    for (int j = 0; j < 2; j++)
+                        acc[i][j] = mfma_mx<FA, FB>(o[b].a[i], o[b].b[j], acc[i][j], o[b].sa[i], o[b].sb[j]);
+            }
+        }
+    }
+    if constexpr (NV) {   // the per-tensor scales T_GY T_X
+        const float tt = *p.tg * *p.tx;
+#pragma unroll
+        for (int i = 0; i < 2; i++)
+#pragma unroll
+            for (int j = 0; j < 2; j++)
+#pragma unroll
+                for (int e = 0; e < 16; e++) acc[i][j][e] *= tt;
     }
 
     // ---- sum the four waves' tiles, then write
@@ -214,10 +254,11 @@ int wgrad_lean_splits(const Conv& cv) {
 }
 
 int launch_wgrad_lean(const Conv& cv, const void* gc, const uint8_t* gs, const void* xc, const uint8_t* xs,
-                      float* dst, int splits, hipStream_t s) {
+                      float* dst, int splits, hipStream_t s, const float* nv_tg, const float* nv_tx) {
     WLArgs a;
     a.gc = (const uint8_t*)gc; a.gs = gs; a.xc = (const uint8_t*)xc; a.xs = xs;
     a.dst = dst;
+    a.tg = nv_tg; a.tx = nv_tx;
     a.direct = splits == 1;
     a.cout = cv.cout; a.cin = cv.cin; a.kh = cv.kh; a.kw = cv.kw; a.sh = cv.sh; a.sw = cv.sw;
     a.ph = cv.ph; a.pw = cv.pw; a.ho = cv.ho; a.wo = cv.wo; a.h = cv.h; a.w = cv.w;
@@ -233,6 +274,11 @@ int launch_wgrad_lean(const Conv& cv, const void* gc, const uint8_t* gs, const v
     const long grid = ((long)a.ntiles * splits + 7) / 8 * 8;
     if (grid > 0x7FFFFFFFL) return MXC_ERR_SHAPE;
     const dim3 gd((unsigned)grid);
+    if (nv_tg) {
+        if (cv.fa != MXC_E2M1 || cv.fb != MXC_E2M1) return MXC_ERR_ARG;
+        hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E2M1, MXC_E2M1, true>), gd, dim3(WT), 0, s, a);
+        return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
+    }
     if (cv.fa == MXC_E4M3 && cv.fb == MXC_E4M3)      hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E4M3, MXC_E4M3>), gd, dim3(WT), 0, s, a);
     else if (cv.fa == MXC_E2M1 && cv.fb == MXC_E2M1) hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E2M1, MXC_E2M1>), gd, dim3(WT), 0, s, a);
     else if (cv.fa == MXC_E2M3 && cv.fb == MXC_E2M3) hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E2M3, MXC_E2M3>), gd, dim3(WT), 0, s, a);

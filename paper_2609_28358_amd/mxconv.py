@@ -64,6 +64,9 @@ def lib():
         "mxconv_nvfp_scales_bytes": (sz, [i32] * 6),
         "mxconv_nvfp_workspace_bytes": (sz, []),
         "mxconv_nvfp_quantize": (i32, [P, i32, i32, i32, i32, i32, i32, i32, i32, P, P, P, P, sz, P]),
+        "mxconv_nvfp_fwd": (i32, [CP, i32, P, P, P, P, P, P, P, i32, P]),
+        "mxconv_nvfp_dgrad": (i32, [CP, i32, P, P, P, P, P, P, P, i32, P]),
+        "mxconv_nvfp_wgrad": (i32, [CP, i32, P, P, P, P, P, P, P, P, sz, P]),
         "mxconv_im2col_cbf": (i32, [CP, i32, P, P, P, P, P]),
         "mxconv_fwd": (i32, [CP, i32, P, P, P, P, P, i32, P]),
         "mxconv_dgrad": (i32, [CP, i32, P, P, P, P, P, i32, P]),
@@ -238,6 +241,36 @@ def nvfp_quantize(src, role, fmt, layout=NCHW, shape=None, workspace=None, strea
                                   _ptr(out.tscale), _ptr(workspace), workspace.numel() * workspace.element_size(),
                                   _stream(stream)), "mxconv_nvfp_quantize")
     return out
+
+
+def nvfp_fwd(cv, w, x, layout=NCHW, out=None, stream=None):
+    """Y = W * X on NVFP4 operands (NvfpTensor)."""
+    y = _out((cv["n"], cv["cout"], *out_size(cv)), layout, batch_block(cv["n"]), x.codes.device, out)
+    _check(lib().mxconv_nvfp_fwd(ctypes.byref(conv_struct(cv)), x.fmt, _ptr(w.codes), _ptr(w.scales), _ptr(w.tscale),
+                                 _ptr(x.codes), _ptr(x.scales), _ptr(x.tscale), _ptr(y), layout, _stream(stream)),
+           "mxconv_nvfp_fwd")
+    return y
+
+
+def nvfp_dgrad(cv, w, gy, layout=NCHW, out=None, stream=None):
+    gx = _out((cv["n"], cv["cin"], cv["h"], cv["w"]), layout, batch_block(cv["n"]), gy.codes.device, out)
+    _check(lib().mxconv_nvfp_dgrad(ctypes.byref(conv_struct(cv)), gy.fmt, _ptr(w.codes), _ptr(w.scales),
+                                   _ptr(w.tscale), _ptr(gy.codes), _ptr(gy.scales), _ptr(gy.tscale), _ptr(gx), layout,
+                                   _stream(stream)), "mxconv_nvfp_dgrad")
+    return gx
+
+
+def nvfp_wgrad(cv, gy, x, out=None, workspace=None, stream=None):
+    gw = out if out is not None else torch.empty((cv["cout"], cv["cin"], cv["kh"], cv["kw"]),
+                                                 dtype=torch.float32, device=x.codes.device)
+    need = wgrad_workspace_bytes(cv, x.fmt)
+    if workspace is None and need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=x.codes.device)
+    wsz = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(lib().mxconv_nvfp_wgrad(ctypes.byref(conv_struct(cv)), x.fmt, _ptr(gy.codes), _ptr(gy.scales),
+                                   _ptr(gy.tscale), _ptr(x.codes), _ptr(x.scales), _ptr(x.tscale), _ptr(gw),
+                                   _ptr(workspace), wsz, _stream(stream)), "mxconv_nvfp_wgrad")
+    return gw
 
 
 def im2col_cbf(cv, x, stream=None):

@@ -80,3 +80,109 @@ def test_nvfp_full_size_activation(mx, fmt):
     x, _, gy = synth.layer_inputs(cv, 1001, kind="sweep")
     for t in (x, gy):
         _check(mx, t, mx.ACT, fmt, mx.CBF, synth.nchw_to_cbf(t, 32))
+
+
+# ------------------------------------------------------------------ GEMMs on NVFP4 operands
+TOL = 1e-5
+
+NV_CONVS = [
+    synth.conv_dict(32, 64, 64, 12, 10, 3, 1, 1),
+    synth.conv_dict(32, 64, 96, 9, 9, 1, 1, 0),
+    synth.conv_dict(32, 64, 48, 11, 9, 3, 2, 1),               # stride 2 (input gradient in phases)
+    synth.conv_dict(64, 32, 128, 6, 5, 3, 1, 1),               # two batch groups
+    synth.conv_dict(32, 128, 64, 8, 8, 1, 2, 0),               # 1x1 stride 2: a phase with no taps
+    synth.conv_dict(32, 96, 200, 7, 9, 3, 2, 1),               # ragged channels
+    synth.conv_dict(32, 40, 72, 13, 11, 3, 1, 1),
+]
+
+
+def _nv_ids(c):
+    return f"n{c['n']}_{c['cin']}to{c['cout']}_{c['h']}x{c['w']}_k{c['kh']}{c['kw']}_s{c['sh']}{c['sw']}"
+
+
+def _nv_layer(mx, cv, seed, kind="unit"):
+    x, w, gy = synth.layer_inputs(cv, seed, kind=kind)
+    q, d = {}, {}
+    for k, t, role in (("x", x, mx.ACT), ("w", w, mx.WEIGHT), ("gy", gy, mx.ACT)):
+        src = synth.nchw_to_cbf(t, 32) if role == mx.ACT else t
+        q[k] = _check(mx, t, role, 1, mx.CBF if role == mx.ACT else mx.NCHW, src)   # bit-exact quantize first
+        rc, rs, rt = oracle.nvfp_quantize(t.numpy(), oracle.NCHW, role, 1, *t.shape)
+        d[k] = oracle.nvfp_dequant(rc, rs, rt, role, 1, *t.shape)
+    return q, d
+
+
+def _nv_err(got, ref, sabs):
+    got = got.astype(np.float64)
+    zero = sabs == 0
+    assert np.all(got[zero] == 0)
+    nz = ~zero
+    return float(np.max(np.abs(got[nz] - ref[nz]) / (TOL * sabs[nz]))) if nz.any() else 0.0
+
+
+@pytest.mark.parametrize("cv", NV_CONVS, ids=_nv_ids)
+@pytest.mark.parametrize("layout", ["nchw", "cbf"])
+def test_nvfp_gemms(mx, cv, layout):
+    """Forward, input gradient and weight gradient of the fake-quantized
+    NVFP4 tensors against the oracle's direct convolutions of Eqs. (1)-(3)
+    (fp64), within 1e-5 of the sum of absolute products."""
+    lay = mx.NCHW if layout == "nchw" else mx.CBF
+    q, d = _nv_layer(mx, cv, 31)
+    ho, wo = synth.out_hw(cv)
+    y = mx.nvfp_fwd(cv, q["w"], q["x"], layout=lay)
+    gw = mx.nvfp_wgrad(cv, q["gy"], q["x"])
+    dg_ok = (cv["sh"], cv["sw"]) in ((1, 1), (2, 2))
+    gx = mx.nvfp_dgrad(cv, q["w"], q["gy"], layout=lay) if dg_ok else None
+    torch.cuda.synchronize()
+    if lay == mx.CBF:
+        y = synth.cbf_to_nchw(y.cpu(), cv["n"], cv["cout"], ho, wo, 32)
+        if gx is not None:
+            gx = synth.cbf_to_nchw(gx.cpu(), cv["n"], cv["cin"], cv["h"], cv["w"], 32)
+    e = [_nv_err(y.cpu().numpy(), oracle.direct_fwd(cv, d["w"], d["x"]),
+                 oracle.direct_fwd(cv, np.abs(d["w"]), np.abs(d["x"]))),
+         _nv_err(gw.cpu().numpy(), oracle.direct_wgrad(cv, d["gy"], d["x"]),
+                 oracle.direct_wgrad(cv, np.abs(d["gy"]), np.abs(d["x"])))]
+    if gx is not None:
+        e.append(_nv_err(gx.cpu().numpy(), oracle.direct_dgrad(cv, d["w"], d["gy"]),
+                         oracle.direct_dgrad(cv, np.abs(d["w"]), np.abs(d["gy"]))))
+    assert max(e) <= 1.0, e
+
+
+def test_nvfp_gemms_full_size_layer(mx):
+    """The 3x3 s1 64->64 56x56 layer at batch 32: 2048 sampled outputs of
+    each GEMM against dot products of the dequantized operands."""
+    name, cv = synth.SWEEP_LAYERS[0]
+    q, d = _nv_layer(mx, cv, 3000, kind="sweep")
+    ho, wo = synth.out_hw(cv)
+    y = synth.cbf_to_nchw(mx.nvfp_fwd(cv, q["w"], q["x"], layout=mx.CBF).cpu(), cv["n"], cv["cout"], ho, wo, 32).numpy()
+    gx = synth.cbf_to_nchw(mx.nvfp_dgrad(cv, q["w"], q["gy"], layout=mx.CBF).cpu(), cv["n"], cv["cin"], cv["h"],
+                           cv["w"], 32).numpy()
+    gw = mx.nvfp_wgrad(cv, q["gy"], q["x"]).cpu().numpy()
+    rng = np.random.default_rng(9)
+    xp = np.pad(d["x"], ((0, 0), (0, 0), (1, 1), (1, 1)))
+    gp = np.pad(d["gy"], ((0, 0), (0, 0), (1, 1), (1, 1)))
+    wf = d["w"][:, :, ::-1, ::-1]
+    errs = []
+    for _ in range(2048):
+        n, co, oy, ox = (int(rng.integers(s)) for s in (cv["n"], cv["cout"], ho, wo))
+        t = d["w"][co] * xp[n, :, oy:oy + 3, ox:ox + 3]
+        errs.append(abs(y[n, co, oy, ox] - t.sum()) / (TOL * np.abs(t).sum() + 1e-300))
+        n, ci, iy, ix = (int(rng.integers(s)) for s in (cv["n"], cv["cin"], cv["h"], cv["w"]))
+        t = wf[:, ci] * gp[n, :, iy:iy + 3, ix:ix + 3]
+        errs.append(abs(gx[n, ci, iy, ix] - t.sum()) / (TOL * np.abs(t).sum() + 1e-300))
+    for _ in range(256):
+        co, ci, a, b = (int(rng.integers(s)) for s in (cv["cout"], cv["cin"], 3, 3))
+        t = d["gy"][:, co] * xp[:, ci, a:a + ho, b:b + wo]
+        errs.append(abs(gw[co, ci, a, b] - t.sum()) / (TOL * np.abs(t).sum() + 1e-300))
+    assert max(errs) <= 1.0, max(errs)
+
+
+def test_nvfp_gemm_refusals(mx):
+    """Other element formats and layers outside the batch-block-32 kernels are refused."""
+    cv = synth.conv_dict(32, 32, 32, 9, 9, 5, 1, 2)                 # kernel width 5
+    q, _ = _nv_layer(mx, cv, 5)
+    with pytest.raises(mx.MxconvError, match="code -3"):
+        mx.nvfp_fwd(cv, q["w"], q["x"])
+    x8 = mx.nvfp_quantize(synth.nchw_to_cbf(synth.normal((32, 32, 9, 9), 1.0, 3), 32).to(DEV), mx.ACT, 0,
+                          layout=mx.CBF, shape=(32, 32, 9, 9))
+    with pytest.raises(mx.MxconvError, match="code -2"):
+        mx.nvfp_fwd(cv, q["w"], x8)
