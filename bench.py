@@ -249,6 +249,7 @@ def main():
     ap.add_argument("--no-fused", action="store_true", help="skip the fused-epilogue leg")
     ap.add_argument("--no-fp6", action="store_true", help="skip the FP6-method leg")
     ap.add_argument("--no-sr", action="store_true", help="skip the stochastic-rounding leg")
+    ap.add_argument("--no-nvfp", action="store_true", help="skip the NVFP4 leg")
     ap.add_argument("--pmc-pass", action="store_true",
                     help="counter-collection pass: every op once in step order, then a copy of known size")
     ap.add_argument("--layers", default="all", help="comma list of layer indices (profiling aid)")
@@ -398,6 +399,12 @@ def main():
 
     import statistics
     LLC_BYTES = 256 << 20
+
+    def rotated(base):
+        # copies of a quantize source that together exceed the last-level cache
+        ncopy = min(48, -(-(LLC_BYTES + (64 << 20)) // (base.numel() * base.element_size())))
+        return [base] + [base.clone() for _ in range(ncopy - 1)]
+
     steady = {}
     for j, op in seq:
         srcs = [None]
@@ -476,10 +483,6 @@ def main():
             b = mx.codes_bytes(role, f, *shape) + mx.scales_bytes(role, f, *shape)
             return b - (FP6_SLACK if f in (2, 3) else 0)
 
-        def rotated(base):
-            ncopy = min(48, -(-(LLC_BYTES + (64 << 20)) // (base.numel() * base.element_size())))
-            return [base] + [base.clone() for _ in range(ncopy - 1)]
-
         seen = set()
         for j in jobs:
             cv = j["cv"]
@@ -556,6 +559,51 @@ def main():
             run_op(j, "quant_gy")
         torch.cuda.synchronize()
 
+    # The paper-literal NVFP4 format (outside the step): per layer, the two-
+    # launch quantize of X, W and G_Y and the three GEMMs on fp16 MFMAs,
+    # timed like `ops`, against the MXFP4 layer of the step.
+    nvfp = {}
+    if not args.no_nvfp:
+        seen = set()
+        for j in jobs:
+            cv = j["cv"]
+            lname = j["name"].split("/")[0]
+            if lname in seen:
+                continue
+            seen.add(lname)
+            wsh = tuple(j["w"].shape)
+            xsrc, gsrc = rotated(j["x"]), rotated(j["gy"])
+            wsn = torch.empty(mx.lib().mxconv_nvfp_workspace_bytes(), dtype=torch.uint8, device=dev)
+            it = {"x": 0, "g": 0}
+            qx = mx.nvfp_quantize(j["x"], mx.ACT, 1, layout=mx.CBF, shape=j["xs"], workspace=wsn)
+            qw = mx.nvfp_quantize(j["w"], mx.WEIGHT, 1, workspace=wsn)
+            qg = mx.nvfp_quantize(j["gy"], mx.ACT, 1, layout=mx.CBF, shape=j["gs"], workspace=wsn)
+
+            def nq(t, src_list, key, shape):
+                it[key] += 1
+                c = mx.lib().mxconv_nvfp_quantize(
+                    mx._ptr(src_list[it[key] % len(src_list)]), mx.F32, mx.CBF, mx.ACT, 1, *shape,
+                    mx._ptr(t.codes), mx._ptr(t.scales), mx._ptr(t.tscale), mx._ptr(wsn), wsn.numel(), mx._stream(None))
+                if c:
+                    raise mx.MxconvError(mx.strerror(c))
+
+            kq = max(12, len(xsrc), len(gsrc))
+            ws4 = torch.empty(max(1, mx.wgrad_workspace_bytes(cv, 1)), dtype=torch.uint8, device=dev)
+            t = {"quant_x": steady_ms(lambda: nq(qx, xsrc, "x", j["xs"]), kq),
+                 "quant_w": steady_ms(lambda: mx.nvfp_quantize(j["w"], mx.WEIGHT, 1, workspace=wsn)),
+                 "quant_gy": steady_ms(lambda: nq(qg, gsrc, "g", j["gs"]), kq),
+                 "fwd": steady_ms(lambda: mx.nvfp_fwd(cv, qw, qx, layout=mx.CBF, out=j["y"])),
+                 "dgrad": steady_ms(lambda: mx.nvfp_dgrad(cv, qw, qg, layout=mx.CBF, out=j["gx"])),
+                 "wgrad": steady_ms(lambda: mx.nvfp_wgrad(cv, qg, qx, out=j["gw"], workspace=ws4))}
+            fl = j["nums"]["fwd"][0]
+            fp4 = sum(steady[(f"{lname}/mxfp4", op)] for op in ("quant_xw", "quant_gy", "fwd", "dgrad", "wgrad"))
+            r = {k + "_ms": round(v, 4) for k, v in t.items()}
+            r.update({g + "_tflops": round(fl / (t[g] * 1e-3) / 1e12, 1) for g in ("fwd", "dgrad", "wgrad")})
+            r["layer_ms"] = round(sum(t.values()), 4)
+            r["layer_ms_vs_mxfp4"] = round(sum(t.values()) / fp4, 3)
+            nvfp[f"{lname}/nvfp4"] = r
+            del xsrc, gsrc
+
     gemm_flops = sum(j["nums"][op][0] for j in jobs for op in ("fwd", "dgrad", "wgrad"))
     value = gemm_flops / (ms_step * 1e-3) / 1e12
 
@@ -607,6 +655,8 @@ def main():
         out["fp6_methods"] = fp6
     if sr:
         out["stochastic_rounding"] = sr
+    if nvfp:
+        out["nvfp4"] = nvfp
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline()
     print(json.dumps(out))
