@@ -230,16 +230,20 @@ def test_quantizer_invariants(fmt):
     assert np.array_equal(c2, codes) and np.array_equal(s2, scales)
 
 
+def _fp6_ok(fmt, n):
+    """FP6 activation codes fill whole bytes per channel row only with a batch
+    block of at least 4, so smaller batches are not a valid FP6 case."""
+    fs = fmt if isinstance(fmt, tuple) else (fmt,)
+    return n >= 4 or all(BITS[f] != 6 for f in fs)
+
+
 def _pos(n, c, h, w, bn, H, W, Cp):
     """Stated code layout [N/Bn][H][W][Cp][Bn] (a spec, not the method)."""
     return ((((n // bn) * H + h) * W + w) * Cp + c) * bn + n % bn
 
 
-@pytest.mark.parametrize("fmt", ALL_FMTS)
-@pytest.mark.parametrize("N", [2, 4, 16, 64])
+@pytest.mark.parametrize("fmt,N", [(f, N) for N in [2, 4, 16, 64] for f in ALL_FMTS if _fp6_ok(f, N)])
 def test_layout_single_element(fmt, N):
-    if BITS[fmt] == 6 and N < 4:
-        pytest.skip("FP6 activations need Bn >= 4")
     C, H, W = 40, 3, 5
     Cp, bn = 64, min(32, N)
     rng = np.random.default_rng(N)
@@ -330,6 +334,17 @@ CONVS = [
 ]
 
 
+def _conv_fmts(convs, fmts):
+    return [(cv, f) for cv in convs for f in fmts if _fp6_ok(f, cv["n"])]
+
+
+def _cv_fmt_id(v):
+    if isinstance(v, dict):
+        return f"n{v['n']}c{v['cin']}k{v['kh']}{v['kw']}s{v['sh']}"
+    names = {k: n for n, k in FMTS.items()}
+    return "-".join(names[t] for t in v) if isinstance(v, tuple) else names[v]
+
+
 def _unfold_as_tensor(x, cv):
     """fp32 im2col via F.unfold, viewed as (N, C, Ho*Wo*Kh*Kw, 1) with pixel
     index ((ho*Wo+wo)*Kh+kh)*Kw+kw."""
@@ -340,13 +355,10 @@ def _unfold_as_tensor(x, cv):
     return u.reshape(n, c, ho * wo * cv["kh"] * cv["kw"], 1).contiguous()
 
 
-@pytest.mark.parametrize("fmt", ALL_FMTS)
-@pytest.mark.parametrize("cv", CONVS, ids=lambda c: f"n{c['n']}c{c['cin']}k{c['kh']}{c['kw']}s{c['sh']}")
+@pytest.mark.parametrize("cv,fmt", _conv_fmts(CONVS, ALL_FMTS), ids=_cv_fmt_id)
 def test_im2col_commutes_with_quantize(fmt, cv):
     """quantize(im2col(X)) == im2col_cbf(quantize(X)), bit for bit (Sec. IV-B:
     quantizing X_{Cin,N} keeps its blocks whole through the CBF im2col)."""
-    if BITS[fmt] == 6 and cv["n"] < 4:
-        pytest.skip("FP6 activations need Bn >= 4")
     x = torch.from_numpy(_rand_tensor((cv["n"], cv["cin"], cv["h"], cv["w"]), 31))
     q = oracle.quantize(x.numpy(), oracle.NCHW, oracle.ACT, fmt, cv["n"], cv["cin"], cv["h"], cv["w"])
     col = oracle.im2col_cbf(cv, fmt, *q)
@@ -416,11 +428,8 @@ def _close(a, b, s):
     return np.max(np.abs(a - b) / scale) <= 1e-12
 
 
-@pytest.mark.parametrize("fmt", LAYER_FMTS, ids=_fmt_id)
-@pytest.mark.parametrize("cv", CONVS, ids=lambda c: f"n{c['n']}c{c['cin']}k{c['kh']}{c['kw']}s{c['sh']}")
+@pytest.mark.parametrize("cv,fmt", _conv_fmts(CONVS, LAYER_FMTS), ids=_cv_fmt_id)
 def test_gemms_match_torch_fp64(fmt, cv):
-    if isinstance(fmt, tuple) and cv["n"] < 4:
-        pytest.skip("FP6 activations need Bn >= 4")
     qx, qw, qg, xd, wd, gd = _quantized_layer(cv, fmt, 5)
     pf, pd_, pw = _pairs(fmt)
     st, pd = (cv["sh"], cv["sw"]), (cv["ph"], cv["pw"])
@@ -440,11 +449,9 @@ def test_gemms_match_torch_fp64(fmt, cv):
     assert np.allclose(sgw, sgw_ref, rtol=1e-12, atol=0)
 
 
-@pytest.mark.parametrize("fmt", [oracle.E4M3, (oracle.E2M1, oracle.E3M2, oracle.E2M1)], ids=_fmt_id)
-@pytest.mark.parametrize("cv", CONVS[:4], ids=lambda c: f"n{c['n']}c{c['cin']}k{c['kh']}{c['kw']}s{c['sh']}")
+@pytest.mark.parametrize("cv,fmt", _conv_fmts(CONVS[:4], [oracle.E4M3, (oracle.E2M1, oracle.E3M2, oracle.E2M1)]),
+                         ids=_cv_fmt_id)
 def test_gemms_match_direct_definitions(cv, fmt):
-    if isinstance(fmt, tuple) and cv["n"] < 4:
-        pytest.skip("FP6 activations need Bn >= 4")
     qx, qw, qg, xd, wd, gd = _quantized_layer(cv, fmt, 6)
     pf, pd_, pw = _pairs(fmt)
     y, sy = oracle.fwd(cv, pf, qw, qx)
@@ -455,11 +462,9 @@ def test_gemms_match_direct_definitions(cv, fmt):
     assert _close(gw, oracle.direct_wgrad(cv, gd, xd), sgw)
 
 
-@pytest.mark.parametrize("fmt", [oracle.E2M1, (oracle.E2M3, oracle.E3M2, oracle.E2M1)], ids=_fmt_id)
-@pytest.mark.parametrize("cv", CONVS[:4], ids=lambda c: f"n{c['n']}c{c['cin']}k{c['kh']}{c['kw']}s{c['sh']}")
+@pytest.mark.parametrize("cv,fmt", _conv_fmts(CONVS[:4], [oracle.E2M1, (oracle.E2M3, oracle.E3M2, oracle.E2M1)]),
+                         ids=_cv_fmt_id)
 def test_single_output_routines_match_full(cv, fmt):
-    if isinstance(fmt, tuple) and cv["n"] < 4:
-        pytest.skip("FP6 activations need Bn >= 4")
     qx, qw, qg, xd, wd, gd = _quantized_layer(cv, fmt, 8)
     pf, pd_, pw = _pairs(fmt)
     ho, wo = synth.out_hw(cv)
