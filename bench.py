@@ -409,9 +409,7 @@ def main():
     for j, op in seq:
         srcs = [None]
         if op in ("quant_xw", "quant_x", "quant_gy"):
-            base = j["x"] if op in ("quant_xw", "quant_x") else j["gy"]
-            ncopy = min(48, -(-(LLC_BYTES + (64 << 20)) // (base.numel() * base.element_size())))
-            srcs = [base] + [base.clone() for _ in range(ncopy - 1)]
+            srcs = rotated(j["x"] if op in ("quant_xw", "quant_x") else j["gy"])
         kl = max(12, len(srcs))
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
@@ -539,8 +537,7 @@ def main():
     if not args.no_sr:
         for j in jobs:
             fmt = j["fmt"]
-            gsrc = [j["gy"]] + [j["gy"].clone() for _ in range(min(48, -(-(LLC_BYTES + (64 << 20)) // (
-                j["gy"].numel() * j["gy"].element_size()))) - 1)]
+            gsrc = rotated(j["gy"])
             it = [0]
 
             def qsr():
