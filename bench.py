@@ -149,31 +149,37 @@ def naive_numbers(cv, fmt, mx):
     return by, 2 * P * K + 2 * nw + 2 * ny
 
 
-def cpu_baseline():
-    """The oracle on the benchmark's own workload, once: every layer of the
-    sweep in both formats -- quantize X, W, G_Y, CBF im2col, fwd, dgrad,
-    wgrad in fp64 loops on the host -- i.e. one step on the CPU."""
+def cpu_baseline(min_s=10.0, max_steps=8):
+    """The oracle on the benchmark's own workload: every layer of the sweep in
+    both formats -- quantize X, W, G_Y, CBF im2col, fwd, dgrad, wgrad in fp64
+    loops on the host -- i.e. one step on the CPU, repeated until at least
+    min_s seconds of oracle work (at most max_steps steps)."""
     import oracle
     from paper_2609_28358_amd import synth
-    flops, dt = 0.0, 0.0
+    inputs = []
     for li, (name, cv) in enumerate(synth.SWEEP_LAYERS):
         x, w, gy = synth.layer_inputs(cv, 1000 + li, kind="sweep")
-        xn, wn, gn = x.numpy(), w.numpy(), gy.numpy()
-        ho, wo = synth.out_hw(cv)
-        for fmt in (0, 1):
-            t0 = time.perf_counter()
-            ox = oracle.quantize(xn, oracle.NCHW, oracle.ACT, fmt, *x.shape)
-            ow = oracle.quantize(wn, oracle.NCHW, oracle.WEIGHT, fmt, *w.shape)
-            og = oracle.quantize(gn, oracle.NCHW, oracle.ACT, fmt, *gy.shape)
-            oracle.im2col_cbf(cv, fmt, *ox)
-            oracle.fwd(cv, fmt, ow, ox)
-            oracle.dgrad(cv, fmt, ow, og)
-            oracle.wgrad(cv, fmt, og, ox)
-            dt += time.perf_counter() - t0
-            flops += 3 * 2.0 * cv["n"] * cv["cout"] * ho * wo * cv["cin"] * cv["kh"] * cv["kw"]
+        inputs.append((cv, x, w, gy))
+    flops, dt, steps = 0.0, 0.0, 0
+    while steps < max_steps and (steps == 0 or dt < min_s):
+        for cv, x, w, gy in inputs:
+            xn, wn, gn = x.numpy(), w.numpy(), gy.numpy()
+            ho, wo = synth.out_hw(cv)
+            for fmt in (0, 1):
+                t0 = time.perf_counter()
+                ox = oracle.quantize(xn, oracle.NCHW, oracle.ACT, fmt, *x.shape)
+                ow = oracle.quantize(wn, oracle.NCHW, oracle.WEIGHT, fmt, *w.shape)
+                og = oracle.quantize(gn, oracle.NCHW, oracle.ACT, fmt, *gy.shape)
+                oracle.im2col_cbf(cv, fmt, *ox)
+                oracle.fwd(cv, fmt, ow, ox)
+                oracle.dgrad(cv, fmt, ow, og)
+                oracle.wgrad(cv, fmt, og, ox)
+                dt += time.perf_counter() - t0
+                flops += 3 * 2.0 * cv["n"] * cv["cout"] * ho * wo * cv["cin"] * cv["kh"] * cv["kw"]
+        steps += 1
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.get_threads(), "kind": "oracle",
-            "sample": f"one full step of the benchmark workload (all three layers, MXFP8 and MXFP4) through "
-                      f"the fp64 oracle: {dt:.1f} s"}
+            "sample": f"{steps} full step{'s' if steps > 1 else ''} of the benchmark workload (all three layers, MXFP8 and MXFP4, "
+                      f"every op of the path) through the fp64 oracle: {dt:.1f} s"}
 
 
 def naive_leg(jobs, op_ms, mx, synth, dev, stream, reps=3):
