@@ -98,3 +98,47 @@ SWEEP_LAYERS = (
 
 # The small single-layer case: N=2, 32->32, 8x8, 3x3 s1 p1, MXFP8, one seed.
 UNIT_LAYER = conv_dict(2, 32, 32, 8, 8, 3, 1, 1)
+
+
+# YOLOv8n-shaped backbone + neck (batch 16 in MXFP8, batch 64 in MXFP4; a
+# 3x640x640 input, bf16 master tensors).  Representative layers at their full
+# sizes: the stride-2 3x3 stem (3 -> 16 channels, 640x640 -> 320x320), a
+# C2f-style 3x3 at half the stage width (16 channels, 160x160) and a C2f-style
+# 1x1 merging 3c/2 -> c at the deepest stage (384 -> 256, 20x20).
+def yolo_layers(n):
+    return (
+        ("stem_3to16_s2_640", conv_dict(n, 3, 16, 640, 640, 3, 2, 1)),
+        ("c2f_3x3_16_160", conv_dict(n, 16, 16, 160, 160, 3, 1, 1)),
+        ("c2f_1x1_384to256_20", conv_dict(n, 384, 256, 20, 20, 1, 1, 0)),
+    )
+
+
+def yolo_inputs(name, cv, seed):
+    """X and W as bf16 (the master tensors), G_Y fp32.  The stem reads the
+    image, U(0, 1); deeper layers read SiLU feature maps; W Kaiming-normal;
+    G_Y ~ N(0, 1e-3)."""
+    ho, wo = out_hw(cv)
+    xs = (cv["n"], cv["cin"], cv["h"], cv["w"])
+    x = uniform(xs, seed * 3) if name.startswith("stem") else silu_normal(xs, seed * 3)
+    w = kaiming(cv["cout"], cv["cin"], cv["kh"], cv["kw"], seed * 3 + 1)
+    gy = normal((cv["n"], cv["cout"], ho, wo), 1e-3, seed * 3 + 2)
+    return x.to(torch.bfloat16), w.to(torch.bfloat16), gy
+
+
+# Quantized latent replay: a buffer of 8192 latents of 128 x 16 x 16 (the
+# output of a frozen front stack, SiLU-activated; drawn here as SiLU of
+# N(0, 1)), kept as MX codes in groups of 32 samples; the trainable back stack
+# of 3x3 s1 p1 convolutions (128 -> 256, then 256 -> 256 at 16x16) runs on
+# batches of 128 = 96 replayed + 32 fresh latents.
+QLR_BUFFER = 8192
+QLR_LATENT = (128, 16, 16)
+QLR_BATCH = 128
+QLR_LAYERS = (
+    ("back_3x3_128to256_16", conv_dict(QLR_BATCH, 128, 256, 16, 16, 3, 1, 1)),
+    ("back_3x3_256to256_16", conv_dict(QLR_BATCH, 256, 256, 16, 16, 3, 1, 1)),
+)
+
+
+def qlr_latents(count, seed):
+    """`count` latents (count, 128, 16, 16), fp32."""
+    return silu_normal((count,) + QLR_LATENT, seed)

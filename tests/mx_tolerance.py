@@ -138,3 +138,32 @@ def nt_group_bound(EA, EB, gsize=8):
         s = EA[:, g:g + gsize][:, None, :] + EB[:, g:g + gsize][None, :, :]
         out += np.exp2(s.max(-1))
     return out
+
+
+def gemm_err(got, ref, sabs, gbound=None, tol=1e-5):
+    """Largest |gpu - oracle| as a fraction of the allowed error (<= 1 passes):
+    tol * S, plus 2^-10 * G for the FP8 group truncation when gbound (G) is
+    given.  Outputs with no non-zero products must be exactly zero."""
+    got = got.astype(np.float64)
+    zero = sabs == 0
+    assert np.all(got[zero] == 0), "outputs with no non-zero products must be exactly 0"
+    allowed = tol * sabs
+    if gbound is not None:
+        allowed = allowed + 2.0 ** -10 * gbound
+    nz = ~zero
+    return float(np.max(np.abs(got[nz] - ref[nz]) / allowed[nz])) if nz.any() else 0.0
+
+
+def layer_exponents(o, cv, fmt):
+    """elem_exponents of a layer's X, W and G_Y from the oracle's quantized
+    tensors o = {"x": (codes, scales), "w": ..., "gy": ...}."""
+    import oracle
+    ho = (cv["h"] + 2 * cv["ph"] - cv["kh"]) // cv["sh"] + 1
+    wo = (cv["w"] + 2 * cv["pw"] - cv["kw"]) // cv["sw"] + 1
+    shapes = {"x": (cv["n"], cv["cin"], cv["h"], cv["w"]), "w": (cv["cout"], cv["cin"], cv["kh"], cv["kw"]),
+              "gy": (cv["n"], cv["cout"], ho, wo)}
+    out = {}
+    for k, role in (("x", oracle.ACT), ("w", oracle.WEIGHT), ("gy", oracle.ACT)):
+        d = oracle.dequant(*o[k], role, fmt, *shapes[k])
+        out[k] = elem_exponents(d, o[k][1], role, fmt, shapes[k])
+    return out

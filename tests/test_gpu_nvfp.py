@@ -9,6 +9,7 @@ import numpy as np
 import pytest
 import torch
 
+import mx_tolerance as mxt
 import oracle
 from paper_2609_28358_amd import synth
 
@@ -112,11 +113,7 @@ def _nv_layer(mx, cv, seed, kind="unit"):
 
 
 def _nv_err(got, ref, sabs):
-    got = got.astype(np.float64)
-    zero = sabs == 0
-    assert np.all(got[zero] == 0)
-    nz = ~zero
-    return float(np.max(np.abs(got[nz] - ref[nz]) / (TOL * sabs[nz]))) if nz.any() else 0.0
+    return mxt.gemm_err(got, ref, sabs, tol=TOL)
 
 
 @pytest.mark.parametrize("cv", NV_CONVS, ids=_nv_ids)

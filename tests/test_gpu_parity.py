@@ -144,31 +144,14 @@ def test_im2col(mx, fmt, ci):
 
 
 # ------------------------------------------------------------------ GEMMs
-def _err(got, ref, sabs, gbound=None):
-    """Largest |gpu - oracle| as a fraction of the allowed error (<= 1 passes)."""
-    got = got.astype(np.float64)
-    zero = sabs == 0
-    assert np.all(got[zero] == 0), "outputs with no non-zero products must be exactly 0"
-    tol = TOL * sabs
-    if gbound is not None:
-        tol = tol + 2.0 ** -10 * gbound
-    nz = ~zero
-    return float(np.max(np.abs(got[nz] - ref[nz]) / tol[nz])) if nz.any() else 0.0
+_err = mxt.gemm_err
 
 
 def _all_idx(*dims):
     return np.stack(np.meshgrid(*[np.arange(d) for d in dims], indexing="ij"), -1).reshape(-1, len(dims))
 
 
-def _exps(o, cv, fmt):
-    ho, wo = synth.out_hw(cv)
-    shapes = {"x": (cv["n"], cv["cin"], cv["h"], cv["w"]), "w": (cv["cout"], cv["cin"], cv["kh"], cv["kw"]),
-              "gy": (cv["n"], cv["cout"], ho, wo)}
-    out = {}
-    for k, role in (("x", oracle.ACT), ("w", oracle.WEIGHT), ("gy", oracle.ACT)):
-        d = oracle.dequant(*o[k], role, fmt, *shapes[k])
-        out[k] = mxt.elem_exponents(d, o[k][1], role, fmt, shapes[k])
-    return out
+_exps = mxt.layer_exponents
 
 
 def _layer(mx, cv, fmt, seed, kind="sweep"):
