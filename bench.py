@@ -177,9 +177,31 @@ def cpu_baseline(min_s=10.0, max_steps=8):
                 dt += time.perf_counter() - t0
                 flops += 3 * 2.0 * cv["n"] * cv["cout"] * ho * wo * cv["cin"] * cv["kh"] * cv["kw"]
         steps += 1
-    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.get_threads(), "kind": "oracle",
-            "sample": f"{steps} full step{'s' if steps > 1 else ''} of the benchmark workload (all three layers, MXFP8 and MXFP4, "
-                      f"every op of the path) through the fp64 oracle: {dt:.1f} s"}
+    out = {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.get_threads(), "kind": "oracle",
+           "sample": f"{steps} full step{'s' if steps > 1 else ''} of the benchmark workload (all three layers, MXFP8 and MXFP4, "
+                     f"every op of the path) through the fp64 oracle: {dt:.1f} s"}
+    # the same oracle on one thread, over one layer in one format (about 10 s)
+    threads = oracle.get_threads()
+    oracle.set_threads(1)
+    try:
+        cv, x, w, gy = inputs[0]
+        ho, wo = synth.out_hw(cv)
+        fmt = 1
+        t0 = time.perf_counter()
+        ox = oracle.quantize(x.numpy(), oracle.NCHW, oracle.ACT, fmt, *x.shape)
+        ow = oracle.quantize(w.numpy(), oracle.NCHW, oracle.WEIGHT, fmt, *w.shape)
+        og = oracle.quantize(gy.numpy(), oracle.NCHW, oracle.ACT, fmt, *gy.shape)
+        oracle.im2col_cbf(cv, fmt, *ox)
+        oracle.fwd(cv, fmt, ow, ox)
+        oracle.dgrad(cv, fmt, ow, og)
+        oracle.wgrad(cv, fmt, og, ox)
+        t1 = time.perf_counter() - t0
+    finally:
+        oracle.set_threads(threads)
+    fl1 = 3 * 2.0 * cv["n"] * cv["cout"] * ho * wo * cv["cin"] * cv["kh"] * cv["kw"]
+    out["one_thread"] = {"value": fl1 / t1 / 1e12, "unit": "TFLOP/s", "cores": 1,
+                         "sample": f"the 3x3 s1 64->64 56x56 layer in MXFP4, every op of the path: {t1:.1f} s"}
+    return out
 
 
 def naive_leg(jobs, op_ms, mx, synth, dev, stream, reps=3):
@@ -411,6 +433,22 @@ def main():
         ncopy = min(48, -(-(LLC_BYTES + (64 << 20)) // (base.numel() * base.element_size())))
         return [base] + [base.clone() for _ in range(ncopy - 1)]
 
+    # measured device-copy bandwidth (read + write bytes / time) beside the
+    # 8 TB/s datasheet peak: a graph of back-to-back 256 MiB copies
+    csrc = torch.empty(COPY_BYTES, dtype=torch.uint8, device=dev)
+    cdst = torch.empty_like(csrc)
+    cdst.copy_(csrc)
+    torch.cuda.synchronize()
+    cg = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(cg):
+        for _ in range(8):
+            cdst.copy_(csrc)
+    cg.replay()
+    torch.cuda.synchronize()
+    copy_ms = statistics.median(replay_ms(cg, 3) for _ in range(3)) / 8
+    hbm_copy_gbps = 2 * COPY_BYTES / (copy_ms * 1e-3) / 1e9
+    del cg, csrc, cdst
+
     steady = {}
     for j, op in seq:
         srcs = [None]
@@ -635,6 +673,8 @@ def main():
         ops[f"{nm}/{op}"] = {"ms": round(ms, 4), "ms_alone": round(op_ms[(nm, op)], 4),
                              "tflops": round(fl / (ms * 1e-3) / 1e12, 2) if fl else None,
                              "gbps": round(by / (ms * 1e-3) / 1e9, 1), "bound": r["bound"], "frac": r["frac"]}
+        if fl:   # a GEMM: also its fraction of the MFMA peak, whatever bounds it
+            ops[f"{nm}/{op}"]["mfma_frac"] = round(fl / (ms * 1e-3) / 1e12 / MFMA_TFLOPS[jmap[nm]["fmt"]], 4)
 
     out = {
         "metric": "conv fwd+bwd TFLOPS (MXFP8/MXFP4) + quantize/im2col HBM GB/s, % of roofline",
@@ -649,6 +689,7 @@ def main():
         "roofline": rl,
         "ops": ops,
         "ops_sum_ms": round(sum(steady.values()), 4),
+        "hbm_copy_gbps": round(hbm_copy_gbps, 1),
     }
     if naive:
         out["vs_naive"] = naive
