@@ -145,6 +145,68 @@ def test_encode_matches_brute_force(fmt):
             assert oracle.encode(s, fmt) == _brute_encode(s, fmt), (s, fmt)
 
 
+def _brute_encode_vec(v, fmt):
+    """_brute_encode over an array: nearest grid value of min(|v|, max),
+    ties to the even code, sign bit from the sign of v."""
+    grid = _grid(fmt)
+    codes = np.array([c for c, _ in grid], dtype=np.int64)
+    vals = np.array([g for _, g in grid], dtype=np.float64)
+    order = np.argsort(vals)
+    codes, vals = codes[order], vals[order]
+    a = np.minimum(np.abs(v.astype(np.float64)), MAXV[fmt])
+    hi = np.clip(np.searchsorted(vals, a, side="left"), 1, len(vals) - 1)
+    lo = hi - 1
+    dlo, dhi = a - vals[lo], vals[hi] - a
+    pick_hi = (dhi < dlo) | ((dhi == dlo) & (codes[hi] % 2 == 0))
+    c = np.where(pick_hi, codes[hi], codes[lo])
+    return c | (np.signbit(v).astype(np.int64) << (BITS[fmt] - 1))
+
+
+def _unpack_codes(codes, fmt, count):
+    """All codes of a packed array, in stored order (packing as in _code_at)."""
+    b = codes.astype(np.int64)
+    if fmt == oracle.E4M3:
+        return b[:count]
+    if BITS[fmt] == 4:
+        return np.stack([b & 0xF, b >> 4], 1).reshape(-1)[:count]
+    b = b[:count // 4 * 3].reshape(-1, 3)
+    c = np.stack([b[:, 0] & 63, (b[:, 0] >> 6) | ((b[:, 1] & 15) << 2),
+                  (b[:, 1] >> 4) | ((b[:, 2] & 3) << 4), b[:, 2] >> 2], 1)
+    return c.reshape(-1)[:count]
+
+
+@pytest.mark.parametrize("fmt", ALL_FMTS)
+def test_encode_brute_force_ten_million(fmt):
+    """10^7 random values through the tensor quantizer with every block scale
+    forced to 2^0 (an anchor 1.5 * 2^emax per block, all else below 2^(emax+1)),
+    so each code is encode(x) itself, against the nearest-value search."""
+    blocks = 9766                                        # 32 x 32 elements each: >= 10^7 values
+    rng = np.random.default_rng(100 + fmt)
+    top = 2.0 ** (EMAX[fmt] + 1)
+    n = blocks * 1024
+    lin = (rng.random(n) * 2 - 1) * top                  # the whole range, saturation included
+    sub = np.exp2(rng.uniform(EMAX[fmt] - 14, EMAX[fmt] + 1, n)) * np.where(rng.random(n) < 0.5, -1, 1)
+    v = np.where(rng.random(n) < 0.5, lin, sub).astype(np.float32)
+    v = np.where(np.abs(v) >= top, np.float32(0.0), v)  # keep every |x| < 2^(emax+1)
+    grid = sorted(g for _, g in _grid(fmt))
+    special = []                                         # grid values, midpoints (ties) and their neighbours
+    for lo_, hi_ in zip(grid[:-1], grid[1:]):
+        m = np.float32((lo_ + hi_) / 2)
+        special += [lo_, m, np.nextafter(m, np.float32(-1)), np.nextafter(m, np.float32(top))]
+    special += [MAXV[fmt], np.nextafter(np.float32(top), np.float32(0))]
+    special = np.array(special, dtype=np.float32)
+    special = np.concatenate([special, -special])
+    v[1:1 + special.size] = special                      # inside the first block, clear of its anchor
+    v = v.reshape(blocks, 32, 32)                        # CBF: [pixel][channel][sample]
+    v[:, 0, 0] = 1.5 * 2.0 ** EMAX[fmt]
+    codes, scales = oracle.quantize(v.reshape(-1), oracle.CBF, oracle.ACT, fmt, 32, 32, 1, blocks)
+    assert np.all(scales == 127)
+    got = _unpack_codes(codes, fmt, n)
+    want = _brute_encode_vec(v.reshape(-1), fmt)
+    bad = np.flatnonzero(got != want)
+    assert bad.size == 0, (bad[:5], v.reshape(-1)[bad[:5]], got[bad[:5]], want[bad[:5]])
+
+
 def test_encode_e4m3_matches_torch_cast():
     rng = np.random.default_rng(11)
     mag = 2.0 ** rng.uniform(-14, 9.2, size=20000)
