@@ -43,7 +43,8 @@ def build(verbose=False):
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr}")
     # a kernel instantiation the host pass dropped shows up as an undefined
-    # symbol only when the library is loaded: load it here, not on the GPU machine
+    # symbol only when the library is loaded: load it at build time, so such
+    # a library is never installed
     import ctypes
     try:
         ctypes.CDLL(tmp)
