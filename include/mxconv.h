@@ -76,8 +76,10 @@
  * Conventions for every entry point
  *   - Device pointers are caller-owned (allocated by the caller, e.g. as
  *     PyTorch tensors); the library never allocates, frees or synchronizes
- *     and keeps no global state.  All pointers to device memory must be
- *     16-byte aligned.
+ *     and keeps no state between calls beyond, per device, whether a kernel's
+ *     large-LDS launch attribute has been raised (set once, safe to race).
+ *     Calls from several host threads are safe.  All pointers to device
+ *     memory must be 16-byte aligned.
  *   - Work is enqueued on `stream` (a hipStream_t passed as void*; NULL is
  *     the default stream) and runs asynchronously.
  *   - Arguments are validated on the host before anything is launched; a

@@ -31,6 +31,8 @@
 // reused by every tap that reaches it.  The MFMAs compute the transposed
 // tile (samples x channels) so that each lane ends up holding four
 // consecutive samples of one channel: one 16-byte store in the CBF layout.
+#include <atomic>
+
 #include "mx_internal.h"
 
 namespace mxc {
@@ -645,13 +647,22 @@ inline size_t lean_lds(const LeanArgs& a, int nbufs_used) {
     return lds < 4 * 4096 ? 4 * 4096 : lds;
 }
 
+// Dynamic LDS above 64 KB needs the kernel's attribute raised, once per
+// device: `devs` holds one bit per device that has it (devices past the 64th
+// raise it on every launch).  Concurrent first calls may both raise it, which
+// is harmless.
 template <typename K>
-int lean_launch(K kernel, bool& attr, const LeanArgs& a, int ntiles, size_t lds, hipStream_t s) {
-    if (lds > 65536 && !attr) {
-        if (hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, LDS_MAX) !=
-            hipSuccess)
-            return MXC_ERR_HIP;
-        attr = true;
+int lean_launch(K kernel, std::atomic<uint64_t>& devs, const LeanArgs& a, int ntiles, size_t lds, hipStream_t s) {
+    if (lds > 65536) {
+        int dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess) return MXC_ERR_HIP;
+        const uint64_t bit = dev < 64 ? (uint64_t)1 << dev : 0;
+        if (!bit || !(devs.load(std::memory_order_acquire) & bit)) {
+            if (hipFuncSetAttribute((const void*)kernel, hipFuncAttributeMaxDynamicSharedMemorySize, LDS_MAX) !=
+                hipSuccess)
+                return MXC_ERR_HIP;
+            devs.fetch_or(bit, std::memory_order_release);
+        }
     }
     const int grid = (ntiles + 7) / 8 * 8;
     hipLaunchKernelGGL(kernel, dim3(grid), dim3(LT), lds, s, a);
@@ -660,14 +671,14 @@ int lean_launch(K kernel, bool& attr, const LeanArgs& a, int ntiles, size_t lds,
 
 template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW, bool NV = false>
 int launch_lean_t(const LeanArgs& a, int nbufs_used, hipStream_t s) {
-    static bool attr = false;
-    return lean_launch(conv_lean_kernel<FW, FX, DG, KW, S, WGM, PW, NV>, attr, a, a.ntiles, lean_lds(a, nbufs_used), s);
+    static std::atomic<uint64_t> devs{0};
+    return lean_launch(conv_lean_kernel<FW, FX, DG, KW, S, WGM, PW, NV>, devs, a, a.ntiles, lean_lds(a, nbufs_used), s);
 }
 
 template <int FW, int FX, int KWF, int PW, bool NV = false>
 int launch_lean_dg2(const LeanArgs& a, int nbufs_used, hipStream_t s) {
-    static bool attr = false;
-    return lean_launch(conv_lean_dg2_kernel<FW, FX, KWF, 1, PW, NV>, attr, a, a.pofs[4], lean_lds(a, nbufs_used), s);
+    static std::atomic<uint64_t> devs{0};
+    return lean_launch(conv_lean_dg2_kernel<FW, FX, KWF, 1, PW, NV>, devs, a, a.pofs[4], lean_lds(a, nbufs_used), s);
 }
 
 // (WGM, PW) in use: (1, 1), (1, 2), (2, 2), (4, 2); the NV kernels run (1, 1)
