@@ -585,7 +585,7 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                 for (int i = 0; i < 4; i++) {
                     const int row = er + 8 * i;
                     const float4 v = *(const float4*)(ep + row * 128 + ((ec ^ (row & 7)) << 4));
-                    if (m0 + row < p.M) *(float4*)(o + row * 32 + 4 * ec) = v;
+                    if (m0 + row < p.M) store_nt(o + row * 32 + 4 * ec, v);
                 }
             }
         } else {

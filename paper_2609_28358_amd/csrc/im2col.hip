@@ -4,7 +4,7 @@
 // X'[g][ho][wo][kh][kw][Cp][Bn] = X[g][ho*sh+kh-ph][wo*sw+kw-pw][Cp][Bn]:
 // for one (group, output pixel, tap) the destination run and the source
 // pixel's run are both Cp*Bn codes long and contiguous, so the kernel is a
-// 16-byte-vector copy (one chunk per thread); blocks stay whole, so nothing is requantized, and
+// 16-byte-vector copy (one chunk per thread, non-temporal stores); blocks stay whole, so nothing is requantized, and
 // padding taps become zero codes with scale code 0.  Pure HBM stream:
 // |X'| codes written, the source re-read from L2/MALL across taps.
 #include "mx_internal.h"
@@ -35,7 +35,7 @@ __global__ __launch_bounds__(256) void im2col_kernel(const uint4* __restrict__ s
     const bool inside = ih >= 0 && ih < cv.h && iw >= 0 && iw < cv.w;
     const size_t srun = ((size_t)g * cv.h + (inside ? ih : 0)) * cv.w + (inside ? iw : 0);
     const size_t run = ((size_t)blockIdx.y * cv.wo + ow) * (cv.kh * cv.kw) + tap;
-    dst[run * run16 + within] = inside ? __ldg(src + srun * run16 + within) : make_uint4(0, 0, 0, 0);
+    store_nt(dst + run * run16 + within, inside ? __ldg(src + srun * run16 + within) : make_uint4(0, 0, 0, 0));
     const int ncb = cv.x.ncb;
     if (within < ncb) sdst[run * ncb + within] = inside ? ssrc[srun * ncb + within] : 0;
 }
