@@ -269,9 +269,9 @@ __device__ __forceinline__ void quantize_block16(const void* __restrict__ src, c
 #pragma unroll
         for (int q = 0; q < 4; q++) {
             if (DTYPE == MXC_F32) {
-                x[q] = __ldg((const float4*)((const float*)src + i0 + 4 * q));
+                x[q] = load_nt((const float*)src + i0 + 4 * q);
             } else {
-                const uint2 b = __ldg((const uint2*)((const unsigned short*)src + i0 + 4 * q));
+                const uint2 b = load_nt((const unsigned short*)src + i0 + 4 * q);
                 x[q] = make_float4(__uint_as_float(b.x << 16), __uint_as_float(b.x & 0xFFFF0000u),
                                    __uint_as_float(b.y << 16), __uint_as_float(b.y & 0xFFFF0000u));
             }
@@ -365,9 +365,9 @@ __device__ __forceinline__ void quantize_block_body(const void* __restrict__ src
             const bool ok = c < g.c;
             const size_t i = ((size_t)rest * g.c + (ok ? c : 0)) * 32 + j;
             if (DTYPE == MXC_F32) {
-                x[q] = __ldg((const float4*)((const float*)src + i));
+                x[q] = load_nt((const float*)src + i);
             } else {
-                const uint2 b = __ldg((const uint2*)((const unsigned short*)src + i));
+                const uint2 b = load_nt((const unsigned short*)src + i);
                 x[q] = make_float4(__uint_as_float(b.x << 16), __uint_as_float(b.x & 0xFFFF0000u),
                                    __uint_as_float(b.y << 16), __uint_as_float(b.y & 0xFFFF0000u));
             }
