@@ -5,10 +5,10 @@ One step = one pass of the whole path over the layer sweep (batch 32, inputs
 resident in HBM): for each layer
     3x3 s1 p1 64->64 at 56x56,  1x1 64->256 at 56x56,  3x3 s2 p1 128->256 at 28x28
 and each format (MXFP8 E4M3, MXFP4 E2M1): quantize X, W and G_Y once
-(activations arrive channel-batch-first in fp32, weights OIHW fp32; X and W,
-the forward operands, in one call and one launch), the explicit CBF im2col
-of X, then the forward, input-gradient and weight-gradient GEMMs: 42
-kernels.  Activations are SiLU(N(0,1)), weights Kaiming-normal,
+(activations arrive channel-batch-first in fp32, weights OIHW fp32), with the
+explicit CBF im2col of X written by the same launch that quantizes X and W
+(the forward operands), then the forward, input-gradient and weight-gradient
+GEMMs: 36 kernels.  Activations are SiLU(N(0,1)), weights Kaiming-normal,
 gradients N(0, 1e-3), all seeded.
 
 `value` is the conv fwd+bwd GEMM throughput of the whole step: the three
@@ -23,8 +23,9 @@ the stream its kernels run on and bracketed by HIP events (median of
 rounds); quantize launches rotate over enough copies of their fp32 source
 that it is read from HBM, not from the 256 MB last-level cache -- and
 `ms_alone`, one eager launch bracketed by HIP events behind a GPU spin
-(launch and event overhead included).  The op with the largest `ms` gets the
-`roofline` object.
+(launch and event overhead included).  The op of the step with the largest
+`ms` gets the `roofline` object.  The unfused X+W quantize and the standalone
+im2col kernel are timed too (`in_step` false), outside the step.
 
     python bench.py [--steps K] [--warmup W] [--no-cpu-baseline]
 """
@@ -70,6 +71,8 @@ def layer_numbers(cv, fmt, mx):
         "quant_x": (0.0, 4.0 * n * ci * cv["h"] * cv["w"] + X),
         "quant_w": (0.0, 4.0 * co * ci * kh * kw + W),
         "quant_xw": (0.0, 4.0 * n * ci * cv["h"] * cv["w"] + X + 4.0 * co * ci * kh * kw + W),
+        # X and W quantized in one launch that also writes X's CBF im2col
+        "quant_xw_im2col": (0.0, 4.0 * n * ci * cv["h"] * cv["w"] + X + 4.0 * co * ci * kh * kw + W + XC),
         "quant_gy": (0.0, 4.0 * n * co * ho * wo + G),
         "im2col": (0.0, X + XC),
         "fwd": (flops, W + X + 4.0 * n * co * ho * wo),
@@ -318,12 +321,21 @@ def main():
             jobs.append(j)
 
     stream = torch.cuda.current_stream()
-    # a layer's forward operands X and W are quantized together (one launch)
-    OPS = ("quant_xw", "quant_gy", "im2col", "fwd", "dgrad", "wgrad")
+    # a layer's forward operands X and W are quantized together, in one launch
+    # that also writes X's explicit CBF im2col (the quantizer copies each block
+    # to its im2col positions as it produces it)
+    OPS = ("quant_xw_im2col", "quant_gy", "fwd", "dgrad", "wgrad")
+    # timed beside the step, not part of it: the unfused forward-operand
+    # quantize and the standalone im2col kernel
+    REF_OPS = ("quant_xw", "im2col")
 
     def run_op(j, op, src=None):
         cv, fmt = j["cv"], j["fmt"]
-        if op == "quant_xw":
+        if op == "quant_xw_im2col":
+            mx.quantize_multi([(j["x"] if src is None else src, mx.ACT, fmt, mx.CBF, j["xs"], j["qx"],
+                                (cv, j["col"][0], j["col"][1])),
+                               (j["w"], mx.WEIGHT, fmt, mx.NCHW, tuple(j["w"].shape), j["qw"])])
+        elif op == "quant_xw":
             mx.quantize_multi([(j["x"] if src is None else src, mx.ACT, fmt, mx.CBF, j["xs"], j["qx"]),
                                (j["w"], mx.WEIGHT, fmt, mx.NCHW, tuple(j["w"].shape), j["qw"])])
         elif op == "quant_x":
@@ -395,7 +407,7 @@ def main():
         torch.cuda.synchronize()
         return sum(a.elapsed_time(b) for a, b in marks) / reps
 
-    op_ms = {(j["name"], op): op_time(j, op) for j, op in seq}
+    op_ms = {(j["name"], op): op_time(j, op) for j, op in seq + [(j, op) for j in jobs for op in REF_OPS]}
 
     # The step is launched as one HIP graph (captured once), so host-side
     # launch cost does not enter the step time.
@@ -450,10 +462,10 @@ def main():
     del cg, csrc, cdst
 
     steady = {}
-    for j, op in seq:
+    for j, op in seq + [(j, op) for j in jobs for op in REF_OPS]:
         srcs = [None]
-        if op in ("quant_xw", "quant_x", "quant_gy"):
-            srcs = rotated(j["x"] if op in ("quant_xw", "quant_x") else j["gy"])
+        if op in ("quant_xw_im2col", "quant_xw", "quant_x", "quant_gy"):
+            srcs = rotated(j["gy"] if op == "quant_gy" else j["x"])
         kl = max(12, len(srcs))
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
@@ -463,7 +475,8 @@ def main():
         torch.cuda.synchronize()
         steady[(j["name"], op)] = statistics.median(replay_ms(g, 3) for _ in range(3)) / kl
         del g, srcs
-    dom = max(steady, key=steady.get)
+    in_step = {(j["name"], op) for j, op in seq}
+    dom = max(in_step, key=steady.get)
     dom_ms = steady[dom]
 
     naive = {} if args.no_naive else naive_leg(jobs, op_ms, mx, synth, dev, stream)
@@ -672,7 +685,8 @@ def main():
         r = roof(jmap[nm], op, ms)
         ops[f"{nm}/{op}"] = {"ms": round(ms, 4), "ms_alone": round(op_ms[(nm, op)], 4),
                              "tflops": round(fl / (ms * 1e-3) / 1e12, 2) if fl else None,
-                             "gbps": round(by / (ms * 1e-3) / 1e9, 1), "bound": r["bound"], "frac": r["frac"]}
+                             "gbps": round(by / (ms * 1e-3) / 1e9, 1), "bound": r["bound"], "frac": r["frac"],
+                             "in_step": (nm, op) in in_step}
         if fl:   # a GEMM: also its fraction of the MFMA peak, whatever bounds it
             ops[f"{nm}/{op}"]["mfma_frac"] = round(fl / (ms * 1e-3) / 1e12 / MFMA_TFLOPS[jmap[nm]["fmt"]], 4)
 
@@ -682,13 +696,13 @@ def main():
         "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "mxfp8+mxfp4 (fp32 accumulate)", "data": "synthetic",
         "config": {"workload": "conv layer sweep, batch 32: 3x3 s1 64->64 56x56, 1x1 64->256 56x56, "
-                               "3x3 s2 128->256 28x28; each in MXFP8 and MXFP4; quantize X+W (one launch) + G_Y + im2col + fwd + "
-                               "dgrad + wgrad per layer",
+                               "3x3 s2 128->256 28x28; each in MXFP8 and MXFP4; quantize X+W with X's CBF im2col (one "
+                               "launch) + quantize G_Y + fwd + dgrad + wgrad per layer",
                    "global_batch": 32, "layers": [n for n, _ in synth.SWEEP_LAYERS], "formats": ["mxfp8", "mxfp4"],
                    "parallelism": "single GPU"},
         "roofline": rl,
         "ops": ops,
-        "ops_sum_ms": round(sum(steady.values()), 4),
+        "ops_sum_ms": round(sum(steady[k] for k in in_step), 4),
         "hbm_copy_gbps": round(hbm_copy_gbps, 1),
     }
     if naive:

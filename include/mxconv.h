@@ -158,15 +158,32 @@ int mxconv_quantize(const void* src, int dtype, int layout, int role, int fmt,
  * that read a channel-batch-first activation with batch block 32 or OIHW
  * weights share one launch, any other job gets a launch of its own.  The
  * jobs' outputs must not overlap.
+ *
+ * A job may also ask for the channel-batch-first im2col of its activation
+ * (a2): with `conv` non-NULL, `col_codes` / `col_scales` receive exactly
+ * what mxconv_im2col_cbf(conv, fmt, codes, scales, ...) would write (layout
+ * and sizes there).  For FP8 / FP4 activations read from the CBF layout with
+ * batch block 32, the quantizer writes each block to its im2col positions as
+ * it produces it (one launch for quantize and im2col, the codes not read
+ * back); the wave of the block at pixel (y, x) also writes the zero blocks
+ * of the padding taps of output pixel (y, x), which needs Ho <= h and
+ * Wo <= w.  Any other such job is quantized and then copied by the im2col
+ * kernel (a launch of its own after the quantizations).
  *   count  0 .. MXC_QMULTI_MAX;  jobs  host array of count descriptors.
+ *   conv   NULL, or the layer whose input this job's tensor is: role
+ *          MXC_ACT and (n, cin, h, w) equal to the job's (n, c, h, w).
  * Errors: as mxconv_quantize (checked for every job before anything is
- * launched), ARG for a count out of range. */
+ * launched), ARG for a count out of range, SHAPE for a conv that does not
+ * match its job. */
 #define MXC_QMULTI_MAX 8
 typedef struct mxc_qjob {
     const void* src;
     int dtype, layout, role, fmt, n, c, h, w;
     void* codes;
     uint8_t* scales;
+    const mxc_conv* conv;         /* optional im2col of the activation (NULL: none) */
+    void* col_codes;
+    uint8_t* col_scales;
 } mxc_qjob;
 int mxconv_quantize_multi(int count, const mxc_qjob* jobs, void* stream);
 

@@ -42,14 +42,22 @@ __global__ __launch_bounds__(256) void im2col_kernel(const uint4* __restrict__ s
 
 }  // namespace
 
-int launch_im2col(const Conv& cv, const void* xc, const uint8_t* xs, void* cc, uint8_t* cs,
-                  hipStream_t s) {
-    const long run_bytes = (long)cv.x.cp * cv.x.bn * cv.x.bits / 8;   // a multiple of 16 (FP6: Bn >= 4)
-    const int run16 = (int)(run_bytes / 16);
+int im2col_check(const Conv& cv) {
+    const long run16 = (long)cv.x.cp * cv.x.bn * cv.x.bits / 8 / 16;   // run bytes: a multiple of 16 (FP6: Bn >= 4)
     const long row = (long)cv.wo * run16;            // chunks of one output row, one tap
     const long rows = (long)cv.x.ng * cv.ho;
     if (row > 0x7FFFFFFFL - 256 || rows > 0x7FFFFFFFL || cv.kh * cv.kw > 65535 || cv.x.ncb > run16)
         return MXC_ERR_SHAPE;
+    return MXC_OK;
+}
+
+int launch_im2col(const Conv& cv, const void* xc, const uint8_t* xs, void* cc, uint8_t* cs,
+                  hipStream_t s) {
+    const int rc = im2col_check(cv);
+    if (rc) return rc;
+    const int run16 = (int)((long)cv.x.cp * cv.x.bn * cv.x.bits / 8 / 16);
+    const long row = (long)cv.wo * run16;
+    const long rows = (long)cv.x.ng * cv.ho;
     int log2run = -1;
     for (int k = 0; k < 31; k++)
         if ((1 << k) == run16) log2run = k;

@@ -57,6 +57,7 @@ int conv_init(Conv* cv, const mxc_conv* p, int fmt, int op = CONV_ONE);
 // seed != NULL: elements rounded stochastically with that Philox key
 int launch_quantize(const void* src, int dtype, int layout, int role, const Geom& g, int fmt,
                     void* codes, uint8_t* scales, hipStream_t s, const uint64_t* seed = nullptr);
+int im2col_check(const Conv& cv);     // MXC_ERR_SHAPE for sizes the im2col kernel cannot index
 int launch_im2col(const Conv& cv, const void* xc, const uint8_t* xs, void* cc, uint8_t* cs,
                   hipStream_t s);
 // several quantizations, one launch for those of the one-wave-per-block kind
@@ -66,6 +67,10 @@ struct QuantJob {
     Geom g;
     void* codes;
     uint8_t* scales;
+    bool col;                     // also write the CBF im2col of this activation
+    Conv cv;                      // (col) the layer it is the input of
+    void* col_codes;
+    uint8_t* col_scales;
 };
 int launch_quantize_multi(int count, const QuantJob* jobs, hipStream_t s);
 // NVFP (nvfp.hip): partial maxima in the workspace (NVFP_PARTS words at most)
@@ -140,6 +145,11 @@ __device__ __forceinline__ void store_nt(void* p, uint4 v) {
     v4i t;
     t[0] = (int)v.x; t[1] = (int)v.y; t[2] = (int)v.z; t[3] = (int)v.w;
     __builtin_nontemporal_store(t, (v4i*)p);
+}
+__device__ __forceinline__ void store_nt(void* p, uint2 v) {
+    v2i t;
+    t[0] = (int)v.x; t[1] = (int)v.y;
+    __builtin_nontemporal_store(t, (v2i*)p);
 }
 __device__ __forceinline__ void store_nt(void* p, float4 v) {
     store_nt(p, make_uint4(__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z), __float_as_uint(v.w)));

@@ -150,6 +150,17 @@ int mxconv_quantize_multi(int count, const mxc_qjob* jobs, void* stream) {
         if (!aligned16(j.src) || !aligned16(j.codes) || !aligned16(j.scales)) return MXC_ERR_ALIGN;
         q[i].src = j.src; q[i].dtype = j.dtype; q[i].layout = j.layout; q[i].role = j.role; q[i].fmt = j.fmt;
         q[i].codes = j.codes; q[i].scales = j.scales;
+        q[i].col = j.conv != nullptr;
+        q[i].col_codes = j.col_codes; q[i].col_scales = j.col_scales;
+        if (q[i].col) {
+            if (!j.col_codes || !j.col_scales) return MXC_ERR_NULL;
+            const mxc_conv& p = *j.conv;
+            if (j.role != MXC_ACT || p.n != j.n || p.cin != j.c || p.h != j.h || p.w != j.w) return MXC_ERR_SHAPE;
+            int rc2 = conv_init(&q[i].cv, j.conv, j.fmt);
+            if (!rc2) rc2 = im2col_check(q[i].cv);
+            if (rc2) return rc2;
+            if (!aligned16(j.col_codes) || !aligned16(j.col_scales)) return MXC_ERR_ALIGN;
+        }
     }
     return launch_quantize_multi(count, q, (hipStream_t)stream);
 }

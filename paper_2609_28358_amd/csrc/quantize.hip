@@ -347,10 +347,96 @@ __device__ __forceinline__ void quantize_block16(const void* __restrict__ src, c
     }
 }
 
+// Optional im2col output of a CBF activation quantized one block per wave
+// (Sec. IV-A: the quantized blocks are what the channel-batch-first im2col
+// moves).  The wave of block (group gi, pixel (y, x), channel block cb) copies
+// its codes and scale to every im2col position (output pixel, tap) whose
+// source pixel is (y, x), and writes the zero blocks of the padding taps of
+// output pixel (y, x) itself; with Ho <= h and Wo <= w every output pixel has
+// such a wave, so every im2col block is written exactly once.  All indices are
+// wave-uniform.  Layout as mxconv_im2col_cbf: [Np/32][Ho][Wo][Kh][Kw][Cp][32].
+struct ColOut {
+    uint8_t* codes;                // nullptr: no im2col output
+    uint8_t* scales;
+    int ho, wo, kh, kw, sh, sw, ph, pw;
+};
+
+// One im2col block: the wave's 16 (FP8) or 8 (FP4) contiguous code bytes per
+// lane, or zeros, and the scale byte.
+template <int FMT>
+__device__ __forceinline__ void col_put(const ColOut& col, size_t bi, int lane, uint4 v, uint32_t sc, bool zero) {
+    if constexpr (FMT == MXC_E4M3)
+        store_nt(col.codes + bi * 1024 + 16 * lane, zero ? make_uint4(0u, 0u, 0u, 0u) : v);
+    else
+        store_nt(col.codes + bi * 512 + 8 * lane, zero ? make_uint2(0u, 0u) : make_uint2(v.x, v.y));
+    if (lane == 0) col.scales[bi] = zero ? (uint8_t)0 : (uint8_t)sc;
+}
+
+template <int FMT>
+__device__ __forceinline__ void col_scatter(const ColOut& col, const Geom& g, int blk, int lane,
+                                            const uint32_t* wq, uint32_t sc) {
+    // the quantizer leaves lane l with the codes of rows 8 q + l / 8 (q = 0..3);
+    // one pass through 1 KB of LDS gives each lane 16 (FP8) or 8 (FP4)
+    // consecutive bytes of the stored block, so each copy is one wide store.
+    // LDS operations of a wave complete in order: waiting for the writes
+    // (and keeping the compiler from moving the read above them) suffices.
+    __shared__ __attribute__((aligned(16))) uint32_t stage[QT / 64][256];
+    uint32_t* st = stage[threadIdx.x >> 6];
+    if constexpr (FMT == MXC_E4M3) {
+#pragma unroll
+        for (int q = 0; q < 4; q++) st[lane + 64 * q] = wq[q];
+    } else {
+#pragma unroll
+        for (int q = 0; q < 4; q++) ((unsigned short*)st)[lane + 64 * q] = (unsigned short)wq[q];
+    }
+    __asm__ volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    uint4 v;
+    if constexpr (FMT == MXC_E4M3) {
+        v = ((const uint4*)st)[lane];
+    } else {
+        const uint2 h = ((const uint2*)st)[lane];
+        v = make_uint4(h.x, h.y, 0u, 0u);
+    }
+    const int cb = blk % g.ncb;
+    int r = blk / g.ncb;
+    const int x = r % g.w;
+    r /= g.w;
+    const int y = r % g.h, gi = r / g.h;
+    const int taps = col.kh * col.kw;
+    auto block = [&](int oh, int ow, int tap) {
+        return ((((size_t)gi * col.ho + oh) * col.wo + ow) * taps + tap) * g.ncb + cb;
+    };
+    for (int a = 0; a < col.kh; a++) {                   // output rows whose tap row a reads y
+        const int t = y + col.ph - a;
+        if (t < 0) break;
+        if (t % col.sh) continue;
+        const int oh = t / col.sh;
+        if (oh >= col.ho) continue;
+        for (int b = 0; b < col.kw; b++) {
+            const int u = x + col.pw - b;
+            if (u < 0) break;
+            if (u % col.sw) continue;
+            const int ow = u / col.sw;
+            if (ow < col.wo) col_put<FMT>(col, block(oh, ow, a * col.kw + b), lane, v, sc, false);
+        }
+    }
+    if (y < col.ho && x < col.wo) {                      // padding taps of output pixel (y, x)
+        for (int a = 0; a < col.kh; a++) {
+            const int iy = y * col.sh + a - col.ph;
+            const bool rowout = iy < 0 || iy >= g.h;
+            for (int b = 0; b < col.kw; b++) {
+                const int ix = x * col.sw + b - col.pw;
+                if (rowout || ix < 0 || ix >= g.w) col_put<FMT>(col, block(y, x, a * col.kw + b), lane, v, sc, true);
+            }
+        }
+    }
+}
+
 template <int SRC, int DTYPE, int FMT, bool SR>
 __device__ __forceinline__ void quantize_block_body(const void* __restrict__ src, const Geom& g,
                                                     uint8_t* __restrict__ codes, uint8_t* __restrict__ scales,
-                                                    int blk, int lane, uint32_t k0, uint32_t k1) {
+                                                    int blk, int lane, uint32_t k0, uint32_t k1,
+                                                    const ColOut* col = nullptr) {
     if constexpr (SR || fmt_bits(FMT) == 6) {
         quantize_block16<SRC, DTYPE, FMT, SR>(src, g, codes, scales, blk, lane, k0, k1);
         return;
@@ -403,15 +489,23 @@ __device__ __forceinline__ void quantize_block_body(const void* __restrict__ src
     if (lane == 0) scales[blk] = (uint8_t)sc;
     const float inv = inv_scale(sc);
     const bool bad = sc == 0xFFu;
+    uint32_t wq[4];                                          // the lane's codes of rows 8 q + lane / 8
     if (FMT == MXC_E4M3) {
         uint32_t* d = (uint32_t*)(codes + (size_t)blk * 1024) + lane;
 #pragma unroll
-        for (int q = 0; q < 4; q++) d[64 * q] = bad ? 0u : pack4_e4m3(x[q], inv);
+        for (int q = 0; q < 4; q++) {
+            wq[q] = bad ? 0u : pack4_e4m3(x[q], inv);
+            d[64 * q] = wq[q];
+        }
     } else {
         unsigned short* d = (unsigned short*)(codes + (size_t)blk * 512) + lane;
 #pragma unroll
-        for (int q = 0; q < 4; q++) d[64 * q] = bad ? (unsigned short)0 : pack4_e2m1(x[q], inv);
+        for (int q = 0; q < 4; q++) {
+            wq[q] = bad ? 0u : pack4_e2m1(x[q], inv);
+            d[64 * q] = (unsigned short)wq[q];
+        }
     }
+    if (SRC == 0 && col && col->codes) col_scatter<FMT>(*col, g, blk, lane, wq, sc);
 }
 
 template <int SRC, int DTYPE, int FMT, bool SR>
@@ -436,6 +530,7 @@ struct QJob {
     Geom g;
     int kind, dtype, fmt;          // kind 0: CBF activation, 1: OIHW weights
     int blk0, nblocks;
+    ColOut col;                    // kind 0, FP8 / FP4: optional im2col output
 };
 constexpr int QMULTI_MAX = 8;
 struct QMulti {
@@ -445,7 +540,7 @@ struct QMulti {
 
 template <int SRC>
 __device__ __forceinline__ void qmulti_dispatch(const QJob& q, int blk, int lane) {
-#define QM_CASE(D, F) quantize_block_body<SRC, D, F, false>(q.src, q.g, q.codes, q.scales, blk, lane, 0u, 0u)
+#define QM_CASE(D, F) quantize_block_body<SRC, D, F, false>(q.src, q.g, q.codes, q.scales, blk, lane, 0u, 0u, &q.col)
     if (q.dtype == MXC_F32) {
         switch (q.fmt) {
             case MXC_E4M3: QM_CASE(MXC_F32, MXC_E4M3); break;
@@ -552,6 +647,8 @@ int launch_quantize_multi(int count, const QuantJob* jobs, hipStream_t s) {
     QMulti m;
     int nq = 0;
     long long nb = 0;
+    int deferred[QMULTI_MAX];      // jobs whose im2col runs as its own launch afterwards
+    int nd = 0;
     for (int i = 0; i < count; i++) {
         const QuantJob& q = jobs[i];
         const bool block = (q.layout == MXC_CBF && q.role == MXC_ACT && q.g.bn == 32) ||
@@ -561,20 +658,39 @@ int launch_quantize_multi(int count, const QuantJob* jobs, hipStream_t s) {
             // a tensor of another kind: its own launch
             const int rc = launch_quantize(q.src, q.dtype, q.layout, q.role, q.g, q.fmt, q.codes, q.scales, s);
             if (rc) return rc;
+            if (q.col) deferred[nd++] = i;
             continue;
         }
         QJob& d = m.j[nq++];
         d.src = q.src; d.codes = (uint8_t*)q.codes; d.scales = q.scales; d.g = q.g;
         d.kind = q.role == MXC_WEIGHT ? 1 : 0; d.dtype = q.dtype; d.fmt = q.fmt;
         d.blk0 = (int)nb; d.nblocks = (int)qb;
+        d.col.codes = nullptr; d.col.scales = nullptr;
+        if (q.col) {
+            // fused: FP8 / FP4 activation blocks, and an output no larger than the input
+            if ((q.fmt == MXC_E4M3 || q.fmt == MXC_E2M1) && q.cv.ho <= q.g.h && q.cv.wo <= q.g.w) {
+                d.col.codes = (uint8_t*)q.col_codes; d.col.scales = q.col_scales;
+                d.col.ho = q.cv.ho; d.col.wo = q.cv.wo; d.col.kh = q.cv.kh; d.col.kw = q.cv.kw;
+                d.col.sh = q.cv.sh; d.col.sw = q.cv.sw; d.col.ph = q.cv.ph; d.col.pw = q.cv.pw;
+            } else {
+                deferred[nd++] = i;
+            }
+        }
         nb += qb;
     }
-    if (nq == 0) return MXC_OK;
-    m.count = nq;
-    m.nblocks = (int)nb;
-    for (int i = nq; i < QMULTI_MAX; i++) m.j[i] = m.j[nq - 1];
-    hipLaunchKernelGGL(quantize_multi_kernel, dim3((unsigned)((nb + 3) / 4)), dim3(QT), 0, s, m);
-    return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
+    if (nq > 0) {
+        m.count = nq;
+        m.nblocks = (int)nb;
+        for (int i = nq; i < QMULTI_MAX; i++) m.j[i] = m.j[nq - 1];
+        hipLaunchKernelGGL(quantize_multi_kernel, dim3((unsigned)((nb + 3) / 4)), dim3(QT), 0, s, m);
+        if (hipGetLastError() != hipSuccess) return MXC_ERR_HIP;
+    }
+    for (int k = 0; k < nd; k++) {
+        const QuantJob& q = jobs[deferred[k]];
+        const int rc = launch_im2col(q.cv, q.codes, q.scales, q.col_codes, q.col_scales, s);
+        if (rc) return rc;
+    }
+    return MXC_OK;
 }
 
 int launch_quantize(const void* src, int dtype, int layout, int role, const Geom& g, int fmt, void* codes,

@@ -25,12 +25,6 @@ class MxconvError(RuntimeError):
     pass
 
 
-class MxcQJob(ctypes.Structure):
-    _fields_ = [("src", ctypes.c_void_p)] + [(k, ctypes.c_int32) for k in
-                                           ("dtype", "layout", "role", "fmt", "n", "c", "h", "w")] + \
-               [("codes", ctypes.c_void_p), ("scales", ctypes.c_void_p)]
-
-
 QMULTI_MAX = 8
 FP6_SLACK = 16          # bytes of read slack at the end of an FP6 code buffer
 
@@ -38,6 +32,13 @@ FP6_SLACK = 16          # bytes of read slack at the end of an FP6 code buffer
 class MxcConv(ctypes.Structure):
     _fields_ = [(k, ctypes.c_int32) for k in
                 ("n", "cin", "cout", "h", "w", "kh", "kw", "sh", "sw", "ph", "pw")]
+
+
+class MxcQJob(ctypes.Structure):
+    _fields_ = [("src", ctypes.c_void_p)] + [(k, ctypes.c_int32) for k in
+                                           ("dtype", "layout", "role", "fmt", "n", "c", "h", "w")] + \
+               [("codes", ctypes.c_void_p), ("scales", ctypes.c_void_p),
+                ("conv", ctypes.POINTER(MxcConv)), ("col_codes", ctypes.c_void_p), ("col_scales", ctypes.c_void_p)]
 
 
 def lib():
@@ -188,17 +189,29 @@ def quantize(src, role, fmt, layout=NCHW, shape=None, out=None, stream=None):
 def quantize_multi(items, stream=None):
     """Several quantize() calls in one library call (one launch for the CBF
     batch-block-32 activations and OIHW weights among them).  items: tuples
-    (src, role, fmt, layout, shape, out); returns the MX tensors."""
+    (src, role, fmt, layout, shape, out[, col]); col = (cv, col_codes,
+    col_scales) also writes the activation's CBF im2col for layer cv into the
+    two uint8 device tensors (sizes: mxconv_im2col_{codes,scales}_bytes).
+    Returns the MX tensors."""
     if len(items) > QMULTI_MAX:
         raise MxconvError(f"at most {QMULTI_MAX} tensors per call")
     jobs = (MxcQJob * max(1, len(items)))()
+    convs = []                       # kept alive for the call
     outs = []
-    for k, (src, role, fmt, layout, shape, out) in enumerate(items):
+    for k, item in enumerate(items):
+        src, role, fmt, layout, shape, out = item[:6]
+        col = item[6] if len(item) > 6 else None
         dtype, shape = _quant_args(src, layout, shape)
         if out is None:
             out = MxTensor.empty(role, fmt, shape, src.device)
         jobs[k] = MxcQJob(src.data_ptr(), dtype, layout, role, fmt, *shape, out.codes.data_ptr(),
                           out.scales.data_ptr())
+        if col is not None:
+            cv, cc, cs = col
+            convs.append(conv_struct(cv))
+            jobs[k].conv = ctypes.pointer(convs[-1])
+            jobs[k].col_codes = cc.data_ptr()
+            jobs[k].col_scales = cs.data_ptr()
         outs.append(out)
     _check(lib().mxconv_quantize_multi(len(items), jobs, _stream(stream)), "mxconv_quantize_multi")
     return outs

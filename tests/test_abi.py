@@ -282,6 +282,28 @@ def test_quantize_multi_errors():
     assert call(job(), job(layout=2, role=1)) == -2                     # CBF weights
     assert call(job(), job(n=48)) == -3
     assert call(job(), job(codes=0x10001)) == -4
+    # the optional im2col output: NULL outputs, a layer that does not match its
+    # tensor, weights, a bad layer, misaligned outputs
+    cv = mx.conv_struct(synth.conv_dict(32, 32, 16, 4, 4, 3, 1, 1))
+
+    def colj(conv=cv, cc=0x10000, cs=0x10000, **kw):
+        j = job(**kw)
+        j.conv = ctypes.pointer(conv)
+        j.col_codes, j.col_scales = cc, cs
+        return j
+
+    assert call(job(), colj(cc=0)) == -1
+    assert call(job(), colj(cs=0)) == -1
+    assert call(job(), colj(c=64)) == -3                               # conv.cin != c
+    assert call(job(), colj(h=5)) == -3
+    assert call(job(), colj(layout=0, role=1)) == -3                   # weights have no im2col
+    bad = mx.conv_struct(synth.conv_dict(32, 32, 16, 4, 4, 3, 1, 1))
+    bad.sh = 0
+    assert call(job(), colj(conv=bad)) == -2
+    big = mx.conv_struct(synth.conv_dict(32, 32, 16, 4, 4, 7, 1, 0))  # kernel larger than the padded input
+    assert call(job(), colj(conv=big)) == -3
+    assert call(job(), colj(cc=0x10008)) == -4
+    assert call(job(), colj(cs=0x10001)) == -4
 
 
 def test_nvfp_gemm_errors():

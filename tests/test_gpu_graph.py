@@ -48,11 +48,10 @@ def test_graph_replay_matches_eager(mx, fmt, cv):
     outs = [qx.codes, qx.scales, qw.codes, qw.scales, qg.codes, qg.scales, col[0], col[1], y, gx, gw]
 
     def step():
-        mx.quantize_multi([(xd, mx.ACT, fmt, mx.CBF, xs, qx), (wd, mx.WEIGHT, fmt, mx.NCHW, tuple(wd.shape), qw)])
+        # X (with its CBF im2col) and W in one launch, as the benchmark step does
+        mx.quantize_multi([(xd, mx.ACT, fmt, mx.CBF, xs, qx, (cv, col[0], col[1])),
+                           (wd, mx.WEIGHT, fmt, mx.NCHW, tuple(wd.shape), qw)])
         mx.quantize(gd, mx.ACT, fmt, layout=mx.CBF, shape=gs, out=qg)
-        rc = mx.lib().mxconv_im2col_cbf(ctypes.byref(c), fmt, mx._ptr(qx.codes), mx._ptr(qx.scales),
-                                        mx._ptr(col[0]), mx._ptr(col[1]), mx._stream(None))
-        assert rc == 0
         mx.fwd(cv, qw, qx, layout=mx.CBF, out=y)
         mx.dgrad(cv, qw, qg, layout=mx.CBF, out=gx)
         mx.wgrad(cv, qg, qx, out=gw, workspace=ws)
