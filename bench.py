@@ -8,8 +8,9 @@ and each format (MXFP8 E4M3, MXFP4 E2M1): quantize X, W and G_Y once
 (activations arrive channel-batch-first in fp32, weights OIHW fp32), with the
 explicit CBF im2col of X written by the same launch that quantizes X and W
 (the forward operands), then the forward, input-gradient and weight-gradient
-GEMMs: 36 kernels.  Activations are SiLU(N(0,1)), weights Kaiming-normal,
-gradients N(0, 1e-3), all seeded.
+GEMMs, the weight gradients' split-K partial sums of all layers finished by
+one reduction launch at the end: 31 kernels.  Activations are SiLU(N(0,1)),
+weights Kaiming-normal, gradients N(0, 1e-3), all seeded.
 
 `value` is the conv fwd+bwd GEMM throughput of the whole step: the three
 GEMMs' algorithmic flops (2 N Cout Ho Wo Cin Kh Kw each, real channels) over
@@ -24,8 +25,9 @@ rounds); quantize launches rotate over enough copies of their fp32 source
 that it is read from HBM, not from the 256 MB last-level cache -- and
 `ms_alone`, one eager launch bracketed by HIP events behind a GPU spin
 (launch and event overhead included).  The op of the step with the largest
-`ms` gets the `roofline` object.  The unfused X+W quantize and the standalone
-im2col kernel are timed too (`in_step` false), outside the step.
+`ms` gets the `roofline` object.  The unfused X+W quantize, the standalone
+im2col kernel and the whole weight gradient (GEMM and its own reduction) are
+timed too (`in_step` false), outside the step.
 
     python bench.py [--steps K] [--warmup W] [--no-cpu-baseline]
 """
@@ -78,6 +80,9 @@ def layer_numbers(cv, fmt, mx):
         "fwd": (flops, W + X + 4.0 * n * co * ho * wo),
         "dgrad": (flops, W + G + 4.0 * n * ci * cv["h"] * cv["w"]),
         "wgrad": (flops, G + X + 4.0 * co * ci * kh * kw),
+        # the weight-gradient GEMM with its split-K reduction deferred to the
+        # step's batched reduction (credited with the same algorithmic work)
+        "wgrad_partial": (flops, G + X + 4.0 * co * ci * kh * kw),
     }
 
 
@@ -324,10 +329,13 @@ def main():
     # a layer's forward operands X and W are quantized together, in one launch
     # that also writes X's explicit CBF im2col (the quantizer copies each block
     # to its im2col positions as it produces it)
-    OPS = ("quant_xw_im2col", "quant_gy", "fwd", "dgrad", "wgrad")
+    # and each weight gradient leaves its split-K partial sums for one batched
+    # reduction of all layers at the end of the step (as at the end of a
+    # backward pass)
+    OPS = ("quant_xw_im2col", "quant_gy", "fwd", "dgrad", "wgrad_partial")
     # timed beside the step, not part of it: the unfused forward-operand
-    # quantize and the standalone im2col kernel
-    REF_OPS = ("quant_xw", "im2col")
+    # quantize, the standalone im2col kernel and the whole weight gradient
+    REF_OPS = ("quant_xw", "im2col", "wgrad")
 
     def run_op(j, op, src=None):
         cv, fmt = j["cv"], j["fmt"]
@@ -348,6 +356,8 @@ def main():
             mx.fwd(cv, j["qw"], j["qx"], layout=mx.CBF, out=j["y"])
         elif op == "dgrad":
             mx.dgrad(cv, j["qw"], j["qg"], layout=mx.CBF, out=j["gx"])
+        elif op == "wgrad_partial":
+            mx.wgrad(cv, j["qg"], j["qx"], out=j["gw"], workspace=j["ws"], deferred=True)
         else:
             mx.wgrad(cv, j["qg"], j["qx"], out=j["gw"], workspace=j["ws"])
 
@@ -365,10 +375,19 @@ def main():
         if rc:
             raise mx.MxconvError(mx.strerror(rc))
 
-    seq = [(j, op) for j in jobs for op in OPS]
+    # the step-level op: one launch finishing every layer's weight gradient
+    red_bytes = sum(j["ws"].numel() + 4.0 * j["gw"].numel() for j in jobs
+                    if mx.wgrad_workspace_bytes(j["cv"], j["fmt"]) > 0)
+    step_job = {"name": "all_layers", "nums": {"wgrad_reduce_all": (0.0, red_bytes)}, "fmt": 0}
+    seq = [(j, op) for j in jobs for op in OPS] + [(step_job, "wgrad_reduce_all")]
 
     def run(j, op):
-        run_im2col(j) if op == "im2col" else run_op(j, op)
+        if op == "im2col":
+            run_im2col(j)
+        elif op == "wgrad_reduce_all":
+            mx.wgrad_reduce_multi([(k["cv"], k["fmt"], k["ws"], k["gw"]) for k in jobs])
+        else:
+            run_op(j, op)
 
     def step():
         for j, op in seq:
@@ -470,7 +489,7 @@ def main():
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
             for k in range(kl):
-                run_op(j, op, srcs[k % len(srcs)]) if op != "im2col" else run_im2col(j)
+                run_op(j, op, srcs[k % len(srcs)]) if op not in ("im2col", "wgrad_reduce_all") else run(j, op)
         g.replay()
         torch.cuda.synchronize()
         steady[(j["name"], op)] = statistics.median(replay_ms(g, 3) for _ in range(3)) / kl
@@ -674,7 +693,7 @@ def main():
         return {"bound": "mfma", "achieved": round(ach, 1), "peak": MFMA_TFLOPS[fmt], "unit": "TFLOP/s",
                 "frac": round(ach / MFMA_TFLOPS[fmt], 4)}
 
-    jmap = {j["name"]: j for j in jobs}
+    jmap = {j["name"]: j for j in jobs + [step_job]}
     rl = roof(jmap[dom[0]], dom[1], dom_ms)
     rl.update({"kernel": f"{dom[1]} {dom[0]}", "ms": round(dom_ms, 4),
                "ms_alone": round(op_ms[dom], 4),
@@ -697,7 +716,8 @@ def main():
         "dtype": "mxfp8+mxfp4 (fp32 accumulate)", "data": "synthetic",
         "config": {"workload": "conv layer sweep, batch 32: 3x3 s1 64->64 56x56, 1x1 64->256 56x56, "
                                "3x3 s2 128->256 28x28; each in MXFP8 and MXFP4; quantize X+W with X's CBF im2col (one "
-                               "launch) + quantize G_Y + fwd + dgrad + wgrad per layer",
+                               "launch) + quantize G_Y + fwd + dgrad + wgrad per layer, the six weight "
+                               "gradients' split-K reductions in one launch at the end",
                    "global_batch": 32, "layers": [n for n, _ in synth.SWEEP_LAYERS], "formats": ["mxfp8", "mxfp4"],
                    "parallelism": "single GPU"},
         "roofline": rl,

@@ -327,6 +327,32 @@ int mxconv_wgrad(const mxc_conv* cv, int fmt,
                  const void* x_codes, const uint8_t* x_scales,
                  float* gw, void* workspace, size_t ws_bytes, void* stream);
 
+/* The weight gradient in two parts, for callers that finish several layers'
+ * weight gradients together (at the end of a backward pass, say):
+ * mxconv_wgrad_deferred takes mxconv_wgrad's arguments and runs its GEMM but
+ * leaves the split-K partial sums in the workspace (a layer without split
+ * gets its G_W written directly); mxconv_wgrad_reduce_multi then finishes up
+ * to MXC_WREDUCE_MAX such layers with one launch.  The result is bit for bit
+ * mxconv_wgrad's (the same partial sums, added in the same order).  Each job
+ * names the layer and format of its deferred call, that call's workspace
+ * (untouched in between) and G_W; the reduction must follow the deferred
+ * calls on the stream.
+ * Errors: as mxconv_wgrad for every job (checked before anything is
+ * launched), ARG for a count out of range. */
+#define MXC_WREDUCE_MAX 8
+typedef struct mxc_wjob {
+    const mxc_conv* conv;
+    int fmt;
+    const void* workspace;
+    size_t ws_bytes;
+    float* gw;
+} mxc_wjob;
+int mxconv_wgrad_deferred(const mxc_conv* cv, int fmt,
+                          const void* gy_codes, const uint8_t* gy_scales,
+                          const void* x_codes, const uint8_t* x_scales,
+                          float* gw, void* workspace, size_t ws_bytes, void* stream);
+int mxconv_wgrad_reduce_multi(int count, const mxc_wjob* jobs, void* stream);
+
 /* ------------------------------------------------------------------ a6 */
 /* Naive comparator (the baseline of Sec. III-C and Table I): the im2col is
  * done in full precision first, and every GEMM operand is then quantized

@@ -586,34 +586,107 @@ __global__ __launch_bounds__(NT) void wgrad_kernel(WgradArgs p) {
 // A workgroup takes 64 consecutive partial columns; its four waves each sum
 // every fourth split (eight loads in flight per lane), and the four sums are
 // added in a fixed order through LDS, so the result does not depend on timing.
-__global__ __launch_bounds__(256) void wgrad_reduce(const float* __restrict__ part, float* __restrict__ gw,
-                                                    Conv cv, int ntot, int splits) {
+struct RedGeom {
+    int cout, cin, kh, kw, gy_cp, x_cp, ntot, splits;
+};
+
+// Up to 4 splits: a workgroup takes 256 columns, a thread one column, with
+// the same association as the four-wave sum ((s0 + s1) + (s2 + s3), each
+// term starting from +0), so both forms give the same bits.
+constexpr int RED_NARROW = 4;
+
+__device__ __forceinline__ void store_gw(float* __restrict__ gw, const RedGeom& r, int co, int col, float sum) {
+    const int tap = col / r.x_cp, ci = col % r.x_cp;
+    if (ci < r.cin)
+        gw[(((size_t)co * r.cin + ci) * r.kh + tap / r.kw) * r.kw + tap % r.kw] = sum;
+}
+
+__device__ __forceinline__ void reduce_cols(const float* __restrict__ part, float* __restrict__ gw,
+                                            const RedGeom& r, long wg) {
     __shared__ float red[4][64];
+    if (r.splits <= RED_NARROW) {                                  // uniform per workgroup
+        const long i = wg * 256 + threadIdx.x;
+        if (i >= (long)r.cout * r.ntot) return;
+        const int co = (int)(i / r.ntot), col = (int)(i % r.ntot);
+        const size_t stride = (size_t)r.gy_cp * r.ntot;
+        const float* q = part + (size_t)co * r.ntot + col;
+        float s[RED_NARROW];
+#pragma unroll
+        for (int k = 0; k < RED_NARROW; k++) s[k] = k < r.splits ? 0.0f + __ldg(q + (size_t)k * stride) : 0.0f;
+        store_gw(gw, r, co, col, (s[0] + s[1]) + (s[2] + s[3]));
+        return;
+    }
     const int lane = threadIdx.x & 63, quarter = threadIdx.x >> 6;
-    const long i = (long)blockIdx.x * 64 + lane;                  // over (co, col) of the partial layout
-    const long total = (long)cv.cout * ntot;
+    const long i = wg * 64 + lane;                                // over (co, col) of the partial layout
+    const long total = (long)r.cout * r.ntot;
     const bool live = i < total;
-    const int co = live ? (int)(i / ntot) : 0;
-    const int col = live ? (int)(i % ntot) : 0;
-    const size_t stride = (size_t)cv.gy.cp * ntot;
-    const float* q = part + (size_t)co * ntot + col;
+    const int co = live ? (int)(i / r.ntot) : 0;
+    const int col = live ? (int)(i % r.ntot) : 0;
+    const size_t stride = (size_t)r.gy_cp * r.ntot;
+    const float* q = part + (size_t)co * r.ntot + col;
     float acc = 0.0f;
     int k = quarter;
-    for (; k + 28 < splits; k += 32) {
+    for (; k + 28 < r.splits; k += 32) {
         float v[8];
 #pragma unroll
         for (int j = 0; j < 8; j++) v[j] = __ldg(q + (size_t)(k + 4 * j) * stride);
 #pragma unroll
         for (int j = 0; j < 8; j++) acc += v[j];
     }
-    for (; k < splits; k += 4) acc += __ldg(q + (size_t)k * stride);
+    for (; k < r.splits; k += 4) acc += __ldg(q + (size_t)k * stride);
     red[quarter][lane] = acc;
     __syncthreads();
     if (quarter != 0 || !live) return;
-    const float sum = (red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane]);
-    const int tap = col / cv.x.cp, ci = col % cv.x.cp;
-    if (ci < cv.cin)
-        gw[(((size_t)co * cv.cin + ci) * cv.kh + tap / cv.kw) * cv.kw + tap % cv.kw] = sum;
+    store_gw(gw, r, co, col, (red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane]));
+}
+
+// workgroups of one reduction
+long reduce_wgs(const Conv& cv, int splits) {
+    const long cols = (long)cv.cout * cv.kh * cv.kw * cv.x.cp;
+    const int per = splits <= RED_NARROW ? 256 : 64;
+    return (cols + per - 1) / per;
+}
+
+RedGeom red_geom(const Conv& cv, int splits) {
+    RedGeom r;
+    r.cout = cv.cout; r.cin = cv.cin; r.kh = cv.kh; r.kw = cv.kw;
+    r.gy_cp = cv.gy.cp; r.x_cp = cv.x.cp; r.ntot = cv.kh * cv.kw * cv.x.cp; r.splits = splits;
+    return r;
+}
+
+__global__ __launch_bounds__(256) void wgrad_reduce(const float* __restrict__ part, float* __restrict__ gw,
+                                                    RedGeom r) {
+    reduce_cols(part, gw, r, blockIdx.x);
+}
+
+// Several layers' reductions in one launch: the workgroups of job i take
+// [wg0_i, wg0_i + (cout_i ntot_i + 63) / 64); the job is picked with scalar
+// selects, as in the batched quantizer.
+struct RJob {
+    const float* part;
+    float* gw;
+    RedGeom r;
+    int wg0;
+};
+struct RMulti {
+    RJob j[MXC_WREDUCE_MAX];
+    int count, nwg;
+};
+
+__global__ __launch_bounds__(256) void wgrad_reduce_multi(RMulti m) {
+    const int wg = (int)blockIdx.x;
+    if (wg >= m.nwg) return;                                      // the whole workgroup
+    RJob q = m.j[0];
+#pragma unroll
+    for (int t = 1; t < MXC_WREDUCE_MAX; t++)
+        if (t < m.count && wg >= m.j[t].wg0) q = m.j[t];
+    reduce_cols(q.part, q.gw, q.r, wg - q.wg0);
+}
+
+int launch_reduce(const Conv& cv, const float* part, float* gw, int splits, hipStream_t s) {
+    hipLaunchKernelGGL(wgrad_reduce, dim3((unsigned)reduce_wgs(cv, splits)), dim3(256), 0, s, part, gw,
+                       red_geom(cv, splits));
+    return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
 }
 
 struct WgradPlan {
@@ -1303,16 +1376,13 @@ size_t wgrad_workspace(const Conv& cv) {
 }
 
 int launch_wgrad(const Conv& cv, const void* gc, const uint8_t* gs, const void* xc, const uint8_t* xs,
-                 float* gw, void* ws, hipStream_t s, const float* nv_tg, const float* nv_tx) {
+                 float* gw, void* ws, hipStream_t s, const float* nv_tg, const float* nv_tx, bool defer) {
     const int ls = wgrad_lean_splits(cv);
     if (nv_tg && ls == 0) return MXC_ERR_SHAPE;
     if (ls > 0) {
         const int rc = launch_wgrad_lean(cv, gc, gs, xc, xs, ls > 1 ? (float*)ws : gw, ls, s, nv_tg, nv_tx);
-        if (rc || ls == 1) return rc;
-        const long cols = (long)cv.cout * cv.kh * cv.kw * cv.x.cp;
-        hipLaunchKernelGGL(wgrad_reduce, dim3((unsigned)((cols + 63) / 64)), dim3(256), 0, s,
-                           (const float*)ws, gw, cv, cv.kh * cv.kw * cv.x.cp, ls);
-        return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
+        if (rc || ls == 1 || defer) return rc;
+        return launch_reduce(cv, (const float*)ws, gw, ls, s);
     }
     if (!general_fmt(cv)) return MXC_ERR_SHAPE;
     const WgradPlan pl = wgrad_plan(cv);
@@ -1336,10 +1406,34 @@ int launch_wgrad(const Conv& cv, const void* gc, const uint8_t* gs, const void* 
     } else {
         rc = cv.fmt == MXC_E4M3 ? launch_wgrad_f<MXC_E4M3>(a, grid, s) : launch_wgrad_f<MXC_E2M1>(a, grid, s);
     }
-    if (rc) return rc;
-    const long cols = (long)cv.cout * pl.ntot;
-    hipLaunchKernelGGL(wgrad_reduce, dim3((unsigned)((cols + 63) / 64)), dim3(256), 0, s, (const float*)ws, gw,
-                       cv, pl.ntot, pl.splits);
+    if (rc || defer) return rc;
+    return launch_reduce(cv, (const float*)ws, gw, pl.splits, s);
+}
+
+int wgrad_pending_splits(const Conv& cv) {
+    const int ls = wgrad_lean_splits(cv);
+    if (ls > 0) return ls > 1 ? ls : 0;
+    return general_fmt(cv) ? wgrad_plan(cv).splits : 0;
+}
+
+int launch_wgrad_reduce_multi(int count, const WReduceJob* jobs, hipStream_t s) {
+    RMulti m;
+    int nq = 0;
+    long nwg = 0;
+    for (int i = 0; i < count; i++) {
+        const int splits = wgrad_pending_splits(jobs[i].cv);
+        if (splits == 0) continue;                        // G_W was written by the weight-gradient kernel
+        const long wgs = reduce_wgs(jobs[i].cv, splits);
+        if (nwg + wgs > 0x7FFFFFFFL) return MXC_ERR_SHAPE;
+        RJob& d = m.j[nq++];
+        d.part = (const float*)jobs[i].ws; d.gw = jobs[i].gw; d.r = red_geom(jobs[i].cv, splits); d.wg0 = (int)nwg;
+        nwg += wgs;
+    }
+    if (nq == 0) return MXC_OK;
+    m.count = nq;
+    m.nwg = (int)nwg;
+    for (int i = nq; i < MXC_WREDUCE_MAX; i++) m.j[i] = m.j[nq - 1];
+    hipLaunchKernelGGL(wgrad_reduce_multi, dim3((unsigned)nwg), dim3(256), 0, s, m);
     return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
 }
 

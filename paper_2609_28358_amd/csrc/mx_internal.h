@@ -109,7 +109,16 @@ int launch_wgrad_lean(const Conv& cv, const void* gc, const uint8_t* gs, const v
 size_t wgrad_workspace(const Conv& cv);
 int launch_wgrad(const Conv& cv, const void* gc, const uint8_t* gs, const void* xc,
                  const uint8_t* xs, float* gw, void* ws, hipStream_t s, const float* nv_tg = nullptr,
-                 const float* nv_tx = nullptr);
+                 const float* nv_tx = nullptr, bool defer = false);
+// Split-K partial sums a deferred weight gradient leaves in its workspace
+// (0: the kernel wrote G_W itself), and their reduction for several layers.
+int wgrad_pending_splits(const Conv& cv);
+struct WReduceJob {
+    Conv cv;
+    const void* ws;
+    float* gw;
+};
+int launch_wgrad_reduce_multi(int count, const WReduceJob* jobs, hipStream_t s);
 
 // naive comparator (naive.hip): a line matrix stores each 1-D-blocked line
 // zero-padded to a multiple of 64 elements (one K step of the MFMA)

@@ -285,8 +285,8 @@ int mxconv_dgrad(const mxc_conv* p, int fmt, const void* wc, const uint8_t* ws, 
     return launch_dgrad(cv, wc, ws, gc, gs, gx, gx_layout, (hipStream_t)stream);
 }
 
-int mxconv_wgrad(const mxc_conv* p, int fmt, const void* gc, const uint8_t* gs, const void* xc,
-                 const uint8_t* xs, float* gw, void* workspace, size_t ws_bytes, void* stream) {
+static int wgrad_call(const mxc_conv* p, int fmt, const void* gc, const uint8_t* gs, const void* xc,
+                      const uint8_t* xs, float* gw, void* workspace, size_t ws_bytes, void* stream, bool defer) {
     if (!p || !gc || !gs || !xc || !xs || !gw) return MXC_ERR_NULL;
     Conv cv;
     int rc = conv_init(&cv, p, fmt, CONV_WGRAD);
@@ -296,7 +296,35 @@ int mxconv_wgrad(const mxc_conv* p, int fmt, const void* gc, const uint8_t* gs, 
     if (!aligned16(gc) || !aligned16(gs) || !aligned16(xc) || !aligned16(xs) || !aligned16(gw) ||
         (need && !aligned16(workspace)))
         return MXC_ERR_ALIGN;
-    return launch_wgrad(cv, gc, gs, xc, xs, gw, workspace, (hipStream_t)stream);
+    return launch_wgrad(cv, gc, gs, xc, xs, gw, workspace, (hipStream_t)stream, nullptr, nullptr, defer);
+}
+
+int mxconv_wgrad(const mxc_conv* p, int fmt, const void* gc, const uint8_t* gs, const void* xc,
+                 const uint8_t* xs, float* gw, void* workspace, size_t ws_bytes, void* stream) {
+    return wgrad_call(p, fmt, gc, gs, xc, xs, gw, workspace, ws_bytes, stream, false);
+}
+
+int mxconv_wgrad_deferred(const mxc_conv* p, int fmt, const void* gc, const uint8_t* gs, const void* xc,
+                          const uint8_t* xs, float* gw, void* workspace, size_t ws_bytes, void* stream) {
+    return wgrad_call(p, fmt, gc, gs, xc, xs, gw, workspace, ws_bytes, stream, true);
+}
+
+int mxconv_wgrad_reduce_multi(int count, const mxc_wjob* jobs, void* stream) {
+    if (count < 0 || count > MXC_WREDUCE_MAX) return MXC_ERR_ARG;
+    if (count > 0 && !jobs) return MXC_ERR_NULL;
+    WReduceJob q[MXC_WREDUCE_MAX];
+    for (int i = 0; i < count; i++) {
+        const mxc_wjob& j = jobs[i];
+        if (!j.conv || !j.gw) return MXC_ERR_NULL;
+        const int rc = conv_init(&q[i].cv, j.conv, j.fmt, CONV_WGRAD);
+        if (rc) return rc;
+        const size_t need = wgrad_workspace(q[i].cv);
+        if (need && (!j.workspace || j.ws_bytes < need)) return MXC_ERR_WORKSPACE;
+        if (!aligned16(j.gw) || (need && !aligned16(j.workspace))) return MXC_ERR_ALIGN;
+        q[i].ws = j.workspace;
+        q[i].gw = j.gw;
+    }
+    return launch_wgrad_reduce_multi(count, q, (hipStream_t)stream);
 }
 
 namespace {

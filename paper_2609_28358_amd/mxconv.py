@@ -34,6 +34,14 @@ class MxcConv(ctypes.Structure):
                 ("n", "cin", "cout", "h", "w", "kh", "kw", "sh", "sw", "ph", "pw")]
 
 
+class MxcWJob(ctypes.Structure):
+    _fields_ = [("conv", ctypes.POINTER(MxcConv)), ("fmt", ctypes.c_int32), ("workspace", ctypes.c_void_p),
+                ("ws_bytes", ctypes.c_size_t), ("gw", ctypes.c_void_p)]
+
+
+WREDUCE_MAX = 8
+
+
 class MxcQJob(ctypes.Structure):
     _fields_ = [("src", ctypes.c_void_p)] + [(k, ctypes.c_int32) for k in
                                            ("dtype", "layout", "role", "fmt", "n", "c", "h", "w")] + \
@@ -72,6 +80,8 @@ def lib():
         "mxconv_fwd": (i32, [CP, i32, P, P, P, P, P, i32, P]),
         "mxconv_dgrad": (i32, [CP, i32, P, P, P, P, P, i32, P]),
         "mxconv_wgrad": (i32, [CP, i32, P, P, P, P, P, P, sz, P]),
+        "mxconv_wgrad_deferred": (i32, [CP, i32, P, P, P, P, P, P, sz, P]),
+        "mxconv_wgrad_reduce_multi": (i32, [i32, ctypes.POINTER(MxcWJob), P]),
         "mxconv_fwd_quant": (i32, [CP, i32, P, P, P, P, i32, i32, P, P, P, P]),
         "mxconv_dgrad_quant": (i32, [CP, i32, P, P, P, P, i32, P, i32, P, P, P, P]),
         "mxconv_naive_codes_bytes": (sz, [i64, i64, i32]),
@@ -326,17 +336,37 @@ def dgrad(cv, w, gy, layout=NCHW, out=None, stream=None):
     return gx
 
 
-def wgrad(cv, gy, x, out=None, workspace=None, stream=None):
+def wgrad(cv, gy, x, out=None, workspace=None, stream=None, deferred=False):
+    """G_W = G_Y * X^T.  deferred: leave the split-K partial sums in the
+    workspace for wgrad_reduce_multi (the workspace must then be passed)."""
     gw = out if out is not None else torch.empty((cv["cout"], cv["cin"], cv["kh"], cv["kw"]),
                                                  dtype=torch.float32, device=x.codes.device)
     need = wgrad_workspace_bytes(cv, pair(gy.fmt, x.fmt))
     if workspace is None and need:
+        if deferred:
+            raise MxconvError("a deferred weight gradient needs the caller's workspace")
         workspace = torch.empty(need, dtype=torch.uint8, device=x.codes.device)
     wsz = workspace.numel() * workspace.element_size() if workspace is not None else 0
-    _check(lib().mxconv_wgrad(ctypes.byref(conv_struct(cv)), pair(gy.fmt, x.fmt), _ptr(gy.codes), _ptr(gy.scales),
-                              _ptr(x.codes), _ptr(x.scales), _ptr(gw), _ptr(workspace), wsz,
-                              _stream(stream)), "mxconv_wgrad")
+    fn, name = (lib().mxconv_wgrad_deferred, "mxconv_wgrad_deferred") if deferred else (lib().mxconv_wgrad,
+                                                                                          "mxconv_wgrad")
+    _check(fn(ctypes.byref(conv_struct(cv)), pair(gy.fmt, x.fmt), _ptr(gy.codes), _ptr(gy.scales),
+              _ptr(x.codes), _ptr(x.scales), _ptr(gw), _ptr(workspace), wsz, _stream(stream)), name)
     return gw
+
+
+def wgrad_reduce_multi(items, stream=None):
+    """Finish deferred weight gradients in one launch.  items: tuples
+    (cv, fmt, workspace, gw) of the deferred calls (fmt as passed to them:
+    pair(gy.fmt, x.fmt))."""
+    if len(items) > WREDUCE_MAX:
+        raise MxconvError(f"at most {WREDUCE_MAX} layers per call")
+    jobs = (MxcWJob * max(1, len(items)))()
+    convs = []
+    for k, (cv, fmt, ws, gw) in enumerate(items):
+        convs.append(conv_struct(cv))
+        jobs[k] = MxcWJob(ctypes.pointer(convs[-1]), fmt, ws.data_ptr() if ws is not None else None,
+                          ws.numel() * ws.element_size() if ws is not None else 0, gw.data_ptr())
+    _check(lib().mxconv_wgrad_reduce_multi(len(items), jobs, _stream(stream)), "mxconv_wgrad_reduce_multi")
 
 
 def fwd_quant(cv, w, x, fn=FN_NONE, out_fmt=None, out=None, act_out=None, stream=None):

@@ -324,3 +324,32 @@ def test_nvfp_gemm_errors():
     assert w(big, 1, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, None, 0, None) == -6
     r16 = ctypes.byref(mx.conv_struct(synth.conv_dict(16, 64, 64, 8, 8, 3, 1, 1)))
     assert w(r16, 1, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, 1 << 30, None) == -3
+
+
+def test_wgrad_reduce_multi_errors():
+    L = mx.lib()
+    cv = mx.conv_struct(synth.conv_dict(32, 64, 64, 56, 56, 3, 1, 1))        # needs a split-K workspace
+    need = L.mxconv_wgrad_workspace_bytes(ctypes.byref(cv), 0)
+    assert need > 0
+
+    def job(conv=cv, fmt=0, ws=0x10000, wsb=None, gw=0x10000):
+        return mx.MxcWJob(ctypes.pointer(conv) if conv is not None else None, fmt, ws, need if wsb is None else wsb, gw)
+
+    def call(*jobs):
+        arr = (mx.MxcWJob * max(1, len(jobs)))(*jobs)
+        return L.mxconv_wgrad_reduce_multi(len(jobs), arr, None)
+
+    assert L.mxconv_wgrad_reduce_multi(9, None, None) == -2
+    assert L.mxconv_wgrad_reduce_multi(-1, None, None) == -2
+    assert L.mxconv_wgrad_reduce_multi(1, None, None) == -1
+    assert L.mxconv_wgrad_reduce_multi(0, None, None) == 0
+    assert call(job(), job(conv=None)) == -1
+    assert call(job(), job(gw=0)) == -1
+    assert call(job(), job(fmt=9)) == -2
+    assert call(job(), job(ws=0)) == -6
+    assert call(job(), job(wsb=need - 1)) == -6
+    assert call(job(), job(gw=0x10004)) == -4
+    assert call(job(), job(ws=0x10008)) == -4
+    r = ctypes.byref(cv)
+    assert L.mxconv_wgrad_deferred(r, 0, GOOD, GOOD, GOOD, GOOD, GOOD, None, 0, None) == -6
+    assert L.mxconv_wgrad_deferred(None, 0, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, need, None) == -1

@@ -54,7 +54,9 @@ def test_graph_replay_matches_eager(mx, fmt, cv):
         mx.quantize(gd, mx.ACT, fmt, layout=mx.CBF, shape=gs, out=qg)
         mx.fwd(cv, qw, qx, layout=mx.CBF, out=y)
         mx.dgrad(cv, qw, qg, layout=mx.CBF, out=gx)
-        mx.wgrad(cv, qg, qx, out=gw, workspace=ws)
+        # the weight gradient's split-K reduction as a batched launch, as in the benchmark step
+        mx.wgrad(cv, qg, qx, out=gw, workspace=ws, deferred=True)
+        mx.wgrad_reduce_multi([(cv, fmt, ws, gw)])
 
     step()
     torch.cuda.synchronize()
