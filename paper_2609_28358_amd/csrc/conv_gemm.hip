@@ -583,68 +583,41 @@ __global__ __launch_bounds__(NT) void wgrad_kernel(WgradArgs p) {
 }
 
 // G_W[co][ci][kh][kw] = sum over splits of the partial (co, tap*Cin_p + ci).
-// A workgroup takes 64 consecutive partial columns; its four waves each sum
-// every fourth split (eight loads in flight per lane), and the four sums are
-// added in a fixed order through LDS, so the result does not depend on timing.
+// A workgroup takes 256 consecutive partial columns, a thread one column.
+// The thread keeps four sums, sum q adding splits q, q + 4, q + 8, ... in
+// increasing order, and returns (sum0 + sum1) + (sum2 + sum3): a fixed order,
+// so the result does not depend on timing, and the same bits whether one
+// layer or several are reduced by the launch.
 struct RedGeom {
     int cout, cin, kh, kw, gy_cp, x_cp, ntot, splits;
 };
 
-// Up to 4 splits: a workgroup takes 256 columns, a thread one column, with
-// the same association as the four-wave sum ((s0 + s1) + (s2 + s3), each
-// term starting from +0), so both forms give the same bits.
-constexpr int RED_NARROW = 4;
-
-__device__ __forceinline__ void store_gw(float* __restrict__ gw, const RedGeom& r, int co, int col, float sum) {
+__device__ __forceinline__ void reduce_cols(const float* __restrict__ part, float* __restrict__ gw,
+                                            const RedGeom& r, long wg) {
+    const long i = wg * 256 + threadIdx.x;
+    if (i >= (long)r.cout * r.ntot) return;
+    const int co = (int)(i / r.ntot), col = (int)(i % r.ntot);
+    const size_t stride = (size_t)r.gy_cp * r.ntot;
+    const float* q = part + (size_t)co * r.ntot + col;
+    float a[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    int k = 0;
+    for (; k + 8 <= r.splits; k += 8) {                 // eight loads in flight
+        float v[8];
+#pragma unroll
+        for (int j = 0; j < 8; j++) v[j] = __ldg(q + (size_t)(k + j) * stride);
+#pragma unroll
+        for (int j = 0; j < 8; j++) a[j & 3] += v[j];
+    }
+    for (; k < r.splits; k++) a[k & 3] += __ldg(q + (size_t)k * stride);
+    const float sum = (a[0] + a[1]) + (a[2] + a[3]);
     const int tap = col / r.x_cp, ci = col % r.x_cp;
     if (ci < r.cin)
         gw[(((size_t)co * r.cin + ci) * r.kh + tap / r.kw) * r.kw + tap % r.kw] = sum;
 }
 
-__device__ __forceinline__ void reduce_cols(const float* __restrict__ part, float* __restrict__ gw,
-                                            const RedGeom& r, long wg) {
-    __shared__ float red[4][64];
-    if (r.splits <= RED_NARROW) {                                  // uniform per workgroup
-        const long i = wg * 256 + threadIdx.x;
-        if (i >= (long)r.cout * r.ntot) return;
-        const int co = (int)(i / r.ntot), col = (int)(i % r.ntot);
-        const size_t stride = (size_t)r.gy_cp * r.ntot;
-        const float* q = part + (size_t)co * r.ntot + col;
-        float s[RED_NARROW];
-#pragma unroll
-        for (int k = 0; k < RED_NARROW; k++) s[k] = k < r.splits ? 0.0f + __ldg(q + (size_t)k * stride) : 0.0f;
-        store_gw(gw, r, co, col, (s[0] + s[1]) + (s[2] + s[3]));
-        return;
-    }
-    const int lane = threadIdx.x & 63, quarter = threadIdx.x >> 6;
-    const long i = wg * 64 + lane;                                // over (co, col) of the partial layout
-    const long total = (long)r.cout * r.ntot;
-    const bool live = i < total;
-    const int co = live ? (int)(i / r.ntot) : 0;
-    const int col = live ? (int)(i % r.ntot) : 0;
-    const size_t stride = (size_t)r.gy_cp * r.ntot;
-    const float* q = part + (size_t)co * r.ntot + col;
-    float acc = 0.0f;
-    int k = quarter;
-    for (; k + 28 < r.splits; k += 32) {
-        float v[8];
-#pragma unroll
-        for (int j = 0; j < 8; j++) v[j] = __ldg(q + (size_t)(k + 4 * j) * stride);
-#pragma unroll
-        for (int j = 0; j < 8; j++) acc += v[j];
-    }
-    for (; k < r.splits; k += 4) acc += __ldg(q + (size_t)k * stride);
-    red[quarter][lane] = acc;
-    __syncthreads();
-    if (quarter != 0 || !live) return;
-    store_gw(gw, r, co, col, (red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane]));
-}
-
 // workgroups of one reduction
-long reduce_wgs(const Conv& cv, int splits) {
-    const long cols = (long)cv.cout * cv.kh * cv.kw * cv.x.cp;
-    const int per = splits <= RED_NARROW ? 256 : 64;
-    return (cols + per - 1) / per;
+long reduce_wgs(const Conv& cv, int) {
+    return ((long)cv.cout * cv.kh * cv.kw * cv.x.cp + 255) / 256;
 }
 
 RedGeom red_geom(const Conv& cv, int splits) {
