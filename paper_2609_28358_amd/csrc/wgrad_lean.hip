@@ -245,9 +245,9 @@ int wgrad_lean_splits(const Conv& cv) {
     const long npairs = (npix + 1) / 2;
     const long ntiles = (long)cv.kh * cv.kw * ((cv.gy.ncb + 1) / 2) * ((cv.x.ncb + 1) / 2);
     if (npix > 0x3FFFFFFFL || ntiles > 0x7FFFFFL) return 0;
-    // about two workgroups per CU, each wave with at least 8 pixel pairs
+    // about two workgroups per CU, each wave with at least 4 pixel pairs
     long splits = 512 / ntiles;
-    const long cap = npairs / (4 * 8);
+    const long cap = npairs / (4 * 4);
     if (splits > cap) splits = cap;
     if (splits < 1) splits = 1;
     return (int)splits;
