@@ -211,8 +211,8 @@ def test_fp6_format_pairs():
             assert fn(r, f, GOOD, GOOD, GOOD, GOOD, ODD, 0, None) == -4, f
         for f in refused:
             assert fn(r, f, GOOD, GOOD, GOOD, GOOD, GOOD, 0, None) == -2, f
-    for f in accepted:
-        assert L.mxconv_wgrad(r, f, GOOD, GOOD, GOOD, GOOD, ODD, None, 0, None) == -4, f
+    for f in accepted:     # a workspace large enough for any split count, so alignment is what fails
+        assert L.mxconv_wgrad(r, f, GOOD, GOOD, GOOD, GOOD, ODD, GOOD, 1 << 40, None) == -4, f
     for f in refused:
         assert L.mxconv_wgrad(r, f, GOOD, GOOD, GOOD, GOOD, GOOD, None, 0, None) == -2, f
     # im2col and the size queries take a single format
@@ -353,3 +353,23 @@ def test_wgrad_reduce_multi_errors():
     r = ctypes.byref(cv)
     assert L.mxconv_wgrad_deferred(r, 0, GOOD, GOOD, GOOD, GOOD, GOOD, None, 0, None) == -6
     assert L.mxconv_wgrad_deferred(None, 0, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, need, None) == -1
+
+
+def test_size_limits():
+    """Geometries past the 32-bit block and pixel indices the kernels use are
+    refused on the host; the largest admitted sizes are still computed."""
+    L = mx.lib()
+    # activation blocks (n / Bn) * h * w * (Cp / 32) must stay below 2^31
+    assert mx.codes_bytes(mx.ACT, mx.E4M3, 32, 32, 46340, 46340) == 46340 * 46340 * 1024
+    assert mx.codes_bytes(mx.ACT, mx.E4M3, 32, 32, 46341, 46341) == 0
+    assert mx.scales_bytes(mx.ACT, mx.E4M3, 32, 32, 46341, 46341) == 0
+    assert L.mxconv_quantize(GOOD, 0, 2, 0, 0, 32, 32, 46341, 46341, GOOD, GOOD, None) == -3
+    # the explicit im2col indexes taps with 16 bits, alone or asked for by a quantize job
+    big = mx.conv_struct(synth.conv_dict(32, 32, 32, 300, 300, 257, 1, 128))      # 66049 taps
+    assert L.mxconv_im2col_cbf(ctypes.byref(big), 0, GOOD, GOOD, GOOD, GOOD, None) == -3
+    j = mx.MxcQJob(0x10000, 0, 2, 0, 0, 32, 32, 300, 300, 0x10000, 0x10000)
+    j.conv = ctypes.pointer(big)
+    j.col_codes, j.col_scales = 0x10000, 0x10000
+    assert L.mxconv_quantize_multi(1, (mx.MxcQJob * 1)(j), None) == -3
+    ok = mx.conv_struct(synth.conv_dict(32, 32, 32, 300, 300, 255, 1, 127))       # 65025 taps
+    assert L.mxconv_im2col_codes_bytes(ctypes.byref(ok), 0) > 0
