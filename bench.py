@@ -575,30 +575,32 @@ def main():
                 wsb = torch.empty(max(1, mx.wgrad_workspace_bytes(cv, mx.pair(fg, fx))), dtype=torch.uint8, device=dev)
                 it = {"x": 0, "g": 0}
 
-                def qxr():
+                def qxwr():     # X and W in one call, as the MXFP4 layer's quant_xw
                     it["x"] += 1
-                    mx.quantize(xsrc[it["x"] % len(xsrc)], mx.ACT, fx, layout=mx.CBF, shape=j["xs"], out=qx)
+                    mx.quantize_multi([(xsrc[it["x"] % len(xsrc)], mx.ACT, fx, mx.CBF, j["xs"], qx),
+                                       (j["w"], mx.WEIGHT, fw, mx.NCHW, wsh, qw)])
 
                 def qgr():
                     it["g"] += 1
                     mx.quantize(gsrc[it["g"] % len(gsrc)], mx.ACT, fg, layout=mx.CBF, shape=j["gs"], out=qg)
 
-                qxr(); qgr(); mx.quantize(j["w"], mx.WEIGHT, fw, out=qw)
+                qxwr(); qgr()
                 kq = max(12, len(xsrc), len(gsrc))
-                t = {"quant_x": steady_ms(qxr, kq),
-                     "quant_w": steady_ms(lambda: mx.quantize(j["w"], mx.WEIGHT, fw, out=qw)),
+                t = {"quant_xw": steady_ms(qxwr, kq),
                      "quant_gy": steady_ms(qgr, kq)}
-                qxr(); qgr()
+                qxwr(); qgr()
                 t["fwd"] = steady_ms(lambda: mx.fwd(cv, qw, qx, layout=mx.CBF, out=j["y"]))
                 t["dgrad"] = steady_ms(lambda: mx.dgrad(cv, qw, qg, layout=mx.CBF, out=j["gx"]))
                 t["wgrad"] = steady_ms(lambda: mx.wgrad(cv, qg, qx, out=j["gw"], workspace=wsb))
                 X, W, G = mxbytes(mx.ACT, fx, j["xs"]), mxbytes(mx.WEIGHT, fw, wsh), mxbytes(mx.ACT, fg, j["gs"])
-                fp4 = sum(steady[(f"{lname}/mxfp4", op)] for op in t if (f"{lname}/mxfp4", op) in steady)
+                # the MXFP4 layer measured the same way (every op timed beside or in the step)
+                fp4 = sum(steady[(f"{lname}/mxfp4", op)] for op in ("quant_xw", "quant_gy", "fwd", "dgrad", "wgrad"))
                 r = {k + "_ms": round(v, 4) for k, v in t.items()}
                 r.update({"fwd_tflops": round(fl / (t["fwd"] * 1e-3) / 1e12, 1),
                           "dgrad_tflops": round(fl / (t["dgrad"] * 1e-3) / 1e12, 1),
                           "wgrad_tflops": round(fl / (t["wgrad"] * 1e-3) / 1e12, 1),
-                          "quant_x_gbps": round((4.0 * math.prod(j["xs"]) + X) / (t["quant_x"] * 1e-3) / 1e9, 1),
+                          "quant_xw_gbps": round((4.0 * math.prod(j["xs"]) + X + 4.0 * math.prod(wsh) + W)
+                                                 / (t["quant_xw"] * 1e-3) / 1e9, 1),
                           "x_bytes": X, "w_bytes": W, "gy_bytes": G,
                           "layer_ms": round(sum(t.values()), 4)})
                 if fp4:
