@@ -7,9 +7,10 @@ resident in HBM): for each layer
 and each format (MXFP8 E4M3, MXFP4 E2M1): quantize X, W and G_Y once
 (activations arrive channel-batch-first in fp32, weights OIHW fp32), with the
 explicit CBF im2col of X written by the same launch that quantizes X and W
-(the forward operands), then the forward, input-gradient and weight-gradient
-GEMMs, the weight gradients' split-K partial sums of all layers finished by
-one reduction launch at the end: 31 kernels.  Activations are SiLU(N(0,1)),
+(the forward operands), then the forward GEMM, and the input-gradient and
+weight-gradient GEMMs as one launch per layer (both read the quantized G_Y),
+the weight gradients' split-K partial sums of all layers finished by one
+reduction launch at the end: 25 kernels.  Activations are SiLU(N(0,1)),
 weights Kaiming-normal, gradients N(0, 1e-3), all seeded.
 
 `value` is the conv fwd+bwd GEMM throughput of the whole step: the three
@@ -26,8 +27,8 @@ that it is read from HBM, not from the 256 MB last-level cache -- and
 `ms_alone`, one eager launch bracketed by HIP events behind a GPU spin
 (launch and event overhead included).  The op of the step with the largest
 `ms` gets the `roofline` object.  The unfused X+W quantize, the standalone
-im2col kernel and the whole weight gradient (GEMM and its own reduction) are
-timed too (`in_step` false), outside the step.
+im2col kernel, the input gradient alone and the whole weight gradient (GEMM
+and its own reduction) are timed too (`in_step` false), outside the step.
 
     python bench.py [--steps K] [--warmup W] [--no-cpu-baseline]
 """
@@ -80,9 +81,10 @@ def layer_numbers(cv, fmt, mx):
         "fwd": (flops, W + X + 4.0 * n * co * ho * wo),
         "dgrad": (flops, W + G + 4.0 * n * ci * cv["h"] * cv["w"]),
         "wgrad": (flops, G + X + 4.0 * co * ci * kh * kw),
-        # the weight-gradient GEMM with its split-K reduction deferred to the
-        # step's batched reduction (credited with the same algorithmic work)
-        "wgrad_partial": (flops, G + X + 4.0 * co * ci * kh * kw),
+        # input gradient and weight-gradient GEMM in one launch, the split-K
+        # reduction deferred to the step's batched reduction (credited with
+        # the two products' flops and their distinct operands and results)
+        "backward": (2.0 * flops, W + G + X + 4.0 * n * ci * cv["h"] * cv["w"] + 4.0 * co * ci * kh * kw),
     }
 
 
@@ -329,13 +331,14 @@ def main():
     # a layer's forward operands X and W are quantized together, in one launch
     # that also writes X's explicit CBF im2col (the quantizer copies each block
     # to its im2col positions as it produces it)
+    # a layer's input and weight gradients run as one launch (mxconv_backward),
     # and each weight gradient leaves its split-K partial sums for one batched
     # reduction of all layers at the end of the step (as at the end of a
     # backward pass)
-    OPS = ("quant_xw_im2col", "quant_gy", "fwd", "dgrad", "wgrad_partial")
+    OPS = ("quant_xw_im2col", "quant_gy", "fwd", "backward")
     # timed beside the step, not part of it: the unfused forward-operand
     # quantize, the standalone im2col kernel and the whole weight gradient
-    REF_OPS = ("quant_xw", "im2col", "wgrad")
+    REF_OPS = ("quant_xw", "im2col", "dgrad", "wgrad")
 
     def run_op(j, op, src=None):
         cv, fmt = j["cv"], j["fmt"]
@@ -356,8 +359,9 @@ def main():
             mx.fwd(cv, j["qw"], j["qx"], layout=mx.CBF, out=j["y"])
         elif op == "dgrad":
             mx.dgrad(cv, j["qw"], j["qg"], layout=mx.CBF, out=j["gx"])
-        elif op == "wgrad_partial":
-            mx.wgrad(cv, j["qg"], j["qx"], out=j["gw"], workspace=j["ws"], deferred=True)
+        elif op == "backward":
+            mx.backward(cv, j["qw"], j["qg"], j["qx"], layout=mx.CBF, gx_out=j["gx"], gw_out=j["gw"],
+                        workspace=j["ws"], deferred=True)
         else:
             mx.wgrad(cv, j["qg"], j["qx"], out=j["gw"], workspace=j["ws"])
 
@@ -718,7 +722,7 @@ def main():
         "dtype": "mxfp8+mxfp4 (fp32 accumulate)", "data": "synthetic",
         "config": {"workload": "conv layer sweep, batch 32: 3x3 s1 64->64 56x56, 1x1 64->256 56x56, "
                                "3x3 s2 128->256 28x28; each in MXFP8 and MXFP4; quantize X+W with X's CBF im2col (one "
-                               "launch) + quantize G_Y + fwd + dgrad + wgrad per layer, the six weight "
+                               "launch) + quantize G_Y + fwd + dgrad and wgrad in one launch per layer, the six weight "
                                "gradients' split-K reductions in one launch at the end",
                    "global_batch": 32, "layers": [n for n, _ in synth.SWEEP_LAYERS], "formats": ["mxfp8", "mxfp4"],
                    "parallelism": "single GPU"},

@@ -353,6 +353,26 @@ int mxconv_wgrad_deferred(const mxc_conv* cv, int fmt,
                           float* gw, void* workspace, size_t ws_bytes, void* stream);
 int mxconv_wgrad_reduce_multi(int count, const mxc_wjob* jobs, void* stream);
 
+/* Both gradients of one layer (Eqs. (2) and (3), Sec. II-C) from one call:
+ * mxconv_dgrad's result in gx and mxconv_wgrad's (deferred = 0) or
+ * mxconv_wgrad_deferred's (deferred = 1) in gw / workspace, bit for bit.
+ * Both products read the same quantized G_Y; with batch block 32, kernel
+ * width 1 or 3, stride 1 or 2 and format MXFP8 or MXFP4 they run as one
+ * launch, otherwise as the two calls one after the other.
+ *   fmt              passed to both products as their fmt (so the pair
+ *                    (W, G_Y) and the pair (G_Y, X) have the same formats).
+ *   w_*, gy_*, x_*   as for mxconv_dgrad and mxconv_wgrad; gx, gx_layout as
+ *                    for mxconv_dgrad; gw, workspace, ws_bytes as for
+ *                    mxconv_wgrad.
+ * Errors: NULL, ARG (also deferred not 0 or 1), SHAPE, WORKSPACE, ALIGN, HIP,
+ * all checked before anything is launched. */
+int mxconv_backward(const mxc_conv* cv, int fmt,
+                    const void* w_codes, const uint8_t* w_scales,
+                    const void* gy_codes, const uint8_t* gy_scales,
+                    const void* x_codes, const uint8_t* x_scales,
+                    float* gx, int gx_layout, float* gw,
+                    void* workspace, size_t ws_bytes, int deferred, void* stream);
+
 /* ------------------------------------------------------------------ a6 */
 /* Naive comparator (the baseline of Sec. III-C and Table I): the im2col is
  * done in full precision first, and every GEMM operand is then quantized

@@ -1383,6 +1383,22 @@ int launch_wgrad(const Conv& cv, const void* gc, const uint8_t* gs, const void* 
     return launch_reduce(cv, (const float*)ws, gw, pl.splits, s);
 }
 
+int launch_backward(const Conv& dcv, const void* wc, const uint8_t* ws, const void* gc, const uint8_t* gs,
+                    float* gx, int layout, const Conv& wcv, const void* xc, const uint8_t* xs, float* gw,
+                    void* wsp, hipStream_t s, bool defer) {
+    const int ls = wgrad_lean_splits(wcv);
+    if (ls > 0) {
+        const int rc = launch_lean_bwd(dcv, wc, ws, gc, gs, gx, layout, wcv, xc, xs, ls > 1 ? (float*)wsp : gw, ls, s);
+        if (rc != 1) {
+            if (rc || ls == 1 || defer) return rc;
+            return launch_reduce(wcv, (const float*)wsp, gw, ls, s);
+        }
+    }
+    const int rc = launch_dgrad(dcv, wc, ws, gc, gs, gx, layout, s);
+    if (rc) return rc;
+    return launch_wgrad(wcv, gc, gs, xc, xs, gw, wsp, s, nullptr, nullptr, defer);
+}
+
 int wgrad_pending_splits(const Conv& cv) {
     const int ls = wgrad_lean_splits(cv);
     if (ls > 0) return ls > 1 ? ls : 0;

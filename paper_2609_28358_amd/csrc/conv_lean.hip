@@ -36,6 +36,8 @@
 #include "mx_internal.h"
 
 namespace mxc {
+#include "wgrad_tile.h"
+
 namespace {
 
 constexpr int LT = 256;
@@ -605,11 +607,12 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
     }
 }
 
+// Workgroup `bid` of `nblk` (a multiple of 8).
 template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW, bool NV = false>
-__global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
+__device__ __forceinline__ void lean_body(const LeanArgs& p, int bid, int nblk) {
     // XCD-aware order: consecutive tiles (same output row) on one XCD
-    const int per_xcd = (gridDim.x + 7) / 8;
-    const int lin = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+    const int per_xcd = (nblk + 7) / 8;
+    const int lin = (bid % 8) * per_xcd + bid / 8;
     if (lin >= p.ntiles) return;
     Phase f;
     f.ry = 0; f.rx = 0; f.kh0 = 0; f.nvh = p.kh; f.kw0 = 0;
@@ -617,12 +620,17 @@ __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
     lean_tile<FW, FX, DG, KW, S, WGM, PW, NV>(p, lin, f);
 }
 
+template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW, bool NV = false>
+__global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
+    lean_body<FW, FX, DG, KW, S, WGM, PW, NV>(p, blockIdx.x, gridDim.x);
+}
+
 // Stride-2 input gradient for kernel width KWF (1 or 3): the four phases in
 // one launch, tiles of phase (ry, rx) at [pofs[2 ry + rx], pofs[2 ry + rx + 1]).
 template <int FW, int FX, int KWF, int WGM, int PW, bool NV = false>
-__global__ __launch_bounds__(LT) void conv_lean_dg2_kernel(LeanArgs p) {
-    const int per_xcd = (gridDim.x + 7) / 8;
-    int lin = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+__device__ __forceinline__ void lean_dg2_body(const LeanArgs& p, int bid, int nblk) {
+    const int per_xcd = (nblk + 7) / 8;
+    int lin = (bid % 8) * per_xcd + bid / 8;
     if (lin >= p.pofs[4]) return;
     int ph = 0;
     while (ph < 3 && lin >= p.pofs[ph + 1]) ph++;
@@ -640,6 +648,29 @@ __global__ __launch_bounds__(LT) void conv_lean_dg2_kernel(LeanArgs p) {
     else                      lean_tile<FW, FX, true, 1, 2, WGM, PW, NV>(p, lin, f);
 }
 
+template <int FW, int FX, int KWF, int WGM, int PW, bool NV = false>
+__global__ __launch_bounds__(LT) void conv_lean_dg2_kernel(LeanArgs p) {
+    lean_dg2_body<FW, FX, KWF, WGM, PW, NV>(p, blockIdx.x, gridDim.x);
+}
+
+// The input gradient of a layer (stride 1 with KW taps per row, or, with
+// DG2, the four stride-2 phases of kernel width KW) and its weight gradient
+// in one launch: workgroups [0, nl) take input-gradient tiles, the rest
+// weight-gradient tiles.  Both only read the quantized G_Y (with W, resp. X),
+// so neither waits for the other, and the tail of one fills the CUs the
+// other leaves idle.  Format F for every operand.
+template <int F, int KW, int PW, bool DG2>
+__global__ __launch_bounds__(LT) void conv_lean_bwd_kernel(LeanArgs p, WLArgs q, int nl) {
+    extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
+    const int b = blockIdx.x;
+    if (b < nl) {
+        if constexpr (DG2) lean_dg2_body<F, F, KW, 1, PW>(p, b, nl);
+        else               lean_body<F, F, true, KW, 1, 1, PW>(p, b, nl);
+    } else {
+        wgrad_tile<F, F>(q, b - nl, (int)gridDim.x - nl, (float (*)[64 * 64])smem);
+    }
+}
+
 // LDS bytes of one launch: the stage ring, and at least the 4 x 4 KB the
 // epilogue stages through.
 inline size_t lean_lds(const LeanArgs& a, int nbufs_used) {
@@ -652,7 +683,7 @@ inline size_t lean_lds(const LeanArgs& a, int nbufs_used) {
 // raise it on every launch).  Concurrent first calls may both raise it, which
 // is harmless.
 template <typename K>
-int lean_launch(K kernel, std::atomic<uint64_t>& devs, const LeanArgs& a, int ntiles, size_t lds, hipStream_t s) {
+int raise_lds(K kernel, std::atomic<uint64_t>& devs, size_t lds) {
     if (lds > 65536) {
         int dev = 0;
         if (hipGetDevice(&dev) != hipSuccess) return MXC_ERR_HIP;
@@ -664,6 +695,12 @@ int lean_launch(K kernel, std::atomic<uint64_t>& devs, const LeanArgs& a, int nt
             devs.fetch_or(bit, std::memory_order_release);
         }
     }
+    return MXC_OK;
+}
+
+template <typename K>
+int lean_launch(K kernel, std::atomic<uint64_t>& devs, const LeanArgs& a, int ntiles, size_t lds, hipStream_t s) {
+    if (raise_lds(kernel, devs, lds)) return MXC_ERR_HIP;
     const int grid = (ntiles + 7) / 8 * 8;
     hipLaunchKernelGGL(kernel, dim3(grid), dim3(LT), lds, s, a);
     return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
@@ -713,11 +750,18 @@ int launch_lean_dir(const LeanArgs& a, bool dg, int kw, int sw, int wgm, int pw,
 
 }  // namespace
 
-// Returns 1 when the layer is outside this kernel's shapes (the caller then
-// uses the general kernels), else an MXC_* code.
-int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const void* sc,
-                     const uint8_t* ss, float* out, int layout, hipStream_t s, const FusedEpi* q,
-                     const float* nv_tw, const float* nv_tx) {
+namespace {
+
+struct LeanPlan {
+    LeanArgs a;
+    int wgm, pw, nstage, used;
+    bool dg2;
+};
+
+// The tile shape, stage layout and ring depth of one launch; returns 0, 1
+// when the layer is outside this kernel's shapes, or an MXC_* code.
+int lean_plan(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const void* sc, const uint8_t* ss,
+              float* out, int layout, const FusedEpi* q, const float* nv_tw, const float* nv_tx, LeanPlan& P) {
     const bool nv = nv_tw != nullptr;
     if (nv && (q || cv.fa != MXC_E2M1 || cv.fb != MXC_E2M1)) return MXC_ERR_ARG;
     if (cv.x.bn != 32) return 1;
@@ -726,7 +770,7 @@ int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws,
     // column stride 1 or 2, any row stride
     const bool dg2 = dg && cv.sh == 2 && cv.sw == 2;
     if (dg ? !(dg2 || (cv.sh == 1 && cv.sw == 1)) : (cv.sw != 1 && cv.sw != 2)) return 1;
-    LeanArgs a;
+    LeanArgs& a = P.a;
     a.wc = (const uint8_t*)wc; a.ws = ws; a.sc = (const uint8_t*)sc; a.ss = ss;
     a.out = out; a.layout = layout;
     a.M = dg ? cv.cin : cv.cout;
@@ -799,6 +843,42 @@ int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws,
         if ((long)per_cu * b * a.stage_bytes <= LDS_MAX) { nbuf = b; break; }
     a.nbuf = nbuf;
     const int used = nbuf < nstage ? nbuf : nstage;
+    P.wgm = wgm; P.pw = pw; P.nstage = nstage; P.used = used; P.dg2 = dg2;
+    return 0;
+}
+
+template <int F, int KW, int PW, bool DG2>
+int bwd_launch(const LeanArgs& a, const WLArgs& q, int nl, int grid, size_t lds, hipStream_t s) {
+    static std::atomic<uint64_t> devs{0};
+    if (raise_lds(conv_lean_bwd_kernel<F, KW, PW, DG2>, devs, lds)) return MXC_ERR_HIP;
+    hipLaunchKernelGGL((conv_lean_bwd_kernel<F, KW, PW, DG2>), dim3(grid), dim3(LT), lds, s, a, q, nl);
+    return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
+}
+
+template <int F>
+int bwd_launch_f(const LeanArgs& a, const WLArgs& q, int nl, int grid, size_t lds, bool dg2, int kw, int pw,
+                 hipStream_t s) {
+    if (dg2) {
+        if (kw == 3) return pw == 1 ? bwd_launch<F, 3, 1, true>(a, q, nl, grid, lds, s) : bwd_launch<F, 3, 2, true>(a, q, nl, grid, lds, s);
+        return pw == 1 ? bwd_launch<F, 1, 1, true>(a, q, nl, grid, lds, s) : bwd_launch<F, 1, 2, true>(a, q, nl, grid, lds, s);
+    }
+    if (kw == 3) return pw == 1 ? bwd_launch<F, 3, 1, false>(a, q, nl, grid, lds, s) : bwd_launch<F, 3, 2, false>(a, q, nl, grid, lds, s);
+    return pw == 1 ? bwd_launch<F, 1, 1, false>(a, q, nl, grid, lds, s) : bwd_launch<F, 1, 2, false>(a, q, nl, grid, lds, s);
+}
+
+}  // namespace
+
+// Returns 1 when the layer is outside this kernel's shapes (the caller then
+// uses the general kernels), else an MXC_* code.
+int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const void* sc,
+                     const uint8_t* ss, float* out, int layout, hipStream_t s, const FusedEpi* q,
+                     const float* nv_tw, const float* nv_tx) {
+    LeanPlan P;
+    const int prc = lean_plan(cv, dg, wc, ws, sc, ss, out, layout, q, nv_tw, nv_tx, P);
+    if (prc) return prc;
+    const LeanArgs& a = P.a;
+    const bool nv = nv_tw != nullptr;
+    const int wgm = P.wgm, pw = P.pw, used = P.used;
     if (nv) return launch_lean_dir<MXC_E2M1, MXC_E2M1, true>(a, dg, cv.kw, cv.sw, wgm, pw, used, s);
     if (cv.fa == MXC_E4M3 && cv.fb == MXC_E4M3)
         return launch_lean_dir<MXC_E4M3, MXC_E4M3>(a, dg, cv.kw, cv.sw, wgm, pw, used, s);
@@ -809,6 +889,40 @@ int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws,
     if (cv.fa == MXC_E2M1 && cv.fb == MXC_E3M2)
         return launch_lean_dir<MXC_E2M1, MXC_E3M2>(a, dg, cv.kw, cv.sw, wgm, pw, used, s);
     return MXC_ERR_ARG;
+}
+
+// Input gradient (dcv) and weight gradient (wcv, `splits` ways into wdst) of
+// one layer in one launch; returns 1 when the layer or its formats are
+// outside the grouped kernel (the caller then launches the two separately).
+int launch_lean_bwd(const Conv& dcv, const void* wc, const uint8_t* ws, const void* gc, const uint8_t* gs,
+                    float* gx, int layout, const Conv& wcv, const void* xc, const uint8_t* xs, float* wdst,
+                    int splits, hipStream_t s) {
+    const int f = dcv.fa;
+    if ((f != MXC_E4M3 && f != MXC_E2M1) || dcv.fb != f || wcv.fa != f || wcv.fb != f) return 1;
+    LeanPlan P;
+    const int prc = lean_plan(dcv, true, wc, ws, gc, gs, gx, layout, nullptr, nullptr, nullptr, P);
+    if (prc) return prc;
+    WLArgs q;
+    const long wg = wgrad_lean_fill(wcv, gc, gs, xc, xs, wdst, splits, nullptr, nullptr, q);
+    if (wg < 0) return MXC_ERR_SHAPE;
+    LeanArgs& a = P.a;
+    const long nl = ((long)(P.dg2 ? a.pofs[4] : a.ntiles) + 7) / 8 * 8;
+    if (nl + wg > 0x7FFFFFFFL) return MXC_ERR_SHAPE;
+    // ring depth for the combined grid, every workgroup holding at least the
+    // 64 KB the weight-gradient tile sums its waves through
+    const long per_cu = (nl + wg + 255) / 256;
+    int nbuf = 2;
+    for (int b = 4; b > 2; b--) {
+        const long need = (long)b * a.stage_bytes > 65536 ? (long)b * a.stage_bytes : 65536;
+        if (per_cu * need <= LDS_MAX) { nbuf = b; break; }
+    }
+    a.nbuf = nbuf;
+    const int used = nbuf < P.nstage ? nbuf : P.nstage;
+    size_t lds = lean_lds(a, used);
+    if (lds < 65536) lds = 65536;
+    const int grid = (int)(nl + wg);
+    return f == MXC_E4M3 ? bwd_launch_f<MXC_E4M3>(a, q, (int)nl, grid, lds, P.dg2, dcv.kw, P.pw, s)
+                         : bwd_launch_f<MXC_E2M1>(a, q, (int)nl, grid, lds, P.dg2, dcv.kw, P.pw, s);
 }
 
 }  // namespace mxc

@@ -99,6 +99,15 @@ struct FusedEpi {
 int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const void* sc,
                      const uint8_t* ss, float* out, int layout, hipStream_t s, const FusedEpi* q = nullptr,
                      const float* nv_tw = nullptr, const float* nv_tx = nullptr);
+// input gradient and batch-block-32 weight gradient of one layer in one
+// launch (conv_lean.hip); 1 when the layer or its formats are outside it
+int launch_lean_bwd(const Conv& dcv, const void* wc, const uint8_t* ws, const void* gc, const uint8_t* gs,
+                    float* gx, int layout, const Conv& wcv, const void* xc, const uint8_t* xs, float* wdst,
+                    int splits, hipStream_t s);
+// dgrad then wgrad (conv_gemm.hip), grouped into one launch where it applies
+int launch_backward(const Conv& dcv, const void* wc, const uint8_t* ws, const void* gc, const uint8_t* gs,
+                    float* gx, int layout, const Conv& wcv, const void* xc, const uint8_t* xs, float* gw,
+                    void* wsp, hipStream_t s, bool defer);
 // weight gradient for batch block 32 (wgrad_lean.hip): number of K splits
 // (0: not applicable); with more than one split the partial tiles go to the
 // workspace and are reduced by the caller

@@ -309,6 +309,26 @@ int mxconv_wgrad_deferred(const mxc_conv* p, int fmt, const void* gc, const uint
     return wgrad_call(p, fmt, gc, gs, xc, xs, gw, workspace, ws_bytes, stream, true);
 }
 
+int mxconv_backward(const mxc_conv* p, int fmt, const void* wc, const uint8_t* ws, const void* gc,
+                    const uint8_t* gs, const void* xc, const uint8_t* xs, float* gx, int gx_layout, float* gw,
+                    void* workspace, size_t ws_bytes, int deferred, void* stream) {
+    if (!p || !wc || !ws || !gc || !gs || !xc || !xs || !gx || !gw) return MXC_ERR_NULL;
+    if (gx_layout != MXC_NCHW && gx_layout != MXC_CBF) return MXC_ERR_ARG;
+    if (deferred != 0 && deferred != 1) return MXC_ERR_ARG;
+    Conv dcv, wcv;
+    int rc = conv_init(&dcv, p, fmt, CONV_DGRAD);
+    if (rc) return rc;
+    rc = conv_init(&wcv, p, fmt, CONV_WGRAD);
+    if (rc) return rc;
+    const size_t need = wgrad_workspace(wcv);
+    if (need && (!workspace || ws_bytes < need)) return MXC_ERR_WORKSPACE;
+    if (!aligned16(wc) || !aligned16(ws) || !aligned16(gc) || !aligned16(gs) || !aligned16(xc) ||
+        !aligned16(xs) || !aligned16(gx) || !aligned16(gw) || (need && !aligned16(workspace)))
+        return MXC_ERR_ALIGN;
+    return launch_backward(dcv, wc, ws, gc, gs, gx, gx_layout, wcv, xc, xs, gw, workspace, (hipStream_t)stream,
+                           deferred == 1);
+}
+
 int mxconv_wgrad_reduce_multi(int count, const mxc_wjob* jobs, void* stream) {
     if (count < 0 || count > MXC_WREDUCE_MAX) return MXC_ERR_ARG;
     if (count > 0 && !jobs) return MXC_ERR_NULL;

@@ -1,0 +1,245 @@
+// wgrad_tile.h -- the weight-gradient tile of the batch-block-32 kernel
+// (a5), shared by its own kernel and by the grouped backward launch.
+// Included inside namespace mxc by .hip files only.
+#pragma once
+
+namespace {
+
+
+constexpr int WT = 256;
+
+__device__ __attribute__((aligned(16))) uint8_t g_zero_wl[64];
+
+struct WLArgs {
+    const uint8_t* gc;
+    const uint8_t* gs;
+    const uint8_t* xc;
+    const uint8_t* xs;
+    float* dst;
+    int direct;                    // 1: dst is G_W (OIHW); 0: partial tiles
+    int cout, cin, kh, kw, sh, sw, ph, pw, ho, wo, h, w;
+    int gy_ncb, x_ncb, gy_cp, x_cp, ntot;
+    int npix, npairs;              // output pixels (all batch groups), pixel pairs
+    int cot, cit, ntiles;          // 64-row / 64-column tile counts, tiles
+    int ppw;                       // pixel pairs per wave
+    int nsplit;
+    // NVFP4 operands: gs / xs hold E4M3 scales per 8x8 block ([pixel][Cp/8][4]:
+    // a row's four sample groups in four consecutive bytes); tg, tx the
+    // per-tensor scales
+    const float* tg;
+    const float* tx;
+};
+
+// One operand's fragment for a K step: K block 0 from pixel row p0, K block
+// 1 from p1 (rows already offset to this lane's row; zero block if invalid).
+// FP8: 16 bytes of each (the lane's half of the row); FP4 and FP6: the whole
+// row of the lane's own K block (ph = p0 or p1 by lane half).
+template <int F>
+__device__ __forceinline__ v8i row_frag(const uint8_t* p0, const uint8_t* p1, const uint8_t* ph) {
+    v8i o;
+    if constexpr (F == MXC_E4M3) {
+        const v4i u = *(const v4i*)p0, v = *(const v4i*)p1;
+#pragma unroll
+        for (int e = 0; e < 4; e++) { o[e] = u[e]; o[4 + e] = v[e]; }
+    } else if constexpr (fmt_bits(F) == 6) {
+        const v2i a = *(const v2i*)ph, b = *(const v2i*)(ph + 8), c = *(const v2i*)(ph + 16);
+        o[0] = a[0]; o[1] = a[1]; o[2] = b[0]; o[3] = b[1]; o[4] = c[0]; o[5] = c[1];
+        o[6] = o[7] = 0;
+    } else {
+        const v4i u = *(const v4i*)ph;
+#pragma unroll
+        for (int e = 0; e < 4; e++) { o[e] = u[e]; o[4 + e] = 0; }
+    }
+    return o;
+}
+
+// NV: NVFP4 operands, decoded to fp16 per fragment and multiplied on fp16
+// MFMAs (the 8-sample groups of a row each have their own E4M3 scale).
+template <int FA, int FB, bool NV = false>
+__device__ __forceinline__ void wgrad_tile(const WLArgs& p, int bid, int nblk, float (*red)[64 * 64]) {
+    static_assert(!NV || (FA == MXC_E2M1 && FB == MXC_E2M1), "NVFP4 operands only");
+    constexpr int RBA = 32 * fmt_bits(FA) / 8;    // bytes of one block row (32 samples): G_Y
+    constexpr int RBB = 32 * fmt_bits(FB) / 8;    // X
+    constexpr int TBA = 32 * RBA, TBB = 32 * RBB; // bytes of one block
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    // XCD-aware order: workgroups are dealt round-robin to the 8 XCDs; give
+    // each XCD a contiguous range of (split, tile), so the tiles (taps, channel
+    // blocks) that read the same pixels share that XCD's L2
+    const int per_xcd = (nblk + 7) / 8;
+    const int lin = (bid % 8) * per_xcd + bid / 8;
+    if (lin >= p.ntiles * p.nsplit) return;
+    const int tile = lin % p.ntiles, split = lin / p.ntiles;
+    const int tap = tile / (p.cot * p.cit);
+    const int rc = tile % (p.cot * p.cit);
+    const int cop = rc / p.cit, cip = rc % p.cit;
+    const int th = tap / p.kw, tw = tap % p.kw;
+    const int r = lane & 31, hf = lane >> 5;
+
+    // lane offsets inside one pixel's codes, and block validity
+    uint32_t a_off[2], b_off[2];
+    bool a_ok[2], b_ok[2];
+#pragma unroll
+    for (int i = 0; i < 2; i++) {
+        const int cob = 2 * cop + i, cib = 2 * cip + i;
+        a_ok[i] = cob < p.gy_ncb;
+        b_ok[i] = cib < p.x_ncb;
+        a_off[i] = (uint32_t)(a_ok[i] ? cob : 0) * TBA + r * RBA + (FA == MXC_E4M3 ? 16 * hf : 0);
+        b_off[i] = (uint32_t)(b_ok[i] ? cib : 0) * TBB + r * RBB + (FB == MXC_E4M3 ? 16 * hf : 0);
+    }
+    const uint32_t gy_pix = (uint32_t)p.gy_ncb * TBA, x_pix = (uint32_t)p.x_ncb * TBB;
+
+    v16f acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; i++)
+#pragma unroll
+        for (int j = 0; j < 2; j++)
+#pragma unroll
+            for (int e = 0; e < 16; e++) acc[i][j][e] = 0.0f;
+
+    const int wid = split * 4 + wave;
+    const int q0 = wid * p.ppw;
+    const int q1 = min(p.npairs, q0 + p.ppw);
+
+    // operands of pair q (pixels 2q, 2q + 1)
+    struct Ops {
+        v8i a[2], b[2];
+        int sa[2], sb[2];
+        uint32_t na[2], nb[2];     // NV: the four E4M3 scales of the lane's row
+    };
+    auto load = [&](int q, bool live, Ops& o) {
+        int pg[2];                 // pixel index (or -1) of K block 0 / 1
+        int qpix[2];               // tap's input pixel (or -1)
+#pragma unroll
+        for (int k = 0; k < 2; k++) {
+            const int P = 2 * q + k;
+            pg[k] = live && P < p.npix ? P : -1;
+            qpix[k] = -1;
+            if (pg[k] >= 0) {
+                const int ox = P % p.wo, t = P / p.wo;
+                const int oy = t % p.ho, g = t / p.ho;
+                const int iy = oy * p.sh + th - p.ph, ix = ox * p.sw + tw - p.pw;
+                if (iy >= 0 && iy < p.h && ix >= 0 && ix < p.w) qpix[k] = (g * p.h + iy) * p.w + ix;
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < 2; i++) {
+            const uint8_t* ap[2];
+            const uint8_t* bp[2];
+#pragma unroll
+            for (int k = 0; k < 2; k++) {
+                ap[k] = (pg[k] >= 0 && a_ok[i]) ? p.gc + (size_t)pg[k] * gy_pix + a_off[i] : g_zero_wl;
+                bp[k] = (qpix[k] >= 0 && b_ok[i]) ? p.xc + (size_t)qpix[k] * x_pix + b_off[i] : g_zero_wl;
+            }
+            o.a[i] = row_frag<FA>(ap[0], ap[1], ap[hf]);
+            o.b[i] = row_frag<FB>(bp[0], bp[1], bp[hf]);
+            // scale of (row, K block hf): the pixel of this lane's half
+            const int P = pg[hf], Q = qpix[hf];
+            const int cob = 2 * cop + i, cib = 2 * cip + i;
+            const uint8_t sa = p.gs[(P >= 0 && a_ok[i]) ? (size_t)P * p.gy_ncb + cob : 0];
+            const uint8_t sb = p.xs[(Q >= 0 && b_ok[i]) ? (size_t)Q * p.x_ncb + cib : 0];
+            o.sa[i] = (P >= 0 && a_ok[i]) ? sa : 0;
+            o.sb[i] = (Q >= 0 && b_ok[i]) ? sb : 0;
+            if constexpr (NV) {
+                const uint32_t* ga = (const uint32_t*)p.gs;
+                const uint32_t* xa = (const uint32_t*)p.xs;
+                const uint32_t va = ga[(P >= 0 && a_ok[i]) ? ((size_t)P * (p.gy_cp / 8) + cob * 4 + (r >> 3)) : 0];
+                const uint32_t vb = xa[(Q >= 0 && b_ok[i]) ? ((size_t)Q * (p.x_cp / 8) + cib * 4 + (r >> 3)) : 0];
+                o.na[i] = (P >= 0 && a_ok[i]) ? va : 0u;
+                o.nb[i] = (Q >= 0 && b_ok[i]) ? vb : 0u;
+            }
+        }
+    };
+
+    // batches of PB pairs: all loads of a batch are in flight together (the
+    // loop is bound by memory latency, not by the MFMAs); pairs past the
+    // wave's range get a zero G_Y operand and add nothing
+    constexpr int PB = NV ? 2 : 4;
+    for (int q = q0; q < q1; q += PB) {
+        Ops o[PB];
+#pragma unroll
+        for (int b = 0; b < PB; b++) load(q + b, q + b < q1, o[b]);
+#pragma unroll
+        for (int b = 0; b < PB; b++) {
+            if constexpr (NV) {
+                uint32_t ad[2][16], bd[2][16];
+#pragma unroll
+                for (int i = 0; i < 2; i++) {
+                    nv_decode32(o[b].a[i], o[b].na[i], ad[i]);
+                    nv_decode32(o[b].b[i], o[b].nb[i], bd[i]);
+                }
+#pragma unroll
+                for (int i = 0; i < 2; i++)
+#pragma unroll
+                    for (int j = 0; j < 2; j++) acc[i][j] = mfma_nv(ad[i], bd[j], acc[i][j]);
+            } else {
+#pragma unroll
+                for (int i = 0; i < 2; i++)
+#pragma unroll
+                    for (int j = 0; j < 2; j++)
+                        acc[i][j] = mfma_mx<FA, FB>(o[b].a[i], o[b].b[j], acc[i][j], o[b].sa[i], o[b].sb[j]);
+            }
+        }
+    }
+    if constexpr (NV) {   // the per-tensor scales T_GY T_X
+        const float tt = *p.tg * *p.tx;
+#pragma unroll
+        for (int i = 0; i < 2; i++)
+#pragma unroll
+            for (int j = 0; j < 2; j++)
+#pragma unroll
+                for (int e = 0; e < 16; e++) acc[i][j][e] *= tt;
+    }
+
+    // ---- sum the four waves' tiles, then write
+#pragma unroll
+    for (int i = 0; i < 2; i++)
+#pragma unroll
+        for (int j = 0; j < 2; j++)
+#pragma unroll
+            for (int e = 0; e < 16; e++) {
+                const int row = 32 * i + 8 * (e >> 2) + 4 * hf + (e & 3);
+                red[wave][row * 64 + 32 * j + r] = acc[i][j][e];
+            }
+    __syncthreads();
+#pragma unroll 4
+    for (int k = 0; k < 16; k++) {
+        const int idx = tid + WT * k;
+        const int row = idx >> 6, col = idx & 63;
+        const float v = (red[0][idx] + red[1][idx]) + (red[2][idx] + red[3][idx]);
+        const int co = cop * 64 + row, ci = cip * 64 + col;
+        if (p.direct) {
+            if (co < p.cout && ci < p.cin)
+                p.dst[(((size_t)co * p.cin + ci) * p.kh + th) * p.kw + tw] = v;
+        } else if (co < p.gy_cp && ci < p.x_cp) {
+            p.dst[((size_t)split * p.gy_cp + co) * p.ntot + (size_t)tap * p.x_cp + ci] = v;
+        }
+    }
+}
+
+// The tile arguments for one layer split `splits` ways over its pixel pairs
+// (dst: G_W when splits == 1, else the partial tiles); returns the workgroup
+// count (a multiple of 8), or -1 past the 32-bit grid.
+inline long wgrad_lean_fill(const Conv& cv, const void* gc, const uint8_t* gs, const void* xc, const uint8_t* xs,
+                            float* dst, int splits, const float* nv_tg, const float* nv_tx, WLArgs& a) {
+    a.gc = (const uint8_t*)gc; a.gs = gs; a.xc = (const uint8_t*)xc; a.xs = xs;
+    a.dst = dst;
+    a.tg = nv_tg; a.tx = nv_tx;
+    a.direct = splits == 1;
+    a.cout = cv.cout; a.cin = cv.cin; a.kh = cv.kh; a.kw = cv.kw; a.sh = cv.sh; a.sw = cv.sw;
+    a.ph = cv.ph; a.pw = cv.pw; a.ho = cv.ho; a.wo = cv.wo; a.h = cv.h; a.w = cv.w;
+    a.gy_ncb = cv.gy.ncb; a.x_ncb = cv.x.ncb; a.gy_cp = cv.gy.cp; a.x_cp = cv.x.cp;
+    a.ntot = cv.kh * cv.kw * cv.x.cp;
+    a.npix = cv.x.ng * cv.ho * cv.wo;
+    a.npairs = (a.npix + 1) / 2;
+    a.cot = (cv.gy.ncb + 1) / 2; a.cit = (cv.x.ncb + 1) / 2;
+    a.ntiles = cv.kh * cv.kw * a.cot * a.cit;
+    const int waves = splits * 4;
+    a.ppw = (a.npairs + waves - 1) / waves;
+    a.nsplit = splits;
+    const long grid = ((long)a.ntiles * splits + 7) / 8 * 8;
+    return grid > 0x7FFFFFFFL ? -1 : grid;
+}
+
+}  // namespace

@@ -81,6 +81,7 @@ def lib():
         "mxconv_dgrad": (i32, [CP, i32, P, P, P, P, P, i32, P]),
         "mxconv_wgrad": (i32, [CP, i32, P, P, P, P, P, P, sz, P]),
         "mxconv_wgrad_deferred": (i32, [CP, i32, P, P, P, P, P, P, sz, P]),
+        "mxconv_backward": (i32, [CP, i32, P, P, P, P, P, P, P, i32, P, P, sz, i32, P]),
         "mxconv_wgrad_reduce_multi": (i32, [i32, ctypes.POINTER(MxcWJob), P]),
         "mxconv_fwd_quant": (i32, [CP, i32, P, P, P, P, i32, i32, P, P, P, P]),
         "mxconv_dgrad_quant": (i32, [CP, i32, P, P, P, P, i32, P, i32, P, P, P, P]),
@@ -352,6 +353,28 @@ def wgrad(cv, gy, x, out=None, workspace=None, stream=None, deferred=False):
     _check(fn(ctypes.byref(conv_struct(cv)), pair(gy.fmt, x.fmt), _ptr(gy.codes), _ptr(gy.scales),
               _ptr(x.codes), _ptr(x.scales), _ptr(gw), _ptr(workspace), wsz, _stream(stream)), name)
     return gw
+
+
+def backward(cv, w, gy, x, layout=NCHW, gx_out=None, gw_out=None, workspace=None, stream=None, deferred=False):
+    """Input and weight gradients of one layer from one call: (G_X, G_W), bit
+    for bit what dgrad() and wgrad() give (one launch where the layer allows)."""
+    f = pair(w.fmt, gy.fmt)
+    if pair(gy.fmt, x.fmt) != f:
+        raise MxconvError("backward needs the same format pair for (W, G_Y) and (G_Y, X)")
+    dev = gy.codes.device
+    gx = _out((cv["n"], cv["cin"], cv["h"], cv["w"]), layout, batch_block(cv["n"]), dev, gx_out)
+    gw = gw_out if gw_out is not None else torch.empty((cv["cout"], cv["cin"], cv["kh"], cv["kw"]),
+                                                       dtype=torch.float32, device=dev)
+    need = wgrad_workspace_bytes(cv, f)
+    if workspace is None and need:
+        if deferred:
+            raise MxconvError("a deferred weight gradient needs the caller's workspace")
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    wsz = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(lib().mxconv_backward(ctypes.byref(conv_struct(cv)), f, _ptr(w.codes), _ptr(w.scales), _ptr(gy.codes),
+                                 _ptr(gy.scales), _ptr(x.codes), _ptr(x.scales), _ptr(gx), layout, _ptr(gw),
+                                 _ptr(workspace), wsz, 1 if deferred else 0, _stream(stream)), "mxconv_backward")
+    return gx, gw
 
 
 def wgrad_reduce_multi(items, stream=None):

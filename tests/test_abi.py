@@ -373,3 +373,27 @@ def test_size_limits():
     assert L.mxconv_quantize_multi(1, (mx.MxcQJob * 1)(j), None) == -3
     ok = mx.conv_struct(synth.conv_dict(32, 32, 32, 300, 300, 255, 1, 127))       # 65025 taps
     assert L.mxconv_im2col_codes_bytes(ctypes.byref(ok), 0) > 0
+
+
+def test_backward_errors():
+    L = mx.lib()
+    cv = mx.conv_struct(synth.conv_dict(32, 64, 64, 56, 56, 3, 1, 1))        # needs a split-K workspace
+    r = ctypes.byref(cv)
+    need = L.mxconv_wgrad_workspace_bytes(r, 0)
+    assert need > 0
+
+    def call(conv=r, fmt=0, gx=GOOD, layout=mx.CBF, gw=GOOD, ws=GOOD, wsb=need, deferred=0, x=GOOD):
+        return L.mxconv_backward(conv, fmt, GOOD, GOOD, GOOD, GOOD, x, GOOD, gx, layout, gw, ws, wsb, deferred, None)
+
+    assert call(conv=None) == -1
+    assert call(gx=None) == -1
+    assert call(gw=None) == -1
+    assert call(x=None) == -1
+    assert call(layout=7) == -2
+    assert call(deferred=2) == -2
+    assert call(fmt=9) == -2
+    assert call(ws=None) == -6
+    assert call(wsb=need - 1) == -6
+    assert call(gw=0x10004) == -4
+    assert call(ws=0x10008) == -4
+    assert call(x=0x10002) == -4
