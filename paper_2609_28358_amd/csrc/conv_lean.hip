@@ -655,19 +655,22 @@ __global__ __launch_bounds__(LT) void conv_lean_dg2_kernel(LeanArgs p) {
 
 // The input gradient of a layer (stride 1 with KW taps per row, or, with
 // DG2, the four stride-2 phases of kernel width KW) and its weight gradient
-// in one launch: workgroups [0, nl) take input-gradient tiles, the rest
-// weight-gradient tiles.  Both only read the quantized G_Y (with W, resp. X),
-// so neither waits for the other, and the tail of one fills the CUs the
-// other leaves idle.  Format F for every operand.
+// in one launch: the last nl workgroups take input-gradient tiles, the ones
+// before them weight-gradient tiles (dispatched first: measured faster than
+// the other order).  Both only read the quantized G_Y (with W, resp. X), so
+// neither waits for the other, and the tail of one fills the CUs the other
+// leaves idle.  Both counts are multiples of 8, so each part keeps its own
+// kernel's XCD mapping.  Format F for every operand.
 template <int F, int KW, int PW, bool DG2>
 __global__ __launch_bounds__(LT) void conv_lean_bwd_kernel(LeanArgs p, WLArgs q, int nl) {
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
     const int b = blockIdx.x;
-    if (b < nl) {
-        if constexpr (DG2) lean_dg2_body<F, F, KW, 1, PW>(p, b, nl);
-        else               lean_body<F, F, true, KW, 1, 1, PW>(p, b, nl);
+    const int nw = (int)gridDim.x - nl;
+    if (b >= nw) {
+        if constexpr (DG2) lean_dg2_body<F, F, KW, 1, PW>(p, b - nw, nl);
+        else               lean_body<F, F, true, KW, 1, 1, PW>(p, b - nw, nl);
     } else {
-        wgrad_tile<F, F>(q, b - nl, (int)gridDim.x - nl, (float (*)[64 * 64])smem);
+        wgrad_tile<F, F>(q, b, nw, (float (*)[64 * 64])smem);
     }
 }
 
