@@ -361,6 +361,9 @@ int mxconv_wgrad_reduce_multi(int count, const mxc_wjob* jobs, void* stream);
  * launch, otherwise as the two calls one after the other.
  *   fmt              passed to both products as their fmt (so the pair
  *                    (W, G_Y) and the pair (G_Y, X) have the same formats).
+ *                    A mixed MXC_PAIR(a, b) with a != b is refused (ARG):
+ *                    G_Y would have to be read as b by the input gradient
+ *                    and as a by the weight gradient.
  *   w_*, gy_*, x_*   as for mxconv_dgrad and mxconv_wgrad; gx, gx_layout as
  *                    for mxconv_dgrad; gw, workspace, ws_bytes as for
  *                    mxconv_wgrad.

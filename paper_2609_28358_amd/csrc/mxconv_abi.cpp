@@ -315,6 +315,9 @@ int mxconv_backward(const mxc_conv* p, int fmt, const void* wc, const uint8_t* w
     if (!p || !wc || !ws || !gc || !gs || !xc || !xs || !gx || !gw) return MXC_ERR_NULL;
     if (gx_layout != MXC_NCHW && gx_layout != MXC_CBF) return MXC_ERR_ARG;
     if (deferred != 0 && deferred != 1) return MXC_ERR_ARG;
+    // one fmt names (W, G_Y) for the input gradient and (G_Y, X) for the
+    // weight gradient, so G_Y would take both halves of a mixed pair
+    if ((fmt & 0x10) && ((fmt >> 2) & 3) != (fmt & 3)) return MXC_ERR_ARG;
     Conv dcv, wcv;
     int rc = conv_init(&dcv, p, fmt, CONV_DGRAD);
     if (rc) return rc;

@@ -392,6 +392,11 @@ def test_backward_errors():
     assert call(layout=7) == -2
     assert call(deferred=2) == -2
     assert call(fmt=9) == -2
+    # a mixed pair would make G_Y one format for the input gradient and the
+    # other for the weight gradient: refused, while a pair of equal halves
+    # passes the format check (and reaches the workspace check here)
+    assert call(fmt=mx.pair(mx.E2M1, mx.E3M2)) == -2
+    assert call(fmt=mx.pair(mx.E2M1, mx.E2M1), ws=None) == -6
     assert call(ws=None) == -6
     assert call(wsb=need - 1) == -6
     assert call(gw=0x10004) == -4

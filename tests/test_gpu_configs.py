@@ -70,25 +70,21 @@ def _check_gemms(mx, cv, fmt, q, o, layout, seed):
     gx = mx.dgrad(cv, q["w"], q["gy"], layout=lay)
     gw = mx.wgrad(cv, q["gy"], q["x"])
     torch.cuda.synchronize()
-    ex = mxt.layer_exponents(o, cv, fmt) if fmt == oracle.E4M3 else None
     rng = np.random.default_rng(seed)
     errs = {}
     idx = _idx(rng, (cv["n"], cv["cout"], ho, wo), SAMPLES)
     r, s = oracle.fwd_at(cv, fmt, o["w"], o["x"], idx)
-    g = mxt.fwd_bound(cv, ex["x"], ex["w"], idx) if ex else None
-    errs["fwd"] = mxt.gemm_err(_gather(y, idx, (cv["n"], cv["cout"], ho, wo), layout, bn), r, s, g)
+    errs["fwd"] = mxt.gemm_err(_gather(y, idx, (cv["n"], cv["cout"], ho, wo), layout, bn), r, s)
     idx = _idx(rng, (cv["n"], cv["cin"], cv["h"], cv["w"]), SAMPLES)
     r, s = oracle.dgrad_at(cv, fmt, o["w"], o["gy"], idx)
-    g = mxt.dgrad_bound(cv, ex["gy"], ex["w"], idx) if ex else None
-    errs["dgrad"] = mxt.gemm_err(_gather(gx, idx, (cv["n"], cv["cin"], cv["h"], cv["w"]), layout, bn), r, s, g)
+    errs["dgrad"] = mxt.gemm_err(_gather(gx, idx, (cv["n"], cv["cin"], cv["h"], cv["w"]), layout, bn), r, s)
     wdims = (cv["cout"], cv["cin"], cv["kh"], cv["kw"])
     if np.prod(wdims) <= SAMPLES:                       # small weights: every element
         idx = np.stack(np.meshgrid(*[np.arange(d) for d in wdims], indexing="ij"), -1).reshape(-1, 4)
     else:
         idx = _idx(rng, wdims, SAMPLES // 4)
     r, s = oracle.wgrad_at(cv, fmt, o["gy"], o["x"], idx)
-    g = mxt.wgrad_bound(cv, ex["gy"], ex["x"], idx) if ex else None
-    errs["wgrad"] = mxt.gemm_err(gw.cpu().numpy()[tuple(idx.T)], r, s, g)
+    errs["wgrad"] = mxt.gemm_err(gw.cpu().numpy()[tuple(idx.T)], r, s)
     assert max(errs.values()) <= 1.0, errs
 
 

@@ -9,15 +9,16 @@ quantized.  Three checks per case:
     mxconv_dgrad output bit for bit (same kernel arithmetic);
   * the values agree with the oracle's fp64 result passed through the
     activation (forward) or multiplied by its derivative at z (input
-    gradient), within the GEMM bound of test_gpu_parity (1e-5 * S, plus
-    2^-10 * G for MXFP8) times the activation's Lipschitz constant (1 for
-    ReLU, 1.1 for SiLU), plus 1e-6 relative for the GPU's fp32 exp.
+    gradient), within the GEMM bound of test_gpu_parity (1e-5 * S) times
+    the activation's Lipschitz constant (1 for ReLU, 1.1 for SiLU), plus
+    1e-6 relative: the epilogue evaluates the activation in fp32 with the
+    hardware exp2 and reciprocal (about 1 ulp each), and an fp32 result
+    cannot be nearer than half an ulp to the fp64 reference anyway.
 """
 import numpy as np
 import pytest
 import torch
 
-import mx_tolerance as mxt
 import oracle
 from paper_2609_28358_amd import synth
 
@@ -47,20 +48,7 @@ def _layer(mx, cv, fmt, seed, kind="unit"):
 
 
 def _bound(cv, fmt, o, which, ref_shape, sabs):
-    tol = TOL * sabs
-    if fmt == 0:
-        ho, wo = synth.out_hw(cv)
-        shapes = {"x": (cv["n"], cv["cin"], cv["h"], cv["w"]), "w": (cv["cout"], cv["cin"], cv["kh"], cv["kw"]),
-                  "gy": (cv["n"], cv["cout"], ho, wo)}
-        e = {}
-        for k, role in (("x", oracle.ACT), ("w", oracle.WEIGHT), ("gy", oracle.ACT)):
-            d = oracle.dequant(*o[k], role, fmt, *shapes[k])
-            e[k] = mxt.elem_exponents(d, o[k][1], role, fmt, shapes[k])
-        idx = np.stack(np.meshgrid(*[np.arange(d) for d in ref_shape], indexing="ij"), -1).reshape(-1, 4)
-        g = (mxt.fwd_bound(cv, e["x"], e["w"], idx) if which == "fwd"
-             else mxt.dgrad_bound(cv, e["gy"], e["w"], idx)).reshape(ref_shape)
-        tol = tol + 2.0 ** -10 * g
-    return tol
+    return TOL * sabs
 
 
 def _codes_match(mx, act_cbf, shape, ofmt, q):
@@ -154,11 +142,6 @@ def test_fused_full_size_layer(mx, fmt):
     idx = np.stack([rng.integers(0, d, 2048) for d in shape], 1)
     r, s = oracle.fwd_at(cv, fmt, ow, ox, idx)
     tol = TOL * s
-    if fmt == 0:
-        d = {"x": oracle.dequant(*ox, oracle.ACT, fmt, *x.shape), "w": oracle.dequant(*ow, oracle.WEIGHT, fmt, *w.shape)}
-        ex = mxt.elem_exponents(d["x"], ox[1], oracle.ACT, fmt, tuple(x.shape))
-        ew = mxt.elem_exponents(d["w"], ow[1], oracle.WEIGHT, fmt, tuple(w.shape))
-        tol = tol + 2.0 ** -10 * mxt.fwd_bound(cv, ex, ew, idx)
     ref = oracle.act_fn(r, oracle.FN_SILU)
     got = a[tuple(idx.T)].astype(np.float64)
     assert np.all(np.abs(got - ref) <= 1.1 * tol + 1e-6 * np.abs(ref))

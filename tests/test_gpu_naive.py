@@ -2,13 +2,11 @@
 blocks along each GEMM's contraction) against the oracle's comparator.
 
 Codes and scales bit for bit; im2col bit for bit (a copy); GEMM outputs
-within 1e-5 * S (+ 2^-10 * G for MXFP8, the FP8 MFMA's grouped truncation;
-see mx_tolerance.py), with S and G from the oracle's operands."""
+within 1e-5 * S, with S = sum_k |a_k b_k| from the oracle's operands."""
 import numpy as np
 import pytest
 import torch
 
-import mx_tolerance as mxt
 import oracle
 from paper_2609_28358_amd import synth
 
@@ -82,14 +80,8 @@ def _nhwc(t):
     return t.permute(0, 2, 3, 1).contiguous()
 
 
-def _exps(m, direction, fmt):
-    codes, scales = oracle.quantize_1d(m, direction, fmt)
-    d = oracle.dequant_1d(codes, scales, m.shape[0], m.shape[1], direction, fmt)
-    return d, mxt.elem_exponents_1d(d, scales, direction, fmt)
-
-
-def _check(got, ref, sabs, gbound, what):
-    tol = 1e-5 * sabs + 2.0 ** -10 * gbound
+def _check(got, ref, sabs, what):
+    tol = 1e-5 * sabs
     err = np.abs(got.astype(np.float64) - ref)
     zero = sabs == 0
     assert not np.any(got[zero]), f"{what}: nonzero output where every product is zero"
@@ -120,19 +112,6 @@ def test_naive_path_matches_oracle(mx, fmt, cv):
     y_ref, sy = oracle.naive_fwd(cv, fmt, xn.numpy(), wm.numpy())
     gx_ref, sgx = oracle.naive_dgrad(cv, fmt, gyn.numpy(), wm.numpy())
     gw_ref, sgw = oracle.naive_wgrad(cv, fmt, gyn.numpy(), xn.numpy())
-    if fmt == 0:
-        _, e_c0 = _exps(ocol, 0, fmt)
-        _, e_w0 = _exps(wm.numpy(), 0, fmt)
-        _, e_g0 = _exps(gym.numpy(), 0, fmt)
-        _, e_w1 = _exps(wm.numpy(), 1, fmt)
-        _, e_g1 = _exps(gym.numpy(), 1, fmt)
-        _, e_c1 = _exps(ocol, 1, fmt)
-        g_y = mxt.nt_group_bound(e_c0, e_w0)                       # [P][cout], groups along K
-        g_col = mxt.nt_group_bound(e_g0, e_w1.T)                   # [P][K], groups along cout
-        g_gx = oracle.naive_col2im(cv, g_col)
-        g_gw = mxt.nt_group_bound(e_g1.T, e_c1.T)                  # [cout][K], groups along P
-    else:
-        g_y = g_gx = g_gw = 0.0
-    _check(y.cpu().numpy(), y_ref, sy, g_y, "fwd")
-    _check(gx.cpu().numpy(), gx_ref, sgx, g_gx, "dgrad")
-    _check(gw.cpu().numpy(), gw_ref, sgw, g_gw, "wgrad")
+    _check(y.cpu().numpy(), y_ref, sy, "fwd")
+    _check(gx.cpu().numpy(), gx_ref, sgx, "dgrad")
+    _check(gw.cpu().numpy(), gw_ref, sgw, "wgrad")

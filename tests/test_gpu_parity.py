@@ -3,9 +3,7 @@
 Codes and scales must match bit for bit.  GEMM outputs are compared with
 the oracle's fp64 results element by element: |gpu - oracle| <= 1e-5 * S,
 S = sum_k |a_k b_k| (the oracle's sum of absolute products, the error scale
-of an fp32 accumulation), for MXFP4; for MXFP8 the bound adds 2^-10 * G for
-the FP8 MFMA's grouped, truncating product alignment (see mx_tolerance.py).
-An output whose products are all zero must be exactly zero.  Inputs come from
+of an fp32 accumulation), for every format.  An output whose products are all zero must be exactly zero.  Inputs come from
 the seeded generators in paper_2609_28358_amd.synth.
 """
 import numpy as np
@@ -151,9 +149,6 @@ def _all_idx(*dims):
     return np.stack(np.meshgrid(*[np.arange(d) for d in dims], indexing="ij"), -1).reshape(-1, len(dims))
 
 
-_exps = mxt.layer_exponents
-
-
 def _layer(mx, cv, fmt, seed, kind="sweep"):
     x, w, gy = synth.layer_inputs(cv, seed, kind=kind)
     q = {k: mx.quantize(t.to(DEV), role, fmt) for k, t, role in
@@ -210,14 +205,7 @@ def test_gemms(mx, fmt, cv, layout):
     ry, sy = oracle.fwd(cv, fmt, o["w"], o["x"])
     rgx, sgx = oracle.dgrad(cv, fmt, o["w"], o["gy"])
     rgw, sgw = oracle.wgrad(cv, fmt, o["gy"], o["x"])
-    gy_, ggx, ggw = None, None, None
-    if fmt == 0:
-        e = _exps(o, cv, fmt)
-        gy_ = mxt.fwd_bound(cv, e["x"], e["w"], _all_idx(*ry.shape)).reshape(ry.shape)
-        ggx = mxt.dgrad_bound(cv, e["gy"], e["w"], _all_idx(*rgx.shape)).reshape(rgx.shape)
-        ggw = mxt.wgrad_bound(cv, e["gy"], e["x"], _all_idx(*rgw.shape)).reshape(rgw.shape)
-    e = (_err(y.cpu().numpy(), ry, sy, gy_), _err(gx.cpu().numpy(), rgx, sgx, ggx),
-         _err(gw.cpu().numpy(), rgw, sgw, ggw))
+    e = (_err(y.cpu().numpy(), ry, sy), _err(gx.cpu().numpy(), rgx, sgx), _err(gw.cpu().numpy(), rgw, sgw))
     assert max(e) <= 1.0, f"fwd/dgrad/wgrad error / allowed = {e}"
 
 
@@ -261,14 +249,13 @@ def test_sweep_layer_full_size(mx, fmt, li):
     gx = synth.cbf_to_nchw(gx.cpu(), cv["n"], cv["cin"], cv["h"], cv["w"], bn).numpy()
     gw = gw.cpu().numpy()
     S = 2048
-    ex = _exps(o, cv, fmt) if fmt == 0 else None
     idx = np.stack([rng.integers(0, d, S) for d in (cv["n"], cv["cout"], ho, wo)], 1)
     r, s = oracle.fwd_at(cv, fmt, o["w"], o["x"], idx)
-    ey = _err(y[tuple(idx.T)], r, s, mxt.fwd_bound(cv, ex["x"], ex["w"], idx) if ex else None)
+    ey = _err(y[tuple(idx.T)], r, s)
     idx = np.stack([rng.integers(0, d, S) for d in (cv["n"], cv["cin"], cv["h"], cv["w"])], 1)
     r, s = oracle.dgrad_at(cv, fmt, o["w"], o["gy"], idx)
-    egx = _err(gx[tuple(idx.T)], r, s, mxt.dgrad_bound(cv, ex["gy"], ex["w"], idx) if ex else None)
+    egx = _err(gx[tuple(idx.T)], r, s)
     idx = np.stack([rng.integers(0, d, S // 8) for d in (cv["cout"], cv["cin"], cv["kh"], cv["kw"])], 1)
     r, s = oracle.wgrad_at(cv, fmt, o["gy"], o["x"], idx)
-    egw = _err(gw[tuple(idx.T)], r, s, mxt.wgrad_bound(cv, ex["gy"], ex["x"], idx) if ex else None)
+    egw = _err(gw[tuple(idx.T)], r, s)
     assert max(ey, egx, egw) <= 1.0, (ey, egx, egw)
