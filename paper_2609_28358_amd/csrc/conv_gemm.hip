@@ -323,12 +323,14 @@ __global__ __launch_bounds__(NT) void conv_kernel(ConvArgs p) {
                           : frag_tr<FMT>(lds_a[buf], ASTR, 32 * wm);
         const int h = lane >> 5;
         const int sa = sc_a[buf][h][wm];
+        AFrag<FMT> ad;
+        ad.set(af, sa);
 #pragma unroll
         for (int c = 0; c < 2; c++) {
             const int colbase = 64 * wn + 32 * c;
             const v8i bf = frag_tr<FMT>(lds_b[buf], BSTR, colbase);
             const int sb = sc_b[buf][h][(colbase + (lane & 31)) / bn];
-            acc[c] = mfma_mx<FMT>(af, bf, acc[c], sa, sb);
+            acc[c] = mfma_mx_a<FMT>(ad, bf, acc[c], sb);
         }
         if (s + 1 < nsteps) store_step(buf ^ 1);
         __syncthreads();
@@ -558,11 +560,13 @@ __global__ __launch_bounds__(NT) void wgrad_kernel(WgradArgs p) {
         const int h = lane >> 5;
         const v8i af = frag_rows<FMT>(lds_a[buf], STR, 32 * wm);
         const int sa = sc_a[buf][h][wm];
+        AFrag<FMT> ad;
+        ad.set(af, sa);
 #pragma unroll
         for (int c = 0; c < 2; c++) {
             const v8i bf = frag_rows<FMT>(lds_b[buf], STR, 64 * wn + 32 * c);
             const int sb = sc_b[buf][h][2 * wn + c];
-            acc[c] = mfma_mx<FMT>(af, bf, acc[c], sa, sb);
+            acc[c] = mfma_mx_a<FMT>(ad, bf, acc[c], sb);
         }
         if (s + 1 < nsteps) store_step(buf ^ 1);
         __syncthreads();
@@ -975,6 +979,8 @@ __global__ __launch_bounds__(NT) void conv_stream_kernel(StreamArgs p) {
                 }
             }
             const int sa = SC[(t * 2 + h) * 2 + wm];
+            AFrag<FMT> ad;
+            ad.set(af, sa);
 #pragma unroll
             for (int c = 0; c < 2; c++) {
                 v8i bf;
@@ -1000,7 +1006,7 @@ __global__ __launch_bounds__(NT) void conv_stream_kernel(StreamArgs p) {
                     bf[4] = bf[5] = bf[6] = bf[7] = 0;
                 }
                 const int sb = SC[ntw * 4 + h * HC + s_hc[c] + co];
-                acc[c] = mfma_mx<FMT>(af, bf, acc[c], sa, sb);
+                acc[c] = mfma_mx_a<FMT>(ad, bf, acc[c], sb);
             }
         }
         if (st + 1 < nstage) {
@@ -1276,6 +1282,8 @@ __global__ __launch_bounds__(NT) void wgrad_stream_kernel(WStreamArgs p) {
                 af[4] = af[5] = af[6] = af[7] = 0;
             }
             const int sa = SC[(2 * ks + h) * 2 + wm];
+            AFrag<FMT> ad;
+            ad.set(af, sa);
 #pragma unroll
             for (int c = 0; c < 2; c++) {
                 const int cbk = 2 * wn + c;
@@ -1291,7 +1299,7 @@ __global__ __launch_bounds__(NT) void wgrad_stream_kernel(WStreamArgs p) {
                     bf[4] = bf[5] = bf[6] = bf[7] = 0;
                 }
                 const int sb = SC[SP * 2 + (2 * ks + h) * 4 + cbk];
-                acc[c] = mfma_mx<FMT>(af, bf, acc[c], sa, sb);
+                acc[c] = mfma_mx_a<FMT>(ad, bf, acc[c], sb);
             }
         }
         if (st + 1 < nstage) {

@@ -145,6 +145,10 @@ template <int F> struct LdsBlock {
 template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW, bool NV = false>
 __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phase& f) {
     static_assert(!NV || (FW == MXC_E2M1 && FX == MXC_E2M1), "NVFP4 operands only");
+    // X8: MXFP8 operands, decoded once per fragment to bf16 (exact products,
+    // fp32 accumulation); NV or X8: the products run on decoded fragments
+    constexpr bool X8 = FX == MXC_E4M3 && !NV;
+    constexpr bool DEC = NV || X8;
     typedef LdsBlock<FW> BW;
     typedef LdsBlock<FX> BX;
     constexpr int TBW = BW::TBG, TBX = BX::TBG;     // stored block bytes (weights, activations)
@@ -318,7 +322,7 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
         // fragments of the wave's ND halo pixels (both K halves)
         v8i bf[ND];
         int sb[ND];
-        uint32_t bfd[NV ? ND : 1][16];          // NV: decoded to fp16
+        uint32_t bfd[DEC ? ND : 1][16];         // NV: decoded to fp16; X8: to bf16
 #pragma unroll
         for (int d = 0; d < ND; d++) {
             const int hc = hbase + d;
@@ -350,6 +354,8 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                 bf[d][4] = bf[d][5] = bf[d][6] = bf[d][7] = 0;
             }
             sb[d] = SC[4 * (NSA + h * HP + hc)];
+            if constexpr (X8)   // both K blocks' scales (h = 0, 1) of the pixel
+                e4m3_decode32(bf[d], SC[4 * (NSA + hc)], SC[4 * (NSA + HP + hc)], bfd[d]);
             if constexpr (NV) {
                 // scales of (channel group o, this lane's sample group): byte 4 o + (lane % 32) / 8
                 const uint4 u = *(const uint4*)(SC + 16 * (NSA + h * HP + hc));
@@ -416,7 +422,14 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                 }
                 sa[rb] = SC[4 * ((t * 2 + h) * RBW + rbi)];
             }
-            uint32_t afd[NV ? 2 : 1][16];
+            uint32_t afd[DEC ? 2 : 1][16];
+            if constexpr (X8) {
+#pragma unroll
+                for (int rb = 0; rb < 2; rb++) {
+                    const int rbi = 2 * wm + rb;
+                    e4m3_decode32(af[rb], SC[4 * ((t * 2 + 0) * RBW + rbi)], SC[4 * ((t * 2 + 1) * RBW + rbi)], afd[rb]);
+                }
+            }
             if constexpr (NV) {
 #pragma unroll
                 for (int rb = 0; rb < 2; rb++) {
@@ -440,6 +453,7 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
 #pragma unroll
                 for (int rb = 0; rb < 2; rb++) {  // transposed product: rows = samples, columns = channels
                     if constexpr (NV) acc[rb][cn] = mfma_nv(bfd[d], afd[rb], acc[rb][cn]);
+                    else if constexpr (X8) acc[rb][cn] = mfma_x8(bfd[d], afd[rb], acc[rb][cn]);
                     else acc[rb][cn] = mfma_mx<FX, FW>(bf[d], af[rb], acc[rb][cn], sb[d], sa[rb]);
                 }
             }

@@ -505,6 +505,29 @@ __device__ __forceinline__ v16f mfma_mx(v8i a, v8i b, v16f c, int sa, int sb) {
     }
 }
 
+// An A fragment multiplied by several B fragments: an FP8 one is decoded
+// once (set), the others are kept as they are.
+template <int F> struct AFrag {
+    v8i f;
+    int s;
+    uint32_t d[F == MXC_E4M3 ? 16 : 1];
+    __device__ __forceinline__ void set(const v8i& f_, int s_) {
+        f = f_;
+        s = s_;
+        if constexpr (F == MXC_E4M3) e4m3_decode32_lane(f, s, d);
+    }
+};
+template <int F>
+__device__ __forceinline__ v16f mfma_mx_a(const AFrag<F>& a, v8i b, v16f c, int sb) {
+    if constexpr (F == MXC_E4M3) {
+        uint32_t bd[16];
+        e4m3_decode32_lane(b, sb, bd);
+        return mfma_x8(a.d, bd, c);
+    } else {
+        return mfma_mx<F>(a.f, b, c, a.s, sb);
+    }
+}
+
 // Asynchronous global -> LDS copies (global_load_lds).  Every lane supplies
 // its own source address; the LDS destination is the wave-uniform base in M0
 // plus 16 * lane for the 16-byte form, plus 4 * lane for the one-byte form

@@ -255,10 +255,23 @@ __global__ __launch_bounds__(NT) void naive_gemm_kernel(const uint8_t* __restric
                 na[i] = frag(ap[i], kn); nb[i] = frag(bp[i], kn);
                 nsa[i] = asp[i][2 * kn]; nsb[i] = bsp[i][2 * kn];
             }
+            if constexpr (FMT == MXC_E4M3) {   // each fragment decoded to bf16 once (exact products)
+                uint32_t ad[2][16], bd[2][16];
 #pragma unroll
-            for (int i = 0; i < 2; i++)
+                for (int i = 0; i < 2; i++) {
+                    e4m3_decode32_lane(fa[i], sa[i], ad[i]);
+                    e4m3_decode32_lane(fb[i], sb[i], bd[i]);
+                }
 #pragma unroll
-                for (int j = 0; j < 2; j++) acc[i][j] = mfma_mx<FMT>(fa[i], fb[j], acc[i][j], sa[i], sb[j]);
+                for (int i = 0; i < 2; i++)
+#pragma unroll
+                    for (int j = 0; j < 2; j++) acc[i][j] = mfma_x8(ad[i], bd[j], acc[i][j]);
+            } else {
+#pragma unroll
+                for (int i = 0; i < 2; i++)
+#pragma unroll
+                    for (int j = 0; j < 2; j++) acc[i][j] = mfma_mx<FMT>(fa[i], fb[j], acc[i][j], sa[i], sb[j]);
+            }
 #pragma unroll
             for (int i = 0; i < 2; i++) { fa[i] = na[i]; fb[i] = nb[i]; sa[i] = nsa[i]; sb[i] = nsb[i]; }
         }

@@ -173,6 +173,17 @@ __device__ __forceinline__ void wgrad_tile(const WLArgs& p, int bid, int nblk, f
                 for (int i = 0; i < 2; i++)
 #pragma unroll
                     for (int j = 0; j < 2; j++) acc[i][j] = mfma_nv(ad[i], bd[j], acc[i][j]);
+            } else if constexpr (FA == MXC_E4M3) {   // MXFP8: each fragment decoded to bf16 once
+                uint32_t ad[2][16], bd[2][16];
+#pragma unroll
+                for (int i = 0; i < 2; i++) {
+                    e4m3_decode32_lane(o[b].a[i], o[b].sa[i], ad[i]);
+                    e4m3_decode32_lane(o[b].b[i], o[b].sb[i], bd[i]);
+                }
+#pragma unroll
+                for (int i = 0; i < 2; i++)
+#pragma unroll
+                    for (int j = 0; j < 2; j++) acc[i][j] = mfma_x8(ad[i], bd[j], acc[i][j]);
             } else {
 #pragma unroll
                 for (int i = 0; i < 2; i++)
