@@ -111,6 +111,9 @@ typedef enum { MXC_F32 = 0, MXC_BF16 = 1 } mxc_dtype;
 typedef enum { MXC_NCHW = 0, MXC_NHWC = 1, MXC_CBF = 2 } mxc_layout;
 typedef enum { MXC_ACT = 0, MXC_WEIGHT = 1 } mxc_role;
 typedef enum { MXC_FN_NONE = 0, MXC_FN_RELU = 1, MXC_FN_SILU = 2 } mxc_fn;   /* activation function */
+/* Flag or-ed into mxconv_fwd_quant's fn: its fp32 output receives the values
+ * before the activation (the pre-activation a backward pass needs for fn'). */
+#define MXC_FN_PRE_OUT 0x100
 
 /* One convolution layer: batch n, channels cin -> cout, input h x w,
  * kernel kh x kw, stride sh, sw, zero padding ph, pw. */
@@ -468,7 +471,8 @@ int mxconv_naive_wgrad(const mxc_conv* cv, int fmt,
  *                       MXC_ACT, out_fmt, n, cout, Ho, Wo) bytes, written
  *                       (out_fmt any mxc_fmt; FP6 slack not written).
  *   y_act               NULL, or device fp32 n x cout x Ho x Wo in CBF
- *                       layout: receives the values that were quantized.
+ *                       layout: receives the values that were quantized,
+ *                       or, with fn | MXC_FN_PRE_OUT, W * X before fn.
  * Input gradient: G_Z = (W^T * G_Y) . fn'(z), the gradient at the
  * pre-activation z of this layer's input X = fn(z) (fn' = 1 for
  * MXC_FN_NONE, [z > 0] for ReLU, s (1 + z (1 - s)) with s = 1 / (1 +
@@ -492,6 +496,69 @@ int mxconv_dgrad_quant(const mxc_conv* cv, int fmt,
                        const void* gy_codes, const uint8_t* gy_scales,
                        int fn, const float* z, int out_fmt,
                        void* gx_codes, uint8_t* gx_scales, float* gx_act, void* stream);
+
+/* ------------------------------------------------------------------ network steps */
+/* Between the convolutions of a whole network's training step (the YOLO
+ * backbone + neck and the latent-replay stacks of Sec. VI-VII), two more
+ * operations touch activations and gradients; both keep every tensor
+ * quantized exactly once (Sec. IV-C).
+ *
+ * Channel concatenation and nearest-neighbour 2x upsampling of MX-CBF
+ * activations.  A block is 32 channels x Bn samples at one pixel (Sec. IV-A,
+ * IV-B), so both are index maps on whole blocks: codes and E8M0 scales are
+ * copied, never requantized.  The destination is the MX-CBF tensor of
+ * (n, 32 * sum_k ncb_k, h, w) (role MXC_ACT, format fmt): part k fills the
+ * channel blocks [off_k, off_k + ncb_k), off_k = sum_{i<k} ncb_i, in order,
+ * so a part whose channel count is not a multiple of 32 brings its zero
+ * padding channels along as channels of the destination.
+ *   part.codes/scales  device MX-CBF tensor (n, c_k, h_k, w_k) of format fmt
+ *                      (the same batch block as the destination);
+ *   part.ncb           ceil(c_k / 32);
+ *   part.up            0: (h_k, w_k) = (h, w); 1: (h_k, w_k) = (h/2, w/2) and
+ *                      destination pixel (y, x) reads source pixel
+ *                      (y/2, x/2) (h and w even).
+ *   codes / scales     device, written (mxconv_codes_bytes /
+ *                      mxconv_scales_bytes of the destination).
+ * 1 <= nparts <= MXC_CONCAT_MAX.  Errors: NULL, ARG, SHAPE, ALIGN, HIP. */
+#define MXC_CONCAT_MAX 4
+typedef struct {
+    const void* codes;
+    const uint8_t* scales;
+    int ncb;
+    int up;
+} mxc_part;
+int mxconv_concat_cbf(int fmt, int n, int h, int w, int nparts, const mxc_part* parts,
+                      void* codes, uint8_t* scales, void* stream);
+
+/* Quantize the gradient of a tensor a = fn(z) read by several consumers:
+ *   G = fn'(z) . (t_0 + t_1 + ... + t_{nterms-1})
+ * (fn' as for mxconv_dgrad_quant; z may be NULL for MXC_FN_NONE), quantized
+ * once with the rule of mxconv_quantize (role MXC_ACT) into the MX-CBF tensor
+ * of (n, c, h, w) -- the G_Y operand of the layer that produced a.  Each term
+ * is read from an fp32 CBF tensor [n/32][hs][ws][c_src][32] -- a consumer's
+ * input gradient:
+ *   term.src     device fp32;
+ *   term.c_src   channels of that tensor; term.c_off: its channel that is
+ *                channel 0 of the term (c_off + c <= c_src: the slice a
+ *                concatenation's gradient hands back to one part);
+ *   term.down    0: (hs, ws) = (h, w); 1: (hs, ws) = (2h, 2w) and the term
+ *                at (y, x) is (s(2y,2x) + s(2y,2x+1)) + (s(2y+1,2x) +
+ *                s(2y+1,2x+1)) -- the gradient of a 2x upsampling.
+ * The fp32 sum runs over the terms in order (((t_0 + t_1) + t_2) + ...).
+ *   z            device fp32 CBF [n/32][h][w][c][32], the pre-activation;
+ *   codes/scales device, written;
+ *   vals         NULL, or device fp32 CBF [n/32][h][w][c][32]: receives G.
+ * n a multiple of 32; fmt MXC_E4M3 or MXC_E2M1; 1 <= nterms <= MXC_TERMS_MAX.
+ * Errors: NULL, ARG, SHAPE, ALIGN, HIP. */
+#define MXC_TERMS_MAX 4
+typedef struct {
+    const float* src;
+    int c_src;
+    int c_off;
+    int down;
+} mxc_term;
+int mxconv_quantize_sum(int fmt, int n, int c, int h, int w, int nterms, const mxc_term* terms,
+                        int fn, const float* z, void* codes, uint8_t* scales, float* vals, void* stream);
 
 /* Human-readable text for a return code (static storage). */
 const char* mxconv_strerror(int code);

@@ -441,3 +441,72 @@ def act_grad(z, fn):
     with np.errstate(over="ignore"):
         s = 1.0 / (1.0 + np.exp(-z))
     return s * (1.0 + z * (1.0 - s))
+
+
+# ---------------------------------------------------------------- network steps
+def _bn(n):
+    return 32 if n >= 32 else n
+
+
+def concat_cbf(parts, fmt, n, h, w):
+    """Channel concatenation of MX-CBF activations on whole blocks, each part
+    optionally upsampled 2x by nearest neighbour, written out as loops over
+    (group, pixel, part, block).  parts: tuples (codes, scales, c, up) of MX
+    tensors (n, c, h_k, w_k) with (h_k, w_k) = (h/2, w/2) when up else (h, w).
+    A block is 32 channels x Bn samples at one pixel (Sec. IV-A, IV-B), so
+    the result copies codes and scales and requantizes nothing.  Returns the
+    codes and scales of (n, 32 * sum ceil(c_k / 32), h, w)."""
+    bn = _bn(n)
+    ng = -(-n // bn)
+    bb = 32 * bn * BITS[fmt] // 8
+    ncbs = [-(-c // 32) for _, _, c, _ in parts]
+    tot = sum(ncbs)
+    out_c = np.zeros((ng, h, w, tot, bb), np.uint8)
+    out_s = np.zeros((ng, h, w, tot), np.uint8)
+    srcs = []
+    for (codes, scales, c, up), ncb in zip(parts, ncbs):
+        hk, wk = (h // 2, w // 2) if up else (h, w)
+        cd = np.asarray(codes, np.uint8)[:ng * hk * wk * ncb * bb].reshape(ng, hk, wk, ncb, bb)
+        sc = np.asarray(scales, np.uint8)[:ng * hk * wk * ncb].reshape(ng, hk, wk, ncb)
+        srcs.append((cd, sc, ncb, up))
+    for g in range(ng):
+        for y in range(h):
+            for x in range(w):
+                off = 0
+                for cd, sc, ncb, up in srcs:
+                    sy, sx = (y // 2, x // 2) if up else (y, x)
+                    for b in range(ncb):
+                        out_c[g, y, x, off + b] = cd[g, sy, sx, b]
+                        out_s[g, y, x, off + b] = sc[g, sy, sx, b]
+                    off += ncb
+    return out_c.reshape(-1), out_s.reshape(-1)
+
+
+def _cbf_nchw(a, n, c, h, w):
+    """fp32 CBF [n/32][h][w][c][32] -> fp64 (n, c, h, w)."""
+    a = np.asarray(a, np.float32).reshape(n // 32, h, w, c, 32).astype(np.float64)
+    return a.transpose(0, 4, 3, 1, 2).reshape(n, c, h, w)
+
+
+def gradient_sum(terms, fn, z, n, c, h, w):
+    """The gradient of a tensor a = fn(z) read by several consumers, in fp64:
+    fn'(z) times the sum of the consumers' contributions, each the channel
+    slice [c_off, c_off + c) of an fp32 CBF tensor (n, c_src, hs, ws) --
+    what a concatenation's gradient hands back to one part -- and, when down,
+    summed over the 2x2 source pixels that a nearest-neighbour 2x upsampling
+    copied this pixel to.  terms: tuples (src, c_src, c_off, down); z: fp32
+    CBF (n, c, h, w) or None for FN_NONE.  Returns fp64 (n, c, h, w)."""
+    acc = np.zeros((n, c, h, w))
+    for src, c_src, c_off, down in terms:
+        hs, ws = (2 * h, 2 * w) if down else (h, w)
+        t = _cbf_nchw(src, n, c_src, hs, ws)[:, c_off:c_off + c]
+        if down:
+            s = np.zeros((n, c, h, w))
+            for i in range(2):
+                for j in range(2):
+                    s += t[:, :, i::2, j::2]
+            t = s
+        acc += t
+    if fn != FN_NONE:
+        acc *= act_grad(_cbf_nchw(z, n, c, h, w), fn)
+    return acc

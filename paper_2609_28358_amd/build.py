@@ -16,7 +16,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libmxconv.so")
-SOURCES = ["quantize.hip", "nvfp.hip", "im2col.hip", "conv_gemm.hip", "conv_lean.hip", "wgrad_lean.hip", "naive.hip", "mxconv_abi.cpp"]
+SOURCES = ["quantize.hip", "nvfp.hip", "im2col.hip", "conv_gemm.hip", "conv_lean.hip", "wgrad_lean.hip", "naive.hip", "netops.hip", "mxconv_abi.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -44,23 +44,6 @@ constexpr int LT = 256;
 
 __device__ __attribute__((aligned(16))) uint8_t g_zero_lean[1024];
 
-// Activation (forward epilogue) and its derivative (input-gradient epilogue).
-// SiLU uses the hardware exp2 and reciprocal (about 1 ulp each): the
-// logistic s(y) = 1 / (1 + 2^(-y log2 e)); exp2 overflows to +inf for very
-// negative y, where s = 0 and SiLU = -0.
-__device__ __forceinline__ float logistic(float y) {
-    return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-y * 1.4426950408889634f));
-}
-__device__ __forceinline__ float fn_apply(int fn, float y) {
-    if (fn == MXC_FN_RELU) return y > 0.0f ? y : 0.0f;
-    return y * logistic(y);                                     // SiLU
-}
-__device__ __forceinline__ float fn_grad(int fn, float z) {
-    if (fn == MXC_FN_RELU) return z > 0.0f ? 1.0f : 0.0f;
-    const float s = logistic(z);                                // SiLU' = s (1 + z (1 - s))
-    return s * (1.0f + z * (1.0f - s));
-}
-
 // LDS of one stage: NQ 4 KB groups of DMA slices (weight blocks, then halo
 // blocks), then 1 KB of scale entries (entry e at byte 4 e: one dword per
 // lane of the one-byte copies).
@@ -98,6 +81,7 @@ struct LeanArgs {
     uint8_t* qcodes;
     uint8_t* qscales;
     int qfmt, q_ncb, fn;
+    int pre_out;              // forward: `out` receives the values before the activation
     const float* zpre;
     // NVFP4 operands (the NV kernels): per-tensor scales of W and the source;
     // the scale arrays ws / ss then hold E4M3 scales per 8x8 block, the 16 of
@@ -504,6 +488,12 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                 float v[16];
 #pragma unroll
                 for (int e = 0; e < 16; e++) v[e] = acc[rb][cn][e];
+                if (p.out && real && p.pre_out) {   // the pre-activation, for the backward pass
+                    float* o = p.out + (pix * p.M + c) * 32 + 4 * h;
+#pragma unroll
+                    for (int e4 = 0; e4 < 4; e4++)
+                        *(float4*)(o + 8 * e4) = make_float4(v[4 * e4], v[4 * e4 + 1], v[4 * e4 + 2], v[4 * e4 + 3]);
+                }
                 if (p.fn != MXC_FN_NONE) {
                     if (DG) {
                         const float* zp = p.zpre + (pix * p.M + (real ? c : 0)) * 32 + 4 * h;
@@ -520,7 +510,7 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                         for (int e = 0; e < 16; e++) v[e] = fn_apply(p.fn, v[e]);
                     }
                 }
-                if (p.out && real) {
+                if (p.out && real && !p.pre_out) {
                     float* o = p.out + (pix * p.M + c) * 32 + 4 * h;
 #pragma unroll
                     for (int e4 = 0; e4 < 4; e4++)
@@ -796,6 +786,7 @@ int lean_plan(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const 
     a.qfmt = q ? q->fmt : 0;
     a.q_ncb = (a.M + 31) / 32;
     a.fn = q ? q->fn : MXC_FN_NONE;
+    a.pre_out = q && q->pre ? 1 : 0;
     a.zpre = q ? q->z : nullptr;
     a.tw = nv_tw; a.tx = nv_tx;
     const Geom& src = dg ? cv.gy : cv.x;

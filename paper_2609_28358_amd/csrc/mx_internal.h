@@ -89,6 +89,7 @@ struct FusedEpi {
     uint8_t* scales;
     int fmt, fn;
     const float* z;
+    bool pre;            // forward: the fp32 output gets the values before fn
 };
 // fwd / dgrad for batch block 32 and kernel width 1 or 3 (conv_lean.hip);
 // returns 1 when the layer is outside those shapes.  With q, the output is
@@ -128,6 +129,12 @@ struct WReduceJob {
     float* gw;
 };
 int launch_wgrad_reduce_multi(int count, const WReduceJob* jobs, hipStream_t s);
+// network operations (netops.hip): MX-block concatenation / 2x upsampling,
+// and the quantized, fn'-masked sum of gradient terms
+int launch_concat(const Geom& dst, const mxc_part* parts, int nparts, void* codes, uint8_t* scales,
+                  hipStream_t s);
+int launch_quantize_sum(const Geom& dst, int fmt, const mxc_term* terms, int nterms, int fn, const float* z,
+                        void* codes, uint8_t* scales, float* vals, hipStream_t s);
 
 // naive comparator (naive.hip): a line matrix stores each 1-D-blocked line
 // zero-padded to a multiple of 64 elements (one K step of the MFMA)
@@ -421,6 +428,26 @@ __device__ __forceinline__ unsigned short pack4_e2m1(float4 x, float inv) {
     q = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(q, x.x * inv, x.y * inv, 1.0f, 0);
     q = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(q, x.z * inv, x.w * inv, 1.0f, 1);
     return (unsigned short)q;
+}
+
+// ---------------------------------------------------------------- activations
+// Activation of the forward epilogue and its derivative (input-gradient
+// epilogue, gradient quantizer).  SiLU uses the hardware exp2 and reciprocal
+// (about 1 ulp each): the logistic s(y) = 1 / (1 + 2^(-y log2 e)); exp2
+// overflows to +inf for very negative y, where s = 0 and SiLU = -0.
+__device__ __forceinline__ float logistic(float y) {
+    return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-y * 1.4426950408889634f));
+}
+__device__ __forceinline__ float fn_apply(int fn, float y) {
+    if (fn == MXC_FN_NONE) return y;
+    if (fn == MXC_FN_RELU) return y > 0.0f ? y : 0.0f;
+    return y * logistic(y);                                     // SiLU
+}
+__device__ __forceinline__ float fn_grad(int fn, float z) {
+    if (fn == MXC_FN_NONE) return 1.0f;
+    if (fn == MXC_FN_RELU) return z > 0.0f ? 1.0f : 0.0f;
+    const float s = logistic(z);                                // SiLU' = s (1 + z (1 - s))
+    return s * (1.0f + z * (1.0f - s));
 }
 
 // ---------------------------------------------------------------- MXFP8 operands

@@ -363,6 +363,8 @@ int mxconv_fwd_quant(const mxc_conv* p, int fmt, const void* wc, const uint8_t* 
                      const uint8_t* xs, int fn, int out_fmt, void* yc, uint8_t* ysc, float* y_act,
                      void* stream) {
     if (!p || !wc || !ws || !xc || !xs || !yc || !ysc) return MXC_ERR_NULL;
+    const bool pre = (fn & MXC_FN_PRE_OUT) != 0;
+    fn &= ~MXC_FN_PRE_OUT;
     if (fn < MXC_FN_NONE || fn > MXC_FN_SILU || !fmt_ok(out_fmt)) return MXC_ERR_ARG;
     Conv cv;
     int rc = conv_init(&cv, p, fmt, CONV_FWD);
@@ -371,7 +373,7 @@ int mxconv_fwd_quant(const mxc_conv* p, int fmt, const void* wc, const uint8_t* 
     if (!aligned16(wc) || !aligned16(ws) || !aligned16(xc) || !aligned16(xs) || !aligned16(yc) ||
         !aligned16(ysc) || (y_act && !aligned16(y_act)))
         return MXC_ERR_ALIGN;
-    FusedEpi q{yc, ysc, out_fmt, fn, nullptr};
+    FusedEpi q{yc, ysc, out_fmt, fn, nullptr, pre};
     rc = launch_conv_lean(cv, false, wc, ws, xc, xs, y_act, MXC_CBF, (hipStream_t)stream, &q);
     return rc == 1 ? MXC_ERR_SHAPE : rc;
 }
@@ -389,9 +391,55 @@ int mxconv_dgrad_quant(const mxc_conv* p, int fmt, const void* wc, const uint8_t
     if (!aligned16(wc) || !aligned16(ws) || !aligned16(gc) || !aligned16(gs) || !aligned16(gxc) ||
         !aligned16(gxs) || (gx_act && !aligned16(gx_act)) || (fn != MXC_FN_NONE && !aligned16(z)))
         return MXC_ERR_ALIGN;
-    FusedEpi q{gxc, gxs, out_fmt, fn, z};
+    FusedEpi q{gxc, gxs, out_fmt, fn, z, false};
     rc = launch_conv_lean(cv, true, wc, ws, gc, gs, gx_act, MXC_CBF, (hipStream_t)stream, &q);
     return rc == 1 ? MXC_ERR_SHAPE : rc;
+}
+
+int mxconv_concat_cbf(int fmt, int n, int h, int w, int nparts, const mxc_part* parts, void* codes,
+                      uint8_t* scales, void* stream) {
+    if (!parts || !codes || !scales) return MXC_ERR_NULL;
+    if (nparts < 1 || nparts > MXC_CONCAT_MAX || !fmt_ok(fmt)) return MXC_ERR_ARG;
+    int total = 0;
+    for (int k = 0; k < nparts; k++) {
+        const mxc_part& q = parts[k];
+        if (!q.codes || !q.scales) return MXC_ERR_NULL;
+        if (q.ncb <= 0 || (q.up != 0 && q.up != 1)) return MXC_ERR_ARG;
+        if (q.up && ((h & 1) || (w & 1))) return MXC_ERR_SHAPE;
+        if (!aligned16(q.codes) || !aligned16(q.scales)) return MXC_ERR_ALIGN;
+        if (total > 0x3FFFFFF - q.ncb) return MXC_ERR_SHAPE;
+        total += q.ncb;
+    }
+    Geom g;
+    const int rc = geom_init(&g, MXC_ACT, fmt, n, 32 * total, h, w);
+    if (rc) return rc;
+    if (!aligned16(codes) || !aligned16(scales)) return MXC_ERR_ALIGN;
+    return launch_concat(g, parts, nparts, codes, scales, (hipStream_t)stream);
+}
+
+int mxconv_quantize_sum(int fmt, int n, int c, int h, int w, int nterms, const mxc_term* terms, int fn,
+                        const float* z, void* codes, uint8_t* scales, float* vals, void* stream) {
+    if (!terms || !codes || !scales) return MXC_ERR_NULL;
+    if (nterms < 1 || nterms > MXC_TERMS_MAX) return MXC_ERR_ARG;
+    if (fmt != MXC_E4M3 && fmt != MXC_E2M1) return MXC_ERR_ARG;
+    if (fn < MXC_FN_NONE || fn > MXC_FN_SILU) return MXC_ERR_ARG;
+    if (fn != MXC_FN_NONE && !z) return MXC_ERR_NULL;
+    Geom g;
+    int rc = geom_init(&g, MXC_ACT, fmt, n, c, h, w);
+    if (rc) return rc;
+    if (g.bn != 32) return MXC_ERR_SHAPE;
+    for (int t = 0; t < nterms; t++) {
+        const mxc_term& q = terms[t];
+        if (!q.src) return MXC_ERR_NULL;
+        if (q.c_src <= 0 || q.c_off < 0 || (q.down != 0 && q.down != 1)) return MXC_ERR_ARG;
+        if ((long long)q.c_off + c > q.c_src) return MXC_ERR_SHAPE;
+        if (q.down && ((long long)2 * h * 2 * w > 0x7FFFFFFFLL)) return MXC_ERR_SHAPE;
+        if (!aligned16(q.src)) return MXC_ERR_ALIGN;
+    }
+    if (!aligned16(codes) || !aligned16(scales) || (vals && !aligned16(vals)) ||
+        (fn != MXC_FN_NONE && !aligned16(z)))
+        return MXC_ERR_ALIGN;
+    return launch_quantize_sum(g, fmt, terms, nterms, fn, z, codes, scales, vals, (hipStream_t)stream);
 }
 
 size_t mxconv_naive_codes_bytes(int64_t lines, int64_t len, int fmt) {

@@ -1,0 +1,215 @@
+// netops.hip -- the two operations a whole network's training step needs
+// between its convolutions, written so that every tensor is still quantized
+// exactly once (Sec. IV-C).
+//
+// Concatenation and 2x upsampling on MX codes.  A quantization block is 32
+// channels x Bn samples at one pixel (Sec. IV-B's square block in the
+// channel-batch-first layout of Sec. IV-A), so concatenating activations
+// along channels (whole blocks) or repeating each pixel 2x2 (nearest-
+// neighbour upsampling) only moves whole blocks: codes and scales are copied,
+// never requantized.  One thread per 16-byte destination chunk, as in a
+// streaming copy; threads with chunk index below the block count of a pixel
+// also copy that pixel's scale bytes.
+//
+// The gradient of a tensor a = fn(z) that several consumers read.  Its
+// gradient is the sum of what each consumer's input gradient hands back --
+// fp32 slices of wider tensors (the consumer was a concatenation) or the
+// 2x2 pixel sums of a tensor twice as large (the consumer was an upsampling)
+// -- times fn'(z), and it is quantized once, as the G_Y operand of the layer
+// that produced a.  One wave per 32-channel x 32-sample block, the lane
+// layout of the one-block-per-wave quantizer: lane l holds channels
+// 8 q + l / 8 (q = 0..3) and samples 4 (l % 8) .. +3, so every load of a
+// term is a 16-byte vector and the wave's codes are one contiguous run.
+#include "mx_internal.h"
+
+namespace mxc {
+namespace {
+
+struct ConcatArgs {
+    const uint8_t* codes[MXC_CONCAT_MAX];
+    const uint8_t* scales[MXC_CONCAT_MAX];
+    int ncb[MXC_CONCAT_MAX];          // channel blocks of each part
+    int off[MXC_CONCAT_MAX + 1];      // first destination block of each part, off[nparts] = total
+    int up[MXC_CONCAT_MAX];
+    int nparts;
+    int h, w;                         // destination pixel grid
+    int bb16;                         // 16-byte chunks per block
+};
+
+__global__ __launch_bounds__(256) void concat_kernel(ConcatArgs a, uint8_t* __restrict__ dst,
+                                                     uint8_t* __restrict__ sdst, long long nchunks) {
+    const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+    if (i >= nchunks) return;
+    const int run16 = a.off[a.nparts] * a.bb16;           // chunks of one destination pixel
+    const long long pix = i / run16;
+    const int within = (int)(i - pix * run16);
+    const int blk = within / a.bb16, in = within - blk * a.bb16;
+    int k = 0;
+#pragma unroll
+    for (int t = 1; t < MXC_CONCAT_MAX; t++)
+        if (t < a.nparts && blk >= a.off[t]) k = t;
+    const int x = (int)(pix % a.w);
+    const long long gy = pix / a.w;                        // (group, row)
+    const int y = (int)(gy % a.h);
+    const long long g = gy / a.h;
+    long long spix;
+    if (a.up[k]) spix = (g * (a.h >> 1) + (y >> 1)) * (a.w >> 1) + (x >> 1);
+    else spix = pix;
+    const int sb = blk - a.off[k];
+    const uint4* src = (const uint4*)(a.codes[k] + ((size_t)spix * a.ncb[k] + sb) * 16 * a.bb16) + in;
+    store_nt(dst + ((size_t)pix * run16 + within) * 16, __ldg(src));
+    if (within < a.off[a.nparts]) {                        // this pixel's scale byte of block `within`
+        int kk = 0;
+#pragma unroll
+        for (int t = 1; t < MXC_CONCAT_MAX; t++)
+            if (t < a.nparts && within >= a.off[t]) kk = t;
+        const long long sp = a.up[kk] ? (g * (a.h >> 1) + (y >> 1)) * (a.w >> 1) + (x >> 1) : pix;
+        sdst[(size_t)pix * a.off[a.nparts] + within] = a.scales[kk][(size_t)sp * a.ncb[kk] + within - a.off[kk]];
+    }
+}
+
+struct SumArgs {
+    const float* src[MXC_TERMS_MAX];
+    int c_src[MXC_TERMS_MAX];
+    int c_off[MXC_TERMS_MAX];
+    int down[MXC_TERMS_MAX];
+    int nterms;
+    int c, h, w, ncb;                 // destination (n, c, h, w), channel blocks
+    int fn;
+    const float* z;                   // CBF [n/32][h][w][c][32] (fn != NONE)
+    float* vals;                      // optional: the values quantized
+};
+
+// Term t at destination pixel (g, y, x), channel ch, samples j .. j+3.
+__device__ __forceinline__ float4 term4(const SumArgs& a, int t, long long g, int y, int x, int ch, int j) {
+    const float* s = a.src[t];
+    const int cs = a.c_src[t];
+    const int col = a.c_off[t] + ch;
+    if (!a.down[t]) {
+        const size_t i = ((((size_t)g * a.h + y) * a.w + x) * cs + col) * 32 + j;
+        return load_nt(s + i);
+    }
+    const int hs = 2 * a.h, ws = 2 * a.w;
+    const size_t r0 = ((size_t)g * hs + 2 * y) * ws + 2 * x, r1 = r0 + ws;
+    const float4 p = load_nt(s + ((r0 * cs + col) * 32 + j));
+    const float4 q = load_nt(s + (((r0 + 1) * cs + col) * 32 + j));
+    const float4 u = load_nt(s + ((r1 * cs + col) * 32 + j));
+    const float4 v = load_nt(s + (((r1 + 1) * cs + col) * 32 + j));
+    return make_float4((p.x + q.x) + (u.x + v.x), (p.y + q.y) + (u.y + v.y), (p.z + q.z) + (u.z + v.z),
+                       (p.w + q.w) + (u.w + v.w));
+}
+
+template <int FMT>
+__global__ __launch_bounds__(256) void quantize_sum_kernel(SumArgs a, uint8_t* __restrict__ codes,
+                                                           uint8_t* __restrict__ scales, long long nblocks) {
+    const long long blk = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (blk >= nblocks) return;
+    const int lane = threadIdx.x & 63;
+    const int cb = (int)(blk % a.ncb);
+    const long long pix = blk / a.ncb;                     // (group, y, x)
+    const int x = (int)(pix % a.w);
+    const long long gy = pix / a.w;
+    const int y = (int)(gy % a.h);
+    const long long g = gy / a.h;
+    const int j = 4 * (lane & 7);
+    float4 v[4];
+#pragma unroll
+    for (int q = 0; q < 4; q++) {
+        const int ch = cb * 32 + 8 * q + (lane >> 3);
+        float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (ch < a.c) {
+            s = term4(a, 0, g, y, x, ch, j);
+            for (int t = 1; t < a.nterms; t++) {
+                const float4 u = term4(a, t, g, y, x, ch, j);
+                s.x += u.x; s.y += u.y; s.z += u.z; s.w += u.w;
+            }
+            if (a.fn != MXC_FN_NONE) {
+                const float4 zz = load_nt(a.z + ((size_t)pix * a.c + ch) * 32 + j);
+                s.x *= fn_grad(a.fn, zz.x);
+                s.y *= fn_grad(a.fn, zz.y);
+                s.z *= fn_grad(a.fn, zz.z);
+                s.w *= fn_grad(a.fn, zz.w);
+            }
+            if (a.vals) store_nt(a.vals + ((size_t)pix * a.c + ch) * 32 + j, s);
+        }
+        v[q] = s;
+    }
+    uint32_t m = 0;
+#pragma unroll
+    for (int q = 0; q < 4; q++) {
+        m = max(m, __float_as_uint(v[q].x) & 0x7FFFFFFFu);
+        m = max(m, __float_as_uint(v[q].y) & 0x7FFFFFFFu);
+        m = max(m, __float_as_uint(v[q].z) & 0x7FFFFFFFu);
+        m = max(m, __float_as_uint(v[q].w) & 0x7FFFFFFFu);
+    }
+    m = wave_max_u32(m);
+    const uint32_t sc = scale_code_from_bits<fmt_emax(FMT)>(m);
+    if (lane == 0) scales[blk] = (uint8_t)sc;
+    const float inv = inv_scale(sc);
+    const bool bad = sc == 0xFFu;
+    if constexpr (FMT == MXC_E4M3) {
+        uint32_t* d = (uint32_t*)(codes + (size_t)blk * 1024) + lane;
+#pragma unroll
+        for (int q = 0; q < 4; q++) d[64 * q] = bad ? 0u : pack4_e4m3(v[q], inv);
+    } else {
+        unsigned short* d = (unsigned short*)(codes + (size_t)blk * 512) + lane;
+#pragma unroll
+        for (int q = 0; q < 4; q++) d[64 * q] = bad ? (unsigned short)0 : (unsigned short)pack4_e2m1(v[q], inv);
+    }
+}
+
+}  // namespace
+
+int launch_concat(const Geom& dst, const mxc_part* parts, int nparts, void* codes, uint8_t* scales,
+                  hipStream_t s) {
+    ConcatArgs a{};
+    int off = 0;
+    for (int k = 0; k < nparts; k++) {
+        a.codes[k] = (const uint8_t*)parts[k].codes;
+        a.scales[k] = parts[k].scales;
+        a.ncb[k] = parts[k].ncb;
+        a.up[k] = parts[k].up;
+        a.off[k] = off;
+        off += parts[k].ncb;
+    }
+    a.off[nparts] = off;
+    a.nparts = nparts;
+    a.h = dst.h;
+    a.w = dst.w;
+    a.bb16 = 32 * dst.bn * dst.bits / 8 / 16;
+    const long long nchunks = (long long)dst.ng * dst.h * dst.w * off * a.bb16;
+    if (nchunks <= 0) return MXC_OK;
+    const long long grid = (nchunks + 255) / 256;
+    if (grid > 0x7FFFFFFFLL) return MXC_ERR_SHAPE;
+    hipLaunchKernelGGL(concat_kernel, dim3((unsigned)grid), dim3(256), 0, s, a, (uint8_t*)codes, scales, nchunks);
+    return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
+}
+
+int launch_quantize_sum(const Geom& dst, int fmt, const mxc_term* terms, int nterms, int fn, const float* z,
+                        void* codes, uint8_t* scales, float* vals, hipStream_t s) {
+    SumArgs a{};
+    for (int t = 0; t < nterms; t++) {
+        a.src[t] = terms[t].src;
+        a.c_src[t] = terms[t].c_src;
+        a.c_off[t] = terms[t].c_off;
+        a.down[t] = terms[t].down;
+    }
+    a.nterms = nterms;
+    a.c = dst.c; a.h = dst.h; a.w = dst.w; a.ncb = dst.ncb;
+    a.fn = fn;
+    a.z = z;
+    a.vals = vals;
+    const long long nblocks = (long long)dst.ng * dst.h * dst.w * dst.ncb;
+    if (nblocks <= 0) return MXC_OK;
+    const long long grid = (nblocks + 3) / 4;
+    if (grid > 0x7FFFFFFFLL) return MXC_ERR_SHAPE;
+    if (fmt == MXC_E4M3)
+        hipLaunchKernelGGL(quantize_sum_kernel<MXC_E4M3>, dim3((unsigned)grid), dim3(256), 0, s, a, (uint8_t*)codes,
+                           scales, nblocks);
+    else
+        hipLaunchKernelGGL(quantize_sum_kernel<MXC_E2M1>, dim3((unsigned)grid), dim3(256), 0, s, a, (uint8_t*)codes,
+                           scales, nblocks);
+    return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
+}
+
+}  // namespace mxc

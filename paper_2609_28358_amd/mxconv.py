@@ -15,6 +15,7 @@ F32, BF16 = 0, 1
 NCHW, NHWC, CBF = 0, 1, 2
 ACT, WEIGHT = 0, 1
 FN_NONE, FN_RELU, FN_SILU = 0, 1, 2
+FN_PRE_OUT = 0x100      # or-ed into fwd_quant's fn: act_out receives the pre-activation
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libmxconv.so")
@@ -40,6 +41,18 @@ class MxcWJob(ctypes.Structure):
 
 
 WREDUCE_MAX = 8
+CONCAT_MAX = 4
+TERMS_MAX = 4
+
+
+class MxcPart(ctypes.Structure):
+    _fields_ = [("codes", ctypes.c_void_p), ("scales", ctypes.c_void_p), ("ncb", ctypes.c_int32),
+                ("up", ctypes.c_int32)]
+
+
+class MxcTerm(ctypes.Structure):
+    _fields_ = [("src", ctypes.c_void_p), ("c_src", ctypes.c_int32), ("c_off", ctypes.c_int32),
+                ("down", ctypes.c_int32)]
 
 
 class MxcQJob(ctypes.Structure):
@@ -92,6 +105,8 @@ def lib():
         "mxconv_naive_fwd": (i32, [CP, i32, P, P, P, P, P, P]),
         "mxconv_naive_dgrad": (i32, [CP, i32, P, P, P, P, P, P, P]),
         "mxconv_naive_wgrad": (i32, [CP, i32, P, P, P, P, P, P]),
+        "mxconv_concat_cbf": (i32, [i32, i32, i32, i32, i32, ctypes.POINTER(MxcPart), P, P, P]),
+        "mxconv_quantize_sum": (i32, [i32, i32, i32, i32, i32, i32, ctypes.POINTER(MxcTerm), i32, P, P, P, P, P]),
         "mxconv_strerror": (ctypes.c_char_p, [i32]),
     }
     for name, (res, args) in sigs.items():
@@ -416,6 +431,46 @@ def dgrad_quant(cv, w, gy, fn=FN_NONE, z=None, out_fmt=None, out=None, act_out=N
     _check(lib().mxconv_dgrad_quant(ctypes.byref(conv_struct(cv)), pair(w.fmt, gy.fmt), _ptr(w.codes), _ptr(w.scales),
                                     _ptr(gy.codes), _ptr(gy.scales), fn, _ptr(z), out_fmt, _ptr(g.codes),
                                     _ptr(g.scales), _ptr(act_out), _stream(stream)), "mxconv_dgrad_quant")
+    return g
+
+
+# ---------------------------------------------------------------- network steps
+def concat_cbf(parts, out=None, stream=None):
+    """Concatenate MX-CBF activations along channels, whole blocks, in order.
+    parts: MxTensors, or (MxTensor, up) with up = 1 for a 2x nearest-neighbour
+    upsampling of that part.  Returns the MxTensor of (n, 32 * sum ncb, h, w)."""
+    if not 1 <= len(parts) <= CONCAT_MAX:
+        raise MxconvError(f"1 to {CONCAT_MAX} parts")
+    arr = (MxcPart * len(parts))()
+    nb, hw, fmt = 0, None, None
+    for k, p in enumerate(parts):
+        t, up = (p, 0) if isinstance(p, MxTensor) else p
+        n, c, h, w = t.shape
+        ncb = (c + 31) // 32
+        arr[k] = MxcPart(t.codes.data_ptr(), t.scales.data_ptr(), ncb, up)
+        nb += ncb
+        hw = (h * 2, w * 2) if up else (h, w)
+        fmt, dev = t.fmt, t.codes.device
+    shape = (n, 32 * nb, hw[0], hw[1])
+    y = out if out is not None else MxTensor.empty(ACT, fmt, shape, dev)
+    _check(lib().mxconv_concat_cbf(fmt, shape[0], shape[2], shape[3], len(parts), arr, _ptr(y.codes), _ptr(y.scales),
+                                   _stream(stream)), "mxconv_concat_cbf")
+    return y
+
+
+def quantize_sum(terms, shape, fmt, fn=FN_NONE, z=None, out=None, vals=None, stream=None):
+    """MX codes of fn'(z) . (sum of terms) for the (n, c, h, w) tensor `shape`.
+    terms: tuples (src, c_src, c_off, down) with src an fp32 CBF device
+    tensor [n/32][hs][ws][c_src][32]."""
+    if not 1 <= len(terms) <= TERMS_MAX:
+        raise MxconvError(f"1 to {TERMS_MAX} terms")
+    arr = (MxcTerm * len(terms))()
+    for k, (src, c_src, c_off, down) in enumerate(terms):
+        arr[k] = MxcTerm(src.data_ptr(), c_src, c_off, down)
+    n, c, h, w = shape
+    g = out if out is not None else MxTensor.empty(ACT, fmt, shape, terms[0][0].device)
+    _check(lib().mxconv_quantize_sum(fmt, n, c, h, w, len(terms), arr, fn, _ptr(z), _ptr(g.codes), _ptr(g.scales),
+                                     _ptr(vals), _stream(stream)), "mxconv_quantize_sum")
     return g
 
 

@@ -147,6 +147,22 @@ def test_fused_full_size_layer(mx, fmt):
     assert np.all(np.abs(got - ref) <= 1.1 * tol + 1e-6 * np.abs(ref))
 
 
+@pytest.mark.parametrize("fmt", [0, 1], ids=["e4m3", "e2m1"])
+@pytest.mark.parametrize("cv", FUSED_CONVS[:4], ids=_ids)
+def test_fwd_quant_pre_activation_out(mx, cv, fmt):
+    """With MXC_FN_PRE_OUT the fp32 output is W * X before the activation (bit
+    for bit the plain forward), while the codes are those of SiLU(W * X)
+    (equal to the call without the flag)."""
+    q, _ = _layer(mx, cv, fmt, 23)
+    plain = mx.fwd(cv, q["w"], q["x"], layout=mx.CBF)
+    pre = torch.full_like(plain, float("nan"))
+    y1 = mx.fwd_quant(cv, q["w"], q["x"], fn=mx.FN_SILU | mx.FN_PRE_OUT, act_out=pre)
+    y2 = mx.fwd_quant(cv, q["w"], q["x"], fn=mx.FN_SILU)
+    torch.cuda.synchronize()
+    assert torch.equal(pre, plain)
+    assert torch.equal(y1.codes, y2.codes) and torch.equal(y1.scales, y2.scales)
+
+
 def test_fused_unsupported_shapes_refused(mx):
     """Layers outside the fused kernels return MXC_ERR_SHAPE, nothing launched."""
     for cv, which in [(synth.conv_dict(16, 32, 32, 8, 8, 3, 1, 1), "both"),        # batch block 16
