@@ -1,36 +1,37 @@
 #!/usr/bin/env python3
 """Benchmark of the quantize-once MX convolution hot path on one MI355X.
 
-One step = one pass of the whole path over the layer sweep (batch 32, inputs
-resident in HBM): for each layer
-    3x3 s1 p1 64->64 at 56x56,  1x1 64->256 at 56x56,  3x3 s2 p1 128->256 at 28x28
-and each format (MXFP8 E4M3, MXFP4 E2M1): quantize X, W and G_Y once
-(activations arrive channel-batch-first in fp32, weights OIHW fp32), with the
-explicit CBF im2col of X written by the same launch that quantizes X and W
-(the forward operands), then the forward GEMM, and the input-gradient and
-weight-gradient GEMMs as one launch per layer (both read the quantized G_Y),
-the weight gradients' split-K partial sums of all layers finished by one
-reduction launch at the end: 25 kernels.  Activations are SiLU(N(0,1)),
-weights Kaiming-normal, gradients N(0, 1e-3), all seeded.
+Headline (`value`): one fwd+bwd training step of a YOLOv8n-shaped backbone
+and neck (51 convolutions with SiLU, concatenations and 2x upsampling; see
+paper_2609_28358_amd/workloads.py) at batch 64 on a 3x640x640 image, every
+tensor in MXFP4 (E2M1 elements, E8M0 scales) and quantized exactly once:
+weights from their bf16 masters, activations by the producing convolution's
+epilogue, gradients once per layer from the sum its consumers hand back.
+`value` = the step's GEMM flops (forward, input gradient, weight gradient;
+real channels only) over the step's wall time; the step is captured once into
+a HIP graph after warm-up and replayed `--steps` times between
+synchronizations, inputs resident in HBM.
 
-`value` is the conv fwd+bwd GEMM throughput of the whole step: the three
-GEMMs' algorithmic flops (2 N Cout Ho Wo Cin Kh Kw each, real channels) over
-the step's wall time, quantize and im2col included.  The timed step is
-replayed from one HIP graph (captured once after warm-up), so it measures
-GPU time, not Python launch cost.
+`roofline` belongs to the step's call that takes longest inside the step:
+every call's in-step duration is measured with HIP events recorded on the
+step's stream between consecutive calls of an eagerly enqueued step (behind
+a GPU spin, so the events bracket kernels, not host launch latency);
+`achieved` = the call's algorithmic bytes (or flops) / that duration.
+`traffic` comes from the committed FETCH_SIZE / WRITE_SIZE counter summary of
+the same step (profiles/), while the sources still hash to it.
 
-Per op, two times are reported in `ops`: `ms`, the op's kernel time in
-steady state -- a HIP graph of K back-to-back launches of the op, replayed on
-the stream its kernels run on and bracketed by HIP events (median of
-rounds); quantize launches rotate over enough copies of their fp32 source
-that it is read from HBM, not from the 256 MB last-level cache -- and
-`ms_alone`, one eager launch bracketed by HIP events behind a GPU spin
-(launch and event overhead included).  The op of the step with the largest
-`ms` gets the `roofline` object.  The unfused X+W quantize, the standalone
-im2col kernel, the input gradient alone and the whole weight gradient (GEMM
-and its own reduction) are timed too (`in_step` false), outside the step.
+Extra keys: `yolo_step` (every call's in-step time and roofline fraction,
+time by kind, per-layer algorithmic bytes against the naive comparator);
+`latent_replay_step` (the quantized-latent-replay back stack at batch 128,
+MXFP4, measured the same way); `layer_sweep` (the three-layer sweep at batch
+32 in MXFP8 and MXFP4 with steady-state per-op times, the measured naive
+comparator, and the fused-epilogue, FP6, stochastic-rounding and NVFP4
+legs); `cpu_baseline` (the fp64 oracle on a bounded sample of the headline
+workload, on the host).
 
-    python bench.py [--steps K] [--warmup W] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--no-cpu-baseline] [--no-sweep] [--no-qlr]
+    python bench.py --pmc-pass {yolo,qlr,sweep}        (under rocprofv3 --pmc)
+    python bench.py --summarize-trace DIR LOG | --summarize-pmc FDIR WDIR FLOG WLOG
 """
 import argparse
 import json
@@ -89,6 +90,7 @@ def layer_numbers(cv, fmt, mx):
 
 
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "op_traffic_pmc.md")
+PMC_YOLO = os.path.join(ROOT, "profiles", "yolo_b64_mxfp4_traffic_pmc.md")
 COPY_BYTES = 256 << 20                             # calibration copy of the counter pass
 
 
@@ -104,16 +106,18 @@ def source_digest():
     return h.hexdigest()[:16]
 
 
-def counter_traffic(op_key):
-    """HBM bytes per launch of `op_key` ("layer/format/op") from the committed
-    counter summary: FETCH_SIZE and WRITE_SIZE (KiB per dispatch, summed over
-    the op's kernels), each scaled by the factor the same counter gives for a
-    copy of known size.  None if there is no summary, the op is missing, or the
-    sources changed since the counters were taken."""
-    if not os.path.exists(PMC_SUMMARY):
+def counter_traffic(op_key, path=None):
+    """HBM bytes per launch of `op_key` ("layer/format/op", or "workload/call")
+    from a committed counter summary: FETCH_SIZE and WRITE_SIZE (KiB per
+    dispatch, summed over the op's kernels), each scaled by the factor the
+    same counter gives for a copy of known size.  None if there is no
+    summary, the op is missing, or the sources changed since the counters
+    were taken."""
+    path = path or PMC_SUMMARY
+    if not os.path.exists(path):
         return None
     digest, fetch_f, write_f, rows = None, None, None, {}
-    with open(PMC_SUMMARY) as f:
+    with open(path) as f:
         for line in f:
             t = line.strip()
             if t.startswith("source digest:"):
@@ -277,33 +281,13 @@ def naive_leg(jobs, op_ms, mx, synth, dev, stream, reps=3):
     return res
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-naive", action="store_true", help="skip the naive comparator leg")
-    ap.add_argument("--no-fused", action="store_true", help="skip the fused-epilogue leg")
-    ap.add_argument("--no-fp6", action="store_true", help="skip the FP6-method leg")
-    ap.add_argument("--no-sr", action="store_true", help="skip the stochastic-rounding leg")
-    ap.add_argument("--no-nvfp", action="store_true", help="skip the NVFP4 leg")
-    ap.add_argument("--pmc-pass", action="store_true",
-                    help="counter-collection pass: every op once in step order, then a copy of known size")
-    ap.add_argument("--layers", default="all", help="comma list of layer indices (profiling aid)")
-    ap.add_argument("--fmts", default="0,1")
-    args = ap.parse_args()
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the path has no "
-              f"multi-GPU part)", file=sys.stderr)
-        sys.exit(2)
-
+def sweep_leg(args):
+    """The layer sweep at batch 32 (three layers, MXFP8 and MXFP4) as one
+    step, with its per-op times, the naive comparator and the side legs."""
     import torch
     from paper_2609_28358_amd import mxconv as mx
     from paper_2609_28358_amd import synth
-    mx.lib()
     dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
 
     layers = list(range(len(synth.SWEEP_LAYERS))) if args.layers == "all" else [int(v) for v in args.layers.split(",")]
     fmts = [int(v) for v in args.fmts.split(",")]
@@ -412,9 +396,8 @@ def main():
         for _ in range(3):
             dst.copy_(src)
         torch.cuda.synchronize()
-        print(json.dumps({"pmc_pass": [f"{j['name']}/{op}" for j, op in seq], "copy_bytes": COPY_BYTES,
-                          "source_digest": source_digest()}))
-        return
+        return {"pmc_pass": [f"{j['name']}/{op}" for j, op in seq], "copy_bytes": COPY_BYTES,
+                "source_digest": source_digest()}
 
     # Per-op GPU time: each op alone, behind a GPU spin so that the event pair
     # brackets the kernel(s) and not the host's launch latency.
@@ -716,16 +699,12 @@ def main():
             ops[f"{nm}/{op}"]["mfma_frac"] = round(fl / (ms * 1e-3) / 1e12 / MFMA_TFLOPS[jmap[nm]["fmt"]], 4)
 
     out = {
-        "metric": "conv fwd+bwd TFLOPS (MXFP8/MXFP4) + quantize/im2col HBM GB/s, % of roofline",
-        "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "mxfp8+mxfp4 (fp32 accumulate)", "data": "synthetic",
-        "config": {"workload": "conv layer sweep, batch 32: 3x3 s1 64->64 56x56, 1x1 64->256 56x56, "
-                               "3x3 s2 128->256 28x28; each in MXFP8 and MXFP4; quantize X+W with X's CBF im2col (one "
-                               "launch) + quantize G_Y + fwd + dgrad and wgrad in one launch per layer, the six weight "
-                               "gradients' split-K reductions in one launch at the end",
-                   "global_batch": 32, "layers": [n for n, _ in synth.SWEEP_LAYERS], "formats": ["mxfp8", "mxfp4"],
-                   "parallelism": "single GPU"},
+        "value": round(value, 2), "unit": "TFLOP/s", "ms_per_step": round(ms_step, 4),
+        "workload": "conv layer sweep, batch 32: 3x3 s1 64->64 56x56, 1x1 64->256 56x56, 3x3 s2 128->256 28x28; "
+                    "each in MXFP8 and MXFP4; quantize X+W with X's CBF im2col (one launch) + quantize G_Y + fwd + "
+                    "dgrad and wgrad in one launch per layer, the six weight gradients' split-K reductions in one "
+                    "launch at the end",
+        "layers": [n for n, _ in synth.SWEEP_LAYERS], "formats": ["mxfp8", "mxfp4"],
         "roofline": rl,
         "ops": ops,
         "ops_sum_ms": round(sum(steady[k] for k in in_step), 4),
@@ -741,8 +720,436 @@ def main():
         out["stochastic_rounding"] = sr
     if nvfp:
         out["nvfp4"] = nvfp
+    return out
+
+
+def roofline(fl, by, ms, fmt):
+    """Roofline of one op from its algorithmic flops / bytes and time: HBM when
+    its arithmetic intensity is below the ridge of its format's MFMA peak."""
+    ai = fl / by if by else 0.0
+    if fl == 0 or ai * HBM_GBS * 1e9 < MFMA_TFLOPS[fmt] * 1e12:
+        ach = by / (ms * 1e-3) / 1e9
+        return {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_GBS, "unit": "GB/s", "frac": round(ach / HBM_GBS, 4)}
+    ach = fl / (ms * 1e-3) / 1e12
+    return {"bound": "mfma", "achieved": round(ach, 1), "peak": MFMA_TFLOPS[fmt], "unit": "TFLOP/s",
+            "frac": round(ach / MFMA_TFLOPS[fmt], 4)}
+
+
+def spin_rate():
+    """GPU spin cycles per millisecond of torch.cuda._sleep (measured)."""
+    import torch
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    torch.cuda._sleep(2_000_000)
+    e1.record()
+    torch.cuda.synchronize()
+    return 2_000_000 / max(e0.elapsed_time(e1), 1e-3)
+
+
+def instep_times(calls, reps=3):
+    """Duration of every call inside the step: the whole step enqueued
+    eagerly behind a GPU spin long enough for the host to enqueue every
+    call first, with a HIP event recorded on the step's stream between
+    consecutive calls; mean over `reps` steps (ms per call)."""
+    import torch
+    stream = torch.cuda.current_stream()
+    rate = spin_rate()
+    # host enqueue time of one step, measured, with a wide margin
+    t0 = time.perf_counter()
+    for c in calls:
+        c[1]()
+    torch.cuda.synchronize()
+    host_ms = (time.perf_counter() - t0) * 1e3
+    cycles = int(rate * (3.0 * host_ms + 5.0))
+    acc = [0.0] * len(calls)
+    for _ in range(reps):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)]
+        torch.cuda._sleep(cycles)
+        ev[0].record(stream)
+        for i, c in enumerate(calls):
+            c[1]()
+            ev[i + 1].record(stream)
+        torch.cuda.synchronize()
+        for i in range(len(calls)):
+            acc[i] += ev[i].elapsed_time(ev[i + 1]) / reps
+    return acc
+
+
+def step_leg(calls, flops, fmt, args, top=16):
+    """Time one network step: warm-up, then the step captured once into a HIP
+    graph and replayed args.steps times between synchronizations (value =
+    the step's GEMM flops / wall time); every call's in-step duration; the
+    roofline of the call that takes longest."""
+    import torch
+    for _ in range(args.warmup):
+        for c in calls:
+            c[1]()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for c in calls:
+            c[1]()
+    for _ in range(2):
+        g.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        g.replay()
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    del g
+    ins = instep_times(calls)
+    rows = []
+    for (lab, _, fl, by), ms in zip(calls, ins):
+        r = roofline(fl, by, ms, fmt)
+        row = {"call": lab, "ms": round(ms, 4), "bound": r["bound"], "frac": r["frac"],
+               "gbps": round(by / (ms * 1e-3) / 1e9, 1) if ms > 0 else None}
+        if fl:
+            row["tflops"] = round(fl / (ms * 1e-3) / 1e12, 1)
+            row["mfma_frac"] = round(fl / (ms * 1e-3) / 1e12 / MFMA_TFLOPS[fmt], 4)
+        rows.append(row)
+    dom = max(range(len(calls)), key=lambda i: ins[i])
+    rl = roofline(calls[dom][2], calls[dom][3], ins[dom], fmt)
+    rl.update({"kernel": calls[dom][0], "ms": round(ins[dom], 4), "algorithmic_flops": calls[dom][2],
+               "algorithmic_bytes": calls[dom][3]})
+    kinds = {}
+    for row in rows:
+        k = row["call"].split(" ")[0].rstrip("0123456789")
+        kinds[k] = round(kinds.get(k, 0.0) + row["ms"], 4)
+    return {"ms_per_step": round(ms_step, 4), "value": round(flops / (ms_step * 1e-3) / 1e12, 2),
+            "gemm_gflop": round(flops / 1e9, 2), "calls": len(calls), "instep_sum_ms": round(sum(ins), 4),
+            "ms_by_kind": kinds, "roofline": rl,
+            "top_calls": sorted(rows, key=lambda r: -r["ms"])[:top], "all_calls": rows}
+
+
+def net_bytes_vs_naive(net, n, fmt):
+    """Per convolution of the network: algorithmic bytes of one layer step of
+    the method (quantize X, W, G_Y once; the three GEMMs on MX operands,
+    im2col implicit) against the naive comparator's (fp32 im2col, six 1-D
+    quantizations, three GEMMs, col2im), by the same byte model as the layer
+    sweep's measured comparison, and the elements each quantizes."""
+    from paper_2609_28358_amd import mxconv as mx
+    from paper_2609_28358_amd import workloads as wl
+    per, ours_t, naive_t = {}, 0.0, 0.0
+    for t in net.convs():
+        cv = wl.conv_dict(t, n)
+        nums = layer_numbers(cv, fmt, mx)
+        ours = sum(nums[op][1] for op in ("quant_xw", "quant_gy", "fwd", "dgrad", "wgrad"))
+        nby, nq = naive_numbers(cv, fmt, mx)
+        nv = sum(nby.values())
+        ho, wo = t["h"], t["w"]
+        oq = n * cv["cin"] * cv["h"] * cv["w"] + cv["cout"] * cv["cin"] * cv["kh"] * cv["kw"] + n * cv["cout"] * ho * wo
+        per[t["name"]] = {"k": t["k"], "s": t["s"], "bytes_ours": round(ours), "bytes_naive": round(nv),
+                          "ratio": round(nv / ours, 2), "quantized_ours": oq, "quantized_naive": nq}
+        ours_t += ours
+        naive_t += nv
+    return {"total_bytes_ours": round(ours_t), "total_bytes_naive": round(naive_t),
+            "total_ratio": round(naive_t / ours_t, 2),
+            "layers_at_least_3x": sum(1 for v in per.values() if v["ratio"] >= 3.0), "layers": per}
+
+
+def cpu_baseline_net(net, n=32, fmt=1, min_s=10.0, max_s=30.0):
+    """The oracle on a bounded sample of the network workload: the network's
+    convolutions in order, each at one 32-sample group with its real shape
+    -- quantize X, W and G_Y (seeded synthetic tensors), then fwd, dgrad and
+    wgrad in fp64 -- until at least min_s seconds of oracle time."""
+    import oracle
+    from paper_2609_28358_amd import synth
+    from paper_2609_28358_amd import workloads as wl
+    flops, dt, done = 0.0, 0.0, []
+    for li, t in enumerate(net.convs()):
+        if dt >= min_s:
+            break
+        cv = wl.conv_dict(t, n)
+        x, w, gy = synth.layer_inputs(cv, 7000 + li, kind="sweep")
+        f = 2.0 * n * cv["cout"] * t["h"] * t["w"] * cv["cin"] * cv["kh"] * cv["kw"]
+        if dt + 3 * f / 2.0e10 > max_s:     # would overrun the bound at about 0.02 TFLOP/s
+            continue
+        t0 = time.perf_counter()
+        ox = oracle.quantize(x.numpy(), oracle.NCHW, oracle.ACT, fmt, *x.shape)
+        ow = oracle.quantize(w.numpy(), oracle.NCHW, oracle.WEIGHT, fmt, *w.shape)
+        og = oracle.quantize(gy.numpy(), oracle.NCHW, oracle.ACT, fmt, *gy.shape)
+        oracle.fwd(cv, fmt, ow, ox)
+        oracle.dgrad(cv, fmt, ow, og)
+        oracle.wgrad(cv, fmt, og, ox)
+        dt += time.perf_counter() - t0
+        flops += 3 * f
+        done.append(t["name"])
+    return {"value": round(flops / dt / 1e12, 5), "unit": "TFLOP/s", "cores": oracle.get_threads(), "kind": "oracle",
+            "sample": f"{len(done)} of the network's {len(net.convs())} convolutions in order ({done[0]} .. {done[-1]}), "
+                      f"each at one 32-sample group of its real shape with seeded inputs: quantize X, W, G_Y, then "
+                      f"fwd, dgrad and wgrad through the fp64 oracle; {dt:.1f} s, {flops / 1e9:.1f} GFLOP "
+                      f"(the flops as the padded channels the oracle computes)"}
+
+
+def pmc_pass(calls, label):
+    """Counter pass: every call of the step once (eager), each preceded by a
+    GPU spin kernel that delimits its dispatches in the counter output, then
+    a 256 MiB device copy three times (the calibration)."""
+    import torch
+    torch.cuda.synchronize()
+    for c in calls:
+        torch.cuda._sleep(100)
+        c[1]()
+        torch.cuda.synchronize()
+    torch.cuda._sleep(100)
+    src = torch.empty(COPY_BYTES, dtype=torch.uint8, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    return {"pmc_pass": label, "calls": [c[0] for c in calls], "algorithmic_bytes": [c[3] for c in calls],
+            "copy_bytes": COPY_BYTES, "source_digest": source_digest()}
+
+
+def _bench_line(log):
+    with open(log) as f:
+        for line in f:
+            if line.startswith("{"):
+                try:
+                    d = json.loads(line)
+                except ValueError:
+                    continue
+                if "metric" in d or "pmc_pass" in d:
+                    return d
+    raise SystemExit(f"no bench JSON line in {log}")
+
+
+def _csv_rows(d, suffix):
+    import csv
+    import glob
+    paths = sorted(glob.glob(os.path.join(d, "**", "*" + suffix), recursive=True))
+    if not paths:
+        raise SystemExit(f"no *{suffix} under {d}")
+    with open(paths[0]) as f:
+        return list(csv.DictReader(f))
+
+
+def _short(name):
+    return name.replace("mxc::(anonymous namespace)::", "").replace("void ", "").split("(")[0]
+
+
+def summarize_trace(rdir, log):
+    """Markdown summary of `rocprofv3 --kernel-trace --stats` over a default
+    run of this script: the YOLO-shaped step's kernels in step order (median
+    duration over every occurrence of the step in the run, beside the
+    in-step times the bench line measured with HIP events), the roofline
+    kernel's average, and every kernel of the run."""
+    import statistics
+    bench = _bench_line(log)
+    calls = bench["yolo_step"]["all_calls"]
+    rows = _csv_rows(rdir, "kernel_trace.csv")
+    ks = sorted((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), _short(r["Kernel_Name"]),
+                 int(r["Grid_Size_X"]) // max(1, int(r["Workgroup_Size_X"])), r) for r in rows)
+    ks = [k for k in ks if "at::" not in k[2] and "spin" not in k[2]]
+    n = len(calls)
+    # the step's kernel signature: the first n kernels of the run (its first warm-up step)
+    sig = [(k[2], k[3]) for k in ks[:n]]
+    wins, i = [], 0
+    while i + n <= len(ks):
+        if [(k[2], k[3]) for k in ks[i:i + n]] == sig:
+            wins.append(ks[i:i + n])
+            i += n
+        else:
+            i += 1
+    L = ["# Kernel trace: YOLOv8n-shaped fwd+bwd step, batch 64, MXFP4\n"]
+    L.append("Command (repository root on an MI355X machine; summary written by bench.py --summarize-trace):\n")
+    L.append("    cd /tmp && export TMPDIR=/tmp && rocprofv3 --kernel-trace --stats --output-format csv "
+             "-d <repo>/gpurun_out/ktrace -o run -- python3 <repo>/bench.py > <repo>/gpurun_out/ktrace.log\n")
+    rl = bench["roofline"]
+    L.append(f"Bench line of the same run: value {bench['value']} TFLOP/s, {bench['ms_per_step']} ms per step; "
+             f"roofline call `{rl['kernel']}` {rl['ms'] * 1000:.1f} us in the step (bound {rl['bound']}, achieved "
+             f"{rl['achieved']} {rl['unit']}, frac {rl['frac']}).\n")
+    if not wins:
+        L.append("The step's kernel sequence was not found as a repeating window; per-kernel stats only.\n")
+    else:
+        L.append(f"{len(wins)} occurrences of the step's {n}-kernel sequence in the trace (warm-up, graph replays, "
+                 f"in-step timing runs); kernel i of the sequence is call i of the step.\n")
+        L.append("| # | call | kernel | workgroups | median us (trace) | in-step us (bench, HIP events) |")
+        L.append("|---|---|---|---|---|---|")
+        dom = None
+        for j in range(n):
+            d = statistics.median([(w[j][1] - w[j][0]) / 1000 for w in wins])
+            if calls[j]["call"] == rl["kernel"]:
+                dom = (j, d)
+            L.append(f"| {j} | {calls[j]['call']} | {sig[j][0]} | {sig[j][1]} | {d:.1f} | {calls[j]['ms'] * 1000:.1f} |")
+        span = statistics.median([(w[-1][1] - w[0][0]) / 1000 for w in wins])
+        L.append(f"\nMedian span of one step occurrence: {span:.1f} us (bench ms_per_step {bench['ms_per_step'] * 1000:.1f} us).\n")
+        if dom:
+            j, d = dom
+            ds = [(w[j][1] - w[j][0]) / 1000 for w in wins]
+            L.append(f"## Roofline call `{rl['kernel']}`\n")
+            L.append(f"- kernel `{sig[j][0]}`, {sig[j][1]} workgroups: average {statistics.mean(ds):.1f} us over "
+                     f"{len(ds)} launches in the trace (median {d:.1f} us); bench.py in-step {rl['ms'] * 1000:.1f} us\n")
+    stats = {}
+    for k in ks:
+        stats.setdefault((k[2], k[3]), []).append((k[1] - k[0]) / 1000)
+    tot = sum(sum(v) for v in stats.values())
+    L.append("## Kernels of the run by total GPU time (top 30)\n")
+    L.append("| kernel | workgroups | calls | avg us | min us | max us | % of GPU time |")
+    L.append("|---|---|---|---|---|---|---|")
+    for key, v in sorted(stats.items(), key=lambda kv: -sum(kv[1]))[:30]:
+        L.append(f"| {key[0]} | {key[1]} | {len(v)} | {statistics.mean(v):.1f} | {min(v):.1f} | {max(v):.1f} | "
+                 f"{100 * sum(v) / tot:.1f} |")
+    return "\n".join(L) + "\n"
+
+
+def summarize_pmc(fdir, wdir, flog, wlog):
+    """Markdown summary of two `rocprofv3 --pmc` runs (FETCH_SIZE, then
+    WRITE_SIZE) of `bench.py --pmc-pass <workload>`: every call's counters
+    (KiB per dispatch, summed over its kernels; calls are delimited by the
+    spin kernel the pass launches before each), scaled by what the same
+    counter reads for the pass's 256 MiB copy, beside its algorithmic bytes."""
+    fi, wi = _bench_line(flog), _bench_line(wlog)
+    assert fi["calls"] == wi["calls"] and fi["source_digest"] == wi["source_digest"]
+
+    def per_call(d, ctr):
+        rows = [r for r in _csv_rows(d, "counter_collection.csv") if r["Counter_Name"] == ctr]
+        rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+        segs, cur = [], None
+        for r in rows:
+            nm = _short(r["Kernel_Name"])
+            if "spin" in nm or "sleep" in nm:
+                cur = []
+                segs.append(cur)
+            elif cur is not None:
+                cur.append((nm, float(r["Counter_Value"])))
+        segs = segs[-(len(fi["calls"]) + 1):]       # the pass: one segment per call, then the copies
+        if len(segs) != len(fi["calls"]) + 1:
+            raise SystemExit(f"{ctr}: found {len(segs)} delimited segments, expected {len(fi['calls']) + 1}")
+        copy = sorted(v for _, v in segs[-1])
+        return segs[:-1], copy[len(copy) // 2]
+
+    fs, fcopy = per_call(fdir, "FETCH_SIZE")
+    ws, wcopy = per_call(wdir, "WRITE_SIZE")
+    kib = fi["copy_bytes"] / 1024
+    ff, wf = kib / fcopy, kib / wcopy
+    label = fi["pmc_pass"]
+    L = [f"# HBM traffic per call from FETCH_SIZE / WRITE_SIZE counters: {label} step\n"]
+    L.append("Two counter passes over the same command, one counter each (repository root on an MI355X machine; "
+             "summary by bench.py --summarize-pmc):\n")
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        L.append(f"    cd /tmp && export TMPDIR=/tmp && timeout -s KILL 120 rocprofv3 --pmc {c} --output-format csv "
+                 f"-d <repo>/gpurun_out/pmc_{c} -o p -- python3 <repo>/bench.py --pmc-pass {label} --warmup 2")
+    L.append("\nThe pass runs every call of the step once (eager, in step order, each after a spin kernel that "
+             "delimits it), then copies 256 MiB device to device three times; the counters of that copy "
+             f"calibrate both: FETCH_SIZE {fcopy:.1f} KiB, WRITE_SIZE {wcopy:.1f} KiB for {kib:.0f} KiB moved.\n")
+    L.append(f"fetch factor: {ff:.4f}\n\nwrite factor: {wf:.4f}\n")
+    L.append(f"source digest: `{fi['source_digest']}`\n")
+    L.append("| call | kernels | FETCH_SIZE KiB | WRITE_SIZE KiB | HBM bytes (calibrated) | algorithmic bytes | ratio |")
+    L.append("|---|---|---|---|---|---|---|")
+    for c, a, f, w in zip(fi["calls"], fi["algorithmic_bytes"], fs, ws):
+        fk, wk = sum(v for _, v in f), sum(v for _, v in w)
+        hb = (fk * ff + wk * wf) * 1024
+        names = "+".join(sorted({nm for nm, _ in f}))
+        L.append(f"| {label}/{c} | {names} | {fk:.1f} | {wk:.1f} | {hb:.0f} | {a:.0f} | {hb / a if a else 0:.2f} |")
+    return "\n".join(L) + "\n"
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sweep", action="store_true", help="skip the layer-sweep leg")
+    ap.add_argument("--no-qlr", action="store_true", help="skip the latent-replay leg")
+    ap.add_argument("--no-naive", action="store_true", help="skip the naive comparator leg")
+    ap.add_argument("--no-fused", action="store_true", help="skip the fused-epilogue leg")
+    ap.add_argument("--no-fp6", action="store_true", help="skip the FP6-method leg")
+    ap.add_argument("--no-sr", action="store_true", help="skip the stochastic-rounding leg")
+    ap.add_argument("--no-nvfp", action="store_true", help="skip the NVFP4 leg")
+    ap.add_argument("--pmc-pass", default=None, choices=["yolo", "qlr", "sweep"],
+                    help="counter-collection pass over one workload's step (see pmc_pass)")
+    ap.add_argument("--layers", default="all", help="layer sweep: comma list of layer indices (profiling aid)")
+    ap.add_argument("--fmts", default="0,1", help="layer sweep: formats")
+    ap.add_argument("--summarize-trace", nargs=2, metavar=("ROCPROF_DIR", "BENCH_LOG"),
+                    help="write the kernel-trace summary of a rocprofv3 run of this script to stdout")
+    ap.add_argument("--summarize-pmc", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "FETCH_LOG", "WRITE_LOG"),
+                    help="write the counter summary of two rocprofv3 --pmc runs of --pmc-pass to stdout")
+    args = ap.parse_args()
+    if args.summarize_trace:
+        print(summarize_trace(*args.summarize_trace))
+        return
+    if args.summarize_pmc:
+        print(summarize_pmc(*args.summarize_pmc))
+        return
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported: every GPU box here has one GPU, "
+              f"and the path has no multi-GPU part", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_28358_amd import mxconv as mx
+    from paper_2609_28358_amd import workloads as wl
+    mx.lib()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    if args.pmc_pass == "sweep":
+        print(json.dumps(sweep_leg(args)))
+        return
+    N4, F4 = 64, mx.E2M1
+    if args.pmc_pass == "qlr":
+        q = wl.QlrStep(dev, fmt=mx.E2M1)
+        calls = q.calls()
+        for _ in range(2):
+            for c in calls:
+                c[1]()
+        print(json.dumps(pmc_pass(calls, "qlr")))
+        return
+
+    net = wl.yolo_net(640)
+    st = wl.NetStep(net, N4, F4, dev)
+    calls = st.calls()
+    if args.pmc_pass == "yolo":
+        for _ in range(2):
+            for c in calls:
+                c[1]()
+        print(json.dumps(pmc_pass(calls, "yolo")))
+        return
+    yolo = step_leg(calls, st.flops(), F4, args)
+    yolo["bytes_vs_naive"] = net_bytes_vs_naive(net, N4, F4)
+    del st, calls
+    torch.cuda.empty_cache()
+
+    qlr = None
+    if not args.no_qlr:
+        q = wl.QlrStep(dev, fmt=mx.E2M1)
+        qlr = step_leg(q.calls(), q.flops(), mx.E2M1, args)
+        qlr["workload"] = ("quantized latent replay, MXFP4: buffer of 8192 latents 128x16x16 kept as MX codes; batch "
+                           "128 = 3 replayed 32-sample groups (copied codes) + 32 fresh 3x128x128 inputs through the "
+                           "frozen front stack (3x3 s2 convs 3->32->64->128, SiLU); trainable back stack of four 3x3 "
+                           "convs 128->256, 256->256 x3 at 16x16, SiLU, fwd + bwd")
+        del q
+        torch.cuda.empty_cache()
+
+    sweep = None if args.no_sweep else sweep_leg(args)
+
+    rl = dict(yolo["roofline"])
+    rl["traffic"] = counter_traffic(f"yolo/{rl['kernel']}", PMC_YOLO)
+    out = {
+        "metric": "conv fwd+bwd TFLOPS (MXFP8/MXFP4) + quantize/im2col HBM GB/s, % of roofline",
+        "value": yolo["value"], "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": yolo["ms_per_step"], "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "mxfp4 (exact block products, fp32 accumulation)", "data": "synthetic",
+        "config": {"workload": "YOLOv8n-shaped backbone+neck, one fwd+bwd training step at batch 64, 3x640x640 "
+                               "input, MXFP4 E2M1 activations/weights/gradients: 51 convolutions with SiLU "
+                               "(stride-2 3x3 downsampling at widths 16-256, C2f-style 1x1/3x3 blocks, top-down "
+                               "and bottom-up neck with 2x upsampling and concatenation), every tensor quantized "
+                               "once; value = the step's GEMM flops (real channels) / step time",
+                   "global_batch": N4, "image": [3, 640, 640], "format": "mxfp4", "convolutions": len(net.convs()),
+                   "parallelism": "single GPU"},
+        "roofline": rl,
+        "yolo_step": yolo,
+    }
+    if qlr:
+        out["latent_replay_step"] = qlr
+    if sweep:
+        out["layer_sweep"] = sweep
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline()
+        out["cpu_baseline"] = cpu_baseline_net(net)
     print(json.dumps(out))
 
 
