@@ -665,7 +665,7 @@ __global__ __launch_bounds__(LT) void conv_lean_dg2_kernel(LeanArgs p) {
 // neither waits for the other, and the tail of one fills the CUs the other
 // leaves idle.  Both counts are multiples of 8, so each part keeps its own
 // kernel's XCD mapping.  Format F for every operand.
-template <int F, int KW, int PW, bool DG2>
+template <int F, int KW, int PW, bool DG2, int NB>
 __global__ __launch_bounds__(LT) void conv_lean_bwd_kernel(LeanArgs p, WLArgs q, int nl) {
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
     const int b = blockIdx.x;
@@ -674,7 +674,7 @@ __global__ __launch_bounds__(LT) void conv_lean_bwd_kernel(LeanArgs p, WLArgs q,
         if constexpr (DG2) lean_dg2_body<F, F, KW, 1, PW>(p, b - nw, nl);
         else               lean_body<F, F, true, KW, 1, 1, PW>(p, b - nw, nl);
     } else {
-        wgrad_tile<F, F>(q, b, nw, (float (*)[64 * 64])smem);
+        wgrad_tile<F, F, false, NB>(q, b, nw, (float (*)[32 * NB * 32 * NB])smem);
     }
 }
 
@@ -855,23 +855,30 @@ int lean_plan(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const 
     return 0;
 }
 
-template <int F, int KW, int PW, bool DG2>
+template <int F, int KW, int PW, bool DG2, int NB>
 int bwd_launch(const LeanArgs& a, const WLArgs& q, int nl, int grid, size_t lds, hipStream_t s) {
     static std::atomic<uint64_t> devs{0};
-    if (raise_lds(conv_lean_bwd_kernel<F, KW, PW, DG2>, devs, lds)) return MXC_ERR_HIP;
-    hipLaunchKernelGGL((conv_lean_bwd_kernel<F, KW, PW, DG2>), dim3(grid), dim3(LT), lds, s, a, q, nl);
+    if (raise_lds(conv_lean_bwd_kernel<F, KW, PW, DG2, NB>, devs, lds)) return MXC_ERR_HIP;
+    hipLaunchKernelGGL((conv_lean_bwd_kernel<F, KW, PW, DG2, NB>), dim3(grid), dim3(LT), lds, s, a, q, nl);
     return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
+}
+
+template <int F, int NB>
+int bwd_launch_nb(const LeanArgs& a, const WLArgs& q, int nl, int grid, size_t lds, bool dg2, int kw, int pw,
+                  hipStream_t s) {
+    if (dg2) {
+        if (kw == 3) return pw == 1 ? bwd_launch<F, 3, 1, true, NB>(a, q, nl, grid, lds, s) : bwd_launch<F, 3, 2, true, NB>(a, q, nl, grid, lds, s);
+        return pw == 1 ? bwd_launch<F, 1, 1, true, NB>(a, q, nl, grid, lds, s) : bwd_launch<F, 1, 2, true, NB>(a, q, nl, grid, lds, s);
+    }
+    if (kw == 3) return pw == 1 ? bwd_launch<F, 3, 1, false, NB>(a, q, nl, grid, lds, s) : bwd_launch<F, 3, 2, false, NB>(a, q, nl, grid, lds, s);
+    return pw == 1 ? bwd_launch<F, 1, 1, false, NB>(a, q, nl, grid, lds, s) : bwd_launch<F, 1, 2, false, NB>(a, q, nl, grid, lds, s);
 }
 
 template <int F>
 int bwd_launch_f(const LeanArgs& a, const WLArgs& q, int nl, int grid, size_t lds, bool dg2, int kw, int pw,
-                 hipStream_t s) {
-    if (dg2) {
-        if (kw == 3) return pw == 1 ? bwd_launch<F, 3, 1, true>(a, q, nl, grid, lds, s) : bwd_launch<F, 3, 2, true>(a, q, nl, grid, lds, s);
-        return pw == 1 ? bwd_launch<F, 1, 1, true>(a, q, nl, grid, lds, s) : bwd_launch<F, 1, 2, true>(a, q, nl, grid, lds, s);
-    }
-    if (kw == 3) return pw == 1 ? bwd_launch<F, 3, 1, false>(a, q, nl, grid, lds, s) : bwd_launch<F, 3, 2, false>(a, q, nl, grid, lds, s);
-    return pw == 1 ? bwd_launch<F, 1, 1, false>(a, q, nl, grid, lds, s) : bwd_launch<F, 1, 2, false>(a, q, nl, grid, lds, s);
+                 bool nb1, hipStream_t s) {
+    return nb1 ? bwd_launch_nb<F, 1>(a, q, nl, grid, lds, dg2, kw, pw, s)
+               : bwd_launch_nb<F, 2>(a, q, nl, grid, lds, dg2, kw, pw, s);
 }
 
 }  // namespace
@@ -917,20 +924,23 @@ int launch_lean_bwd(const Conv& dcv, const void* wc, const uint8_t* ws, const vo
     const long nl = ((long)(P.dg2 ? a.pofs[4] : a.ntiles) + 7) / 8 * 8;
     if (nl + wg > 0x7FFFFFFFL) return MXC_ERR_SHAPE;
     // ring depth for the combined grid, every workgroup holding at least the
-    // 64 KB the weight-gradient tile sums its waves through
+    // LDS the weight-gradient tile sums its four waves through (64 KB, or
+    // 16 KB on 32 x 32 tiles)
+    const bool nb1 = wgrad_single_block(wcv);
+    const long red = nb1 ? 16384 : 65536;
     const long per_cu = (nl + wg + 255) / 256;
     int nbuf = 2;
     for (int b = 4; b > 2; b--) {
-        const long need = (long)b * a.stage_bytes > 65536 ? (long)b * a.stage_bytes : 65536;
+        const long need = (long)b * a.stage_bytes > red ? (long)b * a.stage_bytes : red;
         if (per_cu * need <= LDS_MAX) { nbuf = b; break; }
     }
     a.nbuf = nbuf;
     const int used = nbuf < P.nstage ? nbuf : P.nstage;
     size_t lds = lean_lds(a, used);
-    if (lds < 65536) lds = 65536;
+    if (lds < (size_t)red) lds = (size_t)red;
     const int grid = (int)(nl + wg);
-    return f == MXC_E4M3 ? bwd_launch_f<MXC_E4M3>(a, q, (int)nl, grid, lds, P.dg2, dcv.kw, P.pw, s)
-                         : bwd_launch_f<MXC_E2M1>(a, q, (int)nl, grid, lds, P.dg2, dcv.kw, P.pw, s);
+    return f == MXC_E4M3 ? bwd_launch_f<MXC_E4M3>(a, q, (int)nl, grid, lds, P.dg2, dcv.kw, P.pw, nb1, s)
+                         : bwd_launch_f<MXC_E2M1>(a, q, (int)nl, grid, lds, P.dg2, dcv.kw, P.pw, nb1, s);
 }
 
 }  // namespace mxc

@@ -113,6 +113,11 @@ int launch_backward(const Conv& dcv, const void* wc, const uint8_t* ws, const vo
 // (0: not applicable); with more than one split the partial tiles go to the
 // workspace and are reduced by the caller
 int wgrad_lean_splits(const Conv& cv);
+// the batch-block-32 weight gradient on 32 x 32 tiles: G_Y and X each a
+// single channel block, formats MXFP8 or MXFP4
+inline bool wgrad_single_block(const Conv& cv) {
+    return cv.gy.ncb == 1 && cv.x.ncb == 1 && cv.fa == cv.fb && (cv.fa == MXC_E4M3 || cv.fa == MXC_E2M1);
+}
 int launch_wgrad_lean(const Conv& cv, const void* gc, const uint8_t* gs, const void* xc, const uint8_t* xs,
                       float* dst, int splits, hipStream_t s, const float* nv_tg = nullptr,
                       const float* nv_tx = nullptr);

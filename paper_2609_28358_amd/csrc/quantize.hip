@@ -508,6 +508,118 @@ __device__ __forceinline__ void quantize_block_body(const void* __restrict__ src
     if (SRC == 0 && col && col->codes) col_scatter<FMT>(*col, g, blk, lane, wq, sc);
 }
 
+// NCHW activations with at most NARROW_C channels (a network's input image)
+// and a batch block of 32.  Their single channel block per pixel holds only
+// C real rows, and in NCHW those rows are C x 32 planes apart, so a block is
+// never one contiguous run.  A workgroup takes one 32-sample group and
+// NARROW_P consecutive pixels: it reads the C x 32 source rows of those
+// pixels as contiguous 16-byte pieces, transposes them through LDS
+// ([pixel][channel][sample], rows padded by one float against bank
+// conflicts), and each wave then quantizes a quarter of the pixels one block
+// at a time in the lane layout of the one-block-per-wave quantizer (lane l:
+// channels 8 q + l / 8, samples 4 (l % 8) .. +3), writing every block as one
+// contiguous run.  Channels C .. 31 are zero codes.
+constexpr int NARROW_C = 4;
+constexpr int NARROW_P = 64;
+
+template <int DTYPE, int FMT, bool VECLOAD>
+__global__ __launch_bounds__(QT) void quantize_narrow_kernel(const void* __restrict__ src, Geom g,
+                                                             uint8_t* __restrict__ codes,
+                                                             uint8_t* __restrict__ scales, int tiles) {
+    constexpr int PS = NARROW_C * 32 + 1;                     // floats per pixel row
+    __shared__ float t[NARROW_P * PS];
+    const int tid = threadIdx.x;
+    const int hw = g.h * g.w;
+    const int grp = blockIdx.x / tiles, p0 = (blockIdx.x - grp * tiles) * NARROW_P;
+    constexpr int VEC = DTYPE == MXC_F32 ? 4 : 8;            // elements per 16-byte load
+    constexpr int LPR = NARROW_P / VEC;                       // lanes per source row
+    constexpr int RPP = QT / LPR;                             // rows per pass
+    const int rows = 32 * g.c;
+    const int k = tid % LPR;
+    for (int r = tid / LPR; r < rows; r += RPP) {
+        const int n = r / g.c, c = r - n * g.c;
+        const int sample = grp * 32 + n;
+        const int px = p0 + k * VEC;
+        float v[VEC];
+        const size_t base = ((size_t)sample * g.c + c) * hw;
+        if (VECLOAD && sample < g.n && px + VEC <= hw) {
+            if (DTYPE == MXC_F32) {
+                const float4 a = load_nt((const float*)src + base + px);
+                v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+            } else {
+                const v4i b = __builtin_nontemporal_load((const v4i*)((const unsigned short*)src + base + px));
+                const uint32_t w4[4] = {(uint32_t)b[0], (uint32_t)b[1], (uint32_t)b[2], (uint32_t)b[3]};
+#pragma unroll
+                for (int e = 0; e < 4; e++) {
+                    v[2 * e] = __uint_as_float(w4[e] << 16);
+                    v[2 * e + 1] = __uint_as_float(w4[e] & 0xFFFF0000u);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int e = 0; e < VEC; e++) {
+                const bool ok = sample < g.n && px + e < hw;
+                const size_t i = ok ? base + px + e : 0;
+                const float x = DTYPE == MXC_F32 ? __ldg((const float*)src + i)
+                                                 : __uint_as_float((uint32_t)__ldg((const unsigned short*)src + i) << 16);
+                v[e] = ok ? x : 0.0f;
+            }
+        }
+#pragma unroll
+        for (int e = 0; e < VEC; e++) t[(k * VEC + e) * PS + c * 32 + n] = v[e];
+    }
+    __syncthreads();
+    const int lane = tid & 63, wave = tid >> 6;
+    const int j = 4 * (lane & 7), row = lane >> 3;
+    constexpr int PPW = NARROW_P / (QT / 64);                 // pixels per wave
+    for (int i = 0; i < PPW; i++) {
+        const int pl = wave * PPW + i, pix = p0 + pl;
+        if (pix >= hw) break;                                 // wave-uniform
+        float4 x[4];
+#pragma unroll
+        for (int q = 0; q < 4; q++) x[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (row < g.c) {
+            const float* tp = t + pl * PS + row * 32 + j;
+            x[0] = make_float4(tp[0], tp[1], tp[2], tp[3]);
+        }
+        uint32_t m = __float_as_uint(x[0].x) & 0x7FFFFFFFu;
+        m = max(m, __float_as_uint(x[0].y) & 0x7FFFFFFFu);
+        m = max(m, __float_as_uint(x[0].z) & 0x7FFFFFFFu);
+        m = max(m, __float_as_uint(x[0].w) & 0x7FFFFFFFu);
+        m = wave_max_u32(m);
+        const uint32_t sc = scale_code_from_bits<fmt_emax(FMT)>(m);
+        const size_t blk = (size_t)grp * hw + pix;             // one channel block per pixel
+        if (lane == 0) scales[blk] = (uint8_t)sc;
+        const float inv = inv_scale(sc);
+        const bool bad = sc == 0xFFu;
+        if (FMT == MXC_E4M3) {
+            uint32_t* d = (uint32_t*)(codes + blk * 1024) + lane;
+#pragma unroll
+            for (int q = 0; q < 4; q++) d[64 * q] = bad ? 0u : pack4_e4m3(x[q], inv);
+        } else {
+            unsigned short* d = (unsigned short*)(codes + blk * 512) + lane;
+#pragma unroll
+            for (int q = 0; q < 4; q++) d[64 * q] = bad ? (unsigned short)0 : (unsigned short)pack4_e2m1(x[q], inv);
+        }
+    }
+}
+
+template <int DTYPE, int FMT>
+int launch_qn(const void* src, const Geom& g, void* codes, uint8_t* scales, hipStream_t s) {
+    const int hw = g.h * g.w;
+    const int tiles = (hw + NARROW_P - 1) / NARROW_P;
+    const long grid = (long)g.ng * tiles;
+    if (grid > 0x7FFFFFFFL) return MXC_ERR_SHAPE;
+    constexpr int VEC = DTYPE == MXC_F32 ? 4 : 8;
+    if (hw % VEC == 0)
+        hipLaunchKernelGGL((quantize_narrow_kernel<DTYPE, FMT, true>), dim3((unsigned)grid), dim3(QT), 0, s, src, g,
+                           (uint8_t*)codes, scales, tiles);
+    else
+        hipLaunchKernelGGL((quantize_narrow_kernel<DTYPE, FMT, false>), dim3((unsigned)grid), dim3(QT), 0, s, src, g,
+                           (uint8_t*)codes, scales, tiles);
+    return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
+}
+
 template <int SRC, int DTYPE, int FMT, bool SR>
 __global__ __launch_bounds__(QT) void quantize_block_kernel(const void* __restrict__ src, Geom g,
                                                             uint8_t* __restrict__ codes,
@@ -705,6 +817,15 @@ int launch_quantize(const void* src, int dtype, int layout, int role, const Geom
     if (blocksrc == 1)
         return dtype == MXC_F32 ? launch_qb_fmt<1, MXC_F32>(src, g, fmt, sr, codes, scales, s, k0, k1)
                                 : launch_qb_fmt<1, MXC_BF16>(src, g, fmt, sr, codes, scales, s, k0, k1);
+    // a few-channel NCHW activation (an input image), round to nearest
+    if (layout == MXC_NCHW && role == MXC_ACT && g.bn == 32 && g.c <= NARROW_C && !sr &&
+        (fmt == MXC_E4M3 || fmt == MXC_E2M1)) {
+        if (dtype == MXC_F32)
+            return fmt == MXC_E4M3 ? launch_qn<MXC_F32, MXC_E4M3>(src, g, codes, scales, s)
+                                   : launch_qn<MXC_F32, MXC_E2M1>(src, g, codes, scales, s);
+        return fmt == MXC_E4M3 ? launch_qn<MXC_BF16, MXC_E4M3>(src, g, codes, scales, s)
+                               : launch_qn<MXC_BF16, MXC_E2M1>(src, g, codes, scales, s);
+    }
     switch (layout) {
         case MXC_NCHW: return launch_q_dt<MXC_NCHW>(src, dtype, g, fmt, sr, codes, scales, s, k0, k1);
         case MXC_NHWC: return launch_q_dt<MXC_NHWC>(src, dtype, g, fmt, sr, codes, scales, s, k0, k1);

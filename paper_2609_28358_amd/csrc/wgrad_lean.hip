@@ -24,10 +24,10 @@ namespace mxc {
 
 namespace {
 
-template <int FA, int FB, bool NV = false>
+template <int FA, int FB, bool NV = false, int NB = 2>
 __global__ __launch_bounds__(WT) void wgrad_lean_kernel(WLArgs p) {
-    __shared__ float red[4][64 * 64];
-    wgrad_tile<FA, FB, NV>(p, blockIdx.x, gridDim.x, red);
+    __shared__ float red[4][32 * NB * 32 * NB];
+    wgrad_tile<FA, FB, NV, NB>(p, blockIdx.x, gridDim.x, red);
 }
 
 }  // namespace
@@ -40,9 +40,13 @@ int wgrad_lean_splits(const Conv& cv) {
     const long npairs = (npix + 1) / 2;
     const long ntiles = (long)cv.kh * cv.kw * ((cv.gy.ncb + 1) / 2) * ((cv.x.ncb + 1) / 2);
     if (npix > 0x3FFFFFFFL || ntiles > 0x7FFFFFL) return 0;
-    // about two workgroups per CU, each wave with at least 4 pixel pairs
-    long splits = 512 / ntiles;
-    const long cap = npairs / (4 * 4);
+    // about two workgroups per CU, each wave with at least 4 pixel pairs; a
+    // layer on 32 x 32 tiles (one channel block on each side) keeps a quarter
+    // of the LDS per workgroup, so about five fit on a CU, each wave with at
+    // least 8 pairs
+    const bool nb1 = wgrad_single_block(cv);
+    long splits = (nb1 ? 1280 : 512) / ntiles;
+    const long cap = npairs / (4 * (nb1 ? 8 : 4));
     if (splits > cap) splits = cap;
     if (splits < 1) splits = 1;
     return (int)splits;
@@ -59,8 +63,14 @@ int launch_wgrad_lean(const Conv& cv, const void* gc, const uint8_t* gs, const v
         hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E2M1, MXC_E2M1, true>), gd, dim3(WT), 0, s, a);
         return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
     }
-    if (cv.fa == MXC_E4M3 && cv.fb == MXC_E4M3)      hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E4M3, MXC_E4M3>), gd, dim3(WT), 0, s, a);
-    else if (cv.fa == MXC_E2M1 && cv.fb == MXC_E2M1) hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E2M1, MXC_E2M1>), gd, dim3(WT), 0, s, a);
+    const bool nb1 = wgrad_single_block(cv);
+    if (cv.fa == MXC_E4M3 && cv.fb == MXC_E4M3) {
+        if (nb1) hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E4M3, MXC_E4M3, false, 1>), gd, dim3(WT), 0, s, a);
+        else     hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E4M3, MXC_E4M3>), gd, dim3(WT), 0, s, a);
+    } else if (cv.fa == MXC_E2M1 && cv.fb == MXC_E2M1) {
+        if (nb1) hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E2M1, MXC_E2M1, false, 1>), gd, dim3(WT), 0, s, a);
+        else     hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E2M1, MXC_E2M1>), gd, dim3(WT), 0, s, a);
+    }
     else if (cv.fa == MXC_E2M3 && cv.fb == MXC_E2M3) hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E2M3, MXC_E2M3>), gd, dim3(WT), 0, s, a);
     else if (cv.fa == MXC_E2M1 && cv.fb == MXC_E3M2) hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E2M1, MXC_E3M2>), gd, dim3(WT), 0, s, a);
     else return MXC_ERR_ARG;

@@ -55,9 +55,15 @@ __device__ __forceinline__ v8i row_frag(const uint8_t* p0, const uint8_t* p1, co
 
 // NV: NVFP4 operands, decoded to fp16 per fragment and multiplied on fp16
 // MFMAs (the 8-sample groups of a row each have their own E4M3 scale).
-template <int FA, int FB, bool NV = false>
-__device__ __forceinline__ void wgrad_tile(const WLArgs& p, int bid, int nblk, float (*red)[64 * 64]) {
+// NB: 32-row blocks per tile side -- 2 (a 64 x 64 tile), or 1 for a layer
+// whose G_Y and X both have a single channel block (a 32 x 32 tile: half the
+// loads and a quarter of the products per pixel pair, so twice the pairs per
+// batch).
+template <int FA, int FB, bool NV = false, int NB = 2>
+__device__ __forceinline__ void wgrad_tile(const WLArgs& p, int bid, int nblk, float (*red)[32 * NB * 32 * NB]) {
     static_assert(!NV || (FA == MXC_E2M1 && FB == MXC_E2M1), "NVFP4 operands only");
+    static_assert(NB == 1 || NB == 2, "one or two blocks per tile side");
+    constexpr int RS = 32 * NB;                   // tile side; red[wave] holds RS x RS floats
     constexpr int RBA = 32 * fmt_bits(FA) / 8;    // bytes of one block row (32 samples): G_Y
     constexpr int RBB = 32 * fmt_bits(FB) / 8;    // X
     constexpr int TBA = 32 * RBA, TBB = 32 * RBB; // bytes of one block
@@ -90,11 +96,11 @@ __device__ __forceinline__ void wgrad_tile(const WLArgs& p, int bid, int nblk, f
     }
     const uint32_t gy_pix = (uint32_t)p.gy_ncb * TBA, x_pix = (uint32_t)p.x_ncb * TBB;
 
-    v16f acc[2][2];
+    v16f acc[NB][NB];
 #pragma unroll
-    for (int i = 0; i < 2; i++)
+    for (int i = 0; i < NB; i++)
 #pragma unroll
-        for (int j = 0; j < 2; j++)
+        for (int j = 0; j < NB; j++)
 #pragma unroll
             for (int e = 0; e < 16; e++) acc[i][j][e] = 0.0f;
 
@@ -124,7 +130,7 @@ __device__ __forceinline__ void wgrad_tile(const WLArgs& p, int bid, int nblk, f
             }
         }
 #pragma unroll
-        for (int i = 0; i < 2; i++) {
+        for (int i = 0; i < NB; i++) {
             const uint8_t* ap[2];
             const uint8_t* bp[2];
 #pragma unroll
@@ -155,7 +161,7 @@ __device__ __forceinline__ void wgrad_tile(const WLArgs& p, int bid, int nblk, f
     // batches of PB pairs: all loads of a batch are in flight together (the
     // loop is bound by memory latency, not by the MFMAs); pairs past the
     // wave's range get a zero G_Y operand and add nothing
-    constexpr int PB = NV ? 2 : 4;
+    constexpr int PB = NV ? 2 : NB == 1 ? 8 : 4;
     for (int q = q0; q < q1; q += PB) {
         Ops o[PB];
 #pragma unroll
@@ -163,32 +169,32 @@ __device__ __forceinline__ void wgrad_tile(const WLArgs& p, int bid, int nblk, f
 #pragma unroll
         for (int b = 0; b < PB; b++) {
             if constexpr (NV) {
-                uint32_t ad[2][16], bd[2][16];
+                uint32_t ad[NB][16], bd[NB][16];
 #pragma unroll
-                for (int i = 0; i < 2; i++) {
+                for (int i = 0; i < NB; i++) {
                     nv_decode32(o[b].a[i], o[b].na[i], ad[i]);
                     nv_decode32(o[b].b[i], o[b].nb[i], bd[i]);
                 }
 #pragma unroll
-                for (int i = 0; i < 2; i++)
+                for (int i = 0; i < NB; i++)
 #pragma unroll
-                    for (int j = 0; j < 2; j++) acc[i][j] = mfma_nv(ad[i], bd[j], acc[i][j]);
+                    for (int j = 0; j < NB; j++) acc[i][j] = mfma_nv(ad[i], bd[j], acc[i][j]);
             } else if constexpr (FA == MXC_E4M3) {   // MXFP8: each fragment decoded to bf16 once
-                uint32_t ad[2][16], bd[2][16];
+                uint32_t ad[NB][16], bd[NB][16];
 #pragma unroll
-                for (int i = 0; i < 2; i++) {
+                for (int i = 0; i < NB; i++) {
                     e4m3_decode32_lane(o[b].a[i], o[b].sa[i], ad[i]);
                     e4m3_decode32_lane(o[b].b[i], o[b].sb[i], bd[i]);
                 }
 #pragma unroll
-                for (int i = 0; i < 2; i++)
+                for (int i = 0; i < NB; i++)
 #pragma unroll
-                    for (int j = 0; j < 2; j++) acc[i][j] = mfma_x8(ad[i], bd[j], acc[i][j]);
+                    for (int j = 0; j < NB; j++) acc[i][j] = mfma_x8(ad[i], bd[j], acc[i][j]);
             } else {
 #pragma unroll
-                for (int i = 0; i < 2; i++)
+                for (int i = 0; i < NB; i++)
 #pragma unroll
-                    for (int j = 0; j < 2; j++)
+                    for (int j = 0; j < NB; j++)
                         acc[i][j] = mfma_mx<FA, FB>(o[b].a[i], o[b].b[j], acc[i][j], o[b].sa[i], o[b].sb[j]);
             }
         }
@@ -196,28 +202,28 @@ __device__ __forceinline__ void wgrad_tile(const WLArgs& p, int bid, int nblk, f
     if constexpr (NV) {   // the per-tensor scales T_GY T_X
         const float tt = *p.tg * *p.tx;
 #pragma unroll
-        for (int i = 0; i < 2; i++)
+        for (int i = 0; i < NB; i++)
 #pragma unroll
-            for (int j = 0; j < 2; j++)
+            for (int j = 0; j < NB; j++)
 #pragma unroll
                 for (int e = 0; e < 16; e++) acc[i][j][e] *= tt;
     }
 
     // ---- sum the four waves' tiles, then write
 #pragma unroll
-    for (int i = 0; i < 2; i++)
+    for (int i = 0; i < NB; i++)
 #pragma unroll
-        for (int j = 0; j < 2; j++)
+        for (int j = 0; j < NB; j++)
 #pragma unroll
             for (int e = 0; e < 16; e++) {
                 const int row = 32 * i + 8 * (e >> 2) + 4 * hf + (e & 3);
-                red[wave][row * 64 + 32 * j + r] = acc[i][j][e];
+                red[wave][row * RS + 32 * j + r] = acc[i][j][e];
             }
     __syncthreads();
 #pragma unroll 4
-    for (int k = 0; k < 16; k++) {
+    for (int k = 0; k < RS * RS / WT; k++) {
         const int idx = tid + WT * k;
-        const int row = idx >> 6, col = idx & 63;
+        const int row = idx / RS, col = idx % RS;
         const float v = (red[0][idx] + red[1][idx]) + (red[2][idx] + red[3][idx]);
         const int co = cop * 64 + row, ci = cip * 64 + col;
         if (p.direct) {

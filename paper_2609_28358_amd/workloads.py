@@ -151,10 +151,11 @@ class NetStep:
     padding channels); the upstream gradient of each output ~ N(0, 1e-3),
     fp32 CBF."""
 
-    def __init__(self, net, n, fmt, device, seed=3000):
+    def __init__(self, net, n, fmt, device, seed=3000, fused_dgrad=True):
         if n % 32:
             raise ValueError("the network step runs batch blocks of 32")
         self.net, self.n, self.fmt, self.dev = net, n, fmt, device
+        self.fused = fused_dgrad
         self.convs = net.convs()
         img = net.nodes[0]
         self.image = synth.uniform((n, img["c"], img["h"], img["w"]), seed).to(torch.bfloat16).to(device)
@@ -207,6 +208,13 @@ class NetStep:
             full[:, off:off + c] = wm[:, r:r + c]
             r += c
         return full
+
+    def _fusable(self, t):
+        """Conv t's input is another conv's output that only t reads and that
+        is no network output: t's input-gradient epilogue can quantize it."""
+        src = self.net.node(t["src"])
+        return (src["kind"] == "conv" and self.consumers[src["name"]] == [("conv", t["name"])]
+                and src["name"] not in self.ext)
 
     # consumers of every tensor: ("conv", conv name) or ("concat", concat name, part index)
     def _plan_backward(self):
@@ -272,21 +280,36 @@ class NetStep:
                 by = sum(mxb(A, fmt, self.t[p].shape) for p, _ in t["parts"]) + mxb(A, fmt, oshape)
                 seq.append((f"concat {nm}", lambda parts=parts, nm=nm: mx.concat_cbf(parts, out=self.t[nm]), 0.0, by))
         # backward, in reverse order: quantize a conv's G_Y once its consumers
-        # have handed back their gradients, then its input and weight gradients
+        # have handed back their gradients, then its input and weight
+        # gradients.  A conv whose input is read by it alone (and is no
+        # output) quantizes that input's gradient in its input-gradient
+        # epilogue (times SiLU' at the producer's pre-activation), so the
+        # producer's G_Y never exists in fp32.
+        fused_in = {t["src"] for t in self.convs if self.fused and self._fusable(t)}
         for t in reversed(self.convs):
             nm = t["name"]
-            terms = self.grad_terms(nm)
             shape = (n, t["c"], t["h"], t["w"])
-            el = math.prod(shape)
-            by = sum(4.0 * el * (4 if d else 1) for _, _, _, d in terms) + 4.0 * el + mxb(A, fmt, shape)
-            seq.append((f"quant_gy {nm}", lambda terms=terms, shape=shape, nm=nm: mx.quantize_sum(
-                terms, shape, fmt, fn=mx.FN_SILU, z=self.y[nm], out=self.gy[nm]), 0.0, by))
+            if nm not in fused_in:
+                terms = self.grad_terms(nm)
+                el = math.prod(shape)
+                by = sum(4.0 * el * (4 if d else 1) for _, _, _, d in terms) + 4.0 * el + mxb(A, fmt, shape)
+                seq.append((f"quant_gy {nm}", lambda terms=terms, shape=shape, nm=nm: mx.quantize_sum(
+                    terms, shape, fmt, fn=mx.FN_SILU, z=self.y[nm], out=self.gy[nm]), 0.0, by))
             src = net.node(t["src"])
-            xb = mxb(A, fmt, (n, src["c"], src["h"], src["w"]))
+            sshape = (n, src["c"], src["h"], src["w"])
+            xb = mxb(A, fmt, sshape)
             wb = mxb(W, fmt, tuple(self.w[nm][0].shape))
             gwb = 4.0 * self.gw[nm].numel()
             f = real_flops(t, n)
-            if nm in self.gx:
+            if t["src"] in fused_in:
+                sn = t["src"]
+                seq.append((f"dgrad_quant {nm}", lambda nm=nm, sn=sn: mx.dgrad_quant(
+                    self.cv[nm], self.w[nm][1], self.gy[nm], fn=mx.FN_SILU, z=self.y[sn], out=self.gy[sn]),
+                    f, wb + mxb(A, fmt, shape) + 4.0 * math.prod(sshape) + mxb(A, fmt, sshape)))
+                seq.append((f"wgrad {nm}", lambda nm=nm, t=t: mx.wgrad(
+                    self.cv[nm], self.gy[nm], self.t[t["src"]], out=self.gw[nm], workspace=self.ws[nm],
+                    deferred=True), f, mxb(A, fmt, shape) + xb + gwb))
+            elif nm in self.gx:
                 seq.append((f"bwd {nm}", lambda nm=nm, t=t: mx.backward(
                     self.cv[nm], self.w[nm][1], self.gy[nm], self.t[t["src"]], layout=mx.CBF, gx_out=self.gx[nm],
                     gw_out=self.gw[nm], workspace=self.ws[nm], deferred=True),

@@ -56,6 +56,25 @@ def test_quantize_nchw_f32(mx, fmt, shape):
     _qcheck(mx, t, mx.ACT, fmt, mx.NCHW, shape)
 
 
+NARROW_SHAPES = [(32, 3, 17, 19), (64, 3, 40, 40), (32, 1, 8, 8), (96, 4, 5, 13), (64, 2, 1, 130), (32, 3, 64, 64)]
+
+
+@pytest.mark.parametrize("fmt", [0, 1], ids=["e4m3", "e2m1"])
+@pytest.mark.parametrize("bf16", [False, True], ids=["f32", "bf16"])
+@pytest.mark.parametrize("shape", NARROW_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_quantize_narrow_nchw(mx, fmt, bf16, shape):
+    """An input image: NCHW with at most 4 channels and batch block 32 (its
+    own kernel; pixel counts that are and are not multiples of the load width,
+    partial pixel tiles, U(0, 1) and wide-range values)."""
+    t = synth.uniform(shape, 17 + shape[1]) if shape[2] > 16 else (
+        synth.normal(shape, 1.0, 3) * torch.exp(synth.normal(shape, 3.0, 4)))
+    if bf16:
+        tb = t.to(torch.bfloat16)
+        _qcheck(mx, tb.float(), mx.ACT, fmt, mx.NCHW, shape, tb)
+    else:
+        _qcheck(mx, t, mx.ACT, fmt, mx.NCHW, shape)
+
+
 @pytest.mark.parametrize("fmt", [0, 1], ids=["e4m3", "e2m1"])
 @pytest.mark.parametrize("layout", ["nhwc", "cbf", "bf16"])
 def test_quantize_layouts_and_bf16(mx, fmt, layout):
@@ -180,6 +199,9 @@ GEMM_CONVS = [
     synth.conv_dict(32, 32, 256, 5, 6, 3, 1, 1),              # 256 output channels: 4 row groups per tile
     synth.conv_dict(32, 256, 64, 6, 7, 1, 1, 0),              # 1x1 with 256 input channels (dgrad rows)
     synth.conv_dict(32, 96, 200, 7, 9, 3, 2, 1),              # ragged channels at stride 2
+    synth.conv_dict(32, 16, 16, 20, 18, 3, 1, 1),             # one channel block on each side (32 x 32 wgrad tiles)
+    synth.conv_dict(64, 3, 16, 24, 22, 3, 2, 1),              # an image layer: 3 channels, stride 2, one block each
+    synth.conv_dict(32, 32, 16, 9, 9, 1, 1, 0),
 ]
 
 
