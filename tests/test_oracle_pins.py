@@ -941,6 +941,40 @@ def test_nvfp_hand_worked_blocks():
     assert scales[2:].tolist() == [0, 0]                  # padded channels 16-31
 
 
+def test_nvfp_element_step_is_a_correctly_rounded_quotient():
+    """Eq. (6)'s element step divides x by the fp32 product B T.  Elements
+    placed exactly on a rounding tie of the E2M1 grid (x = m B with m a
+    midpoint of two grid values, so x / (B T) = m exactly when T = 1) must
+    take the tie's even code; a route through the reciprocal, x * fl(1 / BT),
+    lands a little above or below m and picks the other neighbour for some of
+    them.  The test first checks, in numpy float32 arithmetic, that the
+    reciprocal route does move at least a few of these elements, so it pins
+    the quotient."""
+    mids = [0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0]
+    even = {0.25: 0, 0.75: 2, 1.25: 2, 1.75: 4, 2.5: 4, 3.5: 6, 5.0: 6}     # RNE: the even code of the two
+    bs = [m / 8.0 * 2.0 ** e for m in range(9, 16) for e in (-3, 0, 4)]     # E4M3 block scales, 1.xxx * 2^e
+    nblk = len(bs) + 1
+    x = np.zeros((8, 8 * nblk, 1, 1), dtype=np.float32)
+    x[0, 0, 0, 0] = 2688.0                        # block 0: amax = 448 * 6, so T = 1
+    for k, b in enumerate(bs):
+        ch = 8 * (k + 1)
+        x[0, ch, 0, 0] = 6.0 * b                  # block max: B = CastE4M3(6 b / (1 * 6)) = b exactly
+        for i, m in enumerate(mids):
+            x[1 + i, ch, 0, 0] = m * b            # exact in fp32 (b has 4 significant bits)
+    codes, scales, t = oracle.nvfp_quantize(x, oracle.NCHW, oracle.ACT, oracle.E2M1, 8, 8 * nblk, 1, 1)
+    assert t == 1.0
+    moved = 0
+    for k, b in enumerate(bs):
+        blk = k + 1
+        assert float(oracle.decode(int(scales[blk]), oracle.E4M3)) == b
+        for i, m in enumerate(mids):
+            pos = 8 * blk * 8 + 1 + i             # code position of (channel 8 blk, sample 1 + i)
+            assert _code_at(codes, oracle.E2M1, pos) == even[m], (b, m)
+            recip = np.float32(np.float32(m * b) * (np.float32(1.0) / np.float32(b)))
+            moved += oracle.encode(float(recip), oracle.E2M1) != even[m]
+    assert moved >= 5, moved                      # the reciprocal route would fail this test
+
+
 @pytest.mark.parametrize("fmt", ALL_FMTS)
 def test_nvfp_block_scale_cast_matches_torch(fmt):
     """Eq. (5)'s CastE4M3 of every block against torch's float8 E4M3 cast of
