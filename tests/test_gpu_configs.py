@@ -9,10 +9,14 @@
   the stored codes, no requantization) and 32 fresh ones, and the back stack's
   3x3 convolutions on such a batch.
 
+* Every distinct convolution of the YOLOv8n-shaped network of
+  paper_2609_28358_amd.workloads (the benchmark's headline step) at batch 64
+  in MXFP4, CBF activations, seeded synthetic operands of the layer's shape.
+
 Codes and scales are compared bit for bit over whole tensors (the buffer: on
-sampled groups); GEMM outputs on 2048 seeded samples per GEMM against the
-oracle's single-output routines, within 1e-5 of the sum of absolute products
-(+ 2^-10 G for MXFP8, see mx_tolerance.py).
+sampled groups); GEMM outputs on 4096 seeded samples per GEMM (every element
+of a small weight gradient) against the oracle's single-output routines,
+within 1e-5 of the sum of absolute products.
 """
 import numpy as np
 import pytest
@@ -25,7 +29,7 @@ from paper_2609_28358_amd import synth
 pytestmark = pytest.mark.gpu
 
 DEV = "cuda:0"
-SAMPLES = 2048
+SAMPLES = 4096
 
 
 @pytest.fixture(scope="module")
@@ -82,7 +86,7 @@ def _check_gemms(mx, cv, fmt, q, o, layout, seed):
     if np.prod(wdims) <= SAMPLES:                       # small weights: every element
         idx = np.stack(np.meshgrid(*[np.arange(d) for d in wdims], indexing="ij"), -1).reshape(-1, 4)
     else:
-        idx = _idx(rng, wdims, SAMPLES // 4)
+        idx = _idx(rng, wdims, SAMPLES)
     r, s = oracle.wgrad_at(cv, fmt, o["gy"], o["x"], idx)
     errs["wgrad"] = mxt.gemm_err(gw.cpu().numpy()[tuple(idx.T)], r, s)
     assert max(errs.values()) <= 1.0, errs
@@ -173,3 +177,48 @@ def test_latent_back_stack_second_layer(mx):
         o[k] = oracle.quantize(t.numpy(), oracle.NCHW, role, fmt, *t.shape)
         _same(q[k], o[k], k)
     _check_gemms(mx, cv, fmt, q, o, "cbf", 4013)
+
+
+# ------------------------------------------------------------------ the network step's layers
+def _distinct_net_layers():
+    from paper_2609_28358_amd import workloads as wl
+    seen, out = set(), []
+    for t in wl.yolo_net(640).convs():
+        key = (t["cin"], t["cin_real"], t["cout"], t["k"], t["s"], t["src_h"])
+        if key not in seen:
+            seen.add(key)
+            out.append(t)
+    return out
+
+
+NET_LAYERS = _distinct_net_layers()
+
+
+@pytest.mark.parametrize("t", NET_LAYERS, ids=[t["name"] for t in NET_LAYERS])
+def test_network_layer_full_size(mx, t):
+    """One convolution of the headline network at batch 64, MXFP4: X from a
+    CBF fp32 tensor (the image: bf16 NCHW, U(0, 1)), W bf16, G_Y CBF fp32."""
+    from paper_2609_28358_amd import workloads as wl
+    fmt, n = oracle.E2M1, 64
+    cv = wl.conv_dict(t, n)
+    print(f"network layer {t['name']} {cv}", flush=True)
+    seed = 6000 + NET_LAYERS.index(t)
+    ho, wo = synth.out_hw(cv)
+    xs = (n, cv["cin"], cv["h"], cv["w"])
+    w = synth.kaiming(cv["cout"], cv["cin"], cv["kh"], cv["kw"], seed * 3 + 1).to(torch.bfloat16)
+    gy = synth.normal((n, cv["cout"], ho, wo), 1e-3, seed * 3 + 2)
+    if t["src"] == "image":
+        x = synth.uniform(xs, seed * 3).to(torch.bfloat16)
+        qx = mx.quantize(x.to(DEV), mx.ACT, fmt)
+        xo = x.float()
+    else:
+        xo = synth.silu_normal(xs, seed * 3)
+        qx = mx.quantize(synth.nchw_to_cbf(xo, 32).to(DEV), mx.ACT, fmt, layout=mx.CBF, shape=xs)
+    q = {"x": qx, "w": mx.quantize(w.to(DEV), mx.WEIGHT, fmt),
+         "gy": mx.quantize(synth.nchw_to_cbf(gy, 32).to(DEV), mx.ACT, fmt, layout=mx.CBF, shape=tuple(gy.shape))}
+    torch.cuda.synchronize()
+    o = {}
+    for k, tt, role in (("x", xo, oracle.ACT), ("w", w.float(), oracle.WEIGHT), ("gy", gy, oracle.ACT)):
+        o[k] = oracle.quantize(tt.numpy(), oracle.NCHW, role, fmt, *tt.shape)
+        _same(q[k], o[k], k)
+    _check_gemms(mx, cv, fmt, q, o, "cbf", seed)
