@@ -497,6 +497,25 @@ int mxconv_dgrad_quant(const mxc_conv* cv, int fmt,
                        int fn, const float* z, int out_fmt,
                        void* gx_codes, uint8_t* gx_scales, float* gx_act, void* stream);
 
+/* ------------------------------------------------------------------ no allocation */
+/* mxconv_wgrad for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Same arguments and results as mxconv_wgrad without the workspace: the
+ * split-K partial sums go to a library-owned device array of
+ * MXC_NOALLOC_WS_MAX bytes that every GPU the library runs on holds until
+ * the process ends (its address on a device is looked up on the first call
+ * made with that device current).  The call itself allocates nothing.
+ * Calls that overlap in time on one GPU (different streams or host threads)
+ * share that array and race; the array keeps the last call's partial sums.
+ * Errors: as mxconv_wgrad; WORKSPACE when the layer needs more than
+ * MXC_NOALLOC_WS_MAX bytes (mxconv_wgrad_workspace_bytes), checked before
+ * any launch. */
+#define MXC_NOALLOC_WS_MAX (16u << 20)
+int mxconv_wgrad_noalloc(const mxc_conv* cv, int fmt,
+                         const void* gy_codes, const uint8_t* gy_scales,
+                         const void* x_codes, const uint8_t* x_scales,
+                         float* gw, void* stream);
+
 /* ------------------------------------------------------------------ network steps */
 /* Between the convolutions of a whole network's training step (the YOLO
  * backbone + neck and the latent-replay stacks of Sec. VI-VII), two more

@@ -1,6 +1,8 @@
 // mxconv_abi.cpp -- the C ABI of include/mxconv.h: host-side validation,
 // size helpers and dispatch to the gfx950 kernels.  Every argument check runs
 // on the host before anything is enqueued.
+#include <mutex>
+
 #include "mx_internal.h"
 
 namespace mxc {
@@ -394,6 +396,48 @@ int mxconv_dgrad_quant(const mxc_conv* p, int fmt, const void* wc, const uint8_t
     FusedEpi q{gxc, gxs, out_fmt, fn, z, false};
     rc = launch_conv_lean(cv, true, wc, ws, gc, gs, gx_act, MXC_CBF, (hipStream_t)stream, &q);
     return rc == 1 ? MXC_ERR_SHAPE : rc;
+}
+
+// The weight gradient's split-K partial sums for callers that cannot
+// allocate: one library-owned array per GPU.  Its name is a host-side
+// stand-in; the device address on each GPU is looked up once, with that
+// device current, and only that address is handed to kernels.
+namespace {
+__device__ __attribute__((aligned(256))) uint8_t scratch[MXC_NOALLOC_WS_MAX];
+constexpr int SCRATCH_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[SCRATCH_DEVICES];
+
+int scratch_for_current_device(void** out) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= SCRATCH_DEVICES) return MXC_ERR_HIP;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return MXC_ERR_HIP;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return MXC_OK;
+}
+}  // namespace
+
+int mxconv_wgrad_noalloc(const mxc_conv* p, int fmt, const void* gc, const uint8_t* gs, const void* xc,
+                         const uint8_t* xs, float* gw, void* stream) {
+    if (!p || !gc || !gs || !xc || !xs || !gw) return MXC_ERR_NULL;
+    Conv cv;
+    int rc = conv_init(&cv, p, fmt, CONV_WGRAD);
+    if (rc) return rc;
+    const size_t need = wgrad_workspace(cv);
+    if (need > MXC_NOALLOC_WS_MAX) return MXC_ERR_WORKSPACE;
+    if (!aligned16(gc) || !aligned16(gs) || !aligned16(xc) || !aligned16(xs) || !aligned16(gw))
+        return MXC_ERR_ALIGN;
+    void* ws = nullptr;
+    if (need) {
+        rc = scratch_for_current_device(&ws);
+        if (rc) return rc;
+    }
+    return launch_wgrad(cv, gc, gs, xc, xs, gw, ws, (hipStream_t)stream, nullptr, nullptr, false);
 }
 
 int mxconv_concat_cbf(int fmt, int n, int h, int w, int nparts, const mxc_part* parts, void* codes,

@@ -105,6 +105,7 @@ def lib():
         "mxconv_naive_fwd": (i32, [CP, i32, P, P, P, P, P, P]),
         "mxconv_naive_dgrad": (i32, [CP, i32, P, P, P, P, P, P, P]),
         "mxconv_naive_wgrad": (i32, [CP, i32, P, P, P, P, P, P]),
+        "mxconv_wgrad_noalloc": (i32, [CP, i32, P, P, P, P, P, P]),
         "mxconv_concat_cbf": (i32, [i32, i32, i32, i32, i32, ctypes.POINTER(MxcPart), P, P, P]),
         "mxconv_quantize_sum": (i32, [i32, i32, i32, i32, i32, i32, ctypes.POINTER(MxcTerm), i32, P, P, P, P, P]),
         "mxconv_strerror": (ctypes.c_char_p, [i32]),
