@@ -89,7 +89,7 @@ def layer_numbers(cv, fmt, mx):
     }
 
 
-PMC_SUMMARY = os.path.join(ROOT, "profiles", "op_traffic_pmc.md")
+PMC_SUMMARY = os.path.join(ROOT, "profiles", "layer_sweep_b32_traffic_pmc.md")
 PMC_YOLO = os.path.join(ROOT, "profiles", "yolo_b64_mxfp4_traffic_pmc.md")
 COPY_BYTES = 256 << 20                             # calibration copy of the counter pass
 
@@ -218,14 +218,15 @@ def cpu_baseline(min_s=10.0, max_steps=8):
     return out
 
 
-def naive_leg(jobs, op_ms, mx, synth, dev, stream, reps=3):
-    """Run the naive comparator once per (layer, format) on the same inputs
-    (outside the timed region) and report its time, algorithmic bytes and
-    quantized elements beside the method's.  The method's bytes are its
-    quantize x3 + fwd + dgrad + wgrad (the GEMMs take the im2col implicitly)."""
+def naive_calls(jobs, mx, synth, dev):
+    """The naive comparator's step for every (layer, format) job as separate
+    calls (label "<layer>/<format>/naive_<op>", callable, 0 flops, the op's
+    algorithmic bytes): fp32 im2col, the six 1-D quantizations (X' along K
+    and along P, W along K and along Cout, G_Y along Cout and along P), the
+    three GEMMs (dgrad with its col2im).  Line matrices persist in the
+    returned dict so every call can be repeated on its own."""
     import torch
-    res = {}
-    shared = {}
+    calls, shared = {}, {}
     for j in jobs:
         cv, fmt = j["cv"], j["fmt"]
         ho, wo = synth.out_hw(cv)
@@ -234,7 +235,7 @@ def naive_leg(jobs, op_ms, mx, synth, dev, stream, reps=3):
         if key not in shared:
             x = synth.cbf_to_nchw(j["x"].cpu(), cv["n"], cv["cin"], cv["h"], cv["w"], 32)
             gy = synth.cbf_to_nchw(j["gy"].cpu(), cv["n"], co, ho, wo, 32)
-            shared = {key: dict(
+            shared[key] = dict(
                 x=x.permute(0, 2, 3, 1).contiguous().to(dev),
                 gy=gy.permute(0, 2, 3, 1).reshape(P, co).contiguous().to(dev),
                 w=j["w"].permute(0, 2, 3, 1).reshape(co, K).contiguous(),
@@ -242,42 +243,72 @@ def naive_leg(jobs, op_ms, mx, synth, dev, stream, reps=3):
                 gcol=torch.empty((P, K), dtype=torch.float32, device=dev),
                 y=torch.empty((P, co), dtype=torch.float32, device=dev),
                 gx=torch.empty((cv["n"], cv["h"], cv["w"], cv["cin"]), dtype=torch.float32, device=dev),
-                gw=torch.empty((co, K), dtype=torch.float32, device=dev))}
+                gw=torch.empty((co, K), dtype=torch.float32, device=dev))
         b = shared[key]
+        q = {}
+        nby, _ = naive_numbers(cv, fmt, mx)
 
-        def naive_step():
-            mx.naive_im2col_f32(cv, b["x"], out=b["col"])
-            qc0 = mx.naive_quantize_1d(b["col"], 0, fmt)
-            qw0 = mx.naive_quantize_1d(b["w"], 0, fmt)
-            mx.naive_fwd(cv, qc0, qw0, out=b["y"])
-            qg0 = mx.naive_quantize_1d(b["gy"], 0, fmt)
-            qw1 = mx.naive_quantize_1d(b["w"], 1, fmt)
-            mx.naive_dgrad(cv, qg0, qw1, gcol=b["gcol"], out=b["gx"])
-            qg1 = mx.naive_quantize_1d(b["gy"], 1, fmt)
-            qc1 = mx.naive_quantize_1d(b["col"], 1, fmt)
-            mx.naive_wgrad(cv, qg1, qc1, out=b["gw"])
+        def qd(name, src, d, q=q, fmt=fmt):
+            q[name] = mx.naive_quantize_1d(src, d, fmt, out=q.get(name))
 
-        naive_step()
+        ops = [("im2col_f32", lambda b=b, cv=cv: mx.naive_im2col_f32(cv, b["x"], out=b["col"])),
+               ("quant_col_k", lambda b=b, qd=qd: qd("c0", b["col"], 0)),
+               ("quant_w_k", lambda b=b, qd=qd: qd("w0", b["w"], 0)),
+               ("fwd", lambda b=b, cv=cv, q=q: mx.naive_fwd(cv, q["c0"], q["w0"], out=b["y"])),
+               ("quant_gy_co", lambda b=b, qd=qd: qd("g0", b["gy"], 0)),
+               ("quant_w_co", lambda b=b, qd=qd: qd("w1", b["w"], 1)),
+               ("dgrad", lambda b=b, cv=cv, q=q: mx.naive_dgrad(cv, q["g0"], q["w1"], gcol=b["gcol"], out=b["gx"])),
+               ("quant_gy_p", lambda b=b, qd=qd: qd("g1", b["gy"], 1)),
+               ("quant_col_p", lambda b=b, qd=qd: qd("c1", b["col"], 1)),
+               ("wgrad", lambda b=b, cv=cv, q=q: mx.naive_wgrad(cv, q["g1"], q["c1"], out=b["gw"]))]
+        calls[j["name"]] = [(f"{j['name']}/naive_{op}", fn, 0.0, nby[op]) for op, fn in ops]
+    return calls
+
+
+def naive_leg(jobs, op_ms, mx, synth, dev, stream, reps=3):
+    """Run the naive comparator once per (layer, format) on the same inputs
+    (outside the timed region) and report its time, algorithmic bytes and
+    quantized elements beside the method's; with a committed counter summary
+    of the same sources, the measured HBM bytes of both too.  The method's
+    bytes are its quantize x3 + fwd + dgrad + wgrad (the GEMMs take the
+    im2col implicitly)."""
+    import torch
+    res = {}
+    ncalls = naive_calls(jobs, mx, synth, dev)
+    ours_ops = ("quant_xw", "quant_gy", "fwd", "dgrad", "wgrad")
+    for j in jobs:
+        cv, fmt = j["cv"], j["fmt"]
+        ho, wo = synth.out_hw(cv)
+        P, K, co = cv["n"] * ho * wo, cv["kh"] * cv["kw"] * cv["cin"], cv["cout"]
+        calls = ncalls[j["name"]]
+        for c in calls:
+            c[1]()
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda._sleep(SPIN_CYCLES)
         e0.record(stream)
         for _ in range(reps):
-            naive_step()
+            for c in calls:
+                c[1]()
         e1.record(stream)
         torch.cuda.synchronize()
         ms_naive = e0.elapsed_time(e1) / reps
         nby, nq = naive_numbers(cv, fmt, mx)
-        ours_ops = ("quant_xw", "quant_gy", "fwd", "dgrad", "wgrad")
         oby = sum(j["nums"][op][1] for op in ours_ops)
         ms_ours = sum(op_ms[(j["name"], op)] for op in ours_ops)
         nx = cv["n"] * cv["cin"] * cv["h"] * cv["w"]
         oq = nx + co * K + P * co
-        res[j["name"]] = {"bytes_naive": round(sum(nby.values())), "bytes_ours": round(oby),
-                          "bytes_ratio": round(sum(nby.values()) / oby, 2),
-                          "ms_naive": round(ms_naive, 4), "ms_ours": round(ms_ours, 4),
-                          "speedup": round(ms_naive / ms_ours, 2),
-                          "quantized_naive": nq, "quantized_ours": oq}
+        r = {"bytes_naive": round(sum(nby.values())), "bytes_ours": round(oby),
+             "bytes_ratio": round(sum(nby.values()) / oby, 2),
+             "ms_naive": round(ms_naive, 4), "ms_ours": round(ms_ours, 4),
+             "speedup": round(ms_naive / ms_ours, 2),
+             "quantized_naive": nq, "quantized_ours": oq}
+        mo = [counter_traffic(f"sweep/{j['name']}/{op}") for op in ours_ops]
+        mn = [counter_traffic(f"sweep/{c[0]}") for c in calls]
+        if all(v is not None for v in mo + mn):
+            r.update({"bytes_ours_measured": sum(mo), "bytes_naive_measured": sum(mn),
+                      "bytes_ratio_measured": round(sum(mn) / sum(mo), 2)})
+        res[j["name"]] = r
     return res
 
 
@@ -386,18 +417,16 @@ def sweep_leg(args):
     torch.cuda.synchronize()
 
     if args.pmc_pass:
-        # one eager launch per op, separated, then the calibration copy; the
-        # counter summary maps dispatches to ops in this order
-        for j, op in seq:
-            run(j, op)
-            torch.cuda.synchronize()
-        src = torch.empty(COPY_BYTES, dtype=torch.uint8, device=dev)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        return {"pmc_pass": [f"{j['name']}/{op}" for j, op in seq], "copy_bytes": COPY_BYTES,
-                "source_digest": source_digest()}
+        # every op of the step, the ops timed beside it and the naive
+        # comparator's ops, one call each (see pmc_pass)
+        calls = [(f"{j['name']}/{op}", (lambda j=j, op=op: run(j, op)), j["nums"][op][0], j["nums"][op][1])
+                 for j, op in seq + [(j, op) for j in jobs for op in REF_OPS]]
+        nc = naive_calls(jobs, mx, synth, dev)
+        for j in jobs:
+            calls += nc[j["name"]]
+        for c in calls:
+            c[1]()
+        return pmc_pass(calls, "sweep")
 
     # Per-op GPU time: each op alone, behind a GPU spin so that the event pair
     # brackets the kernel(s) and not the host's launch latency.
@@ -686,7 +715,7 @@ def sweep_leg(args):
     rl = roof(jmap[dom[0]], dom[1], dom_ms)
     rl.update({"kernel": f"{dom[1]} {dom[0]}", "ms": round(dom_ms, 4),
                "ms_alone": round(op_ms[dom], 4),
-               "traffic": counter_traffic(f"{dom[0]}/{dom[1]}")})
+               "traffic": counter_traffic(f"sweep/{dom[0]}/{dom[1]}")})
     ops = {}
     for (nm, op), ms in steady.items():
         fl, by = jmap[nm]["nums"][op]
@@ -942,7 +971,8 @@ def summarize_trace(rdir, log):
     rows = _csv_rows(rdir, "kernel_trace.csv")
     ks = sorted((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), _short(r["Kernel_Name"]),
                  int(r["Grid_Size_X"]) // max(1, int(r["Workgroup_Size_X"])), r) for r in rows)
-    ks = [k for k in ks if "at::" not in k[2] and "spin" not in k[2]]
+    # the library's kernels only (not the runtime's copies and fills, nor torch's)
+    ks = [k for k in ks if not k[4]["Kernel_Name"].startswith(("at::", "void at::", "__amd_rocclr"))]
     n = len(calls)
     # the step's kernel signature: the first n kernels of the run (its first warm-up step)
     sig = [(k[2], k[3]) for k in ks[:n]]
@@ -1010,7 +1040,7 @@ def summarize_pmc(fdir, wdir, flog, wlog):
         segs, cur = [], None
         for r in rows:
             nm = _short(r["Kernel_Name"])
-            if "spin" in nm or "sleep" in nm:
+            if "spin_kernel" in r["Kernel_Name"]:
                 cur = []
                 segs.append(cur)
             elif cur is not None:
@@ -1030,8 +1060,9 @@ def summarize_pmc(fdir, wdir, flog, wlog):
     L.append("Two counter passes over the same command, one counter each (repository root on an MI355X machine; "
              "summary by bench.py --summarize-pmc):\n")
     for c in ("FETCH_SIZE", "WRITE_SIZE"):
-        L.append(f"    cd /tmp && export TMPDIR=/tmp && timeout -s KILL 120 rocprofv3 --pmc {c} --output-format csv "
-                 f"-d <repo>/gpurun_out/pmc_{c} -o p -- python3 <repo>/bench.py --pmc-pass {label} --warmup 2")
+        L.append(f"    cd /tmp && export TMPDIR=/tmp && timeout -s KILL 180 rocprofv3 --pmc {c} --output-format csv "
+                 f"-d <repo>/gpurun_out/pmc_{label}_{c} -o p -- python3 <repo>/bench.py --pmc-pass {label} --warmup 2 "
+                 f"> <repo>/gpurun_out/pmc_{label}_{c}.log")
     L.append("\nThe pass runs every call of the step once (eager, in step order, each after a spin kernel that "
              "delimits it), then copies 256 MiB device to device three times; the counters of that copy "
              f"calibrate both: FETCH_SIZE {fcopy:.1f} KiB, WRITE_SIZE {wcopy:.1f} KiB for {kib:.0f} KiB moved.\n")
@@ -1111,6 +1142,7 @@ def main():
         return
     yolo = step_leg(calls, st.flops(), F4, args)
     yolo["bytes_vs_naive"] = net_bytes_vs_naive(net, N4, F4)
+    print(f"bench: yolo step {yolo['ms_per_step']} ms", file=sys.stderr, flush=True)
     del st, calls
     torch.cuda.empty_cache()
 
@@ -1118,6 +1150,7 @@ def main():
     if not args.no_qlr:
         q = wl.QlrStep(dev, fmt=mx.E2M1)
         qlr = step_leg(q.calls(), q.flops(), mx.E2M1, args)
+        print(f"bench: latent replay step {qlr['ms_per_step']} ms", file=sys.stderr, flush=True)
         qlr["workload"] = ("quantized latent replay, MXFP4: buffer of 8192 latents 128x16x16 kept as MX codes; batch "
                            "128 = 3 replayed 32-sample groups (copied codes) + 32 fresh 3x128x128 inputs through the "
                            "frozen front stack (3x3 s2 convs 3->32->64->128, SiLU); trainable back stack of four 3x3 "
@@ -1126,6 +1159,7 @@ def main():
         torch.cuda.empty_cache()
 
     sweep = None if args.no_sweep else sweep_leg(args)
+    print("bench: layer sweep done", file=sys.stderr, flush=True)
 
     rl = dict(yolo["roofline"])
     rl["traffic"] = counter_traffic(f"yolo/{rl['kernel']}", PMC_YOLO)
