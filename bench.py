@@ -47,9 +47,9 @@ HBM_GBS = 8000.0                                   # MI355X HBM3E
 SPIN_CYCLES = 100000                               # GPU spin ahead of a timed eager launch
 MFMA_TFLOPS = {0: 5000.0, 1: 10100.0}              # dense MXFP8 / MXFP4
 FMT_NAME = {0: "mxfp8", 1: "mxfp4"}
-# FP6 methods of Sec. V as (W, X, G_Y) element formats: MicroQonv+ keeps
-# activations in E3M2 with FP4 weights and gradients; the "-6" methods use
-# E2M3 throughout
+# FP6 methods as (W, X, G_Y) element formats: MicroQonv+ (Sec. IV-D) keeps
+# activations in E3M2 with FP4 weights and gradients; the "-6" methods
+# (Sec. VI-B) use E2M3 throughout
 FP6_METHODS = {"microqonv_plus": (1, 3, 1), "microqonv_6": (2, 2, 2)}
 FP6_SLACK = 16                                     # read slack at the end of an FP6 code buffer
 

@@ -20,8 +20,9 @@
  *             max 28; no inf or NaN), packed as one little-endian bit string:
  *             the element at position p occupies bits 6p .. 6p+5 (bit 0 =
  *             least significant bit of byte 0), so 32 samples take 24 bytes.
- *             Sec. V's MicroQonv+ keeps activations in E3M2 with FP4
- *             weights and gradients; its "-6" methods use E2M3 throughout.
+ *             MicroQonv+ (Sec. IV-D, Tables II and VI) keeps activations
+ *             in E3M2 with FP4 weights and gradients; the "-6" methods
+ *             (Sec. VI-B, Tables VII and VIII) use E2M3 throughout.
  *             FP6 code buffers end with 16 bytes of slack that the library
  *             may read but never writes (included in mxconv_codes_bytes).
  *   Scales: one E8M0 byte per block, value 2^(code-127); 0xFF marks a block

@@ -11,7 +11,9 @@ follows).  ``build()`` compiles it with gcc; ``load()`` builds on first use.
 Parity: every function here is pinned by the ``-m "not gpu"`` tests in
 ``tests/test_oracle_pins.py`` (hand-worked blocks, brute-force element
 rounding, torch's float8 cast, torch's fp64 convolutions, the brute-force
-direct convolutions, invariants).  Nothing here is "parity unpinned".
+direct convolutions, invariants) and ``tests/test_oracle_net.py`` (the
+network-step functions against torch.cat, F.interpolate and autograd).
+Nothing here is "parity unpinned".
 """
 import ctypes
 import os
@@ -418,7 +420,7 @@ def act_fn(y, fn):
     """The activation between two convolutions, in fp64: identity, ReLU
     (y if y > 0 else 0; the ResNets of Sec. VI) or SiLU y / (1 + exp(-y))
     (the YOLO networks of Sec. VI).  The fused forward epilogue quantizes
-    act_fn(Y) as the next layer's X, once (Sec. IV-B, Sec. V)."""
+    act_fn(Y) as the next layer's X, once (Sec. IV-B, Sec. IV-C)."""
     y = np.asarray(y, dtype=np.float64)
     if fn == FN_NONE:
         return y.copy()

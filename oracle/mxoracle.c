@@ -13,9 +13,9 @@
  *   o_encode / o_decode   one element to/from FP8 E4M3, FP4 E2M1, FP6 E2M3
  *                         or FP6 E3M2 (OCP MX element formats; the paper's
  *                         number formats are introduced in Sec. II-D and
- *                         Sec. III-A, its FP6 variants in Sec. V: E3M2
- *                         activations for MicroQonv+, E2M3 for the "-6"
- *                         methods).
+ *                         Sec. III-A; its FP6 variants: E3M2 activations
+ *                         for MicroQonv+ in Sec. IV-D, E2M3 for the "-6"
+ *                         methods in Sec. VI-B).
  *   o_quantize            microscaling quantizer, Sec. III-A Eqs. (4)-(6) in
  *                         its OCP-MX form: one E8M0 power-of-two scale per
  *                         square block (Sec. IV-B), elements rounded to

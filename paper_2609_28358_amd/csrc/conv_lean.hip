@@ -126,7 +126,7 @@ template <int F> struct LdsBlock {
 // each 32-row block it holds (4 KB of scale entries instead of 1 KB), the
 // fragments are decoded to fp16 and multiplied on fp16 MFMAs, and the result
 // is multiplied by the two per-tensor scales.
-template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW, bool NV = false>
+template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW, bool NV = false, int NRB = 2>
 __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phase& f) {
     static_assert(!NV || (FW == MXC_E2M1 && FX == MXC_E2M1), "NVFP4 operands only");
     // X8: MXFP8 operands, decoded once per fragment to bf16 (exact products,
@@ -138,7 +138,8 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
     constexpr int TBW = BW::TBG, TBX = BX::TBG;     // stored block bytes (weights, activations)
     constexpr int RBW_G = 32 * fmt_bits(FW) / 8;    // stored bytes of one 32-code row of a weight block
     constexpr int RB = 32 * fmt_bits(FX) / 8;       // stored bytes of one channel row of an activation block
-    constexpr int RBW = 2 * WGM;                    // 32-row blocks per tile
+    static_assert(NRB == 1 || NRB == 2, "one or two 32-row blocks per wave");
+    constexpr int RBW = NRB * WGM;                   // 32-row blocks per tile
     constexpr int PX = PW * 4 / WGM;                // output pixels per tile
     constexpr int CS = DG ? 1 : S;                  // halo columns per output pixel step
     constexpr int DS = DG ? S : 1;                  // tap step of a phase (stride-2 input gradient)
@@ -280,9 +281,9 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                      : fmt_bits(FX) == 6 ? 32 * i16 + 16 * cg : i16 * RB + 8 * cg;
     const int hbase = PW * wn * CS;                   // first halo pixel of the wave
 
-    v16f acc[2][PW];
+    v16f acc[NRB][PW];
 #pragma unroll
-    for (int i = 0; i < 2; i++)
+    for (int i = 0; i < NRB; i++)
 #pragma unroll
         for (int j = 0; j < PW; j++)
 #pragma unroll
@@ -351,11 +352,11 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
         }
 #pragma unroll
         for (int t = 0; t < KW; t++) {
-            v8i af[2];
-            int sa[2];
+            v8i af[NRB];
+            int sa[NRB];
 #pragma unroll
-            for (int rb = 0; rb < 2; rb++) {
-                const int rbi = 2 * wm + rb;
+            for (int rb = 0; rb < NRB; rb++) {
+                const int rbi = NRB * wm + rb;
                 const uint8_t* a0 = A + ((t * 2 + 0) * RBW + rbi) * BW::TBL + a_lane;
                 const uint8_t* a1 = a0 + RBW * BW::TBL;
                 if (DG) {
@@ -406,18 +407,18 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                 }
                 sa[rb] = SC[4 * ((t * 2 + h) * RBW + rbi)];
             }
-            uint32_t afd[DEC ? 2 : 1][16];
+            uint32_t afd[DEC ? NRB : 1][16];
             if constexpr (X8) {
 #pragma unroll
-                for (int rb = 0; rb < 2; rb++) {
-                    const int rbi = 2 * wm + rb;
+                for (int rb = 0; rb < NRB; rb++) {
+                    const int rbi = NRB * wm + rb;
                     e4m3_decode32(af[rb], SC[4 * ((t * 2 + 0) * RBW + rbi)], SC[4 * ((t * 2 + 1) * RBW + rbi)], afd[rb]);
                 }
             }
             if constexpr (NV) {
 #pragma unroll
-                for (int rb = 0; rb < 2; rb++) {
-                    const int rbi = 2 * wm + rb;
+                for (int rb = 0; rb < NRB; rb++) {
+                    const int rbi = NRB * wm + rb;
                     const uint4 u = *(const uint4*)(SC + 16 * ((t * 2 + h) * RBW + rbi));
                     uint32_t s4;
                     if (DG) {   // rows = input channels: the lane's channel group row, K groups o
@@ -435,7 +436,7 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
             for (int cn = 0; cn < PW; cn++) {
                 const int d = DG ? cn + (KW - 1 - t) : cn * CS + t;
 #pragma unroll
-                for (int rb = 0; rb < 2; rb++) {  // transposed product: rows = samples, columns = channels
+                for (int rb = 0; rb < NRB; rb++) {  // transposed product: rows = samples, columns = channels
                     if constexpr (NV) acc[rb][cn] = mfma_nv(bfd[d], afd[rb], acc[rb][cn]);
                     else if constexpr (X8) acc[rb][cn] = mfma_x8(bfd[d], afd[rb], acc[rb][cn]);
                     else acc[rb][cn] = mfma_mx<FX, FW>(bf[d], af[rb], acc[rb][cn], sb[d], sa[rb]);
@@ -454,13 +455,13 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
     if constexpr (NV) {   // Eq. (6)'s fake-quantized operands carry T_W T_X
         const float tt = *p.tw * *p.tx;
 #pragma unroll
-        for (int rb = 0; rb < 2; rb++)
+        for (int rb = 0; rb < NRB; rb++)
 #pragma unroll
             for (int cn = 0; cn < PW; cn++)
 #pragma unroll
                 for (int e = 0; e < 16; e++) acc[rb][cn][e] *= tt;
     }
-    const int m = mt * 64 * WGM + 64 * wm + (lane & 31);
+    const int m = mt * 32 * RBW + 32 * NRB * wm + (lane & 31);
     if (p.layout == MXC_CBF && !p.qcodes) __syncthreads();   // every wave is done with the stage buffers
     uint8_t* const ep = smem + wave * 4096;
     const int er = lane >> 3, ec = lane & 7;            // read-back: row er + 8 i, chunk ec
@@ -474,26 +475,38 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
         __syncthreads();                                 // every wave is done with the stage buffers
         uint8_t* const ep = smem + wave * 1024;
         const int r = lane & 31;
+        // the fp32 output of one block (32 channels x 32 samples, 4 KB
+        // contiguous in CBF): through 4 KB of LDS per wave (16-byte chunks
+        // XOR-swizzled by row) and out as four whole 1 KB non-temporal runs
+        uint8_t* const ep4 = smem + 4096 + wave * 4096;
+        auto store_block = [&](const float* val, size_t pix, int cb) {
+#pragma unroll
+            for (int e4 = 0; e4 < 4; e4++)
+                *(float4*)(ep4 + r * 128 + (((2 * e4 + h) ^ (r & 7)) << 4)) =
+                    make_float4(val[4 * e4], val[4 * e4 + 1], val[4 * e4 + 2], val[4 * e4 + 3]);
+            float* o = p.out + (pix * p.M + (size_t)cb * 32) * 32;
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                const int row = er + 8 * i;
+                const float4 w = *(const float4*)(ep4 + row * 128 + ((ec ^ (row & 7)) << 4));
+                if (cb * 32 + row < p.M) store_nt(o + row * 32 + 4 * ec, w);
+            }
+        };
 #pragma unroll
         for (int cn = 0; cn < PW; cn++) {
             const int xi = x0 + PW * wn + cn;
             if (xi >= f.gw) continue;
             const size_t pix = ((size_t)g * p.hout + y) * p.wout + (f.rx + DS * xi);
 #pragma unroll
-            for (int rb = 0; rb < 2; rb++) {
-                const int cb = mt * 2 * WGM + 2 * wm + rb;
+            for (int rb = 0; rb < NRB; rb++) {
+                const int cb = mt * RBW + NRB * wm + rb;
                 if (cb >= p.q_ncb) continue;
                 const int c = cb * 32 + r;
                 const bool real = c < p.M;
                 float v[16];
 #pragma unroll
                 for (int e = 0; e < 16; e++) v[e] = acc[rb][cn][e];
-                if (p.out && real && p.pre_out) {   // the pre-activation, for the backward pass
-                    float* o = p.out + (pix * p.M + c) * 32 + 4 * h;
-#pragma unroll
-                    for (int e4 = 0; e4 < 4; e4++)
-                        *(float4*)(o + 8 * e4) = make_float4(v[4 * e4], v[4 * e4 + 1], v[4 * e4 + 2], v[4 * e4 + 3]);
-                }
+                if (p.out && p.pre_out) store_block(v, pix, cb);   // the pre-activation, for the backward pass
                 if (p.fn != MXC_FN_NONE) {
                     if (DG) {
                         const float* zp = p.zpre + (pix * p.M + (real ? c : 0)) * 32 + 4 * h;
@@ -510,12 +523,7 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                         for (int e = 0; e < 16; e++) v[e] = fn_apply(p.fn, v[e]);
                     }
                 }
-                if (p.out && real && !p.pre_out) {
-                    float* o = p.out + (pix * p.M + c) * 32 + 4 * h;
-#pragma unroll
-                    for (int e4 = 0; e4 < 4; e4++)
-                        *(float4*)(o + 8 * e4) = make_float4(v[4 * e4], v[4 * e4 + 1], v[4 * e4 + 2], v[4 * e4 + 3]);
-                }
+                if (p.out && !p.pre_out) store_block(v, pix, cb);
                 uint32_t m = 0;
 #pragma unroll
                 for (int e = 0; e < 16; e++) m = max(m, __float_as_uint(v[e]) & 0x7FFFFFFFu);
@@ -577,8 +585,8 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
         if (p.layout == MXC_CBF) {
             float* px = p.out + (((size_t)g * p.hout + y) * p.wout + x) * p.M * 32;
 #pragma unroll
-            for (int rb = 0; rb < 2; rb++) {
-                const int m0 = mt * 64 * WGM + 64 * wm + 32 * rb;
+            for (int rb = 0; rb < NRB; rb++) {
+                const int m0 = mt * 32 * RBW + 32 * NRB * wm + 32 * rb;
                 if (m0 >= p.M) continue;
                 const int r = lane & 31;
 #pragma unroll
@@ -598,7 +606,7 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
             const size_t hw = (size_t)p.hout * p.wout;
             float* px = p.out + (size_t)y * p.wout + x;
 #pragma unroll
-            for (int rb = 0; rb < 2; rb++) {
+            for (int rb = 0; rb < NRB; rb++) {
                 const int mm = m + 32 * rb;
                 if (mm >= p.M) continue;
 #pragma unroll
@@ -612,7 +620,7 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
 }
 
 // Workgroup `bid` of `nblk` (a multiple of 8).
-template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW, bool NV = false>
+template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW, bool NV = false, int NRB = 2>
 __device__ __forceinline__ void lean_body(const LeanArgs& p, int bid, int nblk) {
     // XCD-aware order: consecutive tiles (same output row) on one XCD
     const int per_xcd = (nblk + 7) / 8;
@@ -621,17 +629,17 @@ __device__ __forceinline__ void lean_body(const LeanArgs& p, int bid, int nblk) 
     Phase f;
     f.ry = 0; f.rx = 0; f.kh0 = 0; f.nvh = p.kh; f.kw0 = 0;
     f.gh = p.hout; f.gw = p.wout; f.c0 = p.pw; f.r0 = p.ph;
-    lean_tile<FW, FX, DG, KW, S, WGM, PW, NV>(p, lin, f);
+    lean_tile<FW, FX, DG, KW, S, WGM, PW, NV, NRB>(p, lin, f);
 }
 
-template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW, bool NV = false>
+template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW, bool NV = false, int NRB = 2>
 __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
-    lean_body<FW, FX, DG, KW, S, WGM, PW, NV>(p, blockIdx.x, gridDim.x);
+    lean_body<FW, FX, DG, KW, S, WGM, PW, NV, NRB>(p, blockIdx.x, gridDim.x);
 }
 
 // Stride-2 input gradient for kernel width KWF (1 or 3): the four phases in
 // one launch, tiles of phase (ry, rx) at [pofs[2 ry + rx], pofs[2 ry + rx + 1]).
-template <int FW, int FX, int KWF, int WGM, int PW, bool NV = false>
+template <int FW, int FX, int KWF, int WGM, int PW, bool NV = false, int NRB = 2>
 __device__ __forceinline__ void lean_dg2_body(const LeanArgs& p, int bid, int nblk) {
     const int per_xcd = (nblk + 7) / 8;
     int lin = (bid % 8) * per_xcd + bid / 8;
@@ -648,13 +656,13 @@ __device__ __forceinline__ void lean_dg2_body(const LeanArgs& p, int bid, int nb
     if (nvw == 0) f.nvh = 0;                       // no tap reaches the phase: its pixels are zero
     f.gh = (p.hout - f.ry + 1) / 2; f.gw = (p.wout - f.rx + 1) / 2;
     f.c0 = (f.rx + p.pw - f.kw0) / 2; f.r0 = (f.ry + p.ph - f.kh0) / 2;
-    if (KWF == 3 && nvw == 2) lean_tile<FW, FX, true, 2, 2, WGM, PW, NV>(p, lin, f);
-    else                      lean_tile<FW, FX, true, 1, 2, WGM, PW, NV>(p, lin, f);
+    if (KWF == 3 && nvw == 2) lean_tile<FW, FX, true, 2, 2, WGM, PW, NV, NRB>(p, lin, f);
+    else                      lean_tile<FW, FX, true, 1, 2, WGM, PW, NV, NRB>(p, lin, f);
 }
 
-template <int FW, int FX, int KWF, int WGM, int PW, bool NV = false>
+template <int FW, int FX, int KWF, int WGM, int PW, bool NV = false, int NRB = 2>
 __global__ __launch_bounds__(LT) void conv_lean_dg2_kernel(LeanArgs p) {
-    lean_dg2_body<FW, FX, KWF, WGM, PW, NV>(p, blockIdx.x, gridDim.x);
+    lean_dg2_body<FW, FX, KWF, WGM, PW, NV, NRB>(p, blockIdx.x, gridDim.x);
 }
 
 // The input gradient of a layer (stride 1 with KW taps per row, or, with
@@ -665,14 +673,14 @@ __global__ __launch_bounds__(LT) void conv_lean_dg2_kernel(LeanArgs p) {
 // neither waits for the other, and the tail of one fills the CUs the other
 // leaves idle.  Both counts are multiples of 8, so each part keeps its own
 // kernel's XCD mapping.  Format F for every operand.
-template <int F, int KW, int PW, bool DG2, int NB>
+template <int F, int KW, int PW, bool DG2, int NB, int NRB = 2>
 __global__ __launch_bounds__(LT) void conv_lean_bwd_kernel(LeanArgs p, WLArgs q, int nl) {
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
     const int b = blockIdx.x;
     const int nw = (int)gridDim.x - nl;
     if (b >= nw) {
-        if constexpr (DG2) lean_dg2_body<F, F, KW, 1, PW>(p, b - nw, nl);
-        else               lean_body<F, F, true, KW, 1, 1, PW>(p, b - nw, nl);
+        if constexpr (DG2) lean_dg2_body<F, F, KW, 1, PW, false, NRB>(p, b - nw, nl);
+        else               lean_body<F, F, true, KW, 1, 1, PW, false, NRB>(p, b - nw, nl);
     } else {
         wgrad_tile<F, F, false, NB>(q, b, nw, (float (*)[32 * NB * 32 * NB])smem);
     }
@@ -682,7 +690,8 @@ __global__ __launch_bounds__(LT) void conv_lean_bwd_kernel(LeanArgs p, WLArgs q,
 // epilogue stages through.
 inline size_t lean_lds(const LeanArgs& a, int nbufs_used) {
     const size_t lds = (size_t)nbufs_used * a.stage_bytes;
-    return lds < 4 * 4096 ? 4 * 4096 : lds;
+    const size_t epi = a.qcodes ? 5 * 4096 : 4 * 4096;     // the fused epilogue: codes + fp32 staging
+    return lds < epi ? epi : lds;
 }
 
 // Dynamic LDS above 64 KB needs the kernel's attribute raised, once per
@@ -713,22 +722,33 @@ int lean_launch(K kernel, std::atomic<uint64_t>& devs, const LeanArgs& a, int nt
     return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
 }
 
-template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW, bool NV = false>
+template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW, bool NV = false, int NRB = 2>
 int launch_lean_t(const LeanArgs& a, int nbufs_used, hipStream_t s) {
     static std::atomic<uint64_t> devs{0};
-    return lean_launch(conv_lean_kernel<FW, FX, DG, KW, S, WGM, PW, NV>, devs, a, a.ntiles, lean_lds(a, nbufs_used), s);
+    return lean_launch(conv_lean_kernel<FW, FX, DG, KW, S, WGM, PW, NV, NRB>, devs, a, a.ntiles, lean_lds(a, nbufs_used), s);
 }
 
-template <int FW, int FX, int KWF, int PW, bool NV = false>
+template <int FW, int FX, int KWF, int PW, bool NV = false, int NRB = 2>
 int launch_lean_dg2(const LeanArgs& a, int nbufs_used, hipStream_t s) {
     static std::atomic<uint64_t> devs{0};
-    return lean_launch(conv_lean_dg2_kernel<FW, FX, KWF, 1, PW, NV>, devs, a, a.pofs[4], lean_lds(a, nbufs_used), s);
+    return lean_launch(conv_lean_dg2_kernel<FW, FX, KWF, 1, PW, NV, NRB>, devs, a, a.pofs[4], lean_lds(a, nbufs_used), s);
 }
 
-// (WGM, PW) in use: (1, 1), (1, 2), (2, 2), (4, 2); the NV kernels run (1, 1)
+// Narrow tiles: output channels (forward) or input channels (input gradient)
+// in a single 32-row block, FP4 operands: each wave owns 32 rows x 4 pixels
+// (the same products per wave as 64 rows x 2 pixels, none of them on padding
+// rows), a tile 32 rows x 16 pixels.
+constexpr int NARROW_PW = 4;
+template <int FW, int FX>
+constexpr bool narrow_ok() { return FW == MXC_E2M1 && FX == MXC_E2M1; }
+
+// (WGM, PW) in use: (1, 1), (1, 2), (2, 2), (4, 2), and narrow (1, 4); the
+// NV kernels run (1, 1)
 template <int FW, int FX, bool DG, int KW, int S, bool NV = false>
 int launch_lean_w(const LeanArgs& a, int wgm, int pw, int nb, hipStream_t s) {
     if constexpr (NV) return launch_lean_t<FW, FX, DG, KW, S, 1, 1, true>(a, nb, s);
+    if constexpr (narrow_ok<FW, FX>())
+        if (pw == NARROW_PW) return launch_lean_t<FW, FX, DG, KW, S, 1, NARROW_PW, false, 1>(a, nb, s);
     if (wgm == 4) return launch_lean_t<FW, FX, DG, KW, S, 4, 2>(a, nb, s);
     if (wgm == 2) return launch_lean_t<FW, FX, DG, KW, S, 2, 2>(a, nb, s);
     return pw == 1 ? launch_lean_t<FW, FX, DG, KW, S, 1, 1>(a, nb, s) : launch_lean_t<FW, FX, DG, KW, S, 1, 2>(a, nb, s);
@@ -739,6 +759,10 @@ int launch_lean_f(const LeanArgs& a, int kw, int sw, int wgm, int pw, int nb, hi
     if constexpr (DG) {
         if (sw == 2) {
             if constexpr (NV) return kw == 3 ? launch_lean_dg2<FW, FX, 3, 1, true>(a, nb, s) : launch_lean_dg2<FW, FX, 1, 1, true>(a, nb, s);
+            if constexpr (narrow_ok<FW, FX>())
+                if (pw == NARROW_PW)
+                    return kw == 3 ? launch_lean_dg2<FW, FX, 3, NARROW_PW, false, 1>(a, nb, s)
+                                   : launch_lean_dg2<FW, FX, 1, NARROW_PW, false, 1>(a, nb, s);
             if (kw == 3) return pw == 1 ? launch_lean_dg2<FW, FX, 3, 1>(a, nb, s) : launch_lean_dg2<FW, FX, 3, 2>(a, nb, s);
             return pw == 1 ? launch_lean_dg2<FW, FX, 1, 1>(a, nb, s) : launch_lean_dg2<FW, FX, 1, 2>(a, nb, s);
         }
@@ -806,11 +830,15 @@ int lean_plan(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const 
     const int mp = (a.M + 63) / 64;
     int wgm = (!dg && cv.sw == 2 && mp >= 2) ? 2 : 1;
     int pw = 2;
+    // a single 32-row block of FP4 rows: narrow tiles (32 rows x 16 pixels)
+    const bool narrow = a.M <= 32 && cv.fa == MXC_E2M1 && cv.fb == MXC_E2M1 && !nv;
+    int rb = 2;
     // tiles of a tile shape; for the stride-2 input gradient, per phase
     // (ry, rx), whose pixel grids are the output rows / columns of that parity
     auto count = [&](int wgm_, int pw_, bool fill) -> long long {
         const int px_ = pw_ * 4 / wgm_;
-        const long long mt = (a.M + 64 * wgm_ - 1) / (64 * wgm_);
+        const int rows = 32 * (pw_ == NARROW_PW ? 1 : 2) * wgm_;
+        const long long mt = (a.M + rows - 1) / rows;
         if (!dg2) return mt * ((a.wout + px_ - 1) / px_) * a.hout * src.ng;
         long long t = 0;
         for (int ph = 0; ph < 4; ph++) {
@@ -824,9 +852,10 @@ int lean_plan(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const 
     // pixel per wave instead: twice the workgroups, more waves streaming
     // operands and storing results at once (measured: faster below ~200
     // tiles, slower from ~400)
-    if (count(wgm, pw, false) < 192 || nv) { wgm = 1; pw = 1; }
+    if (narrow && count(1, NARROW_PW, false) >= 192) { wgm = 1; pw = NARROW_PW; rb = 1; }
+    else if (count(wgm, pw, false) < 192 || nv) { wgm = 1; pw = 1; }
     const int px = pw * 4 / wgm;
-    a.mtiles = (a.M + 64 * wgm - 1) / (64 * wgm);
+    a.mtiles = (a.M + 32 * rb * wgm - 1) / (32 * rb * wgm);
     for (int i = 0; i < 5; i++) a.pofs[i] = 0;
     const long long nt = count(wgm, pw, true);
     if (nt <= 0 || nt > 0x7FFFFFF0LL) return 1;
@@ -838,7 +867,7 @@ int lean_plan(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const 
     const int bpiw = cv.fa == MXC_E2M1 ? 2 : 1, bpix = cv.fb == MXC_E2M1 ? 2 : 1;
     const int kwt = dg2 ? (cv.kw + 1) / 2 : cv.kw;
     const int hp = dg ? px + kwt - 1 : (px - 1) * cv.sw + cv.kw;
-    const int na = kwt * 2 * 2 * wgm, nb = 2 * hp;
+    const int na = kwt * 2 * rb * wgm, nb = 2 * hp;
     const int nq = (na / bpiw + nb / bpix + 3) / 4;
     a.stage_bytes = nq * 4096 + (nv ? 4096 : SCALE_REGION);
     const int nstage = (dg2 ? (cv.kh + 1) / 2 : cv.kh) * ((a.kcb + 1) / 2);
@@ -855,17 +884,25 @@ int lean_plan(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const 
     return 0;
 }
 
-template <int F, int KW, int PW, bool DG2, int NB>
+template <int F, int KW, int PW, bool DG2, int NB, int NRB = 2>
 int bwd_launch(const LeanArgs& a, const WLArgs& q, int nl, int grid, size_t lds, hipStream_t s) {
     static std::atomic<uint64_t> devs{0};
-    if (raise_lds(conv_lean_bwd_kernel<F, KW, PW, DG2, NB>, devs, lds)) return MXC_ERR_HIP;
-    hipLaunchKernelGGL((conv_lean_bwd_kernel<F, KW, PW, DG2, NB>), dim3(grid), dim3(LT), lds, s, a, q, nl);
+    if (raise_lds(conv_lean_bwd_kernel<F, KW, PW, DG2, NB, NRB>, devs, lds)) return MXC_ERR_HIP;
+    hipLaunchKernelGGL((conv_lean_bwd_kernel<F, KW, PW, DG2, NB, NRB>), dim3(grid), dim3(LT), lds, s, a, q, nl);
     return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
 }
 
 template <int F, int NB>
 int bwd_launch_nb(const LeanArgs& a, const WLArgs& q, int nl, int grid, size_t lds, bool dg2, int kw, int pw,
                   hipStream_t s) {
+    if constexpr (F == MXC_E2M1) {
+        if (pw == NARROW_PW) {
+            if (dg2) return kw == 3 ? bwd_launch<F, 3, NARROW_PW, true, NB, 1>(a, q, nl, grid, lds, s)
+                                    : bwd_launch<F, 1, NARROW_PW, true, NB, 1>(a, q, nl, grid, lds, s);
+            return kw == 3 ? bwd_launch<F, 3, NARROW_PW, false, NB, 1>(a, q, nl, grid, lds, s)
+                           : bwd_launch<F, 1, NARROW_PW, false, NB, 1>(a, q, nl, grid, lds, s);
+        }
+    }
     if (dg2) {
         if (kw == 3) return pw == 1 ? bwd_launch<F, 3, 1, true, NB>(a, q, nl, grid, lds, s) : bwd_launch<F, 3, 2, true, NB>(a, q, nl, grid, lds, s);
         return pw == 1 ? bwd_launch<F, 1, 1, true, NB>(a, q, nl, grid, lds, s) : bwd_launch<F, 1, 2, true, NB>(a, q, nl, grid, lds, s);

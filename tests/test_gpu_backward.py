@@ -35,6 +35,8 @@ LAYERS = [
     (synth.conv_dict(32, 16, 16, 40, 36, 3, 1, 1), 1),            # one channel block each side: 32 x 32 wgrad tiles
     (synth.conv_dict(64, 16, 32, 40, 40, 3, 2, 1), 0),            # the same at stride 2
     (synth.conv_dict(32, 32, 16, 12, 12, 1, 1, 0), 1),            # 1x1, one block each side, one split
+    (synth.conv_dict(32, 16, 16, 64, 64, 3, 1, 1), 1),            # narrow input-gradient tiles (FP4)
+    (synth.conv_dict(64, 16, 32, 64, 64, 3, 2, 1), 1),            # the same in stride-2 phases
     (synth.conv_dict(16, 32, 48, 9, 8, 3, 1, 1), 0),              # batch block 16: two launches
     (synth.conv_dict(32, 64, 32, 10, 10, 3, 1, 1), 2),            # FP6: two launches
 ]

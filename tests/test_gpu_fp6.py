@@ -1,8 +1,8 @@
 """GPU parity of the FP6 formats (OCP E2M3 / E3M2) against the oracle.
 
-The two FP6 methods of Sec. V: MicroQonv+ (activations X in E3M2, weights
+The two FP6 methods: MicroQonv+ (Sec. IV-D; activations X in E3M2, weights
 and gradients in E2M1: fwd and wgrad multiply E2M1 by E3M2, dgrad is plain
-E2M1) and the "-6" methods (E2M3 for every operand).
+E2M1) and the "-6" methods (Sec. VI-B; E2M3 for every operand).
 
 Codes and scales bit-exact (the GPU buffers end with 16 bytes of FP6 read
 slack, which are not compared).  GEMM outputs within 1e-5 * S, S = the

@@ -70,6 +70,8 @@ FUSED_CONVS = [
     synth.conv_dict(32, 128, 64, 8, 8, 1, 2, 0),               # 1x1 stride 2: a phase with no taps
     synth.conv_dict(32, 96, 200, 7, 9, 3, 2, 1),               # ragged channels: padded rows in a block
     synth.conv_dict(32, 40, 72, 13, 11, 3, 1, 1),              # ragged on both sides
+    synth.conv_dict(32, 16, 16, 48, 64, 3, 1, 1),              # narrow tiles (FP4: 32 rows x 16 pixels)
+    synth.conv_dict(64, 16, 32, 64, 64, 3, 2, 1),              # narrow input gradient in phases
 ]
 
 

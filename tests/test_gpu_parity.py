@@ -202,6 +202,11 @@ GEMM_CONVS = [
     synth.conv_dict(32, 16, 16, 20, 18, 3, 1, 1),             # one channel block on each side (32 x 32 wgrad tiles)
     synth.conv_dict(64, 3, 16, 24, 22, 3, 2, 1),              # an image layer: 3 channels, stride 2, one block each
     synth.conv_dict(32, 32, 16, 9, 9, 1, 1, 0),
+    # FP4 layers with a single 32-row block of outputs run on narrow tiles (32 rows x 16 pixels)
+    synth.conv_dict(32, 16, 16, 48, 64, 3, 1, 1),             # fwd and dgrad narrow, stride 1
+    synth.conv_dict(64, 3, 16, 128, 96, 3, 2, 1),             # an image layer: fwd narrow at stride 2, dgrad in phases
+    synth.conv_dict(32, 32, 16, 40, 80, 1, 1, 0),             # 1x1 narrow
+    synth.conv_dict(32, 32, 48, 50, 45, 3, 1, 1),             # dgrad narrow, fwd not (48 outputs)
 ]
 
 
