@@ -126,7 +126,7 @@ template <int F> struct LdsBlock {
 // each 32-row block it holds (4 KB of scale entries instead of 1 KB), the
 // fragments are decoded to fp16 and multiplied on fp16 MFMAs, and the result
 // is multiplied by the two per-tensor scales.
-template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW, bool NV = false, int NRB = 2>
+template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW, bool NV = false, int NRB = 2, bool KR = false>
 __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phase& f) {
     static_assert(!NV || (FW == MXC_E2M1 && FX == MXC_E2M1), "NVFP4 operands only");
     // X8: MXFP8 operands, decoded once per fragment to bf16 (exact products,
@@ -194,11 +194,14 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
             const int blk = slice * BW::BPI + (BW::BPI == 2 ? (lane >> 5) : 0);
             const int rb = blk % RBW, kb = (blk / RBW) & 1, t = blk / (2 * RBW);
             const int rowblk = mt * RBW + rb;
+            // K half kb: 32-channel block 2 kk + kb, or with KR kernel row 2 st + kb
+            const uint32_t kbo = KR ? 0u : (uint32_t)kb;
             if (DG) {   // rows = input channels (block rowblk of Cin_p), K = output channels
-                off[q] = (uint32_t)kb * w_cob + (uint32_t)(f.kw0 + DS * t) * w_tap + (uint32_t)rowblk * TBW;
+                off[q] = kbo * w_cob + (uint32_t)(f.kw0 + DS * t) * w_tap + (uint32_t)rowblk * TBW;
             } else {    // rows = output channels (32-Cout block rowblk), K = input channels
-                off[q] = (uint32_t)rowblk * w_cob + (uint32_t)t * w_tap + (uint32_t)kb * TBW;
+                off[q] = (uint32_t)rowblk * w_cob + (uint32_t)t * w_tap + kbo * TBW;
             }
+            if (KR) off[q] += (uint32_t)(kb * DS) * p.kwf * w_tap;
             off[q] += in_w;
             flg[q] = (rowblk < p.w_rowblocks ? 1u : 0u) | (uint32_t)kb << 1;
         } else if (slice < NSW + NSX) {
@@ -207,7 +210,11 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
             const int kb = b / HP, hc = b % HP;
             const int col = cbase + hc;
             const bool ok = col >= 0 && col < p.wsrc;
-            off[q] = (uint32_t)(ok ? col : 0) * x_pix + (uint32_t)kb * TBX + in_x;
+            off[q] = (uint32_t)(ok ? col : 0) * x_pix + (KR ? 0u : (uint32_t)kb) * TBX + in_x;
+            // KR: the next kernel row reads the source row below (forward) or
+            // above (input gradient); offsets wrap modulo 2^32 and are added
+            // to the row base before the pointer
+            if (KR && kb) off[q] += DG ? 0u - x_row : x_row;
             flg[q] = (ok ? 1u : 0u) | (uint32_t)kb << 1 | 4u;
         }
     }
@@ -217,19 +224,25 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
     if (tid < NSA) {
         const int rb = tid % RBW, kb = (tid / RBW) & 1, t = tid / (2 * RBW);
         const int rowblk = mt * RBW + rb;
-        if (DG) s_off = ((uint32_t)kb * p.kh * p.kwf + f.kw0 + DS * t) * p.w_ncb + rowblk;
-        else    s_off = ((uint32_t)rowblk * p.kh * p.kwf + t) * p.w_ncb + kb;
+        const uint32_t kbo = KR ? 0u : (uint32_t)kb;
+        if (DG) s_off = (kbo * p.kh * p.kwf + f.kw0 + DS * t) * p.w_ncb + rowblk;
+        else    s_off = ((uint32_t)rowblk * p.kh * p.kwf + t) * p.w_ncb + kbo;
+        if (KR) s_off += (uint32_t)(kb * DS) * p.kwf * p.w_ncb;
         s_flg = (rowblk < p.w_rowblocks ? 1u : 0u) | (uint32_t)kb << 1 | 8u;
     } else if (tid < NSA + NSB) {
         const int q = tid - NSA, kb = q / HP, hc = q % HP;
         const int col = cbase + hc;
         const bool ok = col >= 0 && col < p.wsrc;
-        s_off = (uint32_t)(ok ? col : 0) * p.x_ncb + kb;
+        s_off = (uint32_t)(ok ? col : 0) * p.x_ncb + (KR ? 0u : (uint32_t)kb);
+        if (KR && kb) s_off += DG ? 0u - (uint32_t)p.wsrc * p.x_ncb : (uint32_t)p.wsrc * p.x_ncb;
         s_flg = (ok ? 1u : 0u) | (uint32_t)kb << 1 | 4u | 8u;
     }
 
+    // stages: (kernel row, pair of 32-channel K blocks), or with krow (a
+    // single K block) pairs of kernel rows, the K halves of a stage holding
+    // the two rows, so no stage carries a zero block
     const int nkk = (p.kcb + 1) / 2;
-    const int nstage = f.nvh * nkk;
+    const int nstage = KR ? (f.nvh + 1) / 2 : f.nvh * nkk;
     const uint8_t* const zero = g_zero_lean;
     // both scale tensors in scalar registers: a per-lane choice between the
     // two argument fields would otherwise be made by a vector load from the
@@ -240,7 +253,36 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
 
     // stage st = (kernel row kh, K pair kk): issue its copies into buffer
     // buf.  Every wave issues exactly NQ + 1 copies per stage.
+    auto issue_rows = [&](int st, int buf) {   // KR: K half kb = kernel row 2 st + kb
+        const int ki0 = 2 * st;
+        const bool has1 = ki0 + 1 < f.nvh;
+        const int kh0 = f.kh0 + DS * ki0;
+        const int sy0 = DG ? yi + f.r0 - ki0 : yi * p.sh + kh0 - p.ph;
+        const int sy1 = DG ? sy0 - 1 : sy0 + 1;
+        const bool ok0 = sy0 >= 0 && sy0 < p.hsrc;
+        const bool ok1 = has1 && sy1 >= 0 && sy1 < p.hsrc;
+        const uint8_t* abase = p.wc + (uint32_t)kh0 * p.kwf * w_tap;
+        const uint32_t row = (uint32_t)g * p.hsrc + (uint32_t)sy0;   // may wrap: only used where valid
+        const uint32_t xrow = row * x_row;
+        const uint8_t* lds = smem + buf * p.stage_bytes;
+#pragma unroll
+        for (int q = 0; q < NQ; q++) {
+            const uint32_t f = flg[q];
+            const bool isb = f & 4u, k1 = f & 2u;
+            const bool ok = (f & 1u) && (isb ? (k1 ? ok1 : ok0) : (!k1 || has1));
+            const uint8_t* src = isb ? p.sc + (xrow + off[q]) : abase + off[q];
+            dma16_async(ok ? src : zero + (isb ? in_x : in_w), lds_addr(lds + (4 * q + wave) * 1024));
+        }
+        const bool isb = s_flg & 4u, k1 = s_flg & 2u;
+        const bool ok = (s_flg & 8u) && (s_flg & 1u) && (isb ? (k1 ? ok1 : ok0) : (!k1 || has1));
+        const uint32_t o = isb ? s_off + row * p.wsrc * p.x_ncb : s_off + (uint32_t)kh0 * p.kwf * p.w_ncb;
+        if constexpr (NV)
+            dma16_async(ok ? (isb ? ssp : wsp) + 16 * o : zero, lds_addr(lds + NQ * 4096 + wave * 1024));
+        else
+            dma1_async(ok ? (isb ? ssp : wsp) + o : zero, lds_addr(lds + NQ * 4096 + wave * 256));
+    };
     auto issue = [&](int st, int buf) {
+        if constexpr (KR) { issue_rows(st, buf); return; }
         const int kk = st % nkk, ki = st / nkk;
         const int kh = f.kh0 + DS * ki;
         const int sy = DG ? yi + f.r0 - ki : yi * p.sh + kh - p.ph;
@@ -620,7 +662,7 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
 }
 
 // Workgroup `bid` of `nblk` (a multiple of 8).
-template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW, bool NV = false, int NRB = 2>
+template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW, bool NV = false, int NRB = 2, bool KR = false>
 __device__ __forceinline__ void lean_body(const LeanArgs& p, int bid, int nblk) {
     // XCD-aware order: consecutive tiles (same output row) on one XCD
     const int per_xcd = (nblk + 7) / 8;
@@ -629,17 +671,17 @@ __device__ __forceinline__ void lean_body(const LeanArgs& p, int bid, int nblk) 
     Phase f;
     f.ry = 0; f.rx = 0; f.kh0 = 0; f.nvh = p.kh; f.kw0 = 0;
     f.gh = p.hout; f.gw = p.wout; f.c0 = p.pw; f.r0 = p.ph;
-    lean_tile<FW, FX, DG, KW, S, WGM, PW, NV, NRB>(p, lin, f);
+    lean_tile<FW, FX, DG, KW, S, WGM, PW, NV, NRB, KR>(p, lin, f);
 }
 
-template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW, bool NV = false, int NRB = 2>
+template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW, bool NV = false, int NRB = 2, bool KR = false>
 __global__ __launch_bounds__(LT) void conv_lean_kernel(LeanArgs p) {
-    lean_body<FW, FX, DG, KW, S, WGM, PW, NV, NRB>(p, blockIdx.x, gridDim.x);
+    lean_body<FW, FX, DG, KW, S, WGM, PW, NV, NRB, KR>(p, blockIdx.x, gridDim.x);
 }
 
 // Stride-2 input gradient for kernel width KWF (1 or 3): the four phases in
 // one launch, tiles of phase (ry, rx) at [pofs[2 ry + rx], pofs[2 ry + rx + 1]).
-template <int FW, int FX, int KWF, int WGM, int PW, bool NV = false, int NRB = 2>
+template <int FW, int FX, int KWF, int WGM, int PW, bool NV = false, int NRB = 2, bool KR = false>
 __device__ __forceinline__ void lean_dg2_body(const LeanArgs& p, int bid, int nblk) {
     const int per_xcd = (nblk + 7) / 8;
     int lin = (bid % 8) * per_xcd + bid / 8;
@@ -656,13 +698,13 @@ __device__ __forceinline__ void lean_dg2_body(const LeanArgs& p, int bid, int nb
     if (nvw == 0) f.nvh = 0;                       // no tap reaches the phase: its pixels are zero
     f.gh = (p.hout - f.ry + 1) / 2; f.gw = (p.wout - f.rx + 1) / 2;
     f.c0 = (f.rx + p.pw - f.kw0) / 2; f.r0 = (f.ry + p.ph - f.kh0) / 2;
-    if (KWF == 3 && nvw == 2) lean_tile<FW, FX, true, 2, 2, WGM, PW, NV, NRB>(p, lin, f);
-    else                      lean_tile<FW, FX, true, 1, 2, WGM, PW, NV, NRB>(p, lin, f);
+    if (KWF == 3 && nvw == 2) lean_tile<FW, FX, true, 2, 2, WGM, PW, NV, NRB, KR>(p, lin, f);
+    else                      lean_tile<FW, FX, true, 1, 2, WGM, PW, NV, NRB, KR>(p, lin, f);
 }
 
-template <int FW, int FX, int KWF, int WGM, int PW, bool NV = false, int NRB = 2>
+template <int FW, int FX, int KWF, int WGM, int PW, bool NV = false, int NRB = 2, bool KR = false>
 __global__ __launch_bounds__(LT) void conv_lean_dg2_kernel(LeanArgs p) {
-    lean_dg2_body<FW, FX, KWF, WGM, PW, NV, NRB>(p, blockIdx.x, gridDim.x);
+    lean_dg2_body<FW, FX, KWF, WGM, PW, NV, NRB, KR>(p, blockIdx.x, gridDim.x);
 }
 
 // The input gradient of a layer (stride 1 with KW taps per row, or, with
@@ -673,14 +715,14 @@ __global__ __launch_bounds__(LT) void conv_lean_dg2_kernel(LeanArgs p) {
 // neither waits for the other, and the tail of one fills the CUs the other
 // leaves idle.  Both counts are multiples of 8, so each part keeps its own
 // kernel's XCD mapping.  Format F for every operand.
-template <int F, int KW, int PW, bool DG2, int NB, int NRB = 2>
+template <int F, int KW, int PW, bool DG2, int NB, int NRB = 2, bool KR = false>
 __global__ __launch_bounds__(LT) void conv_lean_bwd_kernel(LeanArgs p, WLArgs q, int nl) {
     extern __shared__ __attribute__((aligned(16))) uint8_t smem[];
     const int b = blockIdx.x;
     const int nw = (int)gridDim.x - nl;
     if (b >= nw) {
-        if constexpr (DG2) lean_dg2_body<F, F, KW, 1, PW, false, NRB>(p, b - nw, nl);
-        else               lean_body<F, F, true, KW, 1, 1, PW, false, NRB>(p, b - nw, nl);
+        if constexpr (DG2) lean_dg2_body<F, F, KW, 1, PW, false, NRB, KR>(p, b - nw, nl);
+        else               lean_body<F, F, true, KW, 1, 1, PW, false, NRB, KR>(p, b - nw, nl);
     } else {
         wgrad_tile<F, F, false, NB>(q, b, nw, (float (*)[32 * NB * 32 * NB])smem);
     }
@@ -722,16 +764,16 @@ int lean_launch(K kernel, std::atomic<uint64_t>& devs, const LeanArgs& a, int nt
     return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
 }
 
-template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW, bool NV = false, int NRB = 2>
+template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW, bool NV = false, int NRB = 2, bool KR = false>
 int launch_lean_t(const LeanArgs& a, int nbufs_used, hipStream_t s) {
     static std::atomic<uint64_t> devs{0};
-    return lean_launch(conv_lean_kernel<FW, FX, DG, KW, S, WGM, PW, NV, NRB>, devs, a, a.ntiles, lean_lds(a, nbufs_used), s);
+    return lean_launch(conv_lean_kernel<FW, FX, DG, KW, S, WGM, PW, NV, NRB, KR>, devs, a, a.ntiles, lean_lds(a, nbufs_used), s);
 }
 
-template <int FW, int FX, int KWF, int PW, bool NV = false, int NRB = 2>
+template <int FW, int FX, int KWF, int PW, bool NV = false, int NRB = 2, bool KR = false>
 int launch_lean_dg2(const LeanArgs& a, int nbufs_used, hipStream_t s) {
     static std::atomic<uint64_t> devs{0};
-    return lean_launch(conv_lean_dg2_kernel<FW, FX, KWF, 1, PW, NV, NRB>, devs, a, a.pofs[4], lean_lds(a, nbufs_used), s);
+    return lean_launch(conv_lean_dg2_kernel<FW, FX, KWF, 1, PW, NV, NRB, KR>, devs, a, a.pofs[4], lean_lds(a, nbufs_used), s);
 }
 
 // Narrow tiles: output channels (forward) or input channels (input gradient)
@@ -745,38 +787,43 @@ constexpr bool narrow_ok() { return FW == MXC_E2M1 && FX == MXC_E2M1; }
 // (WGM, PW) in use: (1, 1), (1, 2), (2, 2), (4, 2), and narrow (1, 4); the
 // NV kernels run (1, 1)
 template <int FW, int FX, bool DG, int KW, int S, bool NV = false>
-int launch_lean_w(const LeanArgs& a, int wgm, int pw, int nb, hipStream_t s) {
+int launch_lean_w(const LeanArgs& a, int wgm, int pw, bool kr, int nb, hipStream_t s) {
     if constexpr (NV) return launch_lean_t<FW, FX, DG, KW, S, 1, 1, true>(a, nb, s);
     if constexpr (narrow_ok<FW, FX>())
-        if (pw == NARROW_PW) return launch_lean_t<FW, FX, DG, KW, S, 1, NARROW_PW, false, 1>(a, nb, s);
+        if (pw == NARROW_PW) {
+            if constexpr (KW == 3)
+                if (kr) return launch_lean_t<FW, FX, DG, KW, S, 1, NARROW_PW, false, 1, true>(a, nb, s);
+            return launch_lean_t<FW, FX, DG, KW, S, 1, NARROW_PW, false, 1>(a, nb, s);
+        }
     if (wgm == 4) return launch_lean_t<FW, FX, DG, KW, S, 4, 2>(a, nb, s);
     if (wgm == 2) return launch_lean_t<FW, FX, DG, KW, S, 2, 2>(a, nb, s);
     return pw == 1 ? launch_lean_t<FW, FX, DG, KW, S, 1, 1>(a, nb, s) : launch_lean_t<FW, FX, DG, KW, S, 1, 2>(a, nb, s);
 }
 
 template <int FW, int FX, bool DG, bool NV = false>
-int launch_lean_f(const LeanArgs& a, int kw, int sw, int wgm, int pw, int nb, hipStream_t s) {
+int launch_lean_f(const LeanArgs& a, int kw, int sw, int wgm, int pw, bool kr, int nb, hipStream_t s) {
     if constexpr (DG) {
         if (sw == 2) {
             if constexpr (NV) return kw == 3 ? launch_lean_dg2<FW, FX, 3, 1, true>(a, nb, s) : launch_lean_dg2<FW, FX, 1, 1, true>(a, nb, s);
             if constexpr (narrow_ok<FW, FX>())
                 if (pw == NARROW_PW)
-                    return kw == 3 ? launch_lean_dg2<FW, FX, 3, NARROW_PW, false, 1>(a, nb, s)
+                    return kw == 3 ? (kr ? launch_lean_dg2<FW, FX, 3, NARROW_PW, false, 1, true>(a, nb, s)
+                                         : launch_lean_dg2<FW, FX, 3, NARROW_PW, false, 1>(a, nb, s))
                                    : launch_lean_dg2<FW, FX, 1, NARROW_PW, false, 1>(a, nb, s);
             if (kw == 3) return pw == 1 ? launch_lean_dg2<FW, FX, 3, 1>(a, nb, s) : launch_lean_dg2<FW, FX, 3, 2>(a, nb, s);
             return pw == 1 ? launch_lean_dg2<FW, FX, 1, 1>(a, nb, s) : launch_lean_dg2<FW, FX, 1, 2>(a, nb, s);
         }
-        return kw == 3 ? launch_lean_w<FW, FX, DG, 3, 1, NV>(a, wgm, pw, nb, s) : launch_lean_w<FW, FX, DG, 1, 1, NV>(a, wgm, pw, nb, s);
+        return kw == 3 ? launch_lean_w<FW, FX, DG, 3, 1, NV>(a, wgm, pw, kr, nb, s) : launch_lean_w<FW, FX, DG, 1, 1, NV>(a, wgm, pw, kr, nb, s);
     } else {
-        if (kw == 3) return sw == 2 ? launch_lean_w<FW, FX, DG, 3, 2, NV>(a, wgm, pw, nb, s)
-                                    : launch_lean_w<FW, FX, DG, 3, 1, NV>(a, wgm, pw, nb, s);
-        return sw == 2 ? launch_lean_w<FW, FX, DG, 1, 2, NV>(a, wgm, pw, nb, s) : launch_lean_w<FW, FX, DG, 1, 1, NV>(a, wgm, pw, nb, s);
+        if (kw == 3) return sw == 2 ? launch_lean_w<FW, FX, DG, 3, 2, NV>(a, wgm, pw, kr, nb, s)
+                                    : launch_lean_w<FW, FX, DG, 3, 1, NV>(a, wgm, pw, kr, nb, s);
+        return sw == 2 ? launch_lean_w<FW, FX, DG, 1, 2, NV>(a, wgm, pw, kr, nb, s) : launch_lean_w<FW, FX, DG, 1, 1, NV>(a, wgm, pw, kr, nb, s);
     }
 }
 
 template <int FW, int FX, bool NV = false>
-int launch_lean_dir(const LeanArgs& a, bool dg, int kw, int sw, int wgm, int pw, int nb, hipStream_t s) {
-    return dg ? launch_lean_f<FW, FX, true, NV>(a, kw, sw, wgm, pw, nb, s) : launch_lean_f<FW, FX, false, NV>(a, kw, sw, wgm, pw, nb, s);
+int launch_lean_dir(const LeanArgs& a, bool dg, int kw, int sw, int wgm, int pw, bool kr, int nb, hipStream_t s) {
+    return dg ? launch_lean_f<FW, FX, true, NV>(a, kw, sw, wgm, pw, kr, nb, s) : launch_lean_f<FW, FX, false, NV>(a, kw, sw, wgm, pw, kr, nb, s);
 }
 
 }  // namespace
@@ -787,6 +834,7 @@ struct LeanPlan {
     LeanArgs a;
     int wgm, pw, nstage, used;
     bool dg2;
+    bool krow;    // stages pair kernel rows (a single K block, kernel width 3)
 };
 
 // The tile shape, stage layout and ring depth of one launch; returns 0, 1
@@ -870,7 +918,11 @@ int lean_plan(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const 
     const int na = kwt * 2 * rb * wgm, nb = 2 * hp;
     const int nq = (na / bpiw + nb / bpix + 3) / 4;
     a.stage_bytes = nq * 4096 + (nv ? 4096 : SCALE_REGION);
-    const int nstage = (dg2 ? (cv.kh + 1) / 2 : cv.kh) * ((a.kcb + 1) / 2);
+    // a single K block and two or more kernel rows: stages pair kernel rows
+    // (the narrow FP4 kernels; NVFP keeps its own stage layout)
+    const int krows = dg2 ? (cv.kh + 1) / 2 : cv.kh;
+    const bool krow = a.kcb == 1 && krows >= 2 && rb == 1 && cv.kw == 3 && !nv;
+    const int nstage = krow ? (krows + 1) / 2 : krows * ((a.kcb + 1) / 2);
     if (2 * a.stage_bytes > LDS_MAX || nstage < 1) return 1;
     // ring depth: the workgroups that share a CU at this grid size split its
     // LDS; each takes as many stage buffers (2..4) as fit in its share
@@ -880,23 +932,26 @@ int lean_plan(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const 
         if ((long)per_cu * b * a.stage_bytes <= LDS_MAX) { nbuf = b; break; }
     a.nbuf = nbuf;
     const int used = nbuf < nstage ? nbuf : nstage;
-    P.wgm = wgm; P.pw = pw; P.nstage = nstage; P.used = used; P.dg2 = dg2;
+    P.wgm = wgm; P.pw = pw; P.nstage = nstage; P.used = used; P.dg2 = dg2; P.krow = krow;
     return 0;
 }
 
-template <int F, int KW, int PW, bool DG2, int NB, int NRB = 2>
+template <int F, int KW, int PW, bool DG2, int NB, int NRB = 2, bool KR = false>
 int bwd_launch(const LeanArgs& a, const WLArgs& q, int nl, int grid, size_t lds, hipStream_t s) {
     static std::atomic<uint64_t> devs{0};
-    if (raise_lds(conv_lean_bwd_kernel<F, KW, PW, DG2, NB, NRB>, devs, lds)) return MXC_ERR_HIP;
-    hipLaunchKernelGGL((conv_lean_bwd_kernel<F, KW, PW, DG2, NB, NRB>), dim3(grid), dim3(LT), lds, s, a, q, nl);
+    if (raise_lds(conv_lean_bwd_kernel<F, KW, PW, DG2, NB, NRB, KR>, devs, lds)) return MXC_ERR_HIP;
+    hipLaunchKernelGGL((conv_lean_bwd_kernel<F, KW, PW, DG2, NB, NRB, KR>), dim3(grid), dim3(LT), lds, s, a, q, nl);
     return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
 }
 
 template <int F, int NB>
-int bwd_launch_nb(const LeanArgs& a, const WLArgs& q, int nl, int grid, size_t lds, bool dg2, int kw, int pw,
+int bwd_launch_nb(const LeanArgs& a, const WLArgs& q, int nl, int grid, size_t lds, bool dg2, int kw, int pw, bool kr,
                   hipStream_t s) {
     if constexpr (F == MXC_E2M1) {
         if (pw == NARROW_PW) {
+            if (kw == 3 && kr)
+                return dg2 ? bwd_launch<F, 3, NARROW_PW, true, NB, 1, true>(a, q, nl, grid, lds, s)
+                           : bwd_launch<F, 3, NARROW_PW, false, NB, 1, true>(a, q, nl, grid, lds, s);
             if (dg2) return kw == 3 ? bwd_launch<F, 3, NARROW_PW, true, NB, 1>(a, q, nl, grid, lds, s)
                                     : bwd_launch<F, 1, NARROW_PW, true, NB, 1>(a, q, nl, grid, lds, s);
             return kw == 3 ? bwd_launch<F, 3, NARROW_PW, false, NB, 1>(a, q, nl, grid, lds, s)
@@ -912,10 +967,10 @@ int bwd_launch_nb(const LeanArgs& a, const WLArgs& q, int nl, int grid, size_t l
 }
 
 template <int F>
-int bwd_launch_f(const LeanArgs& a, const WLArgs& q, int nl, int grid, size_t lds, bool dg2, int kw, int pw,
+int bwd_launch_f(const LeanArgs& a, const WLArgs& q, int nl, int grid, size_t lds, bool dg2, int kw, int pw, bool kr,
                  bool nb1, hipStream_t s) {
-    return nb1 ? bwd_launch_nb<F, 1>(a, q, nl, grid, lds, dg2, kw, pw, s)
-               : bwd_launch_nb<F, 2>(a, q, nl, grid, lds, dg2, kw, pw, s);
+    return nb1 ? bwd_launch_nb<F, 1>(a, q, nl, grid, lds, dg2, kw, pw, kr, s)
+               : bwd_launch_nb<F, 2>(a, q, nl, grid, lds, dg2, kw, pw, kr, s);
 }
 
 }  // namespace
@@ -931,15 +986,15 @@ int launch_conv_lean(const Conv& cv, bool dg, const void* wc, const uint8_t* ws,
     const LeanArgs& a = P.a;
     const bool nv = nv_tw != nullptr;
     const int wgm = P.wgm, pw = P.pw, used = P.used;
-    if (nv) return launch_lean_dir<MXC_E2M1, MXC_E2M1, true>(a, dg, cv.kw, cv.sw, wgm, pw, used, s);
+    if (nv) return launch_lean_dir<MXC_E2M1, MXC_E2M1, true>(a, dg, cv.kw, cv.sw, wgm, pw, P.krow, used, s);
     if (cv.fa == MXC_E4M3 && cv.fb == MXC_E4M3)
-        return launch_lean_dir<MXC_E4M3, MXC_E4M3>(a, dg, cv.kw, cv.sw, wgm, pw, used, s);
+        return launch_lean_dir<MXC_E4M3, MXC_E4M3>(a, dg, cv.kw, cv.sw, wgm, pw, P.krow, used, s);
     if (cv.fa == MXC_E2M1 && cv.fb == MXC_E2M1)
-        return launch_lean_dir<MXC_E2M1, MXC_E2M1>(a, dg, cv.kw, cv.sw, wgm, pw, used, s);
+        return launch_lean_dir<MXC_E2M1, MXC_E2M1>(a, dg, cv.kw, cv.sw, wgm, pw, P.krow, used, s);
     if (cv.fa == MXC_E2M3 && cv.fb == MXC_E2M3)
-        return launch_lean_dir<MXC_E2M3, MXC_E2M3>(a, dg, cv.kw, cv.sw, wgm, pw, used, s);
+        return launch_lean_dir<MXC_E2M3, MXC_E2M3>(a, dg, cv.kw, cv.sw, wgm, pw, P.krow, used, s);
     if (cv.fa == MXC_E2M1 && cv.fb == MXC_E3M2)
-        return launch_lean_dir<MXC_E2M1, MXC_E3M2>(a, dg, cv.kw, cv.sw, wgm, pw, used, s);
+        return launch_lean_dir<MXC_E2M1, MXC_E3M2>(a, dg, cv.kw, cv.sw, wgm, pw, P.krow, used, s);
     return MXC_ERR_ARG;
 }
 
@@ -976,8 +1031,8 @@ int launch_lean_bwd(const Conv& dcv, const void* wc, const uint8_t* ws, const vo
     size_t lds = lean_lds(a, used);
     if (lds < (size_t)red) lds = (size_t)red;
     const int grid = (int)(nl + wg);
-    return f == MXC_E4M3 ? bwd_launch_f<MXC_E4M3>(a, q, (int)nl, grid, lds, P.dg2, dcv.kw, P.pw, nb1, s)
-                         : bwd_launch_f<MXC_E2M1>(a, q, (int)nl, grid, lds, P.dg2, dcv.kw, P.pw, nb1, s);
+    return f == MXC_E4M3 ? bwd_launch_f<MXC_E4M3>(a, q, (int)nl, grid, lds, P.dg2, dcv.kw, P.pw, P.krow, nb1, s)
+                         : bwd_launch_f<MXC_E2M1>(a, q, (int)nl, grid, lds, P.dg2, dcv.kw, P.pw, P.krow, nb1, s);
 }
 
 }  // namespace mxc
