@@ -68,6 +68,12 @@
  *   MXC_NHWC  (n, h, w, c);
  *   MXC_CBF   channel-batch-first fp32: [n/Bn][h][w][c][Bn] with the real c
  *             and the activation Bn above (Sec. IV-A's layout, unquantized).
+ *   MXC_CBF_BF16  the same index order with bf16 elements: an output layout
+ *             of mxconv_fwd, mxconv_dgrad and mxconv_backward for callers
+ *             that keep their full-precision tensors in bf16.  The fp32
+ *             GEMM result is rounded to the nearest bf16, ties to even (a
+ *             NaN stays a NaN).  The quantize entry points read bf16 through
+ *             their dtype argument and refuse this value (ARG).
  *
  * Convolution (mxc_conv): cross-correlation with zero padding, dilation 1,
  * groups 1; Ho = (h + 2 ph - kh) / sh + 1, Wo likewise (Sec. II-A, Eq. (1)
@@ -109,12 +115,19 @@ typedef enum { MXC_E4M3 = 0, MXC_E2M1 = 1, MXC_E2M3 = 2, MXC_E3M2 = 3 } mxc_fmt;
 /* Different formats for the two MX operands of a GEMM entry point. */
 #define MXC_PAIR(first, second) (0x10 | ((first) << 2) | (second))
 typedef enum { MXC_F32 = 0, MXC_BF16 = 1 } mxc_dtype;
-typedef enum { MXC_NCHW = 0, MXC_NHWC = 1, MXC_CBF = 2 } mxc_layout;
+typedef enum { MXC_NCHW = 0, MXC_NHWC = 1, MXC_CBF = 2, MXC_CBF_BF16 = 3 } mxc_layout;
 typedef enum { MXC_ACT = 0, MXC_WEIGHT = 1 } mxc_role;
 typedef enum { MXC_FN_NONE = 0, MXC_FN_RELU = 1, MXC_FN_SILU = 2 } mxc_fn;   /* activation function */
 /* Flag or-ed into mxconv_fwd_quant's fn: its fp32 output receives the values
  * before the activation (the pre-activation a backward pass needs for fn'). */
 #define MXC_FN_PRE_OUT 0x100
+/* Flag or-ed into the fn of mxconv_fwd_quant, mxconv_dgrad_quant and
+ * mxconv_quantize_sum: the caller's full-precision tensors between layers
+ * (pre-activations and input gradients) are bf16 CBF, and a GEMM result is
+ * rounded to bf16 (as MXC_CBF_BF16) before anything uses it -- the value a
+ * bf16 tensor would hold is the value that is activated, multiplied and
+ * quantized.  Details with each entry point. */
+#define MXC_FN_BF16 0x200
 
 /* One convolution layer: batch n, channels cin -> cout, input h x w,
  * kernel kh x kw, stride sh, sw, zero padding ph, pw. */
@@ -291,13 +304,13 @@ int mxconv_im2col_cbf(const mxc_conv* cv, int fmt,
  *   w_codes / w_scales   device, W quantized with role MXC_WEIGHT
  *                        (n = cout, c = cin, h = kh, w = kw).
  *   x_codes / x_scales   device, X quantized with role MXC_ACT.
- *   y                    device fp32, n x cout x Ho x Wo in y_layout
- *                        (MXC_NCHW or MXC_CBF).
+ *   y                    device, n x cout x Ho x Wo in y_layout
+ *                        (fp32 MXC_NCHW or MXC_CBF, or bf16 MXC_CBF_BF16).
  * Errors: NULL, ARG, SHAPE, ALIGN, HIP. */
 int mxconv_fwd(const mxc_conv* cv, int fmt,
                const void* w_codes, const uint8_t* w_scales,
                const void* x_codes, const uint8_t* x_scales,
-               float* y, int y_layout, void* stream);
+               void* y, int y_layout, void* stream);
 
 /* ------------------------------------------------------------------ a4 */
 /* Input gradient G_X = W^T * G_Y (Eq. (2)), i.e. G_X' = W_f^T G_Yf followed
@@ -308,13 +321,13 @@ int mxconv_fwd(const mxc_conv* cv, int fmt,
  * forward pass (W) and the once-quantized G_Y.
  *   gy_codes / gy_scales  device, G_Y quantized with role MXC_ACT
  *                         (n, cout, Ho, Wo).
- *   gx                    device fp32, n x cin x h x w in gx_layout
- *                         (MXC_NCHW or MXC_CBF).
+ *   gx                    device, n x cin x h x w in gx_layout
+ *                         (fp32 MXC_NCHW or MXC_CBF, or bf16 MXC_CBF_BF16).
  * Errors: NULL, ARG, SHAPE, ALIGN, HIP. */
 int mxconv_dgrad(const mxc_conv* cv, int fmt,
                  const void* w_codes, const uint8_t* w_scales,
                  const void* gy_codes, const uint8_t* gy_scales,
-                 float* gx, int gx_layout, void* stream);
+                 void* gx, int gx_layout, void* stream);
 
 /* ------------------------------------------------------------------ a5 */
 /* Weight gradient G_W[co][ci] = sum_n G_Y[n][co] * X[n][ci] (Eq. (3)), i.e.
@@ -377,7 +390,7 @@ int mxconv_backward(const mxc_conv* cv, int fmt,
                     const void* w_codes, const uint8_t* w_scales,
                     const void* gy_codes, const uint8_t* gy_scales,
                     const void* x_codes, const uint8_t* x_scales,
-                    float* gx, int gx_layout, float* gw,
+                    void* gx, int gx_layout, float* gw,
                     void* workspace, size_t ws_bytes, int deferred, void* stream);
 
 /* ------------------------------------------------------------------ a6 */
@@ -474,14 +487,23 @@ int mxconv_naive_wgrad(const mxc_conv* cv, int fmt,
  *   y_act               NULL, or device fp32 n x cout x Ho x Wo in CBF
  *                       layout: receives the values that were quantized,
  *                       or, with fn | MXC_FN_PRE_OUT, W * X before fn.
+ *                       With fn | MXC_FN_BF16, W * X is rounded to bf16
+ *                       first and fn applied to that; y_act with
+ *                       MXC_FN_PRE_OUT is then bf16 CBF and receives the
+ *                       rounded W * X (the pre-activation a bf16 network
+ *                       keeps), without it fp32 as above.
  * Input gradient: G_Z = (W^T * G_Y) . fn'(z), the gradient at the
  * pre-activation z of this layer's input X = fn(z) (fn' = 1 for
  * MXC_FN_NONE, [z > 0] for ReLU, s (1 + z (1 - s)) with s = 1 / (1 +
  * exp(-z)) for SiLU), quantized into the MX-CBF tensor of (n, cin, h, w) --
  * the G_Y operand of the layer before:
  *   z                   device fp32 n x cin x h x w in CBF layout; may be
- *                       NULL for MXC_FN_NONE.
- *   gx_codes / gx_scales, gx_act  as above for (n, cin, h, w).
+ *                       NULL for MXC_FN_NONE.  With fn | MXC_FN_BF16, z is
+ *                       bf16 CBF and W^T * G_Y is rounded to bf16 before
+ *                       the product (so the result equals mxconv_dgrad into
+ *                       MXC_CBF_BF16 followed by mxconv_quantize_sum).
+ *   gx_codes / gx_scales, gx_act  as above for (n, cin, h, w); gx_act is
+ *                       fp32 in both modes.
  * The fused kernels cover batch block 32 (n a multiple of 32), kernel width
  * 1 or 3, forward column stride 1 or 2, input-gradient stride 1x1 or 2x2;
  * other layers return MXC_ERR_SHAPE (use mxconv_fwd / mxconv_dgrad and
@@ -491,11 +513,11 @@ int mxconv_fwd_quant(const mxc_conv* cv, int fmt,
                      const void* w_codes, const uint8_t* w_scales,
                      const void* x_codes, const uint8_t* x_scales,
                      int fn, int out_fmt, void* y_codes, uint8_t* y_scales,
-                     float* y_act, void* stream);
+                     void* y_act, void* stream);
 int mxconv_dgrad_quant(const mxc_conv* cv, int fmt,
                        const void* w_codes, const uint8_t* w_scales,
                        const void* gy_codes, const uint8_t* gy_scales,
-                       int fn, const float* z, int out_fmt,
+                       int fn, const void* z, int out_fmt,
                        void* gx_codes, uint8_t* gx_scales, float* gx_act, void* stream);
 
 /* ------------------------------------------------------------------ no allocation */
@@ -557,7 +579,7 @@ int mxconv_concat_cbf(int fmt, int n, int h, int w, int nparts, const mxc_part* 
  * of (n, c, h, w) -- the G_Y operand of the layer that produced a.  Each term
  * is read from an fp32 CBF tensor [n/32][hs][ws][c_src][32] -- a consumer's
  * input gradient:
- *   term.src     device fp32;
+ *   term.src     device fp32 (see MXC_FN_BF16 below);
  *   term.c_src   channels of that tensor; term.c_off: its channel that is
  *                channel 0 of the term (c_off + c <= c_src: the slice a
  *                concatenation's gradient hands back to one part);
@@ -568,17 +590,19 @@ int mxconv_concat_cbf(int fmt, int n, int h, int w, int nparts, const mxc_part* 
  *   z            device fp32 CBF [n/32][h][w][c][32], the pre-activation;
  *   codes/scales device, written;
  *   vals         NULL, or device fp32 CBF [n/32][h][w][c][32]: receives G.
+ * With fn | MXC_FN_BF16 every term and z are bf16 CBF instead (read
+ * exactly; the sum, the product and vals stay fp32).
  * n a multiple of 32; fmt MXC_E4M3 or MXC_E2M1; 1 <= nterms <= MXC_TERMS_MAX.
  * Errors: NULL, ARG, SHAPE, ALIGN, HIP. */
 #define MXC_TERMS_MAX 4
 typedef struct {
-    const float* src;
+    const void* src;       /* fp32, or bf16 with MXC_FN_BF16 */
     int c_src;
     int c_off;
     int down;
 } mxc_term;
 int mxconv_quantize_sum(int fmt, int n, int c, int h, int w, int nterms, const mxc_term* terms,
-                        int fn, const float* z, void* codes, uint8_t* scales, float* vals, void* stream);
+                        int fn, const void* z, void* codes, uint8_t* scales, float* vals, void* stream);
 
 /* Human-readable text for a return code (static storage). */
 const char* mxconv_strerror(int code);

@@ -12,7 +12,8 @@ Parity: every function here is pinned by the ``-m "not gpu"`` tests in
 ``tests/test_oracle_pins.py`` (hand-worked blocks, brute-force element
 rounding, torch's float8 cast, torch's fp64 convolutions, the brute-force
 direct convolutions, invariants) and ``tests/test_oracle_net.py`` (the
-network-step functions against torch.cat, F.interpolate and autograd).
+network-step functions against torch.cat, F.interpolate and autograd; the
+bf16 rounding against hand-worked ties and torch's bfloat16 cast).
 Nothing here is "parity unpinned".
 """
 import ctypes
@@ -443,6 +444,29 @@ def act_grad(z, fn):
     with np.errstate(over="ignore"):
         s = 1.0 / (1.0 + np.exp(-z))
     return s * (1.0 + z * (1.0 - s))
+
+
+# ---------------------------------------------------------------- bf16 master tensors
+def round_bf16(x):
+    """fp32 -> bf16 (8 significand bits: the fp32 sign, exponent and top 7
+    fraction bits), round to nearest with ties to even, returned as fp32.
+    Written as the rule: of the two bf16 neighbours -- the fp32 pattern with
+    its low 16 bits cleared, and the next bf16 away from zero -- take the one
+    the dropped 16 bits are nearer to; on an exact half, the one whose last
+    kept bit is 0.  The step past the largest finite bf16 is infinity.  A NaN
+    stays a NaN.  Full-precision tensors between layers are held in bf16
+    when a network keeps bf16 master tensors."""
+    a = np.ascontiguousarray(np.asarray(x, dtype=np.float32))
+    u = a.view(np.uint32).astype(np.int64)
+    lo = u & 0xFFFF0000
+    dropped = u & 0xFFFF
+    odd = (lo >> 16) & 1
+    up = (dropped > 0x8000) | ((dropped == 0x8000) & (odd == 1))
+    r = np.where(up, lo + 0x10000, lo)
+    nan = np.isnan(a)
+    out = (r & 0xFFFFFFFF).astype(np.uint32).view(np.float32).copy()
+    out[nan] = np.float32("nan")
+    return out
 
 
 # ---------------------------------------------------------------- network steps

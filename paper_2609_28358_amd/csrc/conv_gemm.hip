@@ -352,11 +352,12 @@ __global__ __launch_bounds__(NT) void conv_kernel(ConvArgs p) {
             const int m = BM * mt + 32 * wm + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
             if (m >= p.M) continue;
             size_t o;
-            if (p.layout == MXC_CBF)
+            if (p.layout != MXC_NCHW)
                 o = ((((size_t)g * p.hout + oy) * p.wout + ox) * p.M + m) * bn + j;
             else
                 o = (((size_t)n * p.M + m) * p.hout + oy) * p.wout + ox;
-            p.out[o] = acc[c][e];
+            if (p.layout == MXC_CBF_BF16) ((uint16_t*)p.out)[o] = (uint16_t)bf16_bits(acc[c][e]);
+            else                          p.out[o] = acc[c][e];
         }
     }
 }
@@ -1027,7 +1028,7 @@ __global__ __launch_bounds__(NT) void conv_stream_kernel(StreamArgs p) {
         const int ox = DG ? rx + cv.sw * ox_g : ox_g;
         const int m0 = BM * mt + 32 * wm + 4 * h;
         size_t o0, mstride;
-        if (p.layout == MXC_CBF) {
+        if (p.layout != MXC_NCHW) {
             o0 = ((((size_t)g * p.hout + oy) * p.wout + ox) * p.M + m0) * BNS + j;
             mstride = BNS;
         } else {
@@ -1037,7 +1038,9 @@ __global__ __launch_bounds__(NT) void conv_stream_kernel(StreamArgs p) {
 #pragma unroll
         for (int e = 0; e < 16; e++) {
             const int dm = 8 * (e >> 2) + (e & 3);
-            if (m0 + dm < p.M) p.out[o0 + dm * mstride] = acc[c][e];
+            if (m0 + dm >= p.M) continue;
+            if (p.layout == MXC_CBF_BF16) ((uint16_t*)p.out)[o0 + dm * mstride] = (uint16_t)bf16_bits(acc[c][e]);
+            else                          p.out[o0 + dm * mstride] = acc[c][e];
         }
     }
 }

@@ -82,7 +82,8 @@ struct LeanArgs {
     uint8_t* qscales;
     int qfmt, q_ncb, fn;
     int pre_out;              // forward: `out` receives the values before the activation
-    const float* zpre;
+    int bf16;                 // the GEMM result is rounded to bf16 first; zpre and the pre_out output are bf16
+    const void* zpre;
     // NVFP4 operands (the NV kernels): per-tensor scales of W and the source;
     // the scale arrays ws / ss then hold E4M3 scales per 8x8 block, the 16 of
     // one 32-row block in 16 consecutive bytes
@@ -114,6 +115,52 @@ struct Phase {
 // instruction moves 1 KB of LDS: two FP4 blocks, or one FP8 block, or one
 // FP6 block with lane j reading the 16 bytes at 12 j (the last 4 of them
 // belong to the next half row and are never read back).
+// bf16 tiles of one output block (32 channels x 32 samples at one pixel: 2 KB
+// contiguous in the CBF layout, 64 bytes per channel row) pass through 2 KB of
+// LDS per wave, so that global memory sees whole 1 KB runs of 16 bytes per
+// lane rather than the accumulator layout's 8-byte pieces of 32 rows (twice
+// the rows touched per instruction, and four times the instructions per
+// block).  The 16-byte chunk c of row r sits at r * 64 + ((c ^ ((r / 2) % 4))
+// * 16): rows two apart land on different chunks.
+__device__ __forceinline__ int bf16_lds(int row, int chunk) { return row * 64 + ((chunk ^ ((row >> 1) & 3)) << 4); }
+
+// Lane (r, h) = (lane % 32, lane / 32) holds samples 8 e4 + 4 h .. + 3 of row r
+// in v[4 e4 .. 4 e4 + 3] (the MFMA accumulator layout).  Rows >= rows are
+// not written.
+__device__ __forceinline__ void store_bf16_tile(uint8_t* lds, const float* v, uint16_t* dst, int rows, int lane) {
+    const int r = lane & 31, h = lane >> 5;
+#pragma unroll
+    for (int e4 = 0; e4 < 4; e4++)
+        *(uint2*)(lds + bf16_lds(r, e4) + 8 * h) = bf16_pack4(v[4 * e4], v[4 * e4 + 1], v[4 * e4 + 2], v[4 * e4 + 3]);
+#pragma unroll
+    for (int i = 0; i < 2; i++) {
+        const int k = lane + 64 * i, row = k >> 2, c = k & 3;
+        const uint4 d = *(const uint4*)(lds + bf16_lds(row, c));
+        if (row < rows) store_nt(dst + row * 32 + c * 8, d);
+    }
+}
+
+// The inverse: z[4 e4 .. 4 e4 + 3] of lane (r, h) = samples 8 e4 + 4 h .. + 3
+// of row r of the bf16 tile at src, as floats; rows >= rows read as 0.
+__device__ __forceinline__ void load_bf16_tile(uint8_t* lds, const uint16_t* src, int rows, int lane, float* z) {
+#pragma unroll
+    for (int i = 0; i < 2; i++) {
+        const int k = lane + 64 * i, row = k >> 2, c = k & 3;
+        uint4 d = make_uint4(0u, 0u, 0u, 0u);
+        if (row < rows) {   // 16 bytes moved as four fp32 lanes: bits only, no arithmetic
+            const float4 f = load_nt((const float*)(src + row * 32 + c * 8));
+            d = make_uint4(__float_as_uint(f.x), __float_as_uint(f.y), __float_as_uint(f.z), __float_as_uint(f.w));
+        }
+        *(uint4*)(lds + bf16_lds(row, c)) = d;
+    }
+    const int r = lane & 31, h = lane >> 5;
+#pragma unroll
+    for (int e4 = 0; e4 < 4; e4++) {
+        const float4 f = bf16_unpack4(*(const uint2*)(lds + bf16_lds(r, e4) + 8 * h));
+        z[4 * e4] = f.x; z[4 * e4 + 1] = f.y; z[4 * e4 + 2] = f.z; z[4 * e4 + 3] = f.w;
+    }
+}
+
 template <int F> struct LdsBlock {
     static constexpr int TBG = 32 * 32 * fmt_bits(F) / 8;        // stored block bytes
     static constexpr int TBL = F == MXC_E2M1 ? 512 : 1024;       // LDS block bytes
@@ -504,7 +551,8 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                 for (int e = 0; e < 16; e++) acc[rb][cn][e] *= tt;
     }
     const int m = mt * 32 * RBW + 32 * NRB * wm + (lane & 31);
-    if (p.layout == MXC_CBF && !p.qcodes) __syncthreads();   // every wave is done with the stage buffers
+    if ((p.layout == MXC_CBF || p.layout == MXC_CBF_BF16) && !p.qcodes)
+        __syncthreads();                                 // every wave is done with the stage buffers
     uint8_t* const ep = smem + wave * 4096;
     const int er = lane >> 3, ec = lane & 7;            // read-back: row er + 8 i, chunk ec
     const int y = f.ry + DS * yi;
@@ -548,13 +596,31 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                 float v[16];
 #pragma unroll
                 for (int e = 0; e < 16; e++) v[e] = acc[rb][cn][e];
-                if (p.out && p.pre_out) store_block(v, pix, cb);   // the pre-activation, for the backward pass
+                if (p.bf16) {   // the value a bf16 tensor holds is the value used from here on
+#pragma unroll
+                    for (int e = 0; e < 16; e += 2) {
+                        const uint32_t u = bf16_pack2(v[e], v[e + 1]);
+                        v[e] = __uint_as_float(u << 16);
+                        v[e + 1] = __uint_as_float(u & 0xFFFF0000u);
+                    }
+                }
+                const int rows = min(32, p.M - cb * 32);
+                if (p.out && p.pre_out) {   // the pre-activation, for the backward pass
+                    if (p.bf16) store_bf16_tile(ep4, v, (uint16_t*)p.out + (pix * p.M + (size_t)cb * 32) * 32, rows, lane);
+                    else        store_block(v, pix, cb);
+                }
                 if (p.fn != MXC_FN_NONE) {
-                    if (DG) {
-                        const float* zp = p.zpre + (pix * p.M + (real ? c : 0)) * 32 + 4 * h;
+                    if (DG && p.bf16) {
+                        float zz[16];
+                        load_bf16_tile(ep4, (const uint16_t*)p.zpre + (pix * p.M + (size_t)cb * 32) * 32, rows, lane, zz);
+#pragma unroll
+                        for (int e = 0; e < 16; e++) v[e] *= fn_grad(p.fn, zz[e]);
+                    } else if (DG) {
+                        const size_t zo = (pix * p.M + (real ? c : 0)) * 32 + 4 * h;
 #pragma unroll
                         for (int e4 = 0; e4 < 4; e4++) {
-                            const float4 z = real ? *(const float4*)(zp + 8 * e4) : make_float4(0.f, 0.f, 0.f, 0.f);
+                            float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+                            if (real) z = *(const float4*)((const float*)p.zpre + zo + 8 * e4);
                             v[4 * e4] *= fn_grad(p.fn, z.x);
                             v[4 * e4 + 1] *= fn_grad(p.fn, z.y);
                             v[4 * e4 + 2] *= fn_grad(p.fn, z.z);
@@ -624,7 +690,18 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
         const int xi = x0 + PW * wn + cn;
         if (xi >= f.gw) continue;
         const int x = f.rx + DS * xi;
-        if (p.layout == MXC_CBF) {
+        if (p.layout == MXC_CBF_BF16) {
+            uint16_t* px = (uint16_t*)p.out + (((size_t)g * p.hout + y) * p.wout + x) * p.M * 32;
+#pragma unroll
+            for (int rb = 0; rb < NRB; rb++) {
+                const int m0 = mt * 32 * RBW + 32 * NRB * wm + 32 * rb;
+                if (m0 >= p.M) continue;
+                float v[16];
+#pragma unroll
+                for (int e = 0; e < 16; e++) v[e] = acc[rb][cn][e];
+                store_bf16_tile(ep, v, px + (size_t)m0 * 32, min(32, p.M - m0), lane);
+            }
+        } else if (p.layout == MXC_CBF) {
             float* px = p.out + (((size_t)g * p.hout + y) * p.wout + x) * p.M * 32;
 #pragma unroll
             for (int rb = 0; rb < NRB; rb++) {
@@ -859,6 +936,7 @@ int lean_plan(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const 
     a.q_ncb = (a.M + 31) / 32;
     a.fn = q ? q->fn : MXC_FN_NONE;
     a.pre_out = q && q->pre ? 1 : 0;
+    a.bf16 = q && q->bf16 ? 1 : 0;
     a.zpre = q ? q->z : nullptr;
     a.tw = nv_tw; a.tx = nv_tx;
     const Geom& src = dg ? cv.gy : cv.x;

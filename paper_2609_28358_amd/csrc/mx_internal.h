@@ -77,6 +77,7 @@ int launch_quantize_multi(int count, const QuantJob* jobs, hipStream_t s);
 constexpr int NVFP_PARTS = 1024;
 int launch_nvfp_quantize(const void* src, int dtype, int layout, int role, const Geom& g, int fmt, void* codes,
                          uint8_t* scales, float* tscale, void* ws, hipStream_t s);
+// Output pointers are typed float*; with layout MXC_CBF_BF16 they hold bf16.
 int launch_fwd(const Conv& cv, const void* wc, const uint8_t* ws, const void* xc,
                const uint8_t* xs, float* y, int layout, hipStream_t s);
 int launch_dgrad(const Conv& cv, const void* wc, const uint8_t* ws, const void* gc,
@@ -88,8 +89,9 @@ struct FusedEpi {
     void* codes;
     uint8_t* scales;
     int fmt, fn;
-    const float* z;
-    bool pre;            // forward: the fp32 output gets the values before fn
+    const void* z;       // fp32 CBF, or bf16 CBF with bf16
+    bool pre;            // forward: the output gets the values before fn
+    bool bf16;           // round the GEMM result to bf16 first; z and the pre output are bf16
 };
 // fwd / dgrad for batch block 32 and kernel width 1 or 3 (conv_lean.hip);
 // returns 1 when the layer is outside those shapes.  With q, the output is
@@ -138,7 +140,7 @@ int launch_wgrad_reduce_multi(int count, const WReduceJob* jobs, hipStream_t s);
 // and the quantized, fn'-masked sum of gradient terms
 int launch_concat(const Geom& dst, const mxc_part* parts, int nparts, void* codes, uint8_t* scales,
                   hipStream_t s);
-int launch_quantize_sum(const Geom& dst, int fmt, const mxc_term* terms, int nterms, int fn, const float* z,
+int launch_quantize_sum(const Geom& dst, int fmt, const mxc_term* terms, int nterms, int fn, bool bf16, const void* z,
                         void* codes, uint8_t* scales, float* vals, hipStream_t s);
 
 // naive comparator (naive.hip): a line matrix stores each 1-D-blocked line
@@ -197,6 +199,26 @@ __device__ __forceinline__ float4 load_nt(const float* p) {
 __device__ __forceinline__ uint2 load_nt(const unsigned short* p) {
     const v2i t = __builtin_nontemporal_load((const v2i*)p);
     return make_uint2((uint32_t)t[0], (uint32_t)t[1]);
+}
+
+// bf16 full-precision tensors (the MXC_CBF_BF16 layout and the MXC_FN_BF16
+// mode).  fp32 -> bf16 is the hardware conversion (v_cvt_pk_bf16_f32, two
+// values per instruction): round to nearest, ties to even, a NaN stays a NaN.
+typedef float f2v __attribute__((ext_vector_type(2)));
+typedef __bf16 bf2v __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t bf16_pack2(float a, float b) {
+    const f2v v = {a, b};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf2v));
+}
+__device__ __forceinline__ uint32_t bf16_bits(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
+__device__ __forceinline__ float bf16_round(float f) { return __uint_as_float(bf16_bits(f) << 16); }
+// four consecutive bf16 (8 bytes) <-> four floats
+__device__ __forceinline__ uint2 bf16_pack4(float a, float b, float c, float d) {
+    return make_uint2(bf16_pack2(a, b), bf16_pack2(c, d));
+}
+__device__ __forceinline__ float4 bf16_unpack4(uint2 u) {
+    return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xFFFF0000u),
+                       __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xFFFF0000u));
 }
 
 // Largest |x| bit pattern of a block -> E8M0 code (0xFF if any element was

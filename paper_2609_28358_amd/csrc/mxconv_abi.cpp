@@ -83,6 +83,8 @@ int conv_init(Conv* cv, const mxc_conv* p, int fmt, int op) {
 using namespace mxc;
 
 static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+// output layouts of the GEMM entry points: fp32 NCHW / CBF, bf16 CBF
+static bool out_layout_ok(int l) { return l == MXC_NCHW || l == MXC_CBF || l == MXC_CBF_BF16; }
 
 extern "C" {
 
@@ -264,27 +266,27 @@ int mxconv_im2col_cbf(const mxc_conv* p, int fmt, const void* xc, const uint8_t*
 }
 
 int mxconv_fwd(const mxc_conv* p, int fmt, const void* wc, const uint8_t* ws, const void* xc,
-               const uint8_t* xs, float* y, int y_layout, void* stream) {
+               const uint8_t* xs, void* y, int y_layout, void* stream) {
     if (!p || !wc || !ws || !xc || !xs || !y) return MXC_ERR_NULL;
-    if (y_layout != MXC_NCHW && y_layout != MXC_CBF) return MXC_ERR_ARG;
+    if (!out_layout_ok(y_layout)) return MXC_ERR_ARG;
     Conv cv;
     int rc = conv_init(&cv, p, fmt, CONV_FWD);
     if (rc) return rc;
     if (!aligned16(wc) || !aligned16(ws) || !aligned16(xc) || !aligned16(xs) || !aligned16(y))
         return MXC_ERR_ALIGN;
-    return launch_fwd(cv, wc, ws, xc, xs, y, y_layout, (hipStream_t)stream);
+    return launch_fwd(cv, wc, ws, xc, xs, (float*)y, y_layout, (hipStream_t)stream);
 }
 
 int mxconv_dgrad(const mxc_conv* p, int fmt, const void* wc, const uint8_t* ws, const void* gc,
-                 const uint8_t* gs, float* gx, int gx_layout, void* stream) {
+                 const uint8_t* gs, void* gx, int gx_layout, void* stream) {
     if (!p || !wc || !ws || !gc || !gs || !gx) return MXC_ERR_NULL;
-    if (gx_layout != MXC_NCHW && gx_layout != MXC_CBF) return MXC_ERR_ARG;
+    if (!out_layout_ok(gx_layout)) return MXC_ERR_ARG;
     Conv cv;
     int rc = conv_init(&cv, p, fmt, CONV_DGRAD);
     if (rc) return rc;
     if (!aligned16(wc) || !aligned16(ws) || !aligned16(gc) || !aligned16(gs) || !aligned16(gx))
         return MXC_ERR_ALIGN;
-    return launch_dgrad(cv, wc, ws, gc, gs, gx, gx_layout, (hipStream_t)stream);
+    return launch_dgrad(cv, wc, ws, gc, gs, (float*)gx, gx_layout, (hipStream_t)stream);
 }
 
 static int wgrad_call(const mxc_conv* p, int fmt, const void* gc, const uint8_t* gs, const void* xc,
@@ -312,10 +314,10 @@ int mxconv_wgrad_deferred(const mxc_conv* p, int fmt, const void* gc, const uint
 }
 
 int mxconv_backward(const mxc_conv* p, int fmt, const void* wc, const uint8_t* ws, const void* gc,
-                    const uint8_t* gs, const void* xc, const uint8_t* xs, float* gx, int gx_layout, float* gw,
+                    const uint8_t* gs, const void* xc, const uint8_t* xs, void* gx, int gx_layout, float* gw,
                     void* workspace, size_t ws_bytes, int deferred, void* stream) {
     if (!p || !wc || !ws || !gc || !gs || !xc || !xs || !gx || !gw) return MXC_ERR_NULL;
-    if (gx_layout != MXC_NCHW && gx_layout != MXC_CBF) return MXC_ERR_ARG;
+    if (!out_layout_ok(gx_layout)) return MXC_ERR_ARG;
     if (deferred != 0 && deferred != 1) return MXC_ERR_ARG;
     // one fmt names (W, G_Y) for the input gradient and (G_Y, X) for the
     // weight gradient, so G_Y would take both halves of a mixed pair
@@ -330,7 +332,7 @@ int mxconv_backward(const mxc_conv* p, int fmt, const void* wc, const uint8_t* w
     if (!aligned16(wc) || !aligned16(ws) || !aligned16(gc) || !aligned16(gs) || !aligned16(xc) ||
         !aligned16(xs) || !aligned16(gx) || !aligned16(gw) || (need && !aligned16(workspace)))
         return MXC_ERR_ALIGN;
-    return launch_backward(dcv, wc, ws, gc, gs, gx, gx_layout, wcv, xc, xs, gw, workspace, (hipStream_t)stream,
+    return launch_backward(dcv, wc, ws, gc, gs, (float*)gx, gx_layout, wcv, xc, xs, gw, workspace, (hipStream_t)stream,
                            deferred == 1);
 }
 
@@ -362,11 +364,11 @@ bool fused_shape(const Conv& cv, bool dg) {
 }  // namespace
 
 int mxconv_fwd_quant(const mxc_conv* p, int fmt, const void* wc, const uint8_t* ws, const void* xc,
-                     const uint8_t* xs, int fn, int out_fmt, void* yc, uint8_t* ysc, float* y_act,
+                     const uint8_t* xs, int fn, int out_fmt, void* yc, uint8_t* ysc, void* y_act,
                      void* stream) {
     if (!p || !wc || !ws || !xc || !xs || !yc || !ysc) return MXC_ERR_NULL;
-    const bool pre = (fn & MXC_FN_PRE_OUT) != 0;
-    fn &= ~MXC_FN_PRE_OUT;
+    const bool pre = (fn & MXC_FN_PRE_OUT) != 0, bf16 = (fn & MXC_FN_BF16) != 0;
+    fn &= ~(MXC_FN_PRE_OUT | MXC_FN_BF16);
     if (fn < MXC_FN_NONE || fn > MXC_FN_SILU || !fmt_ok(out_fmt)) return MXC_ERR_ARG;
     Conv cv;
     int rc = conv_init(&cv, p, fmt, CONV_FWD);
@@ -375,15 +377,17 @@ int mxconv_fwd_quant(const mxc_conv* p, int fmt, const void* wc, const uint8_t* 
     if (!aligned16(wc) || !aligned16(ws) || !aligned16(xc) || !aligned16(xs) || !aligned16(yc) ||
         !aligned16(ysc) || (y_act && !aligned16(y_act)))
         return MXC_ERR_ALIGN;
-    FusedEpi q{yc, ysc, out_fmt, fn, nullptr, pre};
-    rc = launch_conv_lean(cv, false, wc, ws, xc, xs, y_act, MXC_CBF, (hipStream_t)stream, &q);
+    FusedEpi q{yc, ysc, out_fmt, fn, nullptr, pre, bf16};
+    rc = launch_conv_lean(cv, false, wc, ws, xc, xs, (float*)y_act, MXC_CBF, (hipStream_t)stream, &q);
     return rc == 1 ? MXC_ERR_SHAPE : rc;
 }
 
 int mxconv_dgrad_quant(const mxc_conv* p, int fmt, const void* wc, const uint8_t* ws, const void* gc,
-                       const uint8_t* gs, int fn, const float* z, int out_fmt, void* gxc, uint8_t* gxs,
+                       const uint8_t* gs, int fn, const void* z, int out_fmt, void* gxc, uint8_t* gxs,
                        float* gx_act, void* stream) {
     if (!p || !wc || !ws || !gc || !gs || !gxc || !gxs) return MXC_ERR_NULL;
+    const bool bf16 = (fn & MXC_FN_BF16) != 0;
+    fn &= ~MXC_FN_BF16;
     if (fn < MXC_FN_NONE || fn > MXC_FN_SILU || !fmt_ok(out_fmt)) return MXC_ERR_ARG;
     if (fn != MXC_FN_NONE && !z) return MXC_ERR_NULL;
     Conv cv;
@@ -393,7 +397,7 @@ int mxconv_dgrad_quant(const mxc_conv* p, int fmt, const void* wc, const uint8_t
     if (!aligned16(wc) || !aligned16(ws) || !aligned16(gc) || !aligned16(gs) || !aligned16(gxc) ||
         !aligned16(gxs) || (gx_act && !aligned16(gx_act)) || (fn != MXC_FN_NONE && !aligned16(z)))
         return MXC_ERR_ALIGN;
-    FusedEpi q{gxc, gxs, out_fmt, fn, z, false};
+    FusedEpi q{gxc, gxs, out_fmt, fn, z, false, bf16};
     rc = launch_conv_lean(cv, true, wc, ws, gc, gs, gx_act, MXC_CBF, (hipStream_t)stream, &q);
     return rc == 1 ? MXC_ERR_SHAPE : rc;
 }
@@ -462,9 +466,11 @@ int mxconv_concat_cbf(int fmt, int n, int h, int w, int nparts, const mxc_part* 
 }
 
 int mxconv_quantize_sum(int fmt, int n, int c, int h, int w, int nterms, const mxc_term* terms, int fn,
-                        const float* z, void* codes, uint8_t* scales, float* vals, void* stream) {
+                        const void* z, void* codes, uint8_t* scales, float* vals, void* stream) {
     if (!terms || !codes || !scales) return MXC_ERR_NULL;
     if (nterms < 1 || nterms > MXC_TERMS_MAX) return MXC_ERR_ARG;
+    const bool bf16 = (fn & MXC_FN_BF16) != 0;
+    fn &= ~MXC_FN_BF16;
     if (fmt != MXC_E4M3 && fmt != MXC_E2M1) return MXC_ERR_ARG;
     if (fn < MXC_FN_NONE || fn > MXC_FN_SILU) return MXC_ERR_ARG;
     if (fn != MXC_FN_NONE && !z) return MXC_ERR_NULL;
@@ -483,7 +489,7 @@ int mxconv_quantize_sum(int fmt, int n, int c, int h, int w, int nterms, const m
     if (!aligned16(codes) || !aligned16(scales) || (vals && !aligned16(vals)) ||
         (fn != MXC_FN_NONE && !aligned16(z)))
         return MXC_ERR_ALIGN;
-    return launch_quantize_sum(g, fmt, terms, nterms, fn, z, codes, scales, vals, (hipStream_t)stream);
+    return launch_quantize_sum(g, fmt, terms, nterms, fn, bf16, z, codes, scales, vals, (hipStream_t)stream);
 }
 
 size_t mxconv_naive_codes_bytes(int64_t lines, int64_t len, int fmt) {

@@ -69,37 +69,45 @@ __global__ __launch_bounds__(256) void concat_kernel(ConcatArgs a, uint8_t* __re
 }
 
 struct SumArgs {
-    const float* src[MXC_TERMS_MAX];
+    const void* src[MXC_TERMS_MAX];   // fp32, or bf16 (BF)
     int c_src[MXC_TERMS_MAX];
     int c_off[MXC_TERMS_MAX];
     int down[MXC_TERMS_MAX];
     int nterms;
     int c, h, w, ncb;                 // destination (n, c, h, w), channel blocks
     int fn;
-    const float* z;                   // CBF [n/32][h][w][c][32] (fn != NONE)
+    const void* z;                    // CBF [n/32][h][w][c][32] (fn != NONE), fp32 or bf16 (BF)
     float* vals;                      // optional: the values quantized
 };
 
+// Four consecutive elements at index i of an fp32 or (BF) bf16 tensor.
+template <bool BF>
+__device__ __forceinline__ float4 load4(const void* s, size_t i) {
+    if constexpr (BF) return bf16_unpack4(load_nt((const unsigned short*)s + i));
+    else              return load_nt((const float*)s + i);
+}
+
 // Term t at destination pixel (g, y, x), channel ch, samples j .. j+3.
+template <bool BF>
 __device__ __forceinline__ float4 term4(const SumArgs& a, int t, long long g, int y, int x, int ch, int j) {
-    const float* s = a.src[t];
+    const void* s = a.src[t];
     const int cs = a.c_src[t];
     const int col = a.c_off[t] + ch;
     if (!a.down[t]) {
         const size_t i = ((((size_t)g * a.h + y) * a.w + x) * cs + col) * 32 + j;
-        return load_nt(s + i);
+        return load4<BF>(s, i);
     }
     const int hs = 2 * a.h, ws = 2 * a.w;
     const size_t r0 = ((size_t)g * hs + 2 * y) * ws + 2 * x, r1 = r0 + ws;
-    const float4 p = load_nt(s + ((r0 * cs + col) * 32 + j));
-    const float4 q = load_nt(s + (((r0 + 1) * cs + col) * 32 + j));
-    const float4 u = load_nt(s + ((r1 * cs + col) * 32 + j));
-    const float4 v = load_nt(s + (((r1 + 1) * cs + col) * 32 + j));
+    const float4 p = load4<BF>(s, (r0 * cs + col) * 32 + j);
+    const float4 q = load4<BF>(s, ((r0 + 1) * cs + col) * 32 + j);
+    const float4 u = load4<BF>(s, (r1 * cs + col) * 32 + j);
+    const float4 v = load4<BF>(s, ((r1 + 1) * cs + col) * 32 + j);
     return make_float4((p.x + q.x) + (u.x + v.x), (p.y + q.y) + (u.y + v.y), (p.z + q.z) + (u.z + v.z),
                        (p.w + q.w) + (u.w + v.w));
 }
 
-template <int FMT>
+template <int FMT, bool BF>
 __global__ __launch_bounds__(256) void quantize_sum_kernel(SumArgs a, uint8_t* __restrict__ codes,
                                                            uint8_t* __restrict__ scales, long long nblocks) {
     const long long blk = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -118,13 +126,13 @@ __global__ __launch_bounds__(256) void quantize_sum_kernel(SumArgs a, uint8_t* _
         const int ch = cb * 32 + 8 * q + (lane >> 3);
         float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
         if (ch < a.c) {
-            s = term4(a, 0, g, y, x, ch, j);
+            s = term4<BF>(a, 0, g, y, x, ch, j);
             for (int t = 1; t < a.nterms; t++) {
-                const float4 u = term4(a, t, g, y, x, ch, j);
+                const float4 u = term4<BF>(a, t, g, y, x, ch, j);
                 s.x += u.x; s.y += u.y; s.z += u.z; s.w += u.w;
             }
             if (a.fn != MXC_FN_NONE) {
-                const float4 zz = load_nt(a.z + ((size_t)pix * a.c + ch) * 32 + j);
+                const float4 zz = load4<BF>(a.z, ((size_t)pix * a.c + ch) * 32 + j);
                 s.x *= fn_grad(a.fn, zz.x);
                 s.y *= fn_grad(a.fn, zz.y);
                 s.z *= fn_grad(a.fn, zz.z);
@@ -185,8 +193,8 @@ int launch_concat(const Geom& dst, const mxc_part* parts, int nparts, void* code
     return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
 }
 
-int launch_quantize_sum(const Geom& dst, int fmt, const mxc_term* terms, int nterms, int fn, const float* z,
-                        void* codes, uint8_t* scales, float* vals, hipStream_t s) {
+int launch_quantize_sum(const Geom& dst, int fmt, const mxc_term* terms, int nterms, int fn, bool bf16,
+                        const void* z, void* codes, uint8_t* scales, float* vals, hipStream_t s) {
     SumArgs a{};
     for (int t = 0; t < nterms; t++) {
         a.src[t] = terms[t].src;
@@ -203,12 +211,15 @@ int launch_quantize_sum(const Geom& dst, int fmt, const mxc_term* terms, int nte
     if (nblocks <= 0) return MXC_OK;
     const long long grid = (nblocks + 3) / 4;
     if (grid > 0x7FFFFFFFLL) return MXC_ERR_SHAPE;
-    if (fmt == MXC_E4M3)
-        hipLaunchKernelGGL(quantize_sum_kernel<MXC_E4M3>, dim3((unsigned)grid), dim3(256), 0, s, a, (uint8_t*)codes,
-                           scales, nblocks);
-    else
-        hipLaunchKernelGGL(quantize_sum_kernel<MXC_E2M1>, dim3((unsigned)grid), dim3(256), 0, s, a, (uint8_t*)codes,
-                           scales, nblocks);
+    const dim3 gd((unsigned)grid);
+    uint8_t* const cd = (uint8_t*)codes;
+    if (fmt == MXC_E4M3) {
+        if (bf16) hipLaunchKernelGGL((quantize_sum_kernel<MXC_E4M3, true>), gd, dim3(256), 0, s, a, cd, scales, nblocks);
+        else      hipLaunchKernelGGL((quantize_sum_kernel<MXC_E4M3, false>), gd, dim3(256), 0, s, a, cd, scales, nblocks);
+    } else {
+        if (bf16) hipLaunchKernelGGL((quantize_sum_kernel<MXC_E2M1, true>), gd, dim3(256), 0, s, a, cd, scales, nblocks);
+        else      hipLaunchKernelGGL((quantize_sum_kernel<MXC_E2M1, false>), gd, dim3(256), 0, s, a, cd, scales, nblocks);
+    }
     return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
 }
 

@@ -12,10 +12,11 @@ import torch
 
 E4M3, E2M1, E2M3, E3M2 = 0, 1, 2, 3
 F32, BF16 = 0, 1
-NCHW, NHWC, CBF = 0, 1, 2
+NCHW, NHWC, CBF, CBF_BF16 = 0, 1, 2, 3
 ACT, WEIGHT = 0, 1
 FN_NONE, FN_RELU, FN_SILU = 0, 1, 2
 FN_PRE_OUT = 0x100      # or-ed into fwd_quant's fn: act_out receives the pre-activation
+FN_BF16 = 0x200         # or-ed into fwd_quant / dgrad_quant / quantize_sum's fn: bf16 full-precision tensors
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libmxconv.so")
@@ -324,13 +325,22 @@ def im2col_cbf(cv, x, stream=None):
     return codes, scales
 
 
+def _want(t, dtype, what):
+    """A device tensor argument must have the element type the call reads or
+    writes through its pointer."""
+    if t is not None and t.dtype != dtype:
+        raise MxconvError(f"{what} must be {dtype}, got {t.dtype}")
+
+
 def _out(shape, layout, bn, device, out):
     n, c, h, w = shape
+    dtype = torch.bfloat16 if layout == CBF_BF16 else torch.float32
     if out is not None:
+        _want(out, dtype, "the output")
         return out
-    if layout == CBF:
-        return torch.empty((n // bn, h, w, c, bn), dtype=torch.float32, device=device)
-    return torch.empty((n, c, h, w), dtype=torch.float32, device=device)
+    if layout in (CBF, CBF_BF16):
+        return torch.empty((n // bn, h, w, c, bn), dtype=dtype, device=device)
+    return torch.empty((n, c, h, w), dtype=dtype, device=device)
 
 
 def batch_block(n):
@@ -411,7 +421,9 @@ def wgrad_reduce_multi(items, stream=None):
 def fwd_quant(cv, w, x, fn=FN_NONE, out_fmt=None, out=None, act_out=None, stream=None):
     """Forward with the quantizing epilogue: MX codes of fn(W * X) for
     (n, cout, Ho, Wo); `act_out` (CBF fp32, optional) receives the values
-    that were quantized.  Returns the MxTensor."""
+    that were quantized (with FN_PRE_OUT: W * X; with FN_BF16 | FN_PRE_OUT
+    it is bf16 and receives W * X rounded to bf16).  Returns the MxTensor."""
+    _want(act_out, torch.bfloat16 if (fn & FN_BF16) and (fn & FN_PRE_OUT) else torch.float32, "act_out")
     ho, wo = out_size(cv)
     out_fmt = x.fmt if out_fmt is None else out_fmt
     shape = (cv["n"], cv["cout"], ho, wo)
@@ -424,8 +436,11 @@ def fwd_quant(cv, w, x, fn=FN_NONE, out_fmt=None, out=None, act_out=None, stream
 
 def dgrad_quant(cv, w, gy, fn=FN_NONE, z=None, out_fmt=None, out=None, act_out=None, stream=None):
     """Input gradient with the quantizing epilogue: MX codes of
-    (W^T * G_Y) . fn'(z) for (n, cin, h, w); z is the CBF fp32 pre-activation
-    of this layer's input (not needed for FN_NONE)."""
+    (W^T * G_Y) . fn'(z) for (n, cin, h, w); z is the CBF pre-activation of
+    this layer's input (not needed for FN_NONE), fp32, or bf16 with FN_BF16.
+    act_out (optional) is fp32."""
+    _want(z, torch.bfloat16 if fn & FN_BF16 else torch.float32, "z")
+    _want(act_out, torch.float32, "act_out")
     out_fmt = gy.fmt if out_fmt is None else out_fmt
     shape = (cv["n"], cv["cin"], cv["h"], cv["w"])
     g = out if out is not None else MxTensor.empty(ACT, out_fmt, shape, gy.codes.device)
@@ -461,12 +476,17 @@ def concat_cbf(parts, out=None, stream=None):
 
 def quantize_sum(terms, shape, fmt, fn=FN_NONE, z=None, out=None, vals=None, stream=None):
     """MX codes of fn'(z) . (sum of terms) for the (n, c, h, w) tensor `shape`.
-    terms: tuples (src, c_src, c_off, down) with src an fp32 CBF device
-    tensor [n/32][hs][ws][c_src][32]."""
+    terms: tuples (src, c_src, c_off, down) with src a CBF device tensor
+    [n/32][hs][ws][c_src][32]; terms and z are fp32, or bf16 with FN_BF16;
+    vals (optional) is fp32."""
     if not 1 <= len(terms) <= TERMS_MAX:
         raise MxconvError(f"1 to {TERMS_MAX} terms")
+    dt = torch.bfloat16 if fn & FN_BF16 else torch.float32
+    _want(z, dt, "z")
+    _want(vals, torch.float32, "vals")
     arr = (MxcTerm * len(terms))()
     for k, (src, c_src, c_off, down) in enumerate(terms):
+        _want(src, dt, f"term {k}")
         arr[k] = MxcTerm(src.data_ptr(), c_src, c_off, down)
     n, c, h, w = shape
     g = out if out is not None else MxTensor.empty(ACT, fmt, shape, terms[0][0].device)

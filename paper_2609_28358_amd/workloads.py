@@ -148,21 +148,33 @@ class NetStep:
 
     Inputs (seeded): the image ~ U(0, 1) as bf16 NCHW; bf16 master weights,
     Kaiming-normal over the real input channels (zero on a concatenation's
-    padding channels); the upstream gradient of each output ~ N(0, 1e-3),
-    fp32 CBF."""
+    padding channels); the upstream gradient of each output ~ N(0, 1e-3) as
+    a CBF tensor of the master dtype.
 
-    def __init__(self, net, n, fmt, device, seed=3000, fused_dgrad=True):
+    Full-precision tensors between layers (pre-activations, input gradients,
+    upstream gradients) are kept in `master`: bf16 by default, each GEMM
+    result rounded to bf16 before it is activated, multiplied or quantized
+    (the library's MXC_FN_BF16 / MXC_CBF_BF16 mode), or fp32."""
+
+    def __init__(self, net, n, fmt, device, seed=3000, fused_dgrad=True, master=torch.bfloat16):
         if n % 32:
             raise ValueError("the network step runs batch blocks of 32")
+        if master not in (torch.bfloat16, torch.float32):
+            raise ValueError("master tensors are bf16 or fp32")
         self.net, self.n, self.fmt, self.dev = net, n, fmt, device
         self.fused = fused_dgrad
+        self.master = master
+        bf = master == torch.bfloat16
+        self.es = 2.0 if bf else 4.0                       # bytes per full-precision element
+        self.fbf = mx.FN_BF16 if bf else 0                 # fn flag of the fused calls
+        self.gx_layout = mx.CBF_BF16 if bf else mx.CBF
         self.convs = net.convs()
         img = net.nodes[0]
         self.image = synth.uniform((n, img["c"], img["h"], img["w"]), seed).to(torch.bfloat16).to(device)
         self.t = {}      # tensor name -> MxTensor (activations as stored)
-        self.y = {}      # conv name -> fp32 CBF pre-activation
+        self.y = {}      # conv name -> CBF pre-activation (master dtype)
         self.w = {}      # conv name -> (bf16 master, MxTensor)
-        self.gx = {}     # conv name -> fp32 CBF input gradient
+        self.gx = {}     # conv name -> CBF input gradient (master dtype)
         self.gy = {}     # conv name -> MxTensor G_Y
         self.ws = {}     # conv name -> split-K workspace
         self.gw = {}     # conv name -> fp32 G_W
@@ -178,7 +190,7 @@ class NetStep:
                 cv = conv_dict(t, n)
                 self.cv[nm] = cv
                 self.t[nm] = mx.MxTensor.empty(mx.ACT, fmt, shape, device)
-                self.y[nm] = torch.empty((n // 32, t["h"], t["w"], t["c"], 32), dtype=torch.float32, device=device)
+                self.y[nm] = torch.empty((n // 32, t["h"], t["w"], t["c"], 32), dtype=master, device=device)
                 wm = synth.kaiming(t["cout"], t["cin_real"], t["k"], t["k"], seed + 7 * i + 1)
                 if t["cin"] != t["cin_real"]:
                     wm = self._spread(wm, net.node(t["src"]))
@@ -186,7 +198,7 @@ class NetStep:
                 self.w[nm] = (wm, mx.MxTensor.empty(mx.WEIGHT, fmt, tuple(wm.shape), device))
                 self.gy[nm] = mx.MxTensor.empty(mx.ACT, fmt, shape, device)
                 if net.node(t["src"])["kind"] != "input":
-                    self.gx[nm] = torch.empty((n // 32, cv["h"], cv["w"], cv["cin"], 32), dtype=torch.float32,
+                    self.gx[nm] = torch.empty((n // 32, cv["h"], cv["w"], cv["cin"], 32), dtype=master,
                                               device=device)
                 self.ws[nm] = torch.empty(max(16, mx.wgrad_workspace_bytes(cv, fmt)), dtype=torch.uint8, device=device)
                 self.gw[nm] = torch.empty(tuple(wm.shape), dtype=torch.float32, device=device)
@@ -194,7 +206,7 @@ class NetStep:
         for k, o in enumerate(net.outputs):
             t = net.node(o)
             g = synth.normal((n, t["c"], t["h"], t["w"]), 1e-3, seed + 1000 + k)
-            self.ext[o] = synth.nchw_to_cbf(g, 32).to(device)
+            self.ext[o] = synth.nchw_to_cbf(g, 32).to(master).to(device)
         self._plan_backward()
 
     @staticmethod
@@ -229,7 +241,8 @@ class NetStep:
         self.consumers = cons
 
     def grad_terms(self, name):
-        """fp32 terms (src, c_src, c_off, down) of the gradient of tensor `name`."""
+        """Terms (src, c_src, c_off, down) of the gradient of tensor `name`
+        (master-dtype CBF tensors)."""
         net = self.net
         terms = []
         for c in self.consumers[name]:
@@ -251,7 +264,7 @@ class NetStep:
         bytes): flops of a GEMM with real channels only; bytes = every operand
         read once and every result written once (codes + scales of MX
         tensors, 4 bytes per fp32 element, 2 per bf16 element)."""
-        net, n, fmt = self.net, self.n, self.fmt
+        net, n, fmt, es, fbf = self.net, self.n, self.fmt, self.es, self.fbf
         A, W = mx.ACT, mx.WEIGHT
         seq = []
         img = net.nodes[0]
@@ -271,9 +284,9 @@ class NetStep:
             if t["kind"] == "conv":
                 src = net.node(t["src"])
                 by = (mxb(W, fmt, tuple(self.w[nm][0].shape)) + mxb(A, fmt, (n, src["c"], src["h"], src["w"])) +
-                      mxb(A, fmt, oshape) + 4.0 * math.prod(oshape))
+                      mxb(A, fmt, oshape) + es * math.prod(oshape))
                 seq.append((f"fwd {nm}", lambda nm=nm, t=t: mx.fwd_quant(
-                    self.cv[nm], self.w[nm][1], self.t[t["src"]], fn=mx.FN_SILU | mx.FN_PRE_OUT, out=self.t[nm],
+                    self.cv[nm], self.w[nm][1], self.t[t["src"]], fn=mx.FN_SILU | mx.FN_PRE_OUT | fbf, out=self.t[nm],
                     act_out=self.y[nm]), real_flops(t, n), by))
             else:
                 parts = [(self.t[p], up) for p, up in t["parts"]]
@@ -292,9 +305,9 @@ class NetStep:
             if nm not in fused_in:
                 terms = self.grad_terms(nm)
                 el = math.prod(shape)
-                by = sum(4.0 * el * (4 if d else 1) for _, _, _, d in terms) + 4.0 * el + mxb(A, fmt, shape)
+                by = sum(es * el * (4 if d else 1) for _, _, _, d in terms) + es * el + mxb(A, fmt, shape)
                 seq.append((f"quant_gy {nm}", lambda terms=terms, shape=shape, nm=nm: mx.quantize_sum(
-                    terms, shape, fmt, fn=mx.FN_SILU, z=self.y[nm], out=self.gy[nm]), 0.0, by))
+                    terms, shape, fmt, fn=mx.FN_SILU | fbf, z=self.y[nm], out=self.gy[nm]), 0.0, by))
             src = net.node(t["src"])
             sshape = (n, src["c"], src["h"], src["w"])
             xb = mxb(A, fmt, sshape)
@@ -304,16 +317,16 @@ class NetStep:
             if t["src"] in fused_in:
                 sn = t["src"]
                 seq.append((f"dgrad_quant {nm}", lambda nm=nm, sn=sn: mx.dgrad_quant(
-                    self.cv[nm], self.w[nm][1], self.gy[nm], fn=mx.FN_SILU, z=self.y[sn], out=self.gy[sn]),
-                    f, wb + mxb(A, fmt, shape) + 4.0 * math.prod(sshape) + mxb(A, fmt, sshape)))
+                    self.cv[nm], self.w[nm][1], self.gy[nm], fn=mx.FN_SILU | fbf, z=self.y[sn], out=self.gy[sn]),
+                    f, wb + mxb(A, fmt, shape) + es * math.prod(sshape) + mxb(A, fmt, sshape)))
                 seq.append((f"wgrad {nm}", lambda nm=nm, t=t: mx.wgrad(
                     self.cv[nm], self.gy[nm], self.t[t["src"]], out=self.gw[nm], workspace=self.ws[nm],
                     deferred=True), f, mxb(A, fmt, shape) + xb + gwb))
             elif nm in self.gx:
                 seq.append((f"bwd {nm}", lambda nm=nm, t=t: mx.backward(
-                    self.cv[nm], self.w[nm][1], self.gy[nm], self.t[t["src"]], layout=mx.CBF, gx_out=self.gx[nm],
-                    gw_out=self.gw[nm], workspace=self.ws[nm], deferred=True),
-                    2.0 * f, wb + mxb(A, fmt, shape) + xb + 4.0 * self.gx[nm].numel() + gwb))
+                    self.cv[nm], self.w[nm][1], self.gy[nm], self.t[t["src"]], layout=self.gx_layout,
+                    gx_out=self.gx[nm], gw_out=self.gw[nm], workspace=self.ws[nm], deferred=True),
+                    2.0 * f, wb + mxb(A, fmt, shape) + xb + es * self.gx[nm].numel() + gwb))
             else:
                 seq.append((f"wgrad {nm}", lambda nm=nm, t=t: mx.wgrad(
                     self.cv[nm], self.gy[nm], self.t[t["src"]], out=self.gw[nm], workspace=self.ws[nm],
@@ -353,9 +366,16 @@ class QlrStep:
     FRONT = ((3, 32), (32, 64), (64, 128))
     BACK = ((128, 256), (256, 256), (256, 256), (256, 256))
 
-    def __init__(self, device, fmt=mx.E2M1, buffer=8192, batch=128, seed=5000, fused_dgrad=True):
+    def __init__(self, device, fmt=mx.E2M1, buffer=8192, batch=128, seed=5000, fused_dgrad=True,
+                 master=torch.bfloat16):
+        if master not in (torch.bfloat16, torch.float32):
+            raise ValueError("master tensors are bf16 or fp32")
         self.dev, self.fmt, self.batch = device, fmt, batch
         self.fused = fused_dgrad
+        bf = master == torch.bfloat16
+        self.es = 2.0 if bf else 4.0
+        self.fbf = mx.FN_BF16 if bf else 0
+        self.gx_layout = mx.CBF_BF16 if bf else mx.CBF
         g = torch.Generator()
         g.manual_seed(seed)
         self.front_cv = []
@@ -397,16 +417,16 @@ class QlrStep:
         self.y, self.gy, self.gx, self.gw, self.ws = [], [], [], [], []
         for i, cv in enumerate(self.back_cv):
             shp = (n, cv["cout"], cv["h"], cv["w"])
-            self.y.append(torch.empty((n // 32, cv["h"], cv["w"], cv["cout"], 32), dtype=torch.float32, device=device))
+            self.y.append(torch.empty((n // 32, cv["h"], cv["w"], cv["cout"], 32), dtype=master, device=device))
             self.x.append(mx.MxTensor.empty(mx.ACT, fmt, shp, device))
             self.gy.append(mx.MxTensor.empty(mx.ACT, fmt, shp, device))
-            self.gx.append(torch.empty((n // 32, cv["h"], cv["w"], cv["cin"], 32), dtype=torch.float32, device=device)
+            self.gx.append(torch.empty((n // 32, cv["h"], cv["w"], cv["cin"], 32), dtype=master, device=device)
                            if i > 0 else None)
             self.gw.append(torch.empty((cv["cout"], cv["cin"], 3, 3), dtype=torch.float32, device=device))
             self.ws.append(torch.empty(max(16, mx.wgrad_workspace_bytes(cv, fmt)), dtype=torch.uint8, device=device))
         last = self.back_cv[-1]
         ge = synth.normal((n, last["cout"], last["h"], last["w"]), 1e-3, seed + 98)
-        self.ext = synth.nchw_to_cbf(ge, 32).to(device)
+        self.ext = synth.nchw_to_cbf(ge, 32).to(master).to(device)
 
     def _group(self, codes, scales, k):
         return mx.MxTensor(codes[k * self.lc:(k + 1) * self.lc], scales[k * self.ls:(k + 1) * self.ls], mx.ACT,
@@ -425,7 +445,7 @@ class QlrStep:
     def calls(self):
         """The step as (label, callable, algorithmic flops, algorithmic bytes)
         tuples, with the conventions of NetStep.calls."""
-        fmt, n = self.fmt, self.batch
+        fmt, n, es, fbf = self.fmt, self.batch, self.es, self.fbf
         A, W = mx.ACT, mx.WEIGHT
         seq = [("quant_w", lambda: mx.quantize_multi(
             [(w, W, fmt, mx.NCHW, tuple(w.shape), q) for w, q in zip(self.back_wm, self.back_w)]), 0.0,
@@ -448,15 +468,16 @@ class QlrStep:
             shp = (n, cv["cout"], cv["h"], cv["w"])
             f = 2.0 * n * cv["cout"] * cv["h"] * cv["w"] * cv["cin"] * 9
             by = (mxb(W, fmt, (cv["cout"], cv["cin"], 3, 3)) + mxb(A, fmt, (n, cv["cin"], cv["h"], cv["w"])) +
-                  mxb(A, fmt, shp) + 4.0 * math.prod(shp))
+                  mxb(A, fmt, shp) + es * math.prod(shp))
             seq.append((f"fwd back{i}", lambda i=i, cv=cv: mx.fwd_quant(
-                cv, self.back_w[i], self.x[i], fn=mx.FN_SILU | mx.FN_PRE_OUT, out=self.x[i + 1], act_out=self.y[i]),
+                cv, self.back_w[i], self.x[i], fn=mx.FN_SILU | mx.FN_PRE_OUT | fbf, out=self.x[i + 1],
+                act_out=self.y[i]),
                 f, by))
         lc = self.back_cv[-1]
         shp = (n, lc["cout"], lc["h"], lc["w"])
-        seq.append(("quant_gy back3", lambda: mx.quantize_sum([(self.ext, lc["cout"], 0, 0)], shp, fmt, fn=mx.FN_SILU,
-                                                             z=self.y[-1], out=self.gy[-1]),
-                    0.0, 8.0 * math.prod(shp) + mxb(A, fmt, shp)))
+        seq.append(("quant_gy back3", lambda: mx.quantize_sum([(self.ext, lc["cout"], 0, 0)], shp, fmt,
+                                                             fn=mx.FN_SILU | fbf, z=self.y[-1], out=self.gy[-1]),
+                    0.0, 2.0 * es * math.prod(shp) + mxb(A, fmt, shp)))
         for i in range(len(self.back_cv) - 1, -1, -1):
             cv = self.back_cv[i]
             f = 2.0 * n * cv["cout"] * cv["h"] * cv["w"] * cv["cin"] * 9
@@ -469,19 +490,19 @@ class QlrStep:
                                                                   workspace=self.ws[0], deferred=True), f, wgb))
             elif self.fused:   # this layer's input gradient, times SiLU', quantized as the layer below's G_Y
                 seq.append((f"dgrad_quant back{i}", lambda i=i, cv=cv: mx.dgrad_quant(
-                    cv, self.back_w[i], self.gy[i], fn=mx.FN_SILU, z=self.y[i - 1], out=self.gy[i - 1]),
-                    f, wb + mxb(A, fmt, gshp) + 4.0 * math.prod(xshp) + mxb(A, fmt, xshp)))
+                    cv, self.back_w[i], self.gy[i], fn=mx.FN_SILU | fbf, z=self.y[i - 1], out=self.gy[i - 1]),
+                    f, wb + mxb(A, fmt, gshp) + es * math.prod(xshp) + mxb(A, fmt, xshp)))
                 seq.append((f"wgrad back{i}", lambda i=i, cv=cv: mx.wgrad(
                     cv, self.gy[i], self.x[i], out=self.gw[i], workspace=self.ws[i], deferred=True), f, wgb))
             else:
                 seq.append((f"bwd back{i}", lambda i=i, cv=cv: mx.backward(
-                    cv, self.back_w[i], self.gy[i], self.x[i], layout=mx.CBF, gx_out=self.gx[i], gw_out=self.gw[i],
-                    workspace=self.ws[i], deferred=True), 2.0 * f, wb + wgb + 4.0 * math.prod(xshp)))
+                    cv, self.back_w[i], self.gy[i], self.x[i], layout=self.gx_layout, gx_out=self.gx[i],
+                    gw_out=self.gw[i], workspace=self.ws[i], deferred=True), 2.0 * f, wb + wgb + es * math.prod(xshp)))
                 pc = self.back_cv[i - 1]
                 pshp = (n, pc["cout"], pc["h"], pc["w"])
                 seq.append((f"quant_gy back{i - 1}", lambda i=i, pc=pc, pshp=pshp: mx.quantize_sum(
-                    [(self.gx[i], pc["cout"], 0, 0)], pshp, fmt, fn=mx.FN_SILU, z=self.y[i - 1], out=self.gy[i - 1]),
-                    0.0, 8.0 * math.prod(pshp) + mxb(A, fmt, pshp)))
+                    [(self.gx[i], pc["cout"], 0, 0)], pshp, fmt, fn=mx.FN_SILU | fbf, z=self.y[i - 1],
+                    out=self.gy[i - 1]), 0.0, 2.0 * es * math.prod(pshp) + mxb(A, fmt, pshp)))
         rb = sum(mx.wgrad_workspace_bytes(cv, fmt) + 4.0 * cv["cout"] * cv["cin"] * 9 for cv in self.back_cv
                  if mx.wgrad_workspace_bytes(cv, fmt))
         seq.append(("wgrad_reduce", lambda: mx.wgrad_reduce_multi(

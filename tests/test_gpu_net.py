@@ -6,8 +6,9 @@ how the step strings them together:
   * the step runs and every weight gradient is finite and non-zero;
   * the fused route (a single-consumer gradient quantized in its consumer's
     input-gradient epilogue) gives bit for bit the weight gradients of the
-    unfused route (input gradient in fp32, then mxconv_quantize_sum): both
-    take every rounding decision on the same fp32 values;
+    unfused route (input gradient stored, then mxconv_quantize_sum): both
+    take every rounding decision on the same values, with fp32 and with
+    bf16 master tensors (the GEMM result rounded to bf16 on both routes);
   * the step replayed from a HIP graph, with eager work between replays,
     reproduces the eager step bit for bit on every replay;
   * latent replay: the replayed groups are the stored codes and scales, and
@@ -37,11 +38,12 @@ def _run(calls):
     torch.cuda.synchronize()
 
 
+@pytest.mark.parametrize("master", [torch.bfloat16, torch.float32], ids=["bf16", "fp32"])
 @pytest.mark.parametrize("fmt", [0, 1], ids=["mxfp8", "mxfp4"])
-def test_yolo_step_fused_equals_unfused(mx, fmt):
+def test_yolo_step_fused_equals_unfused(mx, fmt, master):
     net = wl.yolo_net(128)
-    a = wl.NetStep(net, 32, fmt, DEV, fused_dgrad=True)
-    b = wl.NetStep(net, 32, fmt, DEV, fused_dgrad=False)
+    a = wl.NetStep(net, 32, fmt, DEV, fused_dgrad=True, master=master)
+    b = wl.NetStep(net, 32, fmt, DEV, fused_dgrad=False, master=master)
     ca, cb = a.calls(), b.calls()
     assert any(c[0].startswith("dgrad_quant") for c in ca) and not any(c[0].startswith("dgrad_quant") for c in cb)
     _run(ca)
@@ -72,9 +74,10 @@ def test_yolo_step_graph_replay(mx):
             assert torch.equal(st.gw[k], ref[k]), (it, k)
 
 
-def test_latent_replay_step(mx):
-    a = wl.QlrStep(DEV, buffer=256, fused_dgrad=True)
-    b = wl.QlrStep(DEV, buffer=256, fused_dgrad=False)
+@pytest.mark.parametrize("master", [torch.bfloat16, torch.float32], ids=["bf16", "fp32"])
+def test_latent_replay_step(mx, master):
+    a = wl.QlrStep(DEV, buffer=256, fused_dgrad=True, master=master)
+    b = wl.QlrStep(DEV, buffer=256, fused_dgrad=False, master=master)
     _run(a.calls())
     _run(b.calls())
     for i in range(len(a.gw)):

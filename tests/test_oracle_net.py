@@ -88,3 +88,39 @@ def test_gradient_sum_equals_autograd(fn):
     # every input was drawn in fp32, so both sides see the same numbers; only
     # the fp64 summation order differs
     assert np.max(np.abs(got - ref.numpy())) <= 1e-12 * float(np.max(np.abs(ref.numpy())))
+
+
+# ---------------------------------------------------------------- bf16 rounding
+def test_round_bf16_hand_worked():
+    """bf16 keeps 7 fraction bits: near 1 its step is 2^-7.  Ties go to the
+    neighbour with an even last bit; past the largest finite bf16 is inf."""
+    f = np.float32
+    cases = [
+        (1.0, 1.0),
+        (1.0 + 2.0 ** -8, 1.0),                            # half a step above 1: tie, 1 is even
+        (1.0 + 3 * 2.0 ** -8, 1.0 + 2.0 ** -6),            # tie between 1 + 2^-7 (odd) and 1 + 2^-6 (even)
+        (1.0 + 2.0 ** -8 + 2.0 ** -20, 1.0 + 2.0 ** -7),   # just above the tie
+        (1.0 + 2.0 ** -8 - 2.0 ** -20, 1.0),               # just below it
+        (-(1.0 + 3 * 2.0 ** -8), -(1.0 + 2.0 ** -6)),      # the sign is kept
+        (3.0e-39, float(np.uint32(0x00210000).view(np.float32))),   # subnormal: the same bit rule
+        (float(np.uint32(0x7F7FFFFF).view(np.float32)), np.inf),    # largest fp32 rounds past bf16's max
+        (float(np.uint32(0x7F7F7FFF).view(np.float32)), float(np.uint32(0x7F7F0000).view(np.float32))),
+        (np.inf, np.inf), (-0.0, -0.0),
+    ]
+    for x, want in cases:
+        got = oracle.round_bf16(np.array([x], f))[0]
+        assert got == f(want) and np.signbit(got) == np.signbit(f(want)), (x, got, want)
+    assert np.isnan(oracle.round_bf16(np.array([np.nan], f))[0])
+
+
+def test_round_bf16_matches_torch_cast():
+    """Against torch's fp32 -> bfloat16 cast (round to nearest even) on values
+    spanning the exponent range, with many exact ties."""
+    rng = np.random.default_rng(5)
+    x = (rng.standard_normal(200000) * np.exp2(rng.integers(-130, 120, 200000))).astype(np.float32)
+    ties = (x.view(np.uint32) & np.uint32(0xFFFF0000)) | np.uint32(0x8000)
+    x = np.concatenate([x, ties.view(np.float32)])
+    x = x[np.isfinite(x)]
+    want = torch.from_numpy(x).to(torch.bfloat16).to(torch.float32).numpy()
+    got = oracle.round_bf16(x)
+    assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
