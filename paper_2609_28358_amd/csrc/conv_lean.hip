@@ -83,6 +83,10 @@ struct LeanArgs {
     int qfmt, q_ncb, fn;
     int pre_out;              // forward: `out` receives the values before the activation
     int bf16;                 // the GEMM result is rounded to bf16 first; zpre and the pre_out output are bf16
+    int xrows;                // real channel rows of the source's blocks (its channels if it has one block, else 32)
+    int zoff;                 // > 0: the fused input gradient's bf16 z tiles are prefetched to LDS at this offset
+    int zpw, zrb;             // (host) the tile shape the z region is sized for
+    int zsl;                  // 1 KB slots of 16 rows per z tile: 1 if the layer has at most 16 rows, else 2
     const void* zpre;
     // NVFP4 operands (the NV kernels): per-tensor scales of W and the source;
     // the scale arrays ws / ss then hold E4M3 scales per 8x8 block, the 16 of
@@ -257,12 +261,15 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
             const int kb = b / HP, hc = b % HP;
             const int col = cbase + hc;
             const bool ok = col >= 0 && col < p.wsrc;
+            // channel rows past a single block's real channels hold +0 codes:
+            // read the zero block there instead (FP8 / FP4 rows of 32 / 16 bytes)
+            const bool row_real = fmt_bits(FX) == 6 || (int)(in_x / RB) < p.xrows;
             off[q] = (uint32_t)(ok ? col : 0) * x_pix + (KR ? 0u : (uint32_t)kb) * TBX + in_x;
             // KR: the next kernel row reads the source row below (forward) or
             // above (input gradient); offsets wrap modulo 2^32 and are added
             // to the row base before the pointer
             if (KR && kb) off[q] += DG ? 0u - x_row : x_row;
-            flg[q] = (ok ? 1u : 0u) | (uint32_t)kb << 1 | 4u;
+            flg[q] = (ok && row_real ? 1u : 0u) | (uint32_t)kb << 1 | 4u;
         }
     }
     // scale entries: thread e copies entry e; [0, NSA) weight scales
@@ -328,9 +335,13 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
         else
             dma1_async(ok ? (isb ? ssp : wsp) + o : zero, lds_addr(lds + NQ * 4096 + wave * 256));
     };
+    // stages are issued in order 0, 1, 2, ...: (kk, ki) = (st % nkk, st / nkk)
+    // is kept as a counter pair instead of two scalar divisions per stage
+    int iss_kk = 0, iss_ki = 0;
     auto issue = [&](int st, int buf) {
         if constexpr (KR) { issue_rows(st, buf); return; }
-        const int kk = st % nkk, ki = st / nkk;
+        const int kk = iss_kk, ki = iss_ki;
+        if (++iss_kk == nkk) { iss_kk = 0; ++iss_ki; }
         const int kh = f.kh0 + DS * ki;
         const int sy = DG ? yi + f.r0 - ki : yi * p.sh + kh - p.ph;
         const bool row_ok = sy >= 0 && sy < p.hsrc;
@@ -383,9 +394,57 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
     // stage st and frees the buffer of stage st - 1 for the next copy
     const int nbuf = p.nbuf;
     for (int j = 0; j < nbuf - 1 && j < nstage; j++) issue(j, j);
+    // the fused input gradient's z tiles (bf16, 2 KB per output block) are
+    // copied to LDS now, behind the first stages, so the epilogue finds them
+    // there instead of waiting on a load per block; each wave copies the
+    // tiles of its own blocks, so no barrier is needed, and the stage waits
+    // below let the NZ younger copies stay in flight
+    constexpr int NZB = PW * NRB;                   // output blocks of a wave
+    constexpr int NZ = DG && !NV ? 2 * NZB : 0;     // at most this many z copies (1 KB each): zsl per block
+    static_assert(2 * (NQ + 1) + NZ <= 63, "two stages and the z copies must fit the vmcnt counter");
+    const bool zpf = DG && !NV && p.zoff > 0;
+    const int npro = min(nbuf - 1, nstage);         // stages issued before the z copies
+    const int zsl = p.zsl;
+    uint8_t* const zl = smem + p.zoff + wave * (NZB * 1024 * zsl);
+    if (zpf) {
+        const int yz = f.ry + DS * yi;
+#pragma unroll
+        for (int cn = 0; cn < PW; cn++) {
+#pragma unroll
+            for (int rb = 0; rb < NRB; rb++) {
+                const int xi = x0 + PW * wn + cn;
+                const int cb = mt * RBW + NRB * wm + rb;
+                const bool live = xi < f.gw && cb < p.q_ncb;
+                const size_t pix = ((size_t)g * p.hout + yz) * p.wout + (f.rx + DS * (live ? xi : 0));
+                const int rows = min(32, p.M - cb * 32);
+                const uint16_t* zb = (const uint16_t*)p.zpre + (pix * p.M + (size_t)(live ? cb : 0) * 32) * 32;
+                for (int i = 0; i < zsl; i++) {
+                    // LDS slot lane of rows 16 i .. 16 i + 15 holds row 16 i + lane / 4,
+                    // stored chunk lane % 4 = chunk c ^ ((row / 2) % 4) (the layout of bf16_lds)
+                    const int row = 16 * i + (lane >> 2), c = (lane & 3) ^ ((row >> 1) & 3);
+                    const bool ok = live && row < rows;
+                    dma16_async(ok ? (const void*)(zb + row * 32 + c * 8) : (const void*)(zero + lane * 16),
+                                lds_addr(zl + (cn * NRB + rb) * 1024 * zsl + i * 1024));
+                }
+            }
+        }
+    }
     int buf = 0;
     for (int st = 0; st < nstage; st++) {
-        vm_wait_stage<NQ + 1>(min(nbuf - 2, nstage - 1 - st));
+        const int later = min(nbuf - 2, nstage - 1 - st);
+        if (NZ > 0 && zpf && st < npro) {           // the zsl * NZB z copies are younger than this stage
+            if (zsl == 2) {
+                if (later <= 0) vm_wait<NZ>();
+                else if (later == 1) vm_wait<NQ + 1 + NZ>();
+                else vm_wait<2 * (NQ + 1) + NZ>();
+            } else {
+                if (later <= 0) vm_wait<NZ / 2>();
+                else if (later == 1) vm_wait<NQ + 1 + NZ / 2>();
+                else vm_wait<2 * (NQ + 1) + NZ / 2>();
+            }
+        } else {
+            vm_wait_stage<NQ + 1>(later);
+        }
         __syncthreads();
         if (st + nbuf - 1 < nstage) issue(st + nbuf - 1, buf == 0 ? nbuf - 1 : buf - 1);
         const uint8_t* A = smem + buf * p.stage_bytes;
@@ -556,6 +615,7 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
     uint8_t* const ep = smem + wave * 4096;
     const int er = lane >> 3, ec = lane & 7;            // read-back: row er + 8 i, chunk ec
     const int y = f.ry + DS * yi;
+    if (zpf) vm_wait<0>();                               // the z copies (a phase with no taps ran no stage)
     if (p.qcodes) {
         // ---- fused quantizing epilogue: acc[rb][cn] is one whole MX block of
         // the output (32 channels x 32 samples at one pixel); lane l holds
@@ -610,7 +670,19 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                     else        store_block(v, pix, cb);
                 }
                 if (p.fn != MXC_FN_NONE) {
-                    if (DG && p.bf16) {
+                    if (DG && zpf) {
+                        const uint8_t* zt = zl + (cn * NRB + rb) * 1024 * zsl;
+                        const bool zr = r < 16 * zsl;        // rows past the copied slots: padding, z = 0
+#pragma unroll
+                        for (int e4 = 0; e4 < 4; e4++) {
+                            const float4 z = zr ? bf16_unpack4(*(const uint2*)(zt + bf16_lds(r, e4) + 8 * h))
+                                                : make_float4(0.f, 0.f, 0.f, 0.f);
+                            v[4 * e4] *= fn_grad(p.fn, z.x);
+                            v[4 * e4 + 1] *= fn_grad(p.fn, z.y);
+                            v[4 * e4 + 2] *= fn_grad(p.fn, z.z);
+                            v[4 * e4 + 3] *= fn_grad(p.fn, z.w);
+                        }
+                    } else if (DG && p.bf16) {
                         float zz[16];
                         load_bf16_tile(ep4, (const uint16_t*)p.zpre + (pix * p.M + (size_t)cb * 32) * 32, rows, lane, zz);
 #pragma unroll
@@ -807,10 +879,16 @@ __global__ __launch_bounds__(LT) void conv_lean_bwd_kernel(LeanArgs p, WLArgs q,
 
 // LDS bytes of one launch: the stage ring, and at least the 4 x 4 KB the
 // epilogue stages through.
-inline size_t lean_lds(const LeanArgs& a, int nbufs_used) {
+inline size_t lean_ring_lds(const LeanArgs& a, int nbufs_used) {
     const size_t lds = (size_t)nbufs_used * a.stage_bytes;
     const size_t epi = a.qcodes ? 5 * 4096 : 4 * 4096;     // the fused epilogue: codes + fp32 staging
     return lds < epi ? epi : lds;
+}
+// bytes of the prefetched z tiles: 4 waves x (pixels x row blocks per wave)
+// x 1 KB per 16 rows of the layer's rows (at most 32)
+inline size_t lean_z_lds(int pw, int rb, int zsl) { return (size_t)4 * pw * rb * zsl * 1024; }
+inline size_t lean_lds(const LeanArgs& a, int nbufs_used) {
+    return a.zoff > 0 ? (size_t)a.zoff + lean_z_lds(a.zpw, a.zrb, a.zsl) : lean_ring_lds(a, nbufs_used);
 }
 
 // Dynamic LDS above 64 KB needs the kernel's attribute raised, once per
@@ -949,6 +1027,7 @@ int lean_plan(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const 
     a.w_rowblocks = dg ? cv.wt.ncb : cv.wt.np / 32;
     a.w_cp = cv.wt.cp; a.w_ncb = cv.wt.ncb; a.w_nco = cv.wt.np / 32;
     a.x_ncb = src.ncb;
+    a.xrows = src.ncb == 1 ? src.c : 32;
     if (dg && a.w_nco != src.ncb) return 1;
     // rows per tile: the choice that streams the fewest bytes per stage for
     // the same 48 MFMAs -- 64 rows x 8 pixels at column stride 1; at stride 2
@@ -1005,11 +1084,23 @@ int lean_plan(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const 
     // ring depth: the workgroups that share a CU at this grid size split its
     // LDS; each takes as many stage buffers (2..4) as fit in its share
     const int per_cu = (int)((nt + 255) / 256);
+    // the fused input gradient with a bf16 z prefetches its z tiles
+    const bool zpf = dg && q && q->bf16 && q->fn != MXC_FN_NONE && !nv;
+    const int zsl = a.M <= 16 ? 1 : 2;
+    const long zb = zpf ? (long)lean_z_lds(pw, rb, zsl) : 0;
     int nbuf = 2;
     for (int b = 4; b > 2; b--)
-        if ((long)per_cu * b * a.stage_bytes <= LDS_MAX) { nbuf = b; break; }
+        if ((long)per_cu * (b * a.stage_bytes + zb) <= LDS_MAX) { nbuf = b; break; }
     a.nbuf = nbuf;
     const int used = nbuf < nstage ? nbuf : nstage;
+    a.zoff = 0; a.zpw = pw; a.zrb = rb; a.zsl = zsl;
+    if (zpf) {
+        // only where two workgroups still fit a CU's LDS: the kernels hold
+        // two per CU by their registers, and halving that costs more than
+        // the prefetch saves (measured)
+        const size_t ring = lean_ring_lds(a, used);
+        if (ring + lean_z_lds(pw, rb, zsl) <= (size_t)LDS_MAX / 2) a.zoff = (int)ring;
+    }
     P.wgm = wgm; P.pw = pw; P.nstage = nstage; P.used = used; P.dg2 = dg2; P.krow = krow;
     return 0;
 }

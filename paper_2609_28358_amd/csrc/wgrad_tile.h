@@ -8,7 +8,6 @@ namespace {
 
 constexpr int WT = 256;
 
-__device__ __attribute__((aligned(16))) uint8_t g_zero_wl[64];
 
 struct WLArgs {
     const uint8_t* gc;
@@ -19,7 +18,8 @@ struct WLArgs {
     int direct;                    // 1: dst is G_W (OIHW); 0: partial tiles
     int cout, cin, kh, kw, sh, sw, ph, pw, ho, wo, h, w;
     int gy_ncb, x_ncb, gy_cp, x_cp, ntot;
-    int npix, npairs;              // output pixels (all batch groups), pixel pairs
+    int npix, npairs;              // output pixels (all batch groups), pixel pairs (rows x ppr)
+    int ppr;                       // pixel pairs per output row: ceil(wo / 2)
     int cot, cit, ntiles;          // 64-row / 64-column tile counts, tiles
     int ppw;                       // pixel pairs per wave
     int nsplit;
@@ -31,24 +31,36 @@ struct WLArgs {
 };
 
 // One operand's fragment for a K step: K block 0 from pixel row p0, K block
-// 1 from p1 (rows already offset to this lane's row; zero block if invalid).
-// FP8: 16 bytes of each (the lane's half of the row); FP4 and FP6: the whole
-// row of the lane's own K block (ph = p0 or p1 by lane half).
+// 1 from p1 (rows already offset to this lane's row), zeroed where v0 / v1
+// say the block or row does not exist.  FP8: 16 bytes of each (the lane's
+// half of the row); FP4 and FP6: the whole row of the lane's own K block
+// (ph, vh = p0, v0 or p1, v1 by lane half).  Invalid rows still load from a
+// valid address (the caller points them at an existing row) and are zeroed
+// afterwards.  The loads name the global address space explicitly: where
+// the compiler cannot prove it (a per-lane choice between two pointers) it
+// emits flat loads, which also count against the LDS / scalar-load counter,
+// so every later wait on that counter drained the whole batch (measured:
+// the weight gradient of the image layer ran at a quarter of its speed).
+typedef const __attribute__((address_space(1))) v4i g_v4i;
+typedef const __attribute__((address_space(1))) v2i g_v2i;
 template <int F>
-__device__ __forceinline__ v8i row_frag(const uint8_t* p0, const uint8_t* p1, const uint8_t* ph) {
+__device__ __forceinline__ v8i row_frag(const uint8_t* p0, const uint8_t* p1, const uint8_t* ph, bool v0, bool v1,
+                                        bool vh) {
     v8i o;
     if constexpr (F == MXC_E4M3) {
-        const v4i u = *(const v4i*)p0, v = *(const v4i*)p1;
+        const v4i u = *(g_v4i*)p0, v = *(g_v4i*)p1;
 #pragma unroll
-        for (int e = 0; e < 4; e++) { o[e] = u[e]; o[4 + e] = v[e]; }
+        for (int e = 0; e < 4; e++) { o[e] = v0 ? u[e] : 0; o[4 + e] = v1 ? v[e] : 0; }
     } else if constexpr (fmt_bits(F) == 6) {
-        const v2i a = *(const v2i*)ph, b = *(const v2i*)(ph + 8), c = *(const v2i*)(ph + 16);
+        const v2i a = *(g_v2i*)ph, b = *(g_v2i*)(ph + 8), c = *(g_v2i*)(ph + 16);
         o[0] = a[0]; o[1] = a[1]; o[2] = b[0]; o[3] = b[1]; o[4] = c[0]; o[5] = c[1];
         o[6] = o[7] = 0;
-    } else {
-        const v4i u = *(const v4i*)ph;
 #pragma unroll
-        for (int e = 0; e < 4; e++) { o[e] = u[e]; o[4 + e] = 0; }
+        for (int e = 0; e < 6; e++) o[e] = vh ? o[e] : 0;
+    } else {
+        const v4i u = *(g_v4i*)ph;
+#pragma unroll
+        for (int e = 0; e < 4; e++) { o[e] = vh ? u[e] : 0; o[4 + e] = 0; }
     }
     return o;
 }
@@ -85,14 +97,19 @@ __device__ __forceinline__ void wgrad_tile(const WLArgs& p, int bid, int nblk, f
 
     // lane offsets inside one pixel's codes, and block validity
     uint32_t a_off[2], b_off[2];
-    bool a_ok[2], b_ok[2];
+    bool a_ok[2], b_ok[2];      // the block exists
+    bool a_row[2], b_row[2];    // ... and this lane's channel row is real (padding rows hold +0 codes)
 #pragma unroll
     for (int i = 0; i < 2; i++) {
         const int cob = 2 * cop + i, cib = 2 * cip + i;
         a_ok[i] = cob < p.gy_ncb;
         b_ok[i] = cib < p.x_ncb;
-        a_off[i] = (uint32_t)(a_ok[i] ? cob : 0) * TBA + r * RBA + (FA == MXC_E4M3 ? 16 * hf : 0);
-        b_off[i] = (uint32_t)(b_ok[i] ? cib : 0) * TBB + r * RBB + (FB == MXC_E4M3 ? 16 * hf : 0);
+        a_row[i] = a_ok[i] && cob * 32 + r < p.cout;
+        b_row[i] = b_ok[i] && cib * 32 + r < p.cin;
+        // a lane without a real row reads row 0 of its block (or of block 0):
+        // a line the real rows fetch anyway
+        a_off[i] = (uint32_t)(a_ok[i] ? cob : 0) * TBA + (a_row[i] ? r * RBA : 0) + (FA == MXC_E4M3 ? 16 * hf : 0);
+        b_off[i] = (uint32_t)(b_ok[i] ? cib : 0) * TBB + (b_row[i] ? r * RBB : 0) + (FB == MXC_E4M3 ? 16 * hf : 0);
     }
     const uint32_t gy_pix = (uint32_t)p.gy_ncb * TBA, x_pix = (uint32_t)p.x_ncb * TBB;
 
@@ -108,64 +125,100 @@ __device__ __forceinline__ void wgrad_tile(const WLArgs& p, int bid, int nblk, f
     const int q0 = wid * p.ppw;
     const int q1 = min(p.npairs, q0 + p.ppw);
 
-    // operands of pair q (pixels 2q, 2q + 1)
+    // operands of one pair (pixels 2 j and 2 j + 1 of an output row)
     struct Ops {
         v8i a[2], b[2];
         int sa[2], sb[2];
         uint32_t na[2], nb[2];     // NV: the four E4M3 scales of the lane's row
     };
-    auto load = [&](int q, bool live, Ops& o) {
-        int pg[2];                 // pixel index (or -1) of K block 0 / 1
-        int qpix[2];               // tap's input pixel (or -1)
+
+    // Pairs run along output rows: pair pj of row crow = (group, oy) holds
+    // pixels 2 pj and 2 pj + 1 (a row of odd width ends with a half pair).
+    // The wave walks its range with this cursor and per-row bases, so the
+    // per-pair work is a few scalar adds and compares; the lane of half hf
+    // takes pixel 2 pj + hf for FP4 / FP6 (its K block), both for FP8.
+    int crow = q0 / p.ppr, pj = q0 % p.ppr;
+    // per-row state: pixel indices and byte offsets of the row's first G_Y
+    // pixel and of the tap's X row, scale offsets, and whether that X row exists
+    size_t pa_row = 0, px_row = 0, ga_row = 0, xb_row = 0, gs_row = 0, xs_row = 0;
+    bool rv = false;
+    auto set_row = [&]() {
+        const int g = crow / p.ho, oy = crow - g * p.ho;
+        const int iy = oy * p.sh + th - p.ph;
+        rv = iy >= 0 && iy < p.h;
+        pa_row = (size_t)crow * p.wo;
+        px_row = rv ? ((size_t)g * p.h + iy) * p.w : 0;
+        ga_row = pa_row * gy_pix;
+        gs_row = pa_row * p.gy_ncb;
+        xb_row = px_row * x_pix;
+        xs_row = px_row * p.x_ncb;
+    };
+    set_row();
+
+    // pixel 2 pj + k of the cursor's row: validity of G_Y (inside the row and
+    // the wave's range) and of X (also inside the input), and their pixel
+    // offsets within the row bases
+    auto load = [&](bool live, Ops& o) {
+        int oxk[2], ixk[2];
+        bool va[2], vb[2];
 #pragma unroll
         for (int k = 0; k < 2; k++) {
-            const int P = 2 * q + k;
-            pg[k] = live && P < p.npix ? P : -1;
-            qpix[k] = -1;
-            if (pg[k] >= 0) {
-                const int ox = P % p.wo, t = P / p.wo;
-                const int oy = t % p.ho, g = t / p.ho;
-                const int iy = oy * p.sh + th - p.ph, ix = ox * p.sw + tw - p.pw;
-                if (iy >= 0 && iy < p.h && ix >= 0 && ix < p.w) qpix[k] = (g * p.h + iy) * p.w + ix;
-            }
+            const int ox = 2 * pj + k;
+            const int ix = ox * p.sw + tw - p.pw;
+            va[k] = live && ox < p.wo;
+            vb[k] = va[k] && rv && ix >= 0 && ix < p.w;
+            oxk[k] = va[k] ? ox : 0;
+            ixk[k] = vb[k] ? ix : 0;
         }
+        // the lane's own pixel (FP4 / FP6, and the scales of every format)
+        const int oxh = hf ? oxk[1] : oxk[0], ixh = hf ? ixk[1] : ixk[0];
+        const bool vah = hf ? va[1] : va[0], vbh = hf ? vb[1] : vb[0];
+        const uint8_t* const gr = p.gc + ga_row;
+        const uint8_t* const xr = p.xc + xb_row;
 #pragma unroll
         for (int i = 0; i < NB; i++) {
-            const uint8_t* ap[2];
-            const uint8_t* bp[2];
-#pragma unroll
-            for (int k = 0; k < 2; k++) {
-                ap[k] = (pg[k] >= 0 && a_ok[i]) ? p.gc + (size_t)pg[k] * gy_pix + a_off[i] : g_zero_wl;
-                bp[k] = (qpix[k] >= 0 && b_ok[i]) ? p.xc + (size_t)qpix[k] * x_pix + b_off[i] : g_zero_wl;
-            }
-            o.a[i] = row_frag<FA>(ap[0], ap[1], ap[hf]);
-            o.b[i] = row_frag<FB>(bp[0], bp[1], bp[hf]);
+            const uint8_t* a0 = gr + (uint32_t)oxk[0] * gy_pix + a_off[i];
+            const uint8_t* a1 = gr + (uint32_t)oxk[1] * gy_pix + a_off[i];
+            const uint8_t* ah = gr + (uint32_t)oxh * gy_pix + a_off[i];
+            const uint8_t* b0 = xr + (uint32_t)ixk[0] * x_pix + b_off[i];
+            const uint8_t* b1 = xr + (uint32_t)ixk[1] * x_pix + b_off[i];
+            const uint8_t* bh = xr + (uint32_t)ixh * x_pix + b_off[i];
+            o.a[i] = row_frag<FA>(a0, a1, ah, va[0] && a_row[i], va[1] && a_row[i], vah && a_row[i]);
+            o.b[i] = row_frag<FB>(b0, b1, bh, vb[0] && b_row[i], vb[1] && b_row[i], vbh && b_row[i]);
             // scale of (row, K block hf): the pixel of this lane's half
-            const int P = pg[hf], Q = qpix[hf];
             const int cob = 2 * cop + i, cib = 2 * cip + i;
-            const uint8_t sa = p.gs[(P >= 0 && a_ok[i]) ? (size_t)P * p.gy_ncb + cob : 0];
-            const uint8_t sb = p.xs[(Q >= 0 && b_ok[i]) ? (size_t)Q * p.x_ncb + cib : 0];
-            o.sa[i] = (P >= 0 && a_ok[i]) ? sa : 0;
-            o.sb[i] = (Q >= 0 && b_ok[i]) ? sb : 0;
+            const bool sav = vah && a_ok[i], sbv = vbh && b_ok[i];
+            const uint8_t sa = p.gs[gs_row + (uint32_t)oxh * p.gy_ncb + (a_ok[i] ? cob : 0)];
+            const uint8_t sb = p.xs[xs_row + (uint32_t)ixh * p.x_ncb + (b_ok[i] ? cib : 0)];
+            o.sa[i] = sav ? sa : 0;
+            o.sb[i] = sbv ? sb : 0;
             if constexpr (NV) {
                 const uint32_t* ga = (const uint32_t*)p.gs;
                 const uint32_t* xa = (const uint32_t*)p.xs;
-                const uint32_t va = ga[(P >= 0 && a_ok[i]) ? ((size_t)P * (p.gy_cp / 8) + cob * 4 + (r >> 3)) : 0];
-                const uint32_t vb = xa[(Q >= 0 && b_ok[i]) ? ((size_t)Q * (p.x_cp / 8) + cib * 4 + (r >> 3)) : 0];
-                o.na[i] = (P >= 0 && a_ok[i]) ? va : 0u;
-                o.nb[i] = (Q >= 0 && b_ok[i]) ? vb : 0u;
+                const size_t pa = pa_row + oxh, px = px_row + ixh;
+                const uint32_t va4 = ga[pa * (p.gy_cp / 8) + (a_ok[i] ? cob : 0) * 4 + (r >> 3)];
+                const uint32_t vb4 = xa[px * (p.x_cp / 8) + (b_ok[i] ? cib : 0) * 4 + (r >> 3)];
+                o.na[i] = sav ? va4 : 0u;
+                o.nb[i] = sbv ? vb4 : 0u;
             }
         }
     };
 
     // batches of PB pairs: all loads of a batch are in flight together (the
     // loop is bound by memory latency, not by the MFMAs); pairs past the
-    // wave's range get a zero G_Y operand and add nothing
+    // wave's range get zero operands and add nothing
     constexpr int PB = NV ? 2 : NB == 1 ? 8 : 4;
     for (int q = q0; q < q1; q += PB) {
         Ops o[PB];
 #pragma unroll
-        for (int b = 0; b < PB; b++) load(q + b, q + b < q1, o[b]);
+        for (int b = 0; b < PB; b++) {
+            load(q + b < q1, o[b]);
+            if (++pj == p.ppr) {                      // next output row
+                pj = 0;
+                ++crow;
+                if (q + b + 1 < q1) set_row();
+            }
+        }
 #pragma unroll
         for (int b = 0; b < PB; b++) {
             if constexpr (NV) {
@@ -249,7 +302,8 @@ inline long wgrad_lean_fill(const Conv& cv, const void* gc, const uint8_t* gs, c
     a.gy_ncb = cv.gy.ncb; a.x_ncb = cv.x.ncb; a.gy_cp = cv.gy.cp; a.x_cp = cv.x.cp;
     a.ntot = cv.kh * cv.kw * cv.x.cp;
     a.npix = cv.x.ng * cv.ho * cv.wo;
-    a.npairs = (a.npix + 1) / 2;
+    a.ppr = (cv.wo + 1) / 2;
+    a.npairs = cv.x.ng * cv.ho * a.ppr;
     a.cot = (cv.gy.ncb + 1) / 2; a.cit = (cv.x.ncb + 1) / 2;
     a.ntiles = cv.kh * cv.kw * a.cot * a.cit;
     const int waves = splits * 4;
