@@ -291,6 +291,26 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
         if (KR && kb) s_off += DG ? 0u - (uint32_t)p.wsrc * p.x_ncb : (uint32_t)p.wsrc * p.x_ncb;
         s_flg = (ok ? 1u : 0u) | (uint32_t)kb << 1 | 4u | 8u;
     }
+    // Which per-stage condition a lane's copy needs, as bits to test against
+    // the stage's mask: a copy is issued from memory when the test passes,
+    // else from the zero block.  Bitwise tests keep the copies free of the
+    // branches that short-circuit conditions compile to.
+    //   KR (mask: 1 row 0 in range, 2 row 1 in range, 4 always, 8 row 1
+    //   exists): activation copies need 1 or 2, weight copies 4 or 8; any
+    //   bit passes.
+    //   otherwise (mask: 1 always, 2 second K block exists, 4 row in range):
+    //   every needed bit must pass.
+    // A lane whose copy is never valid needs bit 16, which no mask has.
+    auto need_of = [&](uint32_t fl) -> uint32_t {
+        if (!(fl & 1u)) return 16u;
+        const bool isb = fl & 4u, k1 = fl & 2u;
+        if (KR) return isb ? (k1 ? 2u : 1u) : (k1 ? 8u : 4u);
+        return 1u | (k1 ? 2u : 0u) | (isb ? 4u : 0u);
+    };
+    uint32_t need[NQ];
+#pragma unroll
+    for (int q = 0; q < NQ; q++) need[q] = need_of(flg[q]);
+    const uint32_t s_need = (s_flg & 8u) ? need_of(s_flg) : 16u;
 
     // stages: (kernel row, pair of 32-channel K blocks), or with krow (a
     // single K block) pairs of kernel rows, the K halves of a stage holding
@@ -319,16 +339,16 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
         const uint32_t row = (uint32_t)g * p.hsrc + (uint32_t)sy0;   // may wrap: only used where valid
         const uint32_t xrow = row * x_row;
         const uint8_t* lds = smem + buf * p.stage_bytes;
+        const uint32_t okm = (ok0 ? 1u : 0u) | (ok1 ? 2u : 0u) | 4u | (has1 ? 8u : 0u);
 #pragma unroll
         for (int q = 0; q < NQ; q++) {
-            const uint32_t f = flg[q];
-            const bool isb = f & 4u, k1 = f & 2u;
-            const bool ok = (f & 1u) && (isb ? (k1 ? ok1 : ok0) : (!k1 || has1));
+            const bool isb = flg[q] & 4u;
+            const bool ok = (okm & need[q]) != 0u;
             const uint8_t* src = isb ? p.sc + (xrow + off[q]) : abase + off[q];
             dma16_async(ok ? src : zero + (isb ? in_x : in_w), lds_addr(lds + (4 * q + wave) * 1024));
         }
-        const bool isb = s_flg & 4u, k1 = s_flg & 2u;
-        const bool ok = (s_flg & 8u) && (s_flg & 1u) && (isb ? (k1 ? ok1 : ok0) : (!k1 || has1));
+        const bool isb = s_flg & 4u;
+        const bool ok = (okm & s_need) != 0u;
         const uint32_t o = isb ? s_off + row * p.wsrc * p.x_ncb : s_off + (uint32_t)kh0 * p.kwf * p.w_ncb;
         if constexpr (NV)
             dma16_async(ok ? (isb ? ssp : wsp) + 16 * o : zero, lds_addr(lds + NQ * 4096 + wave * 1024));
@@ -350,16 +370,16 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                                (uint32_t)kh * p.kwf * w_tap;
         const uint8_t* bbase = p.sc + ((uint32_t)g * p.hsrc + (row_ok ? sy : 0)) * x_row + (uint32_t)(2 * kk) * TBX;
         const uint8_t* lds = smem + buf * p.stage_bytes;
+        const uint32_t okm = 1u | (kb1_ok ? 2u : 0u) | (row_ok ? 4u : 0u);
 #pragma unroll
         for (int q = 0; q < NQ; q++) {
-            const uint32_t f = flg[q];
-            const bool isb = f & 4u;
-            const bool ok = (f & 1u) && (!(f & 2u) || kb1_ok) && (!isb || row_ok);
+            const bool isb = flg[q] & 4u;
+            const bool ok = (okm & need[q]) == need[q];
             const uint8_t* src = (isb ? bbase : abase) + off[q];
             dma16_async(ok ? src : zero + (isb ? in_x : in_w), lds_addr(lds + (4 * q + wave) * 1024));
         }
         const bool isb = s_flg & 4u;
-        const bool ok = (s_flg & 8u) && (s_flg & 1u) && (!(s_flg & 2u) || kb1_ok) && (!isb || row_ok);
+        const bool ok = (okm & s_need) == s_need;
         const uint32_t o = isb ? s_off + ((uint32_t)g * p.hsrc + (row_ok ? sy : 0)) * p.wsrc * p.x_ncb + 2 * kk
                                : s_off + (uint32_t)kh * p.kwf * p.w_ncb +
                                      (DG ? (uint32_t)(2 * kk) * p.kh * p.kwf * p.w_ncb : (uint32_t)(2 * kk));
