@@ -166,6 +166,102 @@ __global__ __launch_bounds__(256) void quantize_sum_kernel(SumArgs a, uint8_t* _
     }
 }
 
+// bf16 terms and z: the same sums with 16-byte loads.  Lane l takes channels
+// 16 hh + l / 4 (hh = 0, 1) of the block and samples 8 (l % 4) .. + 7 (eight
+// bf16 = 16 bytes per load, half the load instructions of the layout above),
+// and writes their codes as one 4-byte (FP4) or 8-byte (FP8) piece: each
+// store instruction of the wave covers 16 whole channel rows.
+__device__ __forceinline__ void bf16x8(uint4 u, float* f) {
+    const float4 a = bf16_unpack4(make_uint2(u.x, u.y)), b = bf16_unpack4(make_uint2(u.z, u.w));
+    f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w; f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;
+}
+__device__ __forceinline__ uint4 load16_nt(const uint16_t* p) {   // 16 bytes, bits only
+    const float4 f = load_nt((const float*)p);
+    return make_uint4(__float_as_uint(f.x), __float_as_uint(f.y), __float_as_uint(f.z), __float_as_uint(f.w));
+}
+
+template <int FMT>
+__global__ __launch_bounds__(256) void quantize_sum_bf_kernel(SumArgs a, uint8_t* __restrict__ codes,
+                                                              uint8_t* __restrict__ scales, long long nblocks) {
+    const long long blk = (long long)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (blk >= nblocks) return;
+    const int lane = threadIdx.x & 63;
+    const int cb = (int)(blk % a.ncb);
+    const long long pix = blk / a.ncb;                     // (group, y, x)
+    const int x = (int)(pix % a.w);
+    const long long gy = pix / a.w;
+    const int y = (int)(gy % a.h);
+    const long long g = gy / a.h;
+    const int j = 8 * (lane & 3);
+    const int hs = 2 * a.h, ws = 2 * a.w;
+    const size_t r0 = ((size_t)g * hs + 2 * y) * ws + 2 * x, r1 = r0 + ws;   // a 2x2 source patch (down)
+    float v[2][8];
+#pragma unroll
+    for (int hh = 0; hh < 2; hh++) {
+        const int ch = cb * 32 + 16 * hh + (lane >> 2);
+#pragma unroll
+        for (int e = 0; e < 8; e++) v[hh][e] = 0.0f;
+        if (ch >= a.c) continue;
+        for (int t = 0; t < a.nterms; t++) {
+            const uint16_t* src = (const uint16_t*)a.src[t];
+            const int cs = a.c_src[t], col = a.c_off[t] + ch;
+            float u[8];
+            if (!a.down[t]) {
+                bf16x8(load16_nt(src + ((size_t)pix * cs + col) * 32 + j), u);
+            } else {
+                float p0[8], p1[8], p2[8], p3[8];
+                bf16x8(load16_nt(src + (r0 * cs + col) * 32 + j), p0);
+                bf16x8(load16_nt(src + ((r0 + 1) * cs + col) * 32 + j), p1);
+                bf16x8(load16_nt(src + (r1 * cs + col) * 32 + j), p2);
+                bf16x8(load16_nt(src + ((r1 + 1) * cs + col) * 32 + j), p3);
+#pragma unroll
+                for (int e = 0; e < 8; e++) u[e] = (p0[e] + p1[e]) + (p2[e] + p3[e]);
+            }
+            if (t == 0) {
+#pragma unroll
+                for (int e = 0; e < 8; e++) v[hh][e] = u[e];
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; e++) v[hh][e] += u[e];
+            }
+        }
+        if (a.fn != MXC_FN_NONE) {
+            float z[8];
+            bf16x8(load16_nt((const uint16_t*)a.z + ((size_t)pix * a.c + ch) * 32 + j), z);
+#pragma unroll
+            for (int e = 0; e < 8; e++) v[hh][e] *= fn_grad(a.fn, z[e]);
+        }
+        if (a.vals) {
+            float* o = a.vals + ((size_t)pix * a.c + ch) * 32 + j;
+            store_nt(o, make_float4(v[hh][0], v[hh][1], v[hh][2], v[hh][3]));
+            store_nt(o + 4, make_float4(v[hh][4], v[hh][5], v[hh][6], v[hh][7]));
+        }
+    }
+    uint32_t m = 0;
+#pragma unroll
+    for (int hh = 0; hh < 2; hh++)
+#pragma unroll
+        for (int e = 0; e < 8; e++) m = max(m, __float_as_uint(v[hh][e]) & 0x7FFFFFFFu);
+    m = wave_max_u32(m);
+    const uint32_t sc = scale_code_from_bits<fmt_emax(FMT)>(m);
+    if (lane == 0) scales[blk] = (uint8_t)sc;
+    const float inv = inv_scale(sc);
+    const bool bad = sc == 0xFFu;
+#pragma unroll
+    for (int hh = 0; hh < 2; hh++) {
+        const float4 lo = make_float4(v[hh][0], v[hh][1], v[hh][2], v[hh][3]);
+        const float4 hi = make_float4(v[hh][4], v[hh][5], v[hh][6], v[hh][7]);
+        const int row = 16 * hh + (lane >> 2);
+        if constexpr (FMT == MXC_E4M3) {
+            const uint2 c = bad ? make_uint2(0u, 0u) : make_uint2(pack4_e4m3(lo, inv), pack4_e4m3(hi, inv));
+            *(uint2*)(codes + (size_t)blk * 1024 + row * 32 + j) = c;
+        } else {
+            const uint32_t c = bad ? 0u : ((uint32_t)pack4_e2m1(lo, inv) | (uint32_t)pack4_e2m1(hi, inv) << 16);
+            *(uint32_t*)(codes + (size_t)blk * 512 + row * 16 + j / 2) = c;
+        }
+    }
+}
+
 }  // namespace
 
 int launch_concat(const Geom& dst, const mxc_part* parts, int nparts, void* codes, uint8_t* scales,
@@ -214,10 +310,10 @@ int launch_quantize_sum(const Geom& dst, int fmt, const mxc_term* terms, int nte
     const dim3 gd((unsigned)grid);
     uint8_t* const cd = (uint8_t*)codes;
     if (fmt == MXC_E4M3) {
-        if (bf16) hipLaunchKernelGGL((quantize_sum_kernel<MXC_E4M3, true>), gd, dim3(256), 0, s, a, cd, scales, nblocks);
+        if (bf16) hipLaunchKernelGGL((quantize_sum_bf_kernel<MXC_E4M3>), gd, dim3(256), 0, s, a, cd, scales, nblocks);
         else      hipLaunchKernelGGL((quantize_sum_kernel<MXC_E4M3, false>), gd, dim3(256), 0, s, a, cd, scales, nblocks);
     } else {
-        if (bf16) hipLaunchKernelGGL((quantize_sum_kernel<MXC_E2M1, true>), gd, dim3(256), 0, s, a, cd, scales, nblocks);
+        if (bf16) hipLaunchKernelGGL((quantize_sum_bf_kernel<MXC_E2M1>), gd, dim3(256), 0, s, a, cd, scales, nblocks);
         else      hipLaunchKernelGGL((quantize_sum_kernel<MXC_E2M1, false>), gd, dim3(256), 0, s, a, cd, scales, nblocks);
     }
     return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
