@@ -588,47 +588,92 @@ __global__ __launch_bounds__(NT) void wgrad_kernel(WgradArgs p) {
 }
 
 // G_W[co][ci][kh][kw] = sum over splits of the partial (co, tap*Cin_p + ci).
-// A workgroup takes 256 consecutive partial columns, a thread one column.
-// The thread keeps four sums, sum q adding splits q, q + 4, q + 8, ... in
-// increasing order, and returns (sum0 + sum1) + (sum2 + sum3): a fixed order,
-// so the result does not depend on timing, and the same bits whether one
-// layer or several are reduced by the launch.
+// Below 64 splits a thread takes a column and keeps four sums, sum q adding
+// splits q, q + 4, q + 8, ... in increasing order, and returns (sum0 + sum1)
+// + (sum2 + sum3).  From 64 splits on (the first layers: few columns, many
+// splits, where a thread per column left most of the GPU idle behind long
+// load chains) sixteen threads share a column: thread q adds splits q, q +
+// 16, ... in increasing order and the column's result is the pairwise tree
+// ((s0 + s1) + (s2 + s3)) + ... of the sixteen.  Either way a fixed order:
+// the result does not depend on timing, and the same bits whether one layer
+// or several are reduced by the launch.  A workgroup takes 256 / nr
+// consecutive columns (nr = 1 or 16); neighbouring threads read
+// neighbouring columns of one split.
 struct RedGeom {
-    int cout, cin, kh, kw, gy_cp, x_cp, ntot, splits;
+    int cout, cin, kh, kw, gy_cp, x_cp, ntot, splits, nr;
 };
 
-__device__ __forceinline__ void reduce_cols(const float* __restrict__ part, float* __restrict__ gw,
-                                            const RedGeom& r, long wg) {
-    const long i = wg * 256 + threadIdx.x;
-    if (i >= (long)r.cout * r.ntot) return;
+inline int reduce_nr(int splits) { return splits >= 64 ? 16 : 1; }
+
+__device__ __forceinline__ void reduce_store(float* __restrict__ gw, const RedGeom& r, long i, float sum) {
     const int co = (int)(i / r.ntot), col = (int)(i % r.ntot);
-    const size_t stride = (size_t)r.gy_cp * r.ntot;
-    const float* q = part + (size_t)co * r.ntot + col;
-    float a[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-    int k = 0;
-    for (; k + 8 <= r.splits; k += 8) {                 // eight loads in flight
-        float v[8];
-#pragma unroll
-        for (int j = 0; j < 8; j++) v[j] = __ldg(q + (size_t)(k + j) * stride);
-#pragma unroll
-        for (int j = 0; j < 8; j++) a[j & 3] += v[j];
-    }
-    for (; k < r.splits; k++) a[k & 3] += __ldg(q + (size_t)k * stride);
-    const float sum = (a[0] + a[1]) + (a[2] + a[3]);
     const int tap = col / r.x_cp, ci = col % r.x_cp;
     if (ci < r.cin)
         gw[(((size_t)co * r.cin + ci) * r.kh + tap / r.kw) * r.kw + tap % r.kw] = sum;
 }
 
+__device__ __forceinline__ void reduce_cols(const float* __restrict__ part, float* __restrict__ gw,
+                                            const RedGeom& r, long wg) {
+    const size_t stride = (size_t)r.gy_cp * r.ntot;
+    if (r.nr == 1) {
+        const long i = wg * 256 + threadIdx.x;
+        if (i >= (long)r.cout * r.ntot) return;
+        const float* q = part + (size_t)(i / r.ntot) * r.ntot + (i % r.ntot);
+        float a[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+        int k = 0;
+        for (; k + 8 <= r.splits; k += 8) {                 // eight loads in flight
+            float v[8];
+#pragma unroll
+            for (int j = 0; j < 8; j++) v[j] = __ldg(q + (size_t)(k + j) * stride);
+#pragma unroll
+            for (int j = 0; j < 8; j++) a[j & 3] += v[j];
+        }
+        for (; k < r.splits; k++) a[k & 3] += __ldg(q + (size_t)k * stride);
+        reduce_store(gw, r, i, (a[0] + a[1]) + (a[2] + a[3]));
+        return;
+    }
+    __shared__ float red[256];
+    constexpr int NR = 16, PER = 256 / NR;
+    const int t = threadIdx.x, qi = t / PER, cl = t % PER;
+    const long i = wg * PER + cl;
+    const bool live = i < (long)r.cout * r.ntot;
+    float a = 0.0f;
+    if (live) {
+        const float* q = part + (size_t)(i / r.ntot) * r.ntot + (i % r.ntot);
+        int k = qi;
+        for (; k + 7 * NR < r.splits; k += 8 * NR) {        // eight loads in flight
+            float v[8];
+#pragma unroll
+            for (int j = 0; j < 8; j++) v[j] = __ldg(q + (size_t)(k + j * NR) * stride);
+#pragma unroll
+            for (int j = 0; j < 8; j++) a += v[j];
+        }
+        for (; k < r.splits; k += NR) a += __ldg(q + (size_t)k * stride);
+    }
+    red[t] = a;
+    __syncthreads();
+    if (qi != 0 || !live) return;
+    float s[NR];
+#pragma unroll
+    for (int j = 0; j < NR; j++) s[j] = red[j * PER + cl];
+#pragma unroll
+    for (int w = 1; w < NR; w *= 2)                         // pairwise tree
+#pragma unroll
+        for (int j = 0; j + w < NR; j += 2 * w) s[j] = s[j] + s[j + w];
+    reduce_store(gw, r, i, s[0]);
+}
+
 // workgroups of one reduction
-long reduce_wgs(const Conv& cv, int) {
-    return ((long)cv.cout * cv.kh * cv.kw * cv.x.cp + 255) / 256;
+long reduce_wgs(const Conv& cv, int splits) {
+    const long per = 256 / reduce_nr(splits);
+    return ((long)cv.cout * cv.kh * cv.kw * cv.x.cp + per - 1) / per;
 }
 
 RedGeom red_geom(const Conv& cv, int splits) {
     RedGeom r;
     r.cout = cv.cout; r.cin = cv.cin; r.kh = cv.kh; r.kw = cv.kw;
     r.gy_cp = cv.gy.cp; r.x_cp = cv.x.cp; r.ntot = cv.kh * cv.kw * cv.x.cp; r.splits = splits;
+    r.nr = reduce_nr(splits);
     return r;
 }
 
@@ -638,7 +683,7 @@ __global__ __launch_bounds__(256) void wgrad_reduce(const float* __restrict__ pa
 }
 
 // Several layers' reductions in one launch: the workgroups of job i take
-// [wg0_i, wg0_i + (cout_i ntot_i + 63) / 64); the job is picked with scalar
+// [wg0_i, wg0_i + reduce_wgs(job i)); the job is picked with scalar
 // selects, as in the batched quantizer.
 struct RJob {
     const float* part;
