@@ -519,6 +519,19 @@ int mxconv_dgrad_quant(const mxc_conv* cv, int fmt,
                        const void* gy_codes, const uint8_t* gy_scales,
                        int fn, const void* z, int out_fmt,
                        void* gx_codes, uint8_t* gx_scales, float* gx_act, void* stream);
+/* mxconv_dgrad_quant with the gradient's element codes rounded
+ * stochastically (Sec. III-A rounds gradients stochastically; Eq. (6)):
+ * the scales, the fp32 values (gx_act) and every other argument as
+ * mxconv_dgrad_quant; each code is the rule of mxconv_quantize_sr applied to
+ * the value gx_act receives, with the random bits of its linear position in
+ * the gx_codes array under `seed` -- so the codes equal mxconv_quantize_sr of
+ * gx_act (CBF, role MXC_ACT) with the same seed.
+ * Errors: as mxconv_dgrad_quant. */
+int mxconv_dgrad_quant_sr(const mxc_conv* cv, int fmt,
+                          const void* w_codes, const uint8_t* w_scales,
+                          const void* gy_codes, const uint8_t* gy_scales,
+                          int fn, const void* z, int out_fmt,
+                          void* gx_codes, uint8_t* gx_scales, float* gx_act, uint64_t seed, void* stream);
 
 /* ------------------------------------------------------------------ no allocation */
 /* mxconv_wgrad for callers that cannot allocate device memory: code under
@@ -603,6 +616,15 @@ typedef struct {
 } mxc_term;
 int mxconv_quantize_sum(int fmt, int n, int c, int h, int w, int nterms, const mxc_term* terms,
                         int fn, const void* z, void* codes, uint8_t* scales, float* vals, void* stream);
+/* mxconv_quantize_sum with stochastic rounding of the gradient's elements
+ * (Sec. III-A; Eq. (6)): the same sum, product, scales and vals; each code is
+ * the rule of mxconv_quantize_sr applied to the value vals receives, keyed by
+ * its linear position in the code array under `seed` (so the codes equal
+ * mxconv_quantize_sr of vals, CBF, role MXC_ACT, with the same seed).
+ * Errors: as mxconv_quantize_sum. */
+int mxconv_quantize_sum_sr(int fmt, int n, int c, int h, int w, int nterms, const mxc_term* terms,
+                           int fn, const void* z, void* codes, uint8_t* scales, float* vals, uint64_t seed,
+                           void* stream);
 
 /* Human-readable text for a return code (static storage). */
 const char* mxconv_strerror(int code);

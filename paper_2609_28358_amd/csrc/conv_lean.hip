@@ -88,6 +88,8 @@ struct LeanArgs {
     int zpw, zrb;             // (host) the tile shape the z region is sized for
     int zsl;                  // 1 KB slots of 16 rows per z tile: 1 if the layer has at most 16 rows, else 2
     const void* zpre;
+    int sr;                   // fused epilogue: codes by stochastic rounding, generator key (sk0, sk1)
+    uint32_t sk0, sk1;
     // NVFP4 operands (the NV kernels): per-tensor scales of W and the source;
     // the scale arrays ws / ss then hold E4M3 scales per 8x8 block, the 16 of
     // one 32-row block in 16 consecutive bytes
@@ -734,18 +736,50 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                 const float inv = inv_scale(sc);
                 const bool bad = sc == 0xFFu;
                 if (lane == 0) p.qscales[pix * p.q_ncb + cb] = (uint8_t)sc;
-                if (q6) {
-                    // the lane's four runs of four samples: 16 codes in 96 bits,
-                    // run e4 (samples 8 e4 + 4 h ..) in bits 24 e4 .. 24 e4 + 23,
-                    // stored at byte 6 e4 + 3 h of the channel's 24-byte row
+                // the lane's 16 codes: run e4 (samples 8 e4 + 4 h .. + 3) in
+                // bits [nb * 4 e4, nb * 4 (e4 + 1)) of run[e4]
+                uint32_t run[4];
+                if (DG && p.sr) {
+                    // stochastic rounding (gradients): the code of (channel r,
+                    // sample n) sits at position (pix q_ncb + cb) 1024 + 32 r + n
+                    // of the code tensor, which keys its random half-word
+                    const int s = (int)sc - 127;
+                    const uint64_t q0 = (((uint64_t)pix * p.q_ncb + cb) * 1024 + 32 * r) >> 3;
+                    const int nb = q8 ? 8 : q6 ? 6 : 4;
+#pragma unroll
+                    for (int e4 = 0; e4 < 4; e4++) {
+                        const uint4 w = sr_words(q0 + e4, p.sk0, p.sk1);
+                        const uint32_t w0 = h ? w.z : w.x, w1 = h ? w.w : w.y;
+                        const uint32_t rr[4] = {w0 & 0xFFFFu, w0 >> 16, w1 & 0xFFFFu, w1 >> 16};
+                        uint32_t u = 0u;
+#pragma unroll
+                        for (int t = 0; t < 4; t++)
+                            u |= encode_sr_rt(p.qfmt, v[4 * e4 + t], s, inv, rr[t]) << (nb * t);
+                        run[e4] = bad ? 0u : u;
+                    }
+                } else if (q6) {
                     float4 xv[4];
 #pragma unroll
                     for (int e4 = 0; e4 < 4; e4++) xv[e4] = make_float4(v[4 * e4], v[4 * e4 + 1], v[4 * e4 + 2], v[4 * e4 + 3]);
                     const v6i w = p.qfmt == MXC_E2M3 ? pack16_fp6<MXC_E2M3>(xv, inv) : pack16_fp6<MXC_E3M2>(xv, inv);
                     const uint32_t w0 = bad ? 0u : (uint32_t)w[0], w1 = bad ? 0u : (uint32_t)w[1],
                                    w2 = bad ? 0u : (uint32_t)w[2];
-                    const uint32_t run[4] = {w0 & 0xFFFFFFu, (w0 >> 24) | ((w1 & 0xFFFFu) << 8),
-                                             (w1 >> 16) | ((w2 & 0xFFu) << 16), w2 >> 8};
+                    run[0] = w0 & 0xFFFFFFu;
+                    run[1] = (w0 >> 24) | ((w1 & 0xFFFFu) << 8);
+                    run[2] = (w1 >> 16) | ((w2 & 0xFFu) << 16);
+                    run[3] = w2 >> 8;
+                } else if (q8) {
+#pragma unroll
+                    for (int e4 = 0; e4 < 4; e4++)
+                        run[e4] = bad ? 0u : pack4_e4m3(make_float4(v[4 * e4], v[4 * e4 + 1], v[4 * e4 + 2], v[4 * e4 + 3]), inv);
+                } else {
+#pragma unroll
+                    for (int e4 = 0; e4 < 4; e4++)
+                        run[e4] = bad ? 0u
+                                      : pack4_e2m1(make_float4(v[4 * e4], v[4 * e4 + 1], v[4 * e4 + 2], v[4 * e4 + 3]), inv);
+                }
+                if (q6) {
+                    // 24 bits per run, stored at byte 6 e4 + 3 h of the channel's 24-byte row
 #pragma unroll
                     for (int e4 = 0; e4 < 4; e4++) {
                         uint8_t* d = ep + r * 24 + 6 * e4 + 3 * h;
@@ -759,19 +793,14 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                     }
                 } else if (q8) {
 #pragma unroll
-                    for (int e4 = 0; e4 < 4; e4++)
-                        *(uint32_t*)(ep + r * 32 + 8 * e4 + 4 * h) =
-                            bad ? 0u : pack4_e4m3(make_float4(v[4 * e4], v[4 * e4 + 1], v[4 * e4 + 2], v[4 * e4 + 3]), inv);
-                    const uint4 run = *(const uint4*)(ep + lane * 16);
-                    *(uint4*)(p.qcodes + (pix * p.q_ncb + cb) * 1024 + lane * 16) = run;
+                    for (int e4 = 0; e4 < 4; e4++) *(uint32_t*)(ep + r * 32 + 8 * e4 + 4 * h) = run[e4];
+                    const uint4 chunk = *(const uint4*)(ep + lane * 16);
+                    *(uint4*)(p.qcodes + (pix * p.q_ncb + cb) * 1024 + lane * 16) = chunk;
                 } else {
 #pragma unroll
-                    for (int e4 = 0; e4 < 4; e4++)
-                        *(unsigned short*)(ep + r * 16 + 4 * e4 + 2 * h) =
-                            bad ? (unsigned short)0
-                                : pack4_e2m1(make_float4(v[4 * e4], v[4 * e4 + 1], v[4 * e4 + 2], v[4 * e4 + 3]), inv);
-                    const uint2 run = *(const uint2*)(ep + lane * 8);
-                    *(uint2*)(p.qcodes + (pix * p.q_ncb + cb) * 512 + lane * 8) = run;
+                    for (int e4 = 0; e4 < 4; e4++) *(unsigned short*)(ep + r * 16 + 4 * e4 + 2 * h) = (unsigned short)run[e4];
+                    const uint2 chunk = *(const uint2*)(ep + lane * 8);
+                    *(uint2*)(p.qcodes + (pix * p.q_ncb + cb) * 512 + lane * 8) = chunk;
                 }
             }
         }
@@ -1036,6 +1065,9 @@ int lean_plan(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const 
     a.pre_out = q && q->pre ? 1 : 0;
     a.bf16 = q && q->bf16 ? 1 : 0;
     a.zpre = q ? q->z : nullptr;
+    a.sr = q && q->sr ? 1 : 0;
+    a.sk0 = q ? (uint32_t)q->seed : 0u;
+    a.sk1 = q ? (uint32_t)(q->seed >> 32) : 0u;
     a.tw = nv_tw; a.tx = nv_tx;
     const Geom& src = dg ? cv.gy : cv.x;
     a.hsrc = src.h; a.wsrc = src.w;

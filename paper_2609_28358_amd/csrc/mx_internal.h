@@ -92,6 +92,8 @@ struct FusedEpi {
     const void* z;       // fp32 CBF, or bf16 CBF with bf16
     bool pre;            // forward: the output gets the values before fn
     bool bf16;           // round the GEMM result to bf16 first; z and the pre output are bf16
+    bool sr = false;     // codes by stochastic rounding (Philox4x32-10 keyed by seed, by code position)
+    uint64_t seed = 0;
 };
 // fwd / dgrad for batch block 32 and kernel width 1 or 3 (conv_lean.hip);
 // returns 1 when the layer is outside those shapes.  With q, the output is
@@ -141,7 +143,8 @@ int launch_wgrad_reduce_multi(int count, const WReduceJob* jobs, hipStream_t s);
 int launch_concat(const Geom& dst, const mxc_part* parts, int nparts, void* codes, uint8_t* scales,
                   hipStream_t s);
 int launch_quantize_sum(const Geom& dst, int fmt, const mxc_term* terms, int nterms, int fn, bool bf16, const void* z,
-                        void* codes, uint8_t* scales, float* vals, hipStream_t s);
+                        void* codes, uint8_t* scales, float* vals, hipStream_t s, bool sr = false,
+                        uint64_t seed = 0);
 
 // naive comparator (naive.hip): a line matrix stores each 1-D-blocked line
 // zero-padded to a multiple of 64 elements (one K step of the MFMA)
@@ -350,10 +353,12 @@ template <> struct FmtSR<MXC_E3M2> { static constexpr int MB = 2, BIAS = 3; stat
 // with D = M mod 2^k, and r < frac * 2^16 <=> r < ceil(D 2^(16 - k)).
 // k >= 13 for every block scale; M < 2^24, so shifts are capped at 24.
 // Written without branches: every lane takes the same path.
-template <int FMT>
-__device__ __forceinline__ uint32_t encode_sr(float x, int s, float inv, uint32_t r) {
-    typedef FmtSR<FMT> F;
-    constexpr int MB = F::MB, BIAS = F::BIAS, EMIN = 1 - BIAS;
+// The rule's body with the format as values (MB mantissa bits, BIAS, MAXB
+// the fp32 bits of the format maximum, MAXC its code, NB the code width), so
+// that a kernel whose output format is a run-time value shares it.
+__device__ __forceinline__ uint32_t encode_sr_f(float x, int s, float inv, uint32_t r, int MB, int BIAS,
+                                                uint32_t MAXB, uint32_t MAXC, int NB) {
+    const int EMIN = 1 - BIAS;
     const uint32_t b = __float_as_uint(x), ab = b & 0x7FFFFFFFu;
     const uint32_t scaled = __float_as_uint(x * inv) & 0x7FFFFFFFu;   // exact unless far below the maximum
     const uint32_t fe = ab >> 23;
@@ -370,8 +375,37 @@ __device__ __forceinline__ uint32_t encode_sr(float x, int s, float inv, uint32_
     const uint32_t t = sh <= 0 ? D << (-sh) : (D + (1u << shc) - 1u) >> shc;
     const uint32_t up = r < t ? 1u : 0u;
     uint32_t code = (uint32_t)(((te + BIAS) << MB) - (1 << MB)) + mlo + up;
-    code = scaled >= F::MAXB ? F::MAXC : (ab == 0u ? 0u : code);
-    return code | ((b >> 31) << (fmt_bits(FMT) - 1));
+    code = scaled >= MAXB ? MAXC : (ab == 0u ? 0u : code);
+    return code | ((b >> 31) << (NB - 1));
+}
+template <int FMT>
+__device__ __forceinline__ uint32_t encode_sr(float x, int s, float inv, uint32_t r) {
+    typedef FmtSR<FMT> F;
+    return encode_sr_f(x, s, inv, r, F::MB, F::BIAS, F::MAXB, F::MAXC, fmt_bits(FMT));
+}
+// Run-time format: the same rule for an output format known only at run time.
+__device__ __forceinline__ uint32_t encode_sr_rt(int fmt, float x, int s, float inv, uint32_t r) {
+    const int mb = fmt == MXC_E2M1 ? 1 : fmt == MXC_E3M2 ? 2 : 3;
+    const int bias = fmt == MXC_E4M3 ? 7 : fmt == MXC_E3M2 ? 3 : 1;
+    const uint32_t maxb = fmt == MXC_E4M3 ? FmtSR<MXC_E4M3>::MAXB : fmt == MXC_E2M1 ? FmtSR<MXC_E2M1>::MAXB
+                        : fmt == MXC_E2M3 ? FmtSR<MXC_E2M3>::MAXB : FmtSR<MXC_E3M2>::MAXB;
+    const uint32_t maxc = fmt == MXC_E4M3 ? 0x7Eu : fmt == MXC_E2M1 ? 0x7u : 0x1Fu;
+    const int nb = fmt == MXC_E4M3 ? 8 : fmt == MXC_E2M1 ? 4 : 6;
+    return encode_sr_f(x, s, inv, r, mb, bias, maxb, maxc, nb);
+}
+// Stochastic codes of four consecutive elements x whose first code position
+// p is a multiple of 4 (positions p .. p + 3 take half-words p % 8 .. + 3 of
+// the generator call at counter p / 8).
+template <int FMT>
+__device__ __forceinline__ void sr_codes4(float4 x, uint64_t p, int s, float inv, uint32_t k0, uint32_t k1,
+                                          uint32_t* cd) {
+    const uint4 w = sr_words(p >> 3, k0, k1);
+    const bool hi = (p & 4u) != 0u;
+    const uint32_t w0 = hi ? w.z : w.x, w1 = hi ? w.w : w.y;
+    cd[0] = encode_sr<FMT>(x.x, s, inv, w0 & 0xFFFFu);
+    cd[1] = encode_sr<FMT>(x.y, s, inv, w0 >> 16);
+    cd[2] = encode_sr<FMT>(x.z, s, inv, w1 & 0xFFFFu);
+    cd[3] = encode_sr<FMT>(x.w, s, inv, w1 >> 16);
 }
 
 // The same decision for a normal fp32 x (or a zero), in fewer operations:

@@ -382,9 +382,10 @@ int mxconv_fwd_quant(const mxc_conv* p, int fmt, const void* wc, const uint8_t* 
     return rc == 1 ? MXC_ERR_SHAPE : rc;
 }
 
-int mxconv_dgrad_quant(const mxc_conv* p, int fmt, const void* wc, const uint8_t* ws, const void* gc,
-                       const uint8_t* gs, int fn, const void* z, int out_fmt, void* gxc, uint8_t* gxs,
-                       float* gx_act, void* stream) {
+namespace {
+int dgrad_quant_impl(const mxc_conv* p, int fmt, const void* wc, const uint8_t* ws, const void* gc, const uint8_t* gs,
+                int fn, const void* z, int out_fmt, void* gxc, uint8_t* gxs, float* gx_act, void* stream, bool sr,
+                uint64_t seed) {
     if (!p || !wc || !ws || !gc || !gs || !gxc || !gxs) return MXC_ERR_NULL;
     const bool bf16 = (fn & MXC_FN_BF16) != 0;
     fn &= ~MXC_FN_BF16;
@@ -398,8 +399,23 @@ int mxconv_dgrad_quant(const mxc_conv* p, int fmt, const void* wc, const uint8_t
         !aligned16(gxs) || (gx_act && !aligned16(gx_act)) || (fn != MXC_FN_NONE && !aligned16(z)))
         return MXC_ERR_ALIGN;
     FusedEpi q{gxc, gxs, out_fmt, fn, z, false, bf16};
+    q.sr = sr;
+    q.seed = seed;
     rc = launch_conv_lean(cv, true, wc, ws, gc, gs, gx_act, MXC_CBF, (hipStream_t)stream, &q);
     return rc == 1 ? MXC_ERR_SHAPE : rc;
+}
+}  // namespace
+
+int mxconv_dgrad_quant(const mxc_conv* p, int fmt, const void* wc, const uint8_t* ws, const void* gc,
+                       const uint8_t* gs, int fn, const void* z, int out_fmt, void* gxc, uint8_t* gxs,
+                       float* gx_act, void* stream) {
+    return dgrad_quant_impl(p, fmt, wc, ws, gc, gs, fn, z, out_fmt, gxc, gxs, gx_act, stream, false, 0);
+}
+
+int mxconv_dgrad_quant_sr(const mxc_conv* p, int fmt, const void* wc, const uint8_t* ws, const void* gc,
+                          const uint8_t* gs, int fn, const void* z, int out_fmt, void* gxc, uint8_t* gxs,
+                          float* gx_act, uint64_t seed, void* stream) {
+    return dgrad_quant_impl(p, fmt, wc, ws, gc, gs, fn, z, out_fmt, gxc, gxs, gx_act, stream, true, seed);
 }
 
 // The weight gradient's split-K partial sums for callers that cannot
@@ -465,8 +481,9 @@ int mxconv_concat_cbf(int fmt, int n, int h, int w, int nparts, const mxc_part* 
     return launch_concat(g, parts, nparts, codes, scales, (hipStream_t)stream);
 }
 
-int mxconv_quantize_sum(int fmt, int n, int c, int h, int w, int nterms, const mxc_term* terms, int fn,
-                        const void* z, void* codes, uint8_t* scales, float* vals, void* stream) {
+namespace {
+int quantize_sum_impl(int fmt, int n, int c, int h, int w, int nterms, const mxc_term* terms, int fn, const void* z,
+                 void* codes, uint8_t* scales, float* vals, void* stream, bool sr, uint64_t seed) {
     if (!terms || !codes || !scales) return MXC_ERR_NULL;
     if (nterms < 1 || nterms > MXC_TERMS_MAX) return MXC_ERR_ARG;
     const bool bf16 = (fn & MXC_FN_BF16) != 0;
@@ -489,7 +506,19 @@ int mxconv_quantize_sum(int fmt, int n, int c, int h, int w, int nterms, const m
     if (!aligned16(codes) || !aligned16(scales) || (vals && !aligned16(vals)) ||
         (fn != MXC_FN_NONE && !aligned16(z)))
         return MXC_ERR_ALIGN;
-    return launch_quantize_sum(g, fmt, terms, nterms, fn, bf16, z, codes, scales, vals, (hipStream_t)stream);
+    return launch_quantize_sum(g, fmt, terms, nterms, fn, bf16, z, codes, scales, vals, (hipStream_t)stream, sr,
+                               seed);
+}
+}  // namespace
+
+int mxconv_quantize_sum(int fmt, int n, int c, int h, int w, int nterms, const mxc_term* terms, int fn,
+                        const void* z, void* codes, uint8_t* scales, float* vals, void* stream) {
+    return quantize_sum_impl(fmt, n, c, h, w, nterms, terms, fn, z, codes, scales, vals, stream, false, 0);
+}
+
+int mxconv_quantize_sum_sr(int fmt, int n, int c, int h, int w, int nterms, const mxc_term* terms, int fn,
+                           const void* z, void* codes, uint8_t* scales, float* vals, uint64_t seed, void* stream) {
+    return quantize_sum_impl(fmt, n, c, h, w, nterms, terms, fn, z, codes, scales, vals, stream, true, seed);
 }
 
 size_t mxconv_naive_codes_bytes(int64_t lines, int64_t len, int fmt) {

@@ -78,6 +78,8 @@ struct SumArgs {
     int fn;
     const void* z;                    // CBF [n/32][h][w][c][32] (fn != NONE), fp32 or bf16 (BF)
     float* vals;                      // optional: the values quantized
+    int sr;                           // codes by stochastic rounding, generator key (k0, k1)
+    uint32_t k0, k1;
 };
 
 // Four consecutive elements at index i of an fp32 or (BF) bf16 tensor.
@@ -155,14 +157,29 @@ __global__ __launch_bounds__(256) void quantize_sum_kernel(SumArgs a, uint8_t* _
     if (lane == 0) scales[blk] = (uint8_t)sc;
     const float inv = inv_scale(sc);
     const bool bad = sc == 0xFFu;
+    uint32_t run[4];   // the codes of v[q]: channel row 8 q + lane / 8, samples j .. j + 3
+    if (a.sr) {        // stochastic rounding, keyed by code position blk 1024 + 32 row + sample
+        const int s = (int)sc - 127;
+#pragma unroll
+        for (int q = 0; q < 4; q++) {
+            uint32_t cd[4];
+            sr_codes4<FMT>(v[q], (uint64_t)blk * 1024 + (8 * q + (lane >> 3)) * 32 + j, s, inv, a.k0, a.k1, cd);
+            run[q] = FMT == MXC_E4M3 ? cd[0] | cd[1] << 8 | cd[2] << 16 | cd[3] << 24
+                                     : cd[0] | cd[1] << 4 | cd[2] << 8 | cd[3] << 12;
+        }
+    } else {
+#pragma unroll
+        for (int q = 0; q < 4; q++)
+            run[q] = FMT == MXC_E4M3 ? pack4_e4m3(v[q], inv) : (uint32_t)pack4_e2m1(v[q], inv);
+    }
     if constexpr (FMT == MXC_E4M3) {
         uint32_t* d = (uint32_t*)(codes + (size_t)blk * 1024) + lane;
 #pragma unroll
-        for (int q = 0; q < 4; q++) d[64 * q] = bad ? 0u : pack4_e4m3(v[q], inv);
+        for (int q = 0; q < 4; q++) d[64 * q] = bad ? 0u : run[q];
     } else {
         unsigned short* d = (unsigned short*)(codes + (size_t)blk * 512) + lane;
 #pragma unroll
-        for (int q = 0; q < 4; q++) d[64 * q] = bad ? (unsigned short)0 : (unsigned short)pack4_e2m1(v[q], inv);
+        for (int q = 0; q < 4; q++) d[64 * q] = bad ? (unsigned short)0 : (unsigned short)run[q];
     }
 }
 
@@ -252,11 +269,30 @@ __global__ __launch_bounds__(256) void quantize_sum_bf_kernel(SumArgs a, uint8_t
         const float4 lo = make_float4(v[hh][0], v[hh][1], v[hh][2], v[hh][3]);
         const float4 hi = make_float4(v[hh][4], v[hh][5], v[hh][6], v[hh][7]);
         const int row = 16 * hh + (lane >> 2);
+        uint32_t clo, chi;   // the codes of lo and hi (samples j .. j + 3, j + 4 .. j + 7)
+        if (a.sr) {          // stochastic rounding: positions blk 1024 + 32 row + j .., one generator call
+            const int s = (int)sc - 127;
+            const uint4 w = sr_words(((uint64_t)blk * 1024 + row * 32 + j) >> 3, a.k0, a.k1);
+            const uint32_t r[8] = {w.x & 0xFFFFu, w.x >> 16, w.y & 0xFFFFu, w.y >> 16,
+                                   w.z & 0xFFFFu, w.z >> 16, w.w & 0xFFFFu, w.w >> 16};
+            uint32_t cd[8];
+#pragma unroll
+            for (int e = 0; e < 8; e++) cd[e] = encode_sr<FMT>(v[hh][e], s, inv, r[e]);
+            constexpr int NB = FMT == MXC_E4M3 ? 8 : 4;
+            clo = cd[0] | cd[1] << NB | cd[2] << (2 * NB) | cd[3] << (3 * NB);
+            chi = cd[4] | cd[5] << NB | cd[6] << (2 * NB) | cd[7] << (3 * NB);
+        } else if constexpr (FMT == MXC_E4M3) {
+            clo = pack4_e4m3(lo, inv);
+            chi = pack4_e4m3(hi, inv);
+        } else {
+            clo = pack4_e2m1(lo, inv);
+            chi = pack4_e2m1(hi, inv);
+        }
         if constexpr (FMT == MXC_E4M3) {
-            const uint2 c = bad ? make_uint2(0u, 0u) : make_uint2(pack4_e4m3(lo, inv), pack4_e4m3(hi, inv));
+            const uint2 c = bad ? make_uint2(0u, 0u) : make_uint2(clo, chi);
             *(uint2*)(codes + (size_t)blk * 1024 + row * 32 + j) = c;
         } else {
-            const uint32_t c = bad ? 0u : ((uint32_t)pack4_e2m1(lo, inv) | (uint32_t)pack4_e2m1(hi, inv) << 16);
+            const uint32_t c = bad ? 0u : (clo | chi << 16);
             *(uint32_t*)(codes + (size_t)blk * 512 + row * 16 + j / 2) = c;
         }
     }
@@ -290,8 +326,12 @@ int launch_concat(const Geom& dst, const mxc_part* parts, int nparts, void* code
 }
 
 int launch_quantize_sum(const Geom& dst, int fmt, const mxc_term* terms, int nterms, int fn, bool bf16,
-                        const void* z, void* codes, uint8_t* scales, float* vals, hipStream_t s) {
+                        const void* z, void* codes, uint8_t* scales, float* vals, hipStream_t s, bool sr,
+                        uint64_t seed) {
     SumArgs a{};
+    a.sr = sr ? 1 : 0;
+    a.k0 = (uint32_t)seed;
+    a.k1 = (uint32_t)(seed >> 32);
     for (int t = 0; t < nterms; t++) {
         a.src[t] = terms[t].src;
         a.c_src[t] = terms[t].c_src;

@@ -99,6 +99,7 @@ def lib():
         "mxconv_wgrad_reduce_multi": (i32, [i32, ctypes.POINTER(MxcWJob), P]),
         "mxconv_fwd_quant": (i32, [CP, i32, P, P, P, P, i32, i32, P, P, P, P]),
         "mxconv_dgrad_quant": (i32, [CP, i32, P, P, P, P, i32, P, i32, P, P, P, P]),
+        "mxconv_dgrad_quant_sr": (i32, [CP, i32, P, P, P, P, i32, P, i32, P, P, P, ctypes.c_uint64, P]),
         "mxconv_naive_codes_bytes": (sz, [i64, i64, i32]),
         "mxconv_naive_scales_bytes": (sz, [i64, i64]),
         "mxconv_naive_im2col_f32": (i32, [CP, P, P, P]),
@@ -109,6 +110,8 @@ def lib():
         "mxconv_wgrad_noalloc": (i32, [CP, i32, P, P, P, P, P, P]),
         "mxconv_concat_cbf": (i32, [i32, i32, i32, i32, i32, ctypes.POINTER(MxcPart), P, P, P]),
         "mxconv_quantize_sum": (i32, [i32, i32, i32, i32, i32, i32, ctypes.POINTER(MxcTerm), i32, P, P, P, P, P]),
+        "mxconv_quantize_sum_sr": (i32, [i32, i32, i32, i32, i32, i32, ctypes.POINTER(MxcTerm), i32, P, P, P, P,
+                                         ctypes.c_uint64, P]),
         "mxconv_strerror": (ctypes.c_char_p, [i32]),
     }
     for name, (res, args) in sigs.items():
@@ -434,19 +437,23 @@ def fwd_quant(cv, w, x, fn=FN_NONE, out_fmt=None, out=None, act_out=None, stream
     return y
 
 
-def dgrad_quant(cv, w, gy, fn=FN_NONE, z=None, out_fmt=None, out=None, act_out=None, stream=None):
+def dgrad_quant(cv, w, gy, fn=FN_NONE, z=None, out_fmt=None, out=None, act_out=None, stream=None, sr_seed=None):
     """Input gradient with the quantizing epilogue: MX codes of
     (W^T * G_Y) . fn'(z) for (n, cin, h, w); z is the CBF pre-activation of
     this layer's input (not needed for FN_NONE), fp32, or bf16 with FN_BF16.
-    act_out (optional) is fp32."""
+    act_out (optional) is fp32.  sr_seed: round the codes stochastically
+    (mxconv_dgrad_quant_sr) with this 64-bit seed."""
     _want(z, torch.bfloat16 if fn & FN_BF16 else torch.float32, "z")
     _want(act_out, torch.float32, "act_out")
     out_fmt = gy.fmt if out_fmt is None else out_fmt
     shape = (cv["n"], cv["cin"], cv["h"], cv["w"])
     g = out if out is not None else MxTensor.empty(ACT, out_fmt, shape, gy.codes.device)
-    _check(lib().mxconv_dgrad_quant(ctypes.byref(conv_struct(cv)), pair(w.fmt, gy.fmt), _ptr(w.codes), _ptr(w.scales),
-                                    _ptr(gy.codes), _ptr(gy.scales), fn, _ptr(z), out_fmt, _ptr(g.codes),
-                                    _ptr(g.scales), _ptr(act_out), _stream(stream)), "mxconv_dgrad_quant")
+    args = (ctypes.byref(conv_struct(cv)), pair(w.fmt, gy.fmt), _ptr(w.codes), _ptr(w.scales), _ptr(gy.codes),
+            _ptr(gy.scales), fn, _ptr(z), out_fmt, _ptr(g.codes), _ptr(g.scales), _ptr(act_out))
+    if sr_seed is None:
+        _check(lib().mxconv_dgrad_quant(*args, _stream(stream)), "mxconv_dgrad_quant")
+    else:
+        _check(lib().mxconv_dgrad_quant_sr(*args, sr_seed, _stream(stream)), "mxconv_dgrad_quant_sr")
     return g
 
 
@@ -474,11 +481,12 @@ def concat_cbf(parts, out=None, stream=None):
     return y
 
 
-def quantize_sum(terms, shape, fmt, fn=FN_NONE, z=None, out=None, vals=None, stream=None):
+def quantize_sum(terms, shape, fmt, fn=FN_NONE, z=None, out=None, vals=None, stream=None, sr_seed=None):
     """MX codes of fn'(z) . (sum of terms) for the (n, c, h, w) tensor `shape`.
     terms: tuples (src, c_src, c_off, down) with src a CBF device tensor
     [n/32][hs][ws][c_src][32]; terms and z are fp32, or bf16 with FN_BF16;
-    vals (optional) is fp32."""
+    vals (optional) is fp32.  sr_seed: round the codes stochastically
+    (mxconv_quantize_sum_sr) with this 64-bit seed."""
     if not 1 <= len(terms) <= TERMS_MAX:
         raise MxconvError(f"1 to {TERMS_MAX} terms")
     dt = torch.bfloat16 if fn & FN_BF16 else torch.float32
@@ -490,8 +498,11 @@ def quantize_sum(terms, shape, fmt, fn=FN_NONE, z=None, out=None, vals=None, str
         arr[k] = MxcTerm(src.data_ptr(), c_src, c_off, down)
     n, c, h, w = shape
     g = out if out is not None else MxTensor.empty(ACT, fmt, shape, terms[0][0].device)
-    _check(lib().mxconv_quantize_sum(fmt, n, c, h, w, len(terms), arr, fn, _ptr(z), _ptr(g.codes), _ptr(g.scales),
-                                     _ptr(vals), _stream(stream)), "mxconv_quantize_sum")
+    args = (fmt, n, c, h, w, len(terms), arr, fn, _ptr(z), _ptr(g.codes), _ptr(g.scales), _ptr(vals))
+    if sr_seed is None:
+        _check(lib().mxconv_quantize_sum(*args, _stream(stream)), "mxconv_quantize_sum")
+    else:
+        _check(lib().mxconv_quantize_sum_sr(*args, sr_seed, _stream(stream)), "mxconv_quantize_sum_sr")
     return g
 
 
