@@ -251,19 +251,24 @@ int mxconv_nvfp_quantize(const void* src, int dtype, int layout, int role, int f
                          int n, int c, int h, int w, void* codes, uint8_t* scales,
                          float* tscale, void* workspace, size_t ws_bytes, void* stream);
 
-/* The three GEMMs on NVFP4 operands (E2M1 codes with E4M3 8x8 block scales
- * and per-tensor scales, as mxconv_nvfp_quantize writes them): Y = W * X,
- * G_X = W^T * G_Y, G_W = G_Y * X^T (Eqs. (1)-(3)) of the fake-quantized
- * tensors code x B x T.  The block-scaled matrix cores take only E8M0 scales
- * per 32 elements, so the kernels decode each fragment to fp16 (code x B is
- * exact in fp16), run fp16 MFMAs with fp32 accumulation and multiply the
+/* The three GEMMs on NVFP operands (element codes with E4M3 8x8 block
+ * scales and per-tensor scales, as mxconv_nvfp_quantize writes them): Y =
+ * W * X, G_X = W^T * G_Y, G_W = G_Y * X^T (Eqs. (1)-(3)) of the
+ * fake-quantized tensors code x B x T.  The block-scaled matrix cores take
+ * only E8M0 scales per 32 elements, so the kernels decode each fragment --
+ * to fp16 for FP4 and FP6 elements, to bf16 for FP8 (code x B is exact in
+ * either) -- run fp16 / bf16 MFMAs with fp32 accumulation and multiply the
  * result by the two per-tensor scales.  Arguments as mxconv_fwd / dgrad /
  * wgrad, with each operand's E4M3 block scales (mxconv_nvfp_scales_bytes)
- * and its per-tensor scale (w_t, x_t, gy_t: device floats).  fmt must be
- * MXC_E2M1 (NVFP4); layers outside the batch-block-32 kernels (kernel width
- * 1 or 3, forward column stride 1 or 2, input-gradient stride 1x1 or 2x2)
- * return MXC_ERR_SHAPE.  The weight gradient uses the workspace of
- * mxconv_wgrad_workspace_bytes(cv, MXC_E2M1).
+ * and its per-tensor scale (w_t, x_t, gy_t: device floats).  fmt: one
+ * format for both operands -- MXC_E2M1 (NVFP4, the paper's format),
+ * MXC_E2M3 (NVFP6 of the "-6" methods, Sec. VI-B), MXC_E4M3 (NVFP8) -- or
+ * MXC_PAIR(MXC_E2M1, MXC_E3M2), FP4 weights or gradients with E3M2
+ * activations (MicroQonv+, Sec. IV-D), in the operand order of the call
+ * (W, X / W, G_Y / G_Y, X); other pairs return MXC_ERR_ARG.  Layers outside
+ * the batch-block-32 kernels (kernel width 1 or 3, forward column stride 1
+ * or 2, input-gradient stride 1x1 or 2x2) return MXC_ERR_SHAPE.  The weight
+ * gradient uses the workspace of mxconv_wgrad_workspace_bytes(cv, fmt).
  * Errors: NULL, ARG, SHAPE, ALIGN, WORKSPACE, HIP. */
 int mxconv_nvfp_fwd(const mxc_conv* cv, int fmt,
                     const void* w_codes, const uint8_t* w_scales, const float* w_t,

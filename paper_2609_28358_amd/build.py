@@ -16,7 +16,9 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libmxconv.so")
-SOURCES = ["quantize.hip", "nvfp.hip", "im2col.hip", "conv_gemm.hip", "conv_lean.hip", "wgrad_lean.hip", "naive.hip", "netops.hip", "mxconv_abi.cpp"]
+SOURCES = ["quantize.hip", "nvfp.hip", "im2col.hip", "conv_gemm.hip", "conv_lean.hip", "conv_lean_bwd.hip",
+           "conv_lean_e4m3_fwd.hip", "conv_lean_e4m3_dg.hip", "conv_lean_e2m1_fwd.hip", "conv_lean_e2m1_dg.hip",
+           "conv_lean_nv.hip", "conv_lean_nv68.hip", "conv_lean_fp6.hip", "wgrad_lean.hip", "naive.hip", "netops.hip", "mxconv_abi.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
@@ -35,7 +37,7 @@ def _compile(src):
 def build(verbose=False):
     os.makedirs(BUILD, exist_ok=True)
     srcs = [s for s in SOURCES if os.path.exists(os.path.join(CSRC, s))]
-    with ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
+    with ThreadPoolExecutor(max_workers=min(os.cpu_count() or 8, 16, len(srcs))) as ex:
         objs = list(ex.map(_compile, srcs))
     tmp = LIB + ".tmp"
     cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp] + objs

@@ -85,6 +85,12 @@ int launch_dgrad(const Conv& cv, const void* wc, const uint8_t* ws, const void* 
 // Fused quantizing epilogue of fwd / dgrad: the output, after the activation
 // fn (fwd) or times its derivative at z (dgrad), quantized into MX-CBF codes
 // and scales of format fmt.
+// Element-format pairs of the NVFP GEMMs (first operand, second operand):
+// one format (NVFP4, NVFP6 E2M3, NVFP8), or FP4 with E3M2 (MicroQonv+).
+inline bool nv_pair_ok(int fa, int fb) {
+    return (fa == fb && fa != MXC_E3M2) || (fa == MXC_E2M1 && fb == MXC_E3M2);
+}
+
 struct FusedEpi {
     void* codes;
     uint8_t* scales;
@@ -440,33 +446,88 @@ __device__ __forceinline__ bool sr_needs_general(float x) {
     return ab != 0u && ab < 0x800000u;
 }
 
-// ---------------------------------------------------------------- NVFP4 operands
+// ---------------------------------------------------------------- NVFP operands
 // The block-scaled matrix cores take E8M0 scales per 32 K elements; an NVFP
-// block scale is E4M3 per 8 elements.  A code times its E4M3 scale has at most
-// six significant bits and lies in [2^-10, 2688], so it is exact in fp16: the
-// GEMMs decode NVFP4 fragments to fp16 (code x B) and run fp16 MFMAs.  The
-// scaled converts apply only the power of two of their scale operand
-// (measured), so B = 2^E M is split: 2^E goes to the convert, the mantissa
-// factor M (1 + m/8, or m for a subnormal B) is one packed fp16 multiply.
+// block scale is E4M3 per 8 elements.  A code times its E4M3 scale B has at
+// most 2 + 4 = 6 (E2M1), 3 + 4 = 7 (E3M2) or 4 + 4 = 8 (E2M3, E4M3)
+// significant bits.  FP4 and FP6 products lie in [2^-13, 12544], so they are
+// exact in fp16; FP8 products reach 448 x 448, past fp16's range, and are
+// exact in bf16 (8 significant bits, the fp32 exponent range).  The GEMMs
+// therefore decode NVFP fragments to fp16 (FP4, FP6) or bf16 (FP8) and run
+// fp16 / bf16 MFMAs; the product of two decoded values is exact in fp32.
 typedef _Float16 v2h __attribute__((ext_vector_type(2)));
 typedef _Float16 v8h __attribute__((ext_vector_type(8)));
+typedef _Float16 v32h __attribute__((ext_vector_type(32)));
+typedef float v2f __attribute__((ext_vector_type(2)));
 
-// 32 E2M1 codes (f[0..3], element k in nibble k) and the E4M3 scales of
-// their four groups of 8 (byte g of s4) -> 32 fp16 values in out[0..15]
-// (element k in half k).
+// An E4M3 block scale: 2^e2 times m8 / 8 (m8 = 8 + m for a normal code, m
+// for a subnormal one), as the power of two and the mantissa factor.
+__device__ __forceinline__ void e4m3_split(uint32_t sg, float& pw, float& mf) {
+    const uint32_t e = (sg >> 3) & 0xFu, m = sg & 7u;
+    pw = __uint_as_float(e ? (e + 120u) << 23 : (127u - 9u) << 23);   // 2^(e-7), or 2^-9
+    mf = e ? 1.0f + 0.125f * (float)m : (float)m;
+}
+
+// 32 codes of format F (the lane's fragment: FP4 element k in nibble k, FP6
+// code k in bits 6k .. 6k+5, FP8 element k in byte k) and the E4M3 scales of
+// their four groups of 8 (byte g of s4: elements 8g .. 8g+7) -> 32 decoded
+// values code x B in out[0..15] (element k in half k): fp16 for FP4 / FP6,
+// bf16 for FP8.
+template <int F>
 __device__ __forceinline__ void nv_decode32(const v8i& f, uint32_t s4, uint32_t* out) {
+    if constexpr (F == MXC_E2M1) {
+        // the scaled convert applies only the power of two of its scale
+        // operand (measured): 2^E goes to the convert, the mantissa factor is
+        // one packed fp16 multiply
 #pragma unroll
-    for (int g = 0; g < 4; g++) {
-        const uint32_t sg = (s4 >> (8 * g)) & 0xFFu;
-        const uint32_t e = (sg >> 3) & 0xFu, m = sg & 7u;
-        const float pw = __uint_as_float(e ? (e + 120u) << 23 : (127u - 9u) << 23);   // 2^(e-7), or 2^-9
-        const _Float16 mh = e ? (_Float16)(1.0f + 0.125f * (float)m) : (_Float16)(float)m;
-        const v2h mm = {mh, mh};
-        const uint32_t src = (uint32_t)f[g];
+        for (int g = 0; g < 4; g++) {
+            float pw, mf;
+            e4m3_split((s4 >> (8 * g)) & 0xFFu, pw, mf);
+            const _Float16 mh = (_Float16)mf;
+            const v2h mm = {mh, mh};
+            const uint32_t src = (uint32_t)f[g];
 #define NVD(SEL) { const v2h v = __builtin_bit_cast(v2h, __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(src, pw, SEL)) * mm; \
                    out[4 * g + SEL] = __builtin_bit_cast(uint32_t, v); }
-        NVD(0) NVD(1) NVD(2) NVD(3)
+            NVD(0) NVD(1) NVD(2) NVD(3)
 #undef NVD
+        }
+    } else if constexpr (fmt_bits(F) == 6) {
+        // the 32 codes to fp16 with scale 1 (exact), then each group times
+        // its B, exact in fp16 (one packed multiply per pair)
+        v6i src;
+#pragma unroll
+        for (int e = 0; e < 6; e++) src[e] = f[e];
+        const v32h v = F == MXC_E2M3 ? __builtin_amdgcn_cvt_scalef32_pk32_f16_fp6(src, 1.0f)
+                                     : __builtin_amdgcn_cvt_scalef32_pk32_f16_bf6(src, 1.0f);
+#pragma unroll
+        for (int g = 0; g < 4; g++) {
+            float pw, mf;
+            e4m3_split((s4 >> (8 * g)) & 0xFFu, pw, mf);
+            const _Float16 bh = (_Float16)(pw * mf);
+            const v2h bb = {bh, bh};
+#pragma unroll
+            for (int j = 0; j < 4; j++) {
+                const v2h x = {v[8 * g + 2 * j], v[8 * g + 2 * j + 1]};
+                out[4 * g + j] = __builtin_bit_cast(uint32_t, x * bb);
+            }
+        }
+    } else {
+        // FP8: each pair decoded to fp32 (exact), times B in fp32 (exact: at
+        // most 8 significant bits), rounded to bf16 (exact for the same reason)
+#pragma unroll
+        for (int g = 0; g < 4; g++) {
+            float pw, mf;
+            e4m3_split((s4 >> (8 * g)) & 0xFFu, pw, mf);
+            const float b = pw * mf;
+#pragma unroll
+            for (int w = 0; w < 2; w++) {
+                const uint32_t src = (uint32_t)f[2 * g + w];
+                const v2f lo = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(src, 1.0f, false);
+                const v2f hi = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(src, 1.0f, true);
+                out[4 * g + 2 * w] = bf16_pack2(lo[0] * b, lo[1] * b);
+                out[4 * g + 2 * w + 1] = bf16_pack2(hi[0] * b, hi[1] * b);
+            }
+        }
     }
 }
 

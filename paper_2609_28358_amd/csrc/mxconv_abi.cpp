@@ -213,10 +213,11 @@ int mxconv_nvfp_quantize(const void* src, int dtype, int layout, int role, int f
 int mxconv_nvfp_fwd(const mxc_conv* p, int fmt, const void* wc, const uint8_t* ws, const float* wt,
                     const void* xc, const uint8_t* xs, const float* xt, float* y, int y_layout, void* stream) {
     if (!p || !wc || !ws || !wt || !xc || !xs || !xt || !y) return MXC_ERR_NULL;
-    if (fmt != MXC_E2M1 || (y_layout != MXC_NCHW && y_layout != MXC_CBF)) return MXC_ERR_ARG;
+    if (y_layout != MXC_NCHW && y_layout != MXC_CBF) return MXC_ERR_ARG;
     Conv cv;
     int rc = conv_init(&cv, p, fmt, CONV_FWD);
     if (rc) return rc;
+    if (!nv_pair_ok(cv.fa, cv.fb)) return MXC_ERR_ARG;
     if (!aligned16(wc) || !aligned16(ws) || !aligned16(wt) || !aligned16(xc) || !aligned16(xs) ||
         !aligned16(xt) || !aligned16(y))
         return MXC_ERR_ALIGN;
@@ -227,10 +228,11 @@ int mxconv_nvfp_fwd(const mxc_conv* p, int fmt, const void* wc, const uint8_t* w
 int mxconv_nvfp_dgrad(const mxc_conv* p, int fmt, const void* wc, const uint8_t* ws, const float* wt,
                       const void* gc, const uint8_t* gs, const float* gt, float* gx, int gx_layout, void* stream) {
     if (!p || !wc || !ws || !wt || !gc || !gs || !gt || !gx) return MXC_ERR_NULL;
-    if (fmt != MXC_E2M1 || (gx_layout != MXC_NCHW && gx_layout != MXC_CBF)) return MXC_ERR_ARG;
+    if (gx_layout != MXC_NCHW && gx_layout != MXC_CBF) return MXC_ERR_ARG;
     Conv cv;
     int rc = conv_init(&cv, p, fmt, CONV_DGRAD);
     if (rc) return rc;
+    if (!nv_pair_ok(cv.fa, cv.fb)) return MXC_ERR_ARG;
     if (!aligned16(wc) || !aligned16(ws) || !aligned16(wt) || !aligned16(gc) || !aligned16(gs) ||
         !aligned16(gt) || !aligned16(gx))
         return MXC_ERR_ALIGN;
@@ -242,10 +244,10 @@ int mxconv_nvfp_wgrad(const mxc_conv* p, int fmt, const void* gc, const uint8_t*
                       const void* xc, const uint8_t* xs, const float* xt, float* gw, void* workspace,
                       size_t ws_bytes, void* stream) {
     if (!p || !gc || !gs || !gt || !xc || !xs || !xt || !gw) return MXC_ERR_NULL;
-    if (fmt != MXC_E2M1) return MXC_ERR_ARG;
     Conv cv;
     int rc = conv_init(&cv, p, fmt, CONV_WGRAD);
     if (rc) return rc;
+    if (!nv_pair_ok(cv.fa, cv.fb)) return MXC_ERR_ARG;
     if (wgrad_lean_splits(cv) == 0) return MXC_ERR_SHAPE;
     const size_t need = wgrad_workspace(cv);
     if (need && (!workspace || ws_bytes < need)) return MXC_ERR_WORKSPACE;

@@ -59,8 +59,16 @@ int launch_wgrad_lean(const Conv& cv, const void* gc, const uint8_t* gs, const v
     if (grid < 0) return MXC_ERR_SHAPE;
     const dim3 gd((unsigned)grid);
     if (nv_tg) {
-        if (cv.fa != MXC_E2M1 || cv.fb != MXC_E2M1) return MXC_ERR_ARG;
-        hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E2M1, MXC_E2M1, true>), gd, dim3(WT), 0, s, a);
+        if (cv.fa == MXC_E2M1 && cv.fb == MXC_E2M1)
+            hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E2M1, MXC_E2M1, true>), gd, dim3(WT), 0, s, a);
+        else if (cv.fa == MXC_E2M1 && cv.fb == MXC_E3M2)
+            hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E2M1, MXC_E3M2, true>), gd, dim3(WT), 0, s, a);
+        else if (cv.fa == MXC_E2M3 && cv.fb == MXC_E2M3)
+            hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E2M3, MXC_E2M3, true>), gd, dim3(WT), 0, s, a);
+        else if (cv.fa == MXC_E4M3 && cv.fb == MXC_E4M3)
+            hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E4M3, MXC_E4M3, true>), gd, dim3(WT), 0, s, a);
+        else
+            return MXC_ERR_ARG;
         return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
     }
     const bool nb1 = wgrad_single_block(cv);

@@ -65,15 +65,17 @@ __device__ __forceinline__ v8i row_frag(const uint8_t* p0, const uint8_t* p1, co
     return o;
 }
 
-// NV: NVFP4 operands, decoded to fp16 per fragment and multiplied on fp16
-// MFMAs (the 8-sample groups of a row each have their own E4M3 scale).
+// NV: NVFP operands, decoded per fragment (fp16 for FP4 / FP6, bf16 for FP8)
+// and multiplied on fp16 / bf16 MFMAs (the 8-sample groups of a row each
+// have their own E4M3 scale).
 // NB: 32-row blocks per tile side -- 2 (a 64 x 64 tile), or 1 for a layer
 // whose G_Y and X both have a single channel block (a 32 x 32 tile: half the
 // loads and a quarter of the products per pixel pair, so twice the pairs per
 // batch).
 template <int FA, int FB, bool NV = false, int NB = 2>
 __device__ __forceinline__ void wgrad_tile(const WLArgs& p, int bid, int nblk, float (*red)[32 * NB * 32 * NB]) {
-    static_assert(!NV || (FA == MXC_E2M1 && FB == MXC_E2M1), "NVFP4 operands only");
+    static_assert(!NV || (FA == FB && FA != MXC_E3M2) || (FA == MXC_E2M1 && FB == MXC_E3M2),
+                  "NVFP pairs: one format (FP4, E2M3, FP8), or FP4 gradients with E3M2 activations");
     static_assert(NB == 1 || NB == 2, "one or two blocks per tile side");
     constexpr int RS = 32 * NB;                   // tile side; red[wave] holds RS x RS floats
     constexpr int RBA = 32 * fmt_bits(FA) / 8;    // bytes of one block row (32 samples): G_Y
@@ -193,13 +195,31 @@ __device__ __forceinline__ void wgrad_tile(const WLArgs& p, int bid, int nblk, f
             o.sa[i] = sav ? sa : 0;
             o.sb[i] = sbv ? sb : 0;
             if constexpr (NV) {
+                // E4M3 scales of the lane's row: the four sample groups of a
+                // pixel in one word
                 const uint32_t* ga = (const uint32_t*)p.gs;
                 const uint32_t* xa = (const uint32_t*)p.xs;
-                const size_t pa = pa_row + oxh, px = px_row + ixh;
-                const uint32_t va4 = ga[pa * (p.gy_cp / 8) + (a_ok[i] ? cob : 0) * 4 + (r >> 3)];
-                const uint32_t vb4 = xa[px * (p.x_cp / 8) + (b_ok[i] ? cib : 0) * 4 + (r >> 3)];
-                o.na[i] = sav ? va4 : 0u;
-                o.nb[i] = sbv ? vb4 : 0u;
+                const uint32_t ca = (uint32_t)(a_ok[i] ? cob : 0) * 4 + (r >> 3);
+                const uint32_t cb = (uint32_t)(b_ok[i] ? cib : 0) * 4 + (r >> 3);
+                if constexpr (FA == MXC_E4M3) {
+                    // the lane holds samples 16 hf .. 16 hf + 15 of both
+                    // pixels: sample groups 2 hf, 2 hf + 1 of each
+                    uint32_t wa[2], wb[2];
+#pragma unroll
+                    for (int k = 0; k < 2; k++) {
+                        const uint32_t u = ga[(pa_row + oxk[k]) * (p.gy_cp / 8) + ca];
+                        const uint32_t v = xa[(px_row + ixk[k]) * (p.x_cp / 8) + cb];
+                        wa[k] = va[k] && a_ok[i] ? (u >> (16 * hf)) & 0xFFFFu : 0u;
+                        wb[k] = vb[k] && b_ok[i] ? (v >> (16 * hf)) & 0xFFFFu : 0u;
+                    }
+                    o.na[i] = wa[0] | wa[1] << 16;
+                    o.nb[i] = wb[0] | wb[1] << 16;
+                } else {   // all 32 samples of the lane's own pixel
+                    const uint32_t va4 = ga[(pa_row + oxh) * (p.gy_cp / 8) + ca];
+                    const uint32_t vb4 = xa[(px_row + ixh) * (p.x_cp / 8) + cb];
+                    o.na[i] = sav ? va4 : 0u;
+                    o.nb[i] = sbv ? vb4 : 0u;
+                }
             }
         }
     };
@@ -225,13 +245,14 @@ __device__ __forceinline__ void wgrad_tile(const WLArgs& p, int bid, int nblk, f
                 uint32_t ad[NB][16], bd[NB][16];
 #pragma unroll
                 for (int i = 0; i < NB; i++) {
-                    nv_decode32(o[b].a[i], o[b].na[i], ad[i]);
-                    nv_decode32(o[b].b[i], o[b].nb[i], bd[i]);
+                    nv_decode32<FA>(o[b].a[i], o[b].na[i], ad[i]);
+                    nv_decode32<FB>(o[b].b[i], o[b].nb[i], bd[i]);
                 }
 #pragma unroll
                 for (int i = 0; i < NB; i++)
 #pragma unroll
-                    for (int j = 0; j < NB; j++) acc[i][j] = mfma_nv(ad[i], bd[j], acc[i][j]);
+                    for (int j = 0; j < NB; j++)
+                        acc[i][j] = FA == MXC_E4M3 ? mfma_x8(ad[i], bd[j], acc[i][j]) : mfma_nv(ad[i], bd[j], acc[i][j]);
             } else if constexpr (FA == MXC_E4M3) {   // MXFP8: each fragment decoded to bf16 once
                 uint32_t ad[NB][16], bd[NB][16];
 #pragma unroll

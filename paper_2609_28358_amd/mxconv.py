@@ -288,9 +288,10 @@ def nvfp_quantize(src, role, fmt, layout=NCHW, shape=None, workspace=None, strea
 
 
 def nvfp_fwd(cv, w, x, layout=NCHW, out=None, stream=None):
-    """Y = W * X on NVFP4 operands (NvfpTensor)."""
+    """Y = W * X on NVFP operands (NvfpTensor): NVFP4, NVFP6 E2M3, NVFP8, or
+    NVFP4 weights with NVFP6 E3M2 activations."""
     y = _out((cv["n"], cv["cout"], *out_size(cv)), layout, batch_block(cv["n"]), x.codes.device, out)
-    _check(lib().mxconv_nvfp_fwd(ctypes.byref(conv_struct(cv)), x.fmt, _ptr(w.codes), _ptr(w.scales), _ptr(w.tscale),
+    _check(lib().mxconv_nvfp_fwd(ctypes.byref(conv_struct(cv)), pair(w.fmt, x.fmt), _ptr(w.codes), _ptr(w.scales), _ptr(w.tscale),
                                  _ptr(x.codes), _ptr(x.scales), _ptr(x.tscale), _ptr(y), layout, _stream(stream)),
            "mxconv_nvfp_fwd")
     return y
@@ -298,7 +299,7 @@ def nvfp_fwd(cv, w, x, layout=NCHW, out=None, stream=None):
 
 def nvfp_dgrad(cv, w, gy, layout=NCHW, out=None, stream=None):
     gx = _out((cv["n"], cv["cin"], cv["h"], cv["w"]), layout, batch_block(cv["n"]), gy.codes.device, out)
-    _check(lib().mxconv_nvfp_dgrad(ctypes.byref(conv_struct(cv)), gy.fmt, _ptr(w.codes), _ptr(w.scales),
+    _check(lib().mxconv_nvfp_dgrad(ctypes.byref(conv_struct(cv)), pair(w.fmt, gy.fmt), _ptr(w.codes), _ptr(w.scales),
                                    _ptr(w.tscale), _ptr(gy.codes), _ptr(gy.scales), _ptr(gy.tscale), _ptr(gx), layout,
                                    _stream(stream)), "mxconv_nvfp_dgrad")
     return gx
@@ -307,11 +308,12 @@ def nvfp_dgrad(cv, w, gy, layout=NCHW, out=None, stream=None):
 def nvfp_wgrad(cv, gy, x, out=None, workspace=None, stream=None):
     gw = out if out is not None else torch.empty((cv["cout"], cv["cin"], cv["kh"], cv["kw"]),
                                                  dtype=torch.float32, device=x.codes.device)
-    need = wgrad_workspace_bytes(cv, x.fmt)
+    fmt = pair(gy.fmt, x.fmt)
+    need = wgrad_workspace_bytes(cv, fmt)
     if workspace is None and need:
         workspace = torch.empty(need, dtype=torch.uint8, device=x.codes.device)
     wsz = workspace.numel() * workspace.element_size() if workspace is not None else 0
-    _check(lib().mxconv_nvfp_wgrad(ctypes.byref(conv_struct(cv)), x.fmt, _ptr(gy.codes), _ptr(gy.scales),
+    _check(lib().mxconv_nvfp_wgrad(ctypes.byref(conv_struct(cv)), fmt, _ptr(gy.codes), _ptr(gy.scales),
                                    _ptr(gy.tscale), _ptr(x.codes), _ptr(x.scales), _ptr(x.tscale), _ptr(gw),
                                    _ptr(workspace), wsz, _stream(stream)), "mxconv_nvfp_wgrad")
     return gw

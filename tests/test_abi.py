@@ -313,13 +313,15 @@ def test_nvfp_gemm_errors():
     for fn in (L.mxconv_nvfp_fwd, L.mxconv_nvfp_dgrad):   # (cv, fmt, wc, ws, wt, xc, xs, xt, out, layout, stream)
         assert fn(None, 1, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, 0, None) == -1
         assert fn(r, 1, GOOD, GOOD, None, GOOD, GOOD, GOOD, GOOD, 0, None) == -1
-        assert fn(r, 0, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, 0, None) == -2      # NVFP4 only
+        assert fn(r, 3, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, 0, None) == -2      # E3M2 x E3M2
+        assert fn(r, 0x14, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, 0, None) == -2   # FP4 x FP8
         assert fn(r, 1, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, 1, None) == -2      # NHWC output
         assert fn(r, 1, GOOD, GOOD, GOOD, GOOD, GOOD, ODD, GOOD, 0, None) == -4
         assert fn(r5, 1, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, 0, None) == -3     # kernel width 5
     w = L.mxconv_nvfp_wgrad      # (cv, fmt, gc, gs, gt, xc, xs, xt, gw, ws, ws_bytes, stream)
     assert w(r, 1, GOOD, GOOD, GOOD, GOOD, GOOD, None, GOOD, GOOD, 1 << 30, None) == -1
-    assert w(r, 2, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, 1 << 30, None) == -2
+    assert w(r, 3, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, 1 << 30, None) == -2   # E3M2 x E3M2
+    assert w(r, 0x12, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, 1 << 30, None) == -2  # FP8 x E2M3
     big = ctypes.byref(mx.conv_struct(synth.conv_dict(32, 64, 64, 56, 56, 3, 1, 1)))
     assert w(big, 1, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, GOOD, None, 0, None) == -6
     r16 = ctypes.byref(mx.conv_struct(synth.conv_dict(16, 64, 64, 8, 8, 3, 1, 1)))

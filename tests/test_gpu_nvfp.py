@@ -83,7 +83,7 @@ def test_nvfp_full_size_activation(mx, fmt):
         _check(mx, t, mx.ACT, fmt, mx.CBF, synth.nchw_to_cbf(t, 32))
 
 
-# ------------------------------------------------------------------ GEMMs on NVFP4 operands
+# ------------------------------------------------------------------ GEMMs on NVFP operands
 TOL = 1e-5
 
 NV_CONVS = [
@@ -101,14 +101,20 @@ def _nv_ids(c):
     return f"n{c['n']}_{c['cin']}to{c['cout']}_{c['h']}x{c['w']}_k{c['kh']}{c['kw']}_s{c['sh']}{c['sw']}"
 
 
-def _nv_layer(mx, cv, seed, kind="unit"):
+# element formats of (W, X, G_Y): NVFP4 (the paper's format), NVFP8 (its
+# "-8" methods), NVFP6 E2M3 (the "-6" methods, Sec. VI-B) and MicroQonv+
+# (NVFP6 E3M2 activations with NVFP4 weights and gradients, Sec. IV-D)
+NV_METHODS = {"nvfp4": (1, 1, 1), "nvfp8": (0, 0, 0), "nvfp6": (2, 2, 2), "microqonv_plus": (1, 3, 1)}
+
+
+def _nv_layer(mx, cv, seed, kind="unit", fmts=(1, 1, 1)):
     x, w, gy = synth.layer_inputs(cv, seed, kind=kind)
     q, d = {}, {}
-    for k, t, role in (("x", x, mx.ACT), ("w", w, mx.WEIGHT), ("gy", gy, mx.ACT)):
+    for (k, t, role), fmt in zip((("w", w, mx.WEIGHT), ("x", x, mx.ACT), ("gy", gy, mx.ACT)), fmts):
         src = synth.nchw_to_cbf(t, 32) if role == mx.ACT else t
-        q[k] = _check(mx, t, role, 1, mx.CBF if role == mx.ACT else mx.NCHW, src)   # bit-exact quantize first
-        rc, rs, rt = oracle.nvfp_quantize(t.numpy(), oracle.NCHW, role, 1, *t.shape)
-        d[k] = oracle.nvfp_dequant(rc, rs, rt, role, 1, *t.shape)
+        q[k] = _check(mx, t, role, fmt, mx.CBF if role == mx.ACT else mx.NCHW, src)   # bit-exact quantize first
+        rc, rs, rt = oracle.nvfp_quantize(t.numpy(), oracle.NCHW, role, fmt, *t.shape)
+        d[k] = oracle.nvfp_dequant(rc, rs, rt, role, fmt, *t.shape)
     return q, d
 
 
@@ -116,14 +122,20 @@ def _nv_err(got, ref, sabs):
     return mxt.gemm_err(got, ref, sabs, tol=TOL)
 
 
-@pytest.mark.parametrize("cv", NV_CONVS, ids=_nv_ids)
-@pytest.mark.parametrize("layout", ["nchw", "cbf"])
-def test_nvfp_gemms(mx, cv, layout):
-    """Forward, input gradient and weight gradient of the fake-quantized
-    NVFP4 tensors against the oracle's direct convolutions of Eqs. (1)-(3)
-    (fp64), within 1e-5 of the sum of absolute products."""
+# every layer in CBF for every method; the NCHW output epilogue does not
+# depend on the element format: every layer for NVFP4, the first for the rest
+NV_CASES = ([(cv, "cbf", m) for m in NV_METHODS for cv in NV_CONVS] +
+            [(cv, "nchw", "nvfp4") for cv in NV_CONVS] + [(NV_CONVS[0], "nchw", m) for m in NV_METHODS if m != "nvfp4"])
+
+
+@pytest.mark.parametrize("cv,layout,method", NV_CASES, ids=lambda v: _nv_ids(v) if isinstance(v, dict) else v)
+def test_nvfp_gemms(mx, cv, layout, method):
+    """Forward, input gradient and weight gradient of the fake-quantized NVFP
+    tensors against the oracle's direct convolutions of Eqs. (1)-(3) (fp64),
+    within 1e-5 of the sum of absolute products, for every element-format
+    combination the GEMMs take."""
     lay = mx.NCHW if layout == "nchw" else mx.CBF
-    q, d = _nv_layer(mx, cv, 31)
+    q, d = _nv_layer(mx, cv, 31, fmts=NV_METHODS[method])
     ho, wo = synth.out_hw(cv)
     y = mx.nvfp_fwd(cv, q["w"], q["x"], layout=lay)
     gw = mx.nvfp_wgrad(cv, q["gy"], q["x"])
@@ -144,11 +156,12 @@ def test_nvfp_gemms(mx, cv, layout):
     assert max(e) <= 1.0, e
 
 
-def test_nvfp_gemms_full_size_layer(mx):
+@pytest.mark.parametrize("method", list(NV_METHODS))
+def test_nvfp_gemms_full_size_layer(mx, method):
     """The 3x3 s1 64->64 56x56 layer at batch 32: 2048 sampled outputs of
     each GEMM against dot products of the dequantized operands."""
     name, cv = synth.SWEEP_LAYERS[0]
-    q, d = _nv_layer(mx, cv, 3000, kind="sweep")
+    q, d = _nv_layer(mx, cv, 3000, kind="sweep", fmts=NV_METHODS[method])
     ho, wo = synth.out_hw(cv)
     y = synth.cbf_to_nchw(mx.nvfp_fwd(cv, q["w"], q["x"], layout=mx.CBF).cpu(), cv["n"], cv["cout"], ho, wo, 32).numpy()
     gx = synth.cbf_to_nchw(mx.nvfp_dgrad(cv, q["w"], q["gy"], layout=mx.CBF).cpu(), cv["n"], cv["cin"], cv["h"],
@@ -182,4 +195,10 @@ def test_nvfp_gemm_refusals(mx):
     x8 = mx.nvfp_quantize(synth.nchw_to_cbf(synth.normal((32, 32, 9, 9), 1.0, 3), 32).to(DEV), mx.ACT, 0,
                           layout=mx.CBF, shape=(32, 32, 9, 9))
     with pytest.raises(mx.MxconvError, match="code -2"):
-        mx.nvfp_fwd(cv, q["w"], x8)
+        mx.nvfp_fwd(cv, q["w"], x8)                                   # FP4 weights with FP8 activations
+    cv3 = synth.conv_dict(32, 32, 32, 9, 9, 3, 1, 1)
+    shp = (32, 32, 9, 9)
+    x6 = mx.nvfp_quantize(synth.nchw_to_cbf(synth.normal(shp, 1.0, 4), 32).to(DEV), mx.ACT, 3, layout=mx.CBF, shape=shp)
+    w6 = mx.nvfp_quantize(synth.kaiming(32, 32, 3, 3, seed=6).to(DEV), mx.WEIGHT, 3, shape=(32, 32, 3, 3))
+    with pytest.raises(mx.MxconvError, match="code -2"):
+        mx.nvfp_fwd(cv3, w6, x6)                                      # E3M2 x E3M2
