@@ -198,7 +198,10 @@ template <int F> struct LdsBlock {
 // each 32-row block it holds (4 KB of scale entries instead of 1 KB), the
 // fragments are decoded to fp16 and multiplied on fp16 MFMAs, and the result
 // is multiplied by the two per-tensor scales.
-template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW, bool NV = false, int NRB = 2, bool KR = false>
+// Q: the kernel may run the fused quantizing epilogue (p.qcodes); the
+// grouped backward kernel never does and compiles it out.
+template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW, bool NV = false, int NRB = 2, bool KR = false,
+          bool Q = true>
 __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phase& f) {
     static_assert(!NV || (FW == FX && FW != MXC_E3M2) || (FW == MXC_E2M1 && FX == MXC_E3M2),
                   "NVFP pairs: one format (FP4, E2M3, FP8), or FP4 weights with E3M2 activations");
@@ -684,13 +687,13 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                 for (int e = 0; e < 16; e++) acc[rb][cn][e] *= tt;
     }
     const int m = mt * 32 * RBW + 32 * NRB * wm + (lane & 31);
-    if ((p.layout == MXC_CBF || p.layout == MXC_CBF_BF16) && !p.qcodes)
+    if ((p.layout == MXC_CBF || p.layout == MXC_CBF_BF16) && !(Q && p.qcodes))
         __syncthreads();                                 // every wave is done with the stage buffers
     uint8_t* const ep = smem + wave * 4096;
     const int er = lane >> 3, ec = lane & 7;            // read-back: row er + 8 i, chunk ec
     const int y = f.ry + DS * yi;
     if (zpf) vm_wait<0>();                               // the z copies (a phase with no taps ran no stage)
-    if (p.qcodes) {
+    if (Q && p.qcodes) {
         // ---- fused quantizing epilogue: acc[rb][cn] is one whole MX block of
         // the output (32 channels x 32 samples at one pixel); lane l holds
         // channel l % 32 and samples 8 (e / 4) + 4 (l / 32) + e % 4.  The
@@ -739,6 +742,81 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                     }
                 }
                 const int rows = min(32, p.M - cb * 32);
+                const bool q8 = p.qfmt == MXC_E4M3, q6 = p.qfmt == MXC_E2M3 || p.qfmt == MXC_E3M2;
+                if (!DG && rows <= 16 && !q6) {
+                    // ---- a forward block with at most 16 real rows (a
+                    // 16-channel layer): lanes 16..31 of each half hold padding rows.
+                    // Lane (r + 16, h) takes samples 16 + 4 h .. (e4 = 2, 3)
+                    // of row r from lane (r, h), which keeps e4 = 0, 1, so
+                    // each lane activates and quantizes 8 values instead of
+                    // 16 (the values, codes and stored bytes are unchanged).
+                    const int row = r & 15, k0 = (r >> 4) * 2;
+                    float u[8];
+#pragma unroll
+                    for (int i = 0; i < 8; i++) {
+                        const float o = __shfl_xor(v[8 + i], 16);
+                        u[i] = r >= 16 ? o : v[i];
+                    }
+                    // the values of one block through LDS to global memory:
+                    // bf16 (2 KB, 64-byte rows) or fp32 (4 KB, 128-byte rows)
+                    auto stage_out = [&](const float* w, bool as_bf16, void* dst) {
+                        if (as_bf16) {
+#pragma unroll
+                            for (int k = 0; k < 2; k++)
+                                *(uint2*)(ep4 + bf16_lds(row, k0 + k) + 8 * h) =
+                                    bf16_pack4(w[4 * k], w[4 * k + 1], w[4 * k + 2], w[4 * k + 3]);
+                            const int rr = lane >> 2, ch = lane & 3;      // rows 0..15: one chunk per lane
+                            const uint4 d = *(const uint4*)(ep4 + bf16_lds(rr, ch));
+                            if (rr < rows) store_nt((uint16_t*)dst + rr * 32 + ch * 8, d);
+                        } else {
+#pragma unroll
+                            for (int k = 0; k < 2; k++)
+                                *(float4*)(ep4 + row * 128 + (((2 * (k0 + k) + h) ^ (row & 7)) << 4)) =
+                                    make_float4(w[4 * k], w[4 * k + 1], w[4 * k + 2], w[4 * k + 3]);
+#pragma unroll
+                            for (int i = 0; i < 2; i++) {
+                                const int rr = er + 8 * i;
+                                const float4 d = *(const float4*)(ep4 + rr * 128 + ((ec ^ (rr & 7)) << 4));
+                                if (rr < rows) store_nt((float*)dst + rr * 32 + 4 * ec, d);
+                            }
+                        }
+                    };
+                    const size_t ob = (pix * p.M + (size_t)cb * 32) * 32;   // the block in a CBF tensor
+                    if (p.out && p.pre_out)
+                        stage_out(u, p.bf16, p.bf16 ? (void*)((uint16_t*)p.out + ob) : (void*)(p.out + ob));
+                    if (p.fn != MXC_FN_NONE) {
+#pragma unroll
+                        for (int i = 0; i < 8; i++) u[i] = fn_apply(p.fn, u[i]);
+                    }
+                    if (p.out && !p.pre_out) stage_out(u, false, p.out + ob);
+                    uint32_t mm = 0;
+#pragma unroll
+                    for (int i = 0; i < 8; i++) mm = max(mm, __float_as_uint(u[i]) & 0x7FFFFFFFu);
+                    mm = wave_max_u32(mm);
+                    const uint32_t sc = q8 ? scale_code_from_bits<8>(mm) : scale_code_from_bits<2>(mm);
+                    const float inv = inv_scale(sc);
+                    const bool bad = sc == 0xFFu;
+                    if (lane == 0) p.qscales[pix * p.q_ncb + cb] = (uint8_t)sc;
+                    if (q8) {   // 32-byte rows; rows 16..31 are +0 codes
+#pragma unroll
+                        for (int k = 0; k < 2; k++)
+                            *(uint32_t*)(ep + row * 32 + 8 * (k0 + k) + 4 * h) =
+                                bad ? 0u : pack4_e4m3(make_float4(u[4 * k], u[4 * k + 1], u[4 * k + 2], u[4 * k + 3]), inv);
+                        *(uint2*)(ep + 512 + 8 * lane) = make_uint2(0u, 0u);
+                        const uint4 chunk = *(const uint4*)(ep + lane * 16);
+                        *(uint4*)(p.qcodes + (pix * p.q_ncb + cb) * 1024 + lane * 16) = chunk;
+                    } else {    // 16-byte rows
+#pragma unroll
+                        for (int k = 0; k < 2; k++)
+                            *(unsigned short*)(ep + row * 16 + 4 * (k0 + k) + 2 * h) =
+                                bad ? (unsigned short)0
+                                    : pack4_e2m1(make_float4(u[4 * k], u[4 * k + 1], u[4 * k + 2], u[4 * k + 3]), inv);
+                        *(uint32_t*)(ep + 256 + 4 * lane) = 0u;
+                        const uint2 chunk = *(const uint2*)(ep + lane * 8);
+                        *(uint2*)(p.qcodes + (pix * p.q_ncb + cb) * 512 + lane * 8) = chunk;
+                    }
+                    continue;
+                }
                 if (p.out && p.pre_out) {   // the pre-activation, for the backward pass
                     if (p.bf16) store_bf16_tile(ep4, v, (uint16_t*)p.out + (pix * p.M + (size_t)cb * 32) * 32, rows, lane);
                     else        store_block(v, pix, cb);
@@ -782,7 +860,6 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
 #pragma unroll
                 for (int e = 0; e < 16; e++) m = max(m, __float_as_uint(v[e]) & 0x7FFFFFFFu);
                 m = wave_max_u32(m);
-                const bool q8 = p.qfmt == MXC_E4M3, q6 = p.qfmt == MXC_E2M3 || p.qfmt == MXC_E3M2;
                 const uint32_t sc = q8 ? scale_code_from_bits<8>(m)
                                   : p.qfmt == MXC_E3M2 ? scale_code_from_bits<4>(m) : scale_code_from_bits<2>(m);
                 const float inv = inv_scale(sc);
@@ -912,7 +989,8 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
 }
 
 // Workgroup `bid` of `nblk` (a multiple of 8).
-template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW, bool NV = false, int NRB = 2, bool KR = false>
+template <int FW, int FX, bool DG, int KW, int S, int WGM, int PW, bool NV = false, int NRB = 2, bool KR = false,
+          bool Q = true>
 __device__ __forceinline__ void lean_body(const LeanArgs& p, int bid, int nblk) {
     // XCD-aware order: consecutive tiles (same output row) on one XCD
     const int per_xcd = (nblk + 7) / 8;
@@ -921,7 +999,7 @@ __device__ __forceinline__ void lean_body(const LeanArgs& p, int bid, int nblk) 
     Phase f;
     f.ry = 0; f.rx = 0; f.kh0 = 0; f.nvh = p.kh; f.kw0 = 0;
     f.gh = p.hout; f.gw = p.wout; f.c0 = p.pw; f.r0 = p.ph;
-    lean_tile<FW, FX, DG, KW, S, WGM, PW, NV, NRB, KR>(p, lin, f);
+    lean_tile<FW, FX, DG, KW, S, WGM, PW, NV, NRB, KR, Q>(p, lin, f);
 }
 
 // Every lean kernel asks for at least two waves per SIMD.  Left to itself
@@ -938,7 +1016,7 @@ __global__ __launch_bounds__(LT) __attribute__((amdgpu_waves_per_eu(2))) void co
 
 // Stride-2 input gradient for kernel width KWF (1 or 3): the four phases in
 // one launch, tiles of phase (ry, rx) at [pofs[2 ry + rx], pofs[2 ry + rx + 1]).
-template <int FW, int FX, int KWF, int WGM, int PW, bool NV = false, int NRB = 2, bool KR = false>
+template <int FW, int FX, int KWF, int WGM, int PW, bool NV = false, int NRB = 2, bool KR = false, bool Q = true>
 __device__ __forceinline__ void lean_dg2_body(const LeanArgs& p, int bid, int nblk) {
     const int per_xcd = (nblk + 7) / 8;
     int lin = (bid % 8) * per_xcd + bid / 8;
@@ -955,8 +1033,8 @@ __device__ __forceinline__ void lean_dg2_body(const LeanArgs& p, int bid, int nb
     if (nvw == 0) f.nvh = 0;                       // no tap reaches the phase: its pixels are zero
     f.gh = (p.hout - f.ry + 1) / 2; f.gw = (p.wout - f.rx + 1) / 2;
     f.c0 = (f.rx + p.pw - f.kw0) / 2; f.r0 = (f.ry + p.ph - f.kh0) / 2;
-    if (KWF == 3 && nvw == 2) lean_tile<FW, FX, true, 2, 2, WGM, PW, NV, NRB, KR>(p, lin, f);
-    else                      lean_tile<FW, FX, true, 1, 2, WGM, PW, NV, NRB, KR>(p, lin, f);
+    if (KWF == 3 && nvw == 2) lean_tile<FW, FX, true, 2, 2, WGM, PW, NV, NRB, KR, Q>(p, lin, f);
+    else                      lean_tile<FW, FX, true, 1, 2, WGM, PW, NV, NRB, KR, Q>(p, lin, f);
 }
 
 template <int FW, int FX, int KWF, int WGM, int PW, bool NV = false, int NRB = 2, bool KR = false>
@@ -978,8 +1056,8 @@ __global__ __launch_bounds__(LT) __attribute__((amdgpu_waves_per_eu(2))) void co
     const int b = blockIdx.x;
     const int nw = (int)gridDim.x - nl;
     if (b >= nw) {
-        if constexpr (DG2) lean_dg2_body<F, F, KW, 1, PW, false, NRB, KR>(p, b - nw, nl);
-        else               lean_body<F, F, true, KW, 1, 1, PW, false, NRB, KR>(p, b - nw, nl);
+        if constexpr (DG2) lean_dg2_body<F, F, KW, 1, PW, false, NRB, KR, false>(p, b - nw, nl);
+        else               lean_body<F, F, true, KW, 1, 1, PW, false, NRB, KR, false>(p, b - nw, nl);
     } else {
         wgrad_tile<F, F, false, NB>(q, b, nw, (float (*)[32 * NB * 32 * NB])smem);
     }
