@@ -26,12 +26,14 @@ time by kind, per-layer algorithmic bytes against the naive comparator);
 MXFP4, measured the same way); `layer_sweep` (the three-layer sweep at batch
 32 in MXFP8 and MXFP4 with steady-state per-op times, the measured naive
 comparator, and the fused-epilogue, FP6, stochastic-rounding and NVFP4
-legs); `cpu_baseline` (the fp64 oracle on a bounded sample of the headline
+legs, the NVFP GEMMs of every element-format combination); `cpu_baseline`
+(the fp64 oracle on a bounded sample of the headline
 workload, on the host).
 
     python bench.py [--steps K] [--warmup W] [--no-cpu-baseline] [--no-sweep] [--no-qlr]
     python bench.py --pmc-pass {yolo,qlr,sweep}        (under rocprofv3 --pmc)
     python bench.py --summarize-trace DIR LOG | --summarize-pmc FDIR WDIR FLOG WLOG
+    python bench.py --summarize-sq LOG DIR [DIR ...]    (SQ counters of the MFMA-heavy calls)
 """
 import argparse
 import json
@@ -52,6 +54,9 @@ FMT_NAME = {0: "mxfp8", 1: "mxfp4"}
 # (Sec. VI-B) use E2M3 throughout
 FP6_METHODS = {"microqonv_plus": (1, 3, 1), "microqonv_6": (2, 2, 2)}
 FP6_SLACK = 16                                     # read slack at the end of an FP6 code buffer
+# NVFP methods besides NVFP4, as (W, X, G_Y) element formats: the "-8"
+# methods, the "-6" methods (Sec. VI-B, E2M3) and MicroQonv+ (Sec. IV-D)
+NV_METHODS = {"nvfp8": (0, 0, 0), "nvfp6_e2m3": (2, 2, 2), "microqonv_plus": (1, 3, 1)}
 
 
 def layer_numbers(cv, fmt, mx):
@@ -693,6 +698,20 @@ def sweep_leg(args):
             r["layer_ms"] = round(sum(t.values()), 4)
             r["layer_ms_vs_mxfp4"] = round(sum(t.values()) / fp4, 3)
             nvfp[f"{lname}/nvfp4"] = r
+            # the GEMMs of the other NVFP methods: (W, X, G_Y) element formats
+            for meth, (fw_, fx_, fg_) in NV_METHODS.items():
+                mw = mx.nvfp_quantize(j["w"], mx.WEIGHT, fw_, workspace=wsn)
+                mxq = mx.nvfp_quantize(j["x"], mx.ACT, fx_, layout=mx.CBF, shape=j["xs"], workspace=wsn)
+                mg = mx.nvfp_quantize(j["gy"], mx.ACT, fg_, layout=mx.CBF, shape=j["gs"], workspace=wsn)
+                wsm = torch.empty(max(1, mx.wgrad_workspace_bytes(cv, mx.pair(fg_, fx_))), dtype=torch.uint8,
+                                  device=dev)
+                tm = {"fwd": steady_ms(lambda: mx.nvfp_fwd(cv, mw, mxq, layout=mx.CBF, out=j["y"])),
+                      "dgrad": steady_ms(lambda: mx.nvfp_dgrad(cv, mw, mg, layout=mx.CBF, out=j["gx"])),
+                      "wgrad": steady_ms(lambda: mx.nvfp_wgrad(cv, mg, mxq, out=j["gw"], workspace=wsm))}
+                rm = {k + "_ms": round(v, 4) for k, v in tm.items()}
+                rm.update({g + "_tflops": round(fl / (tm[g] * 1e-3) / 1e12, 1) for g in tm})
+                nvfp[f"{lname}/{meth}"] = rm
+                del mw, mxq, mg, wsm
             del xsrc, gsrc
 
     gemm_flops = sum(j["nums"][op][0] for j in jobs for op in ("fwd", "dgrad", "wgrad"))
@@ -929,7 +948,7 @@ def pmc_pass(calls, label):
         dst.copy_(src)
     torch.cuda.synchronize()
     return {"pmc_pass": label, "calls": [c[0] for c in calls], "algorithmic_bytes": [c[3] for c in calls],
-            "copy_bytes": COPY_BYTES, "source_digest": source_digest()}
+            "algorithmic_flops": [c[2] for c in calls], "copy_bytes": COPY_BYTES, "source_digest": source_digest()}
 
 
 def _bench_line(log):
@@ -1078,6 +1097,79 @@ def summarize_pmc(fdir, wdir, flog, wlog):
     return "\n".join(L) + "\n"
 
 
+# Shader-sequencer counters of the MFMA-heavy calls, two passes of eight
+SQ_PASSES = (("SQ_WAVES", "SQ_WAVE_CYCLES", "SQ_WAIT_ANY", "SQ_WAIT_INST_ANY", "SQ_VALU_MFMA_BUSY_CYCLES",
+              "SQ_INSTS_MFMA", "SQ_ACTIVE_INST_ANY", "SQ_BUSY_CYCLES"),
+             ("SQ_WAVES", "SQ_INSTS_LDS", "SQ_INSTS_VALU", "SQ_INSTS_SALU", "SQ_INSTS_VMEM", "SQ_WAIT_INST_LDS",
+              "SQ_LDS_BANK_CONFLICT", "SQ_ACTIVE_INST_LDS"))
+
+
+def summarize_sq(log, *dirs):
+    """Markdown summary of `rocprofv3 --pmc` runs with the SQ_PASSES counter
+    sets over `bench.py --pmc-pass <workload>`: for every call with matrix
+    products, where its waves spend their time (wave-cycles waiting, matrix
+    core busy cycles, instructions issued per wave)."""
+    import statistics
+    info = _bench_line(log)
+    calls, flops = info["calls"], info["algorithmic_flops"]
+    vals = [dict() for _ in calls]
+    durs = [None] * len(calls)
+    names = [set() for _ in calls]
+    for d in dirs:
+        disp = {}
+        for r in _csv_rows(d, "counter_collection.csv"):
+            disp.setdefault(int(r["Dispatch_Id"]), []).append(r)
+        segs, cur = [], None
+        for k in sorted(disp):
+            if "spin_kernel" in disp[k][0]["Kernel_Name"]:
+                cur = []
+                segs.append(cur)
+            elif cur is not None:
+                cur.append(disp[k])
+        segs = segs[-(len(calls) + 1):-1]
+        if len(segs) != len(calls):
+            raise SystemExit(f"{d}: found {len(segs)} delimited segments, expected {len(calls)}")
+        for i, seg in enumerate(segs):
+            got = {}
+            for rs in seg:
+                names[i].add(_short(rs[0]["Kernel_Name"]))
+                for r in rs:
+                    got[r["Counter_Name"]] = got.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+            for k, v in got.items():
+                vals[i].setdefault(k, v)
+            if durs[i] is None:
+                durs[i] = sum((int(rs[0]["End_Timestamp"]) - int(rs[0]["Start_Timestamp"])) / 1000.0 for rs in seg)
+    label = info["pmc_pass"]
+    L = [f"# Shader-sequencer counters of the matrix-product calls: {label} step, MXFP4\n"]
+    L.append("Two counter passes (repository root on an MI355X machine; summary by bench.py --summarize-sq):\n")
+    for j, ps in enumerate(SQ_PASSES):
+        L.append(f"    cd /tmp && export TMPDIR=/tmp && timeout -s KILL 180 rocprofv3 --pmc {' '.join(ps)} "
+                 f"--output-format csv -d <repo>/gpurun_out/sq_{label}_{j} -o p -- python3 <repo>/bench.py "
+                 f"--pmc-pass {label} --warmup 2 > <repo>/gpurun_out/sq_{label}_{j}.log")
+    L.append(f"\nsource digest: `{info['source_digest']}`\n")
+    L.append("Columns: kernel time under counter collection; fraction of the MXFP4 peak (10.1 PFLOP/s) the call's "
+             "flops reach in that time; matrix-core busy cycles over the SIMD-cycles of the call (1024 SIMDs at "
+             "2.4 GHz); a wave's lifetime (SQ_WAVE_CYCLES x 4 / SQ_WAVES); the share of it spent waiting for "
+             "anything (SQ_WAIT_ANY / SQ_WAVE_CYCLES) and waiting to issue (SQ_WAIT_INST_ANY / SQ_WAVE_CYCLES); "
+             "instructions issued per wave; LDS bank-conflict cycles per LDS-active cycle.\n")
+    L.append("| call | kernel | us | frac of peak | MFMA busy | wave cycles | waiting | issue wait | MFMA / VALU / "
+             "SALU / LDS / VMEM per wave | LDS conflict |")
+    L.append("|---|---|---|---|---|---|---|---|---|---|")
+    for i, c in enumerate(calls):
+        v = vals[i]
+        if not flops[i] or not v.get("SQ_INSTS_MFMA"):
+            continue
+        us, w = durs[i], max(v.get("SQ_WAVES", 0.0), 1.0)
+        wc = max(v.get("SQ_WAVE_CYCLES", 0.0), 1.0)
+        per = " / ".join(f"{v.get(k, 0.0) / w:.0f}" for k in ("SQ_INSTS_MFMA", "SQ_INSTS_VALU", "SQ_INSTS_SALU",
+                                                              "SQ_INSTS_LDS", "SQ_INSTS_VMEM"))
+        L.append(f"| {c} | {'+'.join(sorted(names[i]))} | {us:.1f} | {flops[i] / (us * 1e-6) / 10.1e15:.3f} | "
+                 f"{v.get('SQ_VALU_MFMA_BUSY_CYCLES', 0.0) / (1024 * us * 2400.0):.3f} | {4 * wc / w:.0f} | "
+                 f"{v.get('SQ_WAIT_ANY', 0.0) / wc:.2f} | {v.get('SQ_WAIT_INST_ANY', 0.0) / wc:.2f} | {per} | "
+                 f"{v.get('SQ_LDS_BANK_CONFLICT', 0.0) / max(v.get('SQ_ACTIVE_INST_LDS', 0.0), 1.0):.3f} |")
+    return "\n".join(L) + "\n"
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -1097,6 +1189,8 @@ def main():
     ap.add_argument("--fmts", default="0,1", help="layer sweep: formats")
     ap.add_argument("--summarize-trace", nargs=2, metavar=("ROCPROF_DIR", "BENCH_LOG"),
                     help="write the kernel-trace summary of a rocprofv3 run of this script to stdout")
+    ap.add_argument("--summarize-sq", nargs="+", metavar="LOG_THEN_DIRS",
+                    help="SQ-counter summary: the --pmc-pass log, then the rocprofv3 output directories")
     ap.add_argument("--summarize-pmc", nargs=4, metavar=("FETCH_DIR", "WRITE_DIR", "FETCH_LOG", "WRITE_LOG"),
                     help="write the counter summary of two rocprofv3 --pmc runs of --pmc-pass to stdout")
     args = ap.parse_args()
@@ -1105,6 +1199,9 @@ def main():
         return
     if args.summarize_pmc:
         print(summarize_pmc(*args.summarize_pmc))
+        return
+    if args.summarize_sq:
+        print(summarize_sq(*args.summarize_sq))
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported: every GPU box here has one GPU, "
