@@ -1059,7 +1059,7 @@ __global__ __launch_bounds__(LT) __attribute__((amdgpu_waves_per_eu(2))) void co
         if constexpr (DG2) lean_dg2_body<F, F, KW, 1, PW, false, NRB, KR, false>(p, b - nw, nl);
         else               lean_body<F, F, true, KW, 1, 1, PW, false, NRB, KR, false>(p, b - nw, nl);
     } else {
-        wgrad_tile<F, F, false, NB>(q, b, nw, (float (*)[32 * NB * 32 * NB])smem);
+        wgrad_tile<F, F, false, NB, (NB == 1 && KW == 3) ? 3 : 1>(q, b, nw, (float (*)[32 * NB * 32 * NB])smem);
     }
 }
 

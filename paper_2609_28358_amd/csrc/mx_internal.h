@@ -128,6 +128,9 @@ int wgrad_lean_splits(const Conv& cv);
 inline bool wgrad_single_block(const Conv& cv) {
     return cv.gy.ncb == 1 && cv.x.ncb == 1 && cv.fa == cv.fb && (cv.fa == MXC_E4M3 || cv.fa == MXC_E2M1);
 }
+// taps of one kernel row a weight-gradient wave takes together: the three of
+// a 3-wide kernel on 32 x 32 MX tiles (G_Y loaded once for all three), else 1
+inline int wgrad_taps(const Conv& cv, bool nv) { return !nv && wgrad_single_block(cv) && cv.kw == 3 ? 3 : 1; }
 int launch_wgrad_lean(const Conv& cv, const void* gc, const uint8_t* gs, const void* xc, const uint8_t* xs,
                       float* dst, int splits, hipStream_t s, const float* nv_tg = nullptr,
                       const float* nv_tx = nullptr);

@@ -24,10 +24,10 @@ namespace mxc {
 
 namespace {
 
-template <int FA, int FB, bool NV = false, int NB = 2>
+template <int FA, int FB, bool NV = false, int NB = 2, int KT = 1>
 __global__ __launch_bounds__(WT) void wgrad_lean_kernel(WLArgs p) {
     __shared__ float red[4][32 * NB * 32 * NB];
-    wgrad_tile<FA, FB, NV, NB>(p, blockIdx.x, gridDim.x, red);
+    wgrad_tile<FA, FB, NV, NB, KT>(p, blockIdx.x, gridDim.x, red);
 }
 
 }  // namespace
@@ -38,7 +38,7 @@ int wgrad_lean_splits(const Conv& cv) {
     if (cv.x.bn != 32) return 0;
     const long npix = (long)cv.x.ng * cv.ho * cv.wo;
     const long npairs = (npix + 1) / 2;
-    const long ntiles = (long)cv.kh * cv.kw * ((cv.gy.ncb + 1) / 2) * ((cv.x.ncb + 1) / 2);
+    const long ntiles = (long)cv.kh * (cv.kw / wgrad_taps(cv, false)) * ((cv.gy.ncb + 1) / 2) * ((cv.x.ncb + 1) / 2);
     if (npix > 0x3FFFFFFFL || ntiles > 0x7FFFFFL) return 0;
     // about two workgroups per CU, each wave with at least 4 pixel pairs; a
     // layer on 32 x 32 tiles (one channel block on each side) keeps a quarter
@@ -72,12 +72,15 @@ int launch_wgrad_lean(const Conv& cv, const void* gc, const uint8_t* gs, const v
         return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
     }
     const bool nb1 = wgrad_single_block(cv);
+    const bool kt3 = wgrad_taps(cv, false) == 3;
     if (cv.fa == MXC_E4M3 && cv.fb == MXC_E4M3) {
-        if (nb1) hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E4M3, MXC_E4M3, false, 1>), gd, dim3(WT), 0, s, a);
-        else     hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E4M3, MXC_E4M3>), gd, dim3(WT), 0, s, a);
+        if (kt3)      hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E4M3, MXC_E4M3, false, 1, 3>), gd, dim3(WT), 0, s, a);
+        else if (nb1) hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E4M3, MXC_E4M3, false, 1>), gd, dim3(WT), 0, s, a);
+        else          hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E4M3, MXC_E4M3>), gd, dim3(WT), 0, s, a);
     } else if (cv.fa == MXC_E2M1 && cv.fb == MXC_E2M1) {
-        if (nb1) hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E2M1, MXC_E2M1, false, 1>), gd, dim3(WT), 0, s, a);
-        else     hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E2M1, MXC_E2M1>), gd, dim3(WT), 0, s, a);
+        if (kt3)      hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E2M1, MXC_E2M1, false, 1, 3>), gd, dim3(WT), 0, s, a);
+        else if (nb1) hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E2M1, MXC_E2M1, false, 1>), gd, dim3(WT), 0, s, a);
+        else          hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E2M1, MXC_E2M1>), gd, dim3(WT), 0, s, a);
     }
     else if (cv.fa == MXC_E2M3 && cv.fb == MXC_E2M3) hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E2M3, MXC_E2M3>), gd, dim3(WT), 0, s, a);
     else if (cv.fa == MXC_E2M1 && cv.fb == MXC_E3M2) hipLaunchKernelGGL((wgrad_lean_kernel<MXC_E2M1, MXC_E3M2>), gd, dim3(WT), 0, s, a);

@@ -72,11 +72,15 @@ __device__ __forceinline__ v8i row_frag(const uint8_t* p0, const uint8_t* p1, co
 // whose G_Y and X both have a single channel block (a 32 x 32 tile: half the
 // loads and a quarter of the products per pixel pair, so twice the pairs per
 // batch).
-template <int FA, int FB, bool NV = false, int NB = 2>
+// KT: taps of one kernel row per wave (3 for a 3-wide kernel on 32 x 32
+// tiles, else 1): each G_Y fragment of a pixel pair is loaded once and
+// multiplied with the X fragments of all KT taps, instead of once per tap.
+template <int FA, int FB, bool NV = false, int NB = 2, int KT = 1>
 __device__ __forceinline__ void wgrad_tile(const WLArgs& p, int bid, int nblk, float (*red)[32 * NB * 32 * NB]) {
     static_assert(!NV || (FA == FB && FA != MXC_E3M2) || (FA == MXC_E2M1 && FB == MXC_E3M2),
                   "NVFP pairs: one format (FP4, E2M3, FP8), or FP4 gradients with E3M2 activations");
     static_assert(NB == 1 || NB == 2, "one or two blocks per tile side");
+    static_assert(KT == 1 || (NB == 1 && !NV), "several taps per wave on 32 x 32 MX tiles only");
     constexpr int RS = 32 * NB;                   // tile side; red[wave] holds RS x RS floats
     constexpr int RBA = 32 * fmt_bits(FA) / 8;    // bytes of one block row (32 samples): G_Y
     constexpr int RBB = 32 * fmt_bits(FB) / 8;    // X
@@ -94,7 +98,8 @@ __device__ __forceinline__ void wgrad_tile(const WLArgs& p, int bid, int nblk, f
     const int tap = tile / (p.cot * p.cit);
     const int rc = tile % (p.cot * p.cit);
     const int cop = rc / p.cit, cip = rc % p.cit;
-    const int th = tap / p.kw, tw = tap % p.kw;
+    const int kwg = p.kw / KT;                    // tap groups per kernel row
+    const int th = tap / kwg, tw = (tap % kwg) * KT;   // kernel row, first tap of the group
     const int r = lane & 31, hf = lane >> 5;
 
     // lane offsets inside one pixel's codes, and block validity
@@ -115,13 +120,15 @@ __device__ __forceinline__ void wgrad_tile(const WLArgs& p, int bid, int nblk, f
     }
     const uint32_t gy_pix = (uint32_t)p.gy_ncb * TBA, x_pix = (uint32_t)p.x_ncb * TBB;
 
-    v16f acc[NB][NB];
+    v16f acc[KT][NB][NB];
 #pragma unroll
-    for (int i = 0; i < NB; i++)
+    for (int t = 0; t < KT; t++)
 #pragma unroll
-        for (int j = 0; j < NB; j++)
+        for (int i = 0; i < NB; i++)
 #pragma unroll
-            for (int e = 0; e < 16; e++) acc[i][j][e] = 0.0f;
+            for (int j = 0; j < NB; j++)
+#pragma unroll
+                for (int e = 0; e < 16; e++) acc[t][i][j][e] = 0.0f;
 
     const int wid = split * 4 + wave;
     const int q0 = wid * p.ppw;
@@ -129,8 +136,8 @@ __device__ __forceinline__ void wgrad_tile(const WLArgs& p, int bid, int nblk, f
 
     // operands of one pair (pixels 2 j and 2 j + 1 of an output row)
     struct Ops {
-        v8i a[2], b[2];
-        int sa[2], sb[2];
+        v8i a[2], b[KT][2];
+        int sa[2], sb[KT][2];
         uint32_t na[2], nb[2];     // NV: the four E4M3 scales of the lane's row
     };
 
@@ -161,20 +168,25 @@ __device__ __forceinline__ void wgrad_tile(const WLArgs& p, int bid, int nblk, f
     // the wave's range) and of X (also inside the input), and their pixel
     // offsets within the row bases
     auto load = [&](bool live, Ops& o) {
-        int oxk[2], ixk[2];
-        bool va[2], vb[2];
+        int oxk[2];
+        bool va[2];
+        int ixk[KT][2];
+        bool vb[KT][2];
 #pragma unroll
         for (int k = 0; k < 2; k++) {
             const int ox = 2 * pj + k;
-            const int ix = ox * p.sw + tw - p.pw;
             va[k] = live && ox < p.wo;
-            vb[k] = va[k] && rv && ix >= 0 && ix < p.w;
             oxk[k] = va[k] ? ox : 0;
-            ixk[k] = vb[k] ? ix : 0;
+#pragma unroll
+            for (int t = 0; t < KT; t++) {
+                const int ix = ox * p.sw + tw + t - p.pw;
+                vb[t][k] = va[k] && rv && ix >= 0 && ix < p.w;
+                ixk[t][k] = vb[t][k] ? ix : 0;
+            }
         }
         // the lane's own pixel (FP4 / FP6, and the scales of every format)
-        const int oxh = hf ? oxk[1] : oxk[0], ixh = hf ? ixk[1] : ixk[0];
-        const bool vah = hf ? va[1] : va[0], vbh = hf ? vb[1] : vb[0];
+        const int oxh = hf ? oxk[1] : oxk[0];
+        const bool vah = hf ? va[1] : va[0];
         const uint8_t* const gr = p.gc + ga_row;
         const uint8_t* const xr = p.xc + xb_row;
 #pragma unroll
@@ -182,21 +194,29 @@ __device__ __forceinline__ void wgrad_tile(const WLArgs& p, int bid, int nblk, f
             const uint8_t* a0 = gr + (uint32_t)oxk[0] * gy_pix + a_off[i];
             const uint8_t* a1 = gr + (uint32_t)oxk[1] * gy_pix + a_off[i];
             const uint8_t* ah = gr + (uint32_t)oxh * gy_pix + a_off[i];
-            const uint8_t* b0 = xr + (uint32_t)ixk[0] * x_pix + b_off[i];
-            const uint8_t* b1 = xr + (uint32_t)ixk[1] * x_pix + b_off[i];
-            const uint8_t* bh = xr + (uint32_t)ixh * x_pix + b_off[i];
             o.a[i] = row_frag<FA>(a0, a1, ah, va[0] && a_row[i], va[1] && a_row[i], vah && a_row[i]);
-            o.b[i] = row_frag<FB>(b0, b1, bh, vb[0] && b_row[i], vb[1] && b_row[i], vbh && b_row[i]);
             // scale of (row, K block hf): the pixel of this lane's half
             const int cob = 2 * cop + i, cib = 2 * cip + i;
-            const bool sav = vah && a_ok[i], sbv = vbh && b_ok[i];
+            const bool sav = vah && a_ok[i];
             const uint8_t sa = p.gs[gs_row + (uint32_t)oxh * p.gy_ncb + (a_ok[i] ? cob : 0)];
-            const uint8_t sb = p.xs[xs_row + (uint32_t)ixh * p.x_ncb + (b_ok[i] ? cib : 0)];
             o.sa[i] = sav ? sa : 0;
-            o.sb[i] = sbv ? sb : 0;
+            int ixh = 0;
+            bool vbh = false;
+#pragma unroll
+            for (int t = 0; t < KT; t++) {
+                ixh = hf ? ixk[t][1] : ixk[t][0];
+                vbh = hf ? vb[t][1] : vb[t][0];
+                const uint8_t* b0 = xr + (uint32_t)ixk[t][0] * x_pix + b_off[i];
+                const uint8_t* b1 = xr + (uint32_t)ixk[t][1] * x_pix + b_off[i];
+                const uint8_t* bh = xr + (uint32_t)ixh * x_pix + b_off[i];
+                o.b[t][i] = row_frag<FB>(b0, b1, bh, vb[t][0] && b_row[i], vb[t][1] && b_row[i], vbh && b_row[i]);
+                const uint8_t sb = p.xs[xs_row + (uint32_t)ixh * p.x_ncb + (b_ok[i] ? cib : 0)];
+                o.sb[t][i] = vbh && b_ok[i] ? sb : 0;
+            }
             if constexpr (NV) {
                 // E4M3 scales of the lane's row: the four sample groups of a
-                // pixel in one word
+                // pixel in one word (KT == 1 here)
+                const bool sbv = vbh && b_ok[i];
                 const uint32_t* ga = (const uint32_t*)p.gs;
                 const uint32_t* xa = (const uint32_t*)p.xs;
                 const uint32_t ca = (uint32_t)(a_ok[i] ? cob : 0) * 4 + (r >> 3);
@@ -208,9 +228,9 @@ __device__ __forceinline__ void wgrad_tile(const WLArgs& p, int bid, int nblk, f
 #pragma unroll
                     for (int k = 0; k < 2; k++) {
                         const uint32_t u = ga[(pa_row + oxk[k]) * (p.gy_cp / 8) + ca];
-                        const uint32_t v = xa[(px_row + ixk[k]) * (p.x_cp / 8) + cb];
+                        const uint32_t v = xa[(px_row + ixk[0][k]) * (p.x_cp / 8) + cb];
                         wa[k] = va[k] && a_ok[i] ? (u >> (16 * hf)) & 0xFFFFu : 0u;
-                        wb[k] = vb[k] && b_ok[i] ? (v >> (16 * hf)) & 0xFFFFu : 0u;
+                        wb[k] = vb[0][k] && b_ok[i] ? (v >> (16 * hf)) & 0xFFFFu : 0u;
                     }
                     o.na[i] = wa[0] | wa[1] << 16;
                     o.nb[i] = wb[0] | wb[1] << 16;
@@ -227,7 +247,7 @@ __device__ __forceinline__ void wgrad_tile(const WLArgs& p, int bid, int nblk, f
     // batches of PB pairs: all loads of a batch are in flight together (the
     // loop is bound by memory latency, not by the MFMAs); pairs past the
     // wave's range get zero operands and add nothing
-    constexpr int PB = NV ? 2 : NB == 1 ? 8 : 4;
+    constexpr int PB = NV ? 2 : NB == 1 ? (KT > 1 ? 4 : 8) : 4;
     for (int q = q0; q < q1; q += PB) {
         Ops o[PB];
 #pragma unroll
@@ -246,30 +266,37 @@ __device__ __forceinline__ void wgrad_tile(const WLArgs& p, int bid, int nblk, f
 #pragma unroll
                 for (int i = 0; i < NB; i++) {
                     nv_decode32<FA>(o[b].a[i], o[b].na[i], ad[i]);
-                    nv_decode32<FB>(o[b].b[i], o[b].nb[i], bd[i]);
+                    nv_decode32<FB>(o[b].b[0][i], o[b].nb[i], bd[i]);
                 }
 #pragma unroll
                 for (int i = 0; i < NB; i++)
 #pragma unroll
                     for (int j = 0; j < NB; j++)
-                        acc[i][j] = FA == MXC_E4M3 ? mfma_x8(ad[i], bd[j], acc[i][j]) : mfma_nv(ad[i], bd[j], acc[i][j]);
+                        acc[0][i][j] = FA == MXC_E4M3 ? mfma_x8(ad[i], bd[j], acc[0][i][j])
+                                                      : mfma_nv(ad[i], bd[j], acc[0][i][j]);
             } else if constexpr (FA == MXC_E4M3) {   // MXFP8: each fragment decoded to bf16 once
-                uint32_t ad[NB][16], bd[NB][16];
+                uint32_t ad[NB][16];
 #pragma unroll
-                for (int i = 0; i < NB; i++) {
-                    e4m3_decode32_lane(o[b].a[i], o[b].sa[i], ad[i]);
-                    e4m3_decode32_lane(o[b].b[i], o[b].sb[i], bd[i]);
+                for (int i = 0; i < NB; i++) e4m3_decode32_lane(o[b].a[i], o[b].sa[i], ad[i]);
+#pragma unroll
+                for (int t = 0; t < KT; t++) {
+                    uint32_t bd[NB][16];
+#pragma unroll
+                    for (int j = 0; j < NB; j++) e4m3_decode32_lane(o[b].b[t][j], o[b].sb[t][j], bd[j]);
+#pragma unroll
+                    for (int i = 0; i < NB; i++)
+#pragma unroll
+                        for (int j = 0; j < NB; j++) acc[t][i][j] = mfma_x8(ad[i], bd[j], acc[t][i][j]);
                 }
-#pragma unroll
-                for (int i = 0; i < NB; i++)
-#pragma unroll
-                    for (int j = 0; j < NB; j++) acc[i][j] = mfma_x8(ad[i], bd[j], acc[i][j]);
             } else {
 #pragma unroll
-                for (int i = 0; i < NB; i++)
+                for (int t = 0; t < KT; t++)
 #pragma unroll
-                    for (int j = 0; j < NB; j++)
-                        acc[i][j] = mfma_mx<FA, FB>(o[b].a[i], o[b].b[j], acc[i][j], o[b].sa[i], o[b].sb[j]);
+                    for (int i = 0; i < NB; i++)
+#pragma unroll
+                        for (int j = 0; j < NB; j++)
+                            acc[t][i][j] = mfma_mx<FA, FB>(o[b].a[i], o[b].b[t][j], acc[t][i][j], o[b].sa[i],
+                                                           o[b].sb[t][j]);
             }
         }
     }
@@ -280,31 +307,36 @@ __device__ __forceinline__ void wgrad_tile(const WLArgs& p, int bid, int nblk, f
 #pragma unroll
             for (int j = 0; j < NB; j++)
 #pragma unroll
-                for (int e = 0; e < 16; e++) acc[i][j][e] *= tt;
+                for (int e = 0; e < 16; e++) acc[0][i][j][e] *= tt;
     }
 
-    // ---- sum the four waves' tiles, then write
+    // ---- per tap: sum the four waves' tiles, then write
 #pragma unroll
-    for (int i = 0; i < NB; i++)
+    for (int t = 0; t < KT; t++) {
+        if (t > 0) __syncthreads();                   // the previous tap's sums are read
 #pragma unroll
-        for (int j = 0; j < NB; j++)
+        for (int i = 0; i < NB; i++)
 #pragma unroll
-            for (int e = 0; e < 16; e++) {
-                const int row = 32 * i + 8 * (e >> 2) + 4 * hf + (e & 3);
-                red[wave][row * RS + 32 * j + r] = acc[i][j][e];
-            }
-    __syncthreads();
+            for (int j = 0; j < NB; j++)
+#pragma unroll
+                for (int e = 0; e < 16; e++) {
+                    const int row = 32 * i + 8 * (e >> 2) + 4 * hf + (e & 3);
+                    red[wave][row * RS + 32 * j + r] = acc[t][i][j][e];
+                }
+        __syncthreads();
+        const int ttap = th * p.kw + tw + t;
 #pragma unroll 4
-    for (int k = 0; k < RS * RS / WT; k++) {
-        const int idx = tid + WT * k;
-        const int row = idx / RS, col = idx % RS;
-        const float v = (red[0][idx] + red[1][idx]) + (red[2][idx] + red[3][idx]);
-        const int co = cop * 64 + row, ci = cip * 64 + col;
-        if (p.direct) {
-            if (co < p.cout && ci < p.cin)
-                p.dst[(((size_t)co * p.cin + ci) * p.kh + th) * p.kw + tw] = v;
-        } else if (co < p.gy_cp && ci < p.x_cp) {
-            p.dst[((size_t)split * p.gy_cp + co) * p.ntot + (size_t)tap * p.x_cp + ci] = v;
+        for (int k = 0; k < RS * RS / WT; k++) {
+            const int idx = tid + WT * k;
+            const int row = idx / RS, col = idx % RS;
+            const float v = (red[0][idx] + red[1][idx]) + (red[2][idx] + red[3][idx]);
+            const int co = cop * 64 + row, ci = cip * 64 + col;
+            if (p.direct) {
+                if (co < p.cout && ci < p.cin)
+                    p.dst[(((size_t)co * p.cin + ci) * p.kh + th) * p.kw + tw + t] = v;
+            } else if (co < p.gy_cp && ci < p.x_cp) {
+                p.dst[((size_t)split * p.gy_cp + co) * p.ntot + (size_t)ttap * p.x_cp + ci] = v;
+            }
         }
     }
 }
@@ -326,7 +358,7 @@ inline long wgrad_lean_fill(const Conv& cv, const void* gc, const uint8_t* gs, c
     a.ppr = (cv.wo + 1) / 2;
     a.npairs = cv.x.ng * cv.ho * a.ppr;
     a.cot = (cv.gy.ncb + 1) / 2; a.cit = (cv.x.ncb + 1) / 2;
-    a.ntiles = cv.kh * cv.kw * a.cot * a.cit;
+    a.ntiles = cv.kh * (cv.kw / wgrad_taps(cv, nv_tg != nullptr)) * a.cot * a.cit;
     const int waves = splits * 4;
     a.ppw = (a.npairs + waves - 1) / waves;
     a.nsplit = splits;
