@@ -136,6 +136,17 @@ def mxb(role, fmt, shape):
     return mx.codes_bytes(role, fmt, *shape) + mx.scales_bytes(role, fmt, *shape)
 
 
+def mxb_in(role, fmt, shape):
+    """Bytes a GEMM reads of an MX operand: an activation with a single
+    channel block contributes the code rows of its real channels only (its
+    padding rows are known +0 codes, never fetched); otherwise every stored
+    byte, as mxb."""
+    n, c, h, w = shape
+    if role == mx.ACT and c < 32:
+        return mx.codes_bytes(role, fmt, *shape) * c / 32.0 + mx.scales_bytes(role, fmt, *shape)
+    return mxb(role, fmt, shape)
+
+
 def real_flops(node, n):
     """2 N Cout Ho Wo Cin Kh Kw with real channels only (no padding)."""
     return 2.0 * n * node["cout"] * node["h"] * node["w"] * node["cin_real"] * node["k"] * node["k"]
@@ -283,7 +294,7 @@ class NetStep:
             oshape = (n, t["c"], t["h"], t["w"])
             if t["kind"] == "conv":
                 src = net.node(t["src"])
-                by = (mxb(W, fmt, tuple(self.w[nm][0].shape)) + mxb(A, fmt, (n, src["c"], src["h"], src["w"])) +
+                by = (mxb(W, fmt, tuple(self.w[nm][0].shape)) + mxb_in(A, fmt, (n, src["c"], src["h"], src["w"])) +
                       mxb(A, fmt, oshape) + es * math.prod(oshape))
                 seq.append((f"fwd {nm}", lambda nm=nm, t=t: mx.fwd_quant(
                     self.cv[nm], self.w[nm][1], self.t[t["src"]], fn=mx.FN_SILU | mx.FN_PRE_OUT | fbf, out=self.t[nm],
@@ -310,7 +321,8 @@ class NetStep:
                     terms, shape, fmt, fn=mx.FN_SILU | fbf, z=self.y[nm], out=self.gy[nm]), 0.0, by))
             src = net.node(t["src"])
             sshape = (n, src["c"], src["h"], src["w"])
-            xb = mxb(A, fmt, sshape)
+            xb = mxb_in(A, fmt, sshape)
+            gb = mxb_in(A, fmt, shape)
             wb = mxb(W, fmt, tuple(self.w[nm][0].shape))
             gwb = 4.0 * self.gw[nm].numel()
             f = real_flops(t, n)
@@ -318,19 +330,19 @@ class NetStep:
                 sn = t["src"]
                 seq.append((f"dgrad_quant {nm}", lambda nm=nm, sn=sn: mx.dgrad_quant(
                     self.cv[nm], self.w[nm][1], self.gy[nm], fn=mx.FN_SILU | fbf, z=self.y[sn], out=self.gy[sn]),
-                    f, wb + mxb(A, fmt, shape) + es * math.prod(sshape) + mxb(A, fmt, sshape)))
+                    f, wb + gb + es * math.prod(sshape) + mxb(A, fmt, sshape)))
                 seq.append((f"wgrad {nm}", lambda nm=nm, t=t: mx.wgrad(
                     self.cv[nm], self.gy[nm], self.t[t["src"]], out=self.gw[nm], workspace=self.ws[nm],
-                    deferred=True), f, mxb(A, fmt, shape) + xb + gwb))
+                    deferred=True), f, gb + xb + gwb))
             elif nm in self.gx:
                 seq.append((f"bwd {nm}", lambda nm=nm, t=t: mx.backward(
                     self.cv[nm], self.w[nm][1], self.gy[nm], self.t[t["src"]], layout=self.gx_layout,
                     gx_out=self.gx[nm], gw_out=self.gw[nm], workspace=self.ws[nm], deferred=True),
-                    2.0 * f, wb + mxb(A, fmt, shape) + xb + es * self.gx[nm].numel() + gwb))
+                    2.0 * f, wb + gb + xb + es * self.gx[nm].numel() + gwb))
             else:
                 seq.append((f"wgrad {nm}", lambda nm=nm, t=t: mx.wgrad(
                     self.cv[nm], self.gy[nm], self.t[t["src"]], out=self.gw[nm], workspace=self.ws[nm],
-                    deferred=True), f, mxb(A, fmt, shape) + xb + gwb))
+                    deferred=True), f, gb + xb + gwb))
         items = [(self.cv[nm], fmt, self.ws[nm], self.gw[nm]) for nm in names]
         for i in range(0, len(items), mx.WREDUCE_MAX):
             grp = items[i:i + mx.WREDUCE_MAX]
@@ -461,7 +473,7 @@ class QlrStep:
         for i, cv in enumerate(self.front_cv):
             ho, wo = synth.out_hw(cv)
             ffl += 2.0 * 32 * cv["cout"] * ho * wo * cv["cin"] * 9
-            fby += (mxb(W, fmt, (cv["cout"], cv["cin"], 3, 3)) + mxb(A, fmt, (32, cv["cin"], cv["h"], cv["w"])) +
+            fby += (mxb(W, fmt, (cv["cout"], cv["cin"], 3, 3)) + mxb_in(A, fmt, (32, cv["cin"], cv["h"], cv["w"])) +
                     mxb(A, fmt, (32, cv["cout"], ho, wo)))
         seq.append(("front", lambda: self._front(self.fresh, self._group(x0.codes, x0.scales, last)), ffl, fby))
         for i, cv in enumerate(self.back_cv):
