@@ -563,16 +563,35 @@ __device__ __forceinline__ unsigned short pack4_e2m1(float4 x, float inv) {
 __device__ __forceinline__ float logistic(float y) {
     return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-y * 1.4426950408889634f));
 }
-__device__ __forceinline__ float fn_apply(int fn, float y) {
-    if (fn == MXC_FN_NONE) return y;
-    if (fn == MXC_FN_RELU) return y > 0.0f ? y : 0.0f;
-    return y * logistic(y);                                     // SiLU
+template <int F>
+__device__ __forceinline__ float fn_apply_c(float y) {
+    if constexpr (F == MXC_FN_NONE) return y;
+    else if constexpr (F == MXC_FN_RELU) return y > 0.0f ? y : 0.0f;
+    else return y * logistic(y);                                // SiLU
 }
+template <int F>
+__device__ __forceinline__ float fn_grad_c(float z) {
+    if constexpr (F == MXC_FN_NONE) return 1.0f;
+    else if constexpr (F == MXC_FN_RELU) return z > 0.0f ? 1.0f : 0.0f;
+    else {
+        const float s = logistic(z);                            // SiLU' = s (1 + z (1 - s))
+        return s * (1.0f + z * (1.0f - s));
+    }
+}
+// the derivative with the choice made per value (fewer live registers)
 __device__ __forceinline__ float fn_grad(int fn, float z) {
-    if (fn == MXC_FN_NONE) return 1.0f;
-    if (fn == MXC_FN_RELU) return z > 0.0f ? 1.0f : 0.0f;
-    const float s = logistic(z);                                // SiLU' = s (1 + z (1 - s))
-    return s * (1.0f + z * (1.0f - s));
+    return fn == MXC_FN_NONE ? 1.0f : fn == MXC_FN_RELU ? fn_grad_c<MXC_FN_RELU>(z) : fn_grad_c<MXC_FN_SILU>(z);
+}
+// body(FnTag<f>{}) for an activation f other than MXC_FN_NONE: the choice is
+// one uniform branch around straight-line code, so the values' exponentials
+// and reciprocals are independent and overlap.  (A choice per value, inside
+// an unrolled loop, put a scalar branch between every two values and ran
+// each SiLU as one dependent chain.)
+template <int F> struct FnTag { static constexpr int fn = F; };
+template <class Body>
+__device__ __forceinline__ void with_fn(int fn, Body&& body) {
+    if (fn == MXC_FN_RELU) body(FnTag<MXC_FN_RELU>{});
+    else body(FnTag<MXC_FN_SILU>{});
 }
 
 // ---------------------------------------------------------------- MXFP8 operands

@@ -135,10 +135,13 @@ __global__ __launch_bounds__(256) void quantize_sum_kernel(SumArgs a, uint8_t* _
             }
             if (a.fn != MXC_FN_NONE) {
                 const float4 zz = load4<BF>(a.z, ((size_t)pix * a.c + ch) * 32 + j);
-                s.x *= fn_grad(a.fn, zz.x);
-                s.y *= fn_grad(a.fn, zz.y);
-                s.z *= fn_grad(a.fn, zz.z);
-                s.w *= fn_grad(a.fn, zz.w);
+                with_fn(a.fn, [&](auto t) {
+                    constexpr int F = decltype(t)::fn;
+                    s.x *= fn_grad_c<F>(zz.x);
+                    s.y *= fn_grad_c<F>(zz.y);
+                    s.z *= fn_grad_c<F>(zz.z);
+                    s.w *= fn_grad_c<F>(zz.w);
+                });
             }
             if (a.vals) store_nt(a.vals + ((size_t)pix * a.c + ch) * 32 + j, s);
         }
@@ -245,8 +248,10 @@ __global__ __launch_bounds__(256) void quantize_sum_bf_kernel(SumArgs a, uint8_t
         if (a.fn != MXC_FN_NONE) {
             float z[8];
             bf16x8(load16_nt((const uint16_t*)a.z + ((size_t)pix * a.c + ch) * 32 + j), z);
+            with_fn(a.fn, [&](auto t) {
 #pragma unroll
-            for (int e = 0; e < 8; e++) v[hh][e] *= fn_grad(a.fn, z[e]);
+                for (int e = 0; e < 8; e++) v[hh][e] *= fn_grad_c<decltype(t)::fn>(z[e]);
+            });
         }
         if (a.vals) {
             float* o = a.vals + ((size_t)pix * a.c + ch) * 32 + j;
