@@ -149,6 +149,21 @@ constexpr int LDS_MAX = 160 * 1024;       // LDS of one CU
 // * 16): rows two apart land on different chunks.
 __device__ __forceinline__ int bf16_lds(int row, int chunk) { return row * 64 + ((chunk ^ ((row >> 1) & 3)) << 4); }
 
+// v *= fn'(z) for the lane's 16 values, z from a bf16 tile in LDS (zero where
+// zr is false), at most four values in flight
+template <int F>
+__device__ __forceinline__ void grad_lds4(float* v, const uint8_t* zt, bool zr, int r, int h) {
+#pragma unroll
+    for (int e4 = 0; e4 < 4; e4++) {
+        const float4 z = zr ? bf16_unpack4(*(const uint2*)(zt + bf16_lds(r, e4) + 8 * h)) : make_float4(0.f, 0.f, 0.f, 0.f);
+        v[4 * e4] *= fn_grad_c<F>(z.x);
+        v[4 * e4 + 1] *= fn_grad_c<F>(z.y);
+        v[4 * e4 + 2] *= fn_grad_c<F>(z.z);
+        v[4 * e4 + 3] *= fn_grad_c<F>(z.w);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
 // Lane (r, h) = (lane % 32, lane / 32) holds samples 8 e4 + 4 h .. + 3 of row r
 // in v[4 e4 .. 4 e4 + 3] (the MFMA accumulator layout).  Rows >= rows are
 // not written.
@@ -823,29 +838,19 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                     else        store_block(v, pix, cb);
                 }
                 // The activation (forward) or its derivative at z (input
-                // gradient): one uniform branch on fn around the 16 values,
-                // so their exponentials and reciprocals overlap.  The
-                // kernel-row-paired input gradient instead takes fn per value
-                // and overlaps at most four values: overlapping all sixteen
-                // takes it past the registers of three waves per SIMD
-                // (measured on the second layer of the network step: 234 ->
-                // 275 µs, where the unpaired stride-2 input gradient gains
-                // 101 -> 90 µs).
-                if constexpr (DG && KR) {
+                // gradient), with one uniform branch on fn around the values
+                // so that their exponentials and reciprocals overlap.  The
+                // input gradient overlaps four values at a time (scheduling
+                // barriers): all sixteen at once took its kernels past the
+                // registers of three waves per SIMD (measured on the second
+                // layer of the network step: 234 -> 275 µs).
+                if constexpr (DG) {
                     if (p.fn != MXC_FN_NONE) {
                         if (zpf) {
                             const uint8_t* zt = zl + (cn * NRB + rb) * 1024 * zsl;
                             const bool zr = r < 16 * zsl;    // rows past the copied slots: padding, z = 0
-#pragma unroll
-                            for (int e4 = 0; e4 < 4; e4++) {
-                                const float4 z = zr ? bf16_unpack4(*(const uint2*)(zt + bf16_lds(r, e4) + 8 * h))
-                                                    : make_float4(0.f, 0.f, 0.f, 0.f);
-                                v[4 * e4] *= fn_grad(p.fn, z.x);
-                                v[4 * e4 + 1] *= fn_grad(p.fn, z.y);
-                                v[4 * e4 + 2] *= fn_grad(p.fn, z.z);
-                                v[4 * e4 + 3] *= fn_grad(p.fn, z.w);
-                                __builtin_amdgcn_sched_barrier(0);
-                            }
+                            if (p.fn == MXC_FN_RELU) grad_lds4<MXC_FN_RELU>(v, zt, zr, r, h);
+                            else                     grad_lds4<MXC_FN_SILU>(v, zt, zr, r, h);
                         } else if (p.bf16) {
                             float zz[16];
                             load_bf16_tile(ep4, (const uint16_t*)p.zpre + (pix * p.M + (size_t)cb * 32) * 32, rows, lane, zz);
@@ -868,41 +873,12 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                             }
                         }
                     }
-                } else if (p.fn != MXC_FN_NONE) with_fn(p.fn, [&](auto t) {
-                    constexpr int F = decltype(t)::fn;
-                    if (DG && zpf) {
-                        const uint8_t* zt = zl + (cn * NRB + rb) * 1024 * zsl;
-                        const bool zr = r < 16 * zsl;        // rows past the copied slots: padding, z = 0
+                } else if (p.fn != MXC_FN_NONE) {
+                    with_fn(p.fn, [&](auto t) {
 #pragma unroll
-                        for (int e4 = 0; e4 < 4; e4++) {
-                            const float4 z = zr ? bf16_unpack4(*(const uint2*)(zt + bf16_lds(r, e4) + 8 * h))
-                                                : make_float4(0.f, 0.f, 0.f, 0.f);
-                            v[4 * e4] *= fn_grad_c<F>(z.x);
-                            v[4 * e4 + 1] *= fn_grad_c<F>(z.y);
-                            v[4 * e4 + 2] *= fn_grad_c<F>(z.z);
-                            v[4 * e4 + 3] *= fn_grad_c<F>(z.w);
-                        }
-                    } else if (DG && p.bf16) {
-                        float zz[16];
-                        load_bf16_tile(ep4, (const uint16_t*)p.zpre + (pix * p.M + (size_t)cb * 32) * 32, rows, lane, zz);
-#pragma unroll
-                        for (int e = 0; e < 16; e++) v[e] *= fn_grad_c<F>(zz[e]);
-                    } else if (DG) {
-                        const size_t zo = (pix * p.M + (real ? c : 0)) * 32 + 4 * h;
-#pragma unroll
-                        for (int e4 = 0; e4 < 4; e4++) {
-                            float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
-                            if (real) z = *(const float4*)((const float*)p.zpre + zo + 8 * e4);
-                            v[4 * e4] *= fn_grad_c<F>(z.x);
-                            v[4 * e4 + 1] *= fn_grad_c<F>(z.y);
-                            v[4 * e4 + 2] *= fn_grad_c<F>(z.z);
-                            v[4 * e4 + 3] *= fn_grad_c<F>(z.w);
-                        }
-                    } else {
-#pragma unroll
-                        for (int e = 0; e < 16; e++) v[e] = fn_apply_c<F>(v[e]);
-                    }
-                });
+                        for (int e = 0; e < 16; e++) v[e] = fn_apply_c<decltype(t)::fn>(v[e]);
+                    });
+                }
                 if (p.out && !p.pre_out) store_block(v, pix, cb);
                 uint32_t m = 0;
 #pragma unroll
