@@ -748,14 +748,16 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                 float v[16];
 #pragma unroll
                 for (int e = 0; e < 16; e++) v[e] = acc[rb][cn][e];
-                if (p.bf16) {   // the value a bf16 tensor holds is the value used from here on
+                // with bf16, the value a bf16 tensor holds is the value used
+                // from here on
+                auto to_bf16 = [](float* w, int n) {
 #pragma unroll
-                    for (int e = 0; e < 16; e += 2) {
-                        const uint32_t u = bf16_pack2(v[e], v[e + 1]);
-                        v[e] = __uint_as_float(u << 16);
-                        v[e + 1] = __uint_as_float(u & 0xFFFF0000u);
+                    for (int e = 0; e < n; e += 2) {
+                        const uint32_t u = bf16_pack2(w[e], w[e + 1]);
+                        w[e] = __uint_as_float(u << 16);
+                        w[e + 1] = __uint_as_float(u & 0xFFFF0000u);
                     }
-                }
+                };
                 const int rows = min(32, p.M - cb * 32);
                 const bool q8 = p.qfmt == MXC_E4M3, q6 = p.qfmt == MXC_E2M3 || p.qfmt == MXC_E3M2;
                 if (!DG && rows <= 16 && !q6) {
@@ -766,12 +768,18 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                     // each lane activates and quantizes 8 values instead of
                     // 16 (the values, codes and stored bytes are unchanged).
                     const int row = r & 15, k0 = (r >> 4) * 2;
+                    // (v_permlane16_swap with both operands the same
+                    // register: lanes 16..31 and 48..63 of the first result
+                    // hold lanes 0..15 and 32..47, a register move instead
+                    // of an LDS permute)
                     float u[8];
 #pragma unroll
                     for (int i = 0; i < 8; i++) {
-                        const float o = __shfl_xor(v[8 + i], 16);
+                        const uint32_t x = __float_as_uint(v[8 + i]);
+                        const float o = __uint_as_float(__builtin_amdgcn_permlane16_swap(x, x, false, false)[0]);
                         u[i] = r >= 16 ? o : v[i];
                     }
+                    if (p.bf16) to_bf16(u, 8);
                     // the values of one block through LDS to global memory:
                     // bf16 (2 KB, 64-byte rows) or fp32 (4 KB, 128-byte rows)
                     auto stage_out = [&](const float* w, bool as_bf16, void* dst) {
@@ -833,6 +841,7 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                     }
                     continue;
                 }
+                if (p.bf16) to_bf16(v, 16);
                 if (p.out && p.pre_out) {   // the pre-activation, for the backward pass
                     if (p.bf16) store_bf16_tile(ep4, v, (uint16_t*)p.out + (pix * p.M + (size_t)cb * 32) * 32, rows, lane);
                     else        store_block(v, pix, cb);
