@@ -168,6 +168,17 @@ int mxconv_quantize(const void* src, int dtype, int layout, int role, int fmt,
                     int n, int c, int h, int w,
                     void* codes, uint8_t* scales, void* stream);
 
+/* Flag for mxconv_quantize's `layout` (MXC_NCHW | MXC_KEEP_PAD): the codes of
+ * the padding channels (c .. Cp - 1, which hold +0 codes) are not written.
+ * The caller guarantees that `codes` already holds +0 codes there: a
+ * zero-filled buffer, or one this call has filled before with the same
+ * geometry.  For an input image (a few channels in one 32-channel block)
+ * those rows are most of the stored codes: with c = 3, 29 of every 32 rows.
+ * Only the few-channel NCHW path (role MXC_ACT, c <= 4, batch block 32,
+ * FP8 or FP4) skips them; every other call writes them as usual, so the
+ * result is the same either way. */
+#define MXC_KEEP_PAD 0x100
+
 /* Several quantizations in one call, with mxconv_quantize's rule: a layer's
  * forward operands (X and W), which become available together, are
  * quantized once each (Sec. IV-C) in a single launch.  Every job is exactly

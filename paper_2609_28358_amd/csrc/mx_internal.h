@@ -54,9 +54,11 @@ enum { CONV_ONE = 0, CONV_FWD = 1, CONV_DGRAD = 2, CONV_WGRAD = 3 };
 int conv_init(Conv* cv, const mxc_conv* p, int fmt, int op = CONV_ONE);
 
 // ---------------------------------------------------------------- launchers
-// seed != NULL: elements rounded stochastically with that Philox key
+// seed != NULL: elements rounded stochastically with that Philox key;
+// keep_pad: the few-channel path leaves the padding channels' codes unwritten
 int launch_quantize(const void* src, int dtype, int layout, int role, const Geom& g, int fmt,
-                    void* codes, uint8_t* scales, hipStream_t s, const uint64_t* seed = nullptr);
+                    void* codes, uint8_t* scales, hipStream_t s, const uint64_t* seed = nullptr,
+                    bool keep_pad = false);
 int im2col_check(const Conv& cv);     // MXC_ERR_SHAPE for sizes the im2col kernel cannot index
 int launch_im2col(const Conv& cv, const void* xc, const uint8_t* xs, void* cc, uint8_t* cs,
                   hipStream_t s);

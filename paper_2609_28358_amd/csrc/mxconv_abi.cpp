@@ -129,6 +129,8 @@ size_t mxconv_wgrad_workspace_bytes(const mxc_conv* p, int fmt) {
 int mxconv_quantize(const void* src, int dtype, int layout, int role, int fmt, int n, int c,
                     int h, int w, void* codes, uint8_t* scales, void* stream) {
     if (!src || !codes || !scales) return MXC_ERR_NULL;
+    const bool keep_pad = (layout & MXC_KEEP_PAD) != 0;
+    layout &= ~MXC_KEEP_PAD;
     if (dtype != MXC_F32 && dtype != MXC_BF16) return MXC_ERR_ARG;
     if (layout != MXC_NCHW && layout != MXC_NHWC && layout != MXC_CBF) return MXC_ERR_ARG;
     if (layout == MXC_CBF && role != MXC_ACT) return MXC_ERR_ARG;
@@ -136,7 +138,7 @@ int mxconv_quantize(const void* src, int dtype, int layout, int role, int fmt, i
     int rc = geom_init(&g, role, fmt, n, c, h, w);
     if (rc) return rc;
     if (!aligned16(src) || !aligned16(codes) || !aligned16(scales)) return MXC_ERR_ALIGN;
-    return launch_quantize(src, dtype, layout, role, g, fmt, codes, scales, (hipStream_t)stream);
+    return launch_quantize(src, dtype, layout, role, g, fmt, codes, scales, (hipStream_t)stream, nullptr, keep_pad);
 }
 
 int mxconv_quantize_multi(int count, const mxc_qjob* jobs, void* stream) {

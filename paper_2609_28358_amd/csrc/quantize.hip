@@ -515,17 +515,19 @@ __device__ __forceinline__ void quantize_block_body(const void* __restrict__ src
 // NARROW_P consecutive pixels: it reads the C x 32 source rows of those
 // pixels as contiguous 16-byte pieces, transposes them through LDS
 // ([pixel][channel][sample], rows padded by one float against bank
-// conflicts), and each wave then quantizes a quarter of the pixels one block
-// at a time in the lane layout of the one-block-per-wave quantizer (lane l:
-// channels 8 q + l / 8, samples 4 (l % 8) .. +3), writing every block as one
-// contiguous run.  Channels C .. 31 are zero codes.
+// conflicts), and each wave then quantizes a quarter of the pixels, four
+// blocks at a time (16 lanes per block, below).  Channels C .. 31 are zero
+// codes, written with 16-byte stores; with keep_pad they are not written
+// (the buffer already holds them), and a block's stores shrink to its C
+// real rows.
 constexpr int NARROW_C = 4;
 constexpr int NARROW_P = 64;
 
 template <int DTYPE, int FMT, bool VECLOAD>
 __global__ __launch_bounds__(QT) void quantize_narrow_kernel(const void* __restrict__ src, Geom g,
                                                              uint8_t* __restrict__ codes,
-                                                             uint8_t* __restrict__ scales, int tiles) {
+                                                             uint8_t* __restrict__ scales, int tiles,
+                                                             int keep_pad) {
     constexpr int PS = NARROW_C * 32 + 1;                     // floats per pixel row
     __shared__ float t[NARROW_P * PS];
     const int tid = threadIdx.x;
@@ -569,43 +571,56 @@ __global__ __launch_bounds__(QT) void quantize_narrow_kernel(const void* __restr
         for (int e = 0; e < VEC; e++) t[(k * VEC + e) * PS + c * 32 + n] = v[e];
     }
     __syncthreads();
+    // Four pixels per pass of a wave: 16 lanes per pixel, lane (l % 16) holds
+    // row (l / 4) % 4 and samples 8 (l % 4) .. +7 of its pixel's block (rows
+    // 4 .. 31 are padding: NARROW_C <= 4), so the block maximum is a
+    // reduction inside one 16-lane DPP row and the scale a per-lane value.
     const int lane = tid & 63, wave = tid >> 6;
-    const int j = 4 * (lane & 7), row = lane >> 3;
+    const int ps = lane >> 4, row = (lane >> 2) & 3, jj = 8 * (lane & 3);
+    constexpr int RB = FMT == MXC_E4M3 ? 32 : 16;              // bytes of one code row
     constexpr int PPW = NARROW_P / (QT / 64);                 // pixels per wave
-    for (int i = 0; i < PPW; i++) {
-        const int pl = wave * PPW + i, pix = p0 + pl;
-        if (pix >= hw) break;                                 // wave-uniform
-        float4 x[4];
+    for (int i = 0; i < PPW; i += 4) {
+        const int pl = wave * PPW + i + ps, pix = p0 + pl;
+        const bool live = pix < hw;
+        float x[8];
 #pragma unroll
-        for (int q = 0; q < 4; q++) x[q] = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (row < g.c) {
-            const float* tp = t + pl * PS + row * 32 + j;
-            x[0] = make_float4(tp[0], tp[1], tp[2], tp[3]);
+        for (int e = 0; e < 8; e++) x[e] = 0.0f;
+        if (row < g.c) {                                      // pixels past hw hold zeros in t
+            const float* tp = t + pl * PS + row * 32 + jj;
+#pragma unroll
+            for (int e = 0; e < 8; e++) x[e] = tp[e];
         }
-        uint32_t m = __float_as_uint(x[0].x) & 0x7FFFFFFFu;
-        m = max(m, __float_as_uint(x[0].y) & 0x7FFFFFFFu);
-        m = max(m, __float_as_uint(x[0].z) & 0x7FFFFFFFu);
-        m = max(m, __float_as_uint(x[0].w) & 0x7FFFFFFFu);
-        m = wave_max_u32(m);
+        uint32_t m = 0;
+#pragma unroll
+        for (int e = 0; e < 8; e++) m = max(m, __float_as_uint(x[e]) & 0x7FFFFFFFu);
+        m = max(m, (uint32_t)__builtin_amdgcn_mov_dpp((int)m, 0xB1, 0xF, 0xF, false));   // quad_perm 1,0,3,2
+        m = max(m, (uint32_t)__builtin_amdgcn_mov_dpp((int)m, 0x4E, 0xF, 0xF, false));   // quad_perm 2,3,0,1
+        m = max(m, (uint32_t)__builtin_amdgcn_mov_dpp((int)m, 0x141, 0xF, 0xF, false));  // row_half_mirror
+        m = max(m, (uint32_t)__builtin_amdgcn_mov_dpp((int)m, 0x140, 0xF, 0xF, false));  // row_mirror
         const uint32_t sc = scale_code_from_bits<fmt_emax(FMT)>(m);
         const size_t blk = (size_t)grp * hw + pix;             // one channel block per pixel
-        if (lane == 0) scales[blk] = (uint8_t)sc;
+        if (!live) continue;
+        if ((lane & 15) == 0) scales[blk] = (uint8_t)sc;
         const float inv = inv_scale(sc);
         const bool bad = sc == 0xFFu;
-        if (FMT == MXC_E4M3) {
-            uint32_t* d = (uint32_t*)(codes + blk * 1024) + lane;
-#pragma unroll
-            for (int q = 0; q < 4; q++) d[64 * q] = bad ? 0u : pack4_e4m3(x[q], inv);
-        } else {
-            unsigned short* d = (unsigned short*)(codes + blk * 512) + lane;
-#pragma unroll
-            for (int q = 0; q < 4; q++) d[64 * q] = bad ? (unsigned short)0 : (unsigned short)pack4_e2m1(x[q], inv);
+        const float4 lo = make_float4(x[0], x[1], x[2], x[3]), hi = make_float4(x[4], x[5], x[6], x[7]);
+        uint8_t* const b = codes + blk * (32 * RB);
+        if (!keep_pad || row < g.c) {
+            if (FMT == MXC_E4M3)
+                *(uint2*)(b + row * RB + jj) = bad ? make_uint2(0u, 0u) : make_uint2(pack4_e4m3(lo, inv), pack4_e4m3(hi, inv));
+            else
+                *(uint32_t*)(b + row * RB + jj / 2) =
+                    bad ? 0u : (uint32_t)pack4_e2m1(lo, inv) | (uint32_t)pack4_e2m1(hi, inv) << 16;
+        }
+        if (!keep_pad) {                                      // rows 4 .. 31: +0 codes, 16 bytes a store
+            constexpr int NZ = 28 * RB / 16;
+            for (int q = lane & 15; q < NZ; q += 16) *(uint4*)(b + 4 * RB + 16 * q) = make_uint4(0u, 0u, 0u, 0u);
         }
     }
 }
 
 template <int DTYPE, int FMT>
-int launch_qn(const void* src, const Geom& g, void* codes, uint8_t* scales, hipStream_t s) {
+int launch_qn(const void* src, const Geom& g, void* codes, uint8_t* scales, hipStream_t s, bool keep_pad) {
     const int hw = g.h * g.w;
     const int tiles = (hw + NARROW_P - 1) / NARROW_P;
     const long grid = (long)g.ng * tiles;
@@ -613,10 +628,10 @@ int launch_qn(const void* src, const Geom& g, void* codes, uint8_t* scales, hipS
     constexpr int VEC = DTYPE == MXC_F32 ? 4 : 8;
     if (hw % VEC == 0)
         hipLaunchKernelGGL((quantize_narrow_kernel<DTYPE, FMT, true>), dim3((unsigned)grid), dim3(QT), 0, s, src, g,
-                           (uint8_t*)codes, scales, tiles);
+                           (uint8_t*)codes, scales, tiles, keep_pad ? 1 : 0);
     else
         hipLaunchKernelGGL((quantize_narrow_kernel<DTYPE, FMT, false>), dim3((unsigned)grid), dim3(QT), 0, s, src, g,
-                           (uint8_t*)codes, scales, tiles);
+                           (uint8_t*)codes, scales, tiles, keep_pad ? 1 : 0);
     return hipGetLastError() == hipSuccess ? MXC_OK : MXC_ERR_HIP;
 }
 
@@ -806,7 +821,7 @@ int launch_quantize_multi(int count, const QuantJob* jobs, hipStream_t s) {
 }
 
 int launch_quantize(const void* src, int dtype, int layout, int role, const Geom& g, int fmt, void* codes,
-                    uint8_t* scales, hipStream_t s, const uint64_t* seed) {
+                    uint8_t* scales, hipStream_t s, const uint64_t* seed, bool keep_pad) {
     const bool sr = seed != nullptr;
     const uint32_t k0 = sr ? (uint32_t)*seed : 0u, k1 = sr ? (uint32_t)(*seed >> 32) : 0u;
     // blocks that are contiguous (CBF, Bn = 32) or a small gather (weights): one wave per block
@@ -821,10 +836,10 @@ int launch_quantize(const void* src, int dtype, int layout, int role, const Geom
     if (layout == MXC_NCHW && role == MXC_ACT && g.bn == 32 && g.c <= NARROW_C && !sr &&
         (fmt == MXC_E4M3 || fmt == MXC_E2M1)) {
         if (dtype == MXC_F32)
-            return fmt == MXC_E4M3 ? launch_qn<MXC_F32, MXC_E4M3>(src, g, codes, scales, s)
-                                   : launch_qn<MXC_F32, MXC_E2M1>(src, g, codes, scales, s);
-        return fmt == MXC_E4M3 ? launch_qn<MXC_BF16, MXC_E4M3>(src, g, codes, scales, s)
-                               : launch_qn<MXC_BF16, MXC_E2M1>(src, g, codes, scales, s);
+            return fmt == MXC_E4M3 ? launch_qn<MXC_F32, MXC_E4M3>(src, g, codes, scales, s, keep_pad)
+                                   : launch_qn<MXC_F32, MXC_E2M1>(src, g, codes, scales, s, keep_pad);
+        return fmt == MXC_E4M3 ? launch_qn<MXC_BF16, MXC_E4M3>(src, g, codes, scales, s, keep_pad)
+                               : launch_qn<MXC_BF16, MXC_E2M1>(src, g, codes, scales, s, keep_pad);
     }
     switch (layout) {
         case MXC_NCHW: return launch_q_dt<MXC_NCHW>(src, dtype, g, fmt, sr, codes, scales, s, k0, k1);

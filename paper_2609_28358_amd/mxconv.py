@@ -17,6 +17,7 @@ ACT, WEIGHT = 0, 1
 FN_NONE, FN_RELU, FN_SILU = 0, 1, 2
 FN_PRE_OUT = 0x100      # or-ed into fwd_quant's fn: act_out receives the pre-activation
 FN_BF16 = 0x200         # or-ed into fwd_quant / dgrad_quant / quantize_sum's fn: bf16 full-precision tensors
+KEEP_PAD = 0x100        # or-ed into quantize's layout: padding channels' codes already +0, not written
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libmxconv.so")
@@ -206,13 +207,16 @@ def _quant_args(src, layout, shape):
     return dtype, tuple(int(v) for v in shape)
 
 
-def quantize(src, role, fmt, layout=NCHW, shape=None, out=None, stream=None):
+def quantize(src, role, fmt, layout=NCHW, shape=None, out=None, stream=None, keep_pad=False):
     """Quantize `src` (fp32 or bf16 device tensor) once.  `shape` is the
-    logical (n, c, h, w); it defaults to src.shape for NCHW."""
+    logical (n, c, h, w); it defaults to src.shape for NCHW.  keep_pad: the
+    codes of `out`'s padding channels already hold +0 codes (MXC_KEEP_PAD)."""
     dtype, shape = _quant_args(src, layout, shape)
     if out is None:
+        if keep_pad:
+            raise MxconvError("keep_pad needs an output whose padding codes are +0")
         out = MxTensor.empty(role, fmt, shape, src.device)
-    _check(lib().mxconv_quantize(_ptr(src), dtype, layout, role, fmt, *shape,
+    _check(lib().mxconv_quantize(_ptr(src), dtype, layout | (KEEP_PAD if keep_pad else 0), role, fmt, *shape,
                                  _ptr(out.codes), _ptr(out.scales), _stream(stream)), "mxconv_quantize")
     return out
 

@@ -137,10 +137,11 @@ def mxb(role, fmt, shape):
 
 
 def mxb_in(role, fmt, shape):
-    """Bytes a GEMM reads of an MX operand: an activation with a single
-    channel block contributes the code rows of its real channels only (its
-    padding rows are known +0 codes, never fetched); otherwise every stored
-    byte, as mxb."""
+    """Bytes a GEMM reads of an MX operand (or the image quantize writes with
+    keep_pad): an activation with a single channel block contributes the
+    code rows of its real channels only (its padding rows are known +0
+    codes, never fetched or rewritten); otherwise every stored byte, as
+    mxb."""
     n, c, h, w = shape
     if role == mx.ACT and c < 32:
         return mx.codes_bytes(role, fmt, *shape) * c / 32.0 + mx.scales_bytes(role, fmt, *shape)
@@ -193,7 +194,10 @@ class NetStep:
         for i, t in enumerate(net.nodes):
             shape = (n, t["c"], t["h"], t["w"])
             if t["kind"] == "input":
+                # zero-filled once: the image quantize leaves its padding
+                # channels' codes (+0) unwritten on every step
                 self.t[t["name"]] = mx.MxTensor.empty(mx.ACT, fmt, shape, device)
+                self.t[t["name"]].codes.zero_()
             elif t["kind"] == "concat":
                 self.t[t["name"]] = mx.MxTensor.empty(mx.ACT, fmt, shape, device)
             else:
@@ -280,8 +284,8 @@ class NetStep:
         seq = []
         img = net.nodes[0]
         ishape = (n, img["c"], img["h"], img["w"])
-        seq.append(("quant_image", lambda: mx.quantize(self.image, A, fmt, out=self.t[img["name"]]),
-                    0.0, 2.0 * math.prod(ishape) + mxb(A, fmt, ishape)))
+        seq.append(("quant_image", lambda: mx.quantize(self.image, A, fmt, out=self.t[img["name"]], keep_pad=True),
+                    0.0, 2.0 * math.prod(ishape) + mxb_in(A, fmt, ishape)))
         names = [t["name"] for t in self.convs]
         for i in range(0, len(names), mx.QMULTI_MAX):
             grp = names[i:i + mx.QMULTI_MAX]
@@ -404,6 +408,7 @@ class QlrStep:
         self.back_w = [mx.MxTensor.empty(mx.WEIGHT, fmt, tuple(w.shape), device) for w in self.back_wm]
         # front-stack activations for one 32-sample group
         self.front_x = mx.MxTensor.empty(mx.ACT, fmt, (32, 3, 128, 128), device)
+        self.front_x.codes.zero_()     # padding channels' codes stay +0 (quantize with keep_pad)
         self.front_t = []
         for cv in self.front_cv[:-1]:
             ho, wo = synth.out_hw(cv)
@@ -447,7 +452,7 @@ class QlrStep:
     def _front(self, img, out):
         """Front stack forward on 32 images (fp32 NCHW), its last epilogue
         writing the latents' codes into `out`."""
-        mx.quantize(img, mx.ACT, self.fmt, out=self.front_x)
+        mx.quantize(img, mx.ACT, self.fmt, out=self.front_x, keep_pad=True)
         src = self.front_x
         for i, cv in enumerate(self.front_cv):
             dst = out if i == len(self.front_cv) - 1 else self.front_t[i]
@@ -469,7 +474,7 @@ class QlrStep:
                 x0.scales[slot * self.ls:(slot + 1) * self.ls].copy_(self.buf_scales[k * self.ls:(k + 1) * self.ls])),
                 0.0, 2.0 * (self.lc + self.ls)))
         last = n // 32 - 1
-        ffl, fby = 0.0, 4.0 * self.fresh.numel() + mxb(A, fmt, (32, 3, 128, 128))
+        ffl, fby = 0.0, 4.0 * self.fresh.numel() + mxb_in(A, fmt, (32, 3, 128, 128))
         for i, cv in enumerate(self.front_cv):
             ho, wo = synth.out_hw(cv)
             ffl += 2.0 * 32 * cv["cout"] * ho * wo * cv["cin"] * 9

@@ -88,6 +88,13 @@ def test_quantize_errors():
     assert q(GOOD, 0, 0, 0, 1, 1, 32, 4, 4, GOOD, GOOD, None) == -3      # E2M1 with one sample
     assert q(ODD, 0, 0, 0, 0, 32, 32, 4, 4, GOOD, GOOD, None) == -4
     assert q(GOOD, 0, 0, 0, 0, 32, 32, 4, 4, GOOD, ODD, None) == -4
+    # MXC_KEEP_PAD: a flag on layout; the layout under it is still checked
+    hdr = open(os.path.join(ROOT, "include", "mxconv.h")).read()
+    assert int(re.search(r"#define MXC_KEEP_PAD (0x[0-9a-fA-F]+)", hdr).group(1), 16) == mx.KEEP_PAD
+    assert q(GOOD, 0, mx.KEEP_PAD | 0, 0, 0, 32, 3, 4, 4, GOOD, ODD, None) == -4   # accepted up to alignment
+    assert q(GOOD, 0, mx.KEEP_PAD | 3, 0, 0, 32, 3, 4, 4, GOOD, GOOD, None) == -2
+    assert q(GOOD, 0, 0x200, 0, 0, 32, 3, 4, 4, GOOD, GOOD, None) == -2
+
 
 
 def test_gemm_and_im2col_errors():
