@@ -372,7 +372,7 @@ int mxconv_wgrad(const mxc_conv* cv, int fmt,
  * calls on the stream.
  * Errors: as mxconv_wgrad for every job (checked before anything is
  * launched), ARG for a count out of range. */
-#define MXC_WREDUCE_MAX 8
+#define MXC_WREDUCE_MAX 32
 typedef struct mxc_wjob {
     const mxc_conv* conv;
     int fmt;

@@ -42,7 +42,7 @@ class MxcWJob(ctypes.Structure):
                 ("ws_bytes", ctypes.c_size_t), ("gw", ctypes.c_void_p)]
 
 
-WREDUCE_MAX = 8
+WREDUCE_MAX = 32
 CONCAT_MAX = 4
 TERMS_MAX = 4
 

@@ -348,7 +348,7 @@ def test_wgrad_reduce_multi_errors():
         arr = (mx.MxcWJob * max(1, len(jobs)))(*jobs)
         return L.mxconv_wgrad_reduce_multi(len(jobs), arr, None)
 
-    assert L.mxconv_wgrad_reduce_multi(9, None, None) == -2
+    assert L.mxconv_wgrad_reduce_multi(mx.WREDUCE_MAX + 1, None, None) == -2
     assert L.mxconv_wgrad_reduce_multi(-1, None, None) == -2
     assert L.mxconv_wgrad_reduce_multi(1, None, None) == -1
     assert L.mxconv_wgrad_reduce_multi(0, None, None) == 0
