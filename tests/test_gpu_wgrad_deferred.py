@@ -68,3 +68,30 @@ def test_deferred_weight_gradients_reduced_together(mx):
     torch.cuda.synchronize()
     for k, (a, b) in enumerate(zip(ref, outs)):
         assert torch.equal(a, b), f"layer {k}: differs from mxconv_wgrad on the second pass"
+
+
+
+def test_reduce_batch_of_the_most_layers(mx):
+    """As many layers as one call takes (32; a launch once took 8), split-K
+    and direct ones mixed, FP8 and FP4, finished by one call: each equal to
+    mxconv_wgrad.  One more layer is refused."""
+    shapes = [synth.conv_dict(64, 32 * (1 + k % 3), 32 * (1 + (k + 1) % 2), 12 + k % 5, 13 + k % 4,
+                              3 if k % 2 else 1, 1 + (k % 3 == 2)) for k in range(mx.WREDUCE_MAX)]
+    ref, jobs, split = [], [], 0
+    for k, cv in enumerate(shapes):
+        fmt = k % 2
+        qg, qx = _operands(mx, cv, fmt, fmt, 200 + k)
+        ref.append(mx.wgrad(cv, qg, qx))
+        need = mx.wgrad_workspace_bytes(cv, fmt)
+        split += need > 0
+        ws = torch.empty(max(1, need), dtype=torch.uint8, device=DEV) if need else None
+        gw = torch.full((cv["cout"], cv["cin"], cv["kh"], cv["kw"]), 5.0, device=DEV)   # overwritten
+        mx.wgrad(cv, qg, qx, out=gw, workspace=ws, deferred=True)
+        jobs.append((cv, fmt, ws, gw))
+    assert split >= mx.WREDUCE_MAX // 2                   # most of them leave partial sums
+    mx.wgrad_reduce_multi(jobs)
+    torch.cuda.synchronize()
+    for k, (a, j) in enumerate(zip(ref, jobs)):
+        assert torch.equal(a, j[3]), f"layer {k}: differs from mxconv_wgrad"
+    with pytest.raises(mx.MxconvError):
+        mx.wgrad_reduce_multi(jobs + jobs[:1])
