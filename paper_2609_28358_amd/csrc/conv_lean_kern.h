@@ -768,17 +768,16 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                     // each lane activates and quantizes 8 values instead of
                     // 16 (the values, codes and stored bytes are unchanged).
                     const int row = r & 15, k0 = (r >> 4) * 2;
-                    // (v_permlane16_swap with both operands the same
-                    // register: lanes 16..31 and 48..63 of the first result
-                    // hold lanes 0..15 and 32..47, a register move instead
-                    // of an LDS permute)
+                    // (v_permlane16_swap(a, b) swaps the odd 16-lane rows of
+                    // a with the even rows of b: its first result keeps a in
+                    // lanes 0..15 and 32..47 and takes b's lanes 0..15 and
+                    // 32..47 into lanes 16..31 and 48..63 -- with a = v[i]
+                    // and b = v[8 + i], exactly u[i], in registers)
                     float u[8];
 #pragma unroll
-                    for (int i = 0; i < 8; i++) {
-                        const uint32_t x = __float_as_uint(v[8 + i]);
-                        const float o = __uint_as_float(__builtin_amdgcn_permlane16_swap(x, x, false, false)[0]);
-                        u[i] = r >= 16 ? o : v[i];
-                    }
+                    for (int i = 0; i < 8; i++)
+                        u[i] = __uint_as_float(__builtin_amdgcn_permlane16_swap(
+                            __float_as_uint(v[i]), __float_as_uint(v[8 + i]), false, false)[0]);
                     if (p.bf16) to_bf16(u, 8);
                     // the values of one block through LDS to global memory:
                     // bf16 (2 KB, 64-byte rows) or fp32 (4 KB, 128-byte rows)
@@ -847,12 +846,14 @@ __device__ __forceinline__ void lean_tile(const LeanArgs& p, int lin, const Phas
                     else        store_block(v, pix, cb);
                 }
                 // The activation (forward) or its derivative at z (input
-                // gradient), with one uniform branch on fn around the values
-                // so that their exponentials and reciprocals overlap.  The
-                // input gradient overlaps four values at a time (scheduling
+                // gradient).  The forward takes one uniform branch on fn
+                // around the 16 values, so that their exponentials and
+                // reciprocals overlap.  The input gradient, with z from its
+                // LDS tile, does the same four values at a time (scheduling
                 // barriers): all sixteen at once took its kernels past the
                 // registers of three waves per SIMD (measured on the second
-                // layer of the network step: 234 -> 275 µs).
+                // layer of the network step: 234 -> 275 µs); its other z
+                // sources choose fn per value.
                 if constexpr (DG) {
                     if (p.fn != MXC_FN_NONE) {
                         if (zpf) {
