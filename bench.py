@@ -1003,9 +1003,9 @@ def summarize_trace(rdir, log):
         else:
             i += 1
     L = ["# Kernel trace: YOLOv8n-shaped fwd+bwd step, batch 64, MXFP4\n"]
-    L.append("Command (repository root on an MI355X machine; summary written by bench.py --summarize-trace):\n")
+    L.append("Command (repository root on an MI355X machine, <out> an output directory; summary written by bench.py --summarize-trace):\n")
     L.append("    cd /tmp && export TMPDIR=/tmp && rocprofv3 --kernel-trace --stats --output-format csv "
-             "-d <repo>/gpurun_out/ktrace -o run -- python3 <repo>/bench.py > <repo>/gpurun_out/ktrace.log\n")
+             "-d <out>/ktrace -o run -- python3 <repo>/bench.py > <out>/ktrace.log\n")
     rl = bench["roofline"]
     L.append(f"Bench line of the same run: value {bench['value']} TFLOP/s, {bench['ms_per_step']} ms per step; "
              f"roofline call `{rl['kernel']}` {rl['ms'] * 1000:.1f} us in the step (bound {rl['bound']}, achieved "
@@ -1076,12 +1076,13 @@ def summarize_pmc(fdir, wdir, flog, wlog):
     ff, wf = kib / fcopy, kib / wcopy
     label = fi["pmc_pass"]
     L = [f"# HBM traffic per call from FETCH_SIZE / WRITE_SIZE counters: {label} step\n"]
-    L.append("Two counter passes over the same command, one counter each (repository root on an MI355X machine; "
+    L.append("Two counter passes over the same command, one counter each (repository root on an MI355X machine, "
+             "<out> an output directory; "
              "summary by bench.py --summarize-pmc):\n")
     for c in ("FETCH_SIZE", "WRITE_SIZE"):
         L.append(f"    cd /tmp && export TMPDIR=/tmp && timeout -s KILL 180 rocprofv3 --pmc {c} --output-format csv "
-                 f"-d <repo>/gpurun_out/pmc_{label}_{c} -o p -- python3 <repo>/bench.py --pmc-pass {label} --warmup 2 "
-                 f"> <repo>/gpurun_out/pmc_{label}_{c}.log")
+                 f"-d <out>/pmc_{label}_{c} -o p -- python3 <repo>/bench.py --pmc-pass {label} --warmup 2 "
+                 f"> <out>/pmc_{label}_{c}.log")
     L.append("\nThe pass runs every call of the step once (eager, in step order, each after a spin kernel that "
              "delimits it), then copies 256 MiB device to device three times; the counters of that copy "
              f"calibrate both: FETCH_SIZE {fcopy:.1f} KiB, WRITE_SIZE {wcopy:.1f} KiB for {kib:.0f} KiB moved.\n")
@@ -1141,11 +1142,12 @@ def summarize_sq(log, *dirs):
                 durs[i] = sum((int(rs[0]["End_Timestamp"]) - int(rs[0]["Start_Timestamp"])) / 1000.0 for rs in seg)
     label = info["pmc_pass"]
     L = [f"# Shader-sequencer counters of the matrix-product calls: {label} step, MXFP4\n"]
-    L.append("Two counter passes (repository root on an MI355X machine; summary by bench.py --summarize-sq):\n")
+    L.append("Two counter passes (repository root on an MI355X machine, <out> an output directory; "
+             "summary by bench.py --summarize-sq):\n")
     for j, ps in enumerate(SQ_PASSES):
         L.append(f"    cd /tmp && export TMPDIR=/tmp && timeout -s KILL 180 rocprofv3 --pmc {' '.join(ps)} "
-                 f"--output-format csv -d <repo>/gpurun_out/sq_{label}_{j} -o p -- python3 <repo>/bench.py "
-                 f"--pmc-pass {label} --warmup 2 > <repo>/gpurun_out/sq_{label}_{j}.log")
+                 f"--output-format csv -d <out>/sq_{label}_{j} -o p -- python3 <repo>/bench.py "
+                 f"--pmc-pass {label} --warmup 2 > <out>/sq_{label}_{j}.log")
     L.append(f"\nsource digest: `{info['source_digest']}`\n")
     L.append("Columns: kernel time under counter collection; fraction of the MXFP4 peak (10.1 PFLOP/s) the call's "
              "flops reach in that time; matrix-core busy cycles over the SIMD-cycles of the call (1024 SIMDs at "
@@ -1204,8 +1206,8 @@ def main():
         print(summarize_sq(*args.summarize_sq))
         return
     if args.gpus != 1:
-        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported: every GPU box here has one GPU, "
-              f"and the path has no multi-GPU part", file=sys.stderr)
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported: the path has no multi-GPU part",
+              file=sys.stderr)
         sys.exit(2)
 
     import torch
