@@ -203,7 +203,7 @@ int mxconv_quantize(const void* src, int dtype, int layout, int role, int fmt,
  * Errors: as mxconv_quantize (checked for every job before anything is
  * launched), ARG for a count out of range, SHAPE for a conv that does not
  * match its job. */
-#define MXC_QMULTI_MAX 8
+#define MXC_QMULTI_MAX 24
 typedef struct mxc_qjob {
     const void* src;
     int dtype, layout, role, fmt, n, c, h, w;

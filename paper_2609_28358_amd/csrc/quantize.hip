@@ -659,7 +659,7 @@ struct QJob {
     int blk0, nblocks;
     ColOut col;                    // kind 0, FP8 / FP4: optional im2col output
 };
-constexpr int QMULTI_MAX = 8;
+constexpr int QMULTI_MAX = MXC_QMULTI_MAX;     // 24 x 136 bytes of kernel arguments
 struct QMulti {
     QJob j[QMULTI_MAX];
     int count, nblocks;
@@ -690,10 +690,12 @@ __global__ __launch_bounds__(QT) void quantize_multi_kernel(QMulti m) {
     // the wave's block index is uniform: keep it (and the job choice) scalar
     const int blk = __builtin_amdgcn_readfirstlane(blockIdx.x * (QT / 64) + (threadIdx.x >> 6));
     if (blk >= m.nblocks) return;
-    QJob q = m.j[0];
+    // the job: its index from the start blocks, then one copy of it
+    int jt = 0;
 #pragma unroll
     for (int t = 1; t < QMULTI_MAX; t++)
-        if (t < m.count && blk >= m.j[t].blk0) q = m.j[t];
+        if (t < m.count && blk >= m.j[t].blk0) jt = t;
+    const QJob q = m.j[jt];
     if (q.kind == 0) qmulti_dispatch<0>(q, blk - q.blk0, threadIdx.x & 63);
     else             qmulti_dispatch<1>(q, blk - q.blk0, threadIdx.x & 63);
 }

@@ -28,7 +28,7 @@ class MxconvError(RuntimeError):
     pass
 
 
-QMULTI_MAX = 8
+QMULTI_MAX = 24
 FP6_SLACK = 16          # bytes of read slack at the end of an FP6 code buffer
 
 

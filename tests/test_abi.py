@@ -279,7 +279,7 @@ def test_quantize_multi_errors():
         arr = (J * max(1, len(jobs)))(*jobs)
         return L.mxconv_quantize_multi(len(jobs), arr, None)
 
-    assert L.mxconv_quantize_multi(9, None, None) == -2
+    assert L.mxconv_quantize_multi(mx.QMULTI_MAX + 1, None, None) == -2
     assert L.mxconv_quantize_multi(-1, None, None) == -2
     assert L.mxconv_quantize_multi(2, None, None) == -1
     assert L.mxconv_quantize_multi(0, None, None) == 0                  # nothing to do
