@@ -156,9 +156,10 @@ def test_fwd_quant_bf16(mx, cv, fmt):
     assert np.all(np.abs(zb - ry) <= tol)
 
 
+@pytest.mark.parametrize("fn", [1, 2], ids=["relu", "silu"])
 @pytest.mark.parametrize("fmt", [0, 1], ids=["e4m3", "e2m1"])
 @pytest.mark.parametrize("cv", FUSED_CONVS, ids=_ids)
-def test_dgrad_quant_bf16(mx, cv, fmt):
+def test_dgrad_quant_bf16(mx, cv, fmt, fn):
     q, o = _layer(mx, cv, fmt, 35)
     n = cv["n"]
     shape = (n, cv["cin"], cv["h"], cv["w"])
@@ -166,17 +167,18 @@ def test_dgrad_quant_bf16(mx, cv, fmt):
     zc = synth.nchw_to_cbf(z, 32).to(torch.bfloat16).to(DEV)
     plain16 = mx.dgrad(cv, q["w"], q["gy"], layout=mx.CBF_BF16)
     act = torch.full(plain16.shape, float("nan"), device=DEV)
-    g1 = mx.dgrad_quant(cv, q["w"], q["gy"], fn=mx.FN_SILU | mx.FN_BF16, z=zc, act_out=act)
+    g1 = mx.dgrad_quant(cv, q["w"], q["gy"], fn=fn | mx.FN_BF16, z=zc, act_out=act)
     # the unfused route: bf16 input gradient, then the gradient sum in bf16 mode
-    g2 = mx.quantize_sum([(plain16, cv["cin"], 0, 0)], shape, fmt, fn=mx.FN_SILU | mx.FN_BF16, z=zc)
+    g2 = mx.quantize_sum([(plain16, cv["cin"], 0, 0)], shape, fmt, fn=fn | mx.FN_BF16, z=zc)
     torch.cuda.synchronize()
     assert torch.equal(g1.codes, g2.codes) and torch.equal(g1.scales, g2.scales)
     a = _codes_match(act, shape, fmt, g1)
     zb = _cbf(zc, *shape)
-    d = oracle.act_grad(zb, oracle.FN_SILU)
+    d = oracle.act_grad(zb, fn)
     gb = _cbf(plain16, *shape)
     # SiLU' in fp32 with the hardware exp2 and reciprocal: a few ulp of its
-    # largest term, about 1 + |z| (it crosses zero near z = -1.28)
+    # largest term, about 1 + |z| (it crosses zero near z = -1.28); ReLU' is
+    # exact
     assert np.all(np.abs(a - gb * d) <= 1e-6 * np.abs(gb) * (1.0 + np.abs(zb)) + 1e-30)
     rg, sg = oracle.dgrad(cv, fmt, o["w"], o["gy"])
     tol = TOL * sg + RND * (np.abs(rg) + TOL * sg)
@@ -187,6 +189,7 @@ SUM_CASES = [
     (32, 48, 4, 6, [(96, 16, 0), (48, 0, 0)], 2),
     (64, 16, 5, 4, [(48, 32, 1), (16, 0, 0), (32, 16, 0)], 2),
     (32, 64, 3, 3, [(64, 0, 0), (128, 64, 1), (64, 0, 0), (192, 0, 0)], 0),
+    (32, 48, 4, 6, [(96, 16, 0), (48, 0, 1)], 1),                # ReLU
 ]
 
 

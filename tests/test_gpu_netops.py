@@ -90,6 +90,7 @@ SUM_CASES = [
     (64, 16, 5, 4, [(48, 32, 1), (16, 0, 0), (32, 16, 0)], 2),   # a 16-channel part: padded block
     (32, 64, 3, 3, [(64, 0, 0), (128, 64, 1), (64, 0, 0), (192, 0, 0)], 2),
     (32, 40, 7, 9, [(40, 0, 0), (80, 40, 0)], 0),
+    (32, 48, 4, 6, [(96, 16, 0), (48, 0, 1)], 1),                # ReLU
 ]
 
 
