@@ -538,26 +538,24 @@ __global__ __launch_bounds__(QT) void quantize_narrow_kernel(const void* __restr
     constexpr int RPP = QT / LPR;                             // rows per pass
     const int rows = 32 * g.c;
     const int k = tid % LPR;
-    for (int r = tid / LPR; r < rows; r += RPP) {
+    // every pass's 16-byte load is issued before the first is used (the
+    // passes are independent), then the values go to LDS
+    constexpr int MAXP = 32 * NARROW_C / RPP;                 // passes for NARROW_C channels
+    uint4 raw[MAXP];
+#pragma unroll
+    for (int q = 0; q < MAXP; q++) {
+        const int r = tid / LPR + q * RPP;
         const int n = r / g.c, c = r - n * g.c;
         const int sample = grp * 32 + n;
         const int px = p0 + k * VEC;
-        float v[VEC];
         const size_t base = ((size_t)sample * g.c + c) * hw;
+        raw[q] = make_uint4(0u, 0u, 0u, 0u);
+        if (r >= rows) continue;
         if (VECLOAD && sample < g.n && px + VEC <= hw) {
-            if (DTYPE == MXC_F32) {
-                const float4 a = load_nt((const float*)src + base + px);
-                v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-            } else {
-                const v4i b = __builtin_nontemporal_load((const v4i*)((const unsigned short*)src + base + px));
-                const uint32_t w4[4] = {(uint32_t)b[0], (uint32_t)b[1], (uint32_t)b[2], (uint32_t)b[3]};
-#pragma unroll
-                for (int e = 0; e < 4; e++) {
-                    v[2 * e] = __uint_as_float(w4[e] << 16);
-                    v[2 * e + 1] = __uint_as_float(w4[e] & 0xFFFF0000u);
-                }
-            }
+            const v4i b = __builtin_nontemporal_load((const v4i*)((const uint8_t*)src + (base + px) * (DTYPE == MXC_F32 ? 4 : 2)));
+            raw[q] = make_uint4((uint32_t)b[0], (uint32_t)b[1], (uint32_t)b[2], (uint32_t)b[3]);
         } else {
+            float v[VEC];
 #pragma unroll
             for (int e = 0; e < VEC; e++) {
                 const bool ok = sample < g.n && px + e < hw;
@@ -565,6 +563,31 @@ __global__ __launch_bounds__(QT) void quantize_narrow_kernel(const void* __restr
                 const float x = DTYPE == MXC_F32 ? __ldg((const float*)src + i)
                                                  : __uint_as_float((uint32_t)__ldg((const unsigned short*)src + i) << 16);
                 v[e] = ok ? x : 0.0f;
+            }
+            if constexpr (DTYPE == MXC_F32)
+                raw[q] = make_uint4(__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]), __float_as_uint(v[3]));
+            else   // back to bf16 pairs (exact: the values are bf16)
+                raw[q] = make_uint4(__float_as_uint(v[0]) >> 16 | (__float_as_uint(v[1]) & 0xFFFF0000u),
+                                    __float_as_uint(v[2]) >> 16 | (__float_as_uint(v[3]) & 0xFFFF0000u),
+                                    __float_as_uint(v[4]) >> 16 | (__float_as_uint(v[5]) & 0xFFFF0000u),
+                                    __float_as_uint(v[6]) >> 16 | (__float_as_uint(v[7]) & 0xFFFF0000u));
+        }
+    }
+#pragma unroll
+    for (int q = 0; q < MAXP; q++) {
+        const int r = tid / LPR + q * RPP;
+        if (r >= rows) continue;
+        const int n = r / g.c, c = r - n * g.c;
+        const uint32_t w4[4] = {raw[q].x, raw[q].y, raw[q].z, raw[q].w};
+        float v[VEC];
+        if constexpr (DTYPE == MXC_F32) {
+#pragma unroll
+            for (int e = 0; e < 4; e++) v[e] = __uint_as_float(w4[e]);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; e++) {
+                v[2 * e] = __uint_as_float(w4[e] << 16);
+                v[2 * e + 1] = __uint_as_float(w4[e] & 0xFFFF0000u);
             }
         }
 #pragma unroll
