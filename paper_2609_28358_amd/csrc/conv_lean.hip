@@ -73,7 +73,15 @@ int lean_plan(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const 
     // pixel per wave instead: twice the workgroups, more waves streaming
     // operands and storing results at once (measured: faster below ~200
     // tiles, slower from ~400)
-    if (narrow && count(1, NARROW_PW, 1, false) >= 192) { wgm = 1; pw = NARROW_PW; rb = 1; }
+    // Narrow tiles of 8 pixels instead of 16 (half the stage ring, more
+    // workgroups on a CU's LDS) where that measured faster in the network
+    // step: the forward at column stride 2 and the fused input gradient,
+    // except at stride 2 with kernel-row pairing (a single K block), which
+    // keeps 16 (210 vs 246 µs on the second layer); the grouped backward
+    // (no fused epilogue) keeps 16 as well.
+    const bool kr_cand = a.kcb == 1 && cv.kw == 3 && (dg2 ? (cv.kh + 1) / 2 : cv.kh) >= 2;
+    const bool half = dg ? (q != nullptr && !(dg2 && kr_cand)) : cv.sw == 2;
+    if (narrow && count(1, NARROW_PW, 1, false) >= 192) { wgm = 1; pw = half ? NARROW_PW2 : NARROW_PW; rb = 1; }
     else if (count(wgm, pw, 2, false) < 192 || nv) { wgm = 1; pw = 1; }
     const int px = pw * 4 / wgm;
     a.mtiles = (a.M + 32 * rb * wgm - 1) / (32 * rb * wgm);

@@ -56,6 +56,7 @@ int launch_lean_bwd(const Conv& dcv, const void* wc, const uint8_t* ws, const vo
     LeanPlan P;
     const int prc = lean_plan(dcv, true, wc, ws, gc, gs, gx, layout, nullptr, nullptr, nullptr, P);
     if (prc) return prc;
+    if (P.rb == 1 && P.pw != NARROW_PW) return 1;        // a narrow shape this kernel is not built for
     WLArgs q;
     const long wg = wgrad_lean_fill(wcv, gc, gs, xc, xs, wdst, splits, nullptr, nullptr, q);
     if (wg < 0) return MXC_ERR_SHAPE;

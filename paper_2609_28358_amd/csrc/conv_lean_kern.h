@@ -1156,6 +1156,9 @@ int launch_lean_dg2(const LeanArgs& a, int nbufs_used, hipStream_t s) {
 // (the same products per wave as 64 rows x 2 pixels, none of them on padding
 // rows), a tile 32 rows x 16 pixels.
 constexpr int NARROW_PW = 4;
+// ... or 32 rows x 2 pixels (a tile 32 x 8: half the stage, so more
+// workgroups share a CU's LDS)
+constexpr int NARROW_PW2 = 2;
 template <int FW, int FX>
 constexpr bool narrow_ok() { return FW == MXC_E2M1 && FX == MXC_E2M1; }
 
@@ -1166,10 +1169,18 @@ int launch_lean_w(const LeanArgs& a, const LeanShape& h, hipStream_t s) {
     const int wgm = h.wgm, pw = h.pw, nb = h.nb;
     if constexpr (NV) return launch_lean_t<FW, FX, DG, KW, S, 1, 1, true>(a, nb, s);
     if constexpr (narrow_ok<FW, FX>())
-        if (pw == NARROW_PW) {
-            if constexpr (KW == 3)
-                if (h.kr) return launch_lean_t<FW, FX, DG, KW, S, 1, NARROW_PW, false, 1, true>(a, nb, s);
-            return launch_lean_t<FW, FX, DG, KW, S, 1, NARROW_PW, false, 1>(a, nb, s);
+        if (h.rb == 1) {
+            if (pw == NARROW_PW) {
+                if constexpr (KW == 3)
+                    if (h.kr) return launch_lean_t<FW, FX, DG, KW, S, 1, NARROW_PW, false, 1, true>(a, nb, s);
+                return launch_lean_t<FW, FX, DG, KW, S, 1, NARROW_PW, false, 1>(a, nb, s);
+            }
+            if (pw == NARROW_PW2) {
+                if constexpr (KW == 3)
+                    if (h.kr) return launch_lean_t<FW, FX, DG, KW, S, 1, NARROW_PW2, false, 1, true>(a, nb, s);
+                return launch_lean_t<FW, FX, DG, KW, S, 1, NARROW_PW2, false, 1>(a, nb, s);
+            }
+            return MXC_ERR_ARG;
         }
     if (wgm == 4) return launch_lean_t<FW, FX, DG, KW, S, 4, 2>(a, nb, s);
     if (wgm == 2) return launch_lean_t<FW, FX, DG, KW, S, 2, 2>(a, nb, s);
@@ -1183,10 +1194,17 @@ int launch_lean_f(const LeanArgs& a, const LeanShape& h, hipStream_t s) {
         if (sw == 2) {
             if constexpr (NV) return kw == 3 ? launch_lean_dg2<FW, FX, 3, 1, true>(a, nb, s) : launch_lean_dg2<FW, FX, 1, 1, true>(a, nb, s);
             if constexpr (narrow_ok<FW, FX>())
-                if (pw == NARROW_PW)
-                    return kw == 3 ? (h.kr ? launch_lean_dg2<FW, FX, 3, NARROW_PW, false, 1, true>(a, nb, s)
-                                           : launch_lean_dg2<FW, FX, 3, NARROW_PW, false, 1>(a, nb, s))
-                                   : launch_lean_dg2<FW, FX, 1, NARROW_PW, false, 1>(a, nb, s);
+                if (h.rb == 1) {
+                    if (pw == NARROW_PW)
+                        return kw == 3 ? (h.kr ? launch_lean_dg2<FW, FX, 3, NARROW_PW, false, 1, true>(a, nb, s)
+                                               : launch_lean_dg2<FW, FX, 3, NARROW_PW, false, 1>(a, nb, s))
+                                       : launch_lean_dg2<FW, FX, 1, NARROW_PW, false, 1>(a, nb, s);
+                    if (pw == NARROW_PW2)
+                        return kw == 3 ? (h.kr ? launch_lean_dg2<FW, FX, 3, NARROW_PW2, false, 1, true>(a, nb, s)
+                                               : launch_lean_dg2<FW, FX, 3, NARROW_PW2, false, 1>(a, nb, s))
+                                       : launch_lean_dg2<FW, FX, 1, NARROW_PW2, false, 1>(a, nb, s);
+                    return MXC_ERR_ARG;
+                }
             if (kw == 3) return pw == 1 ? launch_lean_dg2<FW, FX, 3, 1>(a, nb, s) : launch_lean_dg2<FW, FX, 3, 2>(a, nb, s);
             return pw == 1 ? launch_lean_dg2<FW, FX, 1, 1>(a, nb, s) : launch_lean_dg2<FW, FX, 1, 2>(a, nb, s);
         }
