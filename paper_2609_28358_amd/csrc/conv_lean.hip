@@ -45,12 +45,12 @@ int lean_plan(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const 
     a.x_ncb = src.ncb;
     a.xrows = src.ncb == 1 ? src.c : 32;
     if (dg && a.w_nco != src.ncb) return 1;
-    // rows per tile: the choice that streams the fewest bytes per stage for
-    // the same 48 MFMAs -- 64 rows x 8 pixels at column stride 1; at stride 2
-    // the halo of 8 pixels is wide, 128 rows x 4 pixels is cheaper
-    const int mp = (a.M + 63) / 64;
-    int wgm = (!dg && cv.sw == 2 && mp >= 2) ? 2 : 1;
-    int pw = 2;
+    // rows per tile: 64 rows x 8 pixels at column stride 1; the forward at
+    // column stride 2, whose halo is twice as wide, takes 64 rows x 4 pixels
+    // (measured faster in the network step than 128 x 4 or 64 x 8: the
+    // five downsampling layers 114 -> 105 µs together)
+    const int wgm = 1;
+    int pw = !dg && cv.sw == 2 ? 1 : 2;
     // a single 32-row block of FP4 rows: narrow tiles (32 rows x 16 pixels)
     const bool narrow = a.M <= 32 && cv.fa == MXC_E2M1 && cv.fb == MXC_E2M1 && !nv;
     int rb = 2;
@@ -69,10 +69,6 @@ int lean_plan(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const 
         }
         return t;
     };
-    // a layer whose tiles would leave a quarter of the CUs idle takes one
-    // pixel per wave instead: twice the workgroups, more waves streaming
-    // operands and storing results at once (measured: faster below ~200
-    // tiles, slower from ~400)
     // Narrow tiles of 8 pixels instead of 16 (half the stage ring, more
     // workgroups on a CU's LDS) where that measured faster in the network
     // step: the forward at column stride 2 and the fused input gradient,
@@ -81,8 +77,12 @@ int lean_plan(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const 
     // (no fused epilogue) keeps 16 as well.
     const bool kr_cand = a.kcb == 1 && cv.kw == 3 && (dg2 ? (cv.kh + 1) / 2 : cv.kh) >= 2;
     const bool half = dg ? (q != nullptr && !(dg2 && kr_cand)) : cv.sw == 2;
-    if (narrow && count(1, NARROW_PW, 1, false) >= 192) { wgm = 1; pw = half ? NARROW_PW2 : NARROW_PW; rb = 1; }
-    else if (count(wgm, pw, 2, false) < 192 || nv) { wgm = 1; pw = 1; }
+    // a layer whose tiles would leave a quarter of the CUs idle takes one
+    // pixel per wave instead: twice the workgroups, more waves streaming
+    // operands and storing results at once (measured: faster below ~200
+    // tiles, slower from ~400)
+    if (narrow && count(1, NARROW_PW, 1, false) >= 192) { pw = half ? NARROW_PW2 : NARROW_PW; rb = 1; }
+    else if (count(wgm, pw, 2, false) < 192 || nv) pw = 1;
     const int px = pw * 4 / wgm;
     a.mtiles = (a.M + 32 * rb * wgm - 1) / (32 * rb * wgm);
     for (int i = 0; i < 5; i++) a.pofs[i] = 0;

@@ -1162,8 +1162,8 @@ constexpr int NARROW_PW2 = 2;
 template <int FW, int FX>
 constexpr bool narrow_ok() { return FW == MXC_E2M1 && FX == MXC_E2M1; }
 
-// (WGM, PW, NRB) in use: (1, 1, 2), (1, 2, 2), (2, 2, 2), (4, 2, 2) and narrow
-// (1, 4, 1); the NV kernels run (1, 1, 2)
+// (WGM, PW, NRB) in use: (1, 1, 2), (1, 2, 2) and narrow (1, NARROW_PW, 1),
+// (1, NARROW_PW2, 1); the NV kernels run (1, 1, 2)
 template <int FW, int FX, bool DG, int KW, int S, bool NV = false>
 int launch_lean_w(const LeanArgs& a, const LeanShape& h, hipStream_t s) {
     const int wgm = h.wgm, pw = h.pw, nb = h.nb;
@@ -1182,8 +1182,7 @@ int launch_lean_w(const LeanArgs& a, const LeanShape& h, hipStream_t s) {
             }
             return MXC_ERR_ARG;
         }
-    if (wgm == 4) return launch_lean_t<FW, FX, DG, KW, S, 4, 2>(a, nb, s);
-    if (wgm == 2) return launch_lean_t<FW, FX, DG, KW, S, 2, 2>(a, nb, s);
+    if (wgm != 1) return MXC_ERR_ARG;
     return pw == 1 ? launch_lean_t<FW, FX, DG, KW, S, 1, 1>(a, nb, s) : launch_lean_t<FW, FX, DG, KW, S, 1, 2>(a, nb, s);
 }
 
