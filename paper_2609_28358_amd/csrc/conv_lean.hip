@@ -48,7 +48,7 @@ int lean_plan(const Conv& cv, bool dg, const void* wc, const uint8_t* ws, const 
     // rows per tile: 64 rows x 8 pixels at column stride 1; the forward at
     // column stride 2, whose halo is twice as wide, takes 64 rows x 4 pixels
     // (measured faster in the network step than 128 x 4 or 64 x 8: the
-    // five downsampling layers 114 -> 105 µs together)
+    // five downsampling layers 142 -> 131 µs together)
     const int wgm = 1;
     int pw = !dg && cv.sw == 2 ? 1 : 2;
     // a single 32-row block of FP4 rows: narrow tiles (32 rows x 16 pixels)
